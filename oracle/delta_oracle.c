@@ -1,0 +1,284 @@
+/*
+ * Plain CPU oracle for the lossless sparse delta checkpoint of AuroraRL
+ * (arXiv 2602.11456).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may link, load or
+ * call this file: only the test suite, the smoke check and the CPU baseline
+ * leg of the benchmark use it.  It shares no code, header, table or helper
+ * with the GPU library; it includes nothing but the C standard library.
+ *
+ * Every function is the plain definition written out as one sequential loop
+ * over elements, with no blocking, vectorisation or reordering:
+ *
+ *   extract        Sec. 5.1 "Sparse encoding": each tensor's delta is
+ *                  flattened to a 1-D index space and its non-zeros are kept
+ *                  as two 1-D arrays, idx and val, with a fixed-width int32 or
+ *                  int64 index and a bfloat16 value.  The index array is
+ *                  sorted (the gap encoding of Sec. 5.1 is defined on it).
+ *                  A position is kept when its bf16 bit pattern changed; the
+ *                  value kept is the updated bf16 word (reading: a bitwise
+ *                  compare and an assignment scatter are what make the
+ *                  round trip lossless, Sec. 5.1 "Lossless precision").
+ *   extract_multi  Sec. 5.1: several tensors share one linear index space by
+ *                  adding a fixed block offset (the sum of the sizes of the
+ *                  tensors before it) to each tensor's own linear indices.
+ *   apply          Sec. 5.1 / Sec. 5.2: the actor writes the streams into the
+ *                  parameter's flat storage in place.
+ *   gap + LEB128   Sec. 5.1 and Fig. "Delta checkpoint index encoding": the
+ *                  sorted index array keeps its first entry as-is and every
+ *                  later entry as the difference from its predecessor; each
+ *                  number is then written as unsigned LEB128 (7 payload bits
+ *                  per byte, least significant group first, high bit set on
+ *                  every byte but the last).
+ *
+ * Conventions shared with the library's C ABI (they are the ABI's contract,
+ * restated here, not code shared with it): bf16 words travel as raw uint16
+ * bit patterns; "count" results are always the true number of entries even
+ * when it exceeds the caller's capacity, and only the first `capacity`
+ * entries are written.
+ */
+#include <stdint.h>
+#include <stddef.h>
+
+/* ------------------------------------------------------------------ */
+/* extract: one tensor, local indices                                  */
+/* ------------------------------------------------------------------ */
+
+/* Sec. 5.1 "Sparse encoding", int64 index variant. */
+uint64_t oracle_extract_i64(const uint16_t *prev, const uint16_t *next,
+                            uint64_t n, int64_t *idx, uint16_t *val,
+                            uint64_t capacity)
+{
+    uint64_t count = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        if (prev[i] != next[i]) {
+            if (count < capacity) {
+                idx[count] = (int64_t)i;
+                val[count] = next[i];
+            }
+            ++count;
+        }
+    }
+    return count;
+}
+
+/* Sec. 5.1 "Sparse encoding", int32 index variant (caller guarantees that
+ * n - 1 fits in int32). */
+uint64_t oracle_extract_i32(const uint16_t *prev, const uint16_t *next,
+                            uint64_t n, int32_t *idx, uint16_t *val,
+                            uint64_t capacity)
+{
+    uint64_t count = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        if (prev[i] != next[i]) {
+            if (count < capacity) {
+                idx[count] = (int32_t)i;
+                val[count] = next[i];
+            }
+            ++count;
+        }
+    }
+    return count;
+}
+
+/* ------------------------------------------------------------------ */
+/* extract_multi: a list of tensors in one global index space          */
+/* ------------------------------------------------------------------ */
+
+/* Sec. 5.1: tensor t contributes global index base_t + i, where base_t is
+ * the total size of tensors 0..t-1.  tensor_offsets (T+1 entries, may be
+ * NULL) receives the output position of each tensor's first entry, and the
+ * total at index T. */
+uint64_t oracle_extract_multi(const uint16_t *const *prevs,
+                              const uint16_t *const *nexts,
+                              const uint64_t *numels, int32_t num_tensors,
+                              int64_t *idx, uint16_t *val, uint64_t capacity,
+                              uint64_t *tensor_offsets)
+{
+    uint64_t count = 0;
+    uint64_t base = 0;
+    for (int32_t t = 0; t < num_tensors; ++t) {
+        if (tensor_offsets)
+            tensor_offsets[t] = count;
+        const uint16_t *p = prevs[t];
+        const uint16_t *q = nexts[t];
+        for (uint64_t i = 0; i < numels[t]; ++i) {
+            if (p[i] != q[i]) {
+                if (count < capacity) {
+                    idx[count] = (int64_t)(base + i);
+                    val[count] = q[i];
+                }
+                ++count;
+            }
+        }
+        base += numels[t];
+    }
+    if (tensor_offsets)
+        tensor_offsets[num_tensors] = count;
+    return count;
+}
+
+/* ------------------------------------------------------------------ */
+/* apply: in-place scatter of the value stream                          */
+/* ------------------------------------------------------------------ */
+
+/* Sec. 5.1 / 5.2: w[idx[k]] = val[k].  Entries whose index is outside
+ * [0, n) are skipped; the return value is how many were skipped. */
+uint64_t oracle_apply_i64(uint16_t *w, uint64_t n, const int64_t *idx,
+                          const uint16_t *val, uint64_t count)
+{
+    uint64_t bad = 0;
+    for (uint64_t k = 0; k < count; ++k) {
+        if (idx[k] < 0 || (uint64_t)idx[k] >= n) {
+            ++bad;
+            continue;
+        }
+        w[idx[k]] = val[k];
+    }
+    return bad;
+}
+
+uint64_t oracle_apply_i32(uint16_t *w, uint64_t n, const int32_t *idx,
+                          const uint16_t *val, uint64_t count)
+{
+    uint64_t bad = 0;
+    for (uint64_t k = 0; k < count; ++k) {
+        if (idx[k] < 0 || (uint64_t)idx[k] >= n) {
+            ++bad;
+            continue;
+        }
+        w[idx[k]] = val[k];
+    }
+    return bad;
+}
+
+/* Sec. 5.1: a global index g belongs to the tensor t with
+ * base_t <= g < base_t + n_t, at local position g - base_t.  The tensor is
+ * found by scanning the bases in order, so any index order is accepted. */
+uint64_t oracle_apply_multi(uint16_t *const *ws, const uint64_t *numels,
+                            int32_t num_tensors, const int64_t *idx,
+                            const uint16_t *val, uint64_t count)
+{
+    uint64_t bad = 0;
+    for (uint64_t k = 0; k < count; ++k) {
+        int64_t g = idx[k];
+        int found = 0;
+        if (g >= 0) {
+            uint64_t base = 0;
+            for (int32_t t = 0; t < num_tensors; ++t) {
+                if ((uint64_t)g < base + numels[t]) {
+                    ws[t][(uint64_t)g - base] = val[k];
+                    found = 1;
+                    break;
+                }
+                base += numels[t];
+            }
+        }
+        if (!found)
+            ++bad;
+    }
+    return bad;
+}
+
+/* ------------------------------------------------------------------ */
+/* gap + unsigned LEB128 index encoding                                */
+/* ------------------------------------------------------------------ */
+
+/* Sec. 5.1: gaps of a sorted index array, first entry kept as-is.
+ * Returns 0 on success, 1 if the input is not strictly increasing or has a
+ * negative first entry. */
+int oracle_gaps(const int64_t *idx, uint64_t count, uint64_t *gaps)
+{
+    for (uint64_t k = 0; k < count; ++k) {
+        if (k == 0) {
+            if (idx[0] < 0)
+                return 1;
+            gaps[0] = (uint64_t)idx[0];
+        } else {
+            if (idx[k] <= idx[k - 1])
+                return 1;
+            gaps[k] = (uint64_t)(idx[k] - idx[k - 1]);
+        }
+    }
+    return 0;
+}
+
+/* Unsigned LEB128 of one number: 7-bit groups, least significant first,
+ * continuation flag (0x80) on every byte except the last.  Writes at most
+ * 10 bytes; returns the number of bytes. */
+static int leb128_put(uint64_t v, uint8_t *out)
+{
+    int nb = 0;
+    do {
+        uint8_t byte = (uint8_t)(v & 0x7F);
+        v >>= 7;
+        if (v != 0)
+            byte |= 0x80;
+        out[nb++] = byte;
+    } while (v != 0);
+    return nb;
+}
+
+/* Encodes the gaps of idx as one LEB128 byte stream.  Returns the true
+ * byte length (only the first `capacity` bytes are written), or
+ * UINT64_MAX if idx is not strictly increasing / non-negative. */
+uint64_t oracle_leb128_encode(const int64_t *idx, uint64_t count,
+                              uint8_t *out, uint64_t capacity)
+{
+    uint64_t len = 0;
+    int64_t prev = 0;
+    for (uint64_t k = 0; k < count; ++k) {
+        uint64_t gap;
+        if (k == 0) {
+            if (idx[0] < 0)
+                return UINT64_MAX;
+            gap = (uint64_t)idx[0];
+        } else {
+            if (idx[k] <= prev)
+                return UINT64_MAX;
+            gap = (uint64_t)(idx[k] - prev);
+        }
+        prev = idx[k];
+        uint8_t tmp[10];
+        int nb = leb128_put(gap, tmp);
+        for (int b = 0; b < nb; ++b) {
+            if (len < capacity)
+                out[len] = tmp[b];
+            ++len;
+        }
+    }
+    return len;
+}
+
+/* Decodes a LEB128 gap stream back to absolute indices (running sum of the
+ * gaps).  Returns the number of indices decoded (only the first
+ * `capacity` written), or UINT64_MAX if the stream ends inside a number or
+ * a number needs more than 64 bits. */
+uint64_t oracle_leb128_decode(const uint8_t *in, uint64_t nbytes,
+                              int64_t *idx, uint64_t capacity)
+{
+    uint64_t count = 0;
+    uint64_t pos = 0;
+    uint64_t acc = 0;
+    while (pos < nbytes) {
+        uint64_t v = 0;
+        int shift = 0;
+        for (;;) {
+            if (pos >= nbytes)
+                return UINT64_MAX;
+            uint8_t byte = in[pos++];
+            uint64_t payload = (uint64_t)(byte & 0x7F);
+            if (shift > 63 || (shift == 63 && payload > 1))
+                return UINT64_MAX;
+            v |= payload << shift;
+            shift += 7;
+            if ((byte & 0x80) == 0)
+                break;
+        }
+        acc = (count == 0) ? v : acc + v;
+        if (count < capacity)
+            idx[count] = (int64_t)acc;
+        ++count;
+    }
+    return count;
+}
