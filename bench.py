@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark of the sparse delta checkpoint hot path on one MI355X.
+
+Workload: a Qwen3-8B-shaped bf16 weight set (399 tensors, 8,190,735,360
+words, untied embedding and LM head) with 1% of the words of every tensor
+changed, drawn on the GPU by ``paper_2602_11456_amd.synth``.  Inputs are
+resident in HBM before timing starts.
+
+One step = delta_extract_multi over the whole set (int64 global indices)
+followed by delta_apply_multi of the result into a rollout copy.  Apply
+assigns the new words, so re-applying the same delta every step is exact
+and idempotent.
+
+Timing: W untimed warm-up steps, then K timed steps between two
+synchronisations; HIP events on the launch stream bracket every extract and
+every apply.  Printed: one JSON line with GB/s scanned by extract (4 bytes
+per word: both copies read once) as ``value``, the extract kernel's
+roofline figures, apply throughput, and the CPU oracle timed on a bounded
+sample of the same weight set.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+METRIC = "delta extract GB/s scanned (% of HBM peak) + apply GB/s, Qwen3-8B shape @1%"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--density", type=float, default=0.01)
+    ap.add_argument("--model", default="qwen3-8b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="oracle time budget for the CPU baseline sample")
+    ap.add_argument("--traffic", default=None,
+                    help="JSON file with measured HBM bytes per extract launch")
+    return ap.parse_args()
+
+
+def cpu_baseline(ws, budget_s):
+    """The CPU oracle on the first tensors of the same set, until the time
+    budget is used: GB/s scanned over the words it processed."""
+    import numpy as np
+    import torch
+    import oracle
+
+    oracle.build(force=False)
+    words = 0
+    spent = 0.0
+    tensors = 0
+    found = 0
+    planted = 0
+    for p, q, k in zip(ws.prev, ws.new, ws.planted):
+        hp = p.view(torch.int16).reshape(-1).cpu().numpy().view(np.uint16)
+        hq = q.view(torch.int16).reshape(-1).cpu().numpy().view(np.uint16)
+        t0 = time.perf_counter()
+        _, _, cnt = oracle.extract(hp, hq, np.int64, capacity=k)
+        spent += time.perf_counter() - t0
+        words += hp.size
+        tensors += 1
+        found += cnt
+        planted += k
+        if spent >= budget_s:
+            break
+    if found != planted:
+        raise RuntimeError(f"oracle found {found} changed words, {planted} planted")
+    return {
+        "value": round(4 * words / spent / 1e9, 3),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"first {tensors} of {len(ws.prev)} tensors of the same weight set "
+                  f"({words} words, {4 * words / 1e9:.2f} GB scanned) in {spent:.1f} s, "
+                  f"single-threaded C loop",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the hot path has no multi-GPU form in this library)", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2602_11456_amd as ad
+    from paper_2602_11456_amd import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    ad.library()   # fail loudly if the HIP library is missing
+
+    t0 = time.time()
+    ws = synth.make_weight_set(args.model, args.density, seed=synth.config_seed(3), device=dev)
+    torch.cuda.synchronize()
+    N = ws.total
+    K_planted = ws.total_planted
+    log(f"generated {len(ws.prev)} tensors, {N} words, {K_planted} changed "
+        f"in {time.time() - t0:.1f} s")
+
+    plan = ad.MultiPlan(ws.prev, ws.new)
+    cap = K_planted + 1024
+    out_idx = torch.empty(cap, dtype=torch.int64, device=dev)
+    out_val = torch.empty(cap, dtype=torch.bfloat16, device=dev)
+    d_count = torch.zeros(1, dtype=torch.int64, device=dev)
+    d_offs = torch.zeros(plan.T + 1, dtype=torch.int64, device=dev)
+    work = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=dev)
+    rollout = [p.clone() for p in ws.prev]
+    apply_ws = torch.empty(max(ad.delta_apply_multi_workspace_bytes(plan.T), 1),
+                           dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def extract():
+        ad.delta_extract_multi_into(plan, out_idx, out_val, d_count, work, d_offs, stream)
+
+    def apply(k):
+        ad.delta_apply_multi(rollout, out_idx[:k], out_val[:k], workspace=apply_ws,
+                             stream=stream)
+
+    # warm-up (also checks the count once)
+    extract()
+    torch.cuda.synchronize()
+    K = int(d_count.item())
+    if K != K_planted:
+        raise RuntimeError(f"extract found {K} changed words, {K_planted} planted")
+    for _ in range(max(args.warmup - 1, 0)):
+        extract()
+        apply(K)
+    apply(K)
+    torch.cuda.synchronize()
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+            torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for e0, e1, e2 in evs:
+        e0.record(stream)
+        extract()
+        e1.record(stream)
+        apply(K)
+        e2.record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+
+    ext_ms = [e0.elapsed_time(e1) for e0, e1, _ in evs]
+    app_ms = [e1.elapsed_time(e2) for _, e1, e2 in evs]
+    total_ms = t_start.elapsed_time(t_end)
+    ext_avg = sum(ext_ms) / len(ext_ms)
+    app_avg = sum(app_ms) / len(app_ms)
+
+    # correctness of the timed state: the rollout equals the new weights
+    for r, q in zip(rollout, ws.new):
+        if not torch.equal(r.view(torch.int16), q.view(torch.int16)):
+            raise RuntimeError("rollout copy differs from the updated weights")
+
+    w = 8   # int64 indices
+    scanned = 4 * N
+    alg_bytes = scanned + K * (w + 2)
+    ext_s = ext_avg / 1e3
+    value = scanned / ext_s / 1e9
+    achieved = alg_bytes / ext_s / 1e9
+    apply_bytes = K * (w + 2) + 2 * K
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            traffic = json.load(f).get("bytes_per_launch")
+
+    ext_sorted = sorted(ext_ms)
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.model} weight set, {len(ws.prev)} tensors, {N} bf16 words, "
+                        f"{args.density:.2%} of words changed per tensor, int64 global indices",
+            "tensors": len(ws.prev),
+            "words": N,
+            "changed": K,
+            "density": args.density,
+            "index": "int64",
+        },
+        "extract": {
+            "ms": round(ext_avg, 4),
+            "ms_p10": round(ext_sorted[len(ext_sorted) // 10], 4),
+            "ms_p90": round(ext_sorted[(9 * len(ext_sorted)) // 10], 4),
+            "GBps_scanned": round(value, 2),
+            "GBps_algorithmic": round(achieved, 2),
+            "pct_hbm_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
+        },
+        "apply": {
+            "ms": round(app_avg, 4),
+            "GBps_algorithmic": round(apply_bytes / (app_avg / 1e3) / 1e9, 2),
+            "changed_words_per_s": round(K / (app_avg / 1e3), 1),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        del rollout
+        result["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

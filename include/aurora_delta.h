@@ -1,0 +1,217 @@
+/*
+ * aurora_delta.h — C ABI of an MI355X (gfx950) library for lossless sparse
+ * delta checkpoints of bf16 model weights, after AuroraRL (arXiv
+ * 2602.11456), Sec. 5.1 "Lossless Sparse Delta Geo-Checkpoints" and
+ * Sec. 5.2 "Streaming Delta Transfer Protocol".
+ *
+ * The operations:
+ *   extract        Compare the previous and the updated bf16 weights word
+ *                  by word and keep every word whose bits changed, as two
+ *                  1-D streams: the flattened positions (int32 or int64)
+ *                  and the new bf16 words (Sec. 5.1 "Sparse encoding").
+ *   extract_multi  The same over a list of tensors in one index space:
+ *                  tensor t's positions are offset by the total size of the
+ *                  tensors before it, the fixed block offsets the paper
+ *                  uses to stack q/k/v or gate/up blocks (Sec. 5.1).
+ *   apply          Write the streams into the flat storage of a rollout
+ *                  copy in place, so that it becomes the updated weights
+ *                  bit for bit (Sec. 5.1, Sec. 5.2 "activation").
+ *   apply_checked  apply, refused unless the caller's active version is
+ *                  the delta's declared base version (Sec. 5.2).
+ *   extract_pipelined
+ *                  extract_multi split into fixed-size chunks of the global
+ *                  index space, spread round-robin over several streams,
+ *                  each chunk's streams copied into pinned host memory as
+ *                  soon as it is done (Sec. 5.2, "Overlapped extraction and
+ *                  transfer": segments emitted as soon as they are encoded
+ *                  and striped round-robin).
+ *
+ * Conventions (all functions):
+ *   - bf16 data crosses the ABI as raw uint16_t bit patterns.  "Changed"
+ *     means the 16-bit patterns differ: +0 -> -0 is a change, an identical
+ *     NaN word is not.  The value stream holds the NEW words (not a
+ *     difference) and apply assigns them, which makes the round trip
+ *     lossless and apply idempotent.
+ *   - Pointers are device pointers (hipMalloc / torch CUDA tensors) unless
+ *     the name starts with h_ (host memory) or the comment says "host
+ *     array".  Weight pointers must be 2-byte aligned; any other alignment
+ *     is accepted (16-byte loads are used where both copies allow them).
+ *   - Index order is the flattened storage order of each tensor (row-major
+ *     for a C-contiguous tensor).  Output indices are strictly increasing.
+ *   - The caller owns all memory.  No entry point allocates device memory;
+ *     scratch space is a caller-provided `workspace` of at least the size
+ *     the matching *_workspace_bytes function returns (256-byte aligned).
+ *   - Asynchrony: extract/apply functions only enqueue work on `stream`
+ *     (0 = the null stream) and return.  The return status covers argument
+ *     validation and launch errors.  Device-side outcomes are read after
+ *     the caller synchronises:
+ *       *d_count      true number of changed words, also when it exceeds
+ *                     `capacity` (then only the first `capacity` entries
+ *                     are written and the caller may retry larger);
+ *       *d_error_flag nonzero if some index was outside [0, numel) and was
+ *                     skipped.
+ *   - Errors: no exception crosses the ABI; the return value is a
+ *     delta_status_t and delta_last_error() holds a detail string for the
+ *     calling thread.  Calls on one workspace must not overlap in time
+ *     (enqueue them on one stream).
+ */
+#ifndef AURORA_DELTA_H
+#define AURORA_DELTA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AURORA_DELTA_ABI_VERSION 1
+
+typedef enum {
+  DELTA_OK = 0,
+  DELTA_ERR_INVALID_ARG = 1,    /* null pointer, odd address, bad count */
+  DELTA_ERR_INDEX_OVERFLOW = 2, /* int32 indices asked for numel - 1 > INT32_MAX */
+  DELTA_ERR_CAPACITY = 3,       /* host-synchronous calls: output did not fit */
+  DELTA_ERR_OUT_OF_RANGE = 4,   /* host-synchronous calls: an index was skipped */
+  DELTA_ERR_VERSION = 5,        /* apply_checked: active != base version */
+  DELTA_ERR_WORKSPACE = 6,      /* workspace missing, too small or misaligned */
+  DELTA_ERR_HIP = 7             /* a HIP runtime call failed */
+} delta_status_t;
+
+typedef enum { DELTA_INDEX_I32 = 0, DELTA_INDEX_I64 = 1 } delta_index_t;
+
+/* AURORA_DELTA_ABI_VERSION of the loaded library. */
+int delta_abi_version(void);
+
+/* Static text naming a status code. */
+const char* delta_status_string(int status);
+
+/* Detail text of the last failed call on this thread ("" if none). */
+const char* delta_last_error(void);
+
+/* Workspace bytes for delta_extract over `numel` words (any alignment). */
+size_t delta_extract_workspace_bytes(uint64_t numel);
+
+/* Workspace bytes for delta_extract_multi over tensors of the given sizes
+ * (`numels` is a host array of `num_tensors` entries). */
+size_t delta_extract_multi_workspace_bytes(const uint64_t* numels, int32_t num_tensors);
+
+/* Workspace bytes for delta_apply_multi over `num_tensors` tensors. */
+size_t delta_apply_multi_workspace_bytes(int32_t num_tensors);
+
+/*
+ * delta_extract — Sec. 5.1 "Sparse encoding", one tensor.
+ *   prev, next    device, `numel` words each: the bf16 bit patterns before
+ *                 and after the step.
+ *   index_type    DELTA_INDEX_I32 (only if numel - 1 <= INT32_MAX, else
+ *                 DELTA_ERR_INDEX_OVERFLOW) or DELTA_INDEX_I64.
+ *   out_idx       device, `capacity` int32 or int64 entries: positions of
+ *                 the changed words, ascending.
+ *   out_val       device, `capacity` words: next[out_idx[k]].
+ *   d_count       device, one uint64: the true number of changed words.
+ *   workspace     device scratch (delta_extract_workspace_bytes(numel)).
+ * numel == 0 and prev == next are legal (count 0).  prev/next must not
+ * overlap the outputs.
+ */
+delta_status_t delta_extract(const uint16_t* prev, const uint16_t* next, uint64_t numel,
+                             delta_index_t index_type, void* out_idx, uint16_t* out_val,
+                             uint64_t capacity, uint64_t* d_count, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * delta_extract_multi — Sec. 5.1, a tensor list in one index space.
+ *   prev_ptrs, next_ptrs, numels
+ *                 host arrays of `num_tensors` entries: device pointers of
+ *                 each tensor's two copies and its number of words (0 is
+ *                 allowed).  Tensor t's word i has global index
+ *                 base_t + i, base_t = numels[0] + ... + numels[t-1].
+ *   out_idx       device int64 [capacity]: global indices, ascending.
+ *   out_val       device uint16 [capacity].
+ *   d_count       device uint64: true total.
+ *   d_tensor_offsets
+ *                 device uint64 [num_tensors + 1] or NULL: entry t is the
+ *                 output position of tensor t's first entry (= number of
+ *                 entries with global index < base_t), entry T the total.
+ *   workspace     delta_extract_multi_workspace_bytes(numels, num_tensors).
+ */
+delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
+                                   const uint16_t* const* next_ptrs, const uint64_t* numels,
+                                   int32_t num_tensors, int64_t* out_idx, uint16_t* out_val,
+                                   uint64_t capacity, uint64_t* d_count,
+                                   uint64_t* d_tensor_offsets, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * delta_apply — Sec. 5.1 / 5.2: weights[idx[k]] = val[k] for k < count,
+ * in place.  Indices must be distinct (any order); entries with an index
+ * outside [0, numel) are skipped and set *d_error_flag (if not NULL) to a
+ * nonzero value (the flag is only ever set, never cleared).
+ *   weights       device uint16 [numel], updated in place.
+ *   idx, val      device streams of `count` entries (int32 or int64 idx).
+ */
+delta_status_t delta_apply(uint16_t* weights, uint64_t numel, delta_index_t index_type,
+                           const void* idx, const uint16_t* val, uint64_t count,
+                           uint32_t* d_error_flag, hipStream_t stream);
+
+/*
+ * delta_apply_multi — the scatter over a tensor list addressed by global
+ * int64 indices as produced by delta_extract_multi (same tensor order and
+ * sizes).  weight_ptrs and numels are host arrays of `num_tensors`
+ * entries.  workspace: delta_apply_multi_workspace_bytes(num_tensors).
+ */
+delta_status_t delta_apply_multi(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                 int32_t num_tensors, const int64_t* idx, const uint16_t* val,
+                                 uint64_t count, uint32_t* d_error_flag, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * delta_apply_checked — Sec. 5.2: a delta is activated only on top of the
+ * version it was made against.  Returns DELTA_ERR_VERSION without touching
+ * the weights when active_version != base_version; otherwise as
+ * delta_apply.
+ */
+delta_status_t delta_apply_checked(uint16_t* weights, uint64_t numel, delta_index_t index_type,
+                                   const void* idx, const uint16_t* val, uint64_t count,
+                                   uint32_t* d_error_flag, uint64_t active_version,
+                                   uint64_t base_version, hipStream_t stream);
+
+/* Options of the chunked pipeline. */
+typedef struct {
+  uint64_t chunk_elems; /* words of the global index space per chunk (> 0) */
+  int32_t num_streams;  /* streams used round-robin, 1..16 */
+  int32_t reserved;
+} delta_pipeline_opts_t;
+
+/* Device staging bytes delta_extract_pipelined needs: per stream, one
+ * chunk's worst-case output plus its workspace. */
+size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
+                                    const delta_pipeline_opts_t* opts);
+
+/*
+ * delta_extract_pipelined — Sec. 5.2: extract_multi over the tensor list,
+ * chunk by chunk, with each chunk's (idx, val) copied into pinned host
+ * memory as soon as that chunk is done, while later chunks are extracted
+ * on the other streams.  The host output equals delta_extract_multi's.
+ *   streams       host array of opts->num_streams HIP streams.
+ *   d_staging     device scratch of delta_pipeline_staging_bytes(...).
+ *   h_idx, h_val  pinned host arrays (hipHostMalloc / pin_memory) of
+ *                 h_capacity entries.
+ *   h_count       host: the true total.
+ * Host-synchronous: returns after every copy has landed.  Returns
+ * DELTA_ERR_CAPACITY (with *h_count = true total, the first h_capacity
+ * entries written) if the output did not fit.
+ */
+delta_status_t delta_extract_pipelined(const uint16_t* const* prev_ptrs,
+                                       const uint16_t* const* next_ptrs, const uint64_t* numels,
+                                       int32_t num_tensors, const delta_pipeline_opts_t* opts,
+                                       hipStream_t* streams, void* d_staging,
+                                       size_t staging_bytes, int64_t* h_idx, uint16_t* h_val,
+                                       uint64_t h_capacity, uint64_t* h_count);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AURORA_DELTA_H */

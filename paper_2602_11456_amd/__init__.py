@@ -1,0 +1,328 @@
+"""MI355X (gfx950) sparse delta checkpoints of bf16 weights, after AuroraRL
+(arXiv 2602.11456) Sec. 5.1-5.2.
+
+The functions here are a thin binding over the C ABI of
+``libaurora_delta.so`` (include/aurora_delta.h) with the same names: they
+check and marshal torch tensors (device pointers, sizes, the current HIP
+stream) and allocate outputs and workspaces with torch's allocator.  Every
+step of extraction and application runs in the library's HIP kernels;
+there is no Python or CPU fallback.
+
+    idx, val = delta_extract(prev, new)              # one tensor
+    idx, val, offs = delta_extract_multi(prevs, news) # global int64 indices
+    delta_apply(rollout, idx, val)                   # in place, bit-exact
+    delta_apply_multi(rollouts, idx, val)
+    h_idx, h_val = delta_extract_pipelined(prevs, news)  # pinned host output
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import List, Optional, Sequence, Tuple
+
+import torch
+
+from . import _abi
+
+__all__ = [
+    "DeltaError", "library", "delta_extract", "delta_extract_into", "delta_extract_multi",
+    "delta_extract_multi_into", "delta_apply", "delta_apply_multi", "delta_apply_checked",
+    "delta_extract_pipelined", "delta_extract_workspace_bytes",
+    "delta_extract_multi_workspace_bytes", "delta_apply_multi_workspace_bytes",
+    "delta_pipeline_staging_bytes", "MultiPlan",
+]
+
+
+class DeltaError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        self.detail = detail
+        name = library().delta_status_string(status).decode()
+        super().__init__(f"{name}: {detail}")
+
+
+def library() -> ctypes.CDLL:
+    return _abi.load()
+
+
+def _check(status: int) -> None:
+    if status != _abi.DELTA_OK:
+        raise DeltaError(status, library().delta_last_error().decode())
+
+
+def _stream(stream: Optional[torch.cuda.Stream]) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _words(t: torch.Tensor, what: str) -> int:
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a GPU tensor")
+    if t.element_size() != 2:
+        raise TypeError(f"{what} must hold 16-bit words (bf16), got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return t.data_ptr()
+
+
+def _u64_array(values) -> ctypes.Array:
+    return (ctypes.c_uint64 * max(len(values), 1))(*[int(v) for v in values])
+
+
+def _ptr_array(values) -> ctypes.Array:
+    return (ctypes.c_void_p * max(len(values), 1))(*[int(v) for v in values])
+
+
+def _index_type(dtype: torch.dtype) -> int:
+    if dtype == torch.int32:
+        return _abi.DELTA_INDEX_I32
+    if dtype == torch.int64:
+        return _abi.DELTA_INDEX_I64
+    raise TypeError("index dtype must be torch.int32 or torch.int64")
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns 512-byte aligned blocks
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+# --------------------------------------------------------------- sizes
+
+def delta_extract_workspace_bytes(numel: int) -> int:
+    return int(library().delta_extract_workspace_bytes(int(numel)))
+
+
+def delta_extract_multi_workspace_bytes(numels: Sequence[int]) -> int:
+    arr = _u64_array(numels)
+    return int(library().delta_extract_multi_workspace_bytes(arr, len(numels)))
+
+
+def delta_apply_multi_workspace_bytes(num_tensors: int) -> int:
+    return int(library().delta_apply_multi_workspace_bytes(int(num_tensors)))
+
+
+def delta_pipeline_staging_bytes(numels: Sequence[int], chunk_elems: int, num_streams: int) -> int:
+    opts = _abi.delta_pipeline_opts_t(int(chunk_elems), int(num_streams), 0)
+    return int(library().delta_pipeline_staging_bytes(_u64_array(numels), len(numels),
+                                                      ctypes.byref(opts)))
+
+
+# ------------------------------------------------------------- extract
+
+def delta_extract_into(prev: torch.Tensor, new: torch.Tensor, out_idx: torch.Tensor,
+                       out_val: torch.Tensor, d_count: torch.Tensor, workspace: torch.Tensor,
+                       stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Enqueue ``delta_extract`` into preallocated buffers (no sync).
+
+    ``out_idx`` (int32/int64) and ``out_val`` (16-bit) give the capacity,
+    ``d_count`` is a 1-element int64/uint64 GPU tensor that receives the
+    true count."""
+    if prev.shape != new.shape:
+        raise ValueError("prev and new differ in shape")
+    cap = min(out_idx.numel(), out_val.numel())
+    _check(library().delta_extract(
+        _words(prev, "prev"), _words(new, "new"), prev.numel(), _index_type(out_idx.dtype),
+        out_idx.data_ptr(), _words(out_val, "out_val"), cap, d_count.data_ptr(),
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def _default_capacity(n: int) -> int:
+    return min(n, n // 16 + 4096)
+
+
+def delta_extract(prev: torch.Tensor, new: torch.Tensor, index_dtype: torch.dtype = torch.int64,
+                  capacity: Optional[int] = None,
+                  stream: Optional[torch.cuda.Stream] = None
+                  ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Sorted positions and new words of every changed bf16 word of one
+    tensor (Sec. 5.1).  Synchronises the stream to read the count; if the
+    first capacity was too small the call is repeated with the exact one."""
+    n = prev.numel()
+    dev = prev.device
+    ws = _workspace(delta_extract_workspace_bytes(n), dev)
+    cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    cap = _default_capacity(n) if capacity is None else int(capacity)
+    for _ in range(2):
+        idx = torch.empty(cap, dtype=index_dtype, device=dev)
+        val = torch.empty(cap, dtype=prev.dtype, device=dev)
+        delta_extract_into(prev, new, idx, val, cnt, ws, stream)
+        (stream or torch.cuda.current_stream()).synchronize()
+        k = int(cnt.item())
+        if k <= cap:
+            return idx[:k], val[:k]
+        cap = k
+    raise AssertionError("count changed between two runs on the same input")
+
+
+class MultiPlan:
+    """Host arrays (pointers, sizes) of a tensor list, built once and reused
+    for every call on the same tensors."""
+
+    def __init__(self, prevs: Sequence[torch.Tensor], news: Sequence[torch.Tensor]):
+        if len(prevs) != len(news):
+            raise ValueError("prev and new lists differ in length")
+        for i, (p, q) in enumerate(zip(prevs, news)):
+            if p.shape != q.shape:
+                raise ValueError(f"tensor {i}: prev and new differ in shape")
+        self.T = len(prevs)
+        self.numels = [p.numel() for p in prevs]
+        self.total = sum(self.numels)
+        self.prev_ptrs = _ptr_array([_words(p, f"prev[{i}]") for i, p in enumerate(prevs)])
+        self.next_ptrs = _ptr_array([_words(q, f"new[{i}]") for i, q in enumerate(news)])
+        self.numel_arr = _u64_array(self.numels)
+        self.device = prevs[0].device if prevs else torch.device("cuda")
+        self.workspace_bytes = delta_extract_multi_workspace_bytes(self.numels)
+        self._keep = (list(prevs), list(news))
+
+
+def delta_extract_multi_into(plan: MultiPlan, out_idx: torch.Tensor, out_val: torch.Tensor,
+                             d_count: torch.Tensor, workspace: torch.Tensor,
+                             d_offsets: Optional[torch.Tensor] = None,
+                             stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Enqueue ``delta_extract_multi`` into preallocated buffers (no sync)."""
+    if out_idx.dtype != torch.int64:
+        raise TypeError("multi-tensor indices are int64")
+    if d_offsets is not None and d_offsets.numel() < plan.T + 1:
+        raise ValueError("d_offsets needs num_tensors + 1 entries")
+    cap = min(out_idx.numel(), out_val.numel())
+    _check(library().delta_extract_multi(
+        plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, plan.T, out_idx.data_ptr(),
+        _words(out_val, "out_val"), cap, d_count.data_ptr(),
+        d_offsets.data_ptr() if d_offsets is not None else None, workspace.data_ptr(),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def delta_extract_multi(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tensor],
+                        capacity: Optional[int] = None,
+                        stream: Optional[torch.cuda.Stream] = None
+                        ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Global int64 indices, new words and per-tensor output offsets
+    (T + 1 entries) over a tensor list (Sec. 5.1 block offsets)."""
+    plan = MultiPlan(prevs, news)
+    dev = plan.device
+    ws = _workspace(plan.workspace_bytes, dev)
+    cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    offs = torch.zeros(plan.T + 1, dtype=torch.int64, device=dev)
+    cap = _default_capacity(plan.total) if capacity is None else int(capacity)
+    dtype = prevs[0].dtype if plan.T else torch.bfloat16
+    for _ in range(2):
+        idx = torch.empty(cap, dtype=torch.int64, device=dev)
+        val = torch.empty(cap, dtype=dtype, device=dev)
+        delta_extract_multi_into(plan, idx, val, cnt, ws, offs, stream)
+        (stream or torch.cuda.current_stream()).synchronize()
+        k = int(cnt.item())
+        if k <= cap:
+            return idx[:k], val[:k], offs
+        cap = k
+    raise AssertionError("count changed between two runs on the same input")
+
+
+# --------------------------------------------------------------- apply
+
+def delta_apply(weights: torch.Tensor, idx: torch.Tensor, val: torch.Tensor,
+                error_flag: Optional[torch.Tensor] = None, check: bool = False,
+                stream: Optional[torch.cuda.Stream] = None) -> None:
+    """``weights.view(-1)[idx] = val`` in place on the GPU (Sec. 5.1/5.2).
+
+    Out-of-range indices are skipped and set ``error_flag`` (a 1-element
+    int32 GPU tensor).  With ``check=True`` the call synchronises and raises
+    ``DeltaError(DELTA_ERR_OUT_OF_RANGE)`` if any index was skipped."""
+    if idx.numel() != val.numel():
+        raise ValueError("idx and val differ in length")
+    if idx.numel() and not idx.is_contiguous():
+        raise ValueError("idx must be contiguous")
+    flag = error_flag
+    if check and flag is None:
+        flag = torch.zeros(1, dtype=torch.int32, device=weights.device)
+    _check(library().delta_apply(
+        _words(weights, "weights"), weights.numel(), _index_type(idx.dtype), idx.data_ptr(),
+        _words(val, "val"), idx.numel(), flag.data_ptr() if flag is not None else None,
+        _stream(stream)))
+    if check:
+        (stream or torch.cuda.current_stream()).synchronize()
+        if int(flag.item()) != 0:
+            raise DeltaError(_abi.DELTA_ERR_OUT_OF_RANGE, "an index was outside the tensor")
+
+
+def delta_apply_checked(weights: torch.Tensor, idx: torch.Tensor, val: torch.Tensor,
+                        active_version: int, base_version: int,
+                        error_flag: Optional[torch.Tensor] = None,
+                        stream: Optional[torch.cuda.Stream] = None) -> None:
+    """delta_apply, refused (DELTA_ERR_VERSION) unless the active version is
+    the delta's base version (Sec. 5.2)."""
+    _check(library().delta_apply_checked(
+        _words(weights, "weights"), weights.numel(), _index_type(idx.dtype), idx.data_ptr(),
+        _words(val, "val"), idx.numel(),
+        error_flag.data_ptr() if error_flag is not None else None, int(active_version),
+        int(base_version), _stream(stream)))
+
+
+def delta_apply_multi(weights: Sequence[torch.Tensor], idx: torch.Tensor, val: torch.Tensor,
+                      error_flag: Optional[torch.Tensor] = None, check: bool = False,
+                      workspace: Optional[torch.Tensor] = None,
+                      stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Scatter global int64 indices into a tensor list in place."""
+    if idx.dtype != torch.int64:
+        raise TypeError("multi-tensor indices are int64")
+    T = len(weights)
+    ptrs = _ptr_array([_words(w, f"weights[{i}]") for i, w in enumerate(weights)])
+    numels = _u64_array([w.numel() for w in weights])
+    dev = weights[0].device if T else idx.device
+    need = delta_apply_multi_workspace_bytes(T)
+    ws = workspace if workspace is not None else _workspace(need, dev)
+    flag = error_flag
+    if check and flag is None:
+        flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    _check(library().delta_apply_multi(
+        ptrs, numels, T, idx.data_ptr(), _words(val, "val"), idx.numel(),
+        flag.data_ptr() if flag is not None else None, ws.data_ptr(),
+        ws.numel() * ws.element_size(), _stream(stream)))
+    if check:
+        (stream or torch.cuda.current_stream()).synchronize()
+        if int(flag.item()) != 0:
+            raise DeltaError(_abi.DELTA_ERR_OUT_OF_RANGE, "an index was outside the tensors")
+
+
+# ------------------------------------------------------------ pipeline
+
+def delta_extract_pipelined(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tensor],
+                            chunk_elems: int = 1 << 27, num_streams: int = 4,
+                            h_idx: Optional[torch.Tensor] = None,
+                            h_val: Optional[torch.Tensor] = None,
+                            staging: Optional[torch.Tensor] = None,
+                            streams: Optional[List[torch.cuda.Stream]] = None
+                            ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Chunked extract with pinned host output (Sec. 5.2).  Returns the host
+    (idx, val) views of the filled part.  Host-synchronous."""
+    plan = MultiPlan(prevs, news)
+    dev = plan.device
+    if streams is None:
+        streams = [torch.cuda.Stream(device=dev) for _ in range(num_streams)]
+    if len(streams) != num_streams:
+        raise ValueError("need one stream per pipeline lane")
+    need = delta_pipeline_staging_bytes(plan.numels, chunk_elems, num_streams)
+    stage = staging if staging is not None else _workspace(need, dev)
+    if h_idx is None:
+        cap = _default_capacity(plan.total)
+        h_idx = torch.empty(cap, dtype=torch.int64, pin_memory=True)
+        h_val = torch.empty(cap, dtype=torch.bfloat16, pin_memory=True)
+    if h_val is None or h_idx.dtype != torch.int64 or h_val.element_size() != 2:
+        raise TypeError("h_idx must be int64 and h_val 16-bit")
+    cap = min(h_idx.numel(), h_val.numel())
+    opts = _abi.delta_pipeline_opts_t(int(chunk_elems), int(num_streams), 0)
+    handles = _ptr_array([s.cuda_stream for s in streams])
+    count = ctypes.c_uint64(0)
+    # the pipeline's streams must see work already queued on the caller's stream
+    torch.cuda.current_stream().synchronize()
+    status = library().delta_extract_pipelined(
+        plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, plan.T, ctypes.byref(opts), handles,
+        stage.data_ptr(), stage.numel(), h_idx.data_ptr(), h_val.data_ptr(), cap,
+        ctypes.byref(count))
+    if status == _abi.DELTA_ERR_CAPACITY and h_idx is not None:
+        k = count.value
+        h_idx2 = torch.empty(k, dtype=torch.int64, pin_memory=True)
+        h_val2 = torch.empty(k, dtype=h_val.dtype, pin_memory=True)
+        return delta_extract_pipelined(prevs, news, chunk_elems, num_streams, h_idx2, h_val2,
+                                       stage, streams)
+    _check(status)
+    k = count.value
+    return h_idx[:k], h_val[:k]

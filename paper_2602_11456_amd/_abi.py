@@ -1,0 +1,80 @@
+"""ctypes declarations of the C ABI in include/aurora_delta.h.
+
+Loading fails loudly: there is no fallback implementation of any entry
+point.  Build the library first (``python -m paper_2602_11456_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libaurora_delta.so")
+
+DELTA_OK = 0
+DELTA_ERR_INVALID_ARG = 1
+DELTA_ERR_INDEX_OVERFLOW = 2
+DELTA_ERR_CAPACITY = 3
+DELTA_ERR_OUT_OF_RANGE = 4
+DELTA_ERR_VERSION = 5
+DELTA_ERR_WORKSPACE = 6
+DELTA_ERR_HIP = 7
+
+DELTA_INDEX_I32 = 0
+DELTA_INDEX_I64 = 1
+
+ABI_VERSION = 1
+
+P = ctypes.c_void_p
+U64 = ctypes.c_uint64
+I32 = ctypes.c_int32
+SZ = ctypes.c_size_t
+STATUS = ctypes.c_int
+
+
+class delta_pipeline_opts_t(ctypes.Structure):
+    _fields_ = [("chunk_elems", ctypes.c_uint64),
+                ("num_streams", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+# name -> (restype, argtypes); every symbol the header declares
+SIGNATURES = {
+    "delta_abi_version": (ctypes.c_int, []),
+    "delta_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "delta_last_error": (ctypes.c_char_p, []),
+    "delta_extract_workspace_bytes": (SZ, [U64]),
+    "delta_extract_multi_workspace_bytes": (SZ, [P, I32]),
+    "delta_apply_multi_workspace_bytes": (SZ, [I32]),
+    "delta_extract": (STATUS, [P, P, U64, ctypes.c_int, P, P, U64, P, P, SZ, P]),
+    "delta_extract_multi": (STATUS, [P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
+    "delta_apply": (STATUS, [P, U64, ctypes.c_int, P, P, U64, P, P]),
+    "delta_apply_multi": (STATUS, [P, P, I32, P, P, U64, P, P, SZ, P]),
+    "delta_apply_checked": (STATUS, [P, U64, ctypes.c_int, P, P, U64, P, U64, U64, P]),
+    "delta_pipeline_staging_bytes": (SZ, [P, I32, ctypes.POINTER(delta_pipeline_opts_t)]),
+    "delta_extract_pipelined": (STATUS, [P, P, P, I32, ctypes.POINTER(delta_pipeline_opts_t), P,
+                                         P, SZ, P, P, U64, P]),
+}
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libaurora_delta.so and declare every entry point."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build it with `python -m paper_2602_11456_amd.build` "
+            "(there is no fallback implementation)")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    if lib.delta_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"ABI version mismatch: library {lib.delta_abi_version()}, "
+                           f"binding {ABI_VERSION}")
+    _lib = lib
+    return lib

@@ -1,0 +1,320 @@
+// C ABI entry points: argument validation, workspace carving, tensor tables
+// and launch order.  Every computation runs in the kernels of extract.hip
+// and apply.hip; this file only prepares and enqueues them.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/aurora_delta.h"
+#include "delta_internal.h"
+
+using namespace aurora;
+
+static thread_local std::string g_last_error;
+
+namespace aurora {
+
+void set_error(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+}  // namespace aurora
+
+namespace {
+
+delta_status_t fail(delta_status_t s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+delta_status_t fail(delta_status_t s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+delta_status_t ok() {
+  g_last_error.clear();
+  return DELTA_OK;
+}
+
+delta_status_t hip_fail(hipError_t e, const char* what) {
+  return fail(DELTA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool odd(const void* p) { return ((uintptr_t)p & 1u) != 0; }
+
+// Host-side description of one slice of a tensor list.
+struct Slice {
+  const uint16_t* prev;
+  const uint16_t* next;
+  uint64_t n;
+  uint64_t base;
+  uint32_t tensor;   // index in the caller's list
+};
+
+// Builds the descriptor table of the non-empty `slices` (tile ranges,
+// alignment, the tensor_offsets slots each slice's first tile writes).
+// Returns the total number of tiles.
+uint64_t build_descs(const std::vector<Slice>& slices, std::vector<TensorDesc>& out) {
+  out.clear();
+  uint64_t tiles = 0;
+  uint32_t next_slot = 0;   // first tensor_offsets slot not yet owned
+  for (const Slice& s : slices) {
+    if (s.n == 0) continue;
+    TensorDesc d;
+    memset(&d, 0, sizeof(d));
+    d.prev = s.prev;
+    d.next = s.next;
+    d.n = s.n;
+    d.base = s.base;
+    d.first_tile = tiles;
+    const uint32_t hp = head_words(s.prev), hq = head_words(s.next);
+    d.vec = (hp == hq) ? 1u : 0u;
+    d.head = d.vec ? hp : 0u;
+    d.off_lo = next_slot;
+    d.slot = s.tensor;
+    next_slot = s.tensor + 1;
+    tiles += tiles_for(d.n, d.head);
+    out.push_back(d);
+  }
+  return tiles;
+}
+
+delta_status_t enqueue_extract(const std::vector<Slice>& slices, uint32_t num_tensors,
+                               bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
+                               uint64_t* d_count, uint64_t* d_offsets, void* workspace,
+                               size_t workspace_needed, hipStream_t stream) {
+  std::vector<TensorDesc> descs;
+  const uint64_t tiles = build_descs(slices, descs);
+  if (tiles * (uint64_t)kThreads > 0xFFFFFFFFull)
+    return fail(DELTA_ERR_INVALID_ARG, "too many words for one launch (%llu tiles)",
+                (unsigned long long)tiles);
+  const WorkspaceLayout L = workspace_layout(tiles, descs.size());
+  if (L.total > workspace_needed)
+    return fail(DELTA_ERR_WORKSPACE, "internal: workspace bound %zu < layout %zu",
+                workspace_needed, L.total);
+  char* ws = (char*)workspace;
+  Control* ctrl = (Control*)ws;
+  uint64_t* states = (uint64_t*)(ws + L.states);
+  uint32_t* map = (uint32_t*)(ws + L.map);
+  TensorDesc* table = (TensorDesc*)(ws + L.table);
+
+  hipError_t e = launch_reset(ctrl, states, tiles, d_count, d_offsets,
+                              d_offsets ? num_tensors + 1 : 0, stream);
+  if (e != hipSuccess) return hip_fail(e, "reset launch");
+  if (tiles == 0) return ok();
+  ExtractArgs a;
+  memset(&a, 0, sizeof(a));
+  a.num_tiles = tiles;
+  a.num_tensors = num_tensors;
+  a.out_idx = out_idx;
+  a.out_val = out_val;
+  a.capacity = capacity;
+  a.d_count = d_count;
+  a.d_tensor_offsets = d_offsets;
+  a.states = states;
+  a.ctrl = ctrl;
+  if (descs.size() > 1) {
+    e = launch_upload_words((const uint64_t*)descs.data(), descs.size() * sizeof(TensorDesc) / 8,
+                            (uint64_t*)table, stream);
+    if (e != hipSuccess) return hip_fail(e, "table upload launch");
+    e = launch_build_tile_map(table, (uint32_t)descs.size(), map, stream);
+    if (e != hipSuccess) return hip_fail(e, "tile map launch");
+    a.table = table;
+    a.tile_map = map;
+  } else {
+    a.table = nullptr;
+    a.tile_map = nullptr;
+    a.single = descs[0];
+  }
+  e = launch_extract(a, idx64, stream);
+  if (e != hipSuccess) return hip_fail(e, "extract launch");
+  return ok();
+}
+
+size_t multi_workspace_bound(const uint64_t* numels, int32_t T) {
+  uint64_t tiles = 0;
+  for (int32_t t = 0; t < T; ++t) tiles += tiles_bound(numels[t]);
+  return workspace_layout(tiles, (uint64_t)(T > 0 ? T : 0)).total;
+}
+
+delta_status_t check_workspace(void* ws, size_t have, size_t need) {
+  if (need == 0) return DELTA_OK;
+  if (!ws) return fail(DELTA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if ((uintptr_t)ws % kAlign)
+    return fail(DELTA_ERR_WORKSPACE, "workspace must be %zu-byte aligned", kAlign);
+  if (have < need)
+    return fail(DELTA_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return DELTA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int delta_abi_version(void) { return AURORA_DELTA_ABI_VERSION; }
+
+const char* delta_status_string(int status) {
+  switch (status) {
+    case DELTA_OK: return "DELTA_OK";
+    case DELTA_ERR_INVALID_ARG: return "DELTA_ERR_INVALID_ARG";
+    case DELTA_ERR_INDEX_OVERFLOW: return "DELTA_ERR_INDEX_OVERFLOW";
+    case DELTA_ERR_CAPACITY: return "DELTA_ERR_CAPACITY";
+    case DELTA_ERR_OUT_OF_RANGE: return "DELTA_ERR_OUT_OF_RANGE";
+    case DELTA_ERR_VERSION: return "DELTA_ERR_VERSION";
+    case DELTA_ERR_WORKSPACE: return "DELTA_ERR_WORKSPACE";
+    case DELTA_ERR_HIP: return "DELTA_ERR_HIP";
+    default: return "DELTA_ERR_UNKNOWN";
+  }
+}
+
+const char* delta_last_error(void) { return g_last_error.c_str(); }
+
+size_t delta_extract_workspace_bytes(uint64_t numel) {
+  return workspace_layout(tiles_bound(numel), 1).total;
+}
+
+size_t delta_extract_multi_workspace_bytes(const uint64_t* numels, int32_t num_tensors) {
+  if (num_tensors < 0 || (num_tensors > 0 && !numels)) return 0;
+  return multi_workspace_bound(numels, num_tensors);
+}
+
+size_t delta_apply_multi_workspace_bytes(int32_t num_tensors) {
+  if (num_tensors < 0) return 0;
+  return align_up(8 * ((size_t)num_tensors + 1)) + align_up(8 * (size_t)num_tensors);
+}
+
+delta_status_t delta_extract(const uint16_t* prev, const uint16_t* next, uint64_t numel,
+                             delta_index_t index_type, void* out_idx, uint16_t* out_val,
+                             uint64_t capacity, uint64_t* d_count, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  if (index_type != DELTA_INDEX_I32 && index_type != DELTA_INDEX_I64)
+    return fail(DELTA_ERR_INVALID_ARG, "unknown index type %d", (int)index_type);
+  if (!d_count) return fail(DELTA_ERR_INVALID_ARG, "d_count is NULL");
+  if (numel > 0 && (!prev || !next)) return fail(DELTA_ERR_INVALID_ARG, "prev/next is NULL");
+  if (odd(prev) || odd(next)) return fail(DELTA_ERR_INVALID_ARG, "prev/next not 2-byte aligned");
+  if (capacity > 0 && (!out_idx || !out_val))
+    return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val is NULL with capacity %llu",
+                (unsigned long long)capacity);
+  if (index_type == DELTA_INDEX_I32 && numel > 0 && numel - 1 > 0x7FFFFFFFull)
+    return fail(DELTA_ERR_INDEX_OVERFLOW, "numel %llu needs int64 indices",
+                (unsigned long long)numel);
+  const size_t need = delta_extract_workspace_bytes(numel);
+  delta_status_t s = check_workspace(workspace, workspace_bytes, need);
+  if (s != DELTA_OK) return s;
+  std::vector<Slice> slices{{prev, next, numel, 0, 0}};
+  return enqueue_extract(slices, 1, index_type == DELTA_INDEX_I64, out_idx, out_val, capacity,
+                         d_count, nullptr, workspace, need, stream);
+}
+
+delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
+                                   const uint16_t* const* next_ptrs, const uint64_t* numels,
+                                   int32_t num_tensors, int64_t* out_idx, uint16_t* out_val,
+                                   uint64_t capacity, uint64_t* d_count,
+                                   uint64_t* d_tensor_offsets, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
+  if (num_tensors < 0) return fail(DELTA_ERR_INVALID_ARG, "num_tensors < 0");
+  if (num_tensors > 0 && (!prev_ptrs || !next_ptrs || !numels))
+    return fail(DELTA_ERR_INVALID_ARG, "tensor arrays are NULL");
+  if (!d_count) return fail(DELTA_ERR_INVALID_ARG, "d_count is NULL");
+  if (capacity > 0 && (!out_idx || !out_val))
+    return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val is NULL with capacity %llu",
+                (unsigned long long)capacity);
+  std::vector<Slice> slices;
+  slices.reserve(num_tensors);
+  uint64_t base = 0;
+  for (int32_t t = 0; t < num_tensors; ++t) {
+    if (numels[t] > 0 && (!prev_ptrs[t] || !next_ptrs[t]))
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: NULL pointer", t);
+    if (odd(prev_ptrs[t]) || odd(next_ptrs[t]))
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: not 2-byte aligned", t);
+    if (base + numels[t] < base) return fail(DELTA_ERR_INVALID_ARG, "total size overflows");
+    slices.push_back({prev_ptrs[t], next_ptrs[t], numels[t], base, (uint32_t)t});
+    base += numels[t];
+  }
+  if (base > 0 && base - 1 > 0x7FFFFFFFFFFFFFFFull)
+    return fail(DELTA_ERR_INDEX_OVERFLOW, "total size exceeds int64");
+  const size_t need = multi_workspace_bound(numels, num_tensors);
+  delta_status_t s = check_workspace(workspace, workspace_bytes, need);
+  if (s != DELTA_OK) return s;
+  return enqueue_extract(slices, (uint32_t)num_tensors, true, out_idx, out_val, capacity,
+                         d_count, d_tensor_offsets, workspace, need, stream);
+}
+
+delta_status_t delta_apply(uint16_t* weights, uint64_t numel, delta_index_t index_type,
+                           const void* idx, const uint16_t* val, uint64_t count,
+                           uint32_t* d_error_flag, hipStream_t stream) {
+  if (index_type != DELTA_INDEX_I32 && index_type != DELTA_INDEX_I64)
+    return fail(DELTA_ERR_INVALID_ARG, "unknown index type %d", (int)index_type);
+  if (count > 0 && (!idx || !val)) return fail(DELTA_ERR_INVALID_ARG, "idx/val is NULL");
+  if (count > 0 && numel > 0 && !weights) return fail(DELTA_ERR_INVALID_ARG, "weights is NULL");
+  if (odd(weights) || odd(val)) return fail(DELTA_ERR_INVALID_ARG, "not 2-byte aligned");
+  if ((uintptr_t)idx % (index_type == DELTA_INDEX_I64 ? 8 : 4))
+    return fail(DELTA_ERR_INVALID_ARG, "idx not aligned to its element size");
+  hipError_t e = launch_apply(weights, numel, index_type == DELTA_INDEX_I64, idx, val, count,
+                              d_error_flag, stream);
+  if (e != hipSuccess) return hip_fail(e, "apply launch");
+  return ok();
+}
+
+delta_status_t delta_apply_checked(uint16_t* weights, uint64_t numel, delta_index_t index_type,
+                                   const void* idx, const uint16_t* val, uint64_t count,
+                                   uint32_t* d_error_flag, uint64_t active_version,
+                                   uint64_t base_version, hipStream_t stream) {
+  if (active_version != base_version)
+    return fail(DELTA_ERR_VERSION, "delta made against version %llu, active version is %llu",
+                (unsigned long long)base_version, (unsigned long long)active_version);
+  return delta_apply(weights, numel, index_type, idx, val, count, d_error_flag, stream);
+}
+
+delta_status_t delta_apply_multi(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                 int32_t num_tensors, const int64_t* idx, const uint16_t* val,
+                                 uint64_t count, uint32_t* d_error_flag, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  if (num_tensors < 0) return fail(DELTA_ERR_INVALID_ARG, "num_tensors < 0");
+  if (num_tensors > 0 && (!weight_ptrs || !numels))
+    return fail(DELTA_ERR_INVALID_ARG, "tensor arrays are NULL");
+  if (count > 0 && (!idx || !val)) return fail(DELTA_ERR_INVALID_ARG, "idx/val is NULL");
+  if (odd(val) || ((uintptr_t)idx % 8)) return fail(DELTA_ERR_INVALID_ARG, "idx/val misaligned");
+  std::vector<uint64_t> bases(num_tensors + 1);
+  std::vector<uint64_t> ptrs(num_tensors);
+  uint64_t base = 0;
+  for (int32_t t = 0; t < num_tensors; ++t) {
+    if (numels[t] > 0 && !weight_ptrs[t])
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: NULL pointer", t);
+    if (odd(weight_ptrs[t])) return fail(DELTA_ERR_INVALID_ARG, "tensor %d: odd address", t);
+    bases[t] = base;
+    ptrs[t] = (uint64_t)(uintptr_t)weight_ptrs[t];
+    if (base + numels[t] < base) return fail(DELTA_ERR_INVALID_ARG, "total size overflows");
+    base += numels[t];
+  }
+  bases[num_tensors] = base;
+  const size_t need = delta_apply_multi_workspace_bytes(num_tensors);
+  delta_status_t s = check_workspace(workspace, workspace_bytes, need);
+  if (s != DELTA_OK) return s;
+  if (count == 0) return ok();
+  char* ws = (char*)workspace;
+  uint64_t* d_bases = (uint64_t*)ws;
+  uint64_t* d_ptrs = (uint64_t*)(ws + align_up(8 * ((size_t)num_tensors + 1)));
+  hipError_t e = launch_upload_words(bases.data(), bases.size(), d_bases, stream);
+  if (e == hipSuccess && num_tensors > 0)
+    e = launch_upload_words(ptrs.data(), ptrs.size(), d_ptrs, stream);
+  if (e != hipSuccess) return hip_fail(e, "table upload launch");
+  e = launch_apply_multi(d_bases, (uint16_t* const*)d_ptrs, (uint32_t)num_tensors, idx, val,
+                         count, d_error_flag, stream);
+  if (e != hipSuccess) return hip_fail(e, "apply_multi launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,146 @@
+"""The C ABI library without a GPU: it loads, exports every declared symbol,
+and rejects bad arguments before anything is launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2602_11456_amd import _abi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "aurora_delta.h")
+
+FAKE = 0x100000   # a non-null, aligned address that is never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(delta_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_abi.LIB_PATH):
+        from paper_2602_11456_amd import build
+        build.build()
+    return _abi.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in _abi.SIGNATURES, f"binding does not declare {n}"
+
+
+def test_binding_declares_nothing_extra():
+    assert set(_abi.SIGNATURES) == set(declared_functions())
+
+
+def test_version_and_strings(lib):
+    assert lib.delta_abi_version() == _abi.ABI_VERSION
+    assert lib.delta_status_string(0) == b"DELTA_OK"
+    assert lib.delta_status_string(_abi.DELTA_ERR_VERSION) == b"DELTA_ERR_VERSION"
+    assert lib.delta_status_string(99) == b"DELTA_ERR_UNKNOWN"
+
+
+def test_workspace_sizes(lib):
+    a = lib.delta_extract_workspace_bytes(0)
+    b = lib.delta_extract_workspace_bytes(8192)
+    c = lib.delta_extract_workspace_bytes(1 << 30)
+    assert 0 < a <= b < c
+    assert a % 256 == 0 and c % 256 == 0
+    # 8 B state + 4 B map per 8192-word tile, plus a few table rows
+    assert c < (1 << 30) // 8192 * 16 + 4096
+    numels = (ctypes.c_uint64 * 3)(0, 100, 1 << 20)
+    m = lib.delta_extract_multi_workspace_bytes(numels, 3)
+    assert m >= lib.delta_extract_workspace_bytes(1 << 20)
+    assert lib.delta_apply_multi_workspace_bytes(3) >= 7 * 8
+    opts = _abi.delta_pipeline_opts_t(1 << 27, 4, 0)
+    st = lib.delta_pipeline_staging_bytes(numels, 3, ctypes.byref(opts))
+    assert st >= 4 * ((1 << 20) + 100) * 10
+    bad = _abi.delta_pipeline_opts_t(0, 4, 0)
+    assert lib.delta_pipeline_staging_bytes(numels, 3, ctypes.byref(bad)) == 0
+
+
+def test_extract_validation(lib):
+    cnt = FAKE
+    ws = FAKE
+    # null d_count
+    assert lib.delta_extract(FAKE, FAKE, 10, 0, FAKE, FAKE, 10, None, ws, 1 << 20, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    # unknown index type
+    assert lib.delta_extract(FAKE, FAKE, 10, 7, FAKE, FAKE, 10, cnt, ws, 1 << 20, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    # odd address
+    assert lib.delta_extract(FAKE + 1, FAKE, 10, 0, FAKE, FAKE, 10, cnt, ws, 1 << 20, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    # null inputs with numel > 0
+    assert lib.delta_extract(None, FAKE, 10, 0, FAKE, FAKE, 10, cnt, ws, 1 << 20, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    # int32 indices for more than 2^31 words
+    assert lib.delta_extract(FAKE, FAKE, 2**31 + 1, _abi.DELTA_INDEX_I32, FAKE, FAKE, 10, cnt,
+                             ws, 1 << 30, None) == _abi.DELTA_ERR_INDEX_OVERFLOW
+    assert b"int64" in lib.delta_last_error()
+    # exactly 2^31 words still fit int32 (numel - 1 == INT32_MAX): fails later, on workspace
+    assert lib.delta_extract(FAKE, FAKE, 2**31, _abi.DELTA_INDEX_I32, FAKE, FAKE, 10, cnt,
+                             ws, 0, None) == _abi.DELTA_ERR_WORKSPACE
+    # workspace too small / missing / misaligned
+    assert lib.delta_extract(FAKE, FAKE, 10, 0, FAKE, FAKE, 10, cnt, ws, 16, None) == \
+        _abi.DELTA_ERR_WORKSPACE
+    assert lib.delta_extract(FAKE, FAKE, 10, 0, FAKE, FAKE, 10, cnt, None, 1 << 20, None) == \
+        _abi.DELTA_ERR_WORKSPACE
+    assert lib.delta_extract(FAKE, FAKE, 10, 0, FAKE, FAKE, 10, cnt, ws + 8, 1 << 20, None) == \
+        _abi.DELTA_ERR_WORKSPACE
+    # outputs missing with a nonzero capacity
+    assert lib.delta_extract(FAKE, FAKE, 10, 0, None, FAKE, 10, cnt, ws, 1 << 20, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+
+
+def test_extract_multi_validation(lib):
+    P = ctypes.c_void_p
+    prevs = (P * 2)(FAKE, FAKE)
+    nexts = (P * 2)(FAKE, None)
+    numels = (ctypes.c_uint64 * 2)(10, 10)
+    assert lib.delta_extract_multi(prevs, nexts, numels, 2, FAKE, FAKE, 10, FAKE, None, FAKE,
+                                   1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
+    assert b"tensor 1" in lib.delta_last_error()
+    assert lib.delta_extract_multi(prevs, prevs, numels, -1, FAKE, FAKE, 10, FAKE, None, FAKE,
+                                   1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_extract_multi(prevs, prevs, numels, 2, FAKE, FAKE, 10, FAKE, None, FAKE,
+                                   64, None) == _abi.DELTA_ERR_WORKSPACE
+
+
+def test_apply_validation(lib):
+    assert lib.delta_apply(FAKE, 10, 3, FAKE, FAKE, 5, None, None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_apply(FAKE, 10, 1, FAKE + 4, FAKE, 5, None, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # int64 idx must be 8-aligned
+    assert lib.delta_apply(FAKE, 10, 1, None, FAKE, 5, None, None) == _abi.DELTA_ERR_INVALID_ARG
+    # base-version check happens on the host, before any launch
+    assert lib.delta_apply_checked(FAKE, 10, 1, FAKE, FAKE, 5, None, 7, 6, None) == \
+        _abi.DELTA_ERR_VERSION
+    assert b"version 6" in lib.delta_last_error()
+    P = ctypes.c_void_p
+    ws = (P * 1)(None)
+    numels = (ctypes.c_uint64 * 1)(10)
+    assert lib.delta_apply_multi(ws, numels, 1, FAKE, FAKE, 5, None, FAKE, 1 << 20, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+
+
+def test_pipeline_validation(lib):
+    P = ctypes.c_void_p
+    prevs = (P * 1)(FAKE)
+    numels = (ctypes.c_uint64 * 1)(100)
+    streams = (P * 4)(None, None, None, None)
+    cnt = ctypes.c_uint64(0)
+    bad = _abi.delta_pipeline_opts_t(100, 0, 0)
+    assert lib.delta_extract_pipelined(prevs, prevs, numels, 1, ctypes.byref(bad), streams,
+                                       FAKE, 1 << 30, FAKE, FAKE, 10, ctypes.byref(cnt)) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    opts = _abi.delta_pipeline_opts_t(100, 4, 0)
+    assert lib.delta_extract_pipelined(prevs, prevs, numels, 1, ctypes.byref(opts), streams,
+                                       FAKE, 8, FAKE, FAKE, 10, ctypes.byref(cnt)) == \
+        _abi.DELTA_ERR_WORKSPACE
