@@ -3,6 +3,7 @@
 // and apply.hip; this file only prepares and enqueues them.
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <string>
@@ -27,6 +28,12 @@ void set_error(const char* fmt, ...) {
 }
 
 void clear_error() { g_last_error.clear(); }
+
+uint32_t spin_limit_from_env() {
+  const char* v = getenv("AURORA_DELTA_SPIN_LIMIT");
+  if (!v || !*v) return kDefaultSpinLimit;
+  return (uint32_t)strtoul(v, nullptr, 10);
+}
 
 }  // namespace aurora
 
@@ -125,6 +132,7 @@ delta_status_t enqueue_extract(const std::vector<Slice>& slices, uint32_t num_te
   a.d_tensor_offsets = d_offsets;
   a.states = states;
   a.ctrl = ctrl;
+  a.spin_limit = spin_limit_from_env();
   if (descs.size() > 1) {
     e = launch_upload_words((const uint64_t*)descs.data(), descs.size() * sizeof(TensorDesc) / 8,
                             (uint64_t*)table, stream);

@@ -25,6 +25,9 @@ constexpr int kChunks = 4;
 constexpr int kGroupsPerWave = kChunks * 64;
 constexpr int kGroupsPerTile = kWaves * kGroupsPerWave;
 constexpr int kElemsPerTile = kGroupsPerTile * 8;
+// Kept entries a tile stages in LDS before writing them out (4 bytes each);
+// tiles with more changed words re-read their data to write.
+constexpr int kStageCap = 4096;
 
 // Tile state word of the decoupled look-back: the top two bits say what the
 // low 62 bits hold.  One 64-bit word is written and read with single
@@ -52,7 +55,7 @@ static_assert(sizeof(TensorDesc) == 64, "TensorDesc layout");
 
 // Device-side control words at the start of every workspace.
 struct Control {
-  uint32_t tile_counter;  // dynamic tile ids
+  uint32_t fallbacks;     // look-back waits that ended in counting a tile directly
   uint32_t pad[63];
 };
 static_assert(sizeof(Control) == 256, "Control layout");
@@ -119,7 +122,13 @@ struct ExtractArgs {
   uint64_t* d_tensor_offsets;  // nullable
   uint64_t* states;
   Control* ctrl;
+  uint32_t spin_limit;         // look-back polls before counting a silent predecessor
 };
+
+// Default look-back patience; AURORA_DELTA_SPIN_LIMIT overrides it (tests
+// set 0 to drive every wait through the fallback).
+constexpr uint32_t kDefaultSpinLimit = 128;
+uint32_t spin_limit_from_env();
 
 hipError_t launch_reset(Control* ctrl, uint64_t* states, uint64_t num_tiles,
                         uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets,

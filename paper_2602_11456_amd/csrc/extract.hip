@@ -3,9 +3,8 @@
 // words, in ascending position order, as two dense streams (AuroraRL
 // Sec. 5.1, "Sparse encoding").
 //
-// Per workgroup (one tile of 8192 words):
-//   1. take a tile id from a device counter (dynamic ids: a tile only ever
-//      waits on tiles that were handed out earlier, hence already running);
+// Per workgroup (one tile of 8192 words, tile id = workgroup id):
+//   1. find the tile's tensor slice (tile -> slice map for tensor lists);
 //   2. read 16 bytes of each copy per lane per unrolled step;
 //   3. compare 16-bit words, count changes per lane, turn the counts into
 //      lane prefixes with four ballots + mbcnt (bit-sliced prefix sum);
@@ -14,6 +13,13 @@
 //      "Single-pass Parallel Prefix Scan with Decoupled Look-back", 2016)
 //      to learn how many kept words precede the tile;
 //   6. write the kept (index, word) pairs at their final positions.
+//
+// Forward progress does not rest on the order in which workgroups are
+// dispatched: a look-back that has waited `spin_limit` polls for a
+// predecessor that has published nothing counts that predecessor's tile
+// itself (one wavefront reads its 8192 words) and goes on.  A tile id
+// counter would also guarantee progress, but one device-scope atomic per
+// tile on a single address serialises the whole grid at the memory side.
 #include "delta_internal.h"
 
 namespace aurora {
@@ -82,51 +88,110 @@ __device__ __forceinline__ uint32_t changed_mask(const u32x4& p, const u32x4& q)
   return m;
 }
 
-template <typename IdxT, bool kMulti>
-__global__ __launch_bounds__(kThreads) void extract_kernel(ExtractArgs a) {
-  __shared__ uint32_t s_tile;
-  __shared__ uint32_t s_wave_total[kWaves];
-  __shared__ uint64_t s_tile_excl;
-
-  if (threadIdx.x == 0)
-    s_tile = __hip_atomic_fetch_add(&a.ctrl->tile_counter, 1u, __ATOMIC_RELAXED,
-                                    __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  const uint64_t tile = s_tile;
-  const TensorDesc d = kMulti ? a.table[a.tile_map[tile]] : a.single;
-  const uint64_t local_tile = tile - d.first_tile;
-
-  const uint32_t lane = lane_id();
-  const uint32_t wave = threadIdx.x >> 6;
-  const int64_t g0 = (int64_t)(local_tile * kGroupsPerTile) + wave * kGroupsPerWave + lane;
-
-  u32x4 p[kChunks], q[kChunks];
+__device__ __forceinline__ uint32_t wave_sum32(uint32_t v) {
 #pragma unroll
-  for (int u = 0; u < kChunks; ++u) load_group(d, g0 + 64 * u, p[u], q[u]);
+  for (int s = 32; s >= 1; s >>= 1) v += __shfl_xor(v, s);
+  return v;
+}
 
-  uint32_t mask[kChunks];
-  uint32_t lane_prefix[kChunks];
+template <bool kMulti>
+__device__ __forceinline__ TensorDesc tile_desc(const ExtractArgs& a, uint64_t tile) {
+  return kMulti ? a.table[a.tile_map[tile]] : a.single;
+}
+
+// Changed words of tile t, counted by one wavefront (look-back fallback).
+// A cold path: plain 2-byte loads keep its register footprint small.
+template <bool kMulti>
+__device__ __forceinline__ uint32_t count_tile_wave(const ExtractArgs& a, uint64_t t, uint32_t lane) {
+  const TensorDesc d = tile_desc<kMulti>(a, t);
+  const int64_t e0 = (int64_t)((t - d.first_tile) * kElemsPerTile) - (int64_t)d.head;
+  uint32_t c = 0;
+#pragma unroll 1
+  for (int64_t i = lane; i < kElemsPerTile; i += 64) {
+    const int64_t e = e0 + i;
+    if (e >= 0 && e < (int64_t)d.n) c += (d.prev[e] != d.next[e]) ? 1u : 0u;
+  }
+  return wave_sum32(c);
+}
+
+// Per-lane state of one tile after the compare: which words changed and
+// where they go inside the tile's output run.
+struct TileScan {
+  u32x4 q[kChunks];               // new words
+  uint32_t mask[kChunks];         // bit j: word j of the lane's group changed
+  uint32_t lane_prefix[kChunks];  // kept words of lower lanes in the same chunk
   uint32_t chunk_base[kChunks];   // wave-uniform: kept words of earlier chunks
-  uint32_t wave_total = 0;
+  uint32_t wave_total;
+};
+
+__device__ __forceinline__ void scan_tile(const TensorDesc& d, int64_t g0, TileScan& s) {
+  u32x4 p[kChunks];
+#pragma unroll
+  for (int u = 0; u < kChunks; ++u) load_group(d, g0 + 64 * u, p[u], s.q[u]);
+  s.wave_total = 0;
 #pragma unroll
   for (int u = 0; u < kChunks; ++u) {
-    mask[u] = changed_mask(p[u], q[u]);
-    const uint32_t c = __popc(mask[u]);
+    s.mask[u] = changed_mask(p[u], s.q[u]);
+    // bit-sliced prefix sum of the per-lane counts (0..8) over the wavefront
+    const uint32_t c = __popc(s.mask[u]);
     const uint64_t b0 = __ballot(c & 1), b1 = __ballot(c & 2);
     const uint64_t b2 = __ballot(c & 4), b3 = __ballot(c & 8);
-    lane_prefix[u] = mbcnt64(b0) + 2 * mbcnt64(b1) + 4 * mbcnt64(b2) + 8 * mbcnt64(b3);
-    chunk_base[u] = wave_total;
-    wave_total += __popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2) + 8 * __popcll(b3);
+    s.lane_prefix[u] = mbcnt64(b0) + 2 * mbcnt64(b1) + 4 * mbcnt64(b2) + 8 * mbcnt64(b3);
+    s.chunk_base[u] = s.wave_total;
+    s.wave_total += __popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2) + 8 * __popcll(b3);
   }
-  if (lane == 0) s_wave_total[wave] = wave_total;
-  __syncthreads();
+}
+
+__device__ __forceinline__ uint16_t word_of(const u32x4& q, int j) {
+  const uint32_t dw = q[j >> 1];
+  return (uint16_t)((j & 1) ? (dw >> 16) : (dw & 0xFFFFu));
+}
+
+template <typename IdxT, bool kMulti>
+__global__ __launch_bounds__(kThreads) void extract_kernel(ExtractArgs a) {
+  __shared__ uint32_t s_wave_total[kWaves];
+  __shared__ uint64_t s_tile_excl;
+  // kept entries of the tile in output order: (new word << 16) | word offset in tile
+  __shared__ uint32_t s_stage[kStageCap];
+
+  const uint64_t tile = blockIdx.x;
+  const TensorDesc d = tile_desc<kMulti>(a, tile);
+  const uint64_t local_tile = tile - d.first_tile;
+  const uint32_t lane = lane_id();
+  const uint32_t wave = threadIdx.x >> 6;
+  const uint32_t lane_group = wave * kGroupsPerWave + lane;   // group of chunk 0 in the tile
+  const int64_t g0 = (int64_t)(local_tile * kGroupsPerTile) + lane_group;
+  // slice word index of the tile's word 0 (negative inside a misaligned head)
+  const int64_t tile_e0 = (int64_t)(local_tile * kElemsPerTile) - (int64_t)d.head;
 
   uint32_t wave_excl = 0, tile_total = 0;
+  {
+    TileScan s;
+    scan_tile(d, g0, s);
+    if (lane == 0) s_wave_total[wave] = s.wave_total;
+    __syncthreads();
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    const uint32_t t = s_wave_total[w];
-    wave_excl += (w < (int)wave) ? t : 0u;
-    tile_total += t;
+    for (int w = 0; w < kWaves; ++w) {
+      const uint32_t t = s_wave_total[w];
+      wave_excl += (w < (int)wave) ? t : 0u;
+      tile_total += t;
+    }
+    // Stage the kept entries in LDS now, so nothing of the tile stays live
+    // in registers through the look-back; the global writes after it are
+    // then contiguous runs.
+    if (tile_total <= (uint32_t)kStageCap) {
+#pragma unroll
+      for (int u = 0; u < kChunks; ++u) {
+        uint32_t m = s.mask[u];
+        uint32_t r = wave_excl + s.chunk_base[u] + s.lane_prefix[u];
+        const uint32_t w0 = (lane_group + 64 * u) * 8;
+        while (m) {
+          const int j = __builtin_ctz(m);
+          m &= m - 1;
+          s_stage[r++] = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
+        }
+      }
+    }
   }
 
   // Decoupled look-back, done by wavefront 0.
@@ -139,15 +204,30 @@ __global__ __launch_bounds__(kThreads) void extract_kernel(ExtractArgs a) {
       int64_t top = (int64_t)tile - 1;
       for (;;) {
         const int64_t t = top - (int64_t)lane;
-        uint64_t st, need, prefix_lanes;
+        uint64_t st = (t >= 0) ? load_state(&a.states[t]) : kStatePrefix;
+        uint64_t need, prefix_lanes;
+        uint32_t spins = 0;
         for (;;) {
-          st = (t >= 0) ? load_state(&a.states[t]) : kStatePrefix;
           const uint64_t empty = __ballot((st & kStateFlagMask) == kStateEmpty);
           prefix_lanes = __ballot((st & kStateFlagMask) == kStatePrefix);
           // lanes that count: up to and including the nearest full prefix
           need = prefix_lanes ? (((prefix_lanes & (0 - prefix_lanes)) << 1) - 1) : ~0ull;
-          if ((empty & need) == 0) break;
+          const uint64_t pending = empty & need;
+          if (pending == 0) break;
+          if (spins >= a.spin_limit) {
+            // count the nearest silent predecessor ourselves
+            const uint32_t l = (uint32_t)__builtin_ctzll(pending);
+            const uint32_t agg = count_tile_wave<kMulti>(a, (uint64_t)(top - (int64_t)l), lane);
+            if (lane == l) st = kStateAggregate | agg;
+            if (lane == 0)
+              __hip_atomic_fetch_add(&a.ctrl->fallbacks, 1u, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+            spins = 0;
+            continue;
+          }
+          ++spins;
           __builtin_amdgcn_s_sleep(1);
+          if ((pending >> lane) & 1ull) st = load_state(&a.states[t]);
         }
         const uint64_t v = ((need >> lane) & 1ull) ? (st & kStateValueMask) : 0ull;
         excl += wave_sum64(v);
@@ -177,23 +257,37 @@ __global__ __launch_bounds__(kThreads) void extract_kernel(ExtractArgs a) {
     }
   }
 
-  // Scatter-free write: every kept word goes to its final slot.
   IdxT* out_idx = reinterpret_cast<IdxT*>(a.out_idx);
-#pragma unroll
-  for (int u = 0; u < kChunks; ++u) {
-    uint32_t m = mask[u];
-    if (m == 0) continue;
-    uint64_t pos = tile_excl + wave_excl + chunk_base[u] + lane_prefix[u];
-    const int64_t e0 = 8 * (g0 + 64 * u) - (int64_t)d.head;
-    while (m) {
-      const int j = __builtin_ctz(m);
-      m &= m - 1;
+  const int64_t out_base = (int64_t)d.base + tile_e0;
+  if (tile_total <= (uint32_t)kStageCap) {
+    // contiguous run [tile_excl, tile_excl + tile_total) of the output
+    for (uint32_t r = threadIdx.x; r < tile_total; r += kThreads) {
+      const uint64_t pos = tile_excl + r;
       if (pos < a.capacity) {
-        const uint32_t dw = q[u][j >> 1];
-        out_idx[pos] = (IdxT)((int64_t)d.base + e0 + j);
-        a.out_val[pos] = (uint16_t)((j & 1) ? (dw >> 16) : (dw & 0xFFFFu));
+        const uint32_t e = s_stage[r];
+        out_idx[pos] = (IdxT)(out_base + (e & 0xFFFFu));
+        a.out_val[pos] = (uint16_t)(e >> 16);
       }
-      ++pos;
+    }
+  } else {
+    // more kept words than the stage holds: read the tile again and write
+    // each entry from registers
+    TileScan s;
+    scan_tile(d, g0, s);
+#pragma unroll
+    for (int u = 0; u < kChunks; ++u) {
+      uint32_t m = s.mask[u];
+      uint64_t pos = tile_excl + wave_excl + s.chunk_base[u] + s.lane_prefix[u];
+      const int64_t e0 = out_base + (int64_t)(lane_group + 64 * u) * 8;
+      while (m) {
+        const int j = __builtin_ctz(m);
+        m &= m - 1;
+        if (pos < a.capacity) {
+          out_idx[pos] = (IdxT)(e0 + j);
+          a.out_val[pos] = word_of(s.q[u], j);
+        }
+        ++pos;
+      }
     }
   }
 }
@@ -206,7 +300,7 @@ __global__ void reset_kernel(Control* ctrl, uint64_t* states, uint64_t num_tiles
   if (d_offsets)
     for (uint64_t i = i0; i < num_offsets; i += stride) d_offsets[i] = 0;
   if (i0 == 0) {
-    ctrl->tile_counter = 0;
+    ctrl->fallbacks = 0;
     *d_count = 0;
   }
 }

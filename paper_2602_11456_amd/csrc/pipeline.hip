@@ -125,6 +125,7 @@ static hipError_t enqueue_chunk(const std::vector<ChunkSlice>& sl, char* stage,
   a.d_tensor_offsets = nullptr;
   a.states = states;
   a.ctrl = ctrl;
+  a.spin_limit = spin_limit_from_env();
   if (descs.size() > 1) {
     e = launch_upload_words((const uint64_t*)descs.data(), descs.size() * sizeof(TensorDesc) / 8,
                             (uint64_t*)table, stream);

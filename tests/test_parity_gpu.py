@@ -330,3 +330,29 @@ def test_pipeline_capacity_retry():
     ref_idx, ref_val, _, _ = oracle.extract_multi([host_u16(p) for p in prevs],
                                                   [host_u16(q) for q in news])
     np.testing.assert_array_equal(i.numpy(), ref_idx)
+
+
+@pytest.mark.parametrize("density", [0.01, 0.6])
+def test_lookback_fallback_forced(monkeypatch, density):
+    """Spin limit 0 (set from the host): every look-back that meets a
+    silent predecessor counts that tile itself.  The result must not
+    change, and the fallback must actually have run."""
+    monkeypatch.setenv("AURORA_DELTA_SPIN_LIMIT", "0")
+    prev, new = rand_pair(700 * TILE + 3, density, seed=17)
+    n = prev.numel()
+    ref_idx, ref_val, ref_cnt = oracle.extract(host_u16(prev), host_u16(new))
+    ws = torch.empty(ad.delta_extract_workspace_bytes(n), dtype=torch.uint8, device=DEV)
+    idx = torch.empty(n, dtype=torch.int64, device=DEV)
+    val = torch.empty(n, dtype=torch.bfloat16, device=DEV)
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    fallbacks = 0
+    for _ in range(3):
+        ad.delta_extract_into(prev, new, idx, val, cnt, ws)
+        torch.cuda.synchronize()
+        assert int(cnt.item()) == ref_cnt
+        np.testing.assert_array_equal(idx[:ref_cnt].cpu().numpy(), ref_idx)
+        np.testing.assert_array_equal(host_u16(val[:ref_cnt]), ref_val)
+        # the first word of the workspace counts fallbacks of the last call
+        fallbacks += int(ws[:4].view(torch.int32).item())
+    say("fallbacks", fallbacks)
+    assert fallbacks > 0
