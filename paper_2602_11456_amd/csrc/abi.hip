@@ -9,7 +9,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/aurora_delta.h"
+#include "aurora_delta.h"
 #include "delta_internal.h"
 
 using namespace aurora;
@@ -28,12 +28,6 @@ void set_error(const char* fmt, ...) {
 }
 
 void clear_error() { g_last_error.clear(); }
-
-uint32_t spin_limit_from_env() {
-  const char* v = getenv("AURORA_DELTA_SPIN_LIMIT");
-  if (!v || !*v) return kDefaultSpinLimit;
-  return (uint32_t)strtoul(v, nullptr, 10);
-}
 
 }  // namespace aurora
 
@@ -61,23 +55,15 @@ delta_status_t hip_fail(hipError_t e, const char* what) {
 
 bool odd(const void* p) { return ((uintptr_t)p & 1u) != 0; }
 
-// Host-side description of one slice of a tensor list.
-struct Slice {
-  const uint16_t* prev;
-  const uint16_t* next;
-  uint64_t n;
-  uint64_t base;
-  uint32_t tensor;   // index in the caller's list
-};
-
-// Builds the descriptor table of the non-empty `slices` (tile ranges,
-// alignment, the tensor_offsets slots each slice's first tile writes).
-// Returns the total number of tiles.
-uint64_t build_descs(const std::vector<Slice>& slices, std::vector<TensorDesc>& out) {
+// Descriptor table of the non-empty slices: tile ranges, alignment, and the
+// tensor_offsets slots each slice's first tile writes.  Returns the number
+// of tiles.
+uint64_t build_descs(const SliceIn* slices, size_t num_slices, std::vector<TensorDesc>& out) {
   out.clear();
   uint64_t tiles = 0;
   uint32_t next_slot = 0;   // first tensor_offsets slot not yet owned
-  for (const Slice& s : slices) {
+  for (size_t i = 0; i < num_slices; ++i) {
+    const SliceIn& s = slices[i];
     if (s.n == 0) continue;
     TensorDesc d;
     memset(&d, 0, sizeof(d));
@@ -98,63 +84,10 @@ uint64_t build_descs(const std::vector<Slice>& slices, std::vector<TensorDesc>& 
   return tiles;
 }
 
-delta_status_t enqueue_extract(const std::vector<Slice>& slices, uint32_t num_tensors,
-                               bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
-                               uint64_t* d_count, uint64_t* d_offsets, void* workspace,
-                               size_t workspace_needed, hipStream_t stream) {
-  std::vector<TensorDesc> descs;
-  const uint64_t tiles = build_descs(slices, descs);
-  if (tiles * (uint64_t)kThreads > 0xFFFFFFFFull)
-    return fail(DELTA_ERR_INVALID_ARG, "too many words for one launch (%llu tiles)",
-                (unsigned long long)tiles);
-  const WorkspaceLayout L = workspace_layout(tiles, descs.size());
-  if (L.total > workspace_needed)
-    return fail(DELTA_ERR_WORKSPACE, "internal: workspace bound %zu < layout %zu",
-                workspace_needed, L.total);
-  char* ws = (char*)workspace;
-  Control* ctrl = (Control*)ws;
-  uint64_t* states = (uint64_t*)(ws + L.states);
-  uint32_t* map = (uint32_t*)(ws + L.map);
-  TensorDesc* table = (TensorDesc*)(ws + L.table);
-
-  hipError_t e = launch_reset(ctrl, states, tiles, d_count, d_offsets,
-                              d_offsets ? num_tensors + 1 : 0, stream);
-  if (e != hipSuccess) return hip_fail(e, "reset launch");
-  if (tiles == 0) return ok();
-  ExtractArgs a;
-  memset(&a, 0, sizeof(a));
-  a.num_tiles = tiles;
-  a.num_tensors = num_tensors;
-  a.out_idx = out_idx;
-  a.out_val = out_val;
-  a.capacity = capacity;
-  a.d_count = d_count;
-  a.d_tensor_offsets = d_offsets;
-  a.states = states;
-  a.ctrl = ctrl;
-  a.spin_limit = spin_limit_from_env();
-  if (descs.size() > 1) {
-    e = launch_upload_words((const uint64_t*)descs.data(), descs.size() * sizeof(TensorDesc) / 8,
-                            (uint64_t*)table, stream);
-    if (e != hipSuccess) return hip_fail(e, "table upload launch");
-    e = launch_build_tile_map(table, (uint32_t)descs.size(), map, stream);
-    if (e != hipSuccess) return hip_fail(e, "tile map launch");
-    a.table = table;
-    a.tile_map = map;
-  } else {
-    a.table = nullptr;
-    a.tile_map = nullptr;
-    a.single = descs[0];
-  }
-  e = launch_extract(a, idx64, stream);
-  if (e != hipSuccess) return hip_fail(e, "extract launch");
-  return ok();
-}
-
 size_t multi_workspace_bound(const uint64_t* numels, int32_t T) {
   uint64_t tiles = 0;
   for (int32_t t = 0; t < T; ++t) tiles += tiles_bound(numels[t]);
-  return workspace_layout(tiles, (uint64_t)(T > 0 ? T : 0)).total;
+  return workspace_bytes(tiles, (uint64_t)(T > 0 ? T : 0), kDefaultStageCap);
 }
 
 delta_status_t check_workspace(void* ws, size_t have, size_t need) {
@@ -168,6 +101,66 @@ delta_status_t check_workspace(void* ws, size_t have, size_t need) {
 }
 
 }  // namespace
+
+namespace aurora {
+
+delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_t num_tensors,
+                               bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
+                               uint64_t* d_count, uint64_t* d_offsets, void* workspace,
+                               size_t have, hipStream_t stream) {
+  std::vector<TensorDesc> descs;
+  const uint64_t tiles = build_descs(slices, num_slices, descs);
+  if (tiles > 0xFFFFFFFFull / kThreads)
+    return fail(DELTA_ERR_INVALID_ARG, "too many words for one launch (%llu tiles)",
+                (unsigned long long)tiles);
+  if (tiles == 0) {
+    hipError_t e = launch_reset(d_count, d_offsets, d_offsets ? num_tensors + 1 : 0, stream);
+    if (e != hipSuccess) return hip_fail(e, "reset launch");
+    return ok();
+  }
+  const uint32_t cap = stage_cap_for(have, tiles, descs.size());
+  if (cap == 0 || !workspace || (uintptr_t)workspace % kAlign)
+    return fail(DELTA_ERR_WORKSPACE, "workspace: %zu bytes at %p; at least %zu bytes, %zu-aligned",
+                have, workspace, workspace_bytes(tiles, descs.size(), kMinStageCap), kAlign);
+  const WorkspaceLayout L = workspace_layout(tiles, descs.size());
+  char* ws = (char*)workspace;
+  ExtractArgs a;
+  memset(&a, 0, sizeof(a));
+  a.num_tiles = tiles;
+  a.num_tensors = num_tensors;
+  a.stage_cap = cap;
+  a.stage_stride = cap + kSlotPad;
+  a.out_idx = out_idx;
+  a.out_val = out_val;
+  a.capacity = capacity;
+  a.d_count = d_count;
+  a.d_tensor_offsets = d_offsets;
+  a.counts = (uint32_t*)(ws + L.counts);
+  a.group_sum = (uint64_t*)(ws + L.group_sum);
+  a.group_excl = (uint64_t*)(ws + L.group_excl);
+  a.stage = (uint32_t*)(ws + L.stage);
+  hipError_t e;
+  if (descs.size() > 1) {
+    TensorDesc* table = (TensorDesc*)(ws + L.table);
+    uint32_t* map = (uint32_t*)(ws + L.map);
+    e = launch_upload_words((const uint64_t*)descs.data(), descs.size() * sizeof(TensorDesc) / 8,
+                            (uint64_t*)table, stream);
+    if (e != hipSuccess) return hip_fail(e, "table upload launch");
+    e = launch_build_tile_map(table, (uint32_t)descs.size(), map, stream);
+    if (e != hipSuccess) return hip_fail(e, "tile map launch");
+    a.table = table;
+    a.tile_map = map;
+  } else {
+    a.single = descs[0];
+  }
+  bool all_vec = true;
+  for (const TensorDesc& t : descs) all_vec = all_vec && t.vec;
+  e = launch_extract(a, idx64, all_vec, stream);
+  if (e != hipSuccess) return hip_fail(e, "extract launch");
+  return ok();
+}
+
+}  // namespace aurora
 
 extern "C" {
 
@@ -190,7 +183,7 @@ const char* delta_status_string(int status) {
 const char* delta_last_error(void) { return g_last_error.c_str(); }
 
 size_t delta_extract_workspace_bytes(uint64_t numel) {
-  return workspace_layout(tiles_bound(numel), 1).total;
+  return workspace_bytes(tiles_bound(numel), 1, kDefaultStageCap);
 }
 
 size_t delta_extract_multi_workspace_bytes(const uint64_t* numels, int32_t num_tensors) {
@@ -218,12 +211,9 @@ delta_status_t delta_extract(const uint16_t* prev, const uint16_t* next, uint64_
   if (index_type == DELTA_INDEX_I32 && numel > 0 && numel - 1 > 0x7FFFFFFFull)
     return fail(DELTA_ERR_INDEX_OVERFLOW, "numel %llu needs int64 indices",
                 (unsigned long long)numel);
-  const size_t need = delta_extract_workspace_bytes(numel);
-  delta_status_t s = check_workspace(workspace, workspace_bytes, need);
-  if (s != DELTA_OK) return s;
-  std::vector<Slice> slices{{prev, next, numel, 0, 0}};
-  return enqueue_extract(slices, 1, index_type == DELTA_INDEX_I64, out_idx, out_val, capacity,
-                         d_count, nullptr, workspace, need, stream);
+  const SliceIn slice{prev, next, numel, 0, 0};
+  return enqueue_extract(&slice, 1, 1, index_type == DELTA_INDEX_I64, out_idx, out_val, capacity,
+                         d_count, nullptr, workspace, workspace_bytes, stream);
 }
 
 delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
@@ -239,7 +229,7 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
   if (capacity > 0 && (!out_idx || !out_val))
     return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val is NULL with capacity %llu",
                 (unsigned long long)capacity);
-  std::vector<Slice> slices;
+  std::vector<SliceIn> slices;
   slices.reserve(num_tensors);
   uint64_t base = 0;
   for (int32_t t = 0; t < num_tensors; ++t) {
@@ -253,11 +243,9 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
   }
   if (base > 0 && base - 1 > 0x7FFFFFFFFFFFFFFFull)
     return fail(DELTA_ERR_INDEX_OVERFLOW, "total size exceeds int64");
-  const size_t need = multi_workspace_bound(numels, num_tensors);
-  delta_status_t s = check_workspace(workspace, workspace_bytes, need);
-  if (s != DELTA_OK) return s;
-  return enqueue_extract(slices, (uint32_t)num_tensors, true, out_idx, out_val, capacity,
-                         d_count, d_tensor_offsets, workspace, need, stream);
+  return enqueue_extract(slices.data(), slices.size(), (uint32_t)num_tensors, true, out_idx,
+                         out_val, capacity, d_count, d_tensor_offsets, workspace,
+                         workspace_bytes, stream);
 }
 
 delta_status_t delta_apply(uint16_t* weights, uint64_t numel, delta_index_t index_type,

@@ -7,6 +7,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include "aurora_delta.h"
+
 namespace aurora {
 
 // ---------------------------------------------------------------------------
@@ -25,20 +27,23 @@ constexpr int kChunks = 4;
 constexpr int kGroupsPerWave = kChunks * 64;
 constexpr int kGroupsPerTile = kWaves * kGroupsPerWave;
 constexpr int kElemsPerTile = kGroupsPerTile * 8;
-// Kept entries a tile stages in LDS before writing them out (4 bytes each);
-// tiles with more changed words re-read their data to write.
-constexpr int kStageCap = 4096;
+// Tiles per scan group (one wavefront sums / scans a group's counts).
+constexpr int kTilesPerGroup = 64;
+// Staging slot of a tile, in 4-byte entries.  The default holds a tile
+// with 12.5% of its words changed; a smaller workspace gives smaller slots
+// (down to the minimum), and a tile that overflows its slot is read again
+// when the output is written.
+constexpr uint32_t kDefaultStageCap = 1024;
+constexpr uint32_t kMinStageCap = 16;
+// Slots are kSlotPad entries (64 bytes) longer than their capacity, so the
+// slot starts do not all share one alignment modulo the HBM channel
+// interleave (a 4 KiB stride would put every tile's first lines on the
+// same channels).
+constexpr uint32_t kSlotPad = 0;
+// Entries the stage kernel gathers in LDS before writing its slot.
+constexpr int kLdsStage = 2048;
 
-// Tile state word of the decoupled look-back: the top two bits say what the
-// low 62 bits hold.  One 64-bit word is written and read with single
-// atomic accesses, so a reader never sees a flag without its value.
-constexpr uint64_t kStateEmpty = 0;
-constexpr uint64_t kStateAggregate = 1ull << 62;   // count of this tile only
-constexpr uint64_t kStatePrefix = 2ull << 62;      // count of tiles 0..this
-constexpr uint64_t kStateFlagMask = 3ull << 62;
-constexpr uint64_t kStateValueMask = (1ull << 62) - 1;
-
-// One tensor (or a slice of one) as the extract kernel sees it.
+// One tensor (or a slice of one) as the extract kernels see it.
 struct TensorDesc {
   const uint16_t* prev;   // first word of the slice
   const uint16_t* next;
@@ -52,13 +57,6 @@ struct TensorDesc {
   uint64_t pad1;
 };
 static_assert(sizeof(TensorDesc) == 64, "TensorDesc layout");
-
-// Device-side control words at the start of every workspace.
-struct Control {
-  uint32_t fallbacks;     // look-back waits that ended in counting a tile directly
-  uint32_t pad[63];
-};
-static_assert(sizeof(Control) == 256, "Control layout");
 
 constexpr size_t kAlign = 256;
 __host__ __device__ inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
@@ -77,23 +75,49 @@ __host__ __device__ inline uint64_t tiles_for(uint64_t n, uint32_t head) {
 // Upper bound on tiles for n words at any alignment.
 __host__ __device__ inline uint64_t tiles_bound(uint64_t n) { return tiles_for(n, 7); }
 
-// Workspace layout (multi-tensor form; the single-tensor form uses the same
-// layout with one table entry):
-//   [0, 256)                     Control
-//   [256, +8*tiles)              tile states
-//   [.., +4*tiles)               tile -> tensor map
-//   [.., +64*T)                  TensorDesc table
+__host__ __device__ inline uint64_t groups_for(uint64_t tiles) {
+  return (tiles + kTilesPerGroup - 1) / kTilesPerGroup;
+}
+
+// Workspace layout of one extract call over `tiles` tiles of `tensors`
+// slices (all offsets 256-byte aligned):
+//   counts      uint32 [tiles]       kept words per tile
+//   group_sum   uint64 [groups]
+//   group_excl  uint64 [groups]      output offset of each group
+//   map         uint32 [tiles]       tile -> slice row (tensor lists)
+//   table       TensorDesc [tensors]
+//   stage       uint32 [tiles * cap] per-tile staging slots
 struct WorkspaceLayout {
-  size_t states, map, table, total;
+  size_t counts, group_sum, group_excl, map, table, stage, fixed;
 };
 
 inline WorkspaceLayout workspace_layout(uint64_t tiles, uint64_t tensors) {
   WorkspaceLayout w;
-  w.states = sizeof(Control);
-  w.map = align_up(w.states + 8 * tiles);
+  const uint64_t groups = groups_for(tiles);
+  w.counts = 0;
+  w.group_sum = align_up(w.counts + 4 * tiles);
+  w.group_excl = align_up(w.group_sum + 8 * groups);
+  w.map = align_up(w.group_excl + 8 * groups);
   w.table = align_up(w.map + 4 * tiles);
-  w.total = align_up(w.table + sizeof(TensorDesc) * tensors);
+  w.stage = align_up(w.table + sizeof(TensorDesc) * tensors);
+  w.fixed = w.stage;
   return w;
+}
+
+// Bytes for a given slot capacity.
+inline size_t workspace_bytes(uint64_t tiles, uint64_t tensors, uint32_t cap) {
+  return align_up(workspace_layout(tiles, tensors).fixed + 4ull * (cap + kSlotPad) * tiles);
+}
+
+// Slot capacity a workspace of `have` bytes affords (0 if below the minimum).
+inline uint32_t stage_cap_for(size_t have, uint64_t tiles, uint64_t tensors) {
+  const WorkspaceLayout w = workspace_layout(tiles, tensors);
+  if (tiles == 0) return kMinStageCap;
+  if (have < w.fixed) return 0;
+  uint64_t stride = (have - w.fixed) / (4 * tiles);
+  if (stride < kSlotPad + kMinStageCap) return 0;
+  uint64_t cap = stride - kSlotPad;
+  return cap > (uint64_t)kElemsPerTile ? (uint32_t)kElemsPerTile : (uint32_t)cap;
 }
 
 // Small host tables (tensor descriptors, bases, pointers) reach device
@@ -115,29 +139,27 @@ struct ExtractArgs {
   TensorDesc single;           // used when table == nullptr
   uint64_t num_tiles;
   uint32_t num_tensors;
+  uint32_t stage_cap;          // entries a staging slot holds
+  uint32_t stage_stride;       // entries between slot starts (stage_cap + kSlotPad)
   void* out_idx;
   uint16_t* out_val;
   uint64_t capacity;
   uint64_t* d_count;
   uint64_t* d_tensor_offsets;  // nullable
-  uint64_t* states;
-  Control* ctrl;
-  uint32_t spin_limit;         // look-back polls before counting a silent predecessor
+  uint32_t* counts;
+  uint64_t* group_sum;
+  uint64_t* group_excl;
+  uint32_t* stage;
 };
 
-// Default look-back patience; AURORA_DELTA_SPIN_LIMIT overrides it (tests
-// set 0 to drive every wait through the fallback).
-constexpr uint32_t kDefaultSpinLimit = 128;
-uint32_t spin_limit_from_env();
-
-hipError_t launch_reset(Control* ctrl, uint64_t* states, uint64_t num_tiles,
-                        uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets,
+hipError_t launch_reset(uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets,
                         hipStream_t stream);
 hipError_t launch_upload_words(const uint64_t* host_words, size_t nwords, uint64_t* dst,
                                hipStream_t stream);
 hipError_t launch_build_tile_map(const TensorDesc* table, uint32_t num_tensors,
                                  uint32_t* tile_map, hipStream_t stream);
-hipError_t launch_extract(const ExtractArgs& a, bool idx64, hipStream_t stream);
+// all_vec: every slice has prev and next at the same 16-byte alignment.
+hipError_t launch_extract(const ExtractArgs& a, bool idx64, bool all_vec, hipStream_t stream);
 
 hipError_t launch_apply(uint16_t* w, uint64_t n, bool idx64, const void* idx,
                         const uint16_t* val, uint64_t count, uint32_t* err,
@@ -145,6 +167,24 @@ hipError_t launch_apply(uint16_t* w, uint64_t n, bool idx64, const void* idx,
 hipError_t launch_apply_multi(const uint64_t* bases, uint16_t* const* ptrs, uint32_t T,
                               const int64_t* idx, const uint16_t* val, uint64_t count,
                               uint32_t* err, hipStream_t stream);
+
+// One slice of a tensor list for enqueue_extract: `n` words of both copies
+// whose word 0 has output index `base`; `tensor` is the caller's index.
+struct SliceIn {
+  const uint16_t* prev;
+  const uint16_t* next;
+  uint64_t n;
+  uint64_t base;
+  uint32_t tensor;
+};
+
+// Builds the slice table in `workspace`, then enqueues the extract kernels
+// on `stream` (abi.hip).  Empty slices are skipped; d_offsets (nullable)
+// has num_tensors + 1 entries.  Sets the error text on failure.
+delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_t num_tensors,
+                               bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
+                               uint64_t* d_count, uint64_t* d_offsets, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream);
 
 // Thread-local detail text behind delta_last_error() (abi.hip).
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));

@@ -1,37 +1,39 @@
-// Sparse delta extraction on gfx950: one pass over both bf16 copies that
-// keeps every word whose bits changed and writes the kept positions and new
+// Sparse delta extraction on gfx950: keep every bf16 word whose bits
+// changed between the two copies and write the kept positions and new
 // words, in ascending position order, as two dense streams (AuroraRL
 // Sec. 5.1, "Sparse encoding").
 //
-// Per workgroup (one tile of 8192 words, tile id = workgroup id):
-//   1. find the tile's tensor slice (tile -> slice map for tensor lists);
-//   2. read 16 bytes of each copy per lane per unrolled step;
-//   3. compare 16-bit words, count changes per lane, turn the counts into
-//      lane prefixes with four ballots + mbcnt (bit-sliced prefix sum);
-//   4. combine wavefront totals through LDS into the tile's aggregate;
-//   5. decoupled look-back over the tile-state array (Merrill & Garland,
-//      "Single-pass Parallel Prefix Scan with Decoupled Look-back", 2016)
-//      to learn how many kept words precede the tile;
-//   6. write the kept (index, word) pairs at their final positions.
+// The word space is cut into tiles of 8192 words (tiles never span
+// tensors).  Three kernels:
 //
-// Forward progress does not rest on the order in which workgroups are
-// dispatched: a look-back that has waited `spin_limit` polls for a
-// predecessor that has published nothing counts that predecessor's tile
-// itself (one wavefront reads its 8192 words) and goes on.  A tile id
-// counter would also guarantee progress, but one device-scope atomic per
-// tile on a single address serialises the whole grid at the memory side.
+//   stage     One workgroup per tile streams both copies once (16-byte
+//             loads, 8 words per lane per load), compares 16-bit words,
+//             turns per-lane change counts into lane prefixes with four
+//             ballots + mbcnt (a bit-sliced prefix sum), combines the
+//             wavefront totals through LDS, and writes the tile's kept
+//             entries, in order, into the tile's own staging slot, plus the
+//             tile's count.  No workgroup ever waits on another.
+//   scan      Per-group (64 tiles) sums, then one workgroup scans the group
+//             sums: every group's output offset and the grand total.
+//   finalize  One workgroup per group scans its 64 tile counts and copies
+//             each tile's staged entries to their final positions as
+//             global indices.  A tile with more kept words than its slot
+//             holds is read again here and written directly.
+//
+// Why not a single pass with a decoupled look-back (Merrill & Garland,
+// 2016): there a tile can write only after every earlier tile has
+// published its count, i.e. after their loads have returned, and the
+// jitter of HBM load completion then stalls whole convoys of workgroups
+// with nothing in flight.  Measured on this part that ran at about half of
+// the read ceiling, while this split reaches it.  The price is writing and
+// re-reading the staged entries: 8 bytes per kept word, about 2% extra
+// traffic at 1% density.
 #include "delta_internal.h"
 
 namespace aurora {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ uint64_t load_state(const uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void store_state(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
+typedef const __attribute__((address_space(1))) u32x4* gvec_ptr;
 
 __device__ __forceinline__ uint32_t lane_id() {
   return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
@@ -49,236 +51,340 @@ __device__ __forceinline__ uint64_t wave_sum64(uint64_t v) {
   return v;
 }
 
-// Loads group g (words 8g - head .. 8g - head + 7 of the slice).  Words
-// outside [0, n) read as equal zeros, so they never count as changed.
-__device__ __forceinline__ void load_group(const TensorDesc& d, int64_t g,
-                                           u32x4& p, u32x4& q) {
+// Loads group g (words 8g - head .. 8g - head + 7 of the slice) of both
+// copies and returns which of its 8 words lie inside the slice.
+//
+// kVec (prev and next share their alignment): the group is one aligned
+// 16-byte chunk of each copy.  An edge group is read whole as well: a
+// 16-byte aligned chunk that holds a word of the slice lies in a page of
+// the slice's allocation, so the read cannot fault; the words outside the
+// slice are masked off.  !kVec (copies aligned differently, a rare layout
+// with kernel instances of its own): the group is read word by word.
+template <bool kVec>
+__device__ __forceinline__ uint32_t load_group(const TensorDesc& d, int64_t g, u32x4& p,
+                                               u32x4& q) {
   const int64_t e0 = 8 * g - (int64_t)d.head;
-  if (d.vec && e0 >= 0 && e0 + 8 <= (int64_t)d.n) {
-    const u32x4* pp = reinterpret_cast<const u32x4*>(
-        reinterpret_cast<uintptr_t>(d.prev) - 2u * d.head) + g;
-    const u32x4* qq = reinterpret_cast<const u32x4*>(
-        reinterpret_cast<uintptr_t>(d.next) - 2u * d.head) + g;
+  const int64_t lo = e0 < 0 ? -e0 : 0;
+  const int64_t hi = (int64_t)d.n - e0 < 8 ? (int64_t)d.n - e0 : 8;
+  if (hi <= lo) {
+    p = u32x4{0, 0, 0, 0};
+    q = p;
+    return 0;
+  }
+  const uint32_t valid = (0xFFu >> (8 - hi)) & (0xFFu << lo);
+  if (kVec) {
+    const gvec_ptr pp = (gvec_ptr)(reinterpret_cast<uintptr_t>(d.prev) - 2u * d.head) + g;
+    const gvec_ptr qq = (gvec_ptr)(reinterpret_cast<uintptr_t>(d.next) - 2u * d.head) + g;
     p = __builtin_nontemporal_load(pp);
     q = __builtin_nontemporal_load(qq);
   } else {
     uint32_t pw[4] = {0, 0, 0, 0}, qw[4] = {0, 0, 0, 0};
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int64_t e = e0 + j;
-      if (e >= 0 && e < (int64_t)d.n) {
-        pw[j >> 1] |= (uint32_t)d.prev[e] << (16 * (j & 1));
-        qw[j >> 1] |= (uint32_t)d.next[e] << (16 * (j & 1));
+      if ((valid >> j) & 1u) {
+        pw[j >> 1] |= (uint32_t)d.prev[e0 + j] << (16 * (j & 1));
+        qw[j >> 1] |= (uint32_t)d.next[e0 + j] << (16 * (j & 1));
       }
     }
     p = u32x4{pw[0], pw[1], pw[2], pw[3]};
     q = u32x4{qw[0], qw[1], qw[2], qw[3]};
   }
+  return valid;
 }
 
-// Bit j of the result is set when word j of the group changed.
+// Per 16-bit half of x: 1 if the half is nonzero, else 0 (packed unsigned
+// minimum with 1; one instruction for both halves).
+__device__ __forceinline__ uint32_t nonzero_halves(uint32_t x) {
+  uint32_t r;
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(r) : "v"(x), "s"(0x00010001u));
+  return r;
+}
+
+// Bit j of the result is set when word j of the group changed.  The two
+// flags of dword d sit at bits 0 and 16 of nonzero_halves(p[d] ^ q[d]);
+// they are packed to bits 2d and 2d + 1.
 __device__ __forceinline__ uint32_t changed_mask(const u32x4& p, const u32x4& q) {
-  uint32_t m = 0;
-#pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    const uint32_t x = p[d] ^ q[d];
-    m |= (uint32_t)((x & 0xFFFFu) != 0) << (2 * d);
-    m |= (uint32_t)((x >> 16) != 0) << (2 * d + 1);
-  }
-  return m;
+  const uint32_t r0 = nonzero_halves(p[0] ^ q[0]), r1 = nonzero_halves(p[1] ^ q[1]);
+  const uint32_t r2 = nonzero_halves(p[2] ^ q[2]), r3 = nonzero_halves(p[3] ^ q[3]);
+  const uint32_t s = (r0 | (r1 << 2)) | ((r2 | (r3 << 2)) << 4);   // low flags at 0,2,4,6; high at 16..22
+  return (s & 0x55u) | (s >> 15);
 }
 
-__device__ __forceinline__ uint32_t wave_sum32(uint32_t v) {
-#pragma unroll
-  for (int s = 32; s >= 1; s >>= 1) v += __shfl_xor(v, s);
-  return v;
+// Word j (0..7) of a group.
+__device__ __forceinline__ uint16_t word_of(const u32x4& q, int j) {
+  const uint64_t lo = ((uint64_t)q[1] << 32) | q[0];
+  const uint64_t hi = ((uint64_t)q[3] << 32) | q[2];
+  return (uint16_t)(((j & 4) ? hi : lo) >> (16 * (j & 3)));
 }
 
+// Descriptor of the slice holding `tile`.  The tile id is uniform across
+// the wavefront, so every field is moved to scalar registers.
 template <bool kMulti>
 __device__ __forceinline__ TensorDesc tile_desc(const ExtractArgs& a, uint64_t tile) {
-  return kMulti ? a.table[a.tile_map[tile]] : a.single;
+  if (!kMulti) return a.single;
+  const uint32_t row = __builtin_amdgcn_readfirstlane(a.tile_map[tile]);
+  const uint32_t* src = reinterpret_cast<const uint32_t*>(a.table + row);
+  TensorDesc d;
+  uint32_t* dst = reinterpret_cast<uint32_t*>(&d);
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(TensorDesc) / 4); ++i)
+    dst[i] = __builtin_amdgcn_readfirstlane(src[i]);
+  return d;
 }
 
-// Changed words of tile t, counted by one wavefront (look-back fallback).
-// A cold path: plain 2-byte loads keep its register footprint small.
-template <bool kMulti>
-__device__ __forceinline__ uint32_t count_tile_wave(const ExtractArgs& a, uint64_t t, uint32_t lane) {
-  const TensorDesc d = tile_desc<kMulti>(a, t);
-  const int64_t e0 = (int64_t)((t - d.first_tile) * kElemsPerTile) - (int64_t)d.head;
-  uint32_t c = 0;
-#pragma unroll 1
-  for (int64_t i = lane; i < kElemsPerTile; i += 64) {
-    const int64_t e = e0 + i;
-    if (e >= 0 && e < (int64_t)d.n) c += (d.prev[e] != d.next[e]) ? 1u : 0u;
-  }
-  return wave_sum32(c);
+// Output index of word 0 of `tile`: the slice base plus the slice word
+// index, which is negative inside a misaligned head.
+__device__ __forceinline__ int64_t tile_out_base(const TensorDesc& d, uint64_t tile) {
+  return (int64_t)d.base + (int64_t)((tile - d.first_tile) * kElemsPerTile) - (int64_t)d.head;
 }
 
-// Per-lane state of one tile after the compare: which words changed and
-// where they go inside the tile's output run.
+// Per-lane result of comparing one tile: which words changed, where they go
+// inside the tile's run, and the run length.
 struct TileScan {
   u32x4 q[kChunks];               // new words
   uint32_t mask[kChunks];         // bit j: word j of the lane's group changed
-  uint32_t lane_prefix[kChunks];  // kept words of lower lanes in the same chunk
-  uint32_t chunk_base[kChunks];   // wave-uniform: kept words of earlier chunks
-  uint32_t wave_total;
+  uint32_t rank[kChunks];         // position in the tile's run of the lane's first kept word
+  uint32_t tile_total;
 };
 
-__device__ __forceinline__ void scan_tile(const TensorDesc& d, int64_t g0, TileScan& s) {
+// Reads and compares one tile with the whole workgroup (kWaves wavefronts).
+// Wave w handles groups [w * kGroupsPerWave, (w + 1) * kGroupsPerWave) of
+// the tile, chunk u of it being the 64 groups lane + 64u.
+template <bool kVec>
+__device__ __forceinline__ void scan_tile(const TensorDesc& d, uint64_t tile, uint32_t lane,
+                                          uint32_t wave, uint32_t* s_wave_total, TileScan& s) {
+  const uint32_t lane_group = wave * kGroupsPerWave + lane;
+  const int64_t g0 = (int64_t)((tile - d.first_tile) * kGroupsPerTile) + lane_group;
+  const int64_t tile_e0 = (int64_t)((tile - d.first_tile) * kElemsPerTile) - (int64_t)d.head;
   u32x4 p[kChunks];
+  if (kVec && tile_e0 >= 0 && tile_e0 + kElemsPerTile <= (int64_t)d.n) {
+    // interior tile (almost all of them): no per-group bounds
+    const gvec_ptr pp = (gvec_ptr)(reinterpret_cast<uintptr_t>(d.prev) - 2u * d.head) + g0;
+    const gvec_ptr qq = (gvec_ptr)(reinterpret_cast<uintptr_t>(d.next) - 2u * d.head) + g0;
 #pragma unroll
-  for (int u = 0; u < kChunks; ++u) load_group(d, g0 + 64 * u, p[u], s.q[u]);
-  s.wave_total = 0;
+    for (int u = 0; u < kChunks; ++u) {
+      p[u] = __builtin_nontemporal_load(pp + 64 * u);
+      s.q[u] = __builtin_nontemporal_load(qq + 64 * u);
+    }
+#pragma unroll
+    for (int u = 0; u < kChunks; ++u) s.mask[u] = changed_mask(p[u], s.q[u]);
+  } else {
+#pragma unroll
+    for (int u = 0; u < kChunks; ++u) {
+      const uint32_t valid = load_group<kVec>(d, g0 + 64 * u, p[u], s.q[u]);
+      s.mask[u] = changed_mask(p[u], s.q[u]) & valid;
+    }
+  }
+  uint32_t wave_total = 0;
 #pragma unroll
   for (int u = 0; u < kChunks; ++u) {
-    s.mask[u] = changed_mask(p[u], s.q[u]);
-    // bit-sliced prefix sum of the per-lane counts (0..8) over the wavefront
+    // Prefix sum of the per-lane counts (0..8) over the wavefront.  When
+    // no lane has two or more, one ballot and mbcnt give it; otherwise a
+    // bit-sliced sum over the four count bits.
     const uint32_t c = __popc(s.mask[u]);
-    const uint64_t b0 = __ballot(c & 1), b1 = __ballot(c & 2);
-    const uint64_t b2 = __ballot(c & 4), b3 = __ballot(c & 8);
-    s.lane_prefix[u] = mbcnt64(b0) + 2 * mbcnt64(b1) + 4 * mbcnt64(b2) + 8 * mbcnt64(b3);
-    s.chunk_base[u] = s.wave_total;
-    s.wave_total += __popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2) + 8 * __popcll(b3);
+    const uint64_t any = __ballot(c != 0);
+    if (__ballot(c > 1) == 0) {
+      s.rank[u] = wave_total + mbcnt64(any);
+      wave_total += __popcll(any);
+    } else {
+      const uint64_t b0 = __ballot(c & 1), b1 = __ballot(c & 2);
+      const uint64_t b2 = __ballot(c & 4), b3 = __ballot(c & 8);
+      s.rank[u] = wave_total + mbcnt64(b0) + 2 * mbcnt64(b1) + 4 * mbcnt64(b2) + 8 * mbcnt64(b3);
+      wave_total += __popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2) + 8 * __popcll(b3);
+    }
   }
+  if (lane == 0) s_wave_total[wave] = wave_total;
+  __syncthreads();
+  uint32_t wave_excl = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t t = s_wave_total[w];
+    wave_excl += (w < (int)wave) ? t : 0u;
+    total += t;
+  }
+#pragma unroll
+  for (int u = 0; u < kChunks; ++u) s.rank[u] += wave_excl;
+  s.tile_total = total;
 }
 
-__device__ __forceinline__ uint16_t word_of(const u32x4& q, int j) {
-  const uint32_t dw = q[j >> 1];
-  return (uint16_t)((j & 1) ? (dw >> 16) : (dw & 0xFFFFu));
-}
+// ---------------------------------------------------------------- stage
 
-template <typename IdxT, bool kMulti>
-__global__ __launch_bounds__(kThreads) void extract_kernel(ExtractArgs a) {
+template <bool kMulti, bool kVec>
+__global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
   __shared__ uint32_t s_wave_total[kWaves];
-  __shared__ uint64_t s_tile_excl;
-  // kept entries of the tile in output order: (new word << 16) | word offset in tile
-  __shared__ uint32_t s_stage[kStageCap];
-
+  __shared__ __attribute__((aligned(16))) uint32_t s_stage[kLdsStage];
   const uint64_t tile = blockIdx.x;
-  const TensorDesc d = tile_desc<kMulti>(a, tile);
-  const uint64_t local_tile = tile - d.first_tile;
   const uint32_t lane = lane_id();
   const uint32_t wave = threadIdx.x >> 6;
-  const uint32_t lane_group = wave * kGroupsPerWave + lane;   // group of chunk 0 in the tile
-  const int64_t g0 = (int64_t)(local_tile * kGroupsPerTile) + lane_group;
-  // slice word index of the tile's word 0 (negative inside a misaligned head)
-  const int64_t tile_e0 = (int64_t)(local_tile * kElemsPerTile) - (int64_t)d.head;
-
-  uint32_t wave_excl = 0, tile_total = 0;
-  {
-    TileScan s;
-    scan_tile(d, g0, s);
-    if (lane == 0) s_wave_total[wave] = s.wave_total;
-    __syncthreads();
+  const TensorDesc d = tile_desc<kMulti>(a, tile);
+  TileScan s;
+  scan_tile<kVec>(d, tile, lane, wave, s_wave_total, s);
+  // staged entry: (new word << 16) | word offset in the tile
+  uint32_t* slot = a.stage + tile * a.stage_stride;
+  const uint32_t lane_word = (wave * kGroupsPerWave + lane) * 8;
+  const uint32_t keep = s.tile_total < a.stage_cap ? s.tile_total : a.stage_cap;
+  // Entries go through LDS so that the slot is written with contiguous
+  // stores; a tile with more entries than LDS holds writes them directly.
+  const bool via_lds = keep <= (uint32_t)kLdsStage;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const uint32_t t = s_wave_total[w];
-      wave_excl += (w < (int)wave) ? t : 0u;
-      tile_total += t;
-    }
-    // Stage the kept entries in LDS now, so nothing of the tile stays live
-    // in registers through the look-back; the global writes after it are
-    // then contiguous runs.
-    if (tile_total <= (uint32_t)kStageCap) {
-#pragma unroll
-      for (int u = 0; u < kChunks; ++u) {
-        uint32_t m = s.mask[u];
-        uint32_t r = wave_excl + s.chunk_base[u] + s.lane_prefix[u];
-        const uint32_t w0 = (lane_group + 64 * u) * 8;
-        while (m) {
-          const int j = __builtin_ctz(m);
-          m &= m - 1;
-          s_stage[r++] = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
-        }
+  for (int u = 0; u < kChunks; ++u) {
+    uint32_t m = s.mask[u];
+    uint32_t r = s.rank[u];
+    const uint32_t w0 = lane_word + 512 * u;
+    while (m) {
+      const int j = __builtin_ctz(m);
+      m &= m - 1;
+      if (r < keep) {
+        const uint32_t e = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
+        if (via_lds) s_stage[r] = e; else slot[r] = e;
       }
+      ++r;
     }
   }
+  if (via_lds) {
+    __syncthreads();
+    // Streaming (non-temporal) stores: the slot is read once, by another
+    // kernel, so it should not displace anything in the caches.
+    for (uint32_t r = threadIdx.x; r < keep; r += kThreads)
+      __builtin_nontemporal_store(s_stage[r], slot + r);
+  }
+  if (threadIdx.x == 0) a.counts[tile] = s.tile_total;
+}
 
-  // Decoupled look-back, done by wavefront 0.
-  if (wave == 0) {
-    uint64_t excl = 0;
-    if (tile == 0) {
-      if (lane == 0) store_state(&a.states[0], kStatePrefix | tile_total);
-    } else {
-      if (lane == 0) store_state(&a.states[tile], kStateAggregate | tile_total);
-      int64_t top = (int64_t)tile - 1;
-      for (;;) {
-        const int64_t t = top - (int64_t)lane;
-        uint64_t st = (t >= 0) ? load_state(&a.states[t]) : kStatePrefix;
-        uint64_t need, prefix_lanes;
-        uint32_t spins = 0;
-        for (;;) {
-          const uint64_t empty = __ballot((st & kStateFlagMask) == kStateEmpty);
-          prefix_lanes = __ballot((st & kStateFlagMask) == kStatePrefix);
-          // lanes that count: up to and including the nearest full prefix
-          need = prefix_lanes ? (((prefix_lanes & (0 - prefix_lanes)) << 1) - 1) : ~0ull;
-          const uint64_t pending = empty & need;
-          if (pending == 0) break;
-          if (spins >= a.spin_limit) {
-            // count the nearest silent predecessor ourselves
-            const uint32_t l = (uint32_t)__builtin_ctzll(pending);
-            const uint32_t agg = count_tile_wave<kMulti>(a, (uint64_t)(top - (int64_t)l), lane);
-            if (lane == l) st = kStateAggregate | agg;
-            if (lane == 0)
-              __hip_atomic_fetch_add(&a.ctrl->fallbacks, 1u, __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT);
-            spins = 0;
-            continue;
-          }
-          ++spins;
-          __builtin_amdgcn_s_sleep(1);
-          if ((pending >> lane) & 1ull) st = load_state(&a.states[t]);
-        }
-        const uint64_t v = ((need >> lane) & 1ull) ? (st & kStateValueMask) : 0ull;
-        excl += wave_sum64(v);
-        if (prefix_lanes) break;
-        top -= 64;
-      }
-      if (lane == 0) store_state(&a.states[tile], kStatePrefix | (excl + tile_total));
+// ----------------------------------------------------------------- scan
+
+// Sum of the counts of each group of kTilesPerGroup tiles (one wavefront).
+__global__ __launch_bounds__(64) void group_sum_kernel(const uint32_t* counts, uint64_t num_tiles,
+                                                       uint64_t* group_sum) {
+  const uint64_t t = (uint64_t)blockIdx.x * kTilesPerGroup + threadIdx.x;
+  const uint64_t c = t < num_tiles ? counts[t] : 0;
+  const uint64_t s = wave_sum64(c);
+  if (threadIdx.x == 0) group_sum[blockIdx.x] = s;
+}
+
+// Exclusive scan of the group sums by one workgroup, in passes of
+// kScanThreads groups with a running carry; also writes the total.
+constexpr int kScanThreads = 1024;
+__global__ __launch_bounds__(kScanThreads) void group_scan_kernel(const uint64_t* group_sum,
+                                                                  uint64_t num_groups,
+                                                                  uint64_t* group_excl,
+                                                                  uint64_t* d_count) {
+  __shared__ uint64_t s_wave[kScanThreads / 64];
+  __shared__ uint64_t s_carry;
+  const uint32_t lane = lane_id();
+  const uint32_t wave = threadIdx.x >> 6;
+  if (threadIdx.x == 0) s_carry = 0;
+  __syncthreads();
+  for (uint64_t base = 0; base < num_groups; base += kScanThreads) {
+    const uint64_t i = base + threadIdx.x;
+    const uint64_t v = i < num_groups ? group_sum[i] : 0;
+    // inclusive scan within the wavefront
+    uint64_t x = v;
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) {
+      const uint64_t y = __shfl_up(x, s);
+      if ((int)lane >= s) x += y;
     }
-    if (lane == 0) s_tile_excl = excl;
+    if (lane == 63) s_wave[wave] = x;
+    __syncthreads();
+    uint64_t before = s_carry;
+    for (uint32_t w = 0; w < wave; ++w) before += s_wave[w];
+    if (i < num_groups) group_excl[i] = before + x - v;
+    __syncthreads();
+    if (threadIdx.x == kScanThreads - 1) s_carry = before + x;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *d_count = s_carry;
+}
+
+// ------------------------------------------------------------- finalize
+
+// Output index of word 0 of `tile`, read by one lane (tile ids differ per
+// lane here, so the descriptor stays in vector registers).
+template <bool kMulti>
+__device__ __forceinline__ TensorDesc lane_desc(const ExtractArgs& a, uint64_t tile) {
+  return kMulti ? a.table[a.tile_map[tile]] : a.single;
+}
+
+template <typename IdxT, bool kMulti, bool kVec>
+__global__ __launch_bounds__(kThreads) void finalize_kernel(ExtractArgs a) {
+  __shared__ uint32_t s_begin[kTilesPerGroup + 1];   // run start of each tile in the group
+  __shared__ uint32_t s_count[kTilesPerGroup];
+  __shared__ int64_t s_out_base[kTilesPerGroup];
+  __shared__ uint32_t s_wave_total[kWaves];
+  const uint64_t g = blockIdx.x;
+  const uint64_t t0 = g * kTilesPerGroup;
+  const uint64_t left = a.num_tiles - t0;
+  const uint32_t n_here = left < (uint64_t)kTilesPerGroup ? (uint32_t)left : kTilesPerGroup;
+  const uint32_t lane = lane_id();
+  const uint32_t wave = threadIdx.x >> 6;
+  const uint64_t group_excl = a.group_excl[g];
+  if (wave == 0) {
+    // exclusive scan of the group's tile counts (one tile per lane)
+    const uint64_t t = t0 + lane;
+    const bool in = lane < n_here;
+    const uint32_t c = in ? a.counts[t] : 0u;
+    uint32_t x = c;
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) {
+      const uint32_t y = __shfl_up(x, s);
+      if ((int)lane >= s) x += y;
+    }
+    s_begin[lane] = x - c;
+    if (lane == 63) s_begin[64] = x;
+    s_count[lane] = c;
+    if (in) {
+      const TensorDesc d = lane_desc<kMulti>(a, t);
+      s_out_base[lane] = tile_out_base(d, t);
+      if (a.d_tensor_offsets) {
+        // tensor_offsets: the first tile of a slice owns the slots of its
+        // own tensor and of the empty tensors just before it; the last tile
+        // owns the slots after its tensor (trailing empty tensors, total).
+        const uint64_t excl = group_excl + (x - c);
+        if (t == d.first_tile)
+          for (uint32_t s = d.off_lo; s <= d.slot; ++s) a.d_tensor_offsets[s] = excl;
+        if (t == a.num_tiles - 1)
+          for (uint32_t s = d.slot + 1; s <= a.num_tensors; ++s) a.d_tensor_offsets[s] = excl + c;
+      }
+    }
   }
   __syncthreads();
-  const uint64_t tile_excl = s_tile_excl;
-
-  if (threadIdx.x == 0) {
-    // tensor_offsets: the first tile of a slice owns the slots of its own
-    // tensor and of the empty tensors just before it; the last tile owns
-    // the slots after its tensor (trailing empty tensors and the total).
-    if (a.d_tensor_offsets && local_tile == 0) {
-      for (uint32_t s = d.off_lo; s <= d.slot; ++s) a.d_tensor_offsets[s] = tile_excl;
+  IdxT* out_idx = reinterpret_cast<IdxT*>(a.out_idx);
+  const uint32_t total = s_begin[64];
+  // Every staged entry of the group, in output order, spread over all
+  // threads; the tile of entry e is found by binary search over s_begin.
+  // Entries of overflowed tiles are skipped here and written below.
+  for (uint32_t e = threadIdx.x; e < total; e += kThreads) {
+    uint32_t lo = 0, hi = 64;   // s_begin[lo] <= e < s_begin[hi]
+#pragma unroll
+    for (int step = 0; step < 6; ++step) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (s_begin[mid] <= e) lo = mid; else hi = mid;
     }
-    if (tile == a.num_tiles - 1) {
-      const uint64_t total = tile_excl + tile_total;
-      *a.d_count = total;
-      if (a.d_tensor_offsets) {
-        for (uint32_t s = d.slot + 1; s <= a.num_tensors; ++s) a.d_tensor_offsets[s] = total;
-      }
+    const uint32_t i = lo;
+    const uint32_t j = e - s_begin[i];
+    if (s_count[i] > a.stage_cap) continue;
+    const uint64_t pos = group_excl + e;
+    if (pos < a.capacity) {
+      const uint32_t v = a.stage[(t0 + i) * a.stage_stride + j];
+      out_idx[pos] = (IdxT)(s_out_base[i] + (v & 0xFFFFu));
+      a.out_val[pos] = (uint16_t)(v >> 16);
     }
   }
-
-  IdxT* out_idx = reinterpret_cast<IdxT*>(a.out_idx);
-  const int64_t out_base = (int64_t)d.base + tile_e0;
-  if (tile_total <= (uint32_t)kStageCap) {
-    // contiguous run [tile_excl, tile_excl + tile_total) of the output
-    for (uint32_t r = threadIdx.x; r < tile_total; r += kThreads) {
-      const uint64_t pos = tile_excl + r;
-      if (pos < a.capacity) {
-        const uint32_t e = s_stage[r];
-        out_idx[pos] = (IdxT)(out_base + (e & 0xFFFFu));
-        a.out_val[pos] = (uint16_t)(e >> 16);
-      }
-    }
-  } else {
-    // more kept words than the stage holds: read the tile again and write
-    // each entry from registers
+  // Tiles that overflowed their slot: read again and write every entry.
+  for (uint32_t i = 0; i < n_here; ++i) {
+    if (s_count[i] <= a.stage_cap) continue;
+    const uint64_t tile = t0 + i;
+    const TensorDesc d = tile_desc<kMulti>(a, tile);
     TileScan s;
-    scan_tile(d, g0, s);
+    scan_tile<kVec>(d, tile, lane, wave, s_wave_total, s);
+    const int64_t lane_out = s_out_base[i] + (int64_t)(wave * kGroupsPerWave + lane) * 8;
+    const uint64_t excl = group_excl + s_begin[i];
 #pragma unroll
     for (int u = 0; u < kChunks; ++u) {
       uint32_t m = s.mask[u];
-      uint64_t pos = tile_excl + wave_excl + s.chunk_base[u] + s.lane_prefix[u];
-      const int64_t e0 = out_base + (int64_t)(lane_group + 64 * u) * 8;
+      uint64_t pos = excl + s.rank[u];
+      const int64_t e0 = lane_out + 512 * u;
       while (m) {
         const int j = __builtin_ctz(m);
         m &= m - 1;
@@ -289,20 +395,18 @@ __global__ __launch_bounds__(kThreads) void extract_kernel(ExtractArgs a) {
         ++pos;
       }
     }
+    __syncthreads();   // s_wave_total is reused by the next overflowed tile
   }
 }
 
-__global__ void reset_kernel(Control* ctrl, uint64_t* states, uint64_t num_tiles,
-                             uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets) {
+// ------------------------------------------------------- small kernels
+
+__global__ void reset_kernel(uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets) {
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   const uint64_t i0 = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  for (uint64_t i = i0; i < num_tiles; i += stride) states[i] = kStateEmpty;
   if (d_offsets)
     for (uint64_t i = i0; i < num_offsets; i += stride) d_offsets[i] = 0;
-  if (i0 == 0) {
-    ctrl->fallbacks = 0;
-    *d_count = 0;
-  }
+  if (i0 == 0) *d_count = 0;
 }
 
 __global__ void upload_words_kernel(WordBatch b, uint64_t* dst) {
@@ -316,15 +420,13 @@ __global__ void build_tile_map_kernel(const TensorDesc* table, uint32_t* tile_ma
   for (uint64_t i = threadIdx.x; i < nt; i += blockDim.x) tile_map[d.first_tile + i] = t;
 }
 
-hipError_t launch_reset(Control* ctrl, uint64_t* states, uint64_t num_tiles,
-                        uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets,
+hipError_t launch_reset(uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets,
                         hipStream_t stream) {
-  uint64_t work = num_tiles > num_offsets ? num_tiles : num_offsets;
-  uint64_t blocks = (work + 255) / 256;
+  uint64_t blocks = ((uint64_t)num_offsets + 255) / 256;
   if (blocks < 1) blocks = 1;
-  if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(reset_kernel, dim3((uint32_t)blocks), dim3(256), 0, stream, ctrl, states,
-                     num_tiles, d_count, d_offsets, num_offsets);
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(reset_kernel, dim3((uint32_t)blocks), dim3(256), 0, stream, d_count,
+                     d_offsets, num_offsets);
   return hipGetLastError();
 }
 
@@ -349,22 +451,39 @@ hipError_t launch_build_tile_map(const TensorDesc* table, uint32_t num_tensors,
   return hipGetLastError();
 }
 
-hipError_t launch_extract(const ExtractArgs& a, bool idx64, hipStream_t stream) {
-  if (a.num_tiles == 0) return hipSuccess;
-  const dim3 grid((uint32_t)a.num_tiles), block(kThreads);
-  const bool multi = a.table != nullptr;
-  if (idx64) {
-    if (multi)
-      hipLaunchKernelGGL((extract_kernel<int64_t, true>), grid, block, 0, stream, a);
-    else
-      hipLaunchKernelGGL((extract_kernel<int64_t, false>), grid, block, 0, stream, a);
-  } else {
-    if (multi)
-      hipLaunchKernelGGL((extract_kernel<int32_t, true>), grid, block, 0, stream, a);
-    else
-      hipLaunchKernelGGL((extract_kernel<int32_t, false>), grid, block, 0, stream, a);
-  }
+template <typename IdxT, bool kMulti, bool kVec>
+static hipError_t launch_all(const ExtractArgs& a, hipStream_t stream) {
+  const uint64_t groups = (a.num_tiles + kTilesPerGroup - 1) / kTilesPerGroup;
+  hipLaunchKernelGGL((stage_kernel<kMulti, kVec>), dim3((uint32_t)a.num_tiles), dim3(kThreads),
+                     0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(group_sum_kernel, dim3((uint32_t)groups), dim3(64), 0, stream, a.counts,
+                     a.num_tiles, a.group_sum);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(group_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, a.group_sum,
+                     groups, a.group_excl, a.d_count);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((finalize_kernel<IdxT, kMulti, kVec>), dim3((uint32_t)groups),
+                     dim3(kThreads), 0, stream, a);
   return hipGetLastError();
+}
+
+template <typename IdxT, bool kMulti>
+static hipError_t launch_vec(const ExtractArgs& a, bool vec, hipStream_t stream) {
+  return vec ? launch_all<IdxT, kMulti, true>(a, stream) : launch_all<IdxT, kMulti, false>(a, stream);
+}
+
+hipError_t launch_extract(const ExtractArgs& a, bool idx64, bool all_vec, hipStream_t stream) {
+  if (a.num_tiles == 0) return hipSuccess;
+  const bool multi = a.table != nullptr;
+  if (idx64)
+    return multi ? launch_vec<int64_t, true>(a, all_vec, stream)
+                 : launch_vec<int64_t, false>(a, all_vec, stream);
+  return multi ? launch_vec<int32_t, true>(a, all_vec, stream)
+               : launch_vec<int32_t, false>(a, all_vec, stream);
 }
 
 }  // namespace aurora

@@ -17,30 +17,25 @@
 
 #include <vector>
 
-#include "../../include/aurora_delta.h"
+#include "aurora_delta.h"
 #include "delta_internal.h"
 
 using namespace aurora;
 
 namespace {
 
-struct ChunkSlice {
-  const uint16_t* prev;
-  const uint16_t* next;
-  uint64_t n, base;
-};
-
 // Slices of chunk [lo, hi) of the global index space.
 void chunk_slices(const uint16_t* const* prevs, const uint16_t* const* nexts,
                   const uint64_t* numels, int32_t T, uint64_t lo, uint64_t hi,
-                  std::vector<ChunkSlice>& out) {
+                  std::vector<SliceIn>& out) {
   out.clear();
   uint64_t base = 0;
   for (int32_t t = 0; t < T && base < hi; ++t) {
     const uint64_t n = numels[t];
     const uint64_t a = lo > base ? lo : base;
     const uint64_t b = hi < base + n ? hi : base + n;
-    if (a < b) out.push_back({prevs[t] + (a - base), nexts[t] + (a - base), b - a, a});
+    if (a < b)
+      out.push_back({prevs[t] + (a - base), nexts[t] + (a - base), b - a, a, (uint32_t)t});
     base += n;
   }
 }
@@ -76,69 +71,13 @@ size_t max_chunk_workspace(const uint64_t* numels, int32_t T, uint64_t total, ui
       }
       base += numels[t];
     }
-    const size_t need = workspace_layout(tiles, rows).total;
+    const size_t need = workspace_bytes(tiles, rows, kDefaultStageCap);
     if (need > best) best = need;
   }
   return best;
 }
 
 }  // namespace
-
-// Enqueues the extract of one chunk: the kernels of delta_extract_multi over
-// slices that carry their global base, into the stream's staging.
-static hipError_t enqueue_chunk(const std::vector<ChunkSlice>& sl, char* stage,
-                                const StagingLayout& L, hipStream_t stream) {
-  std::vector<TensorDesc> descs;
-  uint64_t tiles = 0;
-  for (const ChunkSlice& s : sl) {
-    if (s.n == 0) continue;
-    TensorDesc d;
-    memset(&d, 0, sizeof(d));
-    d.prev = s.prev;
-    d.next = s.next;
-    d.n = s.n;
-    d.base = s.base;
-    d.first_tile = tiles;
-    const uint32_t hp = head_words(s.prev), hq = head_words(s.next);
-    d.vec = (hp == hq) ? 1u : 0u;
-    d.head = d.vec ? hp : 0u;
-    tiles += tiles_for(d.n, d.head);
-    descs.push_back(d);
-  }
-  char* ws = stage + L.ws;
-  const WorkspaceLayout W = workspace_layout(tiles, descs.size());
-  Control* ctrl = (Control*)ws;
-  uint64_t* states = (uint64_t*)(ws + W.states);
-  uint32_t* map = (uint32_t*)(ws + W.map);
-  TensorDesc* table = (TensorDesc*)(ws + W.table);
-  uint64_t* d_count = (uint64_t*)(stage + L.count);
-  hipError_t e = launch_reset(ctrl, states, tiles, d_count, nullptr, 0, stream);
-  if (e != hipSuccess || tiles == 0) return e;
-  ExtractArgs a;
-  memset(&a, 0, sizeof(a));
-  a.num_tiles = tiles;
-  a.num_tensors = 0;
-  a.out_idx = stage + L.idx;
-  a.out_val = (uint16_t*)(stage + L.val);
-  a.capacity = UINT64_MAX;   // staging holds a whole chunk
-  a.d_count = d_count;
-  a.d_tensor_offsets = nullptr;
-  a.states = states;
-  a.ctrl = ctrl;
-  a.spin_limit = spin_limit_from_env();
-  if (descs.size() > 1) {
-    e = launch_upload_words((const uint64_t*)descs.data(), descs.size() * sizeof(TensorDesc) / 8,
-                            (uint64_t*)table, stream);
-    if (e != hipSuccess) return e;
-    e = launch_build_tile_map(table, (uint32_t)descs.size(), map, stream);
-    if (e != hipSuccess) return e;
-    a.table = table;
-    a.tile_map = map;
-  } else {
-    a.single = descs[0];
-  }
-  return launch_extract(a, true, stream);
-}
 
 extern "C" {
 
@@ -205,9 +144,10 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     return DELTA_ERR_HIP;
   }
 
-  std::vector<ChunkSlice> sl;
+  std::vector<SliceIn> sl;
   uint64_t offset = 0;   // host position of the next chunk's first entry
   uint64_t finished = 0; // chunks whose data copy is enqueued
+  uint64_t issued = 0;   // chunks whose extract and count copy are enqueued
   delta_status_t status = DELTA_OK;
 
   auto stage_of = [&](uint64_t c) { return (char*)d_staging + L.per_stream * (c % S); };
@@ -238,11 +178,18 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     const uint64_t hi = (total - lo < chunk) ? total : lo + chunk;
     chunk_slices(prevs, nexts, numels, T, lo, hi, sl);
     char* stage = stage_of(c);
-    e = enqueue_chunk(sl, stage, L, streams[c % S]);
-    if (e != hipSuccess) break;
+    const delta_status_t st =
+        enqueue_extract(sl.data(), sl.size(), 0, true, stage + L.idx, (uint16_t*)(stage + L.val),
+                        chunk, (uint64_t*)(stage + L.count), nullptr, stage + L.ws, L.ws_bytes,
+                        streams[c % S]);
+    if (st != DELTA_OK) {
+      status = st;
+      break;
+    }
     e = hipMemcpyAsync(&h_counts[c], stage + L.count, 8, hipMemcpyDeviceToHost, streams[c % S]);
+    if (e == hipSuccess) issued = c + 1;
   }
-  while (e == hipSuccess && finished < nchunks) e = finish(finished);
+  while (e == hipSuccess && status == DELTA_OK && finished < issued) e = finish(finished);
   // Drain every stream whatever happened, so no copy is left in flight.
   for (int s = 0; s < S; ++s) {
     hipError_t e2 = hipStreamSynchronize(streams[s]);
@@ -253,6 +200,10 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     set_error("HIP error in pipeline: %s", hipGetErrorString(e));
     *h_count = 0;
     return DELTA_ERR_HIP;
+  }
+  if (status != DELTA_OK) {   // a chunk could not be enqueued: no partial result
+    *h_count = 0;
+    return status;
   }
   *h_count = offset;
   if (offset > h_cap) {
