@@ -1,0 +1,129 @@
+"""Full-size weight sets on the GPU, in the launch configuration the
+benchmark times (delta_extract_multi over the whole set with the default
+workspace).
+
+At these sizes every output is checked through properties that hold at
+any size, computed on the GPU with plain torch ops:
+  * the count equals the number of planted changes, per tensor as well
+    (tensor_offsets differences);
+  * indices are strictly increasing, and inside their tensor;
+  * val[k] == new[idx[k]] and prev[idx[k]] != new[idx[k]] (so every kept
+    word really changed; with the count this means none is missing);
+  * applying the delta to a copy of prev gives new, bit for bit.
+In addition a sample of whole tensors (the largest, the smallest and some
+in between) is compared entry by entry with the CPU oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2602_11456_amd as ad
+from paper_2602_11456_amd import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def host_u16(t):
+    return t.detach().reshape(-1).view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def sample_tensors(names, shapes):
+    """Largest, smallest, the first layer's tensors and every 37th."""
+    n = len(names)
+    sizes = [synth.numel(s) for s in shapes]
+    pick = {0, n - 1, int(np.argmax(sizes)), int(np.argmin(sizes))}
+    pick |= set(range(1, min(12, n)))
+    pick |= set(range(0, n, 37))
+    return sorted(pick)
+
+
+def check_set(ws, idx, val, offs, label):
+    T = len(ws.prev)
+    bases = np.concatenate([[0], np.cumsum(ws.numels)])
+    offs_h = offs.cpu().numpy()
+    planted = np.array(ws.planted)
+    assert int(offs_h[-1]) == idx.numel() == ws.total_planted, label
+    np.testing.assert_array_equal(np.diff(offs_h), planted)
+    # strictly increasing global indices
+    if idx.numel() > 1:
+        assert bool((idx[1:] > idx[:-1]).all()), label
+    for t in range(T):
+        a, b = int(offs_h[t]), int(offs_h[t + 1])
+        if a == b:
+            continue
+        local = idx[a:b] - int(bases[t])
+        assert int(local[0]) >= 0 and int(local[-1]) < ws.numels[t]
+        p = ws.prev[t].reshape(-1).view(torch.int16)
+        q = ws.new[t].reshape(-1).view(torch.int16)
+        assert torch.equal(q[local], val[a:b].view(torch.int16)), (label, t)
+        assert bool((p[local] != q[local]).all()), (label, t)
+    # sampled tensors against the oracle
+    for t in sample_tensors(ws.names, ws.shapes):
+        r_idx, r_val, r_cnt = oracle.extract(host_u16(ws.prev[t]), host_u16(ws.new[t]))
+        a, b = int(offs_h[t]), int(offs_h[t + 1])
+        assert b - a == r_cnt, (label, t)
+        np.testing.assert_array_equal(idx[a:b].cpu().numpy() - bases[t], r_idx)
+        np.testing.assert_array_equal(host_u16(val[a:b]), r_val)
+    say(label, "ok:", idx.numel(), "entries,", T, "tensors")
+
+
+def round_trip(ws, idx, val, label):
+    roll = [p.clone() for p in ws.prev]
+    ad.delta_apply_multi(roll, idx, val, check=True)
+    for r, q in zip(roll, ws.new):
+        assert torch.equal(r.view(torch.int16), q.view(torch.int16)), label
+    del roll
+    say(label, "apply round trip ok")
+
+
+@pytest.mark.parametrize("model,density", [("qwen3-4b", 0.01), ("qwen3-8b", 0.001),
+                                           ("qwen3-8b", 0.01), ("qwen3-8b", 0.1)])
+def test_weight_set(model, density):
+    cfg = 2 if model == "qwen3-4b" else 3
+    ws = synth.make_weight_set(model, density, seed=synth.config_seed(cfg), device=DEV)
+    label = f"{model}@{density}"
+    say(label, "generated", ws.total, "words")
+    idx, val, offs = ad.delta_extract_multi(ws.prev, ws.new)
+    torch.cuda.synchronize()
+    check_set(ws, idx, val, offs, label)
+    round_trip(ws, idx, val, label)
+
+
+def test_qwen3_8b_clustered():
+    ws = synth.make_weight_set("qwen3-8b", 0.01, seed=synth.config_seed(4), device=DEV,
+                               clustered=True)
+    hot_rows, H, K, K_hot, K_cold = synth.clustered_plan("qwen3-8b", 0.01)
+    assert ws.total_planted == K
+    say("clustered generated", ws.total, "words", K, "changes")
+    idx, val, offs = ad.delta_extract_multi(ws.prev, ws.new)
+    torch.cuda.synchronize()
+    check_set(ws, idx, val, offs, "qwen3-8b clustered")
+    # the per-tile load really is imbalanced: some 8192-word tiles hold far
+    # more changes than the 1% average
+    tile_hist = torch.bincount(idx // 8192)
+    assert int(tile_hist.max()) > 5 * 82
+    round_trip(ws, idx, val, "qwen3-8b clustered")
+
+
+def test_qwen3_14b_pipeline():
+    ws = synth.make_weight_set("qwen3-14b", 0.01, seed=synth.config_seed(5), device=DEV)
+    say("qwen3-14b generated", ws.total, "words")
+    cap = ws.total_planted + 4096
+    h_idx = torch.empty(cap, dtype=torch.int64, pin_memory=True)
+    h_val = torch.empty(cap, dtype=torch.bfloat16, pin_memory=True)
+    h_idx, h_val = ad.delta_extract_pipelined(ws.prev, ws.new, chunk_elems=1 << 27,
+                                              num_streams=4, h_idx=h_idx, h_val=h_val)
+    say("pipeline done", h_idx.numel())
+    assert h_idx.numel() == ws.total_planted
+    # identical to the device-resident multi-tensor extract
+    idx, val, offs = ad.delta_extract_multi(ws.prev, ws.new)
+    torch.cuda.synchronize()
+    assert torch.equal(h_idx, idx.cpu())
+    assert torch.equal(h_val.view(torch.int16), val.view(torch.int16).cpu())
+    check_set(ws, idx, val, offs, "qwen3-14b")
