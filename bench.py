@@ -30,6 +30,8 @@ import time
 
 METRIC = "delta extract GB/s scanned (% of HBM peak) + apply GB/s, Qwen3-8B shape @1%"
 HBM_PEAK_GBPS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "extract_qwen3-8b_traffic.json")
 
 
 def log(*a):
@@ -46,9 +48,23 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="oracle time budget for the CPU baseline sample")
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured HBM bytes per extract launch")
+    ap.add_argument("--traffic", default=TRAFFIC_FILE,
+                    help="JSON file with measured HBM bytes per extract call")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="after timing, copy BYTES device-to-device three times (a known "
+                         "traffic reference for hardware counters)")
     return ap.parse_args()
+
+
+def kernel_source_digest():
+    """Digest of the extract kernels' sources: stored traffic figures are
+    only used while the kernels they were measured on are unchanged."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("extract.hip", "delta_internal.h"):
+        with open(os.path.join(ROOT, "paper_2602_11456_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def cpu_baseline(ws, budget_s):
@@ -182,7 +198,9 @@ def main():
     traffic = None
     if args.traffic and os.path.exists(args.traffic):
         with open(args.traffic) as f:
-            traffic = json.load(f).get("bytes_per_launch")
+            rec = json.load(f)
+        if rec.get("kernel_source_sha256") == kernel_source_digest():
+            traffic = rec.get("bytes_per_call")
 
     ext_sorted = sorted(ext_ms)
     result = {
@@ -229,6 +247,14 @@ def main():
             "traffic": traffic,
         },
     }
+    if args.copy_calibration > 0:
+        n = args.copy_calibration // 2
+        src = torch.empty(n, dtype=torch.int16, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         del rollout
         result["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
