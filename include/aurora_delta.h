@@ -39,8 +39,12 @@
  *   - Index order is the flattened storage order of each tensor (row-major
  *     for a C-contiguous tensor).  Output indices are strictly increasing.
  *   - The caller owns all memory.  No entry point allocates device memory;
- *     scratch space is a caller-provided `workspace` of at least the size
- *     the matching *_workspace_bytes function returns (256-byte aligned).
+ *     scratch space is a caller-provided, 256-byte aligned `workspace`.
+ *     The matching *_workspace_bytes function returns the recommended size.
+ *     Extract also accepts a smaller workspace (down to a few tens of bytes
+ *     per 8192-word tile; below that DELTA_ERR_WORKSPACE): it then keeps
+ *     fewer staged entries per tile and reads the input of tiles with more
+ *     changed words twice.  Results never depend on the workspace size.
  *   - Asynchrony: extract/apply functions only enqueue work on `stream`
  *     (0 = the null stream) and return.  The return status covers argument
  *     validation and launch errors.  Device-side outcomes are read after
@@ -91,7 +95,9 @@ const char* delta_status_string(int status);
 /* Detail text of the last failed call on this thread ("" if none). */
 const char* delta_last_error(void);
 
-/* Workspace bytes for delta_extract over `numel` words (any alignment). */
+/* Recommended workspace bytes for delta_extract over `numel` words (any
+ * alignment): holds every tile's staged entries up to 12.5% changed words
+ * (about numel / 2 bytes). */
 size_t delta_extract_workspace_bytes(uint64_t numel);
 
 /* Workspace bytes for delta_extract_multi over tensors of the given sizes
