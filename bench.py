@@ -50,6 +50,10 @@ def parse():
                     help="oracle time budget for the CPU baseline sample")
     ap.add_argument("--traffic", default=TRAFFIC_FILE,
                     help="JSON file with measured HBM bytes per extract call")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="skip the chunked extract -> pinned host pipeline measurement "
+                         "(Qwen3-14B-shaped set)")
+    ap.add_argument("--pipeline-reps", type=int, default=3)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after timing, copy BYTES device-to-device three times (a known "
                          "traffic reference for hardware counters)")
@@ -102,6 +106,61 @@ def cpu_baseline(ws, budget_s):
         "sample": f"first {tensors} of {len(ws.prev)} tensors of the same weight set "
                   f"({words} words, {4 * words / 1e9:.2f} GB scanned) in {spent:.1f} s, "
                   f"single-threaded C loop",
+    }
+
+
+def pipeline_measurement(args, dev):
+    """Chunked extract -> pinned host memory over 4 HIP streams on the
+    Qwen3-14B-shaped set at 1% (2^27-word chunks), host-synchronous calls
+    timed with the wall clock, next to a pinned device-to-host copy of the
+    same number of bytes (the host-link ceiling)."""
+    import torch
+    import paper_2602_11456_amd as ad
+    from paper_2602_11456_amd import synth
+
+    ws = synth.make_weight_set("qwen3-14b", args.density, seed=synth.config_seed(5), device=dev)
+    torch.cuda.synchronize()
+    K = ws.total_planted
+    chunk, nstreams = 1 << 27, 4
+    plan = ad.MultiPlan(ws.prev, ws.new)
+    staging = torch.empty(ad.delta_pipeline_staging_bytes(plan.numels, chunk, nstreams),
+                          dtype=torch.uint8, device=dev)
+    streams = [torch.cuda.Stream(device=dev) for _ in range(nstreams)]
+    h_idx = torch.empty(K + 4096, dtype=torch.int64, pin_memory=True)
+    h_val = torch.empty(K + 4096, dtype=torch.bfloat16, pin_memory=True)
+    times = []
+    for rep in range(args.pipeline_reps + 1):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        i, v = ad.delta_extract_pipelined(ws.prev, ws.new, chunk, nstreams, h_idx, h_val,
+                                          staging, streams)
+        t = time.perf_counter() - t0
+        if i.numel() != K:
+            raise RuntimeError(f"pipeline found {i.numel()} changed words, {K} planted")
+        if rep:
+            times.append(t)
+    out_bytes = K * 10
+    # host-link ceiling: one pinned D2H copy of the same bytes
+    src = torch.empty(out_bytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty(out_bytes, dtype=torch.uint8, pin_memory=True)
+    ctimes = []
+    for rep in range(3):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        dst.copy_(src, non_blocking=True)
+        torch.cuda.synchronize()
+        ctimes.append(time.perf_counter() - t0)
+    t = sorted(times)[len(times) // 2]
+    tc = min(ctimes)
+    return {
+        "workload": f"qwen3-14b weight set, {len(ws.prev)} tensors, {ws.total} bf16 words, "
+                    f"{args.density:.2%} changed, {chunk}-word chunks over {nstreams} streams "
+                    "into pinned host memory",
+        "ms": round(t * 1e3, 3),
+        "GBps_scanned": round(4 * ws.total / t / 1e9, 1),
+        "d2h_GBps": round(out_bytes / t / 1e9, 2),
+        "d2h_ceiling_GBps": round(out_bytes / tc / 1e9, 2),
+        "d2h_bytes": out_bytes,
     }
 
 
@@ -258,6 +317,11 @@ def main():
     if not args.no_cpu_baseline:
         del rollout
         result["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
+    if not args.no_pipeline:
+        del ws, plan, out_idx, out_val, work
+        rollout = None
+        torch.cuda.empty_cache()
+        result["pipeline"] = pipeline_measurement(args, dev)
     print(json.dumps(result), flush=True)
     return 0
 
