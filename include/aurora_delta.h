@@ -183,6 +183,64 @@ delta_status_t delta_apply_checked(uint16_t* weights, uint64_t numel, delta_inde
                                    uint32_t* d_error_flag, uint64_t active_version,
                                    uint64_t base_version, hipStream_t stream);
 
+/*
+ * Gap + unsigned LEB128 index encoding — Sec. 5.1 "Sparse encoding" and the
+ * figure "Delta checkpoint index encoding".  A sorted index stream keeps its
+ * first entry as-is and every later entry as the difference from its
+ * predecessor; each number is written as unsigned LEB128 (7 payload bits per
+ * byte, least significant group first, bit 7 set on every byte but the
+ * last; e.g. 198 -> C6 01).
+ *
+ * Segments: entries [seg_offsets[s], seg_offsets[s+1]) form segment s
+ * (seg_offsets: device uint64 [num_segs + 1], nondecreasing, [0] = 0,
+ * [num_segs] = count); the first entry of segment s is coded as
+ * idx - seg_bases[s] (device uint64 [num_segs]).  With the tensor_offsets
+ * of delta_extract_multi and the tensor bases this gives every tensor its
+ * own stream of tensor-local indices, as in the paper.  num_segs = 0: one
+ * segment, base 0 (the seg arrays may be NULL).
+ */
+
+/* Workspace bytes for delta_leb128_encode over `count` entries. */
+size_t delta_leb128_encode_workspace_bytes(uint64_t count);
+
+/* Workspace bytes for delta_leb128_decode of `nbytes` bytes into at most
+ * `capacity` entries with `num_segs` segments. */
+size_t delta_leb128_decode_workspace_bytes(uint64_t nbytes, uint64_t capacity, uint32_t num_segs);
+
+/*
+ * delta_leb128_encode
+ *   idx           device int64 [count], strictly increasing within each
+ *                 segment and >= the segment's base at its first entry;
+ *                 otherwise *d_error_flag is set (if not NULL) and the
+ *                 offending gaps are coded as 0.
+ *   out           device bytes [capacity]; *d_nbytes receives the true
+ *                 length (only the first `capacity` bytes are written).
+ *   d_seg_byte_offsets
+ *                 device uint64 [num_segs + 1] or NULL: byte position where
+ *                 each segment's numbers start, and the total.
+ */
+delta_status_t delta_leb128_encode(const int64_t* idx, uint64_t count,
+                                   const uint64_t* d_seg_offsets, const uint64_t* d_seg_bases,
+                                   uint32_t num_segs, uint8_t* out, uint64_t capacity,
+                                   uint64_t* d_nbytes, uint64_t* d_seg_byte_offsets,
+                                   uint32_t* d_error_flag, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/*
+ * delta_leb128_decode — inverse of delta_leb128_encode.
+ *   in            device bytes [nbytes].
+ *   out_idx       device int64 [capacity]: decoded indices; *d_count gets
+ *                 the number of numbers in the stream (only the first
+ *                 `capacity` decoded).
+ *   *d_error_flag set (if not NULL) when the stream ends inside a number or
+ *                 a number does not fit 64 bits.
+ */
+delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
+                                   const uint64_t* d_seg_offsets, const uint64_t* d_seg_bases,
+                                   uint32_t num_segs, int64_t* out_idx, uint64_t capacity,
+                                   uint64_t* d_count, uint32_t* d_error_flag, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
 /* Options of the chunked pipeline. */
 typedef struct {
   uint64_t chunk_elems; /* words of the global index space per chunk (> 0) */

@@ -28,7 +28,7 @@ __all__ = [
     "delta_extract_multi_into", "delta_apply", "delta_apply_multi", "delta_apply_checked",
     "delta_extract_pipelined", "delta_extract_workspace_bytes",
     "delta_extract_multi_workspace_bytes", "delta_apply_multi_workspace_bytes",
-    "delta_pipeline_staging_bytes", "MultiPlan",
+    "delta_pipeline_staging_bytes", "MultiPlan", "delta_leb128_encode", "delta_leb128_decode",
 ]
 
 
@@ -280,6 +280,80 @@ def delta_apply_multi(weights: Sequence[torch.Tensor], idx: torch.Tensor, val: t
         (stream or torch.cuda.current_stream()).synchronize()
         if int(flag.item()) != 0:
             raise DeltaError(_abi.DELTA_ERR_OUT_OF_RANGE, "an index was outside the tensors")
+
+
+# -------------------------------------------------------------- LEB128
+
+def _segs(seg_offsets, seg_bases, device):
+    if seg_offsets is None:
+        return None, None, 0
+    offs = torch.as_tensor(seg_offsets, dtype=torch.int64, device=device).contiguous()
+    bases = torch.as_tensor(seg_bases, dtype=torch.int64, device=device).contiguous()
+    if bases.numel() + 1 != offs.numel():
+        raise ValueError("seg_offsets needs one entry more than seg_bases")
+    return offs, bases, bases.numel()
+
+
+def delta_leb128_encode(idx: torch.Tensor, seg_offsets=None, seg_bases=None,
+                        capacity: Optional[int] = None,
+                        stream: Optional[torch.cuda.Stream] = None):
+    """Gap + unsigned LEB128 bytes of a sorted int64 index stream (Sec. 5.1).
+
+    With segments (``seg_offsets`` of len S+1 in entries, ``seg_bases`` of
+    len S), segment s starts again from ``idx - seg_bases[s]``.  Returns the
+    uint8 GPU tensor of the bytes and, with segments, the byte offset of
+    every segment (S+1 entries).  Synchronises; raises DeltaError if the
+    indices were not increasing."""
+    if idx.dtype != torch.int64 or not idx.is_cuda or not idx.is_contiguous():
+        raise TypeError("idx must be a contiguous int64 GPU tensor")
+    dev = idx.device
+    offs, bases, S = _segs(seg_offsets, seg_bases, dev)
+    K = idx.numel()
+    ws = _workspace(library().delta_leb128_encode_workspace_bytes(K), dev)
+    nbytes = torch.zeros(1, dtype=torch.int64, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    sbo = torch.zeros(S + 1, dtype=torch.int64, device=dev) if S else None
+    cap = 10 * K if capacity is None else int(capacity)
+    out = torch.empty(max(cap, 1), dtype=torch.uint8, device=dev)
+    _check(library().delta_leb128_encode(
+        idx.data_ptr(), K, offs.data_ptr() if S else None, bases.data_ptr() if S else None, S,
+        out.data_ptr(), cap, nbytes.data_ptr(), sbo.data_ptr() if S else None, flag.data_ptr(),
+        ws.data_ptr(), ws.numel(), _stream(stream)))
+    (stream or torch.cuda.current_stream()).synchronize()
+    if int(flag.item()):
+        raise DeltaError(_abi.DELTA_ERR_INVALID_ARG, "indices not increasing within a segment")
+    n = int(nbytes.item())
+    if n > cap:
+        raise DeltaError(_abi.DELTA_ERR_CAPACITY, f"{n} bytes do not fit {cap}")
+    return out[:n], sbo
+
+
+def delta_leb128_decode(buf: torch.Tensor, seg_offsets=None, seg_bases=None,
+                        capacity: Optional[int] = None,
+                        stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """Indices from a gap + LEB128 byte stream (inverse of the encoder).
+    Synchronises; raises DeltaError on a malformed stream."""
+    if buf.dtype != torch.uint8 or not buf.is_cuda or not buf.is_contiguous():
+        raise TypeError("buf must be a contiguous uint8 GPU tensor")
+    dev = buf.device
+    offs, bases, S = _segs(seg_offsets, seg_bases, dev)
+    nb = buf.numel()
+    cap = nb if capacity is None else int(capacity)
+    ws = _workspace(library().delta_leb128_decode_workspace_bytes(nb, cap, S), dev)
+    out = torch.empty(max(cap, 1), dtype=torch.int64, device=dev)
+    cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    _check(library().delta_leb128_decode(
+        buf.data_ptr(), nb, offs.data_ptr() if S else None, bases.data_ptr() if S else None, S,
+        out.data_ptr(), cap, cnt.data_ptr(), flag.data_ptr(), ws.data_ptr(), ws.numel(),
+        _stream(stream)))
+    (stream or torch.cuda.current_stream()).synchronize()
+    if int(flag.item()):
+        raise DeltaError(_abi.DELTA_ERR_INVALID_ARG, "malformed LEB128 stream")
+    k = int(cnt.item())
+    if k > cap:
+        raise DeltaError(_abi.DELTA_ERR_CAPACITY, f"{k} numbers do not fit {cap}")
+    return out[:k]
 
 
 # ------------------------------------------------------------ pipeline

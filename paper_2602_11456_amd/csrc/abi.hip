@@ -313,4 +313,78 @@ delta_status_t delta_apply_multi(uint16_t* const* weight_ptrs, const uint64_t* n
   return ok();
 }
 
+size_t delta_leb128_encode_workspace_bytes(uint64_t count) { return enc_layout(count).total; }
+
+size_t delta_leb128_decode_workspace_bytes(uint64_t nbytes, uint64_t capacity, uint32_t num_segs) {
+  return dec_layout(nbytes, capacity, num_segs).total;
+}
+
+delta_status_t delta_leb128_encode(const int64_t* idx, uint64_t count,
+                                   const uint64_t* d_seg_offsets, const uint64_t* d_seg_bases,
+                                   uint32_t num_segs, uint8_t* out, uint64_t capacity,
+                                   uint64_t* d_nbytes, uint64_t* d_seg_byte_offsets,
+                                   uint32_t* d_error_flag, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  if (!d_nbytes) return fail(DELTA_ERR_INVALID_ARG, "d_nbytes is NULL");
+  if (count > 0 && !idx) return fail(DELTA_ERR_INVALID_ARG, "idx is NULL");
+  if ((uintptr_t)idx % 8) return fail(DELTA_ERR_INVALID_ARG, "idx not 8-byte aligned");
+  if (capacity > 0 && !out) return fail(DELTA_ERR_INVALID_ARG, "out is NULL with capacity > 0");
+  if (num_segs > 0 && (!d_seg_offsets || !d_seg_bases))
+    return fail(DELTA_ERR_INVALID_ARG, "segment arrays are NULL");
+  if (d_seg_byte_offsets && num_segs == 0)
+    return fail(DELTA_ERR_INVALID_ARG, "segment byte offsets need num_segs > 0");
+  const EncLayout L = enc_layout(count);
+  if (L.tiles > 0xFFFFFFFFull / 256) return fail(DELTA_ERR_INVALID_ARG, "too many entries");
+  delta_status_t st = check_workspace(workspace, workspace_bytes, L.total);
+  if (st != DELTA_OK) return st;
+  char* ws = (char*)workspace;
+  EncArgs a;
+  memset(&a, 0, sizeof(a));
+  a.idx = idx;
+  a.count = count;
+  a.segs = {d_seg_offsets, d_seg_bases, num_segs};
+  a.out = out;
+  a.capacity = capacity;
+  a.d_nbytes = d_nbytes;
+  a.seg_byte_offsets = d_seg_byte_offsets;
+  a.err = d_error_flag;
+  a.tile_bytes = (uint32_t*)(ws + L.tile_bytes);
+  hipError_t e = launch_leb128_encode(a, (uint64_t*)(ws + L.group_sum),
+                                      (uint64_t*)(ws + L.group_excl), stream);
+  if (e != hipSuccess) return hip_fail(e, "leb128 encode launch");
+  return ok();
+}
+
+delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
+                                   const uint64_t* d_seg_offsets, const uint64_t* d_seg_bases,
+                                   uint32_t num_segs, int64_t* out_idx, uint64_t capacity,
+                                   uint64_t* d_count, uint32_t* d_error_flag, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
+  if (!d_count) return fail(DELTA_ERR_INVALID_ARG, "d_count is NULL");
+  if (nbytes > 0 && !in) return fail(DELTA_ERR_INVALID_ARG, "in is NULL");
+  if (capacity > 0 && !out_idx) return fail(DELTA_ERR_INVALID_ARG, "out_idx is NULL");
+  if ((uintptr_t)out_idx % 8) return fail(DELTA_ERR_INVALID_ARG, "out_idx not 8-byte aligned");
+  if (num_segs > 0 && (!d_seg_offsets || !d_seg_bases))
+    return fail(DELTA_ERR_INVALID_ARG, "segment arrays are NULL");
+  const DecLayout L = dec_layout(nbytes, capacity, num_segs);
+  if (L.btiles > 0xFFFFFFFFull / 256 || L.etiles > 0xFFFFFFFFull / 256)
+    return fail(DELTA_ERR_INVALID_ARG, "stream too long");
+  delta_status_t st = check_workspace(workspace, workspace_bytes, L.total);
+  if (st != DELTA_OK) return st;
+  char* ws = (char*)workspace;
+  DecArgs a;
+  memset(&a, 0, sizeof(a));
+  a.in = in;
+  a.nbytes = nbytes;
+  a.segs = {d_seg_offsets, d_seg_bases, num_segs};
+  a.out = out_idx;
+  a.capacity = capacity;
+  a.d_count = d_count;
+  a.err = d_error_flag;
+  a.tile_terms = (uint32_t*)(ws + L.tile_terms);
+  hipError_t e = launch_leb128_decode(a, L, ws, stream);
+  if (e != hipSuccess) return hip_fail(e, "leb128 decode launch");
+  return ok();
+}
+
 }  // extern "C"

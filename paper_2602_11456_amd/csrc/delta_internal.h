@@ -158,6 +158,12 @@ hipError_t launch_upload_words(const uint64_t* host_words, size_t nwords, uint64
                                hipStream_t stream);
 hipError_t launch_build_tile_map(const TensorDesc* table, uint32_t num_tensors,
                                  uint32_t* tile_map, hipStream_t stream);
+// Exclusive scan of per-tile counts in groups of kTilesPerGroup tiles:
+// group_sum / group_excl get one entry per group, *d_total the sum.
+hipError_t launch_group_scan(const uint32_t* counts, uint64_t num_tiles, uint64_t* group_sum,
+                             uint64_t* group_excl, uint64_t* d_total, hipStream_t stream);
+hipError_t launch_group_scan(const uint64_t* counts, uint64_t num_tiles, uint64_t* group_sum,
+                             uint64_t* group_excl, uint64_t* d_total, hipStream_t stream);
 // all_vec: every slice has prev and next at the same 16-byte alignment.
 hipError_t launch_extract(const ExtractArgs& a, bool idx64, bool all_vec, hipStream_t stream);
 
@@ -185,6 +191,60 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
                                bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
                                uint64_t* d_count, uint64_t* d_offsets, void* workspace,
                                size_t workspace_bytes, hipStream_t stream);
+
+// ------------------------------------------------------ LEB128 (leb128.hip)
+
+// Segments of an index stream: entries [offs[s], offs[s + 1]) form segment
+// s (offs has num + 1 entries, device memory); its first entry is coded
+// relative to bases[s].  num == 0: one segment with base 0.
+struct LebSegs {
+  const uint64_t* offs;
+  const uint64_t* bases;
+  uint32_t num;
+};
+
+struct EncArgs {
+  const int64_t* idx;
+  uint64_t count;
+  LebSegs segs;
+  uint8_t* out;
+  uint64_t capacity;
+  uint64_t* d_nbytes;
+  uint64_t* seg_byte_offsets;   // nullable, num + 1 entries
+  uint32_t* err;                // nullable
+  uint32_t* tile_bytes;
+  uint64_t* group_excl;
+};
+
+struct DecArgs {
+  const uint8_t* in;
+  uint64_t nbytes;
+  LebSegs segs;
+  int64_t* out;
+  uint64_t capacity;
+  uint64_t* d_count;
+  uint32_t* err;                // nullable
+  uint32_t* tile_terms;
+  uint64_t* group_excl;
+  uint64_t* sum_tile;
+  uint64_t* sum_group_excl;
+  int64_t* corr;
+};
+
+struct EncLayout {
+  uint64_t tiles;
+  size_t tile_bytes, group_sum, group_excl, total;
+};
+struct DecLayout {
+  uint64_t btiles, etiles;
+  size_t tile_terms, group_sum, group_excl, sum_tile, sum_group_sum, sum_group_excl, sum_total,
+      corr, total;
+};
+EncLayout enc_layout(uint64_t count);
+DecLayout dec_layout(uint64_t nbytes, uint64_t capacity, uint32_t num_segs);
+hipError_t launch_leb128_encode(EncArgs a, uint64_t* group_sum, uint64_t* group_excl,
+                                hipStream_t stream);
+hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStream_t stream);
 
 // Thread-local detail text behind delta_last_error() (abi.hip).
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));

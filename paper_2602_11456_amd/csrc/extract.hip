@@ -254,10 +254,11 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
 // ----------------------------------------------------------------- scan
 
 // Sum of the counts of each group of kTilesPerGroup tiles (one wavefront).
-__global__ __launch_bounds__(64) void group_sum_kernel(const uint32_t* counts, uint64_t num_tiles,
+template <typename CountT>
+__global__ __launch_bounds__(64) void group_sum_kernel(const CountT* counts, uint64_t num_tiles,
                                                        uint64_t* group_sum) {
   const uint64_t t = (uint64_t)blockIdx.x * kTilesPerGroup + threadIdx.x;
-  const uint64_t c = t < num_tiles ? counts[t] : 0;
+  const uint64_t c = t < num_tiles ? (uint64_t)counts[t] : 0;
   const uint64_t s = wave_sum64(c);
   if (threadIdx.x == 0) group_sum[blockIdx.x] = s;
 }
@@ -451,6 +452,30 @@ hipError_t launch_build_tile_map(const TensorDesc* table, uint32_t num_tensors,
   return hipGetLastError();
 }
 
+template <typename CountT>
+static hipError_t launch_group_scan_t(const CountT* counts, uint64_t num_tiles,
+                                      uint64_t* group_sum, uint64_t* group_excl,
+                                      uint64_t* d_total, hipStream_t stream) {
+  const uint64_t groups = groups_for(num_tiles);
+  hipLaunchKernelGGL(group_sum_kernel<CountT>, dim3((uint32_t)groups), dim3(64), 0, stream,
+                     counts, num_tiles, group_sum);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(group_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, group_sum, groups,
+                     group_excl, d_total);
+  return hipGetLastError();
+}
+
+hipError_t launch_group_scan(const uint32_t* counts, uint64_t num_tiles, uint64_t* group_sum,
+                             uint64_t* group_excl, uint64_t* d_total, hipStream_t stream) {
+  return launch_group_scan_t(counts, num_tiles, group_sum, group_excl, d_total, stream);
+}
+
+hipError_t launch_group_scan(const uint64_t* counts, uint64_t num_tiles, uint64_t* group_sum,
+                             uint64_t* group_excl, uint64_t* d_total, hipStream_t stream) {
+  return launch_group_scan_t(counts, num_tiles, group_sum, group_excl, d_total, stream);
+}
+
 template <typename IdxT, bool kMulti, bool kVec>
 static hipError_t launch_all(const ExtractArgs& a, hipStream_t stream) {
   const uint64_t groups = (a.num_tiles + kTilesPerGroup - 1) / kTilesPerGroup;
@@ -458,13 +483,7 @@ static hipError_t launch_all(const ExtractArgs& a, hipStream_t stream) {
                      0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(group_sum_kernel, dim3((uint32_t)groups), dim3(64), 0, stream, a.counts,
-                     a.num_tiles, a.group_sum);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(group_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, a.group_sum,
-                     groups, a.group_excl, a.d_count);
-  e = hipGetLastError();
+  e = launch_group_scan(a.counts, a.num_tiles, a.group_sum, a.group_excl, a.d_count, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((finalize_kernel<IdxT, kMulti, kVec>), dim3((uint32_t)groups),
                      dim3(kThreads), 0, stream, a);

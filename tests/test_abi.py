@@ -145,3 +145,43 @@ def test_pipeline_validation(lib):
     assert lib.delta_extract_pipelined(prevs, prevs, numels, 1, ctypes.byref(opts), streams,
                                        FAKE, 8, FAKE, FAKE, 10, ctypes.byref(cnt)) == \
         _abi.DELTA_ERR_WORKSPACE
+
+
+def test_leb128_sizes_and_validation(lib):
+    e0 = lib.delta_leb128_encode_workspace_bytes(0)
+    e1 = lib.delta_leb128_encode_workspace_bytes(4096)
+    e2 = lib.delta_leb128_encode_workspace_bytes(4097)
+    assert e0 <= e1 <= e2 < lib.delta_leb128_encode_workspace_bytes(1 << 24)
+    d0 = lib.delta_leb128_decode_workspace_bytes(0, 0, 0)
+    d1 = lib.delta_leb128_decode_workspace_bytes(1 << 20, 1 << 20, 0)
+    assert d0 < d1 < lib.delta_leb128_decode_workspace_bytes(1 << 20, 1 << 20, 1000)
+    # capacity only matters up to nbytes (a number takes at least one byte)
+    assert lib.delta_leb128_decode_workspace_bytes(100, 1 << 40, 0) == \
+        lib.delta_leb128_decode_workspace_bytes(100, 100, 0)
+    nb = FAKE
+    ws = FAKE
+    E = lib.delta_leb128_encode
+    assert E(FAKE, 10, None, None, 0, FAKE, 100, None, None, None, ws, e1, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # no d_nbytes
+    assert E(FAKE + 4, 10, None, None, 0, FAKE, 100, nb, None, None, ws, e1, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # misaligned idx
+    assert E(FAKE, 10, None, None, 0, None, 100, nb, None, None, ws, e1, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # no output with capacity
+    assert E(FAKE, 10, None, FAKE, 2, FAKE, 100, nb, None, None, ws, e1, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # segments without offsets
+    assert E(FAKE, 10, None, None, 0, FAKE, 100, nb, FAKE, None, ws, e1, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # segment byte offsets without segments
+    assert E(FAKE, 10, None, None, 0, FAKE, 100, nb, None, None, ws, 8, None) == \
+        _abi.DELTA_ERR_WORKSPACE
+    D = lib.delta_leb128_decode
+    dw = lib.delta_leb128_decode_workspace_bytes(100, 100, 0)
+    assert D(FAKE, 100, None, None, 0, FAKE, 100, None, None, ws, dw, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # no d_count
+    assert D(None, 100, None, None, 0, FAKE, 100, nb, None, ws, dw, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    assert D(FAKE, 100, None, None, 0, FAKE + 2, 100, nb, None, ws, dw, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # misaligned output
+    assert D(FAKE, 100, FAKE, None, 3, FAKE, 100, nb, None, ws, dw, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    assert D(FAKE, 100, None, None, 0, FAKE, 100, nb, None, ws, 8, None) == \
+        _abi.DELTA_ERR_WORKSPACE
