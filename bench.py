@@ -152,6 +152,27 @@ def pipeline_measurement(args, dev):
         ctimes.append(time.perf_counter() - t0)
     t = sorted(times)[len(times) // 2]
     tc = min(ctimes)
+    del src, dst, h_idx, i
+
+    # the same pipeline with the indices gap + LEB128 coded before the copy
+    staging = None
+    torch.cuda.empty_cache()
+    staging = torch.empty(ad.delta_pipeline_leb128_staging_bytes(plan.numels, chunk, nstreams),
+                          dtype=torch.uint8, device=dev)
+    h_bytes = torch.empty(3 * K + 4096, dtype=torch.uint8, pin_memory=True)
+    ltimes = []
+    for rep in range(args.pipeline_reps + 1):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        b, v2, counts, used = ad.delta_extract_pipelined_leb128(
+            ws.prev, ws.new, chunk, nstreams, h_bytes, h_val, staging, streams)
+        tl = time.perf_counter() - t0
+        if v2.numel() != K:
+            raise RuntimeError(f"coded pipeline found {v2.numel()} changed words, {K} planted")
+        if rep:
+            ltimes.append(tl)
+    tl = sorted(ltimes)[len(ltimes) // 2]
+    coded_bytes = b.numel() + 2 * K
     return {
         "workload": f"qwen3-14b weight set, {len(ws.prev)} tensors, {ws.total} bf16 words, "
                     f"{args.density:.2%} changed, {chunk}-word chunks over {nstreams} streams "
@@ -161,7 +182,88 @@ def pipeline_measurement(args, dev):
         "d2h_GBps": round(out_bytes / t / 1e9, 2),
         "d2h_ceiling_GBps": round(out_bytes / tc / 1e9, 2),
         "d2h_bytes": out_bytes,
+        "leb128": {
+            "ms": round(tl * 1e3, 3),
+            "GBps_scanned": round(4 * ws.total / tl / 1e9, 1),
+            "d2h_bytes": coded_bytes,
+            "index_bytes_per_entry": round(b.numel() / K, 4),
+            "d2h_GBps": round(coded_bytes / tl / 1e9, 2),
+        },
     }
+
+
+def leb128_measurement(ad, idx, d_offs, numels, stream, reps):
+    """Gap + LEB128 encode of the extracted global indices with one segment
+    per tensor (tensor-local first index), then decode, each timed with HIP
+    events on the launch stream; the decode must return the indices."""
+    import torch
+    lib = ad.library()
+    dev = idx.device
+    K = idx.numel()
+    T = len(numels)
+    bases = torch.tensor([0] + list(_prefix(numels))[:-1], dtype=torch.int64, device=dev)
+    h = stream.cuda_stream
+    enc_ws = torch.empty(max(lib.delta_leb128_encode_workspace_bytes(K), 1), dtype=torch.uint8,
+                         device=dev)
+    cap = 10 * K
+    buf = torch.empty(max(cap, 1), dtype=torch.uint8, device=dev)
+    nbytes = torch.zeros(1, dtype=torch.int64, device=dev)
+    seg_bytes = torch.zeros(T + 1, dtype=torch.int64, device=dev)
+
+    def encode():
+        st = lib.delta_leb128_encode(idx.data_ptr(), K, d_offs.data_ptr(), bases.data_ptr(), T,
+                                     buf.data_ptr(), cap, nbytes.data_ptr(), seg_bytes.data_ptr(),
+                                     None, enc_ws.data_ptr(), enc_ws.numel(), h)
+        if st:
+            raise RuntimeError(lib.delta_last_error().decode())
+
+    encode()
+    stream.synchronize()
+    nb = int(nbytes.item())
+    dec_ws = torch.empty(lib.delta_leb128_decode_workspace_bytes(nb, K, T), dtype=torch.uint8,
+                         device=dev)
+    out = torch.empty(max(K, 1), dtype=torch.int64, device=dev)
+    cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def decode():
+        st = lib.delta_leb128_decode(buf.data_ptr(), nb, d_offs.data_ptr(), bases.data_ptr(), T,
+                                     out.data_ptr(), K, cnt.data_ptr(), flag.data_ptr(),
+                                     dec_ws.data_ptr(), dec_ws.numel(), h)
+        if st:
+            raise RuntimeError(lib.delta_last_error().decode())
+
+    decode()
+    stream.synchronize()
+    if int(cnt.item()) != K or int(flag.item()) or not torch.equal(out[:K], idx):
+        raise RuntimeError("LEB128 decode does not return the extracted indices")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    for e0, e1, e2 in ev:
+        e0.record(stream)
+        encode()
+        e1.record(stream)
+        decode()
+        e2.record(stream)
+    stream.synchronize()
+    enc = sorted(e0.elapsed_time(e1) for e0, e1, _ in ev)[reps // 2]
+    dec = sorted(e1.elapsed_time(e2) for _, e1, e2 in ev)[reps // 2]
+    return {
+        "workload": f"the {K} extracted int64 global indices, one segment per tensor",
+        "bytes": nb,
+        "bytes_per_entry": round(nb / K, 4),
+        "encode_ms": round(enc, 4),
+        "decode_ms": round(dec, 4),
+        # encode reads the indices (twice: sizes, then bytes) and writes the bytes
+        "encode_GBps_algorithmic": round((8 * K + nb) / (enc / 1e3) / 1e9, 1),
+        "decode_GBps_algorithmic": round((nb + 8 * K) / (dec / 1e3) / 1e9, 1),
+    }
+
+
+def _prefix(xs):
+    s = 0
+    for x in xs:
+        s += x
+        yield s
 
 
 def main():
@@ -306,6 +408,8 @@ def main():
             "traffic": traffic,
         },
     }
+    result["leb128"] = leb128_measurement(ad, out_idx[:K], d_offs, plan.numels, stream,
+                                          args.steps)
     if args.copy_calibration > 0:
         n = args.copy_calibration // 2
         src = torch.empty(n, dtype=torch.int16, device=dev)

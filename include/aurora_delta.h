@@ -274,6 +274,35 @@ delta_status_t delta_extract_pipelined(const uint16_t* const* prev_ptrs,
                                        size_t staging_bytes, int64_t* h_idx, uint16_t* h_val,
                                        uint64_t h_capacity, uint64_t* h_count);
 
+/* Device staging bytes delta_extract_pipelined_leb128 needs: the plain
+ * pipeline's staging plus, per stream, the coded bytes of one chunk and the
+ * encoder's workspace. */
+size_t delta_pipeline_leb128_staging_bytes(const uint64_t* numels, int32_t num_tensors,
+                                           const delta_pipeline_opts_t* opts);
+
+/*
+ * delta_extract_pipelined_leb128 — the Sec. 5.2 pipeline with the index
+ * stream gap + LEB128 coded on the GPU before it crosses the host link
+ * (Sec. 5.1 encoding; at 1% density about 1.3 bytes per index instead of
+ * 8).  Each chunk is one segment of the coded stream, based at the chunk's
+ * first word (c * chunk, chunk = min(opts->chunk_elems, total words)):
+ * delta_leb128_decode with seg_offsets = prefix sums of h_chunk_counts and
+ * seg_bases[c] = c * chunk returns delta_extract_multi's indices exactly.
+ *   h_bytes       pinned host bytes [h_bytes_capacity]: the coded indices.
+ *   h_val         pinned host words [h_val_capacity]: as delta_extract_multi.
+ *   h_chunk_counts host array [h_num_chunks >= ceil(total / chunk)]:
+ *                 entries of each chunk.
+ *   h_count, h_nbytes  host: entry and byte totals.
+ * Host-synchronous.  DELTA_ERR_CAPACITY (totals set, what fits written)
+ * when either output does not fit.
+ */
+delta_status_t delta_extract_pipelined_leb128(
+    const uint16_t* const* prev_ptrs, const uint16_t* const* next_ptrs, const uint64_t* numels,
+    int32_t num_tensors, const delta_pipeline_opts_t* opts, hipStream_t* streams,
+    void* d_staging, size_t staging_bytes, uint8_t* h_bytes, uint64_t h_bytes_capacity,
+    uint16_t* h_val, uint64_t h_val_capacity, uint64_t* h_chunk_counts, uint64_t h_num_chunks,
+    uint64_t* h_count, uint64_t* h_nbytes);
+
 #ifdef __cplusplus
 }
 #endif

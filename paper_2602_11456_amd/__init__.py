@@ -29,6 +29,7 @@ __all__ = [
     "delta_extract_pipelined", "delta_extract_workspace_bytes",
     "delta_extract_multi_workspace_bytes", "delta_apply_multi_workspace_bytes",
     "delta_pipeline_staging_bytes", "MultiPlan", "delta_leb128_encode", "delta_leb128_decode",
+    "delta_extract_pipelined_leb128", "delta_pipeline_leb128_staging_bytes", "chunk_segments",
 ]
 
 
@@ -104,6 +105,13 @@ def delta_pipeline_staging_bytes(numels: Sequence[int], chunk_elems: int, num_st
     opts = _abi.delta_pipeline_opts_t(int(chunk_elems), int(num_streams), 0)
     return int(library().delta_pipeline_staging_bytes(_u64_array(numels), len(numels),
                                                       ctypes.byref(opts)))
+
+
+def delta_pipeline_leb128_staging_bytes(numels: Sequence[int], chunk_elems: int,
+                                        num_streams: int) -> int:
+    opts = _abi.delta_pipeline_opts_t(int(chunk_elems), int(num_streams), 0)
+    return int(library().delta_pipeline_leb128_staging_bytes(_u64_array(numels), len(numels),
+                                                             ctypes.byref(opts)))
 
 
 # ------------------------------------------------------------- extract
@@ -400,3 +408,63 @@ def delta_extract_pipelined(prevs: Sequence[torch.Tensor], news: Sequence[torch.
     _check(status)
     k = count.value
     return h_idx[:k], h_val[:k]
+
+
+def chunk_segments(chunk_counts: Sequence[int], chunk_elems: int):
+    """Segment offsets (entries) and bases (words) of a coded pipeline
+    stream: chunk c is one segment based at its first word c * chunk_elems.
+    Pass them to :func:`delta_leb128_decode`."""
+    counts = [int(c) for c in chunk_counts]
+    offs = [0]
+    for c in counts:
+        offs.append(offs[-1] + c)
+    bases = [c * int(chunk_elems) for c in range(len(counts))]
+    return offs, bases
+
+
+def delta_extract_pipelined_leb128(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tensor],
+                                   chunk_elems: int = 1 << 27, num_streams: int = 4,
+                                   h_bytes: Optional[torch.Tensor] = None,
+                                   h_val: Optional[torch.Tensor] = None,
+                                   staging: Optional[torch.Tensor] = None,
+                                   streams: Optional[List[torch.cuda.Stream]] = None):
+    """Chunked extract whose indices reach the host gap + LEB128 coded
+    (Sec. 5.1 encoding inside the Sec. 5.2 pipeline).  Returns the host
+    views (index bytes, values) of the filled part, the per-chunk entry
+    counts and the chunk size actually used; :func:`chunk_segments` turns
+    the last two into the decoder's segments.  Host-synchronous."""
+    plan = MultiPlan(prevs, news)
+    dev = plan.device
+    if streams is None:
+        streams = [torch.cuda.Stream(device=dev) for _ in range(num_streams)]
+    if len(streams) != num_streams:
+        raise ValueError("need one stream per pipeline lane")
+    need = delta_pipeline_leb128_staging_bytes(plan.numels, chunk_elems, num_streams)
+    stage = staging if staging is not None else _workspace(need, dev)
+    chunk = min(int(chunk_elems), plan.total) if plan.total else 1
+    nchunks = (plan.total + chunk - 1) // chunk
+    if h_val is None:
+        cap = _default_capacity(plan.total)
+        h_val = torch.empty(cap, dtype=torch.bfloat16, pin_memory=True)
+    if h_bytes is None:
+        h_bytes = torch.empty(max(3 * h_val.numel(), 1), dtype=torch.uint8, pin_memory=True)
+    if h_bytes.dtype != torch.uint8 or h_val.element_size() != 2:
+        raise TypeError("h_bytes must be uint8 and h_val 16-bit")
+    counts = (ctypes.c_uint64 * max(nchunks, 1))()
+    opts = _abi.delta_pipeline_opts_t(int(chunk_elems), int(num_streams), 0)
+    handles = _ptr_array([s.cuda_stream for s in streams])
+    count = ctypes.c_uint64(0)
+    nbytes = ctypes.c_uint64(0)
+    torch.cuda.current_stream().synchronize()
+    status = library().delta_extract_pipelined_leb128(
+        plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, plan.T, ctypes.byref(opts), handles,
+        stage.data_ptr(), stage.numel(), h_bytes.data_ptr(), h_bytes.numel(), h_val.data_ptr(),
+        h_val.numel(), counts, nchunks, ctypes.byref(count), ctypes.byref(nbytes))
+    if status == _abi.DELTA_ERR_CAPACITY:
+        hb = torch.empty(max(nbytes.value, 1), dtype=torch.uint8, pin_memory=True)
+        hv = torch.empty(max(count.value, 1), dtype=h_val.dtype, pin_memory=True)
+        return delta_extract_pipelined_leb128(prevs, news, chunk_elems, num_streams, hb, hv,
+                                              stage, streams)
+    _check(status)
+    return (h_bytes[:nbytes.value], h_val[:count.value], [int(c) for c in counts[:nchunks]],
+            chunk)

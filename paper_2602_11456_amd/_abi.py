@@ -58,6 +58,10 @@ SIGNATURES = {
     "delta_pipeline_staging_bytes": (SZ, [P, I32, ctypes.POINTER(delta_pipeline_opts_t)]),
     "delta_extract_pipelined": (STATUS, [P, P, P, I32, ctypes.POINTER(delta_pipeline_opts_t), P,
                                          P, SZ, P, P, U64, P]),
+    "delta_pipeline_leb128_staging_bytes": (SZ, [P, I32, ctypes.POINTER(delta_pipeline_opts_t)]),
+    "delta_extract_pipelined_leb128": (STATUS, [P, P, P, I32,
+                                                ctypes.POINTER(delta_pipeline_opts_t), P, P, SZ,
+                                                P, U64, P, U64, P, U64, P, P]),
 }
 
 _lib = None

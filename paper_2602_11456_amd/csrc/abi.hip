@@ -342,7 +342,7 @@ delta_status_t delta_leb128_encode(const int64_t* idx, uint64_t count,
   memset(&a, 0, sizeof(a));
   a.idx = idx;
   a.count = count;
-  a.segs = {d_seg_offsets, d_seg_bases, num_segs};
+  a.segs = {d_seg_offsets, d_seg_bases, num_segs, 0};
   a.out = out;
   a.capacity = capacity;
   a.d_nbytes = d_nbytes;
@@ -376,7 +376,7 @@ delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
   memset(&a, 0, sizeof(a));
   a.in = in;
   a.nbytes = nbytes;
-  a.segs = {d_seg_offsets, d_seg_bases, num_segs};
+  a.segs = {d_seg_offsets, d_seg_bases, num_segs, 0};
   a.out = out_idx;
   a.capacity = capacity;
   a.d_count = d_count;

@@ -196,11 +196,12 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
 
 // Segments of an index stream: entries [offs[s], offs[s + 1]) form segment
 // s (offs has num + 1 entries, device memory); its first entry is coded
-// relative to bases[s].  num == 0: one segment with base 0.
+// relative to bases[s].  num == 0: one segment based at base0.
 struct LebSegs {
   const uint64_t* offs;
   const uint64_t* bases;
   uint32_t num;
+  int64_t base0;
 };
 
 struct EncArgs {

@@ -35,7 +35,7 @@ __device__ __forceinline__ uint32_t leb_len(uint64_t v) {
 }
 
 // Segment of entry k: the last s < num with offs[s] <= k (num == 0: one
-// segment with base 0).
+// segment, based at base0).
 __device__ __forceinline__ uint32_t seg_of(const LebSegs& g, uint64_t k) {
   if (g.num == 0) return 0;
   uint32_t lo = 0, hi = g.num;
@@ -52,7 +52,7 @@ __device__ __forceinline__ uint64_t seg_hi(const LebSegs& g, uint32_t s) {
   return (g.num && s + 1 < g.num) ? g.offs[s + 1] : ~0ull;
 }
 __device__ __forceinline__ int64_t seg_base(const LebSegs& g, uint32_t s) {
-  return g.num ? (int64_t)g.bases[s] : 0;
+  return g.num ? (int64_t)g.bases[s] : g.base0;
 }
 
 // Exclusive prefix of v over the workgroup (kLebThreads threads) and the

@@ -42,15 +42,29 @@ void chunk_slices(const uint16_t* const* prevs, const uint16_t* const* nexts,
 
 
 struct StagingLayout {
-  size_t idx, val, count, ws, ws_bytes, per_stream;
+  size_t idx, val, count, nbytes, bytes, enc_ws, ws, ws_bytes, per_stream;
 };
 
-StagingLayout staging_layout(uint64_t chunk, size_t ws_bytes) {
+// Longest LEB128 code of a number below `chunk` (every gap inside a chunk,
+// and its first index relative to the chunk start, is below the chunk size).
+uint64_t leb_bytes_per_entry(uint64_t chunk) {
+  uint64_t v = chunk > 0 ? chunk - 1 : 0, n = 1;
+  while (v >= 128) {
+    v >>= 7;
+    ++n;
+  }
+  return n;
+}
+
+StagingLayout staging_layout(uint64_t chunk, size_t ws_bytes, bool leb) {
   StagingLayout L;
   L.idx = 0;
   L.val = align_up(L.idx + 8 * chunk);
   L.count = align_up(L.val + 2 * chunk);
-  L.ws = align_up(L.count + 8);
+  L.nbytes = L.count + 8;
+  L.bytes = align_up(L.nbytes + 8);
+  L.enc_ws = align_up(L.bytes + (leb ? leb_bytes_per_entry(chunk) * chunk : 0));
+  L.ws = align_up(L.enc_ws + (leb ? enc_layout(chunk).total : 0));
   L.ws_bytes = ws_bytes;
   L.per_stream = align_up(L.ws + ws_bytes);
   return L;
@@ -81,8 +95,8 @@ size_t max_chunk_workspace(const uint64_t* numels, int32_t T, uint64_t total, ui
 
 extern "C" {
 
-size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
-                                    const delta_pipeline_opts_t* opts) {
+static size_t staging_bytes_impl(const uint64_t* numels, int32_t num_tensors,
+                                 const delta_pipeline_opts_t* opts, bool leb) {
   if (!opts || opts->chunk_elems == 0 || opts->num_streams < 1 || opts->num_streams > 16 ||
       num_tensors < 0 || (num_tensors > 0 && !numels))
     return 0;
@@ -90,24 +104,49 @@ size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
   for (int32_t t = 0; t < num_tensors; ++t) total += numels[t];
   const uint64_t chunk = opts->chunk_elems < total ? opts->chunk_elems : (total ? total : 1);
   const size_t ws = max_chunk_workspace(numels, num_tensors, total, chunk);
-  return staging_layout(chunk, ws).per_stream * (size_t)opts->num_streams;
+  return staging_layout(chunk, ws, leb).per_stream * (size_t)opts->num_streams;
+}
+
+size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
+                                    const delta_pipeline_opts_t* opts) {
+  return staging_bytes_impl(numels, num_tensors, opts, false);
+}
+
+size_t delta_pipeline_leb128_staging_bytes(const uint64_t* numels, int32_t num_tensors,
+                                           const delta_pipeline_opts_t* opts) {
+  return staging_bytes_impl(numels, num_tensors, opts, true);
 }
 
 }  // extern "C"
 
-// Host-synchronous pipeline.  Defined with C linkage below.
+// Where the pipeline's output goes (pinned host memory).
+struct PipeOut {
+  bool leb;                  // indices gap + LEB128 coded, one segment per chunk
+  int64_t* h_idx;            // plain: indices
+  uint64_t h_idx_cap;
+  uint8_t* h_bytes;          // coded: index bytes
+  uint64_t h_bytes_cap;
+  uint16_t* h_val;
+  uint64_t h_val_cap;
+  uint64_t* h_chunk_counts;  // coded: entries per chunk (host array)
+  uint64_t h_num_chunks;
+};
+
+// Host-synchronous pipeline.  *h_count gets the entry total and, coded,
+// *h_nbytes the byte total.
 static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t* const* nexts,
                                     const uint64_t* numels, int32_t T,
                                     const delta_pipeline_opts_t* opts, hipStream_t* streams,
-                                    void* d_staging, size_t staging_bytes, int64_t* h_idx,
-                                    uint16_t* h_val, uint64_t h_cap, uint64_t* h_count) {
+                                    void* d_staging, size_t staging_bytes, const PipeOut& o,
+                                    uint64_t* h_count, uint64_t* h_nbytes) {
   clear_error();
   if (!opts || opts->chunk_elems == 0 || opts->num_streams < 1 || opts->num_streams > 16) {
     set_error("bad pipeline options");
     return DELTA_ERR_INVALID_ARG;
   }
   if (T < 0 || (T > 0 && (!prevs || !nexts || !numels)) || !streams || !h_count ||
-      (h_cap > 0 && (!h_idx || !h_val))) {
+      (o.h_val_cap > 0 && !o.h_val) || (!o.leb && o.h_idx_cap > 0 && !o.h_idx) ||
+      (o.leb && (!h_nbytes || (o.h_bytes_cap > 0 && !o.h_bytes)))) {
     set_error("NULL argument");
     return DELTA_ERR_INVALID_ARG;
   }
@@ -125,20 +164,29 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
   }
   const int S = opts->num_streams;
   *h_count = 0;
+  if (h_nbytes) *h_nbytes = 0;
+  const uint64_t chunk = total == 0 ? 1 : (opts->chunk_elems < total ? opts->chunk_elems : total);
+  const uint64_t nchunks = (total + chunk - 1) / chunk;
+  if (o.leb && (o.h_num_chunks < nchunks || (nchunks > 0 && !o.h_chunk_counts))) {
+    set_error("h_chunk_counts holds %llu entries, %llu chunks",
+              (unsigned long long)o.h_num_chunks, (unsigned long long)nchunks);
+    return DELTA_ERR_INVALID_ARG;
+  }
   if (total == 0) return DELTA_OK;
-  const uint64_t chunk = opts->chunk_elems < total ? opts->chunk_elems : total;
-  const size_t need = delta_pipeline_staging_bytes(numels, T, opts);
+  const size_t need = staging_bytes_impl(numels, T, opts, o.leb);
   if (!d_staging || (uintptr_t)d_staging % kAlign || staging_bytes < need) {
     set_error("staging: %zu bytes at %p, %zu needed (256-aligned)",
              staging_bytes, d_staging, need);
     return DELTA_ERR_WORKSPACE;
   }
   const size_t ws = max_chunk_workspace(numels, T, total, chunk);
-  const StagingLayout L = staging_layout(chunk, ws);
-  const uint64_t nchunks = (total + chunk - 1) / chunk;
+  const StagingLayout L = staging_layout(chunk, ws, o.leb);
+  const uint64_t bytes_cap = leb_bytes_per_entry(chunk) * chunk;
 
-  uint64_t* h_counts = nullptr;   // per-chunk counts land here (pinned)
-  hipError_t e = hipHostMalloc((void**)&h_counts, sizeof(uint64_t) * nchunks, hipHostMallocDefault);
+  // per chunk: entry count and (coded) byte count land here (pinned)
+  uint64_t* h_counts = nullptr;
+  hipError_t e =
+      hipHostMalloc((void**)&h_counts, sizeof(uint64_t) * 2 * nchunks, hipHostMallocDefault);
   if (e != hipSuccess) {
     set_error("hipHostMalloc: %s", hipGetErrorString(e));
     return DELTA_ERR_HIP;
@@ -146,27 +194,58 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
 
   std::vector<SliceIn> sl;
   uint64_t offset = 0;   // host position of the next chunk's first entry
-  uint64_t finished = 0; // chunks whose data copy is enqueued
+  uint64_t boffset = 0;  // coded: host position of the next chunk's first byte
+  uint64_t finished = 0; // chunks whose data copies are enqueued
   uint64_t issued = 0;   // chunks whose extract and count copy are enqueued
   delta_status_t status = DELTA_OK;
 
   auto stage_of = [&](uint64_t c) { return (char*)d_staging + L.per_stream * (c % S); };
+  auto copy_out = [&](void* dst, const void* src, uint64_t pos, uint64_t cap, uint64_t n,
+                      size_t elem, hipStream_t st) -> hipError_t {
+    if (pos >= cap || n == 0) return hipSuccess;
+    const uint64_t m = (cap - pos < n) ? cap - pos : n;
+    return hipMemcpyAsync((char*)dst + elem * pos, src, elem * m, hipMemcpyDeviceToHost, st);
+  };
   auto finish = [&](uint64_t c) -> hipError_t {
     hipStream_t st = streams[c % S];
     hipError_t err = hipStreamSynchronize(st);
     if (err != hipSuccess) return err;
-    const uint64_t cnt = h_counts[c];
+    const uint64_t cnt = h_counts[2 * c];
     char* stage = stage_of(c);
-    if (offset < h_cap && cnt > 0) {
-      const uint64_t m = (h_cap - offset < cnt) ? h_cap - offset : cnt;
-      err = hipMemcpyAsync(h_idx + offset, stage + L.idx, 8 * m, hipMemcpyDeviceToHost, st);
-      if (err != hipSuccess) return err;
-      err = hipMemcpyAsync(h_val + offset, stage + L.val, 2 * m, hipMemcpyDeviceToHost, st);
-      if (err != hipSuccess) return err;
+    if (!o.leb) {
+      err = copy_out(o.h_idx, stage + L.idx, offset, o.h_idx_cap, cnt, 8, st);
+      if (err == hipSuccess) err = copy_out(o.h_val, stage + L.val, offset, o.h_val_cap, cnt, 2, st);
+    } else {
+      o.h_chunk_counts[c] = cnt;
+      if (cnt > 0) {
+        // the chunk's indices as one segment based at the chunk's first word
+        EncArgs a;
+        memset(&a, 0, sizeof(a));
+        a.idx = (const int64_t*)(stage + L.idx);
+        a.count = cnt;
+        a.segs = {nullptr, nullptr, 0, (int64_t)(c * chunk)};
+        a.out = (uint8_t*)(stage + L.bytes);
+        a.capacity = bytes_cap;
+        a.d_nbytes = (uint64_t*)(stage + L.nbytes);
+        const EncLayout E = enc_layout(cnt);
+        a.tile_bytes = (uint32_t*)(stage + L.enc_ws + E.tile_bytes);
+        err = launch_leb128_encode(a, (uint64_t*)(stage + L.enc_ws + E.group_sum),
+                                   (uint64_t*)(stage + L.enc_ws + E.group_excl), st);
+        if (err == hipSuccess)
+          err = hipMemcpyAsync(&h_counts[2 * c + 1], stage + L.nbytes, 8, hipMemcpyDeviceToHost,
+                               st);
+        if (err == hipSuccess)
+          err = copy_out(o.h_val, stage + L.val, offset, o.h_val_cap, cnt, 2, st);
+        if (err == hipSuccess) err = hipStreamSynchronize(st);
+        if (err != hipSuccess) return err;
+        const uint64_t nb = h_counts[2 * c + 1];
+        err = copy_out(o.h_bytes, stage + L.bytes, boffset, o.h_bytes_cap, nb, 1, st);
+        boffset += nb;
+      }
     }
     offset += cnt;
     finished = c + 1;
-    return hipSuccess;
+    return err;
   };
 
   for (uint64_t c = 0; c < nchunks && e == hipSuccess; ++c) {
@@ -186,7 +265,8 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
       status = st;
       break;
     }
-    e = hipMemcpyAsync(&h_counts[c], stage + L.count, 8, hipMemcpyDeviceToHost, streams[c % S]);
+    e = hipMemcpyAsync(&h_counts[2 * c], stage + L.count, 8, hipMemcpyDeviceToHost,
+                       streams[c % S]);
     if (e == hipSuccess) issued = c + 1;
   }
   while (e == hipSuccess && status == DELTA_OK && finished < issued) e = finish(finished);
@@ -198,17 +278,16 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
   (void)hipHostFree(h_counts);
   if (e != hipSuccess) {
     set_error("HIP error in pipeline: %s", hipGetErrorString(e));
-    *h_count = 0;
     return DELTA_ERR_HIP;
   }
-  if (status != DELTA_OK) {   // a chunk could not be enqueued: no partial result
-    *h_count = 0;
-    return status;
-  }
+  if (status != DELTA_OK) return status;   // a chunk could not be enqueued: no result
   *h_count = offset;
-  if (offset > h_cap) {
-    set_error("output has %llu entries, capacity %llu",
-             (unsigned long long)offset, (unsigned long long)h_cap);
+  if (h_nbytes) *h_nbytes = boffset;
+  const bool fits = offset <= o.h_val_cap && (o.leb ? boffset <= o.h_bytes_cap
+                                                    : offset <= o.h_idx_cap);
+  if (!fits) {
+    set_error("output has %llu entries (%llu index bytes); it does not fit",
+             (unsigned long long)offset, (unsigned long long)boffset);
     status = DELTA_ERR_CAPACITY;
   }
   return status;
@@ -219,6 +298,31 @@ extern "C" delta_status_t delta_extract_pipelined(
     int32_t num_tensors, const delta_pipeline_opts_t* opts, hipStream_t* streams,
     void* d_staging, size_t staging_bytes, int64_t* h_idx, uint16_t* h_val, uint64_t h_capacity,
     uint64_t* h_count) {
+  PipeOut o;
+  memset(&o, 0, sizeof(o));
+  o.h_idx = h_idx;
+  o.h_idx_cap = h_capacity;
+  o.h_val = h_val;
+  o.h_val_cap = h_capacity;
   return pipeline_impl(prev_ptrs, next_ptrs, numels, num_tensors, opts, streams, d_staging,
-                       staging_bytes, h_idx, h_val, h_capacity, h_count);
+                       staging_bytes, o, h_count, nullptr);
+}
+
+extern "C" delta_status_t delta_extract_pipelined_leb128(
+    const uint16_t* const* prev_ptrs, const uint16_t* const* next_ptrs, const uint64_t* numels,
+    int32_t num_tensors, const delta_pipeline_opts_t* opts, hipStream_t* streams,
+    void* d_staging, size_t staging_bytes, uint8_t* h_bytes, uint64_t h_bytes_capacity,
+    uint16_t* h_val, uint64_t h_val_capacity, uint64_t* h_chunk_counts, uint64_t h_num_chunks,
+    uint64_t* h_count, uint64_t* h_nbytes) {
+  PipeOut o;
+  memset(&o, 0, sizeof(o));
+  o.leb = true;
+  o.h_bytes = h_bytes;
+  o.h_bytes_cap = h_bytes_capacity;
+  o.h_val = h_val;
+  o.h_val_cap = h_val_capacity;
+  o.h_chunk_counts = h_chunk_counts;
+  o.h_num_chunks = h_num_chunks;
+  return pipeline_impl(prev_ptrs, next_ptrs, numels, num_tensors, opts, streams, d_staging,
+                       staging_bytes, o, h_count, h_nbytes);
 }

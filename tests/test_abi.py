@@ -185,3 +185,28 @@ def test_leb128_sizes_and_validation(lib):
         _abi.DELTA_ERR_INVALID_ARG
     assert D(FAKE, 100, None, None, 0, FAKE, 100, nb, None, ws, 8, None) == \
         _abi.DELTA_ERR_WORKSPACE
+
+
+def test_pipeline_leb128_validation(lib):
+    P = ctypes.c_void_p
+    prevs = (P * 1)(FAKE)
+    numels = (ctypes.c_uint64 * 1)(100)
+    streams = (P * 4)(None, None, None, None)
+    cnt = ctypes.c_uint64(0)
+    nb = ctypes.c_uint64(0)
+    counts = (ctypes.c_uint64 * 4)()
+    opts = _abi.delta_pipeline_opts_t(30, 4, 0)   # 4 chunks of 30 words
+    plain = lib.delta_pipeline_staging_bytes(numels, 1, ctypes.byref(opts))
+    coded = lib.delta_pipeline_leb128_staging_bytes(numels, 1, ctypes.byref(opts))
+    assert coded > plain > 0
+    F = lib.delta_extract_pipelined_leb128
+    # too few chunk-count slots
+    assert F(prevs, prevs, numels, 1, ctypes.byref(opts), streams, FAKE, coded, FAKE, 100, FAKE,
+             100, counts, 3, ctypes.byref(cnt), ctypes.byref(nb)) == _abi.DELTA_ERR_INVALID_ARG
+    assert b"chunks" in lib.delta_last_error()
+    # no byte total
+    assert F(prevs, prevs, numels, 1, ctypes.byref(opts), streams, FAKE, coded, FAKE, 100, FAKE,
+             100, counts, 4, ctypes.byref(cnt), None) == _abi.DELTA_ERR_INVALID_ARG
+    # staging of the plain pipeline is not enough
+    assert F(prevs, prevs, numels, 1, ctypes.byref(opts), streams, FAKE, plain, FAKE, 100, FAKE,
+             100, counts, 4, ctypes.byref(cnt), ctypes.byref(nb)) == _abi.DELTA_ERR_WORKSPACE

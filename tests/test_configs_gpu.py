@@ -82,6 +82,25 @@ def round_trip(ws, idx, val, label):
     say(label, "apply round trip ok")
 
 
+def leb128_full(ws, idx, offs, label):
+    """Gap + LEB128 code of the whole set's indices with one segment per
+    tensor: decodes to the indices; sampled tensors' segments equal the
+    oracle's bytes for that tensor's local indices."""
+    bases = np.concatenate([[0], np.cumsum(ws.numels)[:-1]]).astype(np.int64)
+    offs_h = offs.cpu().numpy()
+    buf, seg_bytes = ad.delta_leb128_encode(idx, offs_h, bases)
+    back = ad.delta_leb128_decode(buf, offs_h, bases)
+    assert torch.equal(back, idx), label
+    sb = seg_bytes.cpu().numpy()
+    assert sb[0] == 0 and sb[-1] == buf.numel() and np.all(np.diff(sb) >= 0)
+    for t in sample_tensors(ws.names, ws.shapes):
+        a, b = int(offs_h[t]), int(offs_h[t + 1])
+        ref, n = oracle.leb128_encode(idx[a:b].cpu().numpy() - bases[t])
+        assert n == sb[t + 1] - sb[t], (label, t)
+        np.testing.assert_array_equal(buf[sb[t]:sb[t + 1]].cpu().numpy(), ref)
+    say(label, "leb128 ok:", buf.numel(), "bytes for", idx.numel(), "indices")
+
+
 @pytest.mark.parametrize("model,density", [("qwen3-4b", 0.01), ("qwen3-8b", 0.001),
                                            ("qwen3-8b", 0.01), ("qwen3-8b", 0.1)])
 def test_weight_set(model, density):
@@ -93,6 +112,7 @@ def test_weight_set(model, density):
     torch.cuda.synchronize()
     check_set(ws, idx, val, offs, label)
     round_trip(ws, idx, val, label)
+    leb128_full(ws, idx, offs, label)
 
 
 def test_qwen3_8b_clustered():
@@ -109,6 +129,7 @@ def test_qwen3_8b_clustered():
     tile_hist = torch.bincount(idx // 8192)
     assert int(tile_hist.max()) > 5 * 82
     round_trip(ws, idx, val, "qwen3-8b clustered")
+    leb128_full(ws, idx, offs, "qwen3-8b clustered")
 
 
 def test_qwen3_14b_pipeline():
@@ -127,3 +148,14 @@ def test_qwen3_14b_pipeline():
     assert torch.equal(h_idx, idx.cpu())
     assert torch.equal(h_val.view(torch.int16), val.view(torch.int16).cpu())
     check_set(ws, idx, val, offs, "qwen3-14b")
+
+    del h_idx
+    # the coded pipeline: values identical, indices decode to the same stream
+    hb = torch.empty(3 * cap, dtype=torch.uint8, pin_memory=True)
+    hb, hv, counts, used = ad.delta_extract_pipelined_leb128(
+        ws.prev, ws.new, chunk_elems=1 << 27, num_streams=4, h_bytes=hb, h_val=h_val)
+    say("coded pipeline done", hb.numel(), "bytes")
+    assert torch.equal(hv.view(torch.int16), val.view(torch.int16).cpu())
+    o, b = ad.chunk_segments(counts, used)
+    back = ad.delta_leb128_decode(hb.to(DEV), o, b)
+    assert torch.equal(back, idx)

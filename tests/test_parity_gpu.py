@@ -321,6 +321,49 @@ def test_pipeline_equals_multi(chunk, streams):
     np.testing.assert_array_equal(h_val.view(torch.int16).numpy().view(np.uint16), ref_val)
 
 
+def oracle_chunk_stream(ref_idx, chunk, total):
+    """Oracle bytes of the coded pipeline: chunk c's indices minus c * chunk,
+    gap + LEB128 coded alone, concatenated; and the per-chunk counts."""
+    nchunks = -(-total // chunk)
+    edges = np.searchsorted(ref_idx, np.arange(nchunks + 1, dtype=np.int64) * chunk)
+    parts = [oracle.leb128_encode(ref_idx[edges[c]:edges[c + 1]] - c * chunk)[0]
+             for c in range(nchunks)]
+    return (np.concatenate(parts) if parts else np.zeros(0, np.uint8)), np.diff(edges)
+
+
+@pytest.mark.parametrize("chunk,streams", [(10_007, 4), (TILE, 3), (1 << 20, 4), (1 << 27, 2),
+                                           (777, 1)])
+def test_pipeline_leb128_matches_oracle(chunk, streams):
+    sizes = [0, 128, 4096 * 3, 1, 7, 2 * TILE + 5, 5000, 0, 100_000, 33_333]
+    prevs, news = make_list(sizes, 0.02, seed=501)
+    ref_idx, ref_val, _, ref_cnt = oracle.extract_multi(
+        [host_u16(p) for p in prevs], [host_u16(q) for q in news])
+    hb, hv, counts, used = ad.delta_extract_pipelined_leb128(prevs, news, chunk_elems=chunk,
+                                                            num_streams=streams)
+    assert hb.is_pinned() and hv.is_pinned()
+    ref_bytes, ref_counts = oracle_chunk_stream(ref_idx, used, sum(sizes))
+    np.testing.assert_array_equal(np.array(counts), ref_counts)
+    np.testing.assert_array_equal(hb.numpy(), ref_bytes)
+    np.testing.assert_array_equal(hv.view(torch.int16).numpy().view(np.uint16), ref_val)
+    # the receiver's side: decode on the GPU with one segment per chunk
+    offs, bases = ad.chunk_segments(counts, used)
+    back = ad.delta_leb128_decode(hb.to(DEV), offs, bases)
+    np.testing.assert_array_equal(back.cpu().numpy(), ref_idx)
+
+
+def test_pipeline_leb128_capacity_retry():
+    prevs, news = make_list([40_000, 20_000], 0.05, seed=19)
+    hb = torch.empty(5, dtype=torch.uint8, pin_memory=True)
+    hv = torch.empty(10, dtype=torch.bfloat16, pin_memory=True)
+    b, v, counts, used = ad.delta_extract_pipelined_leb128(prevs, news, chunk_elems=5000,
+                                                          num_streams=4, h_bytes=hb, h_val=hv)
+    ref_idx, ref_val, _, _ = oracle.extract_multi([host_u16(p) for p in prevs],
+                                                  [host_u16(q) for q in news])
+    ref_bytes, _ = oracle_chunk_stream(ref_idx, used, 60_000)
+    np.testing.assert_array_equal(b.numpy(), ref_bytes)
+    np.testing.assert_array_equal(v.view(torch.int16).numpy().view(np.uint16), ref_val)
+
+
 def test_pipeline_capacity_retry():
     prevs, news = make_list([40_000, 20_000], 0.05, seed=9)
     h_idx = torch.empty(10, dtype=torch.int64, pin_memory=True)
