@@ -53,7 +53,7 @@ def parse():
     ap.add_argument("--no-pipeline", action="store_true",
                     help="skip the chunked extract -> pinned host pipeline measurement "
                          "(Qwen3-14B-shaped set)")
-    ap.add_argument("--pipeline-reps", type=int, default=3)
+    ap.add_argument("--pipeline-reps", type=int, default=5)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after timing, copy BYTES device-to-device three times (a known "
                          "traffic reference for hardware counters)")

@@ -204,7 +204,8 @@ delta_status_t delta_apply_checked(uint16_t* weights, uint64_t numel, delta_inde
 size_t delta_leb128_encode_workspace_bytes(uint64_t count);
 
 /* Workspace bytes for delta_leb128_decode of `nbytes` bytes into at most
- * `capacity` entries with `num_segs` segments. */
+ * `capacity` entries with `num_segs` segments (the size currently depends
+ * on nbytes alone). */
 size_t delta_leb128_decode_workspace_bytes(uint64_t nbytes, uint64_t capacity, uint32_t num_segs);
 
 /*
@@ -258,7 +259,9 @@ size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
  * chunk by chunk, with each chunk's (idx, val) copied into pinned host
  * memory as soon as that chunk is done, while later chunks are extracted
  * on the other streams.  The host output equals delta_extract_multi's.
- *   streams       host array of opts->num_streams HIP streams.
+ *   streams       host array of opts->num_streams HIP streams; chunks are
+ *                 extracted round-robin on them.  The copies to the host
+ *                 run on one stream that the call creates and destroys.
  *   d_staging     device scratch of delta_pipeline_staging_bytes(...).
  *   h_idx, h_val  pinned host arrays (hipHostMalloc / pin_memory) of
  *                 h_capacity entries.

@@ -11,6 +11,7 @@
 
 #include "aurora_delta.h"
 #include "delta_internal.h"
+#include "leb128.h"
 
 using namespace aurora;
 
@@ -316,7 +317,9 @@ delta_status_t delta_apply_multi(uint16_t* const* weight_ptrs, const uint64_t* n
 size_t delta_leb128_encode_workspace_bytes(uint64_t count) { return enc_layout(count).total; }
 
 size_t delta_leb128_decode_workspace_bytes(uint64_t nbytes, uint64_t capacity, uint32_t num_segs) {
-  return dec_layout(nbytes, capacity, num_segs).total;
+  (void)capacity;
+  (void)num_segs;
+  return dec_layout(nbytes).total;
 }
 
 delta_status_t delta_leb128_encode(const int64_t* idx, uint64_t count,
@@ -366,8 +369,8 @@ delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
   if ((uintptr_t)out_idx % 8) return fail(DELTA_ERR_INVALID_ARG, "out_idx not 8-byte aligned");
   if (num_segs > 0 && (!d_seg_offsets || !d_seg_bases))
     return fail(DELTA_ERR_INVALID_ARG, "segment arrays are NULL");
-  const DecLayout L = dec_layout(nbytes, capacity, num_segs);
-  if (L.btiles > 0xFFFFFFFFull / 256 || L.etiles > 0xFFFFFFFFull / 256)
+  const DecLayout L = dec_layout(nbytes);
+  if (L.btiles > 0xFFFFFFFFull / 256)
     return fail(DELTA_ERR_INVALID_ARG, "stream too long");
   delta_status_t st = check_workspace(workspace, workspace_bytes, L.total);
   if (st != DELTA_OK) return st;
@@ -381,7 +384,6 @@ delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
   a.capacity = capacity;
   a.d_count = d_count;
   a.err = d_error_flag;
-  a.tile_terms = (uint32_t*)(ws + L.tile_terms);
   hipError_t e = launch_leb128_decode(a, L, ws, stream);
   if (e != hipSuccess) return hip_fail(e, "leb128 decode launch");
   return ok();

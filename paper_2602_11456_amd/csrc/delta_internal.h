@@ -192,61 +192,6 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
                                uint64_t* d_count, uint64_t* d_offsets, void* workspace,
                                size_t workspace_bytes, hipStream_t stream);
 
-// ------------------------------------------------------ LEB128 (leb128.hip)
-
-// Segments of an index stream: entries [offs[s], offs[s + 1]) form segment
-// s (offs has num + 1 entries, device memory); its first entry is coded
-// relative to bases[s].  num == 0: one segment based at base0.
-struct LebSegs {
-  const uint64_t* offs;
-  const uint64_t* bases;
-  uint32_t num;
-  int64_t base0;
-};
-
-struct EncArgs {
-  const int64_t* idx;
-  uint64_t count;
-  LebSegs segs;
-  uint8_t* out;
-  uint64_t capacity;
-  uint64_t* d_nbytes;
-  uint64_t* seg_byte_offsets;   // nullable, num + 1 entries
-  uint32_t* err;                // nullable
-  uint32_t* tile_bytes;
-  uint64_t* group_excl;
-};
-
-struct DecArgs {
-  const uint8_t* in;
-  uint64_t nbytes;
-  LebSegs segs;
-  int64_t* out;
-  uint64_t capacity;
-  uint64_t* d_count;
-  uint32_t* err;                // nullable
-  uint32_t* tile_terms;
-  uint64_t* group_excl;
-  uint64_t* sum_tile;
-  uint64_t* sum_group_excl;
-  int64_t* corr;
-};
-
-struct EncLayout {
-  uint64_t tiles;
-  size_t tile_bytes, group_sum, group_excl, total;
-};
-struct DecLayout {
-  uint64_t btiles, etiles;
-  size_t tile_terms, group_sum, group_excl, sum_tile, sum_group_sum, sum_group_excl, sum_total,
-      corr, total;
-};
-EncLayout enc_layout(uint64_t count);
-DecLayout dec_layout(uint64_t nbytes, uint64_t capacity, uint32_t num_segs);
-hipError_t launch_leb128_encode(EncArgs a, uint64_t* group_sum, uint64_t* group_excl,
-                                hipStream_t stream);
-hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStream_t stream);
-
 // Thread-local detail text behind delta_last_error() (abi.hip).
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 void clear_error();

@@ -1,0 +1,64 @@
+// Internal declarations of the gap + LEB128 index coder (leb128.hip), used
+// by the C ABI and the chunked pipeline.  Not part of the public ABI.
+#pragma once
+
+#include "delta_internal.h"
+
+namespace aurora {
+
+// Segments of an index stream: entries [offs[s], offs[s + 1]) form segment
+// s (offs has num + 1 entries, device memory); its first entry is coded
+// relative to bases[s].  num == 0: one segment based at base0.
+struct LebSegs {
+  const uint64_t* offs;
+  const uint64_t* bases;
+  uint32_t num;
+  int64_t base0;
+};
+
+struct EncArgs {
+  const int64_t* idx;
+  uint64_t count;               // entries, or the most there can be if d_count_in is set
+  const uint64_t* d_count_in;   // nullable: the entry count, in device memory
+  LebSegs segs;
+  uint8_t* out;
+  uint64_t capacity;
+  uint64_t* d_nbytes;
+  uint64_t* seg_byte_offsets;   // nullable, num + 1 entries
+  uint32_t* err;                // nullable
+  uint32_t* tile_bytes;
+  uint64_t* group_excl;
+};
+
+struct DecArgs {
+  const uint8_t* in;
+  uint64_t nbytes;
+  LebSegs segs;
+  int64_t* out;
+  uint64_t capacity;
+  uint64_t* d_count;
+  uint32_t* err;                // nullable
+  uint32_t* tile_terms;         // numbers ending in each byte tile
+  uint64_t* group_excl;         // entries before each group of tiles
+  uint32_t* tile_f;             // byte tile holds a segment start
+  uint64_t* tile_v;             // segmented sum of the tile's terms
+  uint64_t* gexcl_v;            // index just before each group of tiles
+};
+
+struct EncLayout {
+  uint64_t tiles;
+  size_t tile_bytes, group_sum, group_excl, total;
+};
+// Encoder grid for up to `count` entries.
+uint32_t enc_grid(uint64_t count, bool count_on_device);
+struct DecLayout {
+  uint64_t btiles;
+  size_t tile_terms, group_sum, group_excl, tile_f, tile_v, gsum_f, gsum_v, gexcl_v, total;
+};
+EncLayout enc_layout(uint64_t count);
+DecLayout dec_layout(uint64_t nbytes);
+hipError_t launch_leb128_encode(EncArgs a, uint64_t* group_sum, uint64_t* group_excl,
+                                hipStream_t stream);
+hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStream_t stream);
+
+}  // namespace aurora

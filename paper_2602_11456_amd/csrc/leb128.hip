@@ -9,30 +9,82 @@
 // every tensor has its own index array): the first entry of segment s is
 // stored as idx - base[s], i.e. as the tensor-local index.
 //
-// Encode: per tile of 4096 entries the LEB128 byte count is summed
-// (enc_count), the tile counts are scanned in groups (the same group scan
-// as extract), and enc_write writes each entry's bytes at its offset.
-// Decode: per tile of 16 KiB the terminating bytes (high bit clear) are
-// counted (dec_count), scanned, and dec_gap turns every terminating byte
-// into its entry's gap; a prefix sum with per-segment restarts
-// (gap_sum, group scan, prefix, seg_corr, seg_add) gives the indices.
+// Encode, per tile of 4096 entries (one workgroup, each wavefront 1024
+// consecutive entries, 64 per step, so every load is coalesced):
+// enc_count sums the tile's code lengths, the tile sums are scanned in
+// groups (the same group scan as extract), and enc_write writes each
+// entry's bytes at its offset (wavefront scan of the lengths per step).
+//
+// Decode, per tile of 16 KiB of bytes: dec_count counts the terminating
+// bytes (high bit clear; 4 bytes per 32-bit test); their scan numbers the
+// entries.  dec_fold decodes every number (a terminating byte and the
+// continuation bytes before it, at most 10) and folds the tile into a
+// segmented sum: an entry that opens a segment contributes base + term and
+// restarts the sum, any other adds its gap.  Those tile folds are scanned
+// (segmented), and dec_write decodes again and writes every index as the
+// segmented running sum.
 #include "delta_internal.h"
+#include "leb128.h"
 
 namespace aurora {
 
 constexpr int kLebThreads = 256;
-constexpr int kEncPer = 16;                       // entries per thread
-constexpr int kEncTile = kLebThreads * kEncPer;   // 4096 entries
-constexpr int kDecPer = 64;                       // bytes per thread
-constexpr int kDecTile = kLebThreads * kDecPer;   // 16 KiB
-constexpr int kDecBack = 16;                      // bytes read before a tile (a number has <= 10)
+constexpr int kLebWaves = kLebThreads / 64;
+constexpr int kEncSteps = 16;                    // 64-entry steps per wavefront
+constexpr int kEncWave = 64 * kEncSteps;         // 1024 entries
+constexpr int kEncTile = kLebWaves * kEncWave;   // 4096 entries
+constexpr int kDecWave = 4096;                   // bytes per wavefront
+constexpr int kDecTile = kLebWaves * kDecWave;   // 16 KiB
+constexpr int kDecBack = 16;                     // bytes kept before a tile (>= 9)
+constexpr int kSegLds = 256;                     // segment starts cached per tile
 
-__device__ __forceinline__ uint32_t lane_of() { return threadIdx.x & 63; }
+__device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ uint32_t wave_id() { return threadIdx.x >> 6; }
 
 __device__ __forceinline__ uint32_t leb_len(uint64_t v) {
   const uint32_t bits = 64 - __builtin_clzll(v | 1ull);
   return (bits + 6) / 7;
 }
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) v += __shfl_xor(v, s);
+  return v;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan(T v) {
+  const uint32_t lane = lane_id();
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) {
+    const T y = __shfl_up(v, s);
+    if ((int)lane >= s) v += y;
+  }
+  return v;
+}
+
+// Segmented inclusive scan over the wavefront: a lane with f set restarts
+// the running sum at its own v.
+__device__ __forceinline__ void wave_seg_scan(uint32_t& f, uint64_t& v) {
+  const uint32_t lane = lane_id();
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) {
+    const uint64_t vp = __shfl_up(v, s);
+    const uint32_t fp = __shfl_up(f, s);
+    if ((int)lane >= s) {
+      if (!f) v += vp;
+      f |= fp;
+    }
+  }
+}
+
+// ------------------------------------------------------------- segments
 
 // Segment of entry k: the last s < num with offs[s] <= k (num == 0: one
 // segment, based at base0).
@@ -45,164 +97,255 @@ __device__ __forceinline__ uint32_t seg_of(const LebSegs& g, uint64_t k) {
   }
   return lo;
 }
-__device__ __forceinline__ uint64_t seg_lo(const LebSegs& g, uint32_t s) {
-  return g.num ? g.offs[s] : 0;
-}
-__device__ __forceinline__ uint64_t seg_hi(const LebSegs& g, uint32_t s) {
-  return (g.num && s + 1 < g.num) ? g.offs[s + 1] : ~0ull;
-}
 __device__ __forceinline__ int64_t seg_base(const LebSegs& g, uint32_t s) {
   return g.num ? (int64_t)g.bases[s] : g.base0;
 }
 
-// Exclusive prefix of v over the workgroup (kLebThreads threads) and the
-// total.  Contains barriers; s_wave has kLebThreads / 64 entries.
-template <typename T>
-__device__ __forceinline__ T block_excl_scan(T v, T* s_wave, T& total) {
-  const uint32_t lane = lane_of(), wave = threadIdx.x >> 6;
-  T x = v;
-#pragma unroll
-  for (int s = 1; s < 64; s <<= 1) {
-    const T y = __shfl_up(x, s);
-    if ((int)lane >= s) x += y;
-  }
-  if (lane == 63) s_wave[wave] = x;
-  __syncthreads();
-  T before = 0, all = 0;
-#pragma unroll
-  for (int w = 0; w < kLebThreads / 64; ++w) {
-    const T t = s_wave[w];
-    before += (w < (int)wave) ? t : (T)0;
-    all += t;
+// The segments that a tile's entries [e0, e1) fall in: first..last, with
+// their starts cached in LDS when there are few.
+struct TileSegs {
+  uint32_t first, last;
+  bool cached;
+};
+
+// Block-wide: contains barriers when there are segments.  e0 < e1.
+__device__ __forceinline__ TileSegs tile_segs(const LebSegs& g, uint64_t e0, uint64_t e1,
+                                              uint64_t* s_lo, uint32_t* s_meta) {
+  TileSegs c{0, 0, false};
+  if (g.num == 0) return c;
+  if (threadIdx.x == 0) {
+    s_meta[0] = seg_of(g, e0);
+    s_meta[1] = seg_of(g, e1 - 1);
   }
   __syncthreads();
-  total = all;
-  return before + x - v;
+  c.first = s_meta[0];
+  c.last = s_meta[1];
+  const uint32_t n = c.last - c.first + 1;
+  if (n <= (uint32_t)kSegLds) {
+    for (uint32_t j = threadIdx.x; j < n; j += kLebThreads) s_lo[j] = g.offs[c.first + j];
+    c.cached = true;
+  }
+  __syncthreads();
+  return c;
 }
 
-// Sum of counts[g * kTilesPerGroup .. tile) (tiles before `tile` in its
-// group), by wavefront 0; valid in thread 0... broadcast through LDS.
+// Segment of entry e of the tile, and whether e opens it (entry 0 always
+// opens the first segment).
+__device__ __forceinline__ uint32_t tile_seg(const LebSegs& g, const TileSegs& c,
+                                             const uint64_t* s_lo, uint64_t e, bool& start) {
+  if (g.num == 0) {
+    start = e == 0;
+    return 0;
+  }
+  uint32_t s;
+  uint64_t lo;
+  if (c.first == c.last) {
+    s = c.first;
+    lo = c.cached ? s_lo[0] : g.offs[s];
+  } else if (c.cached) {
+    uint32_t a = 0, b = c.last - c.first + 1;
+    while (b - a > 1) {
+      const uint32_t mid = (a + b) >> 1;
+      if (s_lo[mid] <= e) a = mid; else b = mid;
+    }
+    s = c.first + a;
+    lo = s_lo[a];
+  } else {
+    s = seg_of(g, e);
+    lo = g.offs[s];
+  }
+  start = e == 0 || e == lo;
+  return s;
+}
+
+// Sum of counts[g * kTilesPerGroup .. tile) by wavefront 0, returned to
+// every thread through LDS (contains a barrier).
 template <typename T>
 __device__ __forceinline__ uint64_t group_before(const T* counts, uint64_t tile, uint64_t* s_out) {
   if (threadIdx.x < 64) {
-    const uint64_t g0 = tile / kTilesPerGroup * kTilesPerGroup;
-    const uint64_t t = g0 + threadIdx.x;
-    uint64_t c = t < tile ? (uint64_t)counts[t] : 0;
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) c += __shfl_xor(c, s);
-    if (threadIdx.x == 0) *s_out = c;
+    const uint64_t t = tile / kTilesPerGroup * kTilesPerGroup + threadIdx.x;
+    uint64_t v = t < tile ? (uint64_t)counts[t] : 0;
+    v = wave_sum(v);
+    if (threadIdx.x == 0) *s_out = v;
   }
   __syncthreads();
   return *s_out;
 }
 
+__device__ __forceinline__ void raise_flag(uint32_t* err) {
+  if (err) __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---------------------------------------------------------------- encode
 
-// Gaps of the thread's kEncPer consecutive entries; returns their LEB128
-// byte count.  s_idx holds the tile's entries with the entry before the
-// tile at s_idx[0].
-__device__ __forceinline__ uint32_t enc_gaps(const EncArgs& a, uint64_t t0, const int64_t* s_idx,
-                                             uint64_t (&gap)[kEncPer], bool& bad) {
-  const uint64_t k0 = t0 + (uint64_t)threadIdx.x * kEncPer;
-  uint32_t bytes = 0;
-  if (k0 >= a.count) {
+constexpr int kEncLds = 16384;   // a tile's code is assembled in LDS up to this size
+
+__device__ __forceinline__ uint64_t enc_count_of(const EncArgs& a) {
+  if (!a.d_count_in) return a.count;
+  const uint64_t c = *a.d_count_in;
+  return c < a.count ? c : a.count;
+}
+
+// Gaps of this lane's entries kw + 64 it (it < kEncSteps) below t1: idx -
+// base for an entry that opens its segment, else idx - previous idx (the
+// previous index comes from the neighbouring lane).  Sets bit it of
+// `starts` for an entry that opens a segment, `bad` for a gap below 0 / 1;
+// returns the lane's code bytes.
+__device__ __forceinline__ uint32_t enc_gaps(const EncArgs& a, const TileSegs& c,
+                                             const uint64_t* s_lo, uint64_t kw, uint64_t t1,
+                                             uint64_t (&gap)[kEncSteps], uint32_t& starts,
+                                             bool& bad) {
+  const uint32_t lane = lane_id();
+  int64_t cur[kEncSteps];
 #pragma unroll
-    for (int j = 0; j < kEncPer; ++j) gap[j] = 0;
-    return 0;
+  for (int it = 0; it < kEncSteps; ++it) {
+    const uint64_t k = kw + 64 * it;
+    cur[it] = k < t1 ? a.idx[k] : 0;
   }
-  uint32_t sg = seg_of(a.segs, k0);
-  uint64_t hi = seg_hi(a.segs, sg);
+  const uint64_t first = kw - lane;   // the wavefront's first entry
+  int64_t last = (first > 0 && first < t1) ? a.idx[first - 1] : 0;
+  uint32_t bytes = 0;
+  starts = 0;
 #pragma unroll
-  for (int j = 0; j < kEncPer; ++j) {
-    const uint64_t k = k0 + j;
-    gap[j] = 0;
-    if (k >= a.count) continue;
-    while (k >= hi) {   // next segment (skips empty ones)
-      ++sg;
-      hi = seg_hi(a.segs, sg);
+  for (int it = 0; it < kEncSteps; ++it) {
+    const uint64_t k = kw + 64 * it;
+    int64_t prev = __shfl_up(cur[it], 1);
+    if (lane == 0) prev = last;
+    last = __shfl(cur[it], 63);
+    gap[it] = 0;
+    if (k < t1) {
+      bool start;
+      const uint32_t seg = tile_seg(a.segs, c, s_lo, k, start);
+      int64_t d;
+      if (start) {
+        d = cur[it] - seg_base(a.segs, seg);
+        bad |= d < 0;
+      } else {
+        d = cur[it] - prev;
+        bad |= d < 1;
+      }
+      gap[it] = d < 0 ? 0 : (uint64_t)d;
+      starts |= (uint32_t)start << it;
+      bytes += leb_len(gap[it]);
     }
-    const int64_t cur = s_idx[k - t0 + 1];
-    int64_t d;
-    if (k == seg_lo(a.segs, sg)) {
-      d = cur - seg_base(a.segs, sg);
-      bad |= d < 0;
-    } else {
-      d = cur - s_idx[k - t0];
-      bad |= d < 1;
-    }
-    gap[j] = d < 0 ? 0 : (uint64_t)d;
-    bytes += leb_len(gap[j]);
   }
   return bytes;
 }
 
-__device__ __forceinline__ void enc_load_tile(const EncArgs& a, uint64_t t0, int64_t* s_idx) {
-  for (uint32_t i = threadIdx.x; i < kEncTile + 1; i += kLebThreads) {
-    // s_idx[i] = idx[t0 + i - 1]
-    int64_t v = 0;
-    if (i > 0 || t0 > 0) {
-      const uint64_t k = t0 + i - 1;
-      if (k < a.count) v = a.idx[k];
+// Tiles loop grid-stride (the entry count may only be known on the device).
+__global__ __launch_bounds__(kLebThreads) void enc_count_kernel(EncArgs a) {
+  __shared__ uint64_t s_lo[kSegLds];
+  __shared__ uint32_t s_meta[2];
+  __shared__ uint32_t s_wave[kLebWaves];
+  const uint64_t count = enc_count_of(a);
+  const uint64_t tiles = (count + kEncTile - 1) / kEncTile;
+  bool bad = false;
+  for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const uint64_t t0 = tile * kEncTile;
+    const uint64_t t1 = t0 + kEncTile < count ? t0 + kEncTile : count;
+    const TileSegs c = tile_segs(a.segs, t0, t1, s_lo, s_meta);
+    uint64_t gap[kEncSteps];
+    uint32_t starts;
+    uint32_t bytes = enc_gaps(a, c, s_lo, t0 + (uint64_t)wave_id() * kEncWave + lane_id(), t1, gap,
+                              starts, bad);
+    bytes = wave_sum(bytes);
+    if (lane_id() == 0) s_wave[wave_id()] = bytes;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t t = 0;
+      for (int w = 0; w < kLebWaves; ++w) t += s_wave[w];
+      a.tile_bytes[tile] = t;
     }
-    s_idx[i] = v;
+    __syncthreads();
   }
-  __syncthreads();
+  if (bad) raise_flag(a.err);
 }
 
-__global__ __launch_bounds__(kLebThreads) void enc_count_kernel(EncArgs a) {
-  __shared__ int64_t s_idx[kEncTile + 1];
-  __shared__ uint32_t s_wave[kLebThreads / 64];
-  const uint64_t tile = blockIdx.x;
-  const uint64_t t0 = tile * kEncTile;
-  enc_load_tile(a, t0, s_idx);
-  uint64_t gap[kEncPer];
-  bool bad = false;
-  const uint32_t bytes = enc_gaps(a, t0, s_idx, gap, bad);
-  uint32_t total;
-  block_excl_scan(bytes, s_wave, total);
-  if (threadIdx.x == 0) a.tile_bytes[tile] = total;
-  if (bad && a.err)
-    __hip_atomic_fetch_or(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Sums of the tile byte counts per group of kTilesPerGroup tiles (tiles
+// past the entry count add nothing).
+__global__ __launch_bounds__(64) void enc_group_sum_kernel(EncArgs a, uint64_t* group_sum) {
+  const uint64_t tiles = (enc_count_of(a) + kEncTile - 1) / kEncTile;
+  const uint64_t t = (uint64_t)blockIdx.x * kTilesPerGroup + lane_id();
+  const uint64_t v = wave_sum(t < tiles ? (uint64_t)a.tile_bytes[t] : 0ull);
+  if (lane_id() == 0) group_sum[blockIdx.x] = v;
+}
+
+// Stores bytes [0, n) of s_out at out + pos (4-byte stores where the
+// destination is aligned).
+__device__ __forceinline__ void enc_flush(const uint8_t* s_out, uint64_t n, uint8_t* out,
+                                          uint64_t pos) {
+  uint8_t* dst = out + pos;
+  const uint64_t head = (4 - ((uintptr_t)dst & 3u)) & 3u;
+  const uint64_t h = head < n ? head : n;
+  const uint64_t words = (n - h) / 4;
+  for (uint64_t i = threadIdx.x; i < h; i += kLebThreads) dst[i] = s_out[i];
+  uint32_t* dw = (uint32_t*)(dst + h);
+  for (uint64_t w = threadIdx.x; w < words; w += kLebThreads) {
+    const uint64_t j = h + 4 * w;
+    dw[w] = (uint32_t)s_out[j] | ((uint32_t)s_out[j + 1] << 8) | ((uint32_t)s_out[j + 2] << 16) |
+            ((uint32_t)s_out[j + 3] << 24);
+  }
+  for (uint64_t i = h + 4 * words + threadIdx.x; i < n; i += kLebThreads) dst[i] = s_out[i];
 }
 
 __global__ __launch_bounds__(kLebThreads) void enc_write_kernel(EncArgs a) {
-  __shared__ int64_t s_idx[kEncTile + 1];
-  __shared__ uint32_t s_wave[kLebThreads / 64];
+  __shared__ uint64_t s_lo[kSegLds];
+  __shared__ uint32_t s_meta[2];
+  __shared__ uint32_t s_wave[kLebWaves];
   __shared__ uint64_t s_before;
-  const uint64_t tile = blockIdx.x;
-  const uint64_t t0 = tile * kEncTile;
-  enc_load_tile(a, t0, s_idx);
-  uint64_t gap[kEncPer];
-  bool bad = false;
-  const uint32_t bytes = enc_gaps(a, t0, s_idx, gap, bad);
-  uint32_t total;
-  const uint32_t excl = block_excl_scan(bytes, s_wave, total);
-  const uint64_t tile_pos =
-      a.group_excl[tile / kTilesPerGroup] + group_before(a.tile_bytes, tile, &s_before);
-  uint64_t pos = tile_pos + excl;
-  const uint64_t k0 = t0 + (uint64_t)threadIdx.x * kEncPer;
-  uint32_t sg = k0 < a.count ? seg_of(a.segs, k0) : 0;
-  uint64_t hi = seg_hi(a.segs, sg);
+  __shared__ uint8_t s_out[kEncLds];
+  const uint64_t count = enc_count_of(a);
+  const uint64_t tiles = (count + kEncTile - 1) / kEncTile;
+  const uint32_t lane = lane_id(), wave = wave_id();
+  for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const uint64_t t0 = tile * kEncTile;
+    const uint64_t t1 = t0 + kEncTile < count ? t0 + kEncTile : count;
+    const TileSegs c = tile_segs(a.segs, t0, t1, s_lo, s_meta);
+    const uint64_t kw = t0 + (uint64_t)wave * kEncWave + lane;
+    uint64_t gap[kEncSteps];
+    uint32_t starts;
+    bool bad = false;   // reported by enc_count
+    uint32_t bytes = enc_gaps(a, c, s_lo, kw, t1, gap, starts, bad);
+    bytes = wave_sum(bytes);
+    if (lane == 0) s_wave[wave] = bytes;
+    const uint64_t tile_pos = a.group_excl[tile / kTilesPerGroup] +
+                              group_before(a.tile_bytes, tile, &s_before);   // barrier
+    const uint64_t total = a.tile_bytes[tile];
+    const bool staged = total <= (uint64_t)kEncLds;
+    uint64_t pos = 0;   // within the tile
+    for (uint32_t w = 0; w < wave; ++w) pos += s_wave[w];
 #pragma unroll
-  for (int j = 0; j < kEncPer; ++j) {
-    const uint64_t k = k0 + j;
-    if (k >= a.count) break;
-    while (k >= hi) {
-      ++sg;
-      hi = seg_hi(a.segs, sg);
+    for (int it = 0; it < kEncSteps; ++it) {
+      const uint64_t k = kw + 64 * it;
+      const uint32_t len = k < t1 ? leb_len(gap[it]) : 0;
+      const uint32_t incl = wave_incl_scan(len);
+      uint64_t p = pos + incl - len;
+      if (((starts >> it) & 1u) && a.seg_byte_offsets && a.segs.num) {
+        // this entry opens its segment and every empty one just before it
+        bool st;
+        const uint32_t sg = tile_seg(a.segs, c, s_lo, k, st);
+        for (int64_t s = sg; s >= 0 && a.segs.offs[s] == k; --s)
+          a.seg_byte_offsets[s] = tile_pos + p;
+      }
+      uint64_t v = gap[it];
+      for (uint32_t m = 0; m < len; ++m) {
+        uint8_t b = (uint8_t)(v & 0x7F);
+        v >>= 7;
+        if (m + 1 < len) b |= 0x80;
+        if (staged)
+          s_out[p] = b;
+        else if (tile_pos + p < a.capacity)
+          a.out[tile_pos + p] = b;
+        ++p;
+      }
+      pos += __shfl(incl, 63);
     }
-    if (a.seg_byte_offsets && a.segs.num && k == seg_lo(a.segs, sg)) {
-      // this entry opens segment sg and every empty segment just before it
-      for (int64_t s = sg; s >= 0 && a.segs.offs[s] == k; --s) a.seg_byte_offsets[s] = pos;
+    __syncthreads();
+    if (staged) {
+      const uint64_t room = a.capacity > tile_pos ? a.capacity - tile_pos : 0;
+      enc_flush(s_out, total < room ? total : room, a.out, tile_pos);
     }
-    uint64_t v = gap[j];
-    do {
-      uint8_t b = (uint8_t)(v & 0x7F);
-      v >>= 7;
-      if (v) b |= 0x80;
-      if (pos < a.capacity) a.out[pos] = b;
-      ++pos;
-    } while (v);
+    __syncthreads();
   }
 }
 
@@ -210,155 +353,384 @@ __global__ __launch_bounds__(kLebThreads) void enc_write_kernel(EncArgs a) {
 // at the total byte count.
 __global__ void enc_seg_tail_kernel(EncArgs a) {
   const uint64_t total = *a.d_nbytes;
+  const uint64_t count = enc_count_of(a);
   for (uint32_t s = threadIdx.x + blockIdx.x * blockDim.x; s <= a.segs.num;
        s += blockDim.x * gridDim.x) {
-    if (s == a.segs.num || a.segs.offs[s] >= a.count) a.seg_byte_offsets[s] = total;
+    if (s == a.segs.num || a.segs.offs[s] >= count) a.seg_byte_offsets[s] = total;
   }
 }
 
 // ---------------------------------------------------------------- decode
 
-__device__ __forceinline__ void dec_load_tile(const DecArgs& a, uint64_t b0, uint8_t* s_bytes) {
-  // s_bytes[i] = in[b0 - kDecBack + i] for i < kDecBack + kDecTile (0 outside)
-  for (uint32_t i = threadIdx.x; i < kDecBack + kDecTile; i += kLebThreads) {
-    const int64_t p = (int64_t)b0 - kDecBack + (int64_t)i;
-    s_bytes[i] = (p >= 0 && (uint64_t)p < a.nbytes) ? a.in[p] : 0;
+// Terminating bytes (high bit clear) among the 4 bytes of w whose
+// positions p0 .. p0+3 are below n.
+__device__ __forceinline__ uint32_t terms_in_word(uint32_t w, uint64_t p0, uint64_t n) {
+  uint32_t m = ~w & 0x80808080u;
+  if (p0 + 4 > n) m &= p0 >= n ? 0u : (0xFFFFFFFFu >> (8 * (4 - (n - p0))));
+  return __builtin_popcount(m);
+}
+
+typedef uint32_t leb_u32x4 __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(1))) leb_u32x4* leb_gvec_ptr;
+
+// The 16 bytes at p (16-aligned; bytes at or past n read as 0).
+__device__ __forceinline__ uint4 load16(const uint8_t* in, uint64_t p, uint64_t n) {
+  if (p + 16 <= n) {
+    const leb_u32x4 v = __builtin_nontemporal_load((leb_gvec_ptr)(uintptr_t)(in + p));
+    return {v.x, v.y, v.z, v.w};
+  }
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+  for (uint32_t i = 0; i < 16 && p + i < n; ++i) w[i >> 2] |= (uint32_t)in[p + i] << (8 * (i & 3));
+  return {w[0], w[1], w[2], w[3]};
+}
+
+__global__ __launch_bounds__(kLebThreads) void dec_count_kernel(DecArgs a, bool aligned) {
+  __shared__ uint32_t s_wave[kLebWaves];
+  const uint64_t b0 = (uint64_t)blockIdx.x * kDecTile;
+  uint32_t c = 0;
+  if (aligned) {
+#pragma unroll
+    for (int j = 0; j < kDecTile / 16 / kLebThreads; ++j) {
+      const uint64_t p = b0 + 16ull * (j * kLebThreads + threadIdx.x);
+      if (p < a.nbytes) {
+        const uint4 v = load16(a.in, p, a.nbytes);
+        c += terms_in_word(v.x, p, a.nbytes) + terms_in_word(v.y, p + 4, a.nbytes) +
+             terms_in_word(v.z, p + 8, a.nbytes) + terms_in_word(v.w, p + 12, a.nbytes);
+      }
+    }
+  } else {
+    for (uint32_t i = threadIdx.x; i < (uint32_t)kDecTile; i += kLebThreads) {
+      const uint64_t p = b0 + i;
+      if (p < a.nbytes && !(a.in[p] & 0x80)) ++c;
+    }
+  }
+  c = wave_sum(c);
+  if (lane_id() == 0) s_wave[wave_id()] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int w = 0; w < kLebWaves; ++w) t += s_wave[w];
+    a.tile_terms[blockIdx.x] = t;
+  }
+}
+
+// s_bytes[i] = in[b0 - kDecBack + i] (0 outside the stream).  Barrier.
+__device__ __forceinline__ void dec_load_tile(const DecArgs& a, uint64_t b0, bool aligned,
+                                              uint8_t* s_bytes) {
+  if (threadIdx.x < kDecBack) {
+    const int64_t p = (int64_t)b0 - kDecBack + threadIdx.x;
+    s_bytes[threadIdx.x] = p >= 0 ? a.in[p] : 0;
+  }
+  if (aligned) {
+    uint4* s4 = (uint4*)(s_bytes + kDecBack);
+#pragma unroll
+    for (int j = 0; j < kDecTile / 16 / kLebThreads; ++j) {
+      const uint32_t q = j * kLebThreads + threadIdx.x;
+      const uint64_t p = b0 + 16ull * q;
+      s4[q] = p < a.nbytes ? load16(a.in, p, a.nbytes) : uint4{0u, 0u, 0u, 0u};
+    }
+  } else {
+    for (uint32_t i = threadIdx.x; i < (uint32_t)kDecTile; i += kLebThreads) {
+      const uint64_t p = b0 + i;
+      s_bytes[kDecBack + i] = p < a.nbytes ? a.in[p] : 0;
+    }
   }
   __syncthreads();
 }
 
-__global__ __launch_bounds__(kLebThreads) void dec_count_kernel(DecArgs a) {
-  __shared__ uint32_t s_wave[kLebThreads / 64];
-  const uint64_t tile = blockIdx.x;
-  const uint64_t p0 = tile * kDecTile + (uint64_t)threadIdx.x * kDecPer;
-  uint32_t c = 0;
-  for (int i = 0; i < kDecPer; ++i) {
-    const uint64_t p = p0 + i;
-    if (p < a.nbytes && (a.in[p] & 0x80) == 0) ++c;
+// The number whose terminating byte sits at LDS position li (stream
+// position p): its value; `bad` if it is longer than 10 bytes or exceeds
+// 64 bits.
+__device__ __forceinline__ uint64_t dec_number(const uint8_t* s_bytes, uint32_t li, uint64_t p,
+                                               bool& bad) {
+  uint32_t len = 1;
+  while (len <= 10 && p >= len && (s_bytes[li - len] & 0x80)) ++len;
+  if (len > 10) {
+    bad = true;
+    return 0;
   }
-  uint32_t total;
-  block_excl_scan(c, s_wave, total);
-  if (threadIdx.x == 0) a.tile_terms[tile] = total;
+  uint64_t v = 0;
+  for (uint32_t m = 0; m < len; ++m) {
+    const uint64_t payload = s_bytes[li - len + 1 + m] & 0x7F;
+    if (m == 9 && payload > 1) bad = true;
+    v |= payload << (7 * m);
+  }
+  return v;
 }
 
-// Every terminating byte gives one entry's gap: its number runs from the
-// byte after the previous terminating byte up to it.
-__global__ __launch_bounds__(kLebThreads) void dec_gap_kernel(DecArgs a) {
-  __shared__ uint8_t s_bytes[kDecBack + kDecTile];
-  __shared__ uint32_t s_wave[kLebThreads / 64];
-  __shared__ uint64_t s_before;
+// Terminating bytes in this wavefront's 4 KiB of the tile (from LDS).
+__device__ __forceinline__ uint32_t dec_wave_terms(const uint8_t* s_bytes, uint64_t b0,
+                                                   uint64_t n) {
+  const uint32_t* w32 = (const uint32_t*)(s_bytes + kDecBack) + wave_id() * (kDecWave / 4);
+  const uint64_t pw = b0 + (uint64_t)wave_id() * kDecWave;
+  uint32_t c = 0;
+#pragma unroll 4
+  for (int j = 0; j < kDecWave / 4 / 64; ++j) {
+    const uint32_t q = j * 64 + lane_id();
+    c += terms_in_word(w32[q], pw + 4ull * q, n);
+  }
+  return wave_sum(c);
+}
+
+// What one byte contributes: valid = it ends a number; flag = that entry
+// opens a segment, and x = base + term then, else x = the gap.
+struct Term {
+  bool valid, flag;
+  uint64_t x;
+};
+
+__device__ __forceinline__ Term dec_term(const DecArgs& a, const TileSegs& c,
+                                         const uint64_t* s_lo, const uint8_t* s_bytes,
+                                         uint32_t li, uint64_t p, uint64_t e, bool& bad) {
+  Term t{false, false, 0};
+  if (p >= a.nbytes) return t;
+  if (s_bytes[li] & 0x80) {
+    if (p == a.nbytes - 1) bad = true;   // the stream ends inside a number
+    return t;
+  }
+  t.valid = true;
+  t.x = dec_number(s_bytes, li, p, bad);
+  bool start;
+  const uint32_t s = tile_seg(a.segs, c, s_lo, e, start);
+  if (start) {
+    t.flag = true;
+    t.x += (uint64_t)seg_base(a.segs, s);
+  }
+  return t;
+}
+
+// One step of 64 bytes of this wavefront: the byte of this lane, the
+// numbers ending in the step, and their entry ids from e.
+struct Step {
+  uint32_t li;
+  uint64_t p;
+  uint64_t terms;   // ballot of terminating bytes
+};
+
+__device__ __forceinline__ Step dec_step(const DecArgs& a, const uint8_t* s_bytes, uint64_t b0,
+                                         int it) {
+  Step s;
+  s.li = kDecBack + wave_id() * kDecWave + it * 64 + lane_id();
+  s.p = b0 + (s.li - kDecBack);
+  s.terms = __ballot(s.p < a.nbytes && !(s_bytes[s.li] & 0x80));
+  return s;
+}
+
+// Segmented fold of this wavefront's entries (first entry id e): whether
+// one opens a segment, and the sum since the last that does (or of all).
+__device__ __forceinline__ void dec_wave_fold(const DecArgs& a, const TileSegs& c,
+                                              const uint64_t* s_lo, const uint8_t* s_bytes,
+                                              uint64_t b0, uint64_t e, bool& bad, uint32_t& f,
+                                              uint64_t& v) {
+  const uint32_t lane = lane_id();
+  bool any = false;
+  uint64_t acc = 0;   // per lane: its terms since the wavefront's last segment start
+  for (int it = 0; it < kDecWave / 64; ++it) {
+    const Step s = dec_step(a, s_bytes, b0, it);
+    const Term t = dec_term(a, c, s_lo, s_bytes, s.li, s.p, e + lanes_below(s.terms), bad);
+    const uint64_t fm = __ballot(t.flag);
+    const uint64_t x = t.valid ? t.x : 0;
+    if (fm) {   // uniform: restart at the last entry that opens a segment
+      const uint32_t L = 63 - __builtin_clzll(fm);
+      acc = lane >= L ? x : 0;
+      any = true;
+    } else {
+      acc += x;
+    }
+    e += __builtin_popcountll(s.terms);
+  }
+  f = any;
+  v = wave_sum(acc);
+}
+
+// First entry id of this wavefront in the tile whose first is e0.
+__device__ __forceinline__ uint64_t dec_wave_e0(uint64_t e0, const uint32_t* s_wterm) {
+  uint64_t e = e0;
+  for (uint32_t w = 0; w < wave_id(); ++w) e += s_wterm[w];
+  return e;
+}
+
+__global__ __launch_bounds__(kLebThreads) void dec_fold_kernel(DecArgs a, bool aligned) {
+  __shared__ __align__(16) uint8_t s_bytes[kDecBack + kDecTile];
+  __shared__ uint64_t s_lo[kSegLds];
+  __shared__ uint32_t s_meta[2];
+  __shared__ uint32_t s_wterm[kLebWaves];
+  __shared__ uint32_t s_wf[kLebWaves];
+  __shared__ uint64_t s_wv[kLebWaves];
+  __shared__ uint64_t s_tmp;
   const uint64_t tile = blockIdx.x;
   const uint64_t b0 = tile * kDecTile;
-  dec_load_tile(a, b0, s_bytes);
-  const uint32_t q0 = threadIdx.x * kDecPer;   // thread's first byte in the tile
-  uint32_t c = 0;
-  for (int i = 0; i < kDecPer; ++i) {
-    const uint64_t p = b0 + q0 + i;
-    if (p < a.nbytes && (s_bytes[kDecBack + q0 + i] & 0x80) == 0) ++c;
-  }
-  uint32_t total;
-  const uint32_t excl = block_excl_scan(c, s_wave, total);
-  uint64_t e = a.group_excl[tile / kTilesPerGroup] + group_before(a.tile_terms, tile, &s_before) +
-               excl;
+  dec_load_tile(a, b0, aligned, s_bytes);                                    // barrier
+  const uint64_t e0 = a.group_excl[tile / kTilesPerGroup] +
+                      group_before(a.tile_terms, tile, &s_tmp);              // barrier
+  const uint32_t terms = a.tile_terms[tile];
+  const uint32_t wt = dec_wave_terms(s_bytes, b0, a.nbytes);
+  if (lane_id() == 0) s_wterm[wave_id()] = wt;
+  __syncthreads();
   bool bad = false;
-  for (int i = 0; i < kDecPer; ++i) {
-    const uint64_t p = b0 + q0 + i;
-    if (p >= a.nbytes) break;
-    const uint32_t li = kDecBack + q0 + i;
-    if (s_bytes[li] & 0x80) {
-      if (p == a.nbytes - 1) bad = true;   // the stream ends inside a number
-      continue;
+  if (terms == 0) {   // uniform: no number ends in this tile
+    if (threadIdx.x == 0) {
+      a.tile_f[tile] = 0;
+      a.tile_v[tile] = 0;
     }
-    // bytes of this number: li - len + 1 .. li
-    uint32_t len = 1;
-    while (len <= 10 && li >= len && p >= len && (s_bytes[li - len] & 0x80)) ++len;
-    uint64_t v = 0;
-    if (len > 10) {
+    const uint64_t last = a.nbytes - 1;   // the stream must not end inside a number
+    if (threadIdx.x == 0 && last >= b0 && last < b0 + kDecTile &&
+        (s_bytes[kDecBack + (last - b0)] & 0x80))
       bad = true;
-    } else {
-      for (uint32_t m = 0; m < len; ++m) {
-        const uint64_t payload = s_bytes[li - len + 1 + m] & 0x7F;
-        if (m == 9 && payload > 1) bad = true;   // more than 64 bits
-        v |= payload << (7 * m);
+    if (bad) raise_flag(a.err);
+    return;
+  }
+  const TileSegs c = tile_segs(a.segs, e0, e0 + terms, s_lo, s_meta);     // barriers
+  uint32_t f;
+  uint64_t v;
+  dec_wave_fold(a, c, s_lo, s_bytes, b0, dec_wave_e0(e0, s_wterm), bad, f, v);
+  if (lane_id() == 0) {
+    s_wf[wave_id()] = f;
+    s_wv[wave_id()] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t tf = 0;
+    uint64_t tv = 0;
+    for (int w = 0; w < kLebWaves; ++w) {
+      if (s_wf[w]) {
+        tf = 1;
+        tv = s_wv[w];
+      } else {
+        tv += s_wv[w];
       }
     }
-    if (e < a.capacity) a.out[e] = (int64_t)v;
-    ++e;
+    a.tile_f[tile] = tf;
+    a.tile_v[tile] = tv;
   }
-  if (bad && a.err)
-    __hip_atomic_fetch_or(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (bad) raise_flag(a.err);
 }
 
-// Number of decoded entries that are in the output.
-__device__ __forceinline__ uint64_t dec_kept(const DecArgs& a) {
-  const uint64_t n = *a.d_count;
-  return n < a.capacity ? n : a.capacity;
-}
-
-__global__ __launch_bounds__(kLebThreads) void gap_sum_kernel(DecArgs a) {
-  __shared__ uint64_t s_wave[kLebThreads / 64];
-  const uint64_t K = dec_kept(a);
-  const uint64_t k0 = (uint64_t)blockIdx.x * kEncTile + (uint64_t)threadIdx.x * kEncPer;
-  uint64_t sum = 0;
-#pragma unroll
-  for (int j = 0; j < kEncPer; ++j)
-    if (k0 + j < K) sum += (uint64_t)a.out[k0 + j];
-  uint64_t total;
-  block_excl_scan(sum, s_wave, total);
-  if (threadIdx.x == 0) a.sum_tile[blockIdx.x] = total;
-}
-
-// In place: out[k] = gap[0] + ... + gap[k].
-__global__ __launch_bounds__(kLebThreads) void prefix_kernel(DecArgs a) {
-  __shared__ uint64_t s_wave[kLebThreads / 64];
-  __shared__ uint64_t s_before;
-  const uint64_t K = dec_kept(a);
-  const uint64_t tile = blockIdx.x;
-  const uint64_t k0 = tile * kEncTile + (uint64_t)threadIdx.x * kEncPer;
-  uint64_t g[kEncPer];
-  uint64_t sum = 0;
-#pragma unroll
-  for (int j = 0; j < kEncPer; ++j) {
-    g[j] = (k0 + j < K) ? (uint64_t)a.out[k0 + j] : 0;
-    sum += g[j];
+// Segmented fold of tiles [lo, end) (end - lo <= 64) by one wavefront.
+__device__ __forceinline__ void seg_fold_tiles(const uint32_t* f, const uint64_t* v, uint64_t lo,
+                                               uint64_t end, uint32_t& out_f, uint64_t& out_v) {
+  const uint64_t t = lo + lane_id();
+  const bool in = t < end;
+  const uint32_t tf = in ? f[t] : 0;
+  const uint64_t tv = in ? v[t] : 0;
+  const uint64_t fm = __ballot(tf != 0);
+  uint64_t x = tv;
+  if (fm) {
+    const uint32_t L = 63 - __builtin_clzll(fm);
+    x = lane_id() >= L ? tv : 0;
   }
-  uint64_t total;
-  const uint64_t excl = block_excl_scan(sum, s_wave, total);
-  uint64_t run = a.sum_group_excl[tile / kTilesPerGroup] +
-                 group_before(a.sum_tile, tile, &s_before) + excl;
-#pragma unroll
-  for (int j = 0; j < kEncPer; ++j) {
-    run += g[j];
-    if (k0 + j < K) a.out[k0 + j] = (int64_t)run;
+  out_f = fm != 0;
+  out_v = wave_sum(x);
+}
+
+__global__ __launch_bounds__(64) void seg_group_sum_kernel(const uint32_t* tile_f,
+                                                           const uint64_t* tile_v,
+                                                           uint64_t num_tiles, uint32_t* gsum_f,
+                                                           uint64_t* gsum_v) {
+  const uint64_t lo = (uint64_t)blockIdx.x * kTilesPerGroup;
+  const uint64_t end = lo + kTilesPerGroup < num_tiles ? lo + kTilesPerGroup : num_tiles;
+  uint32_t f;
+  uint64_t v;
+  seg_fold_tiles(tile_f, tile_v, lo, end, f, v);
+  if (lane_id() == 0) {
+    gsum_f[blockIdx.x] = f;
+    gsum_v[blockIdx.x] = v;
   }
 }
 
-// corr[s] = base[s] - (prefix just before segment s).
-__global__ void seg_corr_kernel(DecArgs a) {
-  const uint64_t K = dec_kept(a);
-  for (uint32_t s = threadIdx.x + blockIdx.x * blockDim.x; s < a.segs.num;
-       s += blockDim.x * gridDim.x) {
-    const uint64_t o = a.segs.offs[s];
-    const int64_t before = (o > 0 && o - 1 < K) ? a.out[o - 1] : 0;
-    a.corr[s] = (int64_t)a.segs.bases[s] - before;
-  }
-}
-
-__global__ __launch_bounds__(kLebThreads) void seg_add_kernel(DecArgs a) {
-  const uint64_t K = dec_kept(a);
-  const uint64_t k0 = (uint64_t)blockIdx.x * kEncTile + (uint64_t)threadIdx.x * kEncPer;
-  if (k0 >= K) return;
-  uint32_t sg = seg_of(a.segs, k0);
-  uint64_t hi = seg_hi(a.segs, sg);
-#pragma unroll
-  for (int j = 0; j < kEncPer; ++j) {
-    const uint64_t k = k0 + j;
-    if (k >= K) break;
-    while (k >= hi) {
-      ++sg;
-      hi = seg_hi(a.segs, sg);
+// Exclusive segmented scan of the group folds: gexcl_v[g] = the index of
+// the last entry before group g (one workgroup, passes of 1024 groups).
+// Without flags (gsum_f NULL) it is a plain exclusive scan; d_total
+// (nullable) gets the inclusive value at the end.
+constexpr int kSegScanThreads = 1024;
+__global__ __launch_bounds__(kSegScanThreads) void seg_group_scan_kernel(const uint32_t* gsum_f,
+                                                                         const uint64_t* gsum_v,
+                                                                         uint64_t num_groups,
+                                                                         uint64_t* gexcl_v,
+                                                                         uint64_t* d_total) {
+  __shared__ uint32_t s_f[kSegScanThreads / 64];
+  __shared__ uint64_t s_v[kSegScanThreads / 64];
+  __shared__ uint64_t s_carry;
+  const uint32_t lane = lane_id(), wave = threadIdx.x >> 6;
+  if (threadIdx.x == 0) s_carry = 0;
+  __syncthreads();
+  for (uint64_t base = 0; base < num_groups; base += kSegScanThreads) {
+    const uint64_t i = base + threadIdx.x;
+    uint32_t f = (gsum_f && i < num_groups) ? gsum_f[i] : 0;
+    uint64_t v = i < num_groups ? gsum_v[i] : 0;
+    wave_seg_scan(f, v);
+    if (lane == 63) {
+      s_f[wave] = f;
+      s_v[wave] = v;
     }
-    a.out[k] += a.corr[sg];
+    __syncthreads();
+    uint64_t before = s_carry;   // index of the entry before this wavefront's groups
+    for (uint32_t w = 0; w < wave; ++w) before = s_f[w] ? s_v[w] : before + s_v[w];
+    const uint64_t incl = f ? v : before + v;
+    const uint64_t prev = __shfl_up(incl, 1);
+    if (i < num_groups) gexcl_v[i] = lane == 0 ? before : prev;
+    __syncthreads();
+    if (threadIdx.x == kSegScanThreads - 1) s_carry = incl;
+    __syncthreads();
+  }
+  if (d_total && threadIdx.x == 0) *d_total = s_carry;
+}
+
+__global__ __launch_bounds__(kLebThreads) void dec_write_kernel(DecArgs a, bool aligned) {
+  __shared__ __align__(16) uint8_t s_bytes[kDecBack + kDecTile];
+  __shared__ uint64_t s_lo[kSegLds];
+  __shared__ uint32_t s_meta[2];
+  __shared__ uint32_t s_wterm[kLebWaves];
+  __shared__ uint32_t s_wf[kLebWaves];
+  __shared__ uint64_t s_wv[kLebWaves];
+  __shared__ uint64_t s_tmp;
+  __shared__ uint64_t s_carry;
+  const uint64_t tile = blockIdx.x;
+  const uint32_t terms = a.tile_terms[tile];
+  if (terms == 0) return;   // uniform
+  const uint64_t b0 = tile * kDecTile;
+  dec_load_tile(a, b0, aligned, s_bytes);                                    // barrier
+  const uint64_t e0 = a.group_excl[tile / kTilesPerGroup] +
+                      group_before(a.tile_terms, tile, &s_tmp);              // barrier
+  if (e0 >= a.capacity) return;   // uniform: nothing of this tile is kept
+  const uint32_t lane = lane_id(), wave = wave_id();
+  if (threadIdx.x < 64) {   // index of the entry just before the tile
+    const uint64_t g = tile / kTilesPerGroup;
+    uint32_t f;
+    uint64_t v;
+    seg_fold_tiles(a.tile_f, a.tile_v, g * kTilesPerGroup, tile, f, v);
+    if (threadIdx.x == 0) s_carry = f ? v : a.gexcl_v[g] + v;
+  }
+  const uint32_t wt = dec_wave_terms(s_bytes, b0, a.nbytes);
+  if (lane == 0) s_wterm[wave] = wt;
+  __syncthreads();
+  const TileSegs c = tile_segs(a.segs, e0, e0 + terms, s_lo, s_meta);     // barriers
+  const uint64_t ew = dec_wave_e0(e0, s_wterm);
+  bool bad = false;   // reported by dec_fold
+  {
+    uint32_t f;
+    uint64_t v;
+    dec_wave_fold(a, c, s_lo, s_bytes, b0, ew, bad, f, v);
+    if (lane == 0) {
+      s_wf[wave] = f;
+      s_wv[wave] = v;
+    }
+  }
+  __syncthreads();
+  uint64_t run = s_carry;   // index of the entry before this wavefront's first
+  for (uint32_t w = 0; w < wave; ++w) run = s_wf[w] ? s_wv[w] : run + s_wv[w];
+  uint64_t e = ew;
+  for (int it = 0; it < kDecWave / 64; ++it) {
+    const Step s = dec_step(a, s_bytes, b0, it);
+    const uint64_t my_e = e + lanes_below(s.terms);
+    const Term t = dec_term(a, c, s_lo, s_bytes, s.li, s.p, my_e, bad);
+    uint64_t v = t.valid ? t.x : 0;
+    uint32_t f = t.flag;
+    wave_seg_scan(f, v);
+    const uint64_t y = f ? v : run + v;
+    if (t.valid && my_e < a.capacity) a.out[my_e] = (int64_t)y;
+    run = __shfl(y, 63);
+    e += __builtin_popcountll(s.terms);
   }
 }
 
@@ -378,39 +750,53 @@ EncLayout enc_layout(uint64_t count) {
   return L;
 }
 
-DecLayout dec_layout(uint64_t nbytes, uint64_t capacity, uint32_t num_segs) {
+DecLayout dec_layout(uint64_t nbytes) {
   DecLayout L;
-  const uint64_t bt = dec_tiles(nbytes);
-  const uint64_t kmax = nbytes < capacity ? nbytes : capacity;   // an entry takes >= 1 byte
-  const uint64_t et = enc_tiles(kmax);
+  const uint64_t bt = dec_tiles(nbytes), gb = groups_for(bt);
   L.btiles = bt;
-  L.etiles = et;
   L.tile_terms = 0;
   L.group_sum = align_up(4 * bt);
-  L.group_excl = align_up(L.group_sum + 8 * groups_for(bt));
-  L.sum_tile = align_up(L.group_excl + 8 * groups_for(bt));
-  L.sum_group_sum = align_up(L.sum_tile + 8 * et);
-  L.sum_group_excl = align_up(L.sum_group_sum + 8 * groups_for(et));
-  L.sum_total = align_up(L.sum_group_excl + 8 * groups_for(et));
-  L.corr = align_up(L.sum_total + 8);
-  L.total = align_up(L.corr + 8 * (uint64_t)num_segs);
+  L.group_excl = align_up(L.group_sum + 8 * gb);
+  L.tile_f = align_up(L.group_excl + 8 * gb);
+  L.tile_v = align_up(L.tile_f + 4 * bt);
+  L.gsum_f = align_up(L.tile_v + 8 * bt);
+  L.gsum_v = align_up(L.gsum_f + 4 * gb);
+  L.gexcl_v = align_up(L.gsum_v + 8 * gb);
+  L.total = align_up(L.gexcl_v + 8 * gb);
   return L;
+}
+
+uint32_t enc_grid(uint64_t count, bool count_on_device) {
+  const uint64_t tiles = enc_tiles(count);
+  const uint64_t cap = count_on_device ? 2048 : 0xFFFFFFFFull;
+  return (uint32_t)(tiles < cap ? (tiles ? tiles : 1) : cap);
 }
 
 hipError_t launch_leb128_encode(EncArgs a, uint64_t* group_sum, uint64_t* group_excl,
                                 hipStream_t stream) {
-  const uint64_t tiles = enc_tiles(a.count);
+  const uint64_t tiles = enc_tiles(a.count);   // at most
   hipError_t e;
   if (tiles == 0) {
     e = launch_reset(a.d_nbytes, nullptr, 0, stream);
   } else {
-    hipLaunchKernelGGL(enc_count_kernel, dim3((uint32_t)tiles), dim3(kLebThreads), 0, stream, a);
+    const uint32_t grid = enc_grid(a.count, a.d_count_in != nullptr);
+    const uint64_t groups = groups_for(tiles);
+    hipLaunchKernelGGL(enc_count_kernel, dim3(grid), dim3(kLebThreads), 0, stream, a);
     e = hipGetLastError();
-    if (e == hipSuccess)
-      e = launch_group_scan(a.tile_bytes, tiles, group_sum, group_excl, a.d_nbytes, stream);
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(enc_group_sum_kernel, dim3((uint32_t)groups), dim3(64), 0, stream, a,
+                         group_sum);
+      e = hipGetLastError();
+    }
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(seg_group_scan_kernel, dim3(1), dim3(kSegScanThreads), 0, stream,
+                         (const uint32_t*)nullptr, (const uint64_t*)group_sum, groups, group_excl,
+                         a.d_nbytes);
+      e = hipGetLastError();
+    }
     a.group_excl = group_excl;
     if (e == hipSuccess) {
-      hipLaunchKernelGGL(enc_write_kernel, dim3((uint32_t)tiles), dim3(kLebThreads), 0, stream, a);
+      hipLaunchKernelGGL(enc_write_kernel, dim3(grid), dim3(kLebThreads), 0, stream, a);
       e = hipGetLastError();
     }
   }
@@ -422,34 +808,34 @@ hipError_t launch_leb128_encode(EncArgs a, uint64_t* group_sum, uint64_t* group_
   return e;
 }
 
+// The decoder's single segment (num == 0) is based at 0.
 hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStream_t stream) {
   hipError_t e;
   if (L.btiles == 0) return launch_reset(a.d_count, nullptr, 0, stream);
-  uint64_t* gs = (uint64_t*)(ws + L.group_sum);
+  a.segs.base0 = 0;
+  a.tile_terms = (uint32_t*)(ws + L.tile_terms);
   a.group_excl = (uint64_t*)(ws + L.group_excl);
-  a.sum_tile = (uint64_t*)(ws + L.sum_tile);
-  a.sum_group_excl = (uint64_t*)(ws + L.sum_group_excl);
-  a.corr = (int64_t*)(ws + L.corr);
-  hipLaunchKernelGGL(dec_count_kernel, dim3((uint32_t)L.btiles), dim3(kLebThreads), 0, stream, a);
+  a.tile_f = (uint32_t*)(ws + L.tile_f);
+  a.tile_v = (uint64_t*)(ws + L.tile_v);
+  a.gexcl_v = (uint64_t*)(ws + L.gexcl_v);
+  const bool aligned = ((uintptr_t)a.in & 15u) == 0;
+  const dim3 grid((uint32_t)L.btiles), block(kLebThreads);
+  hipLaunchKernelGGL(dec_count_kernel, grid, block, 0, stream, a, aligned);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if ((e = launch_group_scan(a.tile_terms, L.btiles, gs, a.group_excl, a.d_count, stream)) !=
-      hipSuccess)
+  if ((e = launch_group_scan(a.tile_terms, L.btiles, (uint64_t*)(ws + L.group_sum), a.group_excl,
+                             a.d_count, stream)) != hipSuccess)
     return e;
-  hipLaunchKernelGGL(dec_gap_kernel, dim3((uint32_t)L.btiles), dim3(kLebThreads), 0, stream, a);
+  hipLaunchKernelGGL(dec_fold_kernel, grid, block, 0, stream, a, aligned);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (L.etiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(gap_sum_kernel, dim3((uint32_t)L.etiles), dim3(kLebThreads), 0, stream, a);
+  const uint64_t groups = groups_for(L.btiles);
+  hipLaunchKernelGGL(seg_group_sum_kernel, dim3((uint32_t)groups), dim3(64), 0, stream, a.tile_f,
+                     a.tile_v, L.btiles, (uint32_t*)(ws + L.gsum_f), (uint64_t*)(ws + L.gsum_v));
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if ((e = launch_group_scan(a.sum_tile, L.etiles, (uint64_t*)(ws + L.sum_group_sum),
-                             a.sum_group_excl, (uint64_t*)(ws + L.sum_total), stream)) !=
-      hipSuccess)
-    return e;
-  hipLaunchKernelGGL(prefix_kernel, dim3((uint32_t)L.etiles), dim3(kLebThreads), 0, stream, a);
+  hipLaunchKernelGGL(seg_group_scan_kernel, dim3(1), dim3(kSegScanThreads), 0, stream,
+                     (const uint32_t*)(ws + L.gsum_f), (const uint64_t*)(ws + L.gsum_v), groups,
+                     a.gexcl_v, (uint64_t*)nullptr);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (a.segs.num == 0) return hipSuccess;
-  hipLaunchKernelGGL(seg_corr_kernel, dim3((a.segs.num + 255) / 256), dim3(256), 0, stream, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(seg_add_kernel, dim3((uint32_t)L.etiles), dim3(kLebThreads), 0, stream, a);
+  hipLaunchKernelGGL(dec_write_kernel, grid, block, 0, stream, a, aligned);
   return hipGetLastError();
 }
 

@@ -5,20 +5,23 @@
 //
 // The global index space of the tensor list is cut into chunks of
 // `chunk_elems` words; a chunk may span several tensors and start inside
-// one.  Chunk c runs on stream c mod S: its extract writes into that
-// stream's device staging, then the chunk's count is copied to the host.
-// The host takes chunks in order: it waits for chunk c's count, which fixes
-// where chunk c's entries land in the host arrays, and enqueues the copy of
-// chunk c's (idx, val) behind it on the same stream, before it enqueues
-// chunk c + S there (so the staging is never overwritten early).  Up to S
-// chunks are in flight: extracts on some streams overlap device-to-host
-// copies on the others.
+// one.  Chunk c is extracted on stream c mod S into that stream's device
+// staging (coded: its indices are then gap + LEB128 coded there), and its
+// count is copied to the host.  The host takes chunks in order: it waits
+// for chunk c's count, which fixes where chunk c's entries land in the host
+// arrays, and enqueues the copies of chunk c on one copy stream of the
+// library's own (device-to-host copies from several streams at once share
+// the host link less well than back-to-back copies from one).  The extract
+// of chunk c + S waits on an event recorded after those copies, so the
+// staging is never overwritten early.  Up to S chunks are in flight:
+// extracts on the compute streams overlap the copies.
 #include <string.h>
 
 #include <vector>
 
 #include "aurora_delta.h"
 #include "delta_internal.h"
+#include "leb128.h"
 
 using namespace aurora;
 
@@ -192,6 +195,12 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     return DELTA_ERR_HIP;
   }
 
+  hipStream_t cs = nullptr;   // carries every data copy
+  std::vector<hipEvent_t> copied(S, nullptr);   // per staging slot: its last copies are done
+  e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+  for (int i = 0; i < S && e == hipSuccess; ++i)
+    e = hipEventCreateWithFlags(&copied[i], hipEventDisableTiming);
+
   std::vector<SliceIn> sl;
   uint64_t offset = 0;   // host position of the next chunk's first entry
   uint64_t boffset = 0;  // coded: host position of the next chunk's first byte
@@ -207,45 +216,42 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     return hipMemcpyAsync((char*)dst + elem * pos, src, elem * m, hipMemcpyDeviceToHost, st);
   };
   auto finish = [&](uint64_t c) -> hipError_t {
-    hipStream_t st = streams[c % S];
-    hipError_t err = hipStreamSynchronize(st);
+    hipError_t err = hipStreamSynchronize(streams[c % S]);
     if (err != hipSuccess) return err;
+    hipStream_t st = cs;
     const uint64_t cnt = h_counts[2 * c];
     char* stage = stage_of(c);
     if (!o.leb) {
       err = copy_out(o.h_idx, stage + L.idx, offset, o.h_idx_cap, cnt, 8, st);
-      if (err == hipSuccess) err = copy_out(o.h_val, stage + L.val, offset, o.h_val_cap, cnt, 2, st);
     } else {
       o.h_chunk_counts[c] = cnt;
-      if (cnt > 0) {
-        // the chunk's indices as one segment based at the chunk's first word
-        EncArgs a;
-        memset(&a, 0, sizeof(a));
-        a.idx = (const int64_t*)(stage + L.idx);
-        a.count = cnt;
-        a.segs = {nullptr, nullptr, 0, (int64_t)(c * chunk)};
-        a.out = (uint8_t*)(stage + L.bytes);
-        a.capacity = bytes_cap;
-        a.d_nbytes = (uint64_t*)(stage + L.nbytes);
-        const EncLayout E = enc_layout(cnt);
-        a.tile_bytes = (uint32_t*)(stage + L.enc_ws + E.tile_bytes);
-        err = launch_leb128_encode(a, (uint64_t*)(stage + L.enc_ws + E.group_sum),
-                                   (uint64_t*)(stage + L.enc_ws + E.group_excl), st);
-        if (err == hipSuccess)
-          err = hipMemcpyAsync(&h_counts[2 * c + 1], stage + L.nbytes, 8, hipMemcpyDeviceToHost,
-                               st);
-        if (err == hipSuccess)
-          err = copy_out(o.h_val, stage + L.val, offset, o.h_val_cap, cnt, 2, st);
-        if (err == hipSuccess) err = hipStreamSynchronize(st);
-        if (err != hipSuccess) return err;
-        const uint64_t nb = h_counts[2 * c + 1];
-        err = copy_out(o.h_bytes, stage + L.bytes, boffset, o.h_bytes_cap, nb, 1, st);
-        boffset += nb;
-      }
+      const uint64_t nb = h_counts[2 * c + 1];
+      err = copy_out(o.h_bytes, stage + L.bytes, boffset, o.h_bytes_cap, nb, 1, st);
+      boffset += nb;
     }
+    if (err == hipSuccess) err = copy_out(o.h_val, stage + L.val, offset, o.h_val_cap, cnt, 2, st);
+    if (err == hipSuccess) err = hipEventRecord(copied[c % S], st);
     offset += cnt;
     finished = c + 1;
     return err;
+  };
+  // Coded: the chunk's indices as one segment based at its first word; the
+  // encoder reads the entry count that the extract left in device memory.
+  const EncLayout E = enc_layout(chunk);
+  auto enqueue_encode = [&](uint64_t c) -> hipError_t {
+    char* stage = stage_of(c);
+    EncArgs a;
+    memset(&a, 0, sizeof(a));
+    a.idx = (const int64_t*)(stage + L.idx);
+    a.count = chunk;
+    a.d_count_in = (const uint64_t*)(stage + L.count);
+    a.segs = {nullptr, nullptr, 0, (int64_t)(c * chunk)};
+    a.out = (uint8_t*)(stage + L.bytes);
+    a.capacity = bytes_cap;
+    a.d_nbytes = (uint64_t*)(stage + L.nbytes);
+    a.tile_bytes = (uint32_t*)(stage + L.enc_ws + E.tile_bytes);
+    return launch_leb128_encode(a, (uint64_t*)(stage + L.enc_ws + E.group_sum),
+                                (uint64_t*)(stage + L.enc_ws + E.group_excl), streams[c % S]);
   };
 
   for (uint64_t c = 0; c < nchunks && e == hipSuccess; ++c) {
@@ -257,6 +263,10 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     const uint64_t hi = (total - lo < chunk) ? total : lo + chunk;
     chunk_slices(prevs, nexts, numels, T, lo, hi, sl);
     char* stage = stage_of(c);
+    if (c >= (uint64_t)S) {   // the slot's previous chunk must have left it
+      e = hipStreamWaitEvent(streams[c % S], copied[c % S], 0);
+      if (e != hipSuccess) break;
+    }
     const delta_status_t st =
         enqueue_extract(sl.data(), sl.size(), 0, true, stage + L.idx, (uint16_t*)(stage + L.val),
                         chunk, (uint64_t*)(stage + L.count), nullptr, stage + L.ws, L.ws_bytes,
@@ -265,8 +275,11 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
       status = st;
       break;
     }
-    e = hipMemcpyAsync(&h_counts[2 * c], stage + L.count, 8, hipMemcpyDeviceToHost,
-                       streams[c % S]);
+    if (o.leb) e = enqueue_encode(c);
+    // the count (and, coded, the byte count right after it) to the host
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(&h_counts[2 * c], stage + L.count, o.leb ? 16 : 8,
+                         hipMemcpyDeviceToHost, streams[c % S]);
     if (e == hipSuccess) issued = c + 1;
   }
   while (e == hipSuccess && status == DELTA_OK && finished < issued) e = finish(finished);
@@ -275,6 +288,13 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     hipError_t e2 = hipStreamSynchronize(streams[s]);
     if (e == hipSuccess) e = e2;
   }
+  if (cs) {
+    hipError_t e2 = hipStreamSynchronize(cs);
+    if (e == hipSuccess) e = e2;
+    (void)hipStreamDestroy(cs);
+  }
+  for (hipEvent_t ev : copied)
+    if (ev) (void)hipEventDestroy(ev);
   (void)hipHostFree(h_counts);
   if (e != hipSuccess) {
     set_error("HIP error in pipeline: %s", hipGetErrorString(e));

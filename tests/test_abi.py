@@ -154,7 +154,7 @@ def test_leb128_sizes_and_validation(lib):
     assert e0 <= e1 <= e2 < lib.delta_leb128_encode_workspace_bytes(1 << 24)
     d0 = lib.delta_leb128_decode_workspace_bytes(0, 0, 0)
     d1 = lib.delta_leb128_decode_workspace_bytes(1 << 20, 1 << 20, 0)
-    assert d0 < d1 < lib.delta_leb128_decode_workspace_bytes(1 << 20, 1 << 20, 1000)
+    assert d0 < d1 < lib.delta_leb128_decode_workspace_bytes(1 << 30, 1 << 20, 0)
     # capacity only matters up to nbytes (a number takes at least one byte)
     assert lib.delta_leb128_decode_workspace_bytes(100, 1 << 40, 0) == \
         lib.delta_leb128_decode_workspace_bytes(100, 100, 0)
