@@ -13,8 +13,9 @@ the C file with gcc into ``liboracle.so`` beside it.
 Pins (what the oracle is checked against, other than itself) are in
 ``tests/test_oracle.py``: brute force over every change mask of small
 inputs, numpy's own ``flatnonzero``, torch's ``index_put_``, bit-pattern
-special cases, the closed-form invariants of the definition, and the LEB128
-worked example printed in Sec. 5.1 (``tests/golden/leb128_example.txt``).
+special cases, the closed-form invariants of the definition, the LEB128
+worked example printed in Sec. 5.1 (``tests/golden/leb128_example.txt``),
+and, for delta chains, replay of the chain with numpy fancy assignment.
 """
 from __future__ import annotations
 
@@ -71,6 +72,8 @@ def _load():
     lib.oracle_leb128_encode.restype = U64
     lib.oracle_leb128_decode.argtypes = [P, U64, P, U64]
     lib.oracle_leb128_decode.restype = U64
+    lib.oracle_compose.argtypes = [P, P, P, ctypes.c_int32, P, P, U64]
+    lib.oracle_compose.restype = U64
     _lib = lib
     return lib
 
@@ -213,3 +216,29 @@ def leb128_decode(buf, capacity=None):
     if n == U64_MAX:
         raise ValueError("malformed LEB128 stream")
     return out[:min(n, cap)].copy(), int(n)
+
+
+def compose(deltas, capacity=None):
+    """One delta equal to replaying ``deltas`` (oldest first, each an
+    ``(idx, val)`` pair with strictly increasing int64 idx): Sec. 5.4 delta
+    catch-up, the last writer wins.  Returns (idx, val, true count)."""
+    lib = _load()
+    idx_arrs = [np.ascontiguousarray(i, dtype=np.int64) for i, _ in deltas]
+    val_arrs = [_u16(v) for _, v in deltas]
+    for i, v in zip(idx_arrs, val_arrs):
+        if i.size != v.size:
+            raise ValueError("idx and val differ in length")
+    K = len(deltas)
+    total = sum(i.size for i in idx_arrs)
+    cap = total if capacity is None else int(capacity)
+    out_idx = np.empty(max(cap, 1), dtype=np.int64)
+    out_val = np.empty(max(cap, 1), dtype=np.uint16)
+    ip = (ctypes.c_void_p * max(K, 1))(*[a.ctypes.data for a in idx_arrs])
+    vp = (ctypes.c_void_p * max(K, 1))(*[a.ctypes.data for a in val_arrs])
+    counts = np.array([a.size for a in idx_arrs] or [0], dtype=np.uint64)
+    n = lib.oracle_compose(ctypes.cast(ip, ctypes.c_void_p), ctypes.cast(vp, ctypes.c_void_p),
+                           _ptr(counts), K, _ptr(out_idx), _ptr(out_val), cap)
+    if n == U64_MAX:
+        raise ValueError("index streams must be strictly increasing")
+    k = min(n, cap)
+    return out_idx[:k].copy(), out_val[:k].copy(), int(n)

@@ -30,6 +30,12 @@
  *                  number is then written as unsigned LEB128 (7 payload bits
  *                  per byte, least significant group first, high bit set on
  *                  every byte but the last).
+ *   compose        Sec. 5.4 "Version-predicate join and delta catch-up": a
+ *                  worker K versions behind replays the missed deltas in
+ *                  order.  Apply assigns, so that replay equals one delta
+ *                  holding every index of the chain with the value of the
+ *                  newest delta that has it (merge of the sorted streams,
+ *                  the last writer wins).
  *
  * Conventions shared with the library's C ABI (they are the ABI's contract,
  * restated here, not code shared with it): bf16 words travel as raw uint16
@@ -39,6 +45,7 @@
  */
 #include <stdint.h>
 #include <stddef.h>
+#include <stdlib.h>
 
 /* ------------------------------------------------------------------ */
 /* extract: one tensor, local indices                                  */
@@ -280,5 +287,59 @@ uint64_t oracle_leb128_decode(const uint8_t *in, uint64_t nbytes,
             idx[count] = (int64_t)acc;
         ++count;
     }
+    return count;
+}
+
+/* ------------------------------------------------------------------ */
+/* delta chain composition                                             */
+/* ------------------------------------------------------------------ */
+
+/* Sec. 5.4: the deltas D_1 .. D_K (oldest first, each with a strictly
+ * increasing index stream) as one delta.  K-pointer merge: take the
+ * smallest index that any stream has not passed yet, keep the value of the
+ * newest stream that holds it, and step past it in every stream that holds
+ * it.  Returns the true count (only the first `capacity` entries written),
+ * or UINT64_MAX if some stream is not strictly increasing. */
+uint64_t oracle_compose(const int64_t *const *idxs, const uint16_t *const *vals,
+                        const uint64_t *counts, int32_t num_deltas, int64_t *out_idx,
+                        uint16_t *out_val, uint64_t capacity)
+{
+    for (int32_t d = 0; d < num_deltas; ++d)
+        for (uint64_t k = 1; k < counts[d]; ++k)
+            if (idxs[d][k] <= idxs[d][k - 1])
+                return UINT64_MAX;
+    uint64_t *pos = calloc(num_deltas > 0 ? (size_t)num_deltas : 1, sizeof(uint64_t));
+    if (!pos)
+        return UINT64_MAX;
+    uint64_t count = 0;
+    for (;;) {
+        int found = 0;
+        int64_t smallest = 0;
+        for (int32_t d = 0; d < num_deltas; ++d) {
+            if (pos[d] < counts[d] && (!found || idxs[d][pos[d]] < smallest)) {
+                smallest = idxs[d][pos[d]];
+                found = 1;
+            }
+        }
+        if (!found)
+            break;
+        uint16_t value = 0;
+        int have = 0;
+        for (int32_t d = num_deltas - 1; d >= 0; --d) {
+            if (pos[d] < counts[d] && idxs[d][pos[d]] == smallest) {
+                if (!have) {
+                    value = vals[d][pos[d]];
+                    have = 1;
+                }
+                ++pos[d];
+            }
+        }
+        if (count < capacity) {
+            out_idx[count] = smallest;
+            out_val[count] = value;
+        }
+        ++count;
+    }
+    free(pos);
     return count;
 }

@@ -11,7 +11,10 @@ oracle with an independent route to the same answer:
   (signed zeros, NaN payloads), which fix the bitwise reading;
 * invariants of the definition (empty on identical inputs, count, order,
   round trip, idempotence, multi == single on the concatenation);
-* the LEB128 worked example printed in Sec. 5.1 (``golden/``).
+* the LEB128 worked example printed in Sec. 5.1 (``golden/``);
+* for delta chains (Sec. 5.4 catch-up): the chain replayed one delta after
+  the other with numpy fancy assignment onto a sentinel-filled vector,
+  which fixes both the index set and every value of the composed delta.
 
 ``test_mutants_are_caught`` plants plausible mistakes in copies of the
 oracle's C source, compiles them on the CPU and checks that the pins reject
@@ -352,6 +355,112 @@ def test_gaps_and_leb128_round_trip():
         oracle.leb128_decode(np.array([0x80], np.uint8))
 
 
+# ---------------------------------------------------------- delta chains
+
+SENTINEL = 0xFFFF   # never a value of a planted delta below
+
+
+def random_delta(n, density, seed):
+    r = rng(seed)
+    k = r.binomial(n, density)
+    idx = np.sort(r.choice(n, size=k, replace=False)).astype(np.int64)
+    val = r.integers(0, SENTINEL, size=k, dtype=np.uint16)
+    return idx, val
+
+
+def replay(n, deltas):
+    """The chain replayed in order with numpy fancy assignment."""
+    w = np.full(n, SENTINEL, dtype=np.uint16)
+    for idx, val in deltas:
+        w[idx] = val
+    return w
+
+
+def check_against_replay(n, deltas):
+    idx, val, cnt = oracle.compose(deltas)
+    w = replay(n, deltas)
+    touched = np.flatnonzero(w != SENTINEL)
+    assert cnt == touched.size
+    np.testing.assert_array_equal(idx, touched)
+    np.testing.assert_array_equal(val, w[touched])
+    return idx, val
+
+
+@pytest.mark.parametrize("K", [1, 2, 3, 5, 8])
+@pytest.mark.parametrize("density", [0.01, 0.3, 0.9])
+def test_compose_equals_replay(K, density):
+    n = 5000
+    deltas = [random_delta(n, density, seed=100 * K + d) for d in range(K)]
+    check_against_replay(n, deltas)
+
+
+def test_compose_bruteforce_small():
+    # every pair and a sample of triples of index subsets of 5 positions,
+    # values distinct per delta so that the writer of every word is visible
+    n = 5
+    subsets = [np.array([i for i in range(n) if (m >> i) & 1], np.int64) for m in range(1 << n)]
+    for a in range(1 << n):
+        for b in range(1 << n):
+            deltas = [(subsets[a], (100 + subsets[a]).astype(np.uint16)),
+                      (subsets[b], (200 + subsets[b]).astype(np.uint16))]
+            check_against_replay(n, deltas)
+    r = rng(4)
+    for _ in range(300):
+        ms = r.integers(0, 1 << n, size=3)
+        deltas = [(subsets[m], (100 * (d + 1) + subsets[m]).astype(np.uint16))
+                  for d, m in enumerate(ms)]
+        check_against_replay(n, deltas)
+
+
+def test_compose_special_cases():
+    a = (np.array([1, 4, 9], np.int64), np.array([10, 40, 90], np.uint16))
+    b = (np.array([4, 9, 12], np.int64), np.array([41, 91, 121], np.uint16))
+    # one delta: itself
+    idx, val, cnt = oracle.compose([a])
+    assert idx.tolist() == [1, 4, 9] and val.tolist() == [10, 40, 90]
+    # no delta / empty deltas: empty
+    assert oracle.compose([])[2] == 0
+    e = (np.zeros(0, np.int64), np.zeros(0, np.uint16))
+    assert oracle.compose([e, e])[2] == 0
+    idx, val, _ = oracle.compose([e, a, e])
+    assert idx.tolist() == [1, 4, 9]
+    # the same indices twice: the second delta's values
+    idx, val, _ = oracle.compose([a, (a[0], a[1] + 1)])
+    assert val.tolist() == [11, 41, 91]
+    # disjoint ranges: the concatenation
+    far = (a[0] + 100, a[1])
+    idx, _, _ = oracle.compose([far, a])
+    assert idx.tolist() == [1, 4, 9, 101, 104, 109]
+    # composition is associative
+    c = (np.array([0, 9, 30], np.int64), np.array([1, 2, 3], np.uint16))
+    ab = oracle.compose([a, b])[:2]
+    bc = oracle.compose([b, c])[:2]
+    left = oracle.compose([ab, c])
+    right = oracle.compose([a, bc])
+    np.testing.assert_array_equal(left[0], right[0])
+    np.testing.assert_array_equal(left[1], right[1])
+    # capacity truncates but counts
+    idx, val, cnt = oracle.compose([a, b], capacity=2)
+    assert cnt == 4 and idx.tolist() == [1, 4]
+    # unsorted streams are refused
+    with pytest.raises(ValueError):
+        oracle.compose([(np.array([3, 3], np.int64), np.array([1, 2], np.uint16))])
+
+
+def test_compose_then_apply_equals_sequential_apply():
+    # the catch-up use: apply(W, compose(D1..DK)) == apply(..apply(W, D1).., DK)
+    n = 3000
+    w0 = rng(8).integers(0, 1 << 16, size=n, dtype=np.uint16)
+    deltas = [random_delta(n, 0.05, seed=300 + d) for d in range(6)]
+    seq = w0.copy()
+    for idx, val in deltas:
+        seq[idx] = val
+    idx, val, _ = oracle.compose(deltas)
+    once = w0.copy()
+    once[idx] = val
+    np.testing.assert_array_equal(once, seq)
+
+
 # ---------------------------------------------------------------- mutants
 
 MUTANTS = {
@@ -373,6 +482,12 @@ MUTANTS = {
     # a wrong LEB128 group order (most significant first)
     "leb_continuation_on_last": ("        if (v != 0)\n            byte |= 0x80;",
                                  "        if (v == 0)\n            byte |= 0x80;"),
+    # the oldest writer wins instead of the newest
+    "compose_first_writer": ("        for (int32_t d = num_deltas - 1; d >= 0; --d) {",
+                             "        for (int32_t d = 0; d < num_deltas; ++d) {"),
+    # a duplicate index stepped past in only one stream
+    "compose_single_advance": ("                    have = 1;\n                }\n                ++pos[d];",
+                               "                    have = 1;\n                    ++pos[d];\n                }"),
 }
 
 
@@ -431,6 +546,23 @@ def _pins_pass(lib):
     out = np.empty(10, np.uint8)
     n = lib.oracle_leb128_encode(np.array([198], np.int64).ctypes.data, 1, out.ctypes.data, 10)
     if bytes(out[:n].tolist()) != b"\xc6\x01":
+        return False
+    # a delta chain against its replay
+    lib.oracle_compose.argtypes = [P, P, P, ctypes.c_int32, P, P, U64]
+    lib.oracle_compose.restype = U64
+    n = 400
+    deltas = [random_delta(n, 0.3, seed=40 + d) for d in range(3)]
+    ip = (P * 3)(*[i.ctypes.data for i, _ in deltas])
+    vp = (P * 3)(*[v.ctypes.data for _, v in deltas])
+    counts = np.array([i.size for i, _ in deltas], np.uint64)
+    oi = np.empty(3 * n, np.int64)
+    ov = np.empty(3 * n, np.uint16)
+    c = lib.oracle_compose(ctypes.cast(ip, P), ctypes.cast(vp, P), counts.ctypes.data, 3,
+                           oi.ctypes.data, ov.ctypes.data, 3 * n)
+    w = replay(n, deltas)
+    touched = np.flatnonzero(w != SENTINEL)
+    if c != touched.size or not np.array_equal(oi[:c], touched) or \
+            not np.array_equal(ov[:c], w[touched]):
         return False
     return True
 
