@@ -259,6 +259,72 @@ def leb128_measurement(ad, idx, d_offs, numels, stream, reps):
     }
 
 
+def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
+    """Sec. 5.4 catch-up over a chain of `chain` deltas, each ~1% of the
+    Qwen3-8B index space at uniformly random positions (drawn on the GPU):
+    delta_compose timed with HIP events, then one apply of the composed
+    delta against replaying the chain delta by delta."""
+    import torch
+    dev = rollout[0].device
+    g = torch.Generator(device=dev)
+    g.manual_seed(11456 + 54)
+    deltas = []
+    for d in range(chain):
+        idx = torch.unique(torch.randint(0, N, (K_entries,), device=dev, generator=g))
+        val = torch.randint(-32768, 32767, (idx.numel(),), device=dev, generator=g,
+                            dtype=torch.int16).view(torch.bfloat16)
+        deltas.append((idx, val))
+    counts = [i.numel() for i, _ in deltas]
+    lib = ad.library()
+    ws = torch.empty(ad.delta_compose_workspace_bytes(counts), dtype=torch.uint8, device=dev)
+    cap = sum(counts)
+    out_i = torch.empty(cap, dtype=torch.int64, device=dev)
+    out_v = torch.empty(cap, dtype=torch.bfloat16, device=dev)
+    cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    ip = ad._ptr_array([i.data_ptr() for i, _ in deltas])
+    vp = ad._ptr_array([v.data_ptr() for _, v in deltas])
+    ca = ad._u64_array(counts)
+    h = stream.cuda_stream
+
+    def compose():
+        st = lib.delta_compose(ip, vp, ca, chain, out_i.data_ptr(), out_v.data_ptr(), cap,
+                               cnt.data_ptr(), None, ws.data_ptr(), ws.numel(), h)
+        if st:
+            raise RuntimeError(lib.delta_last_error().decode())
+
+    compose()
+    stream.synchronize()
+    k = int(cnt.item())
+    apply_ws = torch.empty(max(ad.delta_apply_multi_workspace_bytes(len(rollout)), 1),
+                           dtype=torch.uint8, device=dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+    for e0, e1, e2, e3 in ev:
+        e0.record(stream)
+        compose()
+        e1.record(stream)
+        ad.delta_apply_multi(rollout, out_i[:k], out_v[:k], workspace=apply_ws, stream=stream)
+        e2.record(stream)
+        for idx, val in deltas:
+            ad.delta_apply_multi(rollout, idx, val, workspace=apply_ws, stream=stream)
+        e3.record(stream)
+    stream.synchronize()
+    med = lambda xs: sorted(xs)[len(xs) // 2]
+    tc = med([e0.elapsed_time(e1) for e0, e1, _, _ in ev])
+    ta = med([e1.elapsed_time(e2) for _, e1, e2, _ in ev])
+    tr = med([e2.elapsed_time(e3) for _, _, e2, e3 in ev])
+    moved = (sum(counts) + k) * 10   # every input entry read once, the result written once
+    return {
+        "workload": f"{chain} deltas of ~1% random positions of the {N}-word index space "
+                    f"({sum(counts)} entries), composed into {k}",
+        "compose_ms": round(tc, 4),
+        "compose_GBps_one_pass": round(moved / (tc / 1e3) / 1e9, 1),
+        "entries_per_s": round(sum(counts) / (tc / 1e3), 1),
+        "apply_composed_ms": round(ta, 4),
+        "replay_chain_ms": round(tr, 4),
+        "catch_up_compose_plus_apply_ms": round(tc + ta, 4),
+    }
+
+
 def _prefix(xs):
     s = 0
     for x in xs:
@@ -410,6 +476,7 @@ def main():
     }
     result["leb128"] = leb128_measurement(ad, out_idx[:K], d_offs, plan.numels, stream,
                                           args.steps)
+    result["compose"] = compose_measurement(ad, rollout, N, K, stream, max(args.steps // 2, 3))
     if args.copy_calibration > 0:
         n = args.copy_calibration // 2
         src = torch.empty(n, dtype=torch.int16, device=dev)

@@ -242,6 +242,40 @@ delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
                                    uint64_t* d_count, uint32_t* d_error_flag, void* workspace,
                                    size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Delta chains — Sec. 5.4, "Version-predicate join and delta catch-up": a
+ * worker K versions behind replays the missed deltas D_1 .. D_K in order.
+ * Apply assigns the new words, so that replay equals applying one delta
+ * that holds every index of the chain with the value of the newest delta
+ * that has it (the last writer wins).  delta_compose builds that delta.
+ */
+
+/* Workspace bytes for delta_compose of `num_deltas` deltas with these entry
+ * counts (host array); 0 if the arguments are invalid. */
+size_t delta_compose_workspace_bytes(const uint64_t* counts, int32_t num_deltas);
+
+/*
+ * delta_compose
+ *   idx_ptrs, val_ptrs  host arrays of num_deltas device pointers, oldest
+ *                 delta first: int64 indices (strictly increasing within
+ *                 each delta, as delta_extract_multi writes them) and
+ *                 16-bit words.  Unsorted input gives an unspecified result
+ *                 (never an access out of bounds) and may set the flag.
+ *   counts        host array: entries of each delta.
+ *   out_idx, out_val  device arrays of `capacity` entries: the composed
+ *                 delta, strictly increasing; *d_count gets its true size
+ *                 (only the first `capacity` entries are written).
+ *   d_error_flag  nullable device uint32, set on inconsistent (unsorted)
+ *                 input.
+ * Enqueued on `stream` without any host wait (intermediate counts stay on
+ * the device).  apply(W, compose(D_1..D_K)) == apply(..apply(W, D_1).., D_K).
+ */
+delta_status_t delta_compose(const int64_t* const* idx_ptrs, const uint16_t* const* val_ptrs,
+                             const uint64_t* counts, int32_t num_deltas, int64_t* out_idx,
+                             uint16_t* out_val, uint64_t capacity, uint64_t* d_count,
+                             uint32_t* d_error_flag, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
 /* Options of the chunked pipeline. */
 typedef struct {
   uint64_t chunk_elems; /* words of the global index space per chunk (> 0) */

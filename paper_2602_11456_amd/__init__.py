@@ -30,6 +30,7 @@ __all__ = [
     "delta_extract_multi_workspace_bytes", "delta_apply_multi_workspace_bytes",
     "delta_pipeline_staging_bytes", "MultiPlan", "delta_leb128_encode", "delta_leb128_decode",
     "delta_extract_pipelined_leb128", "delta_pipeline_leb128_staging_bytes", "chunk_segments",
+    "delta_compose", "delta_compose_workspace_bytes", "delta_catch_up",
 ]
 
 
@@ -288,6 +289,61 @@ def delta_apply_multi(weights: Sequence[torch.Tensor], idx: torch.Tensor, val: t
         (stream or torch.cuda.current_stream()).synchronize()
         if int(flag.item()) != 0:
             raise DeltaError(_abi.DELTA_ERR_OUT_OF_RANGE, "an index was outside the tensors")
+
+
+# --------------------------------------------------------- delta chains
+
+def delta_compose_workspace_bytes(counts: Sequence[int]) -> int:
+    return int(library().delta_compose_workspace_bytes(_u64_array(counts), len(counts)))
+
+
+def delta_compose(deltas: Sequence[Tuple[torch.Tensor, torch.Tensor]],
+                  capacity: Optional[int] = None,
+                  stream: Optional[torch.cuda.Stream] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """One delta equal to replaying ``deltas`` (oldest first; each an (int64
+    idx, 16-bit val) pair of GPU tensors with strictly increasing idx): the
+    Sec. 5.4 catch-up chain, the last writer wins.  Synchronises to read
+    the count."""
+    if not deltas:
+        raise ValueError("no deltas")
+    dev = deltas[0][0].device
+    for i, (idx, val) in enumerate(deltas):
+        if idx.dtype != torch.int64 or not idx.is_cuda or not idx.is_contiguous():
+            raise TypeError(f"delta {i}: idx must be a contiguous int64 GPU tensor")
+        _words(val, f"delta {i} val")
+        if idx.numel() != val.numel():
+            raise ValueError(f"delta {i}: idx and val differ in length")
+    counts = [idx.numel() for idx, _ in deltas]
+    ws = _workspace(delta_compose_workspace_bytes(counts), dev)
+    cap = sum(counts) if capacity is None else int(capacity)
+    out_idx = torch.empty(max(cap, 1), dtype=torch.int64, device=dev)
+    out_val = torch.empty(max(cap, 1), dtype=deltas[0][1].dtype, device=dev)
+    cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    _check(library().delta_compose(
+        _ptr_array([i.data_ptr() for i, _ in deltas]), _ptr_array([v.data_ptr() for _, v in deltas]),
+        _u64_array(counts), len(deltas), out_idx.data_ptr(), out_val.data_ptr(), cap,
+        cnt.data_ptr(), flag.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)))
+    (stream or torch.cuda.current_stream()).synchronize()
+    if int(flag.item()):
+        raise DeltaError(_abi.DELTA_ERR_INVALID_ARG, "index streams are not sorted")
+    k = int(cnt.item())
+    if k > cap:
+        raise DeltaError(_abi.DELTA_ERR_CAPACITY, f"{k} entries do not fit {cap}")
+    return out_idx[:k], out_val[:k]
+
+
+def delta_catch_up(weights: Sequence[torch.Tensor],
+                   deltas: Sequence[Tuple[torch.Tensor, torch.Tensor]], compose: bool = True,
+                   stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Bring a rollout copy forward over a chain of missed deltas (Sec. 5.4):
+    either compose them and apply once, or replay them in order."""
+    if compose:
+        idx, val = delta_compose(deltas, stream=stream)
+        delta_apply_multi(weights, idx, val, check=True, stream=stream)
+    else:
+        for idx, val in deltas:
+            delta_apply_multi(weights, idx, val, check=True, stream=stream)
 
 
 # -------------------------------------------------------------- LEB128

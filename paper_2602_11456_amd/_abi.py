@@ -55,6 +55,8 @@ SIGNATURES = {
     "delta_leb128_decode_workspace_bytes": (SZ, [U64, U64, ctypes.c_uint32]),
     "delta_leb128_encode": (STATUS, [P, U64, P, P, ctypes.c_uint32, P, U64, P, P, P, P, SZ, P]),
     "delta_leb128_decode": (STATUS, [P, U64, P, P, ctypes.c_uint32, P, U64, P, P, P, SZ, P]),
+    "delta_compose_workspace_bytes": (SZ, [P, I32]),
+    "delta_compose": (STATUS, [P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
     "delta_pipeline_staging_bytes": (SZ, [P, I32, ctypes.POINTER(delta_pipeline_opts_t)]),
     "delta_extract_pipelined": (STATUS, [P, P, P, I32, ctypes.POINTER(delta_pipeline_opts_t), P,
                                          P, SZ, P, P, U64, P]),

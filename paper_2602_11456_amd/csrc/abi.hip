@@ -389,4 +389,41 @@ delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
   return ok();
 }
 
+size_t delta_compose_workspace_bytes(const uint64_t* counts, int32_t num_deltas) {
+  if (num_deltas < 0 || (num_deltas > 0 && !counts)) return 0;
+  return chain_layout(counts, num_deltas).total;
+}
+
+delta_status_t delta_compose(const int64_t* const* idx_ptrs, const uint16_t* const* val_ptrs,
+                             const uint64_t* counts, int32_t num_deltas, int64_t* out_idx,
+                             uint16_t* out_val, uint64_t capacity, uint64_t* d_count,
+                             uint32_t* d_error_flag, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
+  if (num_deltas < 0) return fail(DELTA_ERR_INVALID_ARG, "num_deltas < 0");
+  if (num_deltas > 0 && (!idx_ptrs || !val_ptrs || !counts))
+    return fail(DELTA_ERR_INVALID_ARG, "NULL host array");
+  if (!d_count) return fail(DELTA_ERR_INVALID_ARG, "d_count is NULL");
+  if (capacity > 0 && (!out_idx || !out_val))
+    return fail(DELTA_ERR_INVALID_ARG, "NULL output with capacity > 0");
+  if ((uintptr_t)out_idx % 8 || (uintptr_t)out_val % 2)
+    return fail(DELTA_ERR_INVALID_ARG, "misaligned output");
+  uint64_t total = 0;
+  for (int32_t d = 0; d < num_deltas; ++d) {
+    if (counts[d] > 0 && (!idx_ptrs[d] || !val_ptrs[d]))
+      return fail(DELTA_ERR_INVALID_ARG, "delta %d: NULL pointer", d);
+    if ((uintptr_t)idx_ptrs[d] % 8 || (uintptr_t)val_ptrs[d] % 2)
+      return fail(DELTA_ERR_INVALID_ARG, "delta %d: misaligned", d);
+    if (counts[d] > (1ull << 56) || total + counts[d] < total)
+      return fail(DELTA_ERR_INVALID_ARG, "delta %d: count too large", d);
+    total += counts[d];
+  }
+  const ChainLayout L = chain_layout(counts, num_deltas);
+  delta_status_t st = check_workspace(workspace, workspace_bytes, L.total);
+  if (st != DELTA_OK) return st;
+  hipError_t e = launch_compose_chain(idx_ptrs, val_ptrs, counts, num_deltas, out_idx, out_val,
+                                      capacity, d_count, d_error_flag, (char*)workspace, stream);
+  if (e != hipSuccess) return hip_fail(e, "compose launch");
+  return ok();
+}
+
 }  // extern "C"

@@ -192,6 +192,18 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
                                uint64_t* d_count, uint64_t* d_offsets, void* workspace,
                                size_t workspace_bytes, hipStream_t stream);
 
+// Delta chain composition (compose.hip): workspace layout for `K` deltas
+// of the given counts, and the enqueue of the whole chain on `stream`.
+struct ChainLayout {
+  size_t scratch, counts, inter, total;
+  uint64_t rounds;
+};
+ChainLayout chain_layout(const uint64_t* counts, int32_t K);
+hipError_t launch_compose_chain(const int64_t* const* idx, const uint16_t* const* val,
+                                const uint64_t* counts, int32_t K, int64_t* out_idx,
+                                uint16_t* out_val, uint64_t capacity, uint64_t* d_count,
+                                uint32_t* err, char* ws, hipStream_t stream);
+
 // Thread-local detail text behind delta_last_error() (abi.hip).
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 void clear_error();

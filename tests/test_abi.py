@@ -210,3 +210,28 @@ def test_pipeline_leb128_validation(lib):
     # staging of the plain pipeline is not enough
     assert F(prevs, prevs, numels, 1, ctypes.byref(opts), streams, FAKE, plain, FAKE, 100, FAKE,
              100, counts, 4, ctypes.byref(cnt), ctypes.byref(nb)) == _abi.DELTA_ERR_WORKSPACE
+
+
+def test_compose_validation(lib):
+    P = ctypes.c_void_p
+    counts = (ctypes.c_uint64 * 3)(100, 0, 50)
+    ws_need = lib.delta_compose_workspace_bytes(counts, 3)
+    assert ws_need > 0
+    assert lib.delta_compose_workspace_bytes(counts, -1) == 0
+    # two deltas need no intermediate round, three do
+    assert lib.delta_compose_workspace_bytes(counts, 2) < ws_need
+    idx = (P * 3)(FAKE, None, FAKE)
+    val = (P * 3)(FAKE, None, FAKE)
+    C = lib.delta_compose
+    assert C(idx, val, counts, 3, FAKE, FAKE, 10, None, None, FAKE, ws_need, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # no d_count
+    assert C(idx, val, counts, -2, FAKE, FAKE, 10, FAKE, None, FAKE, ws_need, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    bad = (P * 3)(FAKE, None, FAKE + 4)
+    assert C(bad, val, counts, 3, FAKE, FAKE, 10, FAKE, None, FAKE, ws_need, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # misaligned idx
+    assert C(idx, val, counts, 3, FAKE, FAKE, 10, FAKE, None, FAKE, 8, None) == \
+        _abi.DELTA_ERR_WORKSPACE
+    nulls = (P * 3)(None, None, FAKE)
+    assert C(nulls, val, counts, 3, FAKE, FAKE, 10, FAKE, None, FAKE, ws_need, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # delta 0 has entries but no pointer

@@ -159,3 +159,24 @@ def test_qwen3_14b_pipeline():
     o, b = ad.chunk_segments(counts, used)
     back = ad.delta_leb128_decode(hb.to(DEV), o, b)
     assert torch.equal(back, idx)
+
+
+def test_compose_chain_full_index_space():
+    # three deltas of ~1% random positions of the Qwen3-8B index space
+    N = 8_190_735_360
+    g = torch.Generator(device=DEV)
+    g.manual_seed(77)
+    deltas = []
+    for d in range(3):
+        idx = torch.unique(torch.randint(0, N, (81_907_354,), device=DEV, generator=g))
+        val = torch.randint(-32768, 32767, (idx.numel(),), device=DEV, generator=g,
+                            dtype=torch.int16).view(torch.bfloat16)
+        deltas.append((idx, val))
+    say("compose: deltas of", [i.numel() for i, _ in deltas], "entries")
+    out_i, out_v = ad.delta_compose(deltas)
+    say("composed", out_i.numel())
+    hd = [(i.cpu().numpy(), v.view(torch.int16).cpu().numpy().view(np.uint16)) for i, v in deltas]
+    ref_i, ref_v, ref_n = oracle.compose(hd)
+    assert out_i.numel() == ref_n
+    np.testing.assert_array_equal(out_i.cpu().numpy(), ref_i)
+    np.testing.assert_array_equal(out_v.view(torch.int16).cpu().numpy().view(np.uint16), ref_v)
