@@ -74,6 +74,10 @@ def _load():
     lib.oracle_leb128_decode.restype = U64
     lib.oracle_compose.argtypes = [P, P, P, ctypes.c_int32, P, P, U64]
     lib.oracle_compose.restype = U64
+    lib.oracle_xxh64.argtypes = [P, U64, U64]
+    lib.oracle_xxh64.restype = U64
+    lib.oracle_hash_segments.argtypes = [P, U64, U64, U64, P]
+    lib.oracle_hash_segments.restype = None
     _lib = lib
     return lib
 
@@ -242,3 +246,25 @@ def compose(deltas, capacity=None):
         raise ValueError("index streams must be strictly increasing")
     k = min(n, cap)
     return out_idx[:k].copy(), out_val[:k].copy(), int(n)
+
+
+def _bytes(data) -> np.ndarray:
+    if isinstance(data, (bytes, bytearray)):
+        return np.frombuffer(bytes(data), dtype=np.uint8)
+    return np.ascontiguousarray(data).reshape(-1).view(np.uint8)
+
+
+def xxh64(data, seed: int = 0) -> int:
+    """XXH64 of the bytes of ``data`` (Sec. 5.1 integrity hash)."""
+    b = _bytes(data)
+    return int(_load().oracle_xxh64(_ptr(b) if b.size else None, b.size, seed))
+
+
+def hash_segments(data, seg_bytes: int, seed: int = 0) -> np.ndarray:
+    """XXH64 of every ``seg_bytes`` piece of ``data`` (Sec. 5.2 segments)."""
+    b = _bytes(data)
+    n = (b.size + seg_bytes - 1) // seg_bytes
+    out = np.empty(max(n, 1), dtype=np.uint64)
+    if n:
+        _load().oracle_hash_segments(_ptr(b), b.size, seg_bytes, seed, _ptr(out))
+    return out[:n].copy()

@@ -30,6 +30,13 @@
  *                  number is then written as unsigned LEB128 (7 payload bits
  *                  per byte, least significant group first, high bit set on
  *                  every byte but the last).
+ *   xxh64          Sec. 5.1 / Sec. 5.2: every delta checkpoint carries an
+ *                  integrity hash and is cut into segments verified against
+ *                  it.  The hash is XXH64 (Y. Collet, "xxHash fast digest
+ *                  algorithm", specification v0.1.1), written out from that
+ *                  specification: four 64-bit accumulators over 32-byte
+ *                  stripes, a merge, the tail in 8/4/1-byte steps, and the
+ *                  final avalanche.
  *   compose        Sec. 5.4 "Version-predicate join and delta catch-up": a
  *                  worker K versions behind replays the missed deltas in
  *                  order.  Apply assigns, so that replay equals one delta
@@ -342,4 +349,101 @@ uint64_t oracle_compose(const int64_t *const *idxs, const uint16_t *const *vals,
     }
     free(pos);
     return count;
+}
+
+/* ------------------------------------------------------------------ */
+/* XXH64 integrity hash                                                */
+/* ------------------------------------------------------------------ */
+
+static const uint64_t XP1 = 11400714785074694791ULL;
+static const uint64_t XP2 = 14029467366897019727ULL;
+static const uint64_t XP3 = 1609587929392839161ULL;
+static const uint64_t XP4 = 9650029242287828579ULL;
+static const uint64_t XP5 = 2870177450012600261ULL;
+
+static uint64_t rotl64(uint64_t x, int r) { return (x << r) | (x >> (64 - r)); }
+
+static uint64_t read_le64(const uint8_t *p)
+{
+    uint64_t v = 0;
+    for (int b = 7; b >= 0; --b)
+        v = (v << 8) | p[b];
+    return v;
+}
+
+static uint32_t read_le32(const uint8_t *p)
+{
+    return (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16) |
+           ((uint32_t)p[3] << 24);
+}
+
+static uint64_t xround(uint64_t acc, uint64_t lane)
+{
+    acc += lane * XP2;
+    acc = rotl64(acc, 31);
+    return acc * XP1;
+}
+
+/* XXH64 of `len` bytes at `data` with `seed`, step by step as the
+ * specification gives it. */
+uint64_t oracle_xxh64(const uint8_t *data, uint64_t len, uint64_t seed)
+{
+    const uint8_t *p = data;
+    uint64_t left = len;
+    uint64_t acc;
+    if (len >= 32) {
+        uint64_t a1 = seed + XP1 + XP2, a2 = seed + XP2, a3 = seed, a4 = seed - XP1;
+        while (left >= 32) {
+            a1 = xround(a1, read_le64(p));
+            a2 = xround(a2, read_le64(p + 8));
+            a3 = xround(a3, read_le64(p + 16));
+            a4 = xround(a4, read_le64(p + 24));
+            p += 32;
+            left -= 32;
+        }
+        acc = rotl64(a1, 1) + rotl64(a2, 7) + rotl64(a3, 12) + rotl64(a4, 18);
+        acc = (acc ^ xround(0, a1)) * XP1 + XP4;
+        acc = (acc ^ xround(0, a2)) * XP1 + XP4;
+        acc = (acc ^ xround(0, a3)) * XP1 + XP4;
+        acc = (acc ^ xround(0, a4)) * XP1 + XP4;
+    } else {
+        acc = seed + XP5;
+    }
+    acc += len;
+    while (left >= 8) {
+        acc ^= xround(0, read_le64(p));
+        acc = rotl64(acc, 27) * XP1 + XP4;
+        p += 8;
+        left -= 8;
+    }
+    if (left >= 4) {
+        acc ^= (uint64_t)read_le32(p) * XP1;
+        acc = rotl64(acc, 23) * XP2 + XP3;
+        p += 4;
+        left -= 4;
+    }
+    while (left >= 1) {
+        acc ^= (uint64_t)(*p) * XP5;
+        acc = rotl64(acc, 11) * XP1;
+        ++p;
+        --left;
+    }
+    acc ^= acc >> 33;
+    acc *= XP2;
+    acc ^= acc >> 29;
+    acc *= XP3;
+    acc ^= acc >> 32;
+    return acc;
+}
+
+/* The hash of each `seg_bytes`-long piece of `data` (the last piece may be
+ * shorter): the per-segment integrity check of Sec. 5.2. */
+void oracle_hash_segments(const uint8_t *data, uint64_t len, uint64_t seg_bytes, uint64_t seed,
+                          uint64_t *hashes)
+{
+    uint64_t s = 0;
+    for (uint64_t off = 0; off < len; off += seg_bytes, ++s) {
+        uint64_t n = len - off < seg_bytes ? len - off : seg_bytes;
+        hashes[s] = oracle_xxh64(data + off, n, seed);
+    }
 }

@@ -14,7 +14,10 @@ oracle with an independent route to the same answer:
 * the LEB128 worked example printed in Sec. 5.1 (``golden/``);
 * for delta chains (Sec. 5.4 catch-up): the chain replayed one delta after
   the other with numpy fancy assignment onto a sentinel-filled vector,
-  which fixes both the index set and every value of the composed delta.
+  which fixes both the index set and every value of the composed delta;
+* for the integrity hash: the independent ``xxhash`` library (a separate
+  implementation of XXH64) on every length from 0 to 100 bytes and larger
+  buffers, several seeds.
 
 ``test_mutants_are_caught`` plants plausible mistakes in copies of the
 oracle's C source, compiles them on the CPU and checks that the pins reject
@@ -461,6 +464,44 @@ def test_compose_then_apply_equals_sequential_apply():
     np.testing.assert_array_equal(once, seq)
 
 
+# ------------------------------------------------------------ integrity
+
+xxhash = pytest.importorskip("xxhash")
+
+
+def test_xxh64_matches_library_every_short_length():
+    r = rng(12)
+    for n in range(0, 101):
+        b = r.integers(0, 256, size=n, dtype=np.uint8).tobytes()
+        for seed in (0, 1, 11456, (1 << 64) - 1):
+            assert oracle.xxh64(b, seed) == xxhash.xxh64(b, seed=seed).intdigest(), (n, seed)
+
+
+@pytest.mark.parametrize("n", [1000, 4096, 65_537, 1 << 20, 3 * (1 << 20) + 5])
+def test_xxh64_matches_library_long(n):
+    b = rng(n).integers(0, 256, size=n, dtype=np.uint8).tobytes()
+    assert oracle.xxh64(b, 7) == xxhash.xxh64(b, seed=7).intdigest()
+
+
+def test_hash_segments_are_per_piece_hashes():
+    b = rng(3).integers(0, 256, size=300_001, dtype=np.uint8).tobytes()
+    for seg in (32, 4096, 65_536, 1 << 20):
+        h = oracle.hash_segments(b, seg, seed=5)
+        want = [xxhash.xxh64(b[o:o + seg], seed=5).intdigest() for o in range(0, len(b), seg)]
+        assert h.tolist() == want
+    assert oracle.hash_segments(b"", 64).size == 0
+
+
+def test_xxh64_detects_any_single_bit_flip():
+    b = bytearray(rng(5).integers(0, 256, size=777, dtype=np.uint8).tobytes())
+    h0 = oracle.xxh64(bytes(b))
+    for pos in range(0, 777, 37):
+        for bit in (0, 7):
+            b[pos] ^= 1 << bit
+            assert oracle.xxh64(bytes(b)) != h0
+            b[pos] ^= 1 << bit
+
+
 # ---------------------------------------------------------------- mutants
 
 MUTANTS = {
@@ -485,6 +526,10 @@ MUTANTS = {
     # the oldest writer wins instead of the newest
     "compose_first_writer": ("        for (int32_t d = num_deltas - 1; d >= 0; --d) {",
                              "        for (int32_t d = 0; d < num_deltas; ++d) {"),
+    # a wrong rotation in the accumulator merge of XXH64
+    "xxh64_merge_rotation": ("acc = rotl64(a1, 1) + rotl64(a2, 7)", "acc = rotl64(a1, 1) + rotl64(a2, 8)"),
+    # the tail's 4-byte step skipped
+    "xxh64_no_word_tail": ("    if (left >= 4) {", "    if (left >= 4 && 0) {"),
     # a duplicate index stepped past in only one stream
     "compose_single_advance": ("                    have = 1;\n                }\n                ++pos[d];",
                                "                    have = 1;\n                    ++pos[d];\n                }"),
@@ -564,6 +609,15 @@ def _pins_pass(lib):
     if c != touched.size or not np.array_equal(oi[:c], touched) or \
             not np.array_equal(ov[:c], w[touched]):
         return False
+    # XXH64 against the independent library
+    lib.oracle_xxh64.argtypes = [P, U64, U64]
+    lib.oracle_xxh64.restype = U64
+    import xxhash as xx
+    for n in (0, 3, 7, 31, 32, 45, 100):
+        b = rng(n).integers(0, 256, size=n, dtype=np.uint8)
+        if lib.oracle_xxh64(b.ctypes.data if n else None, n, 9) != \
+                xx.xxh64(b.tobytes(), seed=9).intdigest():
+            return False
     return True
 
 
