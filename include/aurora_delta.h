@@ -276,6 +276,91 @@ delta_status_t delta_compose(const int64_t* const* idx_ptrs, const uint16_t* con
                              uint32_t* d_error_flag, void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
 
+/*
+ * Versioned delta checkpoints — Sec. 5.1: the trainer writes each step's
+ * delta as an immutable, versioned file with an integrity hash; Sec. 5.2:
+ * it travels as segments that are verified against that hash, and a worker
+ * activates it only onto its declared base version.
+ *
+ * Artifact layout (little-endian, offsets from delta_artifact_layout):
+ *   header        delta_artifact_header_t (128 bytes)
+ *   tensor table  num_tensors x {numel, first entry, first index byte}
+ *                 (3 x uint64 each)
+ *   index stream  idx_bytes: int64 global indices (DELTA_CODING_INT64) or
+ *                 gap + LEB128 with one segment per tensor
+ *                 (DELTA_CODING_LEB128)
+ *   value stream  count x 16-bit words (8-byte aligned start)
+ *   segment hashes  num_segments x uint64: XXH64 (seed = version) of each
+ *                 seg_bytes piece of [tensor table, segment hashes)
+ * The artifact hash is XXH64 of the segment hash table, seeded with the
+ * XXH64 (seed 0) of the header's first 80 bytes.  XXH64 follows Y. Collet's
+ * xxHash specification.
+ */
+typedef enum { DELTA_CODING_INT64 = 0, DELTA_CODING_LEB128 = 1 } delta_index_coding_t;
+
+#define DELTA_ARTIFACT_FORMAT 1
+
+typedef struct {
+  char magic[8];          /* "AURDELTA" (written by seal) */
+  uint32_t format;        /* DELTA_ARTIFACT_FORMAT (written by seal) */
+  uint32_t index_coding;  /* delta_index_coding_t */
+  uint64_t version;       /* the policy version this delta produces */
+  uint64_t base_version;  /* the version it must be applied onto */
+  uint64_t num_tensors;
+  uint64_t total_words;   /* words of the whole tensor list */
+  uint64_t count;         /* entries */
+  uint64_t idx_bytes;     /* bytes of the index stream */
+  uint64_t seg_bytes;     /* hash segment size: a multiple of 32, >= 32 */
+  uint64_t num_segments;  /* written by seal */
+  uint64_t hash;          /* written by seal */
+  uint64_t reserved[5];
+} delta_artifact_header_t;
+
+typedef struct {
+  uint64_t table, idx, val, hashes, total, num_segments;
+} delta_artifact_layout_t;
+
+/* Offsets and total size of an artifact (host only). */
+delta_status_t delta_artifact_layout(uint64_t num_tensors, uint64_t count, uint64_t idx_bytes,
+                                     uint64_t seg_bytes, delta_artifact_layout_t* out);
+
+/*
+ * XXH64 (seed) of each seg_bytes piece of the device buffer `data` (the last
+ * piece may be shorter) into d_hashes[ceil(nbytes / seg_bytes)].  data must
+ * be 8-byte aligned, seg_bytes a multiple of 32.
+ */
+delta_status_t delta_hash_segments(const void* data, uint64_t nbytes, uint64_t seg_bytes,
+                                   uint64_t seed, uint64_t* d_hashes, hipStream_t stream);
+
+/*
+ * delta_artifact_seal — the caller has written the tensor table, the index
+ * stream and the value stream into the device buffer d_artifact at the
+ * layout's offsets; seal writes the header (from *header: magic, format
+ * and num_segments are filled in) and the segment hash table, then the
+ * artifact hash.  d_artifact 8-byte aligned, artifact_bytes >= the
+ * layout's total.
+ */
+delta_status_t delta_artifact_seal(void* d_artifact, size_t artifact_bytes,
+                                   const delta_artifact_header_t* header, hipStream_t stream);
+
+/* Workspace bytes of delta_artifact_verify for this header. */
+size_t delta_artifact_verify_workspace_bytes(const delta_artifact_header_t* header);
+
+/*
+ * delta_artifact_verify — recomputes every segment hash and the artifact
+ * hash.  *header is the caller's host copy of the artifact's header (it
+ * fixes the layout; a header changed on the way fails the artifact hash).
+ *   d_bad_segments  device uint64: segments whose hash differs.
+ *   d_first_bad     nullable device uint64: the first such segment
+ *                   (UINT64_MAX if none).
+ *   d_header_bad    device uint32: 1 if the artifact hash differs.
+ */
+delta_status_t delta_artifact_verify(const void* d_artifact, size_t artifact_bytes,
+                                     const delta_artifact_header_t* header,
+                                     uint64_t* d_bad_segments, uint64_t* d_first_bad,
+                                     uint32_t* d_header_bad, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+
 /* Options of the chunked pipeline. */
 typedef struct {
   uint64_t chunk_elems; /* words of the global index space per chunk (> 0) */

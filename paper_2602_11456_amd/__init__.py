@@ -31,6 +31,8 @@ __all__ = [
     "delta_pipeline_staging_bytes", "MultiPlan", "delta_leb128_encode", "delta_leb128_decode",
     "delta_extract_pipelined_leb128", "delta_pipeline_leb128_staging_bytes", "chunk_segments",
     "delta_compose", "delta_compose_workspace_bytes", "delta_catch_up",
+    "delta_hash_segments", "delta_artifact_layout", "pack_artifact", "read_artifact_header",
+    "delta_artifact_verify", "activate_artifact",
 ]
 
 
@@ -524,3 +526,138 @@ def delta_extract_pipelined_leb128(prevs: Sequence[torch.Tensor], news: Sequence
     _check(status)
     return (h_bytes[:nbytes.value], h_val[:count.value], [int(c) for c in counts[:nchunks]],
             chunk)
+
+
+# ------------------------------------------------- versioned artifacts
+
+def delta_hash_segments(data: torch.Tensor, seg_bytes: int, seed: int = 0,
+                        stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """XXH64 (seed) of every ``seg_bytes`` piece of the bytes of a contiguous
+    GPU tensor (Sec. 5.2 segment integrity); uint64 hashes as int64."""
+    if not data.is_cuda or not data.is_contiguous():
+        raise ValueError("data must be a contiguous GPU tensor")
+    nbytes = data.numel() * data.element_size()
+    n = (nbytes + seg_bytes - 1) // seg_bytes
+    out = torch.empty(max(n, 1), dtype=torch.int64, device=data.device)
+    _check(library().delta_hash_segments(data.data_ptr(), nbytes, int(seg_bytes),
+                                         int(seed) & ((1 << 64) - 1), out.data_ptr(),
+                                         _stream(stream)))
+    return out[:n]
+
+
+def delta_artifact_layout(num_tensors: int, count: int, idx_bytes: int, seg_bytes: int) -> dict:
+    out = _abi.delta_artifact_layout_t()
+    _check(library().delta_artifact_layout(num_tensors, count, idx_bytes, seg_bytes,
+                                           ctypes.byref(out)))
+    return {n: int(getattr(out, n)) for n, _ in out._fields_}
+
+
+def pack_artifact(idx: torch.Tensor, val: torch.Tensor, tensor_offsets: torch.Tensor,
+                  numels: Sequence[int], version: int, base_version: int,
+                  coding: str = "int64", seg_bytes: int = 1 << 20,
+                  stream: Optional[torch.cuda.Stream] = None):
+    """A sealed delta checkpoint (Sec. 5.1) in GPU memory from
+    delta_extract_multi's output: header, tensor table, index stream (int64
+    or gap + LEB128 per tensor), values, segment hashes.  Returns the uint8
+    GPU tensor and the header."""
+    dev = idx.device
+    T = len(numels)
+    bases = [0]
+    for n in numels[:-1]:
+        bases.append(bases[-1] + int(n))
+    offs = tensor_offsets.to(torch.int64)
+    if coding == "leb128":
+        code, seg_starts = delta_leb128_encode(idx, offs.cpu().tolist(), bases, stream=stream)
+        byte_offs = seg_starts
+        idx_bytes = code.numel()
+        coding_id = _abi.DELTA_CODING_LEB128
+    elif coding == "int64":
+        code = idx.contiguous().view(torch.uint8)
+        byte_offs = offs * 8
+        idx_bytes = code.numel()
+        coding_id = _abi.DELTA_CODING_INT64
+    else:
+        raise ValueError("coding must be 'int64' or 'leb128'")
+    K = idx.numel()
+    L = delta_artifact_layout(T, K, idx_bytes, seg_bytes)
+    art = torch.zeros(L["total"], dtype=torch.uint8, device=dev)
+    table = torch.stack([torch.tensor(list(numels), dtype=torch.int64, device=dev),
+                         offs[:T], byte_offs[:T].to(dev)], dim=1).contiguous()
+    art[L["table"]:L["table"] + 24 * T].copy_(table.view(torch.uint8).reshape(-1))
+    art[L["idx"]:L["idx"] + idx_bytes].copy_(code)
+    art[L["val"]:L["val"] + 2 * K].copy_(val.contiguous().view(torch.uint8).reshape(-1))
+    h = _abi.delta_artifact_header_t()
+    h.index_coding = coding_id
+    h.version = int(version)
+    h.base_version = int(base_version)
+    h.num_tensors = T
+    h.total_words = sum(int(n) for n in numels)
+    h.count = K
+    h.idx_bytes = idx_bytes
+    h.seg_bytes = int(seg_bytes)
+    _check(library().delta_artifact_seal(art.data_ptr(), art.numel(), ctypes.byref(h),
+                                         _stream(stream)))
+    (stream or torch.cuda.current_stream()).synchronize()
+    return art, read_artifact_header(art)
+
+
+def read_artifact_header(art: torch.Tensor):
+    """The artifact's header (copied to the host)."""
+    h = _abi.delta_artifact_header_t()
+    raw = art[:ctypes.sizeof(h)].cpu().numpy().tobytes()
+    ctypes.memmove(ctypes.byref(h), raw, ctypes.sizeof(h))
+    return h
+
+
+def delta_artifact_verify(art: torch.Tensor, header=None,
+                          stream: Optional[torch.cuda.Stream] = None):
+    """Recomputes every segment hash and the artifact hash on the GPU.
+    Returns (segments that differ, first such segment or None, artifact
+    hash differs)."""
+    h = header if header is not None else read_artifact_header(art)
+    ws = _workspace(library().delta_artifact_verify_workspace_bytes(ctypes.byref(h)), art.device)
+    bad = torch.zeros(2, dtype=torch.int64, device=art.device)
+    hb = torch.zeros(1, dtype=torch.int32, device=art.device)
+    _check(library().delta_artifact_verify(art.data_ptr(), art.numel(), ctypes.byref(h),
+                                           bad.data_ptr(), bad[1:].data_ptr(), hb.data_ptr(),
+                                           ws.data_ptr(), ws.numel(), _stream(stream)))
+    (stream or torch.cuda.current_stream()).synchronize()
+    n_bad, first = bad.cpu().tolist()
+    return int(n_bad), (None if n_bad == 0 else int(first)), bool(hb.item())
+
+
+def activate_artifact(art: torch.Tensor, weights: Sequence[torch.Tensor], active_version: int,
+                      stream: Optional[torch.cuda.Stream] = None) -> int:
+    """Staged activation (Sec. 5.2): verify the artifact, refuse it unless
+    its base version is the active one, then apply it in place.  Returns
+    the new active version."""
+    h = read_artifact_header(art)
+    n_bad, first, header_bad = delta_artifact_verify(art, h, stream)
+    if n_bad or header_bad:
+        raise DeltaError(_abi.DELTA_ERR_INVALID_ARG,
+                         f"artifact fails its hashes ({n_bad} segments, first {first}; "
+                         f"header {'bad' if header_bad else 'ok'})")
+    if int(h.base_version) != int(active_version):
+        raise DeltaError(_abi.DELTA_ERR_VERSION,
+                         f"delta of version {h.version} is based on {h.base_version}, "
+                         f"active version is {active_version}")
+    if len(weights) != h.num_tensors:
+        raise ValueError("the artifact is for a different tensor list")
+    L = delta_artifact_layout(h.num_tensors, h.count, h.idx_bytes, h.seg_bytes)
+    T, K = int(h.num_tensors), int(h.count)
+    table = art[L["table"]:L["table"] + 24 * T].view(torch.int64).reshape(T, 3)
+    numels = table[:, 0].cpu().tolist()
+    if numels != [w.numel() for w in weights]:
+        raise ValueError("the artifact is for tensors of other sizes")
+    val = art[L["val"]:L["val"] + 2 * K].view(weights[0].dtype if weights else torch.bfloat16)
+    code = art[L["idx"]:L["idx"] + int(h.idx_bytes)]
+    if h.index_coding == _abi.DELTA_CODING_LEB128:
+        bases = [0]
+        for n in numels[:-1]:
+            bases.append(bases[-1] + n)
+        offs = table[:, 1].cpu().tolist() + [K]
+        idx = delta_leb128_decode(code, offs, bases, capacity=K, stream=stream)
+    else:
+        idx = code.view(torch.int64)
+    delta_apply_multi(weights, idx, val, check=True, stream=stream)
+    return int(h.version)

@@ -38,6 +38,32 @@ class delta_pipeline_opts_t(ctypes.Structure):
                 ("reserved", ctypes.c_int32)]
 
 
+DELTA_CODING_INT64 = 0
+DELTA_CODING_LEB128 = 1
+DELTA_ARTIFACT_FORMAT = 1
+
+
+class delta_artifact_header_t(ctypes.Structure):
+    _fields_ = [("magic", ctypes.c_char * 8),
+                ("format", ctypes.c_uint32),
+                ("index_coding", ctypes.c_uint32),
+                ("version", ctypes.c_uint64),
+                ("base_version", ctypes.c_uint64),
+                ("num_tensors", ctypes.c_uint64),
+                ("total_words", ctypes.c_uint64),
+                ("count", ctypes.c_uint64),
+                ("idx_bytes", ctypes.c_uint64),
+                ("seg_bytes", ctypes.c_uint64),
+                ("num_segments", ctypes.c_uint64),
+                ("hash", ctypes.c_uint64),
+                ("reserved", ctypes.c_uint64 * 5)]
+
+
+class delta_artifact_layout_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in ("table", "idx", "val", "hashes", "total",
+                                               "num_segments")]
+
+
 # name -> (restype, argtypes); every symbol the header declares
 SIGNATURES = {
     "delta_abi_version": (ctypes.c_int, []),
@@ -57,6 +83,12 @@ SIGNATURES = {
     "delta_leb128_decode": (STATUS, [P, U64, P, P, ctypes.c_uint32, P, U64, P, P, P, SZ, P]),
     "delta_compose_workspace_bytes": (SZ, [P, I32]),
     "delta_compose": (STATUS, [P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
+    "delta_artifact_layout": (STATUS, [U64, U64, U64, U64, ctypes.POINTER(delta_artifact_layout_t)]),
+    "delta_hash_segments": (STATUS, [P, U64, U64, U64, P, P]),
+    "delta_artifact_seal": (STATUS, [P, SZ, ctypes.POINTER(delta_artifact_header_t), P]),
+    "delta_artifact_verify_workspace_bytes": (SZ, [ctypes.POINTER(delta_artifact_header_t)]),
+    "delta_artifact_verify": (STATUS, [P, SZ, ctypes.POINTER(delta_artifact_header_t), P, P, P,
+                                       P, SZ, P]),
     "delta_pipeline_staging_bytes": (SZ, [P, I32, ctypes.POINTER(delta_pipeline_opts_t)]),
     "delta_extract_pipelined": (STATUS, [P, P, P, I32, ctypes.POINTER(delta_pipeline_opts_t), P,
                                          P, SZ, P, P, U64, P]),

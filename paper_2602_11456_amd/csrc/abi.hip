@@ -12,6 +12,7 @@
 #include "aurora_delta.h"
 #include "delta_internal.h"
 #include "leb128.h"
+#include "hash.h"
 
 using namespace aurora;
 
@@ -423,6 +424,96 @@ delta_status_t delta_compose(const int64_t* const* idx_ptrs, const uint16_t* con
   hipError_t e = launch_compose_chain(idx_ptrs, val_ptrs, counts, num_deltas, out_idx, out_val,
                                       capacity, d_count, d_error_flag, (char*)workspace, stream);
   if (e != hipSuccess) return hip_fail(e, "compose launch");
+  return ok();
+}
+
+static bool layout_of(const delta_artifact_header_t* h, ArtifactLayout* L) {
+  if (!h || h->seg_bytes < 32 || h->seg_bytes % 32 || h->num_tensors > (1ull << 32) ||
+      h->count > (1ull << 56) || h->idx_bytes > (1ull << 60))
+    return false;
+  *L = artifact_layout(h->num_tensors, h->count, h->idx_bytes, h->seg_bytes);
+  return true;
+}
+
+delta_status_t delta_artifact_layout(uint64_t num_tensors, uint64_t count, uint64_t idx_bytes,
+                                     uint64_t seg_bytes, delta_artifact_layout_t* out) {
+  if (!out) return fail(DELTA_ERR_INVALID_ARG, "out is NULL");
+  delta_artifact_header_t h;
+  memset(&h, 0, sizeof(h));
+  h.num_tensors = num_tensors;
+  h.count = count;
+  h.idx_bytes = idx_bytes;
+  h.seg_bytes = seg_bytes;
+  ArtifactLayout L;
+  if (!layout_of(&h, &L))
+    return fail(DELTA_ERR_INVALID_ARG, "seg_bytes must be a multiple of 32; sizes too large");
+  *out = {L.table, L.idx, L.val, L.hashes, L.total, L.num_segments};
+  return ok();
+}
+
+delta_status_t delta_hash_segments(const void* data, uint64_t nbytes, uint64_t seg_bytes,
+                                   uint64_t seed, uint64_t* d_hashes, hipStream_t stream) {
+  if (seg_bytes < 32 || seg_bytes % 32)
+    return fail(DELTA_ERR_INVALID_ARG, "seg_bytes must be a positive multiple of 32");
+  if (nbytes > 0 && (!data || !d_hashes)) return fail(DELTA_ERR_INVALID_ARG, "NULL pointer");
+  if ((uintptr_t)data % 8 || (uintptr_t)d_hashes % 8)
+    return fail(DELTA_ERR_INVALID_ARG, "data and d_hashes must be 8-byte aligned");
+  hipError_t e = launch_hash_segments((const uint8_t*)data, nbytes, seg_bytes, seed, d_hashes,
+                                      stream);
+  if (e != hipSuccess) return hip_fail(e, "hash launch");
+  return ok();
+}
+
+delta_status_t delta_artifact_seal(void* d_artifact, size_t artifact_bytes,
+                                   const delta_artifact_header_t* header, hipStream_t stream) {
+  ArtifactLayout L;
+  if (!layout_of(header, &L))
+    return fail(DELTA_ERR_INVALID_ARG, "bad header (seg_bytes a multiple of 32, sizes)");
+  if (header->index_coding > DELTA_CODING_LEB128)
+    return fail(DELTA_ERR_INVALID_ARG, "unknown index coding %u", header->index_coding);
+  if (!d_artifact || (uintptr_t)d_artifact % 8)
+    return fail(DELTA_ERR_INVALID_ARG, "artifact must be a non-NULL, 8-byte aligned buffer");
+  if (artifact_bytes < L.total)
+    return fail(DELTA_ERR_CAPACITY, "artifact needs %llu bytes, buffer has %zu",
+                (unsigned long long)L.total, artifact_bytes);
+  delta_artifact_header_t h = *header;
+  memcpy(h.magic, "AURDELTA", 8);
+  h.format = DELTA_ARTIFACT_FORMAT;
+  h.num_segments = L.num_segments;
+  h.hash = 0;
+  hipError_t e = launch_artifact_seal((uint8_t*)d_artifact, L, h, stream);
+  if (e != hipSuccess) return hip_fail(e, "seal launch");
+  return ok();
+}
+
+size_t delta_artifact_verify_workspace_bytes(const delta_artifact_header_t* header) {
+  ArtifactLayout L;
+  if (!layout_of(header, &L)) return 0;
+  return align_up(8 * (L.num_segments ? L.num_segments : 1));
+}
+
+delta_status_t delta_artifact_verify(const void* d_artifact, size_t artifact_bytes,
+                                     const delta_artifact_header_t* header,
+                                     uint64_t* d_bad_segments, uint64_t* d_first_bad,
+                                     uint32_t* d_header_bad, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+  ArtifactLayout L;
+  if (!layout_of(header, &L)) return fail(DELTA_ERR_INVALID_ARG, "bad header");
+  if (memcmp(header->magic, "AURDELTA", 8) || header->format != DELTA_ARTIFACT_FORMAT)
+    return fail(DELTA_ERR_VERSION, "not an artifact of format %d", DELTA_ARTIFACT_FORMAT);
+  if (header->num_segments != L.num_segments)
+    return fail(DELTA_ERR_INVALID_ARG, "header says %llu segments, layout %llu",
+                (unsigned long long)header->num_segments, (unsigned long long)L.num_segments);
+  if (!d_artifact || (uintptr_t)d_artifact % 8 || artifact_bytes < L.total)
+    return fail(DELTA_ERR_INVALID_ARG, "artifact buffer too small or misaligned");
+  if (!d_bad_segments || !d_header_bad) return fail(DELTA_ERR_INVALID_ARG, "NULL result");
+  delta_status_t st =
+      check_workspace(workspace, workspace_bytes, delta_artifact_verify_workspace_bytes(header));
+  if (st != DELTA_OK) return st;
+  hipError_t e = launch_artifact_verify((const uint8_t*)d_artifact, L, header->seg_bytes,
+                                        header->version, (uint64_t*)workspace, d_bad_segments,
+                                        d_first_bad, d_header_bad, stream);
+  if (e != hipSuccess) return hip_fail(e, "verify launch");
   return ok();
 }
 

@@ -235,3 +235,34 @@ def test_compose_validation(lib):
     nulls = (P * 3)(None, None, FAKE)
     assert C(nulls, val, counts, 3, FAKE, FAKE, 10, FAKE, None, FAKE, ws_need, None) == \
         _abi.DELTA_ERR_INVALID_ARG   # delta 0 has entries but no pointer
+
+
+def test_artifact_header_and_layout(lib):
+    assert ctypes.sizeof(_abi.delta_artifact_header_t) == 128
+    assert _abi.delta_artifact_header_t.hash.offset == 80
+    out = _abi.delta_artifact_layout_t()
+    assert lib.delta_artifact_layout(3, 10, 37, 64, ctypes.byref(out)) == _abi.DELTA_OK
+    assert out.table == 128 and out.idx == 128 + 72
+    assert out.val == (out.idx + 37 + 7) // 8 * 8
+    assert out.hashes == (out.val + 20 + 7) // 8 * 8
+    hashed = out.hashes - out.table
+    assert out.num_segments == -(-hashed // 64)
+    assert out.total == out.hashes + 8 * out.num_segments
+    assert lib.delta_artifact_layout(3, 10, 37, 48, ctypes.byref(out)) == \
+        _abi.DELTA_ERR_INVALID_ARG   # not a multiple of 32
+    assert lib.delta_hash_segments(FAKE, 100, 40, 0, FAKE, None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_hash_segments(FAKE + 4, 100, 64, 0, FAKE, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # misaligned data
+    h = _abi.delta_artifact_header_t()
+    h.seg_bytes = 64
+    h.count = 10
+    h.num_tensors = 3
+    h.idx_bytes = 37
+    assert lib.delta_artifact_seal(FAKE, 16, ctypes.byref(h), None) == _abi.DELTA_ERR_CAPACITY
+    h.index_coding = 9
+    assert lib.delta_artifact_seal(FAKE, 1 << 20, ctypes.byref(h), None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    # verify wants a sealed header
+    h.index_coding = 0
+    assert lib.delta_artifact_verify(FAKE, 1 << 20, ctypes.byref(h), FAKE, None, FAKE, FAKE,
+                                     1 << 20, None) == _abi.DELTA_ERR_VERSION
