@@ -325,6 +325,32 @@ def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
     }
 
 
+def hash_measurement(ad, buf, stream, reps):
+    """XXH64 segment hashes (Sec. 5.2 integrity) of the extracted delta's
+    bytes, timed with HIP events, for two segment sizes."""
+    import torch
+    lib = ad.library()
+    nbytes = buf.numel()
+    res = {"workload": f"XXH64 segments of the {nbytes}-byte (idx, val) streams of the delta"}
+    for seg in (1 << 20, 1 << 16):
+        n = (nbytes + seg - 1) // seg
+        out = torch.empty(n, dtype=torch.int64, device=buf.device)
+        h = stream.cuda_stream
+        call = lambda: lib.delta_hash_segments(buf.data_ptr(), nbytes, seg, 1, out.data_ptr(), h)
+        call()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+        for e0, e1 in ev:
+            e0.record(stream)
+            call()
+            e1.record(stream)
+        stream.synchronize()
+        t = sorted(e0.elapsed_time(e1) for e0, e1 in ev)[reps // 2]
+        res[f"seg_{seg}"] = {"ms": round(t, 4), "GBps": round(nbytes / (t / 1e3) / 1e9, 1),
+                             "segments": n}
+    return res
+
+
 def _prefix(xs):
     s = 0
     for x in xs:
@@ -476,6 +502,10 @@ def main():
     }
     result["leb128"] = leb128_measurement(ad, out_idx[:K], d_offs, plan.numels, stream,
                                           args.steps)
+    # the delta's two streams as one byte buffer, as an artifact holds them
+    payload = torch.cat([out_idx[:K].view(torch.uint8), out_val[:K].view(torch.uint8)])
+    result["hash"] = hash_measurement(ad, payload, stream, args.steps)
+    del payload
     result["compose"] = compose_measurement(ad, rollout, N, K, stream, max(args.steps // 2, 3))
     if args.copy_calibration > 0:
         n = args.copy_calibration // 2

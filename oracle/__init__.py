@@ -268,3 +268,18 @@ def hash_segments(data, seg_bytes: int, seed: int = 0) -> np.ndarray:
     if n:
         _load().oracle_hash_segments(_ptr(b), b.size, seg_bytes, seed, _ptr(out))
     return out[:n].copy()
+
+
+def extract_fused(prevs, news, sources, target_numels, capacity=None):
+    """Sec. 5.1 fused inference names: each fused tensor is its blocks
+    stacked (block t's flat words at word offset ``sources[t][1]`` of
+    target ``sources[t][0]``); the delta is ``extract_multi`` over the
+    fused tensors in target order.  Returns (idx, val, target_offsets,
+    true count)."""
+    fp = [np.zeros(int(n), dtype=np.uint16) for n in target_numels]
+    fq = [np.zeros(int(n), dtype=np.uint16) for n in target_numels]
+    for (f, off), p, q in zip(sources, prevs, news):
+        p = _u16(p)
+        fp[f][off:off + p.size] = p
+        fq[f][off:off + p.size] = _u16(q)
+    return extract_multi(fp, fq, capacity)

@@ -53,6 +53,9 @@ QWEN3 = {
                      head_dim=128, mlp=12288, vocab=151936, tied=False),
     "qwen3-14b": dict(layers=40, hidden=5120, q_heads=40, kv_heads=8,
                       head_dim=128, mlp=17408, vocab=151936, tied=False),
+    # the same structure at toy sizes, for tests
+    "qwen3-tiny": dict(layers=2, hidden=64, q_heads=4, kv_heads=2,
+                       head_dim=16, mlp=96, vocab=500, tied=False),
 }
 
 NORM_KINDS = ("input_layernorm", "q_norm", "k_norm",
@@ -83,6 +86,50 @@ def qwen3_tensor_table(model: str) -> List[Tuple[str, Tuple[int, ...]]]:
     if not c["tied"]:
         out.append(("lm_head.weight", (c["vocab"], h)))
     return out
+
+
+def qwen3_fused_layout(model: str):
+    """The inference engine's fused parameter list (Sec. 5.1): per layer
+    ``qkv_proj`` stacks the rows of q, k and v and ``gate_up_proj`` those of
+    gate and up; every other tensor keeps its own name.  Target order:
+    ``embed_tokens``; per layer ``qkv_proj, o_proj, q_norm, k_norm,
+    gate_up_proj, down_proj, input_layernorm, post_attention_layernorm``;
+    ``norm``; ``lm_head``.
+
+    Returns ``(targets, sources)``: ``targets`` is a list of ``(name,
+    numel)`` in target order, ``sources[t] = (target index, word offset of
+    its block)`` for every tensor of ``qwen3_tensor_table`` in its order.
+    Stacking rows of row-major matrices puts each block's flat words at a
+    fixed word offset, so a block offset is a sum of numels."""
+    table = qwen3_tensor_table(model)
+    size = {name: numel(shape) for name, shape in table}
+    c = QWEN3[model]
+    targets = [("model.embed_tokens.weight", size["model.embed_tokens.weight"])]
+    where = {"model.embed_tokens.weight": (0, 0)}
+    for layer in range(c["layers"]):
+        p = f"model.layers.{layer}."
+        q, k, v = (p + f"self_attn.{x}_proj.weight" for x in "qkv")
+        g, u = p + "mlp.gate_proj.weight", p + "mlp.up_proj.weight"
+
+        def add(name, parts):
+            off = 0
+            for part in parts:
+                where[part] = (len(targets), off)
+                off += size[part]
+            targets.append((name, off))
+
+        add(p + "self_attn.qkv_proj.weight", [q, k, v])
+        for single in ("self_attn.o_proj", "self_attn.q_norm", "self_attn.k_norm"):
+            add(p + single + ".weight", [p + single + ".weight"])
+        add(p + "mlp.gate_up_proj.weight", [g, u])
+        for single in ("mlp.down_proj", "input_layernorm", "post_attention_layernorm"):
+            add(p + single + ".weight", [p + single + ".weight"])
+    where["model.norm.weight"] = (len(targets), 0)
+    targets.append(("model.norm.weight", size["model.norm.weight"]))
+    if not c["tied"]:
+        where["lm_head.weight"] = (len(targets), 0)
+        targets.append(("lm_head.weight", size["lm_head.weight"]))
+    return targets, [where[name] for name, _ in table]
 
 
 def is_norm(name: str) -> bool:

@@ -82,6 +82,29 @@ def round_trip(ws, idx, val, label):
     say(label, "apply round trip ok")
 
 
+def artifact_full(ws, idx, val, offs, label):
+    """A sealed LEB128 artifact of the whole set: verifies, its segment
+    hashes equal the oracle's on sampled segments, and activating it onto a
+    copy of prev gives new."""
+    art, h = ad.pack_artifact(idx, val, offs, ws.numels, version=2, base_version=1,
+                              coding="leb128", seg_bytes=1 << 20)
+    assert ad.delta_artifact_verify(art, h) == (0, None, False), label
+    L = ad.delta_artifact_layout(h.num_tensors, h.count, h.idx_bytes, h.seg_bytes)
+    stored = art[L["hashes"]:L["total"]].view(torch.int64).cpu().numpy().view(np.uint64)
+    nseg = int(h.num_segments)
+    for s in sorted({0, 1, nseg // 2, nseg - 1}):
+        lo = L["table"] + s * (1 << 20)
+        hi = min(lo + (1 << 20), L["hashes"])
+        piece = art[lo:hi].cpu().numpy()
+        assert stored[s] == oracle.xxh64(piece.tobytes(), seed=2), (label, s)
+    roll = [p.clone() for p in ws.prev]
+    assert ad.activate_artifact(art, roll, active_version=1) == 2
+    for r, q in zip(roll, ws.new):
+        assert torch.equal(r.view(torch.int16), q.view(torch.int16)), label
+    del roll, art
+    say(label, "artifact ok:", int(h.num_segments), "segments")
+
+
 def leb128_full(ws, idx, offs, label):
     """Gap + LEB128 code of the whole set's indices with one segment per
     tensor: decodes to the indices; sampled tensors' segments equal the
@@ -130,6 +153,7 @@ def test_qwen3_8b_clustered():
     assert int(tile_hist.max()) > 5 * 82
     round_trip(ws, idx, val, "qwen3-8b clustered")
     leb128_full(ws, idx, offs, "qwen3-8b clustered")
+    artifact_full(ws, idx, val, offs, "qwen3-8b clustered")
 
 
 def test_qwen3_14b_pipeline():

@@ -464,6 +464,47 @@ def test_compose_then_apply_equals_sequential_apply():
     np.testing.assert_array_equal(once, seq)
 
 
+# ---------------------------------------------------- fused inference layout
+
+def test_fused_equals_multi_over_stacked_tensors():
+    # Sec. 5.1: q/k/v stack into qkv_proj, gate/up into gate_up_proj; the
+    # fused delta must be extract_multi over the tensors stacked by torch.cat
+    from paper_2602_11456_amd import synth
+    table = synth.qwen3_tensor_table("qwen3-tiny")
+    targets, sources = synth.qwen3_fused_layout("qwen3-tiny")
+    r = rng(21)
+    prevs, news = [], []
+    for i, (_, shape) in enumerate(table):
+        p, q, _ = random_pair(synth.numel(shape), 0.05, seed=500 + i)
+        prevs.append(p.reshape(shape))
+        news.append(q.reshape(shape))
+    name_of = [name for name, _ in table]
+
+    def stacked(arrs):
+        out = []
+        for tname, _ in targets:
+            base = tname.replace("qkv_proj", "{}_proj").replace("gate_up_proj", "{}_proj")
+            if "qkv_proj" in tname:
+                parts = [base.format(x) for x in "qkv"]
+            elif "gate_up_proj" in tname:
+                parts = [base.format(x) for x in ("gate", "up")]
+            else:
+                parts = [tname]
+            ts = [torch.from_numpy(arrs[name_of.index(pn)].view(np.int16)) for pn in parts]
+            out.append(torch.cat(ts, dim=0).numpy().view(np.uint16).reshape(-1))
+        return out
+
+    ref_idx, ref_val, ref_offs, ref_cnt = oracle.extract_multi(stacked(prevs), stacked(news))
+    idx, val, offs, cnt = oracle.extract_fused([p.reshape(-1) for p in prevs],
+                                               [q.reshape(-1) for q in news], sources,
+                                               [n for _, n in targets])
+    assert cnt == ref_cnt
+    np.testing.assert_array_equal(idx, ref_idx)
+    np.testing.assert_array_equal(val, ref_val)
+    np.testing.assert_array_equal(offs, ref_offs)
+    assert r is not None
+
+
 # ------------------------------------------------------------ integrity
 
 xxhash = pytest.importorskip("xxhash")

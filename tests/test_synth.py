@@ -25,7 +25,7 @@ def test_tensor_tables(model, T, N, norm_elems):
 
 
 def test_every_tensor_fits_int32_locally_but_not_globally():
-    for model in synth.QWEN3:
+    for model in ("qwen3-4b", "qwen3-8b", "qwen3-14b"):
         table = synth.qwen3_tensor_table(model)
         assert max(synth.numel(s) for _, s in table) - 1 <= 2**31 - 1
         assert sum(synth.numel(s) for _, s in table) - 1 > 2**31 - 1
@@ -91,3 +91,27 @@ def test_prev_scale():
     prev, _, _ = synth.make_pair(200_000, 0.0, seed=3)
     s = prev.float().std().item()
     assert 0.019 < s < 0.021
+
+
+@pytest.mark.parametrize("model", ["qwen3-tiny", "qwen3-4b", "qwen3-8b", "qwen3-14b"])
+def test_fused_layout_tiles_every_target(model):
+    table = synth.qwen3_tensor_table(model)
+    targets, sources = synth.qwen3_fused_layout(model)
+    assert len(sources) == len(table)
+    c = synth.QWEN3[model]
+    # per layer 11 tensors become 8 targets
+    assert len(targets) == len(table) - 3 * c["layers"]
+    blocks = {}
+    for (name, shape), (f, off) in zip(table, sources):
+        blocks.setdefault(f, []).append((off, synth.numel(shape)))
+    for f, (tname, n) in enumerate(targets):
+        parts = sorted(blocks[f])
+        pos = 0
+        for off, size in parts:
+            assert off == pos, (tname, parts)
+            pos += size
+        assert pos == n, tname
+    qkv = [n for name, n in targets if name.endswith("qkv_proj.weight")]
+    q = c["q_heads"] * c["head_dim"]
+    kv = c["kv_heads"] * c["head_dim"]
+    assert qkv and all(n == (q + 2 * kv) * c["hidden"] for n in qkv)
