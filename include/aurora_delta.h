@@ -150,6 +150,34 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
                                    size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * delta_extract_fused — Sec. 5.1: the delta written under the inference
+ * engine's fused names, where blocks of several training tensors are
+ * stacked into one (q, k, v rows into qkv_proj; gate, up into
+ * gate_up_proj) by adding a fixed block offset to each block's linear
+ * indices.  The result equals delta_extract_multi over the fused tensors
+ * (each the concatenation of its blocks' words) in target order, without
+ * building them: indices are global over the targets (target f starts at
+ * the sum of target_numels before it), d_target_offsets (nullable,
+ * num_targets + 1) counts the entries before each target, so
+ * delta_apply_multi on the fused weights applies it directly.
+ *   prev_ptrs, next_ptrs, numels  host arrays: the training tensors.
+ *   target, block_offset  host arrays per training tensor: its fused
+ *                 tensor and the word offset of its block there.
+ *   target_numels host array: words of every fused tensor.  The blocks
+ *                 must tile every target exactly (DELTA_ERR_INVALID_ARG
+ *                 otherwise).
+ *   workspace     delta_extract_multi_workspace_bytes(numels, num_tensors).
+ */
+delta_status_t delta_extract_fused(const uint16_t* const* prev_ptrs,
+                                   const uint16_t* const* next_ptrs, const uint64_t* numels,
+                                   int32_t num_tensors, const int32_t* target,
+                                   const uint64_t* block_offset, const uint64_t* target_numels,
+                                   int32_t num_targets, int64_t* out_idx, uint16_t* out_val,
+                                   uint64_t capacity, uint64_t* d_count,
+                                   uint64_t* d_target_offsets, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
+/*
  * delta_apply — Sec. 5.1 / 5.2: weights[idx[k]] = val[k] for k < count,
  * in place.  Indices must be distinct (any order); entries with an index
  * outside [0, numel) are skipped and set *d_error_flag (if not NULL) to a

@@ -32,7 +32,7 @@ __all__ = [
     "delta_extract_pipelined_leb128", "delta_pipeline_leb128_staging_bytes", "chunk_segments",
     "delta_compose", "delta_compose_workspace_bytes", "delta_catch_up",
     "delta_hash_segments", "delta_artifact_layout", "pack_artifact", "read_artifact_header",
-    "delta_artifact_verify", "activate_artifact",
+    "delta_artifact_verify", "activate_artifact", "delta_extract_fused",
 ]
 
 
@@ -348,6 +348,42 @@ def delta_catch_up(weights: Sequence[torch.Tensor],
             delta_apply_multi(weights, idx, val, check=True, stream=stream)
 
 
+# ---------------------------------------------------------------- fused
+
+def delta_extract_fused(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tensor],
+                        sources: Sequence[Tuple[int, int]], target_numels: Sequence[int],
+                        capacity: Optional[int] = None,
+                        stream: Optional[torch.cuda.Stream] = None):
+    """The delta under fused inference names (Sec. 5.1): ``sources[t] =
+    (target, block word offset)`` for every training tensor.  Returns
+    global int64 indices over the fused targets, the new words and the
+    per-target entry offsets (num_targets + 1).  Synchronises."""
+    plan = MultiPlan(prevs, news)
+    dev = plan.device
+    T, F = plan.T, len(target_numels)
+    tgt = (ctypes.c_int32 * max(T, 1))(*[int(f) for f, _ in sources])
+    boff = _u64_array([off for _, off in sources])
+    tn = _u64_array(target_numels)
+    ws = _workspace(plan.workspace_bytes, dev)
+    cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    offs = torch.zeros(F + 1, dtype=torch.int64, device=dev)
+    cap = _default_capacity(plan.total) if capacity is None else int(capacity)
+    for _ in range(2):
+        idx = torch.empty(max(cap, 1), dtype=torch.int64, device=dev)
+        val = torch.empty(max(cap, 1), dtype=prevs[0].dtype if prevs else torch.bfloat16,
+                          device=dev)
+        _check(library().delta_extract_fused(
+            plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, T, tgt, boff, tn, F,
+            idx.data_ptr(), val.data_ptr(), cap, cnt.data_ptr(), offs.data_ptr(),
+            ws.data_ptr(), ws.numel(), _stream(stream)))
+        (stream or torch.cuda.current_stream()).synchronize()
+        k = int(cnt.item())
+        if k <= cap:
+            return idx[:k], val[:k], offs
+        cap = k
+    raise AssertionError("count changed between two runs on the same input")
+
+
 # -------------------------------------------------------------- LEB128
 
 def _segs(seg_offsets, seg_bases, device):
@@ -554,7 +590,7 @@ def delta_artifact_layout(num_tensors: int, count: int, idx_bytes: int, seg_byte
 
 def pack_artifact(idx: torch.Tensor, val: torch.Tensor, tensor_offsets: torch.Tensor,
                   numels: Sequence[int], version: int, base_version: int,
-                  coding: str = "int64", seg_bytes: int = 1 << 20,
+                  coding: str = "int64", seg_bytes: int = 1 << 14,
                   stream: Optional[torch.cuda.Stream] = None):
     """A sealed delta checkpoint (Sec. 5.1) in GPU memory from
     delta_extract_multi's output: header, tensor table, index stream (int64

@@ -6,6 +6,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -247,6 +248,68 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
     return fail(DELTA_ERR_INDEX_OVERFLOW, "total size exceeds int64");
   return enqueue_extract(slices.data(), slices.size(), (uint32_t)num_tensors, true, out_idx,
                          out_val, capacity, d_count, d_tensor_offsets, workspace,
+                         workspace_bytes, stream);
+}
+
+delta_status_t delta_extract_fused(const uint16_t* const* prev_ptrs,
+                                   const uint16_t* const* next_ptrs, const uint64_t* numels,
+                                   int32_t num_tensors, const int32_t* target,
+                                   const uint64_t* block_offset, const uint64_t* target_numels,
+                                   int32_t num_targets, int64_t* out_idx, uint16_t* out_val,
+                                   uint64_t capacity, uint64_t* d_count,
+                                   uint64_t* d_target_offsets, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
+  if (num_tensors < 0 || num_targets < 0)
+    return fail(DELTA_ERR_INVALID_ARG, "negative tensor count");
+  if (num_tensors > 0 && (!prev_ptrs || !next_ptrs || !numels || !target || !block_offset))
+    return fail(DELTA_ERR_INVALID_ARG, "tensor arrays are NULL");
+  if (num_targets > 0 && !target_numels)
+    return fail(DELTA_ERR_INVALID_ARG, "target_numels is NULL");
+  if (!d_count) return fail(DELTA_ERR_INVALID_ARG, "d_count is NULL");
+  if (capacity > 0 && (!out_idx || !out_val))
+    return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val is NULL with capacity %llu",
+                (unsigned long long)capacity);
+  // global base of every target
+  std::vector<uint64_t> tbase(num_targets + 1, 0);
+  for (int32_t f = 0; f < num_targets; ++f) {
+    if (tbase[f] + target_numels[f] < tbase[f])
+      return fail(DELTA_ERR_INVALID_ARG, "total size overflows");
+    tbase[f + 1] = tbase[f] + target_numels[f];
+  }
+  if (tbase[num_targets] > 0 && tbase[num_targets] - 1 > 0x7FFFFFFFFFFFFFFFull)
+    return fail(DELTA_ERR_INDEX_OVERFLOW, "total size exceeds int64");
+  std::vector<SliceIn> slices;
+  slices.reserve(num_tensors);
+  for (int32_t t = 0; t < num_tensors; ++t) {
+    const int32_t f = target[t];
+    if (f < 0 || f >= num_targets)
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: target %d out of range", t, f);
+    if (numels[t] > 0 && (!prev_ptrs[t] || !next_ptrs[t]))
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: NULL pointer", t);
+    if (odd(prev_ptrs[t]) || odd(next_ptrs[t]))
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: not 2-byte aligned", t);
+    if (block_offset[t] > target_numels[f] || numels[t] > target_numels[f] - block_offset[t])
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: block [%llu, +%llu) outside target %d", t,
+                  (unsigned long long)block_offset[t], (unsigned long long)numels[t], f);
+    slices.push_back({prev_ptrs[t], next_ptrs[t], numels[t], tbase[f] + block_offset[t],
+                      (uint32_t)f});
+  }
+  // output order is the fused index order: blocks sorted by their base
+  std::stable_sort(slices.begin(), slices.end(),
+                   [](const SliceIn& x, const SliceIn& y) { return x.base < y.base; });
+  // the blocks must tile every target exactly (no gap, no overlap)
+  uint64_t pos = 0;
+  for (const SliceIn& sl : slices) {
+    if (sl.base != pos)
+      return fail(DELTA_ERR_INVALID_ARG, "blocks leave a gap or overlap at fused word %llu",
+                  (unsigned long long)pos);
+    pos += sl.n;
+  }
+  if (pos != tbase[num_targets])
+    return fail(DELTA_ERR_INVALID_ARG, "blocks cover %llu of %llu fused words",
+                (unsigned long long)pos, (unsigned long long)tbase[num_targets]);
+  return enqueue_extract(slices.data(), slices.size(), (uint32_t)num_targets, true, out_idx,
+                         out_val, capacity, d_count, d_target_offsets, workspace,
                          workspace_bytes, stream);
 }
 

@@ -266,3 +266,24 @@ def test_artifact_header_and_layout(lib):
     h.index_coding = 0
     assert lib.delta_artifact_verify(FAKE, 1 << 20, ctypes.byref(h), FAKE, None, FAKE, FAKE,
                                      1 << 20, None) == _abi.DELTA_ERR_VERSION
+
+
+def test_fused_validation(lib):
+    P = ctypes.c_void_p
+    ptrs = (P * 2)(FAKE, FAKE)
+    numels = (ctypes.c_uint64 * 2)(10, 6)
+    target = (ctypes.c_int32 * 2)(0, 0)
+    ws = FAKE
+    F = lib.delta_extract_fused
+    def call(boff, tn, nt=1, tgt=target):
+        return F(ptrs, ptrs, numels, 2, tgt, (ctypes.c_uint64 * 2)(*boff),
+                 (ctypes.c_uint64 * max(nt, 1))(*tn), nt, FAKE, FAKE, 16, FAKE, None, ws,
+                 1 << 20, None)
+    assert call([0, 9], [16]) == _abi.DELTA_ERR_INVALID_ARG      # overlap
+    assert b"gap or overlap" in lib.delta_last_error()
+    assert call([0, 11], [17]) == _abi.DELTA_ERR_INVALID_ARG     # gap
+    assert call([0, 10], [17]) == _abi.DELTA_ERR_INVALID_ARG     # target not covered
+    assert b"cover" in lib.delta_last_error()
+    assert call([0, 12], [16]) == _abi.DELTA_ERR_INVALID_ARG     # block outside target
+    bad_t = (ctypes.c_int32 * 2)(0, 2)
+    assert call([0, 0], [10, 6], nt=2, tgt=bad_t) == _abi.DELTA_ERR_INVALID_ARG

@@ -204,3 +204,34 @@ def test_compose_chain_full_index_space():
     assert out_i.numel() == ref_n
     np.testing.assert_array_equal(out_i.cpu().numpy(), ref_i)
     np.testing.assert_array_equal(out_v.view(torch.int16).cpu().numpy().view(np.uint16), ref_v)
+
+
+def test_qwen3_8b_fused_layout():
+    ws = synth.make_weight_set("qwen3-8b", 0.01, seed=synth.config_seed(3), device=DEV)
+    targets, sources = synth.qwen3_fused_layout("qwen3-8b")
+    tn = [n for _, n in targets]
+    idx, val, offs = ad.delta_extract_fused(ws.prev, ws.new, sources, tn)
+    torch.cuda.synchronize()
+    say("qwen3-8b fused:", idx.numel(), "entries over", len(targets), "targets")
+    assert idx.numel() == ws.total_planted
+    if idx.numel() > 1:
+        assert bool((idx[1:] > idx[:-1]).all())
+    offs_h = offs.cpu().numpy()
+    want = [0] * len(targets)
+    for (f, _), k in zip(sources, ws.planted):
+        want[f] += k
+    np.testing.assert_array_equal(np.diff(offs_h), want)
+    tbase = np.concatenate([[0], np.cumsum(tn)])
+    # sampled targets against the oracle on their stacked blocks
+    members = {}
+    for t, (f, off) in enumerate(sources):
+        members.setdefault(f, []).append((off, t))
+    for f in sorted({0, 1, 5, 4, len(targets) // 2, len(targets) - 1}):
+        parts = [t for _, t in sorted(members[f])]
+        p = np.concatenate([host_u16(ws.prev[t]) for t in parts])
+        q = np.concatenate([host_u16(ws.new[t]) for t in parts])
+        r_idx, r_val, r_cnt = oracle.extract(p, q)
+        a, b = int(offs_h[f]), int(offs_h[f + 1])
+        assert b - a == r_cnt, targets[f][0]
+        np.testing.assert_array_equal(idx[a:b].cpu().numpy() - tbase[f], r_idx)
+        np.testing.assert_array_equal(host_u16(val[a:b]), r_val)
