@@ -54,6 +54,9 @@ def parse():
                     help="skip the chunked extract -> pinned host pipeline measurement "
                          "(Qwen3-14B-shaped set)")
     ap.add_argument("--pipeline-reps", type=int, default=5)
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time only the headline step (extract + apply); skip the LEB128, "
+                         "hash, fused-layout and delta-chain measurements")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after timing, copy BYTES device-to-device three times (a known "
                          "traffic reference for hardware counters)")
@@ -398,6 +401,23 @@ def _prefix(xs):
         yield s
 
 
+def extras(args, ad, synth, ws, rollout, plan, out_idx, out_val, d_offs, work, stream, K, N,
+           result):
+    """The measurements beside the headline step: LEB128 coding, integrity
+    hashing, the fused layout and delta chains (the last one overwrites the
+    rollout copy)."""
+    import torch
+    result["leb128"] = leb128_measurement(ad, out_idx[:K], d_offs, plan.numels, stream,
+                                          args.steps)
+    # the delta's two streams as one byte buffer, as an artifact holds them
+    payload = torch.cat([out_idx[:K].view(torch.uint8), out_val[:K].view(torch.uint8)])
+    result["hash"] = hash_measurement(ad, payload, stream, args.steps)
+    del payload
+    result["fused"] = fused_measurement(ad, synth, ws, args.model, out_idx, out_val, work, stream,
+                                        args.steps)
+    result["compose"] = compose_measurement(ad, rollout, N, K, stream, max(args.steps // 2, 3))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -540,15 +560,9 @@ def main():
             "traffic": traffic,
         },
     }
-    result["leb128"] = leb128_measurement(ad, out_idx[:K], d_offs, plan.numels, stream,
-                                          args.steps)
-    # the delta's two streams as one byte buffer, as an artifact holds them
-    payload = torch.cat([out_idx[:K].view(torch.uint8), out_val[:K].view(torch.uint8)])
-    result["hash"] = hash_measurement(ad, payload, stream, args.steps)
-    del payload
-    result["fused"] = fused_measurement(ad, synth, ws, args.model, out_idx, out_val, work, stream,
-                                        args.steps)
-    result["compose"] = compose_measurement(ad, rollout, N, K, stream, max(args.steps // 2, 3))
+    if not args.no_extras:
+        extras(args, ad, synth, ws, rollout, plan, out_idx, out_val, d_offs, work, stream, K, N,
+               result)
     if args.copy_calibration > 0:
         n = args.copy_calibration // 2
         src = torch.empty(n, dtype=torch.int16, device=dev)
