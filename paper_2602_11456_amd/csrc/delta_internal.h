@@ -35,13 +35,16 @@ constexpr int kTilesPerGroup = 64;
 // when the output is written.
 constexpr uint32_t kDefaultStageCap = 1024;
 constexpr uint32_t kMinStageCap = 16;
-// Slots are kSlotPad entries (64 bytes) longer than their capacity, so the
-// slot starts do not all share one alignment modulo the HBM channel
-// interleave (a 4 KiB stride would put every tile's first lines on the
-// same channels).
+// Entries between the end of a slot's capacity and the next slot.  None:
+// padding the 4 KiB slot stride by 64 bytes (to spread slot starts over
+// the HBM channels) measured slower, and packing the slots densely no
+// faster.
 constexpr uint32_t kSlotPad = 0;
-// Entries the stage kernel gathers in LDS before writing its slot.
-constexpr int kLdsStage = 2048;
+// The stage kernel gathers a tile's entries in LDS before writing its slot;
+// the area holds a whole tile.  Its size (32 KiB) also caps residency at
+// four stage workgroups per CU: with eight, the extra loads in flight only
+// add contention in the memory system (measured 3% slower).
+constexpr int kLdsStage = kElemsPerTile;
 
 // One tensor (or a slice of one) as the extract kernels see it.
 struct TensorDesc {

@@ -209,6 +209,8 @@ __device__ __forceinline__ void scan_tile(const TensorDesc& d, uint64_t tile, ui
 
 // ---------------------------------------------------------------- stage
 
+static_assert(kLdsStage >= kElemsPerTile, "the LDS staging area holds a whole tile");
+
 template <bool kMulti, bool kVec>
 __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
   __shared__ uint32_t s_wave_total[kWaves];
@@ -223,9 +225,8 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
   uint32_t* slot = a.stage + tile * a.stage_stride;
   const uint32_t lane_word = (wave * kGroupsPerWave + lane) * 8;
   const uint32_t keep = s.tile_total < a.stage_cap ? s.tile_total : a.stage_cap;
-  // Entries go through LDS so that the slot is written with contiguous
-  // stores; a tile with more entries than LDS holds writes them directly.
-  const bool via_lds = keep <= (uint32_t)kLdsStage;
+  // Entries go through LDS (which holds a whole tile) so that the slot is
+  // written with contiguous stores.
 #pragma unroll
   for (int u = 0; u < kChunks; ++u) {
     uint32_t m = s.mask[u];
@@ -234,20 +235,15 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
     while (m) {
       const int j = __builtin_ctz(m);
       m &= m - 1;
-      if (r < keep) {
-        const uint32_t e = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
-        if (via_lds) s_stage[r] = e; else slot[r] = e;
-      }
+      if (r < keep) s_stage[r] = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
       ++r;
     }
   }
-  if (via_lds) {
-    __syncthreads();
-    // Streaming (non-temporal) stores: the slot is read once, by another
-    // kernel, so it should not displace anything in the caches.
-    for (uint32_t r = threadIdx.x; r < keep; r += kThreads)
-      __builtin_nontemporal_store(s_stage[r], slot + r);
-  }
+  __syncthreads();
+  // Streaming (non-temporal) stores: the slot is read once, by another
+  // kernel, so it should not displace anything in the caches.
+  for (uint32_t r = threadIdx.x; r < keep; r += kThreads)
+    __builtin_nontemporal_store(s_stage[r], slot + r);
   if (threadIdx.x == 0) a.counts[tile] = s.tile_total;
 }
 
@@ -263,39 +259,40 @@ __global__ __launch_bounds__(64) void group_sum_kernel(const CountT* counts, uin
   if (threadIdx.x == 0) group_sum[blockIdx.x] = s;
 }
 
-// Exclusive scan of the group sums by one workgroup, in passes of
-// kScanThreads groups with a running carry; also writes the total.
+// Exclusive scan of the group sums by one workgroup: thread i sums a
+// contiguous run of ceil(num_groups / kScanThreads) groups, the run sums are
+// scanned across the workgroup, and each thread then writes its run's
+// offsets; also writes the total.
 constexpr int kScanThreads = 1024;
 __global__ __launch_bounds__(kScanThreads) void group_scan_kernel(const uint64_t* group_sum,
                                                                   uint64_t num_groups,
                                                                   uint64_t* group_excl,
                                                                   uint64_t* d_count) {
   __shared__ uint64_t s_wave[kScanThreads / 64];
-  __shared__ uint64_t s_carry;
   const uint32_t lane = lane_id();
   const uint32_t wave = threadIdx.x >> 6;
-  if (threadIdx.x == 0) s_carry = 0;
-  __syncthreads();
-  for (uint64_t base = 0; base < num_groups; base += kScanThreads) {
-    const uint64_t i = base + threadIdx.x;
-    const uint64_t v = i < num_groups ? group_sum[i] : 0;
-    // inclusive scan within the wavefront
-    uint64_t x = v;
+  const uint64_t per = (num_groups + kScanThreads - 1) / kScanThreads;
+  const uint64_t b = (uint64_t)threadIdx.x * per;
+  const uint64_t e = b + per < num_groups ? b + per : num_groups;
+  uint64_t run = 0;
+  for (uint64_t i = b; i < e; ++i) run += group_sum[i];
+  // inclusive scan of the run sums within the wavefront
+  uint64_t x = run;
 #pragma unroll
-    for (int s = 1; s < 64; s <<= 1) {
-      const uint64_t y = __shfl_up(x, s);
-      if ((int)lane >= s) x += y;
-    }
-    if (lane == 63) s_wave[wave] = x;
-    __syncthreads();
-    uint64_t before = s_carry;
-    for (uint32_t w = 0; w < wave; ++w) before += s_wave[w];
-    if (i < num_groups) group_excl[i] = before + x - v;
-    __syncthreads();
-    if (threadIdx.x == kScanThreads - 1) s_carry = before + x;
-    __syncthreads();
+  for (int s = 1; s < 64; s <<= 1) {
+    const uint64_t y = __shfl_up(x, s);
+    if ((int)lane >= s) x += y;
   }
-  if (threadIdx.x == 0) *d_count = s_carry;
+  if (lane == 63) s_wave[wave] = x;
+  __syncthreads();
+  uint64_t excl = x - run;
+  for (uint32_t w = 0; w < wave; ++w) excl += s_wave[w];
+  for (uint64_t i = b; i < e; ++i) {
+    const uint64_t v = group_sum[i];
+    group_excl[i] = excl;
+    excl += v;
+  }
+  if (threadIdx.x == kScanThreads - 1) *d_count = excl;
 }
 
 // ------------------------------------------------------------- finalize
@@ -306,6 +303,8 @@ template <bool kMulti>
 __device__ __forceinline__ TensorDesc lane_desc(const ExtractArgs& a, uint64_t tile) {
   return kMulti ? a.table[a.tile_map[tile]] : a.single;
 }
+
+constexpr int kFinBatch = 8;
 
 template <typename IdxT, bool kMulti, bool kVec>
 __global__ __launch_bounds__(kThreads) void finalize_kernel(ExtractArgs a) {
@@ -354,22 +353,34 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(ExtractArgs a) {
   const uint32_t total = s_begin[64];
   // Every staged entry of the group, in output order, spread over all
   // threads; the tile of entry e is found by binary search over s_begin.
-  // Entries of overflowed tiles are skipped here and written below.
-  for (uint32_t e = threadIdx.x; e < total; e += kThreads) {
-    uint32_t lo = 0, hi = 64;   // s_begin[lo] <= e < s_begin[hi]
+  // Each thread loads kFinBatch entries before it stores any, so that many
+  // loads are in flight.  Entries of overflowed tiles are skipped here and
+  // written below.
+  for (uint32_t e0 = 0; e0 < total; e0 += kThreads * kFinBatch) {
+    uint32_t v[kFinBatch], ti[kFinBatch];
 #pragma unroll
-    for (int step = 0; step < 6; ++step) {
-      const uint32_t mid = (lo + hi) >> 1;
-      if (s_begin[mid] <= e) lo = mid; else hi = mid;
+    for (int k = 0; k < kFinBatch; ++k) {
+      const uint32_t e = e0 + threadIdx.x + kThreads * k;
+      uint32_t lo = 0, hi = 64;   // s_begin[lo] <= e < s_begin[hi]
+#pragma unroll
+      for (int step = 0; step < 6; ++step) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (s_begin[mid] <= e) lo = mid; else hi = mid;
+      }
+      ti[k] = lo;
+      const bool take = e < total && s_count[lo] <= a.stage_cap && group_excl + e < a.capacity;
+      v[k] = take ? __builtin_nontemporal_load(a.stage + (t0 + lo) * a.stage_stride +
+                                               (e - s_begin[lo]))
+                  : 0u;
     }
-    const uint32_t i = lo;
-    const uint32_t j = e - s_begin[i];
-    if (s_count[i] > a.stage_cap) continue;
-    const uint64_t pos = group_excl + e;
-    if (pos < a.capacity) {
-      const uint32_t v = a.stage[(t0 + i) * a.stage_stride + j];
-      out_idx[pos] = (IdxT)(s_out_base[i] + (v & 0xFFFFu));
-      a.out_val[pos] = (uint16_t)(v >> 16);
+#pragma unroll
+    for (int k = 0; k < kFinBatch; ++k) {
+      const uint32_t e = e0 + threadIdx.x + kThreads * k;
+      const uint32_t i = ti[k];
+      if (e < total && s_count[i] <= a.stage_cap && group_excl + e < a.capacity) {
+        out_idx[group_excl + e] = (IdxT)(s_out_base[i] + (v[k] & 0xFFFFu));
+        a.out_val[group_excl + e] = (uint16_t)(v[k] >> 16);
+      }
     }
   }
   // Tiles that overflowed their slot: read again and write every entry.
