@@ -397,23 +397,29 @@ typedef struct {
 } delta_pipeline_opts_t;
 
 /* Device staging bytes delta_extract_pipelined needs: per stream, one
- * chunk's worst-case output plus its workspace. */
+ * chunk's worst-case output plus its workspace, and the running totals and
+ * per-chunk counts. */
 size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
                                     const delta_pipeline_opts_t* opts);
 
 /*
  * delta_extract_pipelined — Sec. 5.2: extract_multi over the tensor list,
- * chunk by chunk, with each chunk's (idx, val) copied into pinned host
- * memory as soon as that chunk is done, while later chunks are extracted
- * on the other streams.  The host output equals delta_extract_multi's.
- *   streams       host array of opts->num_streams HIP streams; chunks are
- *                 extracted round-robin on them.  The copies to the host
- *                 run on one stream that the call creates and destroys.
- *   d_staging     device scratch of delta_pipeline_staging_bytes(...).
+ * chunk by chunk, with each chunk's (idx, val) stored into pinned host
+ * memory as soon as that chunk is done, while later chunks are extracted.
+ * The host output equals delta_extract_multi's.
+ *   streams       host array of S = opts->num_streams HIP streams.  S
+ *                 staging slots; chunks are extracted on streams[0] (and
+ *                 streams[1] if S > 2) and delivered in order by one kernel
+ *                 per chunk, storing into the host arrays, on
+ *                 streams[min(S - 1, 2)].  Streams past the third are not
+ *                 used (more streams than hardware queues serialise).
+ *   d_staging     device scratch of delta_pipeline_staging_bytes(...): a
+ *                 ring of S chunk slots plus the running totals.
  *   h_idx, h_val  pinned host arrays (hipHostMalloc / pin_memory) of
- *                 h_capacity entries.
+ *                 h_capacity entries; kernels store into them, so pageable
+ *                 memory is refused with DELTA_ERR_INVALID_ARG.
  *   h_count       host: the true total.
- * Host-synchronous: returns after every copy has landed.  Returns
+ * Host-synchronous: returns after every store has landed.  Returns
  * DELTA_ERR_CAPACITY (with *h_count = true total, the first h_capacity
  * entries written) if the output did not fit.
  */
@@ -438,10 +444,12 @@ size_t delta_pipeline_leb128_staging_bytes(const uint64_t* numels, int32_t num_t
  * first word (c * chunk, chunk = min(opts->chunk_elems, total words)):
  * delta_leb128_decode with seg_offsets = prefix sums of h_chunk_counts and
  * seg_bases[c] = c * chunk returns delta_extract_multi's indices exactly.
+ *   streams, d_staging  as delta_extract_pipelined (the encoder runs on the
+ *                 chunk's extract stream, in its slot).
  *   h_bytes       pinned host bytes [h_bytes_capacity]: the coded indices.
  *   h_val         pinned host words [h_val_capacity]: as delta_extract_multi.
- *   h_chunk_counts host array [h_num_chunks >= ceil(total / chunk)]:
- *                 entries of each chunk.
+ *   h_chunk_counts host array (any memory) [h_num_chunks >=
+ *                 ceil(total / chunk)]: entries of each chunk.
  *   h_count, h_nbytes  host: entry and byte totals.
  * Host-synchronous.  DELTA_ERR_CAPACITY (totals set, what fits written)
  * when either output does not fit.

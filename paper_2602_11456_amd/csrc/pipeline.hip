@@ -5,16 +5,18 @@
 //
 // The global index space of the tensor list is cut into chunks of
 // `chunk_elems` words; a chunk may span several tensors and start inside
-// one.  Chunk c is extracted on stream c mod S into that stream's device
-// staging (coded: its indices are then gap + LEB128 coded there), and its
-// count is copied to the host.  The host takes chunks in order: it waits
-// for chunk c's count, which fixes where chunk c's entries land in the host
-// arrays, and enqueues the copies of chunk c on one copy stream of the
-// library's own (device-to-host copies from several streams at once share
-// the host link less well than back-to-back copies from one).  The extract
-// of chunk c + S waits on an event recorded after those copies, so the
-// staging is never overwritten early.  Up to S chunks are in flight:
-// extracts on the compute streams overlap the copies.
+// one.  Chunk c is extracted into staging slot c mod S (S streams, S slots)
+// on one of up to two extract lanes (streams[0], streams[1]); coded, its
+// indices are then gap + LEB128 coded in the slot.  One more stream
+// (streams[min(S - 1, 2)]) delivers the chunks in order: one kernel per
+// chunk reads the chunk's counts and the running totals from device memory
+// and stores its entries straight into the pinned host arrays over the host
+// link (kernel stores into pinned memory reach the 55 GB/s of DMA copies and
+// need no host round trip per chunk).  A delivery waits on its chunk's
+// extract event; the extract that reuses a slot waits on the delivery of
+// the slot's previous chunk.  The host only enqueues and waits once, at the
+// end.  With S == 1 everything runs in order on the one stream.
+
 #include <string.h>
 
 #include <vector>
@@ -46,6 +48,7 @@ void chunk_slices(const uint16_t* const* prevs, const uint16_t* const* nexts,
 
 struct StagingLayout {
   size_t idx, val, count, nbytes, bytes, enc_ws, ws, ws_bytes, per_stream;
+  size_t run, chunk_counts, total;   // after the S slots: running totals, per-chunk counts
 };
 
 // Longest LEB128 code of a number below `chunk` (every gap inside a chunk,
@@ -59,7 +62,8 @@ uint64_t leb_bytes_per_entry(uint64_t chunk) {
   return n;
 }
 
-StagingLayout staging_layout(uint64_t chunk, size_t ws_bytes, bool leb) {
+StagingLayout staging_layout(uint64_t chunk, size_t ws_bytes, bool leb, int streams,
+                             uint64_t nchunks) {
   StagingLayout L;
   L.idx = 0;
   L.val = align_up(L.idx + 8 * chunk);
@@ -70,7 +74,133 @@ StagingLayout staging_layout(uint64_t chunk, size_t ws_bytes, bool leb) {
   L.ws = align_up(L.enc_ws + (leb ? enc_layout(chunk).total : 0));
   L.ws_bytes = ws_bytes;
   L.per_stream = align_up(L.ws + ws_bytes);
+  L.run = L.per_stream * (size_t)streams;
+  L.chunk_counts = align_up(L.run + 4 * sizeof(uint64_t));
+  L.total = align_up(L.chunk_counts + sizeof(uint64_t) * nchunks);
   return L;
+}
+
+// Device address of a pinned host range, or nullptr if [h, h + bytes) is
+// not pinned host memory the device can reach.
+void* host_range_on_device(const void* h, size_t bytes) {
+  if (!h || bytes == 0) return nullptr;
+  void* d0 = nullptr;
+  void* d1 = nullptr;
+  if (hipHostGetDevicePointer(&d0, const_cast<void*>(h), 0) != hipSuccess ||
+      hipHostGetDevicePointer(&d1, (char*)const_cast<void*>(h) + bytes - 1, 0) != hipSuccess ||
+      (char*)d1 - (char*)d0 != (ptrdiff_t)(bytes - 1)) {
+    (void)hipGetLastError();   // do not leave the lookup's error behind
+    return nullptr;
+  }
+  return d0;
+}
+
+// One chunk's delivery: its entries (and coded bytes) from its staging slot
+// to the host arrays at the running totals, which sit in device memory,
+// double-buffered by chunk parity (every thread reads run[c & 1]; thread 0
+// writes run[(c + 1) & 1]).  Entries past a host array's capacity are
+// dropped; the totals stay true.
+struct DeliverArgs {
+  const int64_t* idx;
+  const uint16_t* val;
+  const uint8_t* bytes;        // coded, else nullptr
+  const uint64_t* d_count;     // entries of the chunk
+  const uint64_t* d_nbytes;    // coded: code bytes of the chunk
+  uint64_t* run;               // [2][2] (entries, bytes)
+  uint64_t* chunk_counts;      // coded: entry count of every chunk
+  uint64_t c;
+  int64_t* h_idx;              // device views of the pinned host arrays
+  uint64_t h_idx_cap;
+  uint8_t* h_bytes;
+  uint64_t h_bytes_cap;
+  uint16_t* h_val;
+  uint64_t h_val_cap;
+};
+
+// At most two extract lanes, so that the lanes and the delivery stream use
+// three streams: a process gets four hardware queues by default, and
+// streams beyond that share a queue, which serialises their work (with four
+// streams the pipeline measured 15% slower than with three).
+constexpr int kMaxExtractLanes = 2;
+constexpr int kDeliverThreads = 256;
+// Stores into host memory are slow to complete, and an XCD with many of
+// them outstanding serves its HBM reads far slower: a host-write kernel
+// spread over all 8 XCDs cut a concurrent HBM read kernel from 6.9 to
+// 1.8 TB/s.  Confined to 2 XCDs with 8 workgroups each it still fills the
+// host link (55.6 GB/s) while the reader keeps 6.6 TB/s.  Workgroup b runs
+// on XCD b mod 8, so the grid holds 8 workgroups per XCD and only those on
+// the first kDeliverXcds XCDs work.
+constexpr int kXcds = 8;
+constexpr int kDeliverXcds = 2;
+constexpr int kDeliverPerXcd = 8;
+constexpr int kDeliverBlocks = kXcds * kDeliverPerXcd;
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// dst[0, n) = src[0, n) by the whole grid, where src is 4-byte aligned and
+// readable up to 4 bytes past n, and dst (host memory) has any alignment:
+// the bytes before dst's first 16-byte boundary and after its last one are
+// stored one by one; in between every store is a whole aligned 16 bytes,
+// assembled from five aligned source dwords with byte-aligning shifts.
+__device__ void copy_bytes(uint8_t* dst, const uint8_t* src, uint64_t n, uint64_t i0,
+                           uint64_t stride) {
+  uint64_t head = (16 - ((uintptr_t)dst & 15)) & 15;
+  if (head > n) head = n;
+  const uint64_t body = (n - head) / 16;
+  const uint64_t tail0 = head + 16 * body;
+  for (uint64_t k = i0; k < head; k += stride) dst[k] = src[k];
+  for (uint64_t k = tail0 + i0; k < n; k += stride) dst[k] = src[k];
+  const uint32_t shift = (uint32_t)(head & 3);
+  const uint32_t* s32 = reinterpret_cast<const uint32_t*>(src + (head & ~(uint64_t)3));
+  u32x4_t* d16 = reinterpret_cast<u32x4_t*>(dst + head);
+  for (uint64_t j = i0; j < body; j += stride) {
+    const uint32_t* w = s32 + 4 * j;
+    const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3];
+    const uint32_t w4 = shift ? w[4] : 0u;
+    u32x4_t v;
+    if (shift) {
+      // byte `shift` of the 8-byte pair (hi:lo) onwards
+      v[0] = __builtin_amdgcn_alignbyte(w1, w0, shift);
+      v[1] = __builtin_amdgcn_alignbyte(w2, w1, shift);
+      v[2] = __builtin_amdgcn_alignbyte(w3, w2, shift);
+      v[3] = __builtin_amdgcn_alignbyte(w4, w3, shift);
+    } else {
+      v = u32x4_t{w0, w1, w2, w3};
+    }
+    __builtin_nontemporal_store(v, d16 + j);
+  }
+}
+
+__global__ __launch_bounds__(kDeliverThreads) void deliver_kernel(DeliverArgs a) {
+  const uint64_t cnt = *a.d_count;
+  const uint64_t nb = a.bytes ? *a.d_nbytes : 0;
+  const uint64_t* r = a.run + 2 * (a.c & 1);
+  const uint64_t be = r[0], bb = r[1];
+  const uint32_t xcd = blockIdx.x % kXcds;
+  if (xcd >= (uint32_t)kDeliverXcds) return;
+  const uint64_t wg = (uint64_t)(blockIdx.x / kXcds) * kDeliverXcds + xcd;
+  const uint64_t i0 = wg * blockDim.x + threadIdx.x;
+  const uint64_t stride = (uint64_t)(gridDim.x / kXcds) * kDeliverXcds * blockDim.x;
+  if (i0 == 0) {
+    uint64_t* w = a.run + 2 * ((a.c + 1) & 1);
+    w[0] = be + cnt;
+    w[1] = bb + nb;
+    if (a.chunk_counts) a.chunk_counts[a.c] = cnt;
+  }
+  const uint64_t ne = be < a.h_val_cap ? (a.h_val_cap - be < cnt ? a.h_val_cap - be : cnt) : 0;
+  copy_bytes((uint8_t*)(a.h_val + be), (const uint8_t*)a.val, 2 * ne, i0, stride);
+  if (a.h_idx) {
+    const uint64_t ni = be < a.h_idx_cap ? (a.h_idx_cap - be < cnt ? a.h_idx_cap - be : cnt) : 0;
+    copy_bytes((uint8_t*)(a.h_idx + be), (const uint8_t*)a.idx, 8 * ni, i0, stride);
+  }
+  if (a.bytes) {
+    const uint64_t n = bb < a.h_bytes_cap ? (a.h_bytes_cap - bb < nb ? a.h_bytes_cap - bb : nb) : 0;
+    copy_bytes(a.h_bytes + bb, a.bytes, n, i0, stride);
+  }
+}
+
+__global__ void run_reset_kernel(uint64_t* run) {
+  if (threadIdx.x < 4) run[threadIdx.x] = 0;
 }
 
 // Largest workspace any chunk's extract needs (tiles at worst alignment).
@@ -106,8 +236,9 @@ static size_t staging_bytes_impl(const uint64_t* numels, int32_t num_tensors,
   uint64_t total = 0;
   for (int32_t t = 0; t < num_tensors; ++t) total += numels[t];
   const uint64_t chunk = opts->chunk_elems < total ? opts->chunk_elems : (total ? total : 1);
+  const uint64_t nchunks = (total + chunk - 1) / chunk;
   const size_t ws = max_chunk_workspace(numels, num_tensors, total, chunk);
-  return staging_layout(chunk, ws, leb).per_stream * (size_t)opts->num_streams;
+  return staging_layout(chunk, ws, leb, opts->num_streams, nchunks).total;
 }
 
 size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
@@ -183,134 +314,136 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     return DELTA_ERR_WORKSPACE;
   }
   const size_t ws = max_chunk_workspace(numels, T, total, chunk);
-  const StagingLayout L = staging_layout(chunk, ws, o.leb);
+  const StagingLayout L = staging_layout(chunk, ws, o.leb, S, nchunks);
   const uint64_t bytes_cap = leb_bytes_per_entry(chunk) * chunk;
 
-  // per chunk: entry count and (coded) byte count land here (pinned)
-  uint64_t* h_counts = nullptr;
-  hipError_t e =
-      hipHostMalloc((void**)&h_counts, sizeof(uint64_t) * 2 * nchunks, hipHostMallocDefault);
-  if (e != hipSuccess) {
-    set_error("hipHostMalloc: %s", hipGetErrorString(e));
-    return DELTA_ERR_HIP;
+  // device views of the pinned host arrays (kernels store into them)
+  DeliverArgs base;
+  memset(&base, 0, sizeof(base));
+  base.h_val_cap = o.h_val_cap;
+  base.h_val = (uint16_t*)host_range_on_device(o.h_val, 2 * o.h_val_cap);
+  bool pinned = o.h_val_cap == 0 || base.h_val;
+  if (!o.leb) {
+    base.h_idx_cap = o.h_idx_cap;
+    base.h_idx = (int64_t*)host_range_on_device(o.h_idx, 8 * o.h_idx_cap);
+    pinned = pinned && (o.h_idx_cap == 0 || base.h_idx);
+  } else {
+    base.h_bytes_cap = o.h_bytes_cap;
+    base.h_bytes = (uint8_t*)host_range_on_device(o.h_bytes, o.h_bytes_cap);
+    pinned = pinned && (o.h_bytes_cap == 0 || base.h_bytes);
   }
+  if (!pinned) {
+    set_error("host output arrays must be pinned host memory (hipHostMalloc / pin_memory)");
+    return DELTA_ERR_INVALID_ARG;
+  }
+  if (base.h_val_cap && !base.h_val) base.h_val_cap = 0;
+  if (base.h_idx_cap && !base.h_idx) base.h_idx_cap = 0;
+  if (base.h_bytes_cap && !base.h_bytes) base.h_bytes_cap = 0;
 
-  hipStream_t cs = nullptr;   // carries every data copy
-  std::vector<hipEvent_t> copied(S, nullptr);   // per staging slot: its last copies are done
-  e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
-  for (int i = 0; i < S && e == hipSuccess; ++i)
-    e = hipEventCreateWithFlags(&copied[i], hipEventDisableTiming);
-
-  std::vector<SliceIn> sl;
-  uint64_t offset = 0;   // host position of the next chunk's first entry
-  uint64_t boffset = 0;  // coded: host position of the next chunk's first byte
-  uint64_t finished = 0; // chunks whose data copies are enqueued
-  uint64_t issued = 0;   // chunks whose extract and count copy are enqueued
+  // E extract lanes, one delivery stream (the same one when S == 1)
+  const int E = S > 1 ? (S - 1 < kMaxExtractLanes ? S - 1 : kMaxExtractLanes) : 1;
+  hipStream_t const ds = S > 1 ? streams[E] : streams[0];
+  std::vector<hipEvent_t> extracted(S, nullptr), delivered(S, nullptr);
+  hipError_t e = hipSuccess;
+  for (int i = 0; i < S && e == hipSuccess; ++i) {
+    e = hipEventCreateWithFlags(&extracted[i], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&delivered[i], hipEventDisableTiming);
+  }
+  char* const stg = (char*)d_staging;
+  uint64_t* const run = (uint64_t*)(stg + L.run);
+  uint64_t* const d_chunk_counts = (uint64_t*)(stg + L.chunk_counts);
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(run_reset_kernel, dim3(1), dim3(64), 0, ds, run);
+    e = hipGetLastError();
+  }
   delta_status_t status = DELTA_OK;
-
-  auto stage_of = [&](uint64_t c) { return (char*)d_staging + L.per_stream * (c % S); };
-  auto copy_out = [&](void* dst, const void* src, uint64_t pos, uint64_t cap, uint64_t n,
-                      size_t elem, hipStream_t st) -> hipError_t {
-    if (pos >= cap || n == 0) return hipSuccess;
-    const uint64_t m = (cap - pos < n) ? cap - pos : n;
-    return hipMemcpyAsync((char*)dst + elem * pos, src, elem * m, hipMemcpyDeviceToHost, st);
-  };
-  auto finish = [&](uint64_t c) -> hipError_t {
-    hipError_t err = hipStreamSynchronize(streams[c % S]);
-    if (err != hipSuccess) return err;
-    hipStream_t st = cs;
-    const uint64_t cnt = h_counts[2 * c];
-    char* stage = stage_of(c);
-    if (!o.leb) {
-      err = copy_out(o.h_idx, stage + L.idx, offset, o.h_idx_cap, cnt, 8, st);
-    } else {
-      o.h_chunk_counts[c] = cnt;
-      const uint64_t nb = h_counts[2 * c + 1];
-      err = copy_out(o.h_bytes, stage + L.bytes, boffset, o.h_bytes_cap, nb, 1, st);
-      boffset += nb;
-    }
-    if (err == hipSuccess) err = copy_out(o.h_val, stage + L.val, offset, o.h_val_cap, cnt, 2, st);
-    if (err == hipSuccess) err = hipEventRecord(copied[c % S], st);
-    offset += cnt;
-    finished = c + 1;
-    return err;
-  };
-  // Coded: the chunk's indices as one segment based at its first word; the
-  // encoder reads the entry count that the extract left in device memory.
-  const EncLayout E = enc_layout(chunk);
-  auto enqueue_encode = [&](uint64_t c) -> hipError_t {
-    char* stage = stage_of(c);
-    EncArgs a;
-    memset(&a, 0, sizeof(a));
-    a.idx = (const int64_t*)(stage + L.idx);
-    a.count = chunk;
-    a.d_count_in = (const uint64_t*)(stage + L.count);
-    a.segs = {nullptr, nullptr, 0, (int64_t)(c * chunk)};
-    a.out = (uint8_t*)(stage + L.bytes);
-    a.capacity = bytes_cap;
-    a.d_nbytes = (uint64_t*)(stage + L.nbytes);
-    a.tile_bytes = (uint32_t*)(stage + L.enc_ws + E.tile_bytes);
-    return launch_leb128_encode(a, (uint64_t*)(stage + L.enc_ws + E.group_sum),
-                                (uint64_t*)(stage + L.enc_ws + E.group_excl), streams[c % S]);
-  };
-
+  std::vector<SliceIn> sl;
+  const EncLayout EL = enc_layout(chunk);
   for (uint64_t c = 0; c < nchunks && e == hipSuccess; ++c) {
-    if (c >= (uint64_t)S) {
-      e = finish(c - S);
+    const int slot = (int)(c % (uint64_t)S);
+    hipStream_t xs = streams[c % (uint64_t)E];
+    char* stage = stg + L.per_stream * (size_t)slot;
+    if (c >= (uint64_t)S) {   // the slot's previous chunk must have been delivered
+      e = hipStreamWaitEvent(xs, delivered[slot], 0);
       if (e != hipSuccess) break;
     }
     const uint64_t lo = c * chunk;
     const uint64_t hi = (total - lo < chunk) ? total : lo + chunk;
     chunk_slices(prevs, nexts, numels, T, lo, hi, sl);
-    char* stage = stage_of(c);
-    if (c >= (uint64_t)S) {   // the slot's previous chunk must have left it
-      e = hipStreamWaitEvent(streams[c % S], copied[c % S], 0);
-      if (e != hipSuccess) break;
-    }
     const delta_status_t st =
         enqueue_extract(sl.data(), sl.size(), 0, true, stage + L.idx, (uint16_t*)(stage + L.val),
-                        chunk, (uint64_t*)(stage + L.count), nullptr, stage + L.ws, L.ws_bytes,
-                        streams[c % S]);
+                        chunk, (uint64_t*)(stage + L.count), nullptr, stage + L.ws, L.ws_bytes, xs);
     if (st != DELTA_OK) {
       status = st;
       break;
     }
-    if (o.leb) e = enqueue_encode(c);
-    // the count (and, coded, the byte count right after it) to the host
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(&h_counts[2 * c], stage + L.count, o.leb ? 16 : 8,
-                         hipMemcpyDeviceToHost, streams[c % S]);
-    if (e == hipSuccess) issued = c + 1;
+    if (o.leb) {
+      // the chunk's indices as one segment based at its first word; the
+      // encoder reads the entry count the extract left in device memory
+      EncArgs a;
+      memset(&a, 0, sizeof(a));
+      a.idx = (const int64_t*)(stage + L.idx);
+      a.count = chunk;
+      a.d_count_in = (const uint64_t*)(stage + L.count);
+      a.segs = {nullptr, nullptr, 0, (int64_t)(c * chunk)};
+      a.out = (uint8_t*)(stage + L.bytes);
+      a.capacity = bytes_cap;
+      a.d_nbytes = (uint64_t*)(stage + L.nbytes);
+      a.tile_bytes = (uint32_t*)(stage + L.enc_ws + EL.tile_bytes);
+      e = launch_leb128_encode(a, (uint64_t*)(stage + L.enc_ws + EL.group_sum),
+                               (uint64_t*)(stage + L.enc_ws + EL.group_excl), xs);
+      if (e != hipSuccess) break;
+    }
+    if (xs != ds) {
+      e = hipEventRecord(extracted[slot], xs);
+      if (e == hipSuccess) e = hipStreamWaitEvent(ds, extracted[slot], 0);
+      if (e != hipSuccess) break;
+    }
+    DeliverArgs d = base;
+    d.idx = (const int64_t*)(stage + L.idx);
+    d.val = (const uint16_t*)(stage + L.val);
+    d.bytes = o.leb ? (const uint8_t*)(stage + L.bytes) : nullptr;
+    d.d_count = (const uint64_t*)(stage + L.count);
+    d.d_nbytes = (const uint64_t*)(stage + L.nbytes);
+    d.run = run;
+    d.chunk_counts = o.leb ? d_chunk_counts : nullptr;
+    d.c = c;
+    hipLaunchKernelGGL(deliver_kernel, dim3(kDeliverBlocks), dim3(kDeliverThreads), 0, ds, d);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipEventRecord(delivered[slot], ds);
   }
-  while (e == hipSuccess && status == DELTA_OK && finished < issued) e = finish(finished);
-  // Drain every stream whatever happened, so no copy is left in flight.
-  for (int s = 0; s < S; ++s) {
-    hipError_t e2 = hipStreamSynchronize(streams[s]);
+  // Drain every stream whatever happened, so nothing is left in flight.
+  for (int i = 0; i < S; ++i) {
+    hipError_t e2 = hipStreamSynchronize(streams[i]);
     if (e == hipSuccess) e = e2;
   }
-  if (cs) {
-    hipError_t e2 = hipStreamSynchronize(cs);
-    if (e == hipSuccess) e = e2;
-    (void)hipStreamDestroy(cs);
+  uint64_t totals[2] = {0, 0};
+  if (e == hipSuccess && status == DELTA_OK) {
+    e = hipMemcpy(totals, run + 2 * (nchunks & 1), sizeof(totals), hipMemcpyDeviceToHost);
+    if (e == hipSuccess && o.leb)
+      e = hipMemcpy(o.h_chunk_counts, d_chunk_counts, sizeof(uint64_t) * nchunks,
+                    hipMemcpyDeviceToHost);
   }
-  for (hipEvent_t ev : copied)
-    if (ev) (void)hipEventDestroy(ev);
-  (void)hipHostFree(h_counts);
+  for (int i = 0; i < S; ++i) {
+    if (extracted[i]) (void)hipEventDestroy(extracted[i]);
+    if (delivered[i]) (void)hipEventDestroy(delivered[i]);
+  }
   if (e != hipSuccess) {
     set_error("HIP error in pipeline: %s", hipGetErrorString(e));
     return DELTA_ERR_HIP;
   }
   if (status != DELTA_OK) return status;   // a chunk could not be enqueued: no result
-  *h_count = offset;
-  if (h_nbytes) *h_nbytes = boffset;
-  const bool fits = offset <= o.h_val_cap && (o.leb ? boffset <= o.h_bytes_cap
-                                                    : offset <= o.h_idx_cap);
+  const uint64_t entries = totals[0], nbytes = totals[1];
+  *h_count = entries;
+  if (h_nbytes) *h_nbytes = nbytes;
+  const bool fits = entries <= o.h_val_cap && (o.leb ? nbytes <= o.h_bytes_cap
+                                                     : entries <= o.h_idx_cap);
   if (!fits) {
     set_error("output has %llu entries (%llu index bytes); it does not fit",
-             (unsigned long long)offset, (unsigned long long)boffset);
-    status = DELTA_ERR_CAPACITY;
+             (unsigned long long)entries, (unsigned long long)nbytes);
+    return DELTA_ERR_CAPACITY;
   }
-  return status;
+  return DELTA_OK;
 }
 
 extern "C" delta_status_t delta_extract_pipelined(

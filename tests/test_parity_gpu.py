@@ -364,6 +364,20 @@ def test_pipeline_leb128_capacity_retry():
     np.testing.assert_array_equal(v.view(torch.int16).numpy().view(np.uint16), ref_val)
 
 
+def test_pipeline_refuses_pageable_host_output():
+    prevs, news = make_list([40_000, 20_000], 0.05, seed=10)
+    h_idx = torch.empty(1000, dtype=torch.int64)   # pageable
+    h_val = torch.empty(1000, dtype=torch.bfloat16, pin_memory=True)
+    with pytest.raises(ad.DeltaError) as ex:
+        ad.delta_extract_pipelined(prevs, news, chunk_elems=5000, num_streams=2,
+                                   h_idx=h_idx, h_val=h_val)
+    assert "pinned" in str(ex.value)
+    hb = torch.empty(1000, dtype=torch.uint8)      # pageable
+    with pytest.raises(ad.DeltaError):
+        ad.delta_extract_pipelined_leb128(prevs, news, chunk_elems=5000, num_streams=2,
+                                          h_bytes=hb, h_val=h_val)
+
+
 def test_pipeline_capacity_retry():
     prevs, news = make_list([40_000, 20_000], 0.05, seed=9)
     h_idx = torch.empty(10, dtype=torch.int64, pin_memory=True)
