@@ -129,7 +129,8 @@ constexpr int kDeliverThreads = 256;
 // 1.8 TB/s.  Confined to 2 XCDs with 8 workgroups each it still fills the
 // host link (55.6 GB/s) while the reader keeps 6.6 TB/s.  Workgroup b runs
 // on XCD b mod 8, so the grid holds 8 workgroups per XCD and only those on
-// the first kDeliverXcds XCDs work.
+// the last kDeliverXcds XCDs work (small kernels of one or a few
+// workgroups, such as the scans, run on the first XCDs).
 constexpr int kXcds = 8;
 constexpr int kDeliverXcds = 2;
 constexpr int kDeliverPerXcd = 8;
@@ -177,8 +178,8 @@ __global__ __launch_bounds__(kDeliverThreads) void deliver_kernel(DeliverArgs a)
   const uint64_t* r = a.run + 2 * (a.c & 1);
   const uint64_t be = r[0], bb = r[1];
   const uint32_t xcd = blockIdx.x % kXcds;
-  if (xcd >= (uint32_t)kDeliverXcds) return;
-  const uint64_t wg = (uint64_t)(blockIdx.x / kXcds) * kDeliverXcds + xcd;
+  if (xcd < (uint32_t)(kXcds - kDeliverXcds)) return;
+  const uint64_t wg = (uint64_t)(blockIdx.x / kXcds) * kDeliverXcds + (xcd - (kXcds - kDeliverXcds));
   const uint64_t i0 = wg * blockDim.x + threadIdx.x;
   const uint64_t stride = (uint64_t)(gridDim.x / kXcds) * kDeliverXcds * blockDim.x;
   if (i0 == 0) {
