@@ -259,40 +259,67 @@ __global__ __launch_bounds__(64) void group_sum_kernel(const CountT* counts, uin
   if (threadIdx.x == 0) group_sum[blockIdx.x] = s;
 }
 
-// Exclusive scan of the group sums by one workgroup: thread i sums a
-// contiguous run of ceil(num_groups / kScanThreads) groups, the run sums are
-// scanned across the workgroup, and each thread then writes its run's
-// offsets; also writes the total.
+// Exclusive scan of the group sums by one workgroup, also writing the
+// total.  Wavefront w owns a contiguous range of the sums, in blocks of 64
+// (one per lane, loaded coalesced, kScanBatch blocks in flight at a time).
+// Pass 1: each wavefront sums its range; the range sums are combined
+// through LDS.  Pass 2: each wavefront scans its blocks in order, carrying
+// the running offset, and writes the exclusive offsets.
 constexpr int kScanThreads = 1024;
+constexpr int kScanWaves = kScanThreads / 64;
+constexpr int kScanBatch = 8;
 __global__ __launch_bounds__(kScanThreads) void group_scan_kernel(const uint64_t* group_sum,
                                                                   uint64_t num_groups,
                                                                   uint64_t* group_excl,
                                                                   uint64_t* d_count) {
-  __shared__ uint64_t s_wave[kScanThreads / 64];
+  __shared__ uint64_t s_wave[kScanWaves];
   const uint32_t lane = lane_id();
   const uint32_t wave = threadIdx.x >> 6;
-  const uint64_t per = (num_groups + kScanThreads - 1) / kScanThreads;
-  const uint64_t b = (uint64_t)threadIdx.x * per;
-  const uint64_t e = b + per < num_groups ? b + per : num_groups;
-  uint64_t run = 0;
-  for (uint64_t i = b; i < e; ++i) run += group_sum[i];
-  // inclusive scan of the run sums within the wavefront
-  uint64_t x = run;
+  const uint64_t blocks = (num_groups + 63) / 64;
+  const uint64_t per = (blocks + kScanWaves - 1) / kScanWaves;   // blocks per wavefront
+  const uint64_t b0 = (uint64_t)wave * per;
+  const uint64_t b1 = b0 + per < blocks ? b0 + per : blocks;
+  uint64_t part = 0;
+  for (uint64_t b = b0; b < b1; b += kScanBatch) {
+    uint64_t v[kScanBatch];
 #pragma unroll
-  for (int s = 1; s < 64; s <<= 1) {
-    const uint64_t y = __shfl_up(x, s);
-    if ((int)lane >= s) x += y;
+    for (int k = 0; k < kScanBatch; ++k) {
+      const uint64_t i = (b + k) * 64 + lane;
+      v[k] = (b + k < b1 && i < num_groups) ? group_sum[i] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) part += v[k];
   }
-  if (lane == 63) s_wave[wave] = x;
+  part = wave_sum64(part);
+  if (lane == 0) s_wave[wave] = part;
   __syncthreads();
-  uint64_t excl = x - run;
-  for (uint32_t w = 0; w < wave; ++w) excl += s_wave[w];
-  for (uint64_t i = b; i < e; ++i) {
-    const uint64_t v = group_sum[i];
-    group_excl[i] = excl;
-    excl += v;
+  uint64_t carry = 0, total = 0;
+  for (uint32_t w = 0; w < (uint32_t)kScanWaves; ++w) {
+    const uint64_t t = s_wave[w];
+    carry += w < wave ? t : 0;
+    total += t;
   }
-  if (threadIdx.x == kScanThreads - 1) *d_count = excl;
+  for (uint64_t b = b0; b < b1; b += kScanBatch) {
+    uint64_t v[kScanBatch];
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) {
+      const uint64_t i = (b + k) * 64 + lane;
+      v[k] = (b + k < b1 && i < num_groups) ? group_sum[i] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) {
+      uint64_t x = v[k];   // inclusive scan of the block within the wavefront
+#pragma unroll
+      for (int s = 1; s < 64; s <<= 1) {
+        const uint64_t y = __shfl_up(x, s);
+        if ((int)lane >= s) x += y;
+      }
+      const uint64_t i = (b + k) * 64 + lane;
+      if (b + k < b1 && i < num_groups) group_excl[i] = carry + x - v[k];
+      carry += __shfl(x, 63);
+    }
+  }
+  if (threadIdx.x == 0) *d_count = total;
 }
 
 // ------------------------------------------------------------- finalize
