@@ -54,6 +54,9 @@ def parse():
                     help="skip the chunked extract -> pinned host pipeline measurement "
                          "(Qwen3-14B-shaped set)")
     ap.add_argument("--pipeline-reps", type=int, default=5)
+    ap.add_argument("--only-pipeline", action="store_true",
+                    help="measure only the pipelines on the Qwen3-14B-shaped set and print "
+                         "their figures (for profiling; not the benchmark line)")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the headline step (extract + apply); skip the LEB128, "
                          "hash, fused-layout and delta-chain measurements")
@@ -435,6 +438,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     ad.library()   # fail loudly if the HIP library is missing
+    if args.only_pipeline:
+        print(json.dumps({"pipeline": pipeline_measurement(args, dev)}), flush=True)
+        return 0
 
     t0 = time.time()
     ws = synth.make_weight_set(args.model, args.density, seed=synth.config_seed(3), device=dev)
