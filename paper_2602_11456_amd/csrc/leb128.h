@@ -42,6 +42,8 @@ struct DecArgs {
   uint64_t* group_excl;         // entries before each group of tiles
   uint32_t* tile_f;             // byte tile holds a segment start
   uint64_t* tile_v;             // segmented sum of the tile's terms
+  uint32_t* wave_f;             // the same per wavefront of a tile (4 per tile)
+  uint64_t* wave_v;
   uint64_t* gexcl_v;            // index just before each group of tiles
 };
 
@@ -53,7 +55,8 @@ struct EncLayout {
 uint32_t enc_grid(uint64_t count, bool count_on_device);
 struct DecLayout {
   uint64_t btiles;
-  size_t tile_terms, group_sum, group_excl, tile_f, tile_v, gsum_f, gsum_v, gexcl_v, total;
+  size_t tile_terms, group_sum, group_excl, tile_f, tile_v, wave_f, wave_v, gsum_f, gsum_v,
+      gexcl_v, total;
 };
 EncLayout enc_layout(uint64_t count);
 DecLayout dec_layout(uint64_t nbytes);

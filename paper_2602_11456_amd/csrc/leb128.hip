@@ -438,26 +438,6 @@ __device__ __forceinline__ void dec_load_tile(const DecArgs& a, uint64_t b0, boo
   __syncthreads();
 }
 
-// The number whose terminating byte sits at LDS position li (stream
-// position p): its value; `bad` if it is longer than 10 bytes or exceeds
-// 64 bits.
-__device__ __forceinline__ uint64_t dec_number(const uint8_t* s_bytes, uint32_t li, uint64_t p,
-                                               bool& bad) {
-  uint32_t len = 1;
-  while (len <= 10 && p >= len && (s_bytes[li - len] & 0x80)) ++len;
-  if (len > 10) {
-    bad = true;
-    return 0;
-  }
-  uint64_t v = 0;
-  for (uint32_t m = 0; m < len; ++m) {
-    const uint64_t payload = s_bytes[li - len + 1 + m] & 0x7F;
-    if (m == 9 && payload > 1) bad = true;
-    v |= payload << (7 * m);
-  }
-  return v;
-}
-
 // Terminating bytes in this wavefront's 4 KiB of the tile (from LDS).
 __device__ __forceinline__ uint32_t dec_wave_terms(const uint8_t* s_bytes, uint64_t b0,
                                                    uint64_t n) {
@@ -472,48 +452,185 @@ __device__ __forceinline__ uint32_t dec_wave_terms(const uint8_t* s_bytes, uint6
   return wave_sum(c);
 }
 
-// What one byte contributes: valid = it ends a number; flag = that entry
-// opens a segment, and x = base + term then, else x = the gap.
-struct Term {
-  bool valid, flag;
-  uint64_t x;
-};
-
-__device__ __forceinline__ Term dec_term(const DecArgs& a, const TileSegs& c,
-                                         const uint64_t* s_lo, const uint8_t* s_bytes,
-                                         uint32_t li, uint64_t p, uint64_t e, bool& bad) {
-  Term t{false, false, 0};
-  if (p >= a.nbytes) return t;
-  if (s_bytes[li] & 0x80) {
-    if (p == a.nbytes - 1) bad = true;   // the stream ends inside a number
-    return t;
-  }
-  t.valid = true;
-  t.x = dec_number(s_bytes, li, p, bad);
-  bool start;
-  const uint32_t s = tile_seg(a.segs, c, s_lo, e, start);
-  if (start) {
-    t.flag = true;
-    t.x += (uint64_t)seg_base(a.segs, s);
-  }
-  return t;
+// First entry id of this wavefront in the tile whose first is e0.
+__device__ __forceinline__ uint64_t dec_wave_e0(uint64_t e0, const uint32_t* s_wterm) {
+  uint64_t e = e0;
+  for (uint32_t w = 0; w < wave_id(); ++w) e += s_wterm[w];
+  return e;
 }
 
-// One step of 64 bytes of this wavefront: the byte of this lane, the
-// numbers ending in the step, and their entry ids from e.
-struct Step {
-  uint32_t li;
-  uint64_t p;
-  uint64_t terms;   // ballot of terminating bytes
+// Every lane decodes 16 bytes per step: a wavefront covers 1 KiB per step
+// and 4 KiB in kDecSteps steps.
+constexpr int kDecSteps = kDecWave / (64 * 16);
+
+// Byte j (0..15) of 16 bytes held as four dwords.
+__device__ __forceinline__ uint32_t byte16(const leb_u32x4& v, int j) {
+  return (v[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+}
+
+// Bit j set: byte j ends a number (high bit clear).
+__device__ __forceinline__ uint32_t ends16(const leb_u32x4& v) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t x = ~v[d] & 0x80808080u;
+    m |= (((x >> 7) & 1u) | ((x >> 14) & 2u) | ((x >> 21) & 4u) | ((x >> 28) & 8u)) << (4 * d);
+  }
+  return m;
+}
+
+// The number that the bytes after the last terminating byte of the 16
+// bytes P open (it continues past P): its payload so far and its length.
+// Length 16 when P holds no terminating byte (a number over 10 bytes).
+__device__ __forceinline__ void open_number(const leb_u32x4& P, uint64_t& v, uint32_t& len) {
+  const uint32_t t = ends16(P);
+  const int h = t ? 31 - __builtin_clz(t) : -1;
+  len = (uint32_t)(15 - h);
+  v = 0;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int k = j - h - 1;   // byte k of the open number
+    if (k >= 0 && k < 10) v |= (uint64_t)(byte16(P, j) & 0x7Fu) << (7 * k);
+  }
+}
+
+// Decodes the valid bytes (mask `valid`) of the 16 bytes C, continuing
+// the open number (v_in, len_in): num[j] is the number that ends at byte j
+// where bit j of the returned mask is set.  `bad`: a number over 10 bytes
+// or over 64 bits.
+__device__ __forceinline__ uint32_t decode16(const leb_u32x4& C, uint32_t valid, uint64_t v_in,
+                                             uint32_t len_in, uint64_t* num, bool& bad) {
+  const uint32_t ends = ends16(C) & valid;
+  uint64_t acc = v_in;
+  uint32_t k = len_in;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const uint64_t pl = byte16(C, j) & 0x7Fu;
+    if ((valid >> j) & 1u) {
+      if (k < 9) {
+        acc |= pl << (7 * k);
+      } else if (k == 9) {
+        if (pl > 1) bad = true;
+        acc |= pl << 63;
+      } else {
+        bad = true;
+      }
+      ++k;
+    }
+    num[j] = acc;
+    if ((ends >> j) & 1u) {
+      acc = 0;
+      k = 0;
+    }
+  }
+  return ends;
+}
+
+// Walks the segments of a tile's entries in increasing entry order.
+struct SegCursor {
+  uint32_t a;       // segment c.first + a (cached) or a (uncached)
+  uint64_t lo;      // first entry of the segment
+  uint64_t next;    // first entry of the next one (~0: none in this tile)
 };
 
-__device__ __forceinline__ Step dec_step(const DecArgs& a, const uint8_t* s_bytes, uint64_t b0,
-                                         int it) {
-  Step s;
-  s.li = kDecBack + wave_id() * kDecWave + it * 64 + lane_id();
-  s.p = b0 + (s.li - kDecBack);
-  s.terms = __ballot(s.p < a.nbytes && !(s_bytes[s.li] & 0x80));
-  return s;
+__device__ __forceinline__ SegCursor seg_cursor(const LebSegs& g, const TileSegs& c,
+                                                const uint64_t* s_lo, uint64_t e) {
+  SegCursor r{0, 0, ~0ull};
+  if (g.num == 0) return r;
+  if (c.cached) {
+    const uint32_t n = c.last - c.first + 1;
+    uint32_t a = 0, b = n;   // last a with s_lo[a] <= e
+    while (b - a > 1) {
+      const uint32_t mid = (a + b) >> 1;
+      if (s_lo[mid] <= e) a = mid; else b = mid;
+    }
+    r.a = a;
+    r.lo = s_lo[a];
+    r.next = a + 1 < n ? s_lo[a + 1] : ~0ull;
+  } else {
+    r.a = seg_of(g, e);
+    r.lo = g.offs[r.a];
+    r.next = r.a + 1 < g.num ? g.offs[r.a + 1] : ~0ull;
+  }
+  return r;
+}
+
+// Moves the cursor to the segment of entry e (>= the cursor's entry) and
+// returns whether e opens it, with the segment's base in `base`.
+__device__ __forceinline__ bool seg_step(const LebSegs& g, const TileSegs& c,
+                                         const uint64_t* s_lo, SegCursor& r, uint64_t e,
+                                         int64_t& base) {
+  if (g.num == 0) {
+    base = g.base0;
+    return e == 0;
+  }
+  while (r.next <= e) {
+    ++r.a;
+    r.lo = r.next;
+    if (c.cached) {
+      r.next = r.a + 1 <= c.last - c.first ? s_lo[r.a + 1] : ~0ull;
+    } else {
+      r.next = r.a + 1 < g.num ? g.offs[r.a + 1] : ~0ull;
+    }
+  }
+  const bool start = e == 0 || e == r.lo;
+  base = start ? (int64_t)g.bases[c.cached ? c.first + r.a : r.a] : 0;
+  return start;
+}
+
+// One step of one lane: the 16 bytes at tile offset q decoded, with the
+// entry id of the lane's first number and the count.
+struct LaneDec {
+  uint64_t num[16];
+  uint32_t ends;
+  uint64_t e;        // entry id of the lane's first number
+};
+
+__device__ __forceinline__ void dec_lane_step(const DecArgs& a, const uint8_t* s_bytes,
+                                              uint64_t b0, int it, uint64_t& e_step,
+                                              LaneDec& d, bool& bad) {
+  const uint32_t q = wave_id() * kDecWave + it * 1024 + lane_id() * 16;   // tile offset
+  const uint64_t p = b0 + q;
+  const leb_u32x4 C = *(const leb_u32x4*)(s_bytes + kDecBack + q);
+  const leb_u32x4 P = *(const leb_u32x4*)(s_bytes + kDecBack + q - 16);
+  uint32_t valid = 0;
+  if (p < a.nbytes) valid = a.nbytes - p >= 16 ? 0xFFFFu : (1u << (a.nbytes - p)) - 1u;
+  uint64_t v_in = 0;
+  uint32_t len_in = 0;
+  if (valid) open_number(P, v_in, len_in);
+  d.ends = decode16(C, valid, v_in, len_in, d.num, bad);
+  // the stream must not end inside a number
+  if (valid && a.nbytes - p <= 16 && (s_bytes[kDecBack + q + (a.nbytes - p - 1)] & 0x80u))
+    bad = true;
+  const uint32_t cnt = __builtin_popcount(d.ends);
+  const uint32_t incl = wave_incl_scan(cnt);
+  d.e = e_step + incl - cnt;
+  e_step += __shfl(incl, 63);
+}
+
+// Segmented fold of one lane's numbers: whether one opens a segment, and
+// the sum since the last that does (base + first term for it).
+__device__ __forceinline__ void lane_fold(const DecArgs& a, const TileSegs& c,
+                                          const uint64_t* s_lo, const LaneDec& d, uint32_t& f,
+                                          uint64_t& v) {
+  f = 0;
+  v = 0;
+  if (!d.ends) return;
+  SegCursor r = seg_cursor(a.segs, c, s_lo, d.e);
+  uint64_t e = d.e;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    if ((d.ends >> j) & 1u) {
+      int64_t base;
+      if (seg_step(a.segs, c, s_lo, r, e, base)) {
+        f = 1;
+        v = d.num[j] + (uint64_t)base;
+      } else {
+        v += d.num[j];
+      }
+      ++e;
+    }
+  }
 }
 
 // Segmented fold of this wavefront's entries (first entry id e): whether
@@ -522,32 +639,24 @@ __device__ __forceinline__ void dec_wave_fold(const DecArgs& a, const TileSegs& 
                                               const uint64_t* s_lo, const uint8_t* s_bytes,
                                               uint64_t b0, uint64_t e, bool& bad, uint32_t& f,
                                               uint64_t& v) {
-  const uint32_t lane = lane_id();
-  bool any = false;
-  uint64_t acc = 0;   // per lane: its terms since the wavefront's last segment start
-  for (int it = 0; it < kDecWave / 64; ++it) {
-    const Step s = dec_step(a, s_bytes, b0, it);
-    const Term t = dec_term(a, c, s_lo, s_bytes, s.li, s.p, e + lanes_below(s.terms), bad);
-    const uint64_t fm = __ballot(t.flag);
-    const uint64_t x = t.valid ? t.x : 0;
-    if (fm) {   // uniform: restart at the last entry that opens a segment
-      const uint32_t L = 63 - __builtin_clzll(fm);
-      acc = lane >= L ? x : 0;
-      any = true;
+  f = 0;
+  v = 0;
+  for (int it = 0; it < kDecSteps; ++it) {
+    LaneDec d;
+    dec_lane_step(a, s_bytes, b0, it, e, d, bad);
+    uint32_t lf;
+    uint64_t lv;
+    lane_fold(a, c, s_lo, d, lf, lv);
+    wave_seg_scan(lf, lv);
+    const uint32_t sf = __shfl(lf, 63);
+    const uint64_t sv = __shfl(lv, 63);
+    if (sf) {
+      f = 1;
+      v = sv;
     } else {
-      acc += x;
+      v += sv;
     }
-    e += __builtin_popcountll(s.terms);
   }
-  f = any;
-  v = wave_sum(acc);
-}
-
-// First entry id of this wavefront in the tile whose first is e0.
-__device__ __forceinline__ uint64_t dec_wave_e0(uint64_t e0, const uint32_t* s_wterm) {
-  uint64_t e = e0;
-  for (uint32_t w = 0; w < wave_id(); ++w) e += s_wterm[w];
-  return e;
 }
 
 __global__ __launch_bounds__(kLebThreads) void dec_fold_kernel(DecArgs a, bool aligned) {
@@ -587,6 +696,8 @@ __global__ __launch_bounds__(kLebThreads) void dec_fold_kernel(DecArgs a, bool a
   if (lane_id() == 0) {
     s_wf[wave_id()] = f;
     s_wv[wave_id()] = v;
+    a.wave_f[tile * kLebWaves + wave_id()] = f;   // read back by dec_write
+    a.wave_v[tile * kLebWaves + wave_id()] = v;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -676,15 +787,18 @@ __global__ __launch_bounds__(kSegScanThreads) void seg_group_scan_kernel(const u
   if (d_total && threadIdx.x == 0) *d_total = s_carry;
 }
 
+// Entries one wavefront decodes in one step, at most (64 lanes x 16 bytes).
+constexpr int kDecStepEntries = 64 * 16;
+
 __global__ __launch_bounds__(kLebThreads) void dec_write_kernel(DecArgs a, bool aligned) {
   __shared__ __align__(16) uint8_t s_bytes[kDecBack + kDecTile];
   __shared__ uint64_t s_lo[kSegLds];
   __shared__ uint32_t s_meta[2];
   __shared__ uint32_t s_wterm[kLebWaves];
-  __shared__ uint32_t s_wf[kLebWaves];
-  __shared__ uint64_t s_wv[kLebWaves];
   __shared__ uint64_t s_tmp;
   __shared__ uint64_t s_carry;
+  // every wavefront's decoded indices of one step, written out coalesced
+  __shared__ uint64_t s_out[kLebWaves][kDecStepEntries];
   const uint64_t tile = blockIdx.x;
   const uint32_t terms = a.tile_terms[tile];
   if (terms == 0) return;   // uniform
@@ -706,31 +820,62 @@ __global__ __launch_bounds__(kLebThreads) void dec_write_kernel(DecArgs a, bool 
   __syncthreads();
   const TileSegs c = tile_segs(a.segs, e0, e0 + terms, s_lo, s_meta);     // barriers
   const uint64_t ew = dec_wave_e0(e0, s_wterm);
+  // index of the entry before this wavefront's first, from dec_fold's
+  // per-wavefront folds
+  uint64_t run = s_carry;
+  for (uint32_t w = 0; w < wave; ++w)
+    run = a.wave_f[tile * kLebWaves + w] ? a.wave_v[tile * kLebWaves + w]
+                                         : run + a.wave_v[tile * kLebWaves + w];
   bool bad = false;   // reported by dec_fold
-  {
-    uint32_t f;
-    uint64_t v;
-    dec_wave_fold(a, c, s_lo, s_bytes, b0, ew, bad, f, v);
-    if (lane == 0) {
-      s_wf[wave] = f;
-      s_wv[wave] = v;
-    }
-  }
-  __syncthreads();
-  uint64_t run = s_carry;   // index of the entry before this wavefront's first
-  for (uint32_t w = 0; w < wave; ++w) run = s_wf[w] ? s_wv[w] : run + s_wv[w];
+  uint64_t* so = s_out[wave];
   uint64_t e = ew;
-  for (int it = 0; it < kDecWave / 64; ++it) {
-    const Step s = dec_step(a, s_bytes, b0, it);
-    const uint64_t my_e = e + lanes_below(s.terms);
-    const Term t = dec_term(a, c, s_lo, s_bytes, s.li, s.p, my_e, bad);
-    uint64_t v = t.valid ? t.x : 0;
-    uint32_t f = t.flag;
-    wave_seg_scan(f, v);
-    const uint64_t y = f ? v : run + v;
-    if (t.valid && my_e < a.capacity) a.out[my_e] = (int64_t)y;
-    run = __shfl(y, 63);
-    e += __builtin_popcountll(s.terms);
+  for (int it = 0; it < kDecSteps; ++it) {
+    const uint64_t e_step = e;
+    LaneDec d;
+    dec_lane_step(a, s_bytes, b0, it, e, d, bad);
+    uint32_t lf;
+    uint64_t lv;
+    lane_fold(a, c, s_lo, d, lf, lv);
+    // index before this lane's first number: segmented exclusive scan
+    uint32_t sf = lf;
+    uint64_t sv = lv;
+    wave_seg_scan(sf, sv);
+    uint32_t xf = __shfl_up(sf, 1);
+    uint64_t xv = __shfl_up(sv, 1);
+    if (lane == 0) {
+      xf = 0;
+      xv = 0;
+    }
+    uint64_t y = xf ? xv : run + xv;
+    const uint32_t f63 = __shfl(sf, 63);
+    const uint64_t v63 = __shfl(sv, 63);
+    run = f63 ? v63 : run + v63;
+    if (d.ends) {
+      SegCursor r = seg_cursor(a.segs, c, s_lo, d.e);
+      uint64_t k = d.e;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        if ((d.ends >> j) & 1u) {
+          int64_t base;
+          y = seg_step(a.segs, c, s_lo, r, k, base) ? d.num[j] + (uint64_t)base : y + d.num[j];
+          so[k - e_step] = y;
+          ++k;
+        }
+      }
+    }
+    // the wavefront's entries of this step are contiguous: store them
+    // coalesced from LDS (LDS operations of one wavefront complete in order)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const uint32_t n = (uint32_t)(e - e_step);
+    for (uint32_t i = lane; i < n; i += 64) {
+      const uint64_t k = e_step + i;
+      if (k < a.capacity) a.out[k] = (int64_t)so[i];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();   // so[] is rewritten by the next step
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
@@ -759,7 +904,9 @@ DecLayout dec_layout(uint64_t nbytes) {
   L.group_excl = align_up(L.group_sum + 8 * gb);
   L.tile_f = align_up(L.group_excl + 8 * gb);
   L.tile_v = align_up(L.tile_f + 4 * bt);
-  L.gsum_f = align_up(L.tile_v + 8 * bt);
+  L.wave_f = align_up(L.tile_v + 8 * bt);
+  L.wave_v = align_up(L.wave_f + 4 * kLebWaves * bt);
+  L.gsum_f = align_up(L.wave_v + 8 * kLebWaves * bt);
   L.gsum_v = align_up(L.gsum_f + 4 * gb);
   L.gexcl_v = align_up(L.gsum_v + 8 * gb);
   L.total = align_up(L.gexcl_v + 8 * gb);
@@ -817,6 +964,8 @@ hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStre
   a.group_excl = (uint64_t*)(ws + L.group_excl);
   a.tile_f = (uint32_t*)(ws + L.tile_f);
   a.tile_v = (uint64_t*)(ws + L.tile_v);
+  a.wave_f = (uint32_t*)(ws + L.wave_f);
+  a.wave_v = (uint64_t*)(ws + L.wave_v);
   a.gexcl_v = (uint64_t*)(ws + L.gexcl_v);
   const bool aligned = ((uintptr_t)a.in & 15u) == 0;
   const dim3 grid((uint32_t)L.btiles), block(kLebThreads);
