@@ -137,6 +137,9 @@ constexpr int kDeliverPerXcd = 8;
 constexpr int kDeliverBlocks = kXcds * kDeliverPerXcd;
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+// four dwords at a 4-byte aligned address (one 16-byte load)
+typedef uint32_t u32x4a_t __attribute__((ext_vector_type(4), aligned(4)));
+constexpr int kCopyUnroll = 4;
 
 // dst[0, n) = src[0, n) by the whole grid, where src is 4-byte aligned and
 // readable up to 4 bytes past n, and dst (host memory) has any alignment:
@@ -154,21 +157,33 @@ __device__ void copy_bytes(uint8_t* dst, const uint8_t* src, uint64_t n, uint64_
   const uint32_t shift = (uint32_t)(head & 3);
   const uint32_t* s32 = reinterpret_cast<const uint32_t*>(src + (head & ~(uint64_t)3));
   u32x4_t* d16 = reinterpret_cast<u32x4_t*>(dst + head);
-  for (uint64_t j = i0; j < body; j += stride) {
-    const uint32_t* w = s32 + 4 * j;
-    const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3];
-    const uint32_t w4 = shift ? w[4] : 0u;
-    u32x4_t v;
-    if (shift) {
-      // byte `shift` of the 8-byte pair (hi:lo) onwards
-      v[0] = __builtin_amdgcn_alignbyte(w1, w0, shift);
-      v[1] = __builtin_amdgcn_alignbyte(w2, w1, shift);
-      v[2] = __builtin_amdgcn_alignbyte(w3, w2, shift);
-      v[3] = __builtin_amdgcn_alignbyte(w4, w3, shift);
-    } else {
-      v = u32x4_t{w0, w1, w2, w3};
+  // kCopyUnroll vectors per thread per round, all loaded before any store,
+  // so that the loads' latency overlaps
+  for (uint64_t j0 = i0; j0 < body; j0 += kCopyUnroll * stride) {
+    u32x4a_t w[kCopyUnroll];
+    uint32_t w4[kCopyUnroll];
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) {
+      const uint64_t j = j0 + u * stride;
+      w[u] = j < body ? *reinterpret_cast<const u32x4a_t*>(s32 + 4 * j) : u32x4a_t{0, 0, 0, 0};
+      w4[u] = (j < body && shift) ? s32[4 * j + 4] : 0u;
     }
-    __builtin_nontemporal_store(v, d16 + j);
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) {
+      const uint64_t j = j0 + u * stride;
+      if (j >= body) break;
+      u32x4_t v;
+      if (shift) {
+        // byte `shift` onwards of each 8-byte pair (hi:lo)
+        v[0] = __builtin_amdgcn_alignbyte(w[u][1], w[u][0], shift);
+        v[1] = __builtin_amdgcn_alignbyte(w[u][2], w[u][1], shift);
+        v[2] = __builtin_amdgcn_alignbyte(w[u][3], w[u][2], shift);
+        v[3] = __builtin_amdgcn_alignbyte(w4[u], w[u][3], shift);
+      } else {
+        v = u32x4_t{w[u][0], w[u][1], w[u][2], w[u][3]};
+      }
+      __builtin_nontemporal_store(v, d16 + j);
+    }
   }
 }
 
