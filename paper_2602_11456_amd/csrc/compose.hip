@@ -24,6 +24,7 @@ namespace aurora {
 constexpr int kCmpThreads = 256;
 constexpr int kCmpPer = 16;                          // merged positions per thread
 constexpr int kCmpTile = kCmpThreads * kCmpPer;      // 4096
+constexpr int kCmpLoad = 8;                          // staging loads in flight per thread
 
 struct ComposeArgs {
   const int64_t* a_idx;
@@ -107,8 +108,20 @@ __device__ __forceinline__ CmpTile cmp_load_tile(const ComposeArgs& a, uint64_t 
   t.positions = (uint32_t)(d1 - d0);
   t.ext = j1 < nb;
   const uint32_t nload = t.la + t.lb + (t.ext ? 1u : 0u);
-  for (uint32_t q = threadIdx.x; q < nload; q += kCmpThreads)
-    s_ab[q] = q < t.la ? a.a_idx[i0 + q] : a.b_idx[j0 + (q - t.la)];
+  // kCmpLoad loads per thread in flight before any LDS store
+  for (uint32_t q0 = 0; q0 < nload; q0 += kCmpThreads * kCmpLoad) {
+    int64_t v[kCmpLoad];
+#pragma unroll
+    for (int k = 0; k < kCmpLoad; ++k) {
+      const uint32_t q = q0 + threadIdx.x + kCmpThreads * k;
+      v[k] = q < nload ? (q < t.la ? a.a_idx[i0 + q] : a.b_idx[j0 + (q - t.la)]) : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kCmpLoad; ++k) {
+      const uint32_t q = q0 + threadIdx.x + kCmpThreads * k;
+      if (q < nload) s_ab[q] = v[k];
+    }
+  }
   __syncthreads();
   t.ok = true;
   return t;
@@ -178,8 +191,19 @@ __global__ __launch_bounds__(kCmpThreads) void compose_write_kernel(ComposeArgs 
   const uint64_t tile = blockIdx.x;
   const CmpTile t = cmp_load_tile(a, tile, na, nb, s_ab);
   if (!t.ok) return;   // uniform
-  for (uint32_t q = threadIdx.x; q < t.la + t.lb; q += kCmpThreads)
-    s_vab[q] = q < t.la ? a.a_val[t.i0 + q] : a.b_val[t.j0 + (q - t.la)];
+  for (uint32_t q0 = 0; q0 < t.la + t.lb; q0 += kCmpThreads * kCmpLoad) {
+    uint16_t v[kCmpLoad];
+#pragma unroll
+    for (int k = 0; k < kCmpLoad; ++k) {
+      const uint32_t q = q0 + threadIdx.x + kCmpThreads * k;
+      v[k] = q < t.la + t.lb ? (q < t.la ? a.a_val[t.i0 + q] : a.b_val[t.j0 + (q - t.la)]) : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kCmpLoad; ++k) {
+      const uint32_t q = q0 + threadIdx.x + kCmpThreads * k;
+      if (q < t.la + t.lb) s_vab[q] = v[k];
+    }
+  }
   __syncthreads();
   // merged position s of this thread: oi[s], ov[s]; bit s of keep: kept
   int64_t oi[kCmpPer];
