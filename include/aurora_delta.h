@@ -95,6 +95,16 @@ const char* delta_status_string(int status);
 /* Detail text of the last failed call on this thread ("" if none). */
 const char* delta_last_error(void);
 
+/* Timing aid for benchmarks and profilers: every later extract call
+ * (delta_extract, delta_extract_multi, delta_extract_fused and the
+ * pipeline's chunks) records `before` and `after` on its launch stream
+ * right around the launch of its scan kernel, the kernel that reads both
+ * copies; hipEventElapsedTime then gives that kernel's duration.  Both
+ * NULL turns it off.  Process-wide, not thread-safe: set it while no
+ * extract call is being enqueued.  Returns DELTA_ERR_INVALID_ARG if only
+ * one of the two is NULL. */
+delta_status_t delta_set_scan_events(hipEvent_t before, hipEvent_t after);
+
 /* Recommended workspace bytes for delta_extract over `numel` words (any
  * alignment): holds every tile's staged entries up to 12.5% changed words
  * (about numel / 2 bytes). */

@@ -69,6 +69,7 @@ SIGNATURES = {
     "delta_abi_version": (ctypes.c_int, []),
     "delta_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "delta_last_error": (ctypes.c_char_p, []),
+    "delta_set_scan_events": (STATUS, [P, P]),
     "delta_extract_workspace_bytes": (SZ, [U64]),
     "delta_extract_multi_workspace_bytes": (SZ, [P, I32]),
     "delta_apply_multi_workspace_bytes": (SZ, [I32]),

@@ -32,6 +32,13 @@ void set_error(const char* fmt, ...) {
 
 void clear_error() { g_last_error.clear(); }
 
+static hipEvent_t g_scan_events[2] = {nullptr, nullptr};
+
+hipError_t record_scan_event(int which, hipStream_t stream) {
+  const hipEvent_t ev = g_scan_events[which];
+  return ev ? hipEventRecord(ev, stream) : hipSuccess;
+}
+
 }  // namespace aurora
 
 namespace {
@@ -184,6 +191,14 @@ const char* delta_status_string(int status) {
 }
 
 const char* delta_last_error(void) { return g_last_error.c_str(); }
+
+delta_status_t delta_set_scan_events(hipEvent_t before, hipEvent_t after) {
+  if ((before == nullptr) != (after == nullptr))
+    return fail(DELTA_ERR_INVALID_ARG, "set both scan events or neither");
+  g_scan_events[0] = before;
+  g_scan_events[1] = after;
+  return ok();
+}
 
 size_t delta_extract_workspace_bytes(uint64_t numel) {
   return workspace_bytes(tiles_bound(numel), 1, kDefaultStageCap);

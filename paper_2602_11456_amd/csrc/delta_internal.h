@@ -207,6 +207,10 @@ hipError_t launch_compose_chain(const int64_t* const* idx, const uint16_t* const
                                 uint16_t* out_val, uint64_t capacity, uint64_t* d_count,
                                 uint32_t* err, char* ws, hipStream_t stream);
 
+// The timing aid of delta_set_scan_events: records the "before" (0) or
+// "after" (1) event on `stream` if it is set (abi.hip).
+hipError_t record_scan_event(int which, hipStream_t stream);
+
 // Thread-local detail text behind delta_last_error() (abi.hip).
 void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 void clear_error();

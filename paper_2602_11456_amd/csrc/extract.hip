@@ -517,9 +517,13 @@ hipError_t launch_group_scan(const uint64_t* counts, uint64_t num_tiles, uint64_
 template <typename IdxT, bool kMulti, bool kVec>
 static hipError_t launch_all(const ExtractArgs& a, hipStream_t stream) {
   const uint64_t groups = (a.num_tiles + kTilesPerGroup - 1) / kTilesPerGroup;
+  hipError_t e = record_scan_event(0, stream);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL((stage_kernel<kMulti, kVec>), dim3((uint32_t)a.num_tiles), dim3(kThreads),
                      0, stream, a);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = record_scan_event(1, stream);
   if (e != hipSuccess) return e;
   e = launch_group_scan(a.counts, a.num_tiles, a.group_sum, a.group_excl, a.d_count, stream);
   if (e != hipSuccess) return e;

@@ -40,6 +40,13 @@ def test_binding_declares_nothing_extra():
     assert set(_abi.SIGNATURES) == set(declared_functions())
 
 
+def test_scan_events_both_or_neither(lib):
+    assert lib.delta_set_scan_events(None, None) == _abi.DELTA_OK
+    assert lib.delta_set_scan_events(ctypes.c_void_p(8), None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_set_scan_events(None, ctypes.c_void_p(8)) == _abi.DELTA_ERR_INVALID_ARG
+    assert b"both" in lib.delta_last_error()
+
+
 def test_version_and_strings(lib):
     assert lib.delta_abi_version() == _abi.ABI_VERSION
     assert lib.delta_status_string(0) == b"DELTA_OK"
