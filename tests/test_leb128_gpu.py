@@ -134,9 +134,19 @@ def make_segments(numels, density, seed):
     return idx, np.array(offs, dtype=np.int64), bases
 
 
-@pytest.mark.parametrize("case", ["mixed", "empty_ends", "all_empty", "one"])
+@pytest.mark.parametrize("case", ["mixed", "empty_ends", "all_empty", "one", "many_tiny",
+                                  "few_hundred"])
 def test_segmented_matches_oracle(case):
-    if case == "mixed":
+    if case == "many_tiny":
+        # thousands of 1..199-word tensors: one 16 KiB decode tile spans far
+        # more segments than it caches, and a lane's 16 bytes open several
+        r = np.random.default_rng(11)
+        numels = [int(x) for x in r.integers(1, 200, size=3000)]
+        dens = [float(x) for x in r.choice([0.0, 0.01, 0.03, 0.2], size=3000)]
+    elif case == "few_hundred":
+        numels = [300] * 200 + [40_000]
+        dens = [0.05] * 200 + [0.01]
+    elif case == "mixed":
         numels = [5000, 1, 70_000, 12_345, 300_000, 4096, 77]
         dens = [0.01, 1.0, 0.05, 0.0, 0.02, 0.5, 0.3]
     elif case == "empty_ends":
