@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--density", type=float, default=0.01)
     ap.add_argument("--model", default="qwen3-8b")
+    ap.add_argument("--clustered", action="store_true",
+                    help="80%% of the changes in 5%% of the rows (the clustered Qwen3-8B set)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="oracle time budget for the CPU baseline sample")
@@ -443,7 +445,9 @@ def main():
         return 0
 
     t0 = time.time()
-    ws = synth.make_weight_set(args.model, args.density, seed=synth.config_seed(3), device=dev)
+    ws = synth.make_weight_set(args.model, args.density,
+                               seed=synth.config_seed(4 if args.clustered else 3), device=dev,
+                               clustered=args.clustered)
     torch.cuda.synchronize()
     N = ws.total
     K_planted = ws.total_planted
@@ -557,7 +561,10 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{args.model} weight set, {len(ws.prev)} tensors, {N} bf16 words, "
-                        f"{args.density:.2%} of words changed per tensor, int64 global indices",
+                        + (f"{args.density:.2%} of words changed, 80% of them in 5% of the rows"
+                           if args.clustered else
+                           f"{args.density:.2%} of words changed per tensor")
+                        + ", int64 global indices",
             "tensors": len(ws.prev),
             "words": N,
             "changed": K,
