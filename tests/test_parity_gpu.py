@@ -364,6 +364,37 @@ def test_pipeline_leb128_capacity_retry():
     np.testing.assert_array_equal(v.view(torch.int16).numpy().view(np.uint16), ref_val)
 
 
+@pytest.mark.parametrize("shift_idx,shift_val", [(1, 1), (3, 5), (0, 7)])
+def test_pipeline_host_arrays_at_odd_offsets(shift_idx, shift_val):
+    # host outputs that start inside a pinned buffer, off any 16-byte line:
+    # the delivery kernel's unaligned heads and tails and the device view of
+    # an interior host pointer
+    sizes = [70_001, 3, 50_000, 8192 * 3 + 1]
+    prevs, news = make_list(sizes, 0.03, seed=77)
+    ref_idx, ref_val, _, ref_cnt = oracle.extract_multi(
+        [host_u16(p) for p in prevs], [host_u16(q) for q in news])
+    big_i = torch.zeros(ref_cnt + 64, dtype=torch.int64, pin_memory=True)
+    big_v = torch.zeros(ref_cnt + 64, dtype=torch.int16, pin_memory=True)
+    h_idx = big_i[shift_idx:shift_idx + ref_cnt + 8]
+    h_val = big_v[shift_val:shift_val + ref_cnt + 8].view(torch.bfloat16)
+    i, v = ad.delta_extract_pipelined(prevs, news, chunk_elems=10_007, num_streams=3,
+                                      h_idx=h_idx, h_val=h_val)
+    np.testing.assert_array_equal(i.numpy(), ref_idx)
+    np.testing.assert_array_equal(v.view(torch.int16).numpy().view(np.uint16), ref_val)
+    # nothing outside the views was touched
+    assert not big_i[:shift_idx].any() and not big_v[:shift_val].any()
+    assert not big_i[shift_idx + ref_cnt:].any() and not big_v[shift_val + ref_cnt:].any()
+    hb_big = torch.zeros(3 * ref_cnt + 64, dtype=torch.uint8, pin_memory=True)
+    hb = hb_big[shift_val:]
+    b, v2, counts, used = ad.delta_extract_pipelined_leb128(prevs, news, chunk_elems=10_007,
+                                                           num_streams=3, h_bytes=hb,
+                                                           h_val=h_val)
+    ref_bytes, ref_counts = oracle_chunk_stream(ref_idx, used, sum(sizes))
+    np.testing.assert_array_equal(b.numpy(), ref_bytes)
+    np.testing.assert_array_equal(np.array(counts), ref_counts)
+    assert not hb_big[:shift_val].any() and not hb_big[shift_val + ref_bytes.size:].any()
+
+
 def test_pipeline_refuses_pageable_host_output():
     prevs, news = make_list([40_000, 20_000], 0.05, seed=10)
     h_idx = torch.empty(1000, dtype=torch.int64)   # pageable
