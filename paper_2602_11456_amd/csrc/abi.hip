@@ -150,7 +150,7 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
   a.group_excl = (uint64_t*)(ws + L.group_excl);
   a.stage = (uint32_t*)(ws + L.stage);
   hipError_t e;
-  if (descs.size() > 1) {
+  if (descs.size() > (size_t)kInlineDescs) {
     TensorDesc* table = (TensorDesc*)(ws + L.table);
     uint32_t* map = (uint32_t*)(ws + L.map);
     e = launch_upload_words((const uint64_t*)descs.data(), descs.size() * sizeof(TensorDesc) / 8,
@@ -161,7 +161,8 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
     a.table = table;
     a.tile_map = map;
   } else {
-    a.single = descs[0];
+    for (size_t i = 0; i < descs.size(); ++i) a.inl[i] = descs[i];
+    a.num_inline = (uint32_t)descs.size();
   }
   bool all_vec = true;
   for (const TensorDesc& t : descs) all_vec = all_vec && t.vec;

@@ -136,10 +136,15 @@ struct WordBatch {
 // Launchers (defined in extract.hip / apply.hip).  They enqueue on `stream`
 // and return the HIP error of the launch.
 // ---------------------------------------------------------------------------
+// Slices passed inside the kernel arguments when there are at most this
+// many (no table upload, no tile map).
+constexpr int kInlineDescs = 16;
+
 struct ExtractArgs {
-  const TensorDesc* table;     // device (multi) or nullptr (single)
-  const uint32_t* tile_map;    // device (multi) or nullptr (single)
-  TensorDesc single;           // used when table == nullptr
+  const TensorDesc* table;     // device table, or nullptr: the slices are in `inl`
+  const uint32_t* tile_map;    // device (with table) or nullptr
+  TensorDesc inl[kInlineDescs];   // used when table == nullptr
+  uint32_t num_inline;
   uint64_t num_tiles;
   uint32_t num_tensors;
   uint32_t stage_cap;          // entries a staging slot holds

@@ -117,11 +117,21 @@ __device__ __forceinline__ uint16_t word_of(const u32x4& q, int j) {
   return (uint16_t)(((j & 4) ? hi : lo) >> (16 * (j & 3)));
 }
 
+// Row of the inline slice holding `tile`: the last whose first tile is at
+// or below it.
+__device__ __forceinline__ uint32_t inline_row(const ExtractArgs& a, uint64_t tile) {
+  uint32_t r = 0;
+#pragma unroll
+  for (int k = 1; k < kInlineDescs; ++k)   // unrolled: all loads issue at once
+    r = ((uint32_t)k < a.num_inline && tile >= a.inl[k].first_tile) ? (uint32_t)k : r;
+  return r;
+}
+
 // Descriptor of the slice holding `tile`.  The tile id is uniform across
 // the wavefront, so every field is moved to scalar registers.
 template <bool kMulti>
 __device__ __forceinline__ TensorDesc tile_desc(const ExtractArgs& a, uint64_t tile) {
-  if (!kMulti) return a.single;
+  if (!kMulti) return a.inl[__builtin_amdgcn_readfirstlane(inline_row(a, tile))];
   const uint32_t row = __builtin_amdgcn_readfirstlane(a.tile_map[tile]);
   const uint32_t* src = reinterpret_cast<const uint32_t*>(a.table + row);
   TensorDesc d;
@@ -322,13 +332,60 @@ __global__ __launch_bounds__(kScanThreads) void group_scan_kernel(const uint64_t
   if (threadIdx.x == 0) *d_count = total;
 }
 
+// Up to 1024 groups (65536 tiles): the group sums and their scan in one
+// workgroup, one launch instead of two.  Wavefront w sums groups w, w + 16,
+// ... (4 of them per round, loads coalesced), into LDS; then every thread
+// scans one group.
+constexpr uint64_t kSmallScanGroups = kScanThreads;
+
+template <typename CountT>
+__global__ __launch_bounds__(kScanThreads) void tile_scan_kernel(const CountT* counts,
+                                                                 uint64_t num_tiles,
+                                                                 uint64_t* group_excl,
+                                                                 uint64_t* d_count) {
+  __shared__ uint64_t s_g[kSmallScanGroups];
+  __shared__ uint64_t s_wave[kScanWaves];
+  const uint32_t lane = lane_id();
+  const uint32_t wave = threadIdx.x >> 6;
+  const uint64_t groups = groups_for(num_tiles);
+  for (uint64_t g0 = wave; g0 < groups; g0 += 4 * kScanWaves) {
+    uint64_t v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint64_t g = g0 + k * kScanWaves;
+      const uint64_t t = g * kTilesPerGroup + lane;
+      v[k] = (g < groups && t < num_tiles) ? (uint64_t)counts[t] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint64_t g = g0 + k * kScanWaves;
+      const uint64_t sum = wave_sum64(v[k]);
+      if (lane == 0 && g < groups) s_g[g] = sum;
+    }
+  }
+  __syncthreads();
+  const uint64_t x0 = threadIdx.x < groups ? s_g[threadIdx.x] : 0;
+  uint64_t x = x0;
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) {
+    const uint64_t y = __shfl_up(x, s);
+    if ((int)lane >= s) x += y;
+  }
+  if (lane == 63) s_wave[wave] = x;
+  __syncthreads();
+  uint64_t carry = 0;
+  for (uint32_t w = 0; w < wave; ++w) carry += s_wave[w];
+  if (threadIdx.x < groups) group_excl[threadIdx.x] = carry + x - x0;
+  if (threadIdx.x == kScanThreads - 1) *d_count = carry + x;
+}
+
 // ------------------------------------------------------------- finalize
 
 // Output index of word 0 of `tile`, read by one lane (tile ids differ per
 // lane here, so the descriptor stays in vector registers).
 template <bool kMulti>
 __device__ __forceinline__ TensorDesc lane_desc(const ExtractArgs& a, uint64_t tile) {
-  return kMulti ? a.table[a.tile_map[tile]] : a.single;
+  return kMulti ? a.table[a.tile_map[tile]] : a.inl[inline_row(a, tile)];
 }
 
 constexpr int kFinBatch = 8;
@@ -495,6 +552,11 @@ static hipError_t launch_group_scan_t(const CountT* counts, uint64_t num_tiles,
                                       uint64_t* group_sum, uint64_t* group_excl,
                                       uint64_t* d_total, hipStream_t stream) {
   const uint64_t groups = groups_for(num_tiles);
+  if (groups <= kSmallScanGroups) {
+    hipLaunchKernelGGL(tile_scan_kernel<CountT>, dim3(1), dim3(kScanThreads), 0, stream, counts,
+                       num_tiles, group_excl, d_total);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(group_sum_kernel<CountT>, dim3((uint32_t)groups), dim3(64), 0, stream,
                      counts, num_tiles, group_sum);
   hipError_t e = hipGetLastError();
