@@ -108,14 +108,34 @@ struct TileSegs {
   bool cached;
 };
 
+// seg_of by a whole wavefront: 64 evenly spaced candidates per round, so
+// that a table of up to 4096 segments takes two dependent loads, not twelve.
+__device__ __forceinline__ uint32_t seg_of_wave(const LebSegs& g, uint64_t k) {
+  if (g.num == 0) return 0;
+  uint32_t lo = 0, hi = g.num;   // the answer is in [lo, hi)
+  while (hi - lo > 1) {
+    const uint32_t step = (hi - lo + 63) / 64;
+    const uint32_t cand = lo + lane_id() * step;
+    const uint64_t m = __ballot(cand < hi && g.offs[cand] <= k);
+    const uint32_t last = m ? 63 - __builtin_clzll(m) : 0;
+    lo = lo + last * step;
+    hi = lo + step < hi ? lo + step : hi;
+  }
+  return lo;
+}
+
 // Block-wide: contains barriers when there are segments.  e0 < e1.
 __device__ __forceinline__ TileSegs tile_segs(const LebSegs& g, uint64_t e0, uint64_t e1,
                                               uint64_t* s_lo, uint32_t* s_meta) {
   TileSegs c{0, 0, false};
   if (g.num == 0) return c;
-  if (threadIdx.x == 0) {
-    s_meta[0] = seg_of(g, e0);
-    s_meta[1] = seg_of(g, e1 - 1);
+  if (threadIdx.x < 64) {   // wavefront 0
+    const uint32_t first = seg_of_wave(g, e0);
+    const uint32_t last = seg_of_wave(g, e1 - 1);
+    if (threadIdx.x == 0) {
+      s_meta[0] = first;
+      s_meta[1] = last;
+    }
   }
   __syncthreads();
   c.first = s_meta[0];
@@ -300,6 +320,13 @@ __global__ __launch_bounds__(kLebThreads) void enc_write_kernel(EncArgs a) {
   for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
     const uint64_t t0 = tile * kEncTile;
     const uint64_t t1 = t0 + kEncTile < count ? t0 + kEncTile : count;
+    // the tile's output position: its group's offset plus the byte counts
+    // of the group's earlier tiles, loaded now so that the loads overlap
+    // the segment lookup and the index loads
+    const uint64_t gt = tile / kTilesPerGroup * kTilesPerGroup + lane;
+    const uint64_t before_part = (wave == 0 && gt < tile) ? (uint64_t)a.tile_bytes[gt] : 0;
+    const uint64_t gexcl = a.group_excl[tile / kTilesPerGroup];
+    const uint64_t total = a.tile_bytes[tile];
     const TileSegs c = tile_segs(a.segs, t0, t1, s_lo, s_meta);
     const uint64_t kw = t0 + (uint64_t)wave * kEncWave + lane;
     uint64_t gap[kEncSteps];
@@ -308,9 +335,12 @@ __global__ __launch_bounds__(kLebThreads) void enc_write_kernel(EncArgs a) {
     uint32_t bytes = enc_gaps(a, c, s_lo, kw, t1, gap, starts, bad);
     bytes = wave_sum(bytes);
     if (lane == 0) s_wave[wave] = bytes;
-    const uint64_t tile_pos = a.group_excl[tile / kTilesPerGroup] +
-                              group_before(a.tile_bytes, tile, &s_before);   // barrier
-    const uint64_t total = a.tile_bytes[tile];
+    if (wave == 0) {
+      const uint64_t b = wave_sum(before_part);
+      if (lane == 0) s_before = b;
+    }
+    __syncthreads();
+    const uint64_t tile_pos = gexcl + s_before;
     const bool staged = total <= (uint64_t)kEncLds;
     uint64_t pos = 0;   // within the tile
     for (uint32_t w = 0; w < wave; ++w) pos += s_wave[w];
