@@ -20,11 +20,15 @@
  *                  the delta's declared base version (Sec. 5.2).
  *   extract_pipelined
  *                  extract_multi split into fixed-size chunks of the global
- *                  index space, spread round-robin over several streams,
- *                  each chunk's streams copied into pinned host memory as
- *                  soon as it is done (Sec. 5.2, "Overlapped extraction and
- *                  transfer": segments emitted as soon as they are encoded
- *                  and striped round-robin).
+ *                  index space, extracted on two streams while a third
+ *                  stores each finished chunk's streams into pinned host
+ *                  memory (Sec. 5.2, "Overlapped extraction and transfer":
+ *                  segments emitted as soon as they are encoded).
+ *   leb128, compose, artifacts, fused
+ *                  the gap + LEB128 index coding (Sec. 5.1), composition
+ *                  of a chain of deltas (Sec. 5.4), versioned hashed
+ *                  artifacts (Sec. 5.1, 5.2) and extraction straight into
+ *                  fused inference tensors (Sec. 5.1).
  *
  * Conventions (all functions):
  *   - bf16 data crosses the ABI as raw uint16_t bit patterns.  "Changed"
@@ -39,7 +43,8 @@
  *   - Index order is the flattened storage order of each tensor (row-major
  *     for a C-contiguous tensor).  Output indices are strictly increasing.
  *   - The caller owns all memory.  No entry point allocates device memory;
- *     scratch space is a caller-provided, 256-byte aligned `workspace`.
+ *     scratch space is a caller-provided, 256-byte aligned `workspace`
+ *     (the pipelines call it `d_staging`).
  *     The matching *_workspace_bytes function returns the recommended size.
  *     Extract also accepts a smaller workspace (down to a few tens of bytes
  *     per 8192-word tile; below that DELTA_ERR_WORKSPACE): it then keeps
