@@ -1,0 +1,105 @@
+"""HIP graph capture: extract and apply recorded once into a graph and
+replayed, with the program's own eager work and synchronisations between
+the replays; every replay is checked against the CPU oracle on the data it
+saw.  The library's extract and apply launch only kernels (no memset, no
+host wait, no allocation), so they can be captured."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2602_11456_amd as ad
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def host_u16(t):
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16).reshape(-1)
+
+
+def fill_random(ts, seed):
+    """Random words in place."""
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    for t in ts:
+        t.view(torch.int16).copy_(torch.randint(-32768, 32767, t.shape, device=DEV,
+                                                generator=g, dtype=torch.int16))
+
+
+@pytest.mark.parametrize("sizes", [[70_001, 3, 50_000, 8192 * 3 + 1],        # inline slices
+                                   [3000 + 17 * i for i in range(40)]])     # tensor table
+def test_extract_multi_graph_replays(sizes):
+    prevs = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    news = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    fill_random(prevs, 1)
+    for p, q in zip(prevs, news):
+        q.copy_(p)
+    plan = ad.MultiPlan(prevs, news)
+    cap = sum(sizes)
+    out_idx = torch.empty(cap, dtype=torch.int64, device=DEV)
+    out_val = torch.empty(cap, dtype=torch.bfloat16, device=DEV)
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    offs = torch.zeros(plan.T + 1, dtype=torch.int64, device=DEV)
+    work = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        ad.delta_extract_multi_into(plan, out_idx, out_val, cnt, work, offs, stream=s)
+    s.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        ad.delta_extract_multi_into(plan, out_idx, out_val, cnt, work, offs, stream=s)
+    for rep, density in enumerate([0.01, 0.2, 0.0, 0.05]):
+        # eager work between replays: new contents for the captured buffers
+        g = torch.Generator(device=DEV)
+        g.manual_seed(100 + rep)
+        for p, q in zip(prevs, news):
+            q.copy_(p)
+            m = torch.rand(q.shape, device=DEV, generator=g) < density
+            q.view(torch.int16)[m] ^= 0x0101
+        out_idx.fill_(-5)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        ref_idx, ref_val, ref_offs, ref_cnt = oracle.extract_multi(
+            [host_u16(p) for p in prevs], [host_u16(q) for q in news])
+        assert int(cnt.item()) == ref_cnt, rep
+        np.testing.assert_array_equal(out_idx[:ref_cnt].cpu().numpy(), ref_idx)
+        np.testing.assert_array_equal(host_u16(out_val[:ref_cnt]), ref_val)
+        np.testing.assert_array_equal(offs.cpu().numpy(), ref_offs)
+
+
+def test_apply_multi_graph_replays():
+    sizes = [70_001, 3, 50_000, 8192 * 3 + 1]
+    prevs = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    fill_random(prevs, 2)
+    news = [p.clone() for p in prevs]
+    g = torch.Generator(device=DEV)
+    g.manual_seed(7)
+    for q in news:
+        m = torch.rand(q.shape, device=DEV, generator=g) < 0.02
+        q.view(torch.int16)[m] ^= 0x00FF
+    idx, val, _ = ad.delta_extract_multi(prevs, news)
+    rollout = [torch.empty_like(p) for p in prevs]
+    work = torch.empty(max(ad.delta_apply_multi_workspace_bytes(len(sizes)), 1),
+                       dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        ad.delta_apply_multi(rollout, idx, val, workspace=work, stream=s)
+    s.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        ad.delta_apply_multi(rollout, idx, val, workspace=work, stream=s)
+    for rep in range(3):
+        for r, p in zip(rollout, prevs):   # eager work: back to the old weights
+            r.copy_(p)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        ref = [host_u16(p).copy() for p in prevs]
+        assert oracle.apply_multi_(ref, idx.cpu().numpy(), host_u16(val)) == 0
+        for r, w in zip(rollout, ref):
+            np.testing.assert_array_equal(host_u16(r), w)
