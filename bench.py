@@ -200,7 +200,7 @@ def pipeline_measurement(args, dev):
     }
 
 
-def leb128_measurement(ad, idx, d_offs, numels, stream, reps):
+def leb128_measurement(ad, idx, val, d_offs, numels, rollout, stream, reps):
     """Gap + LEB128 encode of the extracted global indices with one segment
     per tensor (tensor-local first index), then decode, each timed with HIP
     events on the launch stream; the decode must return the indices."""
@@ -245,16 +245,40 @@ def leb128_measurement(ad, idx, d_offs, numels, stream, reps):
     stream.synchronize()
     if int(cnt.item()) != K or int(flag.item()) or not torch.equal(out[:K], idx):
         raise RuntimeError("LEB128 decode does not return the extracted indices")
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
-    for e0, e1, e2 in ev:
+    # decode-in-apply onto the rollout copy (idempotent), against decode +
+    # apply of the decoded indices
+    apply_ws = torch.empty(ad.delta_apply_leb128_multi_workspace_bytes(nb, T), dtype=torch.uint8,
+                           device=dev)
+    multi_ws = torch.empty(max(ad.delta_apply_multi_workspace_bytes(T), 1), dtype=torch.uint8,
+                           device=dev)
+    flag2 = torch.zeros(1, dtype=torch.int32, device=dev)
+    code = buf[:nb]
+
+    def apply_coded():
+        ad.delta_apply_leb128_multi(rollout, code, d_offs, bases, val, error_flag=flag2,
+                                    workspace=apply_ws, stream=stream)
+
+    apply_coded()
+    stream.synchronize()
+    if int(flag2.item()):
+        raise RuntimeError("decode-in-apply flagged an error")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(reps)]
+    for e0, e1, e2, e3, e4 in ev:
         e0.record(stream)
         encode()
         e1.record(stream)
         decode()
         e2.record(stream)
+        apply_coded()
+        e3.record(stream)
+        ad.delta_apply_multi(rollout, out[:K], val, workspace=multi_ws, stream=stream)
+        e4.record(stream)
     stream.synchronize()
-    enc = sorted(e0.elapsed_time(e1) for e0, e1, _ in ev)[reps // 2]
-    dec = sorted(e1.elapsed_time(e2) for _, e1, e2 in ev)[reps // 2]
+    med = lambda xs: sorted(xs)[len(xs) // 2]
+    enc = med([e[0].elapsed_time(e[1]) for e in ev])
+    dec = med([e[1].elapsed_time(e[2]) for e in ev])
+    app_coded = med([e[2].elapsed_time(e[3]) for e in ev])
+    app_plain = med([e[3].elapsed_time(e[4]) for e in ev])
     return {
         "workload": f"the {K} extracted int64 global indices, one segment per tensor",
         "bytes": nb,
@@ -264,6 +288,8 @@ def leb128_measurement(ad, idx, d_offs, numels, stream, reps):
         # encode reads the indices (twice: sizes, then bytes) and writes the bytes
         "encode_GBps_algorithmic": round((8 * K + nb) / (enc / 1e3) / 1e9, 1),
         "decode_GBps_algorithmic": round((nb + 8 * K) / (dec / 1e3) / 1e9, 1),
+        "apply_from_code_ms": round(app_coded, 4),
+        "decode_then_apply_ms": round(dec + app_plain, 4),
     }
 
 
@@ -412,8 +438,8 @@ def extras(args, ad, synth, ws, rollout, plan, out_idx, out_val, d_offs, work, s
     hashing, the fused layout and delta chains (the last one overwrites the
     rollout copy)."""
     import torch
-    result["leb128"] = leb128_measurement(ad, out_idx[:K], d_offs, plan.numels, stream,
-                                          args.steps)
+    result["leb128"] = leb128_measurement(ad, out_idx[:K], out_val[:K], d_offs, plan.numels,
+                                          rollout, stream, args.steps)
     # the delta's two streams as one byte buffer, as an artifact holds them
     payload = torch.cat([out_idx[:K].view(torch.uint8), out_val[:K].view(torch.uint8)])
     result["hash"] = hash_measurement(ad, payload, stream, args.steps)

@@ -293,6 +293,38 @@ delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
  * that has it (the last writer wins).  delta_compose builds that delta.
  */
 
+/* Workspace bytes for delta_apply_leb128_multi of `nbytes` code bytes onto
+ * `num_tensors` tensors. */
+size_t delta_apply_leb128_workspace_bytes(uint64_t nbytes, int32_t num_tensors);
+
+/*
+ * delta_apply_leb128_multi — Sec. 5.1 / 5.2 on the receiving side: apply a
+ * delta whose indices arrive gap + LEB128 coded straight into the tensor
+ * list, decoding them on the fly (no index stream is materialised).
+ *   weight_ptrs, numels, num_tensors  as delta_apply_multi (host arrays);
+ *                 the decoded indices are global over the concatenation.
+ *   code, nbytes  device bytes of the coded indices.
+ *   d_seg_offsets, d_seg_bases, num_segs  the segments, as for
+ *                 delta_leb128_decode: one per tensor (seg_offsets =
+ *                 tensor_offsets, seg_bases = tensor bases) as
+ *                 delta_leb128_encode writes them for delta_extract_multi's
+ *                 output, or one per chunk as the coded pipeline writes
+ *                 them (seg_bases[c] = c * chunk).
+ *   val, count    device words [count]: entry k's new word.
+ *   d_error_flag  device, nullable: set when the stream is malformed, when
+ *                 it holds a number of entries other than `count`, or when
+ *                 an index falls outside the tensor list (those words are
+ *                 skipped).
+ * Enqueues on `stream`; apply(W, delta) == delta_apply_multi(W, decode(code), val).
+ */
+delta_status_t delta_apply_leb128_multi(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                        int32_t num_tensors, const uint8_t* code, uint64_t nbytes,
+                                        const uint64_t* d_seg_offsets,
+                                        const uint64_t* d_seg_bases, uint32_t num_segs,
+                                        const uint16_t* val, uint64_t count,
+                                        uint32_t* d_error_flag, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
 /* Workspace bytes for delta_compose of `num_deltas` deltas with these entry
  * counts (host array); 0 if the arguments are invalid. */
 size_t delta_compose_workspace_bytes(const uint64_t* counts, int32_t num_deltas);

@@ -29,6 +29,7 @@ __all__ = [
     "delta_extract_pipelined", "delta_extract_workspace_bytes",
     "delta_extract_multi_workspace_bytes", "delta_apply_multi_workspace_bytes",
     "delta_pipeline_staging_bytes", "MultiPlan", "delta_leb128_encode", "delta_leb128_decode",
+    "delta_apply_leb128_multi", "delta_apply_leb128_multi_workspace_bytes",
     "delta_extract_pipelined_leb128", "delta_pipeline_leb128_staging_bytes", "chunk_segments",
     "delta_compose", "delta_compose_workspace_bytes", "delta_catch_up",
     "delta_hash_segments", "delta_artifact_layout", "pack_artifact", "read_artifact_header",
@@ -456,6 +457,45 @@ def delta_leb128_decode(buf: torch.Tensor, seg_offsets=None, seg_bases=None,
     if k > cap:
         raise DeltaError(_abi.DELTA_ERR_CAPACITY, f"{k} numbers do not fit {cap}")
     return out[:k]
+
+
+def delta_apply_leb128_multi_workspace_bytes(nbytes: int, num_tensors: int) -> int:
+    return int(library().delta_apply_leb128_workspace_bytes(int(nbytes), int(num_tensors)))
+
+
+def delta_apply_leb128_multi(weights: Sequence[torch.Tensor], code: torch.Tensor, seg_offsets,
+                             seg_bases, val: torch.Tensor, check: bool = False,
+                             error_flag: Optional[torch.Tensor] = None,
+                             workspace: Optional[torch.Tensor] = None,
+                             stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Apply a delta whose indices are gap + LEB128 coded (Sec. 5.1) straight
+    into a tensor list, decoding them on the fly (Sec. 5.2 activation on the
+    receiving side).  ``seg_offsets`` / ``seg_bases`` as for
+    :func:`delta_leb128_decode`.  With ``check`` it synchronises and raises
+    DeltaError on a malformed stream, a count mismatch or an index outside
+    the tensors."""
+    if code.dtype != torch.uint8 or not code.is_cuda or not code.is_contiguous():
+        raise TypeError("code must be a contiguous uint8 GPU tensor")
+    T = len(weights)
+    dev = code.device
+    offs, bases, S = _segs(seg_offsets, seg_bases, dev)
+    ptrs = _ptr_array([_words(w, f"weights[{i}]") for i, w in enumerate(weights)])
+    numels = _u64_array([w.numel() for w in weights])
+    need = delta_apply_leb128_multi_workspace_bytes(code.numel(), T)
+    ws = workspace if workspace is not None else _workspace(need, dev)
+    flag = error_flag
+    if check and flag is None:
+        flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    _check(library().delta_apply_leb128_multi(
+        ptrs, numels, T, code.data_ptr(), code.numel(), offs.data_ptr() if S else None,
+        bases.data_ptr() if S else None, S, _words(val, "val"), val.numel(),
+        flag.data_ptr() if flag is not None else None, ws.data_ptr(),
+        ws.numel() * ws.element_size(), _stream(stream)))
+    if check:
+        (stream or torch.cuda.current_stream()).synchronize()
+        if int(flag.item()) != 0:
+            raise DeltaError(_abi.DELTA_ERR_INVALID_ARG,
+                             "malformed stream, count mismatch or index outside the tensors")
 
 
 # ------------------------------------------------------------ pipeline

@@ -83,6 +83,9 @@ SIGNATURES = {
     "delta_leb128_decode_workspace_bytes": (SZ, [U64, U64, ctypes.c_uint32]),
     "delta_leb128_encode": (STATUS, [P, U64, P, P, ctypes.c_uint32, P, U64, P, P, P, P, SZ, P]),
     "delta_leb128_decode": (STATUS, [P, U64, P, P, ctypes.c_uint32, P, U64, P, P, P, SZ, P]),
+    "delta_apply_leb128_workspace_bytes": (SZ, [U64, I32]),
+    "delta_apply_leb128_multi": (STATUS, [P, P, I32, P, U64, P, P, ctypes.c_uint32, P, U64, P, P,
+                                          SZ, P]),
     "delta_compose_workspace_bytes": (SZ, [P, I32]),
     "delta_compose": (STATUS, [P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
     "delta_artifact_layout": (STATUS, [U64, U64, U64, U64, ctypes.POINTER(delta_artifact_layout_t)]),

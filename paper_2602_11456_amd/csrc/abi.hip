@@ -469,6 +469,78 @@ delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
   return ok();
 }
 
+// Workspace of delta_apply_leb128_multi: the decoder's, then the tensor
+// bases (T + 1) and pointers (T), then the decoded entry count.
+struct ApplyLebLayout {
+  size_t dec, bases, ptrs, count, total;
+};
+static ApplyLebLayout apply_leb_layout(uint64_t nbytes, int32_t T) {
+  ApplyLebLayout L;
+  L.dec = 0;
+  L.bases = align_up(dec_layout(nbytes).total);
+  L.ptrs = align_up(L.bases + 8 * (uint64_t)(T + 1));
+  L.count = align_up(L.ptrs + 8 * (uint64_t)T);
+  L.total = align_up(L.count + 8);
+  return L;
+}
+
+size_t delta_apply_leb128_workspace_bytes(uint64_t nbytes, int32_t num_tensors) {
+  if (num_tensors < 0) return 0;
+  return apply_leb_layout(nbytes, num_tensors).total;
+}
+
+delta_status_t delta_apply_leb128_multi(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                        int32_t num_tensors, const uint8_t* code, uint64_t nbytes,
+                                        const uint64_t* d_seg_offsets,
+                                        const uint64_t* d_seg_bases, uint32_t num_segs,
+                                        const uint16_t* val, uint64_t count,
+                                        uint32_t* d_error_flag, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  if (num_tensors < 0 || (num_tensors > 0 && (!weight_ptrs || !numels)))
+    return fail(DELTA_ERR_INVALID_ARG, "bad tensor list");
+  if (nbytes > 0 && !code) return fail(DELTA_ERR_INVALID_ARG, "code is NULL");
+  if (count > 0 && !val) return fail(DELTA_ERR_INVALID_ARG, "val is NULL");
+  if (num_segs > 0 && (!d_seg_offsets || !d_seg_bases))
+    return fail(DELTA_ERR_INVALID_ARG, "segment arrays are NULL");
+  if (nbytes == 0 && count > 0)
+    return fail(DELTA_ERR_INVALID_ARG, "%llu values but an empty index stream",
+                (unsigned long long)count);
+  std::vector<uint64_t> bases((size_t)num_tensors + 1, 0);
+  std::vector<uint64_t> ptrs((size_t)num_tensors, 0);
+  for (int32_t t = 0; t < num_tensors; ++t) {
+    if (numels[t] > 0 && (!weight_ptrs[t] || odd(weight_ptrs[t])))
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: NULL or odd pointer", t);
+    bases[t + 1] = bases[t] + numels[t];
+    ptrs[t] = (uint64_t)(uintptr_t)weight_ptrs[t];
+  }
+  const DecLayout D = dec_layout(nbytes);
+  if (D.btiles > 0xFFFFFFFFull / 256) return fail(DELTA_ERR_INVALID_ARG, "stream too long");
+  const ApplyLebLayout L = apply_leb_layout(nbytes, num_tensors);
+  delta_status_t st = check_workspace(workspace, workspace_bytes, L.total);
+  if (st != DELTA_OK) return st;
+  if (nbytes == 0) return ok();   // nothing to apply
+  char* ws = (char*)workspace;
+  hipError_t e = launch_upload_words(bases.data(), bases.size(), (uint64_t*)(ws + L.bases), stream);
+  if (e == hipSuccess && num_tensors > 0)
+    e = launch_upload_words(ptrs.data(), ptrs.size(), (uint64_t*)(ws + L.ptrs), stream);
+  if (e != hipSuccess) return hip_fail(e, "table upload launch");
+  DecArgs a;
+  memset(&a, 0, sizeof(a));
+  a.in = code;
+  a.nbytes = nbytes;
+  a.segs = {d_seg_offsets, d_seg_bases, num_segs, 0};
+  a.capacity = count;
+  a.d_count = (uint64_t*)(ws + L.count);
+  a.err = d_error_flag;
+  a.ptrs = (uint16_t* const*)(ws + L.ptrs);
+  a.tbases = (const uint64_t*)(ws + L.bases);
+  a.num_tensors = (uint32_t)num_tensors;
+  a.val = val;
+  e = launch_leb128_decode(a, D, ws + L.dec, stream, true);
+  if (e != hipSuccess) return hip_fail(e, "leb128 apply launch");
+  return ok();
+}
+
 size_t delta_compose_workspace_bytes(const uint64_t* counts, int32_t num_deltas) {
   if (num_deltas < 0 || (num_deltas > 0 && !counts)) return 0;
   return chain_layout(counts, num_deltas).total;

@@ -44,6 +44,13 @@ struct DecArgs {
   uint64_t* tile_v;             // segmented sum of the tile's terms
   uint32_t* wave_f;             // the same per wavefront of a tile (4 per tile)
   uint64_t* wave_v;
+  // Decode-in-apply (launch_leb128_decode with apply set): instead of
+  // writing index k, write val[k] to the word of the tensor list that
+  // decoded index names.
+  uint16_t* const* ptrs;        // device [num_tensors]
+  const uint64_t* tbases;       // device [num_tensors + 1]: first index of each tensor, total
+  uint32_t num_tensors;
+  const uint16_t* val;          // device [capacity]
   uint64_t* gexcl_v;            // index just before each group of tiles
 };
 
@@ -62,6 +69,10 @@ EncLayout enc_layout(uint64_t count);
 DecLayout dec_layout(uint64_t nbytes);
 hipError_t launch_leb128_encode(EncArgs a, uint64_t* group_sum, uint64_t* group_excl,
                                 hipStream_t stream);
-hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStream_t stream);
+// Decodes a.in; writes the indices to a.out, or, with `apply`, applies
+// a.val to the tensors a.ptrs (capacity = entries of a.val; a stream with
+// another entry count raises a.err).
+hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStream_t stream,
+                                bool apply = false);
 
 }  // namespace aurora

@@ -909,6 +909,128 @@ __global__ __launch_bounds__(kLebThreads) void dec_write_kernel(DecArgs a, bool 
   }
 }
 
+// Global index -> tensor holding it (tbases[t] <= y < tbases[t + 1]).
+__device__ __forceinline__ uint32_t dec_find_tensor(const uint64_t* tbases, uint32_t T,
+                                                    uint64_t y) {
+  uint32_t lo = 0, hi = T;
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (tbases[mid] <= y) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+// Decode-in-apply: decodes like dec_write_kernel, but every number's
+// index y receives its entry's word, w[y] = val[k] in the tensor holding
+// y, with no index stream written.  Each step's indices are staged in LDS
+// so that, as in the plain apply, every store instruction covers 64
+// consecutive entries and the words are loaded coalesced.  Entries past
+// the value count, indices outside the tensor list, and a stream whose
+// entry count differs from the value count raise the error flag; those
+// words are left alone.
+__global__ __launch_bounds__(kLebThreads) void dec_apply_kernel(DecArgs a, bool aligned) {
+  __shared__ __align__(16) uint8_t s_bytes[kDecBack + kDecTile];
+  __shared__ uint64_t s_lo[kSegLds];
+  __shared__ uint32_t s_meta[2];
+  __shared__ uint32_t s_wterm[kLebWaves];
+  __shared__ uint64_t s_tmp;
+  __shared__ uint64_t s_carry;
+  __shared__ uint64_t s_out[kLebWaves][kDecStepEntries];
+  const uint64_t tile = blockIdx.x;
+  if (tile == 0 && threadIdx.x == 0 && *a.d_count != a.capacity) raise_flag(a.err);
+  const uint32_t terms = a.tile_terms[tile];
+  if (terms == 0) return;   // uniform
+  const uint64_t b0 = tile * kDecTile;
+  dec_load_tile(a, b0, aligned, s_bytes);                                    // barrier
+  const uint64_t e0 = a.group_excl[tile / kTilesPerGroup] +
+                      group_before(a.tile_terms, tile, &s_tmp);              // barrier
+  if (e0 >= a.capacity) {   // uniform: no value for any entry of this tile
+    if (threadIdx.x == 0) raise_flag(a.err);
+    return;
+  }
+  const uint32_t lane = lane_id(), wave = wave_id();
+  if (threadIdx.x < 64) {   // index of the entry just before the tile
+    const uint64_t g = tile / kTilesPerGroup;
+    uint32_t f;
+    uint64_t v;
+    seg_fold_tiles(a.tile_f, a.tile_v, g * kTilesPerGroup, tile, f, v);
+    if (threadIdx.x == 0) s_carry = f ? v : a.gexcl_v[g] + v;
+  }
+  const uint32_t wt = dec_wave_terms(s_bytes, b0, a.nbytes);
+  if (lane == 0) s_wterm[wave] = wt;
+  __syncthreads();
+  const TileSegs c = tile_segs(a.segs, e0, e0 + terms, s_lo, s_meta);     // barriers
+  const uint64_t ew = dec_wave_e0(e0, s_wterm);
+  uint64_t run = s_carry;
+  for (uint32_t w = 0; w < wave; ++w)
+    run = a.wave_f[tile * kLebWaves + w] ? a.wave_v[tile * kLebWaves + w]
+                                         : run + a.wave_v[tile * kLebWaves + w];
+  const uint64_t total = a.tbases[a.num_tensors];
+  bool bad = false;
+  uint32_t t = 0;                 // the tensor [lo, hi) last written by this lane
+  uint64_t lo = 1, hi = 0;
+  uint16_t* base_ptr = nullptr;
+  uint64_t* so = s_out[wave];
+  uint64_t e = ew;
+  for (int it = 0; it < kDecSteps; ++it) {
+    const uint64_t e_step = e;
+    LaneDec d;
+    dec_lane_step(a, s_bytes, b0, it, e, d, bad);
+    uint32_t lf;
+    uint64_t lv;
+    lane_fold(a, c, s_lo, d, lf, lv);
+    uint32_t sf = lf;
+    uint64_t sv = lv;
+    wave_seg_scan(sf, sv);
+    uint32_t xf = __shfl_up(sf, 1);
+    uint64_t xv = __shfl_up(sv, 1);
+    if (lane == 0) {
+      xf = 0;
+      xv = 0;
+    }
+    uint64_t y = xf ? xv : run + xv;
+    const uint32_t f63 = __shfl(sf, 63);
+    const uint64_t v63 = __shfl(sv, 63);
+    run = f63 ? v63 : run + v63;
+    if (d.ends) {
+      SegCursor r = seg_cursor(a.segs, c, s_lo, d.e);
+      uint64_t k = d.e;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        if ((d.ends >> j) & 1u) {
+          int64_t base;
+          y = seg_step(a.segs, c, s_lo, r, k, base) ? d.num[j] + (uint64_t)base : y + d.num[j];
+          so[k - e_step] = y;
+          ++k;
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const uint32_t n = (uint32_t)(e - e_step);
+    for (uint32_t i = lane; i < n; i += 64) {
+      const uint64_t k = e_step + i;
+      const uint64_t yi = so[i];
+      if (k < a.capacity && yi < total) {
+        if (!(yi >= lo && yi < hi)) {
+          t = dec_find_tensor(a.tbases, a.num_tensors, yi);
+          lo = a.tbases[t];
+          hi = a.tbases[t + 1];
+          base_ptr = a.ptrs[t];
+        }
+        __builtin_nontemporal_store(a.val[k], base_ptr + (yi - lo));
+      } else {
+        bad = true;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();   // so[] is rewritten by the next step
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  if (bad) raise_flag(a.err);
+}
+
 // --------------------------------------------------------------- launches
 
 static uint64_t enc_tiles(uint64_t count) { return (count + kEncTile - 1) / kEncTile; }
@@ -986,7 +1108,8 @@ hipError_t launch_leb128_encode(EncArgs a, uint64_t* group_sum, uint64_t* group_
 }
 
 // The decoder's single segment (num == 0) is based at 0.
-hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStream_t stream) {
+hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStream_t stream,
+                                bool apply) {
   hipError_t e;
   if (L.btiles == 0) return launch_reset(a.d_count, nullptr, 0, stream);
   a.segs.base0 = 0;
@@ -1014,7 +1137,10 @@ hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStre
                      (const uint32_t*)(ws + L.gsum_f), (const uint64_t*)(ws + L.gsum_v), groups,
                      a.gexcl_v, (uint64_t*)nullptr);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(dec_write_kernel, grid, block, 0, stream, a, aligned);
+  if (apply)
+    hipLaunchKernelGGL(dec_apply_kernel, grid, block, 0, stream, a, aligned);
+  else
+    hipLaunchKernelGGL(dec_write_kernel, grid, block, 0, stream, a, aligned);
   return hipGetLastError();
 }
 

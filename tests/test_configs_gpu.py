@@ -105,7 +105,7 @@ def artifact_full(ws, idx, val, offs, label):
     say(label, "artifact ok:", int(h.num_segments), "segments")
 
 
-def leb128_full(ws, idx, offs, label):
+def leb128_full(ws, idx, val, offs, label):
     """Gap + LEB128 code of the whole set's indices with one segment per
     tensor: decodes to the indices; sampled tensors' segments equal the
     oracle's bytes for that tensor's local indices."""
@@ -116,6 +116,12 @@ def leb128_full(ws, idx, offs, label):
     assert torch.equal(back, idx), label
     sb = seg_bytes.cpu().numpy()
     assert sb[0] == 0 and sb[-1] == buf.numel() and np.all(np.diff(sb) >= 0)
+    # the receiving side: apply straight from the code (decode-in-apply)
+    roll = [p.clone() for p in ws.prev]
+    ad.delta_apply_leb128_multi(roll, buf, offs_h, bases, val, check=True)
+    for r, q in zip(roll, ws.new):
+        assert torch.equal(r.view(torch.int16), q.view(torch.int16)), label
+    del roll
     for t in sample_tensors(ws.names, ws.shapes):
         a, b = int(offs_h[t]), int(offs_h[t + 1])
         ref, n = oracle.leb128_encode(idx[a:b].cpu().numpy() - bases[t])
@@ -135,7 +141,7 @@ def test_weight_set(model, density):
     torch.cuda.synchronize()
     check_set(ws, idx, val, offs, label)
     round_trip(ws, idx, val, label)
-    leb128_full(ws, idx, offs, label)
+    leb128_full(ws, idx, val, offs, label)
 
 
 def test_qwen3_8b_clustered():
@@ -152,7 +158,7 @@ def test_qwen3_8b_clustered():
     tile_hist = torch.bincount(idx // 8192)
     assert int(tile_hist.max()) > 5 * 82
     round_trip(ws, idx, val, "qwen3-8b clustered")
-    leb128_full(ws, idx, offs, "qwen3-8b clustered")
+    leb128_full(ws, idx, val, offs, "qwen3-8b clustered")
     artifact_full(ws, idx, val, offs, "qwen3-8b clustered")
 
 

@@ -285,3 +285,87 @@ def test_ten_byte_number_decodes():
     got = ad.delta_leb128_decode(torch.from_numpy(stream).to(DEV))
     assert m == 1
     np.testing.assert_array_equal(got.cpu().numpy(), ref)
+
+
+# ---------------------------------------------------------- decode-in-apply
+
+def host_u16(t):
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16).reshape(-1)
+
+
+def random_list(sizes, density, seed):
+    g = torch.Generator().manual_seed(seed)
+    prevs = [torch.randint(-32768, 32767, (n,), generator=g, dtype=torch.int16).to(DEV)
+             .view(torch.bfloat16) for n in sizes]
+    news = []
+    for p in prevs:
+        q = p.clone()
+        m = (torch.rand(p.shape, generator=g) < density).to(DEV)
+        q.view(torch.int16)[m] ^= 0x0203
+        news.append(q)
+    return prevs, news
+
+
+@pytest.mark.parametrize("sizes,density", [([5000, 1, 70_000, 12_345, 300_000, 4096], 0.02),
+                                           ([1 << 20], 0.3),
+                                           ([3 + 7 * i for i in range(500)], 0.1)])
+def test_apply_leb128_per_tensor_segments(sizes, density):
+    say("apply leb128", len(sizes), "tensors")
+    prevs, news = random_list(sizes, density, seed=len(sizes))
+    idx, val, toffs = ad.delta_extract_multi(prevs, news)
+    bases = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.int64)
+    offs = toffs.cpu().numpy()
+    code, _ = ad.delta_leb128_encode(idx, offs, bases)
+    roll = [p.clone() for p in prevs]
+    ad.delta_apply_leb128_multi(roll, code, offs, bases, val, check=True)
+    ref = [host_u16(p).copy() for p in prevs]
+    assert oracle.apply_multi_(ref, idx.cpu().numpy(), host_u16(val)) == 0
+    for r, w, q in zip(roll, ref, news):
+        np.testing.assert_array_equal(host_u16(r), w)
+        np.testing.assert_array_equal(host_u16(r), host_u16(q))
+
+
+def test_apply_leb128_pipeline_chunks():
+    sizes = [70_001, 3, 50_000, 8192 * 3 + 1, 100]
+    prevs, news = random_list(sizes, 0.05, seed=21)
+    hb, hv, counts, used = ad.delta_extract_pipelined_leb128(prevs, news, chunk_elems=10_007,
+                                                            num_streams=3)
+    offs, bases = ad.chunk_segments(counts, used)
+    roll = [p.clone() for p in prevs]
+    ad.delta_apply_leb128_multi(roll, hb.to(DEV), offs, bases, hv.to(DEV), check=True)
+    for r, q in zip(roll, news):
+        np.testing.assert_array_equal(host_u16(r), host_u16(q))
+
+
+def test_apply_leb128_flags_count_mismatch_and_range():
+    prevs, news = random_list([40_000, 20_000], 0.05, seed=5)
+    idx, val, toffs = ad.delta_extract_multi(prevs, news)
+    code, _ = ad.delta_leb128_encode(idx)   # one segment, global indices
+    roll = [p.clone() for p in prevs]
+    with pytest.raises(ad.DeltaError):      # one value short
+        ad.delta_apply_leb128_multi(roll, code, None, None, val[:-1], check=True)
+    # every entry but the last was applied
+    got = np.concatenate([host_u16(r) for r in roll])
+    want = np.concatenate([host_u16(p) for p in prevs])
+    ii = idx.cpu().numpy()
+    want[ii[:-1]] = host_u16(val)[:-1]
+    np.testing.assert_array_equal(got, want)
+    # indices past the tensor list: flagged and skipped, the rest applied
+    big = torch.cat([idx, torch.tensor([60_000, 60_017], dtype=torch.int64, device=DEV)])
+    bval = torch.cat([val, val[:2]])
+    code2, _ = ad.delta_leb128_encode(big)
+    roll = [p.clone() for p in prevs]
+    with pytest.raises(ad.DeltaError):
+        ad.delta_apply_leb128_multi(roll, code2, None, None, bval, check=True)
+    for r, q in zip(roll, news):
+        np.testing.assert_array_equal(host_u16(r), host_u16(q))
+
+
+def test_apply_leb128_empty():
+    prevs, _ = random_list([100, 50], 0.0, seed=1)
+    roll = [p.clone() for p in prevs]
+    empty = torch.zeros(0, dtype=torch.uint8, device=DEV)
+    ad.delta_apply_leb128_multi(roll, empty, None, None,
+                                torch.zeros(0, dtype=torch.bfloat16, device=DEV), check=True)
+    for r, p in zip(roll, prevs):
+        assert torch.equal(r.view(torch.int16), p.view(torch.int16))
