@@ -732,8 +732,8 @@ def activate_artifact(art: torch.Tensor, weights: Sequence[torch.Tensor], active
         for n in numels[:-1]:
             bases.append(bases[-1] + n)
         offs = table[:, 1].cpu().tolist() + [K]
-        idx = delta_leb128_decode(code, offs, bases, capacity=K, stream=stream)
+        # decode-in-apply: the indices are never materialised
+        delta_apply_leb128_multi(weights, code, offs, bases, val, check=True, stream=stream)
     else:
-        idx = code.view(torch.int64)
-    delta_apply_multi(weights, idx, val, check=True, stream=stream)
+        delta_apply_multi(weights, code.view(torch.int64), val, check=True, stream=stream)
     return int(h.version)
