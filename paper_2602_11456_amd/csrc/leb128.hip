@@ -517,10 +517,14 @@ __device__ __forceinline__ void open_number(const leb_u32x4& P, uint64_t& v, uin
   const int h = t ? 31 - __builtin_clz(t) : -1;
   len = (uint32_t)(15 - h);
   v = 0;
+  // an open number of at most 9 bytes lies in bytes 7..15; a longer one is
+  // malformed (decode16 flags it) and its value does not matter
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
+  for (int j = 7; j < 16; ++j) {
     const int k = j - h - 1;   // byte k of the open number
-    if (k >= 0 && k < 10) v |= (uint64_t)(byte16(P, j) & 0x7Fu) << (7 * k);
+    const bool in = k >= 0;
+    const uint32_t sh = in ? 7u * (uint32_t)k : 0u;
+    v |= in ? (uint64_t)(byte16(P, j) & 0x7Fu) << sh : 0ull;
   }
 }
 
@@ -533,26 +537,23 @@ __device__ __forceinline__ uint32_t decode16(const leb_u32x4& C, uint32_t valid,
   const uint32_t ends = ends16(C) & valid;
   uint64_t acc = v_in;
   uint32_t k = len_in;
+  bool b = false;
+  // branch free: every byte is a few selects
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
-    const uint64_t pl = byte16(C, j) & 0x7Fu;
-    if ((valid >> j) & 1u) {
-      if (k < 9) {
-        acc |= pl << (7 * k);
-      } else if (k == 9) {
-        if (pl > 1) bad = true;
-        acc |= pl << 63;
-      } else {
-        bad = true;
-      }
-      ++k;
-    }
+    const uint32_t pl = byte16(C, j) & 0x7Fu;
+    const bool vj = (valid >> j) & 1u;
+    const uint32_t sh = k < 9 ? 7u * k : 63u;
+    const uint64_t add = k <= 9 ? (uint64_t)(k < 9 ? pl : (pl & 1u)) << sh : 0ull;
+    b |= vj & ((k == 9 && pl > 1) || k > 9);
+    acc |= vj ? add : 0ull;
+    k += vj ? 1u : 0u;
     num[j] = acc;
-    if ((ends >> j) & 1u) {
-      acc = 0;
-      k = 0;
-    }
+    const bool ej = (ends >> j) & 1u;
+    acc = ej ? 0ull : acc;
+    k = ej ? 0u : k;
   }
+  bad |= b;
   return ends;
 }
 
@@ -638,6 +639,15 @@ __device__ __forceinline__ void dec_lane_step(const DecArgs& a, const uint8_t* s
   e_step += __shfl(incl, 63);
 }
 
+// Whether one of the lane's entries [d.e, d.e + count) opens a segment
+// (`r` is the cursor at d.e).
+__device__ __forceinline__ bool lane_opens(const LebSegs& g, const SegCursor& r,
+                                           const LaneDec& d) {
+  const uint64_t last = d.e + __builtin_popcount(d.ends) - 1;
+  if (g.num == 0) return d.e == 0;
+  return d.e == 0 || d.e == r.lo || r.next <= last;
+}
+
 // Segmented fold of one lane's numbers: whether one opens a segment, and
 // the sum since the last that does (base + first term for it).
 __device__ __forceinline__ void lane_fold(const DecArgs& a, const TileSegs& c,
@@ -647,6 +657,11 @@ __device__ __forceinline__ void lane_fold(const DecArgs& a, const TileSegs& c,
   v = 0;
   if (!d.ends) return;
   SegCursor r = seg_cursor(a.segs, c, s_lo, d.e);
+  if (!lane_opens(a.segs, r, d)) {   // the common case: a plain sum
+#pragma unroll
+    for (int j = 0; j < 16; ++j) v += ((d.ends >> j) & 1u) ? d.num[j] : 0ull;
+    return;
+  }
   uint64_t e = d.e;
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
@@ -883,13 +898,24 @@ __global__ __launch_bounds__(kLebThreads) void dec_write_kernel(DecArgs a, bool 
     if (d.ends) {
       SegCursor r = seg_cursor(a.segs, c, s_lo, d.e);
       uint64_t k = d.e;
+      if (!lane_opens(a.segs, r, d)) {   // the common case: running sums
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        if ((d.ends >> j) & 1u) {
-          int64_t base;
-          y = seg_step(a.segs, c, s_lo, r, k, base) ? d.num[j] + (uint64_t)base : y + d.num[j];
-          so[k - e_step] = y;
-          ++k;
+        for (int j = 0; j < 16; ++j) {
+          if ((d.ends >> j) & 1u) {
+            y += d.num[j];
+            so[k - e_step] = y;
+            ++k;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          if ((d.ends >> j) & 1u) {
+            int64_t base;
+            y = seg_step(a.segs, c, s_lo, r, k, base) ? d.num[j] + (uint64_t)base : y + d.num[j];
+            so[k - e_step] = y;
+            ++k;
+          }
         }
       }
     }
@@ -995,13 +1021,24 @@ __global__ __launch_bounds__(kLebThreads) void dec_apply_kernel(DecArgs a, bool 
     if (d.ends) {
       SegCursor r = seg_cursor(a.segs, c, s_lo, d.e);
       uint64_t k = d.e;
+      if (!lane_opens(a.segs, r, d)) {   // the common case: running sums
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        if ((d.ends >> j) & 1u) {
-          int64_t base;
-          y = seg_step(a.segs, c, s_lo, r, k, base) ? d.num[j] + (uint64_t)base : y + d.num[j];
-          so[k - e_step] = y;
-          ++k;
+        for (int j = 0; j < 16; ++j) {
+          if ((d.ends >> j) & 1u) {
+            y += d.num[j];
+            so[k - e_step] = y;
+            ++k;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          if ((d.ends >> j) & 1u) {
+            int64_t base;
+            y = seg_step(a.segs, c, s_lo, r, k, base) ? d.num[j] + (uint64_t)base : y + d.num[j];
+            so[k - e_step] = y;
+            ++k;
+          }
         }
       }
     }
