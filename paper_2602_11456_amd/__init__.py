@@ -30,7 +30,8 @@ __all__ = [
     "delta_extract_multi_workspace_bytes", "delta_apply_multi_workspace_bytes",
     "delta_pipeline_staging_bytes", "MultiPlan", "delta_leb128_encode", "delta_leb128_decode",
     "delta_apply_leb128_multi", "delta_apply_leb128_multi_workspace_bytes",
-    "delta_extract_pipelined_leb128", "delta_pipeline_leb128_staging_bytes", "chunk_segments",
+    "delta_extract_pipelined_leb128", "delta_extract_pipelined_plan",
+    "delta_extract_pipelined_leb128_plan", "delta_pipeline_leb128_staging_bytes", "chunk_segments",
     "delta_compose", "delta_compose_workspace_bytes", "delta_catch_up",
     "delta_hash_segments", "delta_artifact_layout", "pack_artifact", "read_artifact_header",
     "delta_artifact_verify", "activate_artifact", "delta_extract_fused",
@@ -509,7 +510,20 @@ def delta_extract_pipelined(prevs: Sequence[torch.Tensor], news: Sequence[torch.
                             ) -> Tuple[torch.Tensor, torch.Tensor]:
     """Chunked extract with pinned host output (Sec. 5.2).  Returns the host
     (idx, val) views of the filled part.  Host-synchronous."""
-    plan = MultiPlan(prevs, news)
+    return delta_extract_pipelined_plan(MultiPlan(prevs, news), chunk_elems, num_streams,
+                                        h_idx, h_val, staging, streams)
+
+
+def delta_extract_pipelined_plan(plan: MultiPlan, chunk_elems: int = 1 << 27,
+                                 num_streams: int = 4,
+                                 h_idx: Optional[torch.Tensor] = None,
+                                 h_val: Optional[torch.Tensor] = None,
+                                 staging: Optional[torch.Tensor] = None,
+                                 streams: Optional[List[torch.cuda.Stream]] = None
+                                 ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """:func:`delta_extract_pipelined` over a :class:`MultiPlan` built once
+    for tensors that every step reuses (a training loop's weights): the
+    per-call cost of checking and listing hundreds of tensors goes away."""
     dev = plan.device
     if streams is None:
         streams = [torch.cuda.Stream(device=dev) for _ in range(num_streams)]
@@ -537,8 +551,8 @@ def delta_extract_pipelined(prevs: Sequence[torch.Tensor], news: Sequence[torch.
         k = count.value
         h_idx2 = torch.empty(k, dtype=torch.int64, pin_memory=True)
         h_val2 = torch.empty(k, dtype=h_val.dtype, pin_memory=True)
-        return delta_extract_pipelined(prevs, news, chunk_elems, num_streams, h_idx2, h_val2,
-                                       stage, streams)
+        return delta_extract_pipelined_plan(plan, chunk_elems, num_streams, h_idx2, h_val2,
+                                            stage, streams)
     _check(status)
     k = count.value
     return h_idx[:k], h_val[:k]
@@ -567,7 +581,18 @@ def delta_extract_pipelined_leb128(prevs: Sequence[torch.Tensor], news: Sequence
     views (index bytes, values) of the filled part, the per-chunk entry
     counts and the chunk size actually used; :func:`chunk_segments` turns
     the last two into the decoder's segments.  Host-synchronous."""
-    plan = MultiPlan(prevs, news)
+    return delta_extract_pipelined_leb128_plan(MultiPlan(prevs, news), chunk_elems, num_streams,
+                                               h_bytes, h_val, staging, streams)
+
+
+def delta_extract_pipelined_leb128_plan(plan: MultiPlan, chunk_elems: int = 1 << 27,
+                                        num_streams: int = 4,
+                                        h_bytes: Optional[torch.Tensor] = None,
+                                        h_val: Optional[torch.Tensor] = None,
+                                        staging: Optional[torch.Tensor] = None,
+                                        streams: Optional[List[torch.cuda.Stream]] = None):
+    """:func:`delta_extract_pipelined_leb128` over a :class:`MultiPlan`
+    built once for tensors that every step reuses."""
     dev = plan.device
     if streams is None:
         streams = [torch.cuda.Stream(device=dev) for _ in range(num_streams)]
@@ -597,8 +622,8 @@ def delta_extract_pipelined_leb128(prevs: Sequence[torch.Tensor], news: Sequence
     if status == _abi.DELTA_ERR_CAPACITY:
         hb = torch.empty(max(nbytes.value, 1), dtype=torch.uint8, pin_memory=True)
         hv = torch.empty(max(count.value, 1), dtype=h_val.dtype, pin_memory=True)
-        return delta_extract_pipelined_leb128(prevs, news, chunk_elems, num_streams, hb, hv,
-                                              stage, streams)
+        return delta_extract_pipelined_leb128_plan(plan, chunk_elems, num_streams, hb, hv,
+                                                   stage, streams)
     _check(status)
     return (h_bytes[:nbytes.value], h_val[:count.value], [int(c) for c in counts[:nchunks]],
             chunk)

@@ -351,6 +351,36 @@ def test_pipeline_leb128_matches_oracle(chunk, streams):
     np.testing.assert_array_equal(back.cpu().numpy(), ref_idx)
 
 
+def test_pipeline_plan_reused_across_steps():
+    """One plan and one set of buffers serve several steps while the new
+    weights change in place between calls, as in a training loop."""
+    sizes = [70_001, 3, 2 * TILE + 5, 0, 50_000]
+    prevs, news = make_list(sizes, 0.02, seed=520)
+    plan = ad.MultiPlan(prevs, news)
+    streams = [torch.cuda.Stream() for _ in range(4)]
+    h_idx = torch.empty(sum(sizes), dtype=torch.int64, pin_memory=True)
+    h_val = torch.empty(sum(sizes), dtype=torch.bfloat16, pin_memory=True)
+    h_bytes = torch.empty(3 * sum(sizes), dtype=torch.uint8, pin_memory=True)
+    for step, density in enumerate([0.02, 0.0, 0.3]):
+        g = torch.Generator(device=DEV)
+        g.manual_seed(600 + step)
+        for p, q in zip(prevs, news):
+            q.copy_(p)
+            m = torch.rand(q.shape, device=DEV, generator=g) < density
+            q.view(torch.int16)[m] ^= 0x0041
+        ref_idx, ref_val, _, _ = oracle.extract_multi(
+            [host_u16(p) for p in prevs], [host_u16(q) for q in news])
+        i, v = ad.delta_extract_pipelined_plan(plan, 10_007, 4, h_idx, h_val, streams=streams)
+        np.testing.assert_array_equal(i.numpy(), ref_idx)
+        np.testing.assert_array_equal(v.view(torch.int16).numpy().view(np.uint16), ref_val)
+        b, v2, counts, used = ad.delta_extract_pipelined_leb128_plan(
+            plan, 10_007, 4, h_bytes, h_val, streams=streams)
+        ref_bytes, ref_counts = oracle_chunk_stream(ref_idx, used, sum(sizes))
+        np.testing.assert_array_equal(np.array(counts), ref_counts)
+        np.testing.assert_array_equal(b.numpy(), ref_bytes)
+        np.testing.assert_array_equal(v2.view(torch.int16).numpy().view(np.uint16), ref_val)
+
+
 def test_pipeline_leb128_capacity_retry():
     prevs, news = make_list([40_000, 20_000], 0.05, seed=19)
     hb = torch.empty(5, dtype=torch.uint8, pin_memory=True)
