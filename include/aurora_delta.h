@@ -20,7 +20,8 @@
  *                  the delta's declared base version (Sec. 5.2).
  *   extract_pipelined
  *                  extract_multi split into fixed-size chunks of the global
- *                  index space, extracted on two streams while a third
+ *                  index space: one stream reads chunk after chunk, a
+ *                  second finishes (and codes) each read chunk, a third
  *                  stores each finished chunk's streams into pinned host
  *                  memory (Sec. 5.2, "Overlapped extraction and transfer":
  *                  segments emitted as soon as they are encoded).
@@ -439,7 +440,7 @@ delta_status_t delta_artifact_verify(const void* d_artifact, size_t artifact_byt
 /* Options of the chunked pipeline. */
 typedef struct {
   uint64_t chunk_elems; /* words of the global index space per chunk (> 0) */
-  int32_t num_streams;  /* streams used round-robin, 1..16 */
+  int32_t num_streams;  /* staging slots and streams, 1..16 */
   int32_t reserved;
 } delta_pipeline_opts_t;
 
@@ -454,12 +455,16 @@ size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
  * chunk by chunk, with each chunk's (idx, val) stored into pinned host
  * memory as soon as that chunk is done, while later chunks are extracted.
  * The host output equals delta_extract_multi's.
- *   streams       host array of S = opts->num_streams HIP streams.  S
- *                 staging slots; chunks are extracted on streams[0] (and
- *                 streams[1] if S > 2) and delivered in order by one kernel
- *                 per chunk, storing into the host arrays, on
- *                 streams[min(S - 1, 2)].  Streams past the third are not
- *                 used (more streams than hardware queues serialise).
+ *   streams       host array of S = opts->num_streams HIP streams, and S
+ *                 staging slots.  streams[0] runs the pass over the weights
+ *                 of every chunk, one after the other; streams[1] the
+ *                 kernels that finish a chunk once it has been read;
+ *                 streams[2] delivers the chunks in order, one kernel per
+ *                 chunk storing into the host arrays.  S == 2: streams[0]
+ *                 also finishes the chunks, streams[1] delivers; S == 1:
+ *                 everything in order on streams[0].  Streams past the
+ *                 third are not used (more streams than hardware queues
+ *                 serialise).
  *   d_staging     device scratch of delta_pipeline_staging_bytes(...): a
  *                 ring of S chunk slots plus the running totals.
  *   h_idx, h_val  pinned host arrays (hipHostMalloc / pin_memory) of
@@ -477,9 +482,10 @@ delta_status_t delta_extract_pipelined(const uint16_t* const* prev_ptrs,
                                        size_t staging_bytes, int64_t* h_idx, uint16_t* h_val,
                                        uint64_t h_capacity, uint64_t* h_count);
 
-/* Device staging bytes delta_extract_pipelined_leb128 needs: the plain
- * pipeline's staging plus, per stream, the coded bytes of one chunk and the
- * encoder's workspace. */
+/* Device staging bytes delta_extract_pipelined_leb128 needs: per stream,
+ * one chunk's worst-case values and code bytes plus its workspace (no
+ * index stream: the extract writes the code itself), and the running
+ * totals and per-chunk counts. */
 size_t delta_pipeline_leb128_staging_bytes(const uint64_t* numels, int32_t num_tensors,
                                            const delta_pipeline_opts_t* opts);
 
@@ -491,8 +497,8 @@ size_t delta_pipeline_leb128_staging_bytes(const uint64_t* numels, int32_t num_t
  * first word (c * chunk, chunk = min(opts->chunk_elems, total words)):
  * delta_leb128_decode with seg_offsets = prefix sums of h_chunk_counts and
  * seg_bases[c] = c * chunk returns delta_extract_multi's indices exactly.
- *   streams, d_staging  as delta_extract_pipelined (the encoder runs on the
- *                 chunk's extract stream, in its slot).
+ *   streams, d_staging  as delta_extract_pipelined (the kernels that
+ *                 finish a chunk write its code into its slot).
  *   h_bytes       pinned host bytes [h_bytes_capacity]: the coded indices.
  *   h_val         pinned host words [h_val_capacity]: as delta_extract_multi.
  *   h_chunk_counts host array (any memory) [h_num_chunks >=

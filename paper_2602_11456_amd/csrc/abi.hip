@@ -117,22 +117,30 @@ namespace aurora {
 delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_t num_tensors,
                                bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
                                uint64_t* d_count, uint64_t* d_offsets, void* workspace,
-                               size_t have, hipStream_t stream) {
+                               size_t have, hipStream_t stream, const CodedOut* coded,
+                               const StageSplit* split) {
   std::vector<TensorDesc> descs;
   const uint64_t tiles = build_descs(slices, num_slices, descs);
   if (tiles > 0xFFFFFFFFull / kThreads)
     return fail(DELTA_ERR_INVALID_ARG, "too many words for one launch (%llu tiles)",
                 (unsigned long long)tiles);
+  if (coded) d_offsets = nullptr;
   if (tiles == 0) {
     hipError_t e = launch_reset(d_count, d_offsets, d_offsets ? num_tensors + 1 : 0, stream);
+    if (e == hipSuccess && coded) e = launch_reset(coded->d_nbytes, nullptr, 0, stream);
+    if (e == hipSuccess && split) {
+      e = hipEventRecord(split->staged, stream);
+      if (e == hipSuccess && split->rest != stream) e = hipStreamWaitEvent(split->rest, split->staged, 0);
+    }
     if (e != hipSuccess) return hip_fail(e, "reset launch");
     return ok();
   }
-  const uint32_t cap = stage_cap_for(have, tiles, descs.size());
+  const bool cd = coded != nullptr;
+  const uint32_t cap = stage_cap_for(have, tiles, descs.size(), cd);
   if (cap == 0 || !workspace || (uintptr_t)workspace % kAlign)
     return fail(DELTA_ERR_WORKSPACE, "workspace: %zu bytes at %p; at least %zu bytes, %zu-aligned",
-                have, workspace, workspace_bytes(tiles, descs.size(), kMinStageCap), kAlign);
-  const WorkspaceLayout L = workspace_layout(tiles, descs.size());
+                have, workspace, workspace_bytes(tiles, descs.size(), kMinStageCap, cd), kAlign);
+  const WorkspaceLayout L = workspace_layout(tiles, descs.size(), cd);
   char* ws = (char*)workspace;
   ExtractArgs a;
   memset(&a, 0, sizeof(a));
@@ -166,7 +174,19 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
   }
   bool all_vec = true;
   for (const TensorDesc& t : descs) all_vec = all_vec && t.vec;
-  e = launch_extract(a, idx64, all_vec, stream);
+  if (coded) {
+    a.tile_code = (uint32_t*)(ws + L.tile_code);
+    a.tile_fl = (int64_t*)(ws + L.tile_fl);
+    a.group_bexcl = (uint64_t*)(ws + L.group_bexcl);
+    a.group_prev = (int64_t*)(ws + L.group_prev);
+    a.code_out = coded->out;
+    a.code_capacity = coded->capacity;
+    a.d_nbytes = coded->d_nbytes;
+    a.code_base = coded->base;
+    e = launch_extract_coded(a, all_vec, stream, split);
+  } else {
+    e = launch_extract(a, idx64, all_vec, stream, split);
+  }
   if (e != hipSuccess) return hip_fail(e, "extract launch");
   return ok();
 }

@@ -89,12 +89,18 @@ __host__ __device__ inline uint64_t groups_for(uint64_t tiles) {
 //   group_excl  uint64 [groups]      output offset of each group
 //   map         uint32 [tiles]       tile -> slice row (tensor lists)
 //   table       TensorDesc [tensors]
+//   coded output only (see CodedOut):
+//   tile_code   uint32 [tiles][4]    code bytes of the gaps inside the tile, per wavefront
+//   tile_fl     int64 [tiles][2]     first and last kept index of the tile
+//   group_bexcl uint64 [groups]      code bytes before each group
+//   group_prev  int64 [groups]       index the group's first entry is coded against
 //   stage       uint32 [tiles * cap] per-tile staging slots
 struct WorkspaceLayout {
-  size_t counts, group_sum, group_excl, map, table, stage, fixed;
+  size_t counts, group_sum, group_excl, map, table, tile_code, tile_fl, group_bexcl, group_prev,
+      stage, fixed;
 };
 
-inline WorkspaceLayout workspace_layout(uint64_t tiles, uint64_t tensors) {
+inline WorkspaceLayout workspace_layout(uint64_t tiles, uint64_t tensors, bool coded = false) {
   WorkspaceLayout w;
   const uint64_t groups = groups_for(tiles);
   w.counts = 0;
@@ -102,19 +108,24 @@ inline WorkspaceLayout workspace_layout(uint64_t tiles, uint64_t tensors) {
   w.group_excl = align_up(w.group_sum + 8 * groups);
   w.map = align_up(w.group_excl + 8 * groups);
   w.table = align_up(w.map + 4 * tiles);
-  w.stage = align_up(w.table + sizeof(TensorDesc) * tensors);
+  w.tile_code = align_up(w.table + sizeof(TensorDesc) * tensors);
+  w.tile_fl = align_up(w.tile_code + (coded ? 16 * tiles : 0));
+  w.group_bexcl = align_up(w.tile_fl + (coded ? 16 * tiles : 0));
+  w.group_prev = align_up(w.group_bexcl + (coded ? 8 * groups : 0));
+  w.stage = align_up(w.group_prev + (coded ? 8 * groups : 0));
   w.fixed = w.stage;
   return w;
 }
 
 // Bytes for a given slot capacity.
-inline size_t workspace_bytes(uint64_t tiles, uint64_t tensors, uint32_t cap) {
-  return align_up(workspace_layout(tiles, tensors).fixed + 4ull * (cap + kSlotPad) * tiles);
+inline size_t workspace_bytes(uint64_t tiles, uint64_t tensors, uint32_t cap, bool coded = false) {
+  return align_up(workspace_layout(tiles, tensors, coded).fixed +
+                  4ull * (cap + kSlotPad) * tiles);
 }
 
 // Slot capacity a workspace of `have` bytes affords (0 if below the minimum).
-inline uint32_t stage_cap_for(size_t have, uint64_t tiles, uint64_t tensors) {
-  const WorkspaceLayout w = workspace_layout(tiles, tensors);
+inline uint32_t stage_cap_for(size_t have, uint64_t tiles, uint64_t tensors, bool coded = false) {
+  const WorkspaceLayout w = workspace_layout(tiles, tensors, coded);
   if (tiles == 0) return kMinStageCap;
   if (have < w.fixed) return 0;
   uint64_t stride = (have - w.fixed) / (4 * tiles);
@@ -158,6 +169,17 @@ struct ExtractArgs {
   uint64_t* group_sum;
   uint64_t* group_excl;
   uint32_t* stage;
+  // Coded output (launch_extract_coded): no indices; the kept positions
+  // leave as one gap + LEB128 segment whose first entry is coded against
+  // code_base.  Per-tile and per-group tables as in WorkspaceLayout.
+  uint32_t* tile_code;
+  int64_t* tile_fl;
+  uint64_t* group_bexcl;
+  int64_t* group_prev;
+  uint8_t* code_out;
+  uint64_t code_capacity;
+  uint64_t* d_nbytes;
+  int64_t code_base;
 };
 
 hipError_t launch_reset(uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets,
@@ -172,8 +194,23 @@ hipError_t launch_group_scan(const uint32_t* counts, uint64_t num_tiles, uint64_
                              uint64_t* group_excl, uint64_t* d_total, hipStream_t stream);
 hipError_t launch_group_scan(const uint64_t* counts, uint64_t num_tiles, uint64_t* group_sum,
                              uint64_t* group_excl, uint64_t* d_total, hipStream_t stream);
+// Where the kernels after the stage kernel (the pass that reads both
+// copies) run: `staged` is recorded on the launch stream right after it and
+// `rest` waits for it and takes the scan and finalize kernels.
+struct StageSplit {
+  hipEvent_t staged;
+  hipStream_t rest;
+};
+
 // all_vec: every slice has prev and next at the same 16-byte alignment.
-hipError_t launch_extract(const ExtractArgs& a, bool idx64, bool all_vec, hipStream_t stream);
+// split: nullable, as above.
+hipError_t launch_extract(const ExtractArgs& a, bool idx64, bool all_vec, hipStream_t stream,
+                          const StageSplit* split = nullptr);
+
+// The same extract with coded output: values to out_val, the gap + LEB128
+// code of the positions to code_out, *d_count and *d_nbytes.
+hipError_t launch_extract_coded(const ExtractArgs& a, bool all_vec, hipStream_t stream,
+                                const StageSplit* split = nullptr);
 
 hipError_t launch_apply(uint16_t* w, uint64_t n, bool idx64, const void* idx,
                         const uint16_t* val, uint64_t count, uint32_t* err,
@@ -192,13 +229,28 @@ struct SliceIn {
   uint32_t tensor;
 };
 
+// Coded output of enqueue_extract: the positions as one gap + LEB128
+// segment (first entry relative to `base`) of at most `capacity` bytes at
+// `out`, its length in *d_nbytes; no index stream.
+struct CodedOut {
+  uint8_t* out;
+  uint64_t capacity;
+  uint64_t* d_nbytes;
+  int64_t base;
+};
+
 // Builds the slice table in `workspace`, then enqueues the extract kernels
 // on `stream` (abi.hip).  Empty slices are skipped; d_offsets (nullable)
-// has num_tensors + 1 entries.  Sets the error text on failure.
+// has num_tensors + 1 entries.  With `coded`, out_idx, idx64 and d_offsets
+// are unused and the workspace follows the coded layout.  `split` as for
+// launch_extract (with nothing to read, split->rest still waits for the
+// launch stream).  Sets the error text on failure.
 delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_t num_tensors,
                                bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
                                uint64_t* d_count, uint64_t* d_offsets, void* workspace,
-                               size_t workspace_bytes, hipStream_t stream);
+                               size_t workspace_bytes, hipStream_t stream,
+                               const CodedOut* coded = nullptr,
+                               const StageSplit* split = nullptr);
 
 // Delta chain composition (compose.hip): workspace layout for `K` deltas
 // of the given counts, and the enqueue of the whole chain on `stream`.

@@ -221,7 +221,11 @@ __device__ __forceinline__ void scan_tile(const TensorDesc& d, uint64_t tile, ui
 
 static_assert(kLdsStage >= kElemsPerTile, "the LDS staging area holds a whole tile");
 
-template <bool kMulti, bool kVec>
+// kCoded (the coded output of launch_extract_coded): the LDS area holds
+// every entry of the tile, and the tile also leaves the code bytes of the
+// gaps between its consecutive entries (each below 8192: one or two bytes),
+// one sum per wavefront, and its first and last kept index.
+template <bool kMulti, bool kVec, bool kCoded>
 __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
   __shared__ uint32_t s_wave_total[kWaves];
   __shared__ __attribute__((aligned(16))) uint32_t s_stage[kLdsStage];
@@ -235,6 +239,7 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
   uint32_t* slot = a.stage + tile * a.stage_stride;
   const uint32_t lane_word = (wave * kGroupsPerWave + lane) * 8;
   const uint32_t keep = s.tile_total < a.stage_cap ? s.tile_total : a.stage_cap;
+  const uint32_t in_lds = kCoded ? s.tile_total : keep;
   // Entries go through LDS (which holds a whole tile) so that the slot is
   // written with contiguous stores.
 #pragma unroll
@@ -245,7 +250,7 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
     while (m) {
       const int j = __builtin_ctz(m);
       m &= m - 1;
-      if (r < keep) s_stage[r] = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
+      if (r < in_lds) s_stage[r] = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
       ++r;
     }
   }
@@ -254,6 +259,20 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
   // kernel, so it should not displace anything in the caches.
   for (uint32_t r = threadIdx.x; r < keep; r += kThreads)
     __builtin_nontemporal_store(s_stage[r], slot + r);
+  if (kCoded) {
+    uint64_t bytes = 0;
+    for (uint32_t r = threadIdx.x + 1; r < s.tile_total; r += kThreads) {
+      const uint32_t gap = (s_stage[r] & 0xFFFFu) - (s_stage[r - 1] & 0xFFFFu);
+      bytes += gap < 128u ? 1u : 2u;
+    }
+    bytes = wave_sum64(bytes);
+    if (lane == 0) a.tile_code[4 * tile + wave] = (uint32_t)bytes;
+    if (threadIdx.x == 0 && s.tile_total) {
+      const int64_t ob = tile_out_base(d, tile);
+      a.tile_fl[2 * tile] = ob + (int64_t)(s_stage[0] & 0xFFFFu);
+      a.tile_fl[2 * tile + 1] = ob + (int64_t)(s_stage[s.tile_total - 1] & 0xFFFFu);
+    }
+  }
   if (threadIdx.x == 0) a.counts[tile] = s.tile_total;
 }
 
@@ -495,6 +514,338 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(ExtractArgs a) {
   }
 }
 
+// ------------------------------------------------------------ coded output
+//
+// The chunked pipeline's coded form (gap + LEB128, one segment per call,
+// Sec. 5.1 "Sparse encoding") written straight from the staging slots: no
+// index stream is formed.  An entry's code is that of its gap: the index
+// minus the previous kept index, or minus code_base for the first entry.
+// Inside a tile the gaps come from the staged offsets; a tile's first entry
+// is coded against the last kept index of the nearest earlier tile that
+// kept anything, found by a running maximum of the tiles' last indices
+// (indices grow with the tile id; code_base starts the maximum, as every
+// index is at least code_base).
+
+__device__ __forceinline__ uint32_t leb_bytes(uint64_t v) {
+  const uint32_t bits = 64 - __builtin_clzll(v | 1ull);
+  return (bits + 6) / 7;
+}
+
+__device__ __forceinline__ int64_t wave_max_incl(int64_t x, uint32_t lane) {
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) {
+    const int64_t y = __shfl_up(x, s);
+    if ((int)lane >= s) x = y > x ? y : x;
+  }
+  return x;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_incl_sum(T x, uint32_t lane) {
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) {
+    const T y = __shfl_up(x, s);
+    if ((int)lane >= s) x += y;
+  }
+  return x;
+}
+
+// Per group of kTilesPerGroup tiles (one wavefront each): its entries, the
+// code bytes of every entry whose predecessor lies in the group, its last
+// (largest) index and the first index of its first tile that kept
+// anything; that first entry's code length is settled by the scan, once
+// the group's predecessor index is known.  Written into the tables the
+// scan then overwrites in place: group_sum = entries | bytes << 32,
+// group_prev = last index, group_bexcl = first index (-1: none kept).
+__global__ __launch_bounds__(64) void coded_group_kernel(ExtractArgs a) {
+  const uint32_t lane = lane_id();
+  const uint64_t g = blockIdx.x;
+  const uint64_t t = g * kTilesPerGroup + lane;
+  const bool in = t < a.num_tiles;
+  const uint32_t c = in ? a.counts[t] : 0u;
+  const u32x4 code = in ? *reinterpret_cast<const u32x4*>(a.tile_code + 4 * t) : u32x4{0, 0, 0, 0};
+  const int64_t f = in ? a.tile_fl[2 * t] : 0;
+  const int64_t l = in ? a.tile_fl[2 * t + 1] : 0;
+  const int64_t incl = wave_max_incl(c ? l : -1, lane);
+  int64_t before = __shfl_up(incl, 1);
+  if (lane == 0) before = -1;
+  const uint64_t inner = (uint64_t)code[0] + code[1] + code[2] + code[3];
+  const uint64_t own = c ? inner + (before >= 0 ? leb_bytes((uint64_t)(f - before)) : 0u) : 0u;
+  const uint64_t nz = __ballot(c != 0);
+  const int64_t first = nz ? __shfl(f, (int)__builtin_ctzll(nz)) : -1;
+  const uint64_t cnt = wave_sum64(c);
+  const uint64_t bytes = wave_sum64(own);
+  const int64_t last = __shfl(incl, 63);
+  if (lane == 0) {
+    a.group_sum[g] = cnt | (bytes << 32);
+    a.group_prev[g] = last;
+    a.group_bexcl[g] = (uint64_t)first;
+  }
+}
+
+// One workgroup: per group, the entries and code bytes before it and the
+// index its first entry is coded against; the totals.  Groups are taken
+// kScanThreads at a time, one per thread, with carries between rounds; a
+// thread reads its group's sums before it overwrites them.
+__global__ __launch_bounds__(kScanThreads) void coded_scan_kernel(ExtractArgs a) {
+  __shared__ int64_t s_wmax[kScanWaves];
+  __shared__ uint64_t s_wcnt[kScanWaves];
+  __shared__ uint64_t s_wbytes[kScanWaves];
+  const uint32_t lane = lane_id();
+  const uint32_t wave = threadIdx.x >> 6;
+  const uint64_t groups = groups_for(a.num_tiles);
+  uint64_t carry_cnt = 0, carry_bytes = 0;
+  int64_t carry_prev = a.code_base;
+  for (uint64_t r0 = 0; r0 < groups; r0 += kScanThreads) {
+    const uint64_t gi = r0 + threadIdx.x;
+    const bool in = gi < groups;
+    const uint64_t packed = in ? a.group_sum[gi] : 0;
+    const int64_t last = in ? a.group_prev[gi] : -1;
+    const int64_t first = in ? (int64_t)a.group_bexcl[gi] : -1;
+    const uint64_t cnt = packed & 0xFFFFFFFFull;
+    const int64_t incl = wave_max_incl(last, lane);
+    if (lane == 63) s_wmax[wave] = incl;
+    __syncthreads();
+    int64_t prev = carry_prev;
+    for (uint32_t w = 0; w < wave; ++w) prev = s_wmax[w] > prev ? s_wmax[w] : prev;
+    const int64_t below = __shfl_up(incl, 1);
+    if (lane > 0 && below > prev) prev = below;
+    const uint64_t bytes =
+        (packed >> 32) + (first >= 0 ? leb_bytes((uint64_t)(first - prev)) : 0u);
+    const uint64_t xc = wave_incl_sum(cnt, lane);
+    const uint64_t xb = wave_incl_sum(bytes, lane);
+    if (lane == 63) {
+      s_wcnt[wave] = xc;
+      s_wbytes[wave] = xb;
+    }
+    __syncthreads();
+    uint64_t oc = carry_cnt, ob = carry_bytes;
+    for (uint32_t w = 0; w < wave; ++w) {
+      oc += s_wcnt[w];
+      ob += s_wbytes[w];
+    }
+    if (in) {
+      a.group_excl[gi] = oc + xc - cnt;
+      a.group_bexcl[gi] = ob + xb - bytes;
+      a.group_prev[gi] = prev;
+    }
+    for (int w = 0; w < kScanWaves; ++w) {
+      carry_cnt += s_wcnt[w];
+      carry_bytes += s_wbytes[w];
+      carry_prev = s_wmax[w] > carry_prev ? s_wmax[w] : carry_prev;
+    }
+    __syncthreads();   // the LDS sums are rewritten by the next round
+  }
+  if (threadIdx.x == 0) {
+    *a.d_count = carry_cnt;
+    *a.d_nbytes = carry_bytes;
+  }
+}
+
+// A group's entries are coded in windows of kCodeWin consecutive entries,
+// eight per thread.  A window's code is at most two bytes per entry plus
+// the longer codes of at most one first entry per tile (an index gap of
+// up to 2^63 takes 9 bytes).
+constexpr int kCodeWin = kThreads * 8;
+constexpr int kCodeWinBytes = 2 * kCodeWin + kTilesPerGroup * 8;
+
+struct CodedGroup {
+  uint32_t begin[kTilesPerGroup + 1];   // first entry of each tile within the group, total
+  uint32_t count[kTilesPerGroup];
+  int64_t out_base[kTilesPerGroup];     // index of word 0 of each tile
+  int64_t prev[kTilesPerGroup];         // index each tile's first entry is coded against
+  uint32_t win[kCodeWin];               // the window's entries, (word << 16) | offset
+  uint8_t code[kCodeWinBytes];
+  uint32_t wave_total[kWaves];
+  uint32_t last_off;                    // offset of the previous window's last entry
+  uint32_t overflow;
+};
+
+// Stores bytes [0, n) of `src` at dst (4-byte stores where dst is aligned).
+__device__ __forceinline__ void flush_code(const uint8_t* src, uint32_t n, uint8_t* dst) {
+  const uint32_t head = (uint32_t)((4u - ((uintptr_t)dst & 3u)) & 3u);
+  const uint32_t h = head < n ? head : n;
+  const uint32_t words = (n - h) / 4;
+  for (uint32_t i = threadIdx.x; i < h; i += kThreads) dst[i] = src[i];
+  uint32_t* dw = reinterpret_cast<uint32_t*>(dst + h);
+  for (uint32_t w = threadIdx.x; w < words; w += kThreads) {
+    const uint32_t j = h + 4 * w;
+    dw[w] = (uint32_t)src[j] | ((uint32_t)src[j + 1] << 8) | ((uint32_t)src[j + 2] << 16) |
+            ((uint32_t)src[j + 3] << 24);
+  }
+  for (uint32_t i = h + 4 * words + threadIdx.x; i < n; i += kThreads) dst[i] = src[i];
+}
+
+// Codes the window of n entries that starts at group entry e_lo (entries in
+// sg.win): values to out_val, code bytes after the `written` bytes the
+// group has already put out.  Returns the window's code bytes.
+__device__ __forceinline__ uint32_t code_window(const ExtractArgs& a, CodedGroup& sg,
+                                                uint32_t e_lo, uint32_t n, uint64_t eg,
+                                                uint64_t bg, uint64_t written) {
+  const uint32_t lane = lane_id();
+  const uint32_t wave = threadIdx.x >> 6;
+  const uint32_t j0 = 8 * threadIdx.x;
+  uint64_t gap[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  uint32_t len[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  uint32_t sum = 0;
+  if (j0 < n) {
+    uint32_t lo = 0, hi = kTilesPerGroup;   // begin[lo] <= e_lo + j0 < begin[hi]
+#pragma unroll
+    for (int step = 0; step < 6; ++step) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (sg.begin[mid] <= e_lo + j0) lo = mid; else hi = mid;
+    }
+    uint32_t ti = lo;
+    uint32_t prev_off = j0 > 0 ? (sg.win[j0 - 1] & 0xFFFFu) : sg.last_off;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const uint32_t j = j0 + k;
+      if (j < n) {
+        const uint32_t e = e_lo + j;
+        while (e >= sg.begin[ti + 1]) ++ti;
+        const uint32_t v = sg.win[j];
+        const uint32_t off = v & 0xFFFFu;
+        gap[k] = e == sg.begin[ti] ? (uint64_t)(sg.out_base[ti] + (int64_t)off - sg.prev[ti])
+                                   : (uint64_t)(off - prev_off);
+        prev_off = off;
+        len[k] = leb_bytes(gap[k]);
+        sum += len[k];
+        if (eg + e < a.capacity) a.out_val[eg + e] = (uint16_t)(v >> 16);
+      }
+    }
+  }
+  const uint32_t incl = wave_incl_sum(sum, lane);
+  if (lane == 63) sg.wave_total[wave] = incl;
+  __syncthreads();
+  uint32_t pos = incl - sum, nb = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    pos += (uint32_t)w < wave ? sg.wave_total[w] : 0u;
+    nb += sg.wave_total[w];
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    uint64_t v = gap[k];
+    for (uint32_t m = 0; m < len[k]; ++m) {
+      sg.code[pos++] = (uint8_t)((v & 0x7Fu) | (m + 1 < len[k] ? 0x80u : 0u));
+      v >>= 7;
+    }
+  }
+  __syncthreads();
+  const uint64_t at = bg + written;
+  const uint64_t room = a.code_capacity > at ? a.code_capacity - at : 0;
+  flush_code(sg.code, room < nb ? (uint32_t)room : nb, a.code_out + at);
+  if (threadIdx.x == 0) sg.last_off = sg.win[n - 1] & 0xFFFFu;
+  __syncthreads();
+  return nb;
+}
+
+// One workgroup per group: the window entries come from the staging slots,
+// loaded kFinBatch per thread at a time.  A group with a tile that
+// overflowed its slot is coded tile by tile instead, that tile read again
+// and its entries placed into the window by rank.
+template <bool kMulti, bool kVec>
+__global__ __launch_bounds__(kThreads) void finalize_coded_kernel(ExtractArgs a) {
+  __shared__ CodedGroup sg;
+  __shared__ uint32_t s_wave_total[kWaves];
+  const uint64_t g = blockIdx.x;
+  const uint64_t t0 = g * kTilesPerGroup;
+  const uint64_t left = a.num_tiles - t0;
+  const uint32_t n_here = left < (uint64_t)kTilesPerGroup ? (uint32_t)left : kTilesPerGroup;
+  const uint32_t lane = lane_id();
+  const uint32_t wave = threadIdx.x >> 6;
+  if (wave == 0) {
+    const uint64_t t = t0 + lane;
+    const bool in = lane < n_here;
+    const uint32_t c = in ? a.counts[t] : 0u;
+    const int64_t l = in ? a.tile_fl[2 * t + 1] : 0;
+    const int64_t incl = wave_max_incl(c ? l : -1, lane);
+    int64_t before = __shfl_up(incl, 1);
+    const int64_t gp = a.group_prev[g];
+    if (lane == 0 || before < gp) before = gp;
+    const uint32_t x = wave_incl_sum(c, lane);
+    sg.begin[lane] = x - c;
+    if (lane == 63) sg.begin[64] = x;
+    sg.count[lane] = c;
+    sg.prev[lane] = before;
+    sg.out_base[lane] = in ? tile_out_base(lane_desc<kMulti>(a, t), t) : 0;
+    const uint64_t over = __ballot(c > a.stage_cap);
+    if (lane == 0) {
+      sg.overflow = over != 0;
+      sg.last_off = 0;
+    }
+  }
+  __syncthreads();
+  const uint64_t eg = a.group_excl[g];
+  const uint64_t bg = a.group_bexcl[g];
+  const uint32_t total = sg.begin[64];
+  uint64_t written = 0;
+  if (!sg.overflow) {
+    for (uint32_t w0 = 0; w0 < total; w0 += kCodeWin) {
+      const uint32_t n = total - w0 < (uint32_t)kCodeWin ? total - w0 : (uint32_t)kCodeWin;
+      uint32_t v[kFinBatch];
+#pragma unroll
+      for (int k = 0; k < kFinBatch; ++k) {
+        const uint32_t j = threadIdx.x + kThreads * k;
+        uint32_t lo = 0, hi = kTilesPerGroup;
+#pragma unroll
+        for (int step = 0; step < 6; ++step) {
+          const uint32_t mid = (lo + hi) >> 1;
+          if (sg.begin[mid] <= w0 + j) lo = mid; else hi = mid;
+        }
+        v[k] = j < n ? __builtin_nontemporal_load(a.stage + (t0 + lo) * a.stage_stride +
+                                                  (w0 + j - sg.begin[lo]))
+                     : 0u;
+      }
+#pragma unroll
+      for (int k = 0; k < kFinBatch; ++k) {
+        const uint32_t j = threadIdx.x + kThreads * k;
+        if (j < n) sg.win[j] = v[k];
+      }
+      __syncthreads();
+      written += code_window(a, sg, w0, n, eg, bg, written);
+    }
+    return;
+  }
+  for (uint32_t i = 0; i < n_here; ++i) {
+    const uint32_t c = sg.count[i];
+    if (c == 0) continue;
+    const uint64_t tile = t0 + i;
+    if (c <= a.stage_cap) {
+      const uint32_t* slot = a.stage + tile * a.stage_stride;
+      for (uint32_t r0 = 0; r0 < c; r0 += kCodeWin) {
+        const uint32_t n = c - r0 < (uint32_t)kCodeWin ? c - r0 : (uint32_t)kCodeWin;
+        for (uint32_t j = threadIdx.x; j < n; j += kThreads) sg.win[j] = slot[r0 + j];
+        __syncthreads();
+        written += code_window(a, sg, sg.begin[i] + r0, n, eg, bg, written);
+      }
+      continue;
+    }
+    const TensorDesc d = tile_desc<kMulti>(a, tile);
+    TileScan s;
+    scan_tile<kVec>(d, tile, lane, wave, s_wave_total, s);
+    const uint32_t lane_word = (wave * kGroupsPerWave + lane) * 8;
+    for (uint32_t r0 = 0; r0 < c; r0 += kCodeWin) {
+      const uint32_t n = c - r0 < (uint32_t)kCodeWin ? c - r0 : (uint32_t)kCodeWin;
+#pragma unroll
+      for (int u = 0; u < kChunks; ++u) {
+        uint32_t m = s.mask[u];
+        uint32_t r = s.rank[u];
+        const uint32_t w0 = lane_word + 512 * u;
+        while (m) {
+          const int j = __builtin_ctz(m);
+          m &= m - 1;
+          if (r >= r0 && r < r0 + n) sg.win[r - r0] = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
+          ++r;
+        }
+      }
+      __syncthreads();
+      written += code_window(a, sg, sg.begin[i] + r0, n, eg, bg, written);
+    }
+    __syncthreads();   // s_wave_total is reused by the next overflowed tile
+  }
+}
+
 // ------------------------------------------------------- small kernels
 
 __global__ void reset_kernel(uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets) {
@@ -576,37 +927,88 @@ hipError_t launch_group_scan(const uint64_t* counts, uint64_t num_tiles, uint64_
   return launch_group_scan_t(counts, num_tiles, group_sum, group_excl, d_total, stream);
 }
 
+static hipError_t split_after_stage(hipStream_t stream, const StageSplit* split,
+                                    hipStream_t& rest);
+
 template <typename IdxT, bool kMulti, bool kVec>
-static hipError_t launch_all(const ExtractArgs& a, hipStream_t stream) {
+static hipError_t launch_all(const ExtractArgs& a, hipStream_t stream, const StageSplit* split) {
   const uint64_t groups = (a.num_tiles + kTilesPerGroup - 1) / kTilesPerGroup;
   hipError_t e = record_scan_event(0, stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((stage_kernel<kMulti, kVec>), dim3((uint32_t)a.num_tiles), dim3(kThreads),
-                     0, stream, a);
+  hipLaunchKernelGGL((stage_kernel<kMulti, kVec, false>), dim3((uint32_t)a.num_tiles),
+                     dim3(kThreads), 0, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   e = record_scan_event(1, stream);
+  hipStream_t rest;
+  if (e == hipSuccess) e = split_after_stage(stream, split, rest);
   if (e != hipSuccess) return e;
-  e = launch_group_scan(a.counts, a.num_tiles, a.group_sum, a.group_excl, a.d_count, stream);
+  e = launch_group_scan(a.counts, a.num_tiles, a.group_sum, a.group_excl, a.d_count, rest);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((finalize_kernel<IdxT, kMulti, kVec>), dim3((uint32_t)groups),
-                     dim3(kThreads), 0, stream, a);
+                     dim3(kThreads), 0, rest, a);
   return hipGetLastError();
 }
 
-template <typename IdxT, bool kMulti>
-static hipError_t launch_vec(const ExtractArgs& a, bool vec, hipStream_t stream) {
-  return vec ? launch_all<IdxT, kMulti, true>(a, stream) : launch_all<IdxT, kMulti, false>(a, stream);
+// After the stage kernel: the stream that takes the remaining kernels.
+static hipError_t split_after_stage(hipStream_t stream, const StageSplit* split,
+                                    hipStream_t& rest) {
+  rest = stream;
+  if (!split) return hipSuccess;
+  hipError_t e = hipEventRecord(split->staged, stream);
+  if (e == hipSuccess && split->rest != stream) e = hipStreamWaitEvent(split->rest, split->staged, 0);
+  rest = split->rest;
+  return e;
 }
 
-hipError_t launch_extract(const ExtractArgs& a, bool idx64, bool all_vec, hipStream_t stream) {
-  if (a.num_tiles == 0) return hipSuccess;
+template <bool kMulti, bool kVec>
+static hipError_t launch_coded(const ExtractArgs& a, hipStream_t stream, const StageSplit* split) {
+  const uint64_t groups = (a.num_tiles + kTilesPerGroup - 1) / kTilesPerGroup;
+  hipLaunchKernelGGL((stage_kernel<kMulti, kVec, true>), dim3((uint32_t)a.num_tiles),
+                     dim3(kThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  hipStream_t rest;
+  if (e == hipSuccess) e = split_after_stage(stream, split, rest);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(coded_group_kernel, dim3((uint32_t)groups), dim3(64), 0, rest, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(coded_scan_kernel, dim3(1), dim3(kScanThreads), 0, rest, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((finalize_coded_kernel<kMulti, kVec>), dim3((uint32_t)groups),
+                     dim3(kThreads), 0, rest, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_extract_coded(const ExtractArgs& a, bool all_vec, hipStream_t stream,
+                                const StageSplit* split) {
+  hipStream_t rest;
+  if (a.num_tiles == 0) return split_after_stage(stream, split, rest);
+  if (a.table != nullptr)
+    return all_vec ? launch_coded<true, true>(a, stream, split)
+                   : launch_coded<true, false>(a, stream, split);
+  return all_vec ? launch_coded<false, true>(a, stream, split)
+                 : launch_coded<false, false>(a, stream, split);
+}
+
+template <typename IdxT, bool kMulti>
+static hipError_t launch_vec(const ExtractArgs& a, bool vec, hipStream_t stream,
+                             const StageSplit* split) {
+  return vec ? launch_all<IdxT, kMulti, true>(a, stream, split)
+             : launch_all<IdxT, kMulti, false>(a, stream, split);
+}
+
+hipError_t launch_extract(const ExtractArgs& a, bool idx64, bool all_vec, hipStream_t stream,
+                          const StageSplit* split) {
+  hipStream_t rest;
+  if (a.num_tiles == 0) return split_after_stage(stream, split, rest);
   const bool multi = a.table != nullptr;
   if (idx64)
-    return multi ? launch_vec<int64_t, true>(a, all_vec, stream)
-                 : launch_vec<int64_t, false>(a, all_vec, stream);
-  return multi ? launch_vec<int32_t, true>(a, all_vec, stream)
-               : launch_vec<int32_t, false>(a, all_vec, stream);
+    return multi ? launch_vec<int64_t, true>(a, all_vec, stream, split)
+                 : launch_vec<int64_t, false>(a, all_vec, stream, split);
+  return multi ? launch_vec<int32_t, true>(a, all_vec, stream, split)
+               : launch_vec<int32_t, false>(a, all_vec, stream, split);
 }
 
 }  // namespace aurora

@@ -5,17 +5,21 @@
 //
 // The global index space of the tensor list is cut into chunks of
 // `chunk_elems` words; a chunk may span several tensors and start inside
-// one.  Chunk c is extracted into staging slot c mod S (S streams, S slots)
-// on one of up to two extract lanes (streams[0], streams[1]); coded, its
-// indices are then gap + LEB128 coded in the slot.  One more stream
-// (streams[min(S - 1, 2)]) delivers the chunks in order: one kernel per
-// chunk reads the chunk's counts and the running totals from device memory
-// and stores its entries straight into the pinned host arrays over the host
-// link (kernel stores into pinned memory reach the 55 GB/s of DMA copies and
-// need no host round trip per chunk).  A delivery waits on its chunk's
-// extract event; the extract that reuses a slot waits on the delivery of
-// the slot's previous chunk.  The host only enqueues and waits once, at the
-// end.  With S == 1 everything runs in order on the one stream.
+// one.  Chunk c is extracted into staging slot c mod S (S streams, S slots).
+// Three streams have roles: streams[0] reads, running every chunk's stage
+// kernel (the pass over both copies) back to back; streams[1] codes,
+// taking each chunk's scan and finalize kernels once its stage kernel is
+// done, while the next chunk is being read; streams[2] delivers the chunks
+// in order: one kernel per chunk reads the chunk's counts and the running
+// totals from device memory and stores its entries straight into the
+// pinned host arrays over the host link (kernel stores into pinned memory
+// reach the 55 GB/s of DMA copies and need no host round trip per chunk).
+// Coded, the extract writes the chunk's positions gap + LEB128 coded
+// instead of as indices (three kernels per chunk, no index stream in
+// between).  A delivery waits on its chunk's coding; the reading of a chunk
+// that reuses a slot waits on the delivery of the slot's previous chunk.
+// The host only enqueues and waits once, at the end.  With S == 2 reading
+// and coding share streams[0]; with S == 1 everything runs in order on it.
 
 #include <string.h>
 
@@ -23,7 +27,6 @@
 
 #include "aurora_delta.h"
 #include "delta_internal.h"
-#include "leb128.h"
 
 using namespace aurora;
 
@@ -47,7 +50,7 @@ void chunk_slices(const uint16_t* const* prevs, const uint16_t* const* nexts,
 
 
 struct StagingLayout {
-  size_t idx, val, count, nbytes, bytes, enc_ws, ws, ws_bytes, per_stream;
+  size_t idx, val, count, nbytes, bytes, ws, ws_bytes, per_stream;
   size_t run, chunk_counts, total;   // after the S slots: running totals, per-chunk counts
 };
 
@@ -62,16 +65,16 @@ uint64_t leb_bytes_per_entry(uint64_t chunk) {
   return n;
 }
 
+// Coded, a slot holds no index stream: the extract writes the code itself.
 StagingLayout staging_layout(uint64_t chunk, size_t ws_bytes, bool leb, int streams,
                              uint64_t nchunks) {
   StagingLayout L;
   L.idx = 0;
-  L.val = align_up(L.idx + 8 * chunk);
+  L.val = align_up(L.idx + (leb ? 0 : 8 * chunk));
   L.count = align_up(L.val + 2 * chunk);
   L.nbytes = L.count + 8;
   L.bytes = align_up(L.nbytes + 8);
-  L.enc_ws = align_up(L.bytes + (leb ? leb_bytes_per_entry(chunk) * chunk : 0));
-  L.ws = align_up(L.enc_ws + (leb ? enc_layout(chunk).total : 0));
+  L.ws = align_up(L.bytes + (leb ? leb_bytes_per_entry(chunk) * chunk : 0));
   L.ws_bytes = ws_bytes;
   L.per_stream = align_up(L.ws + ws_bytes);
   L.run = L.per_stream * (size_t)streams;
@@ -115,26 +118,31 @@ struct DeliverArgs {
   uint64_t h_bytes_cap;
   uint16_t* h_val;
   uint64_t h_val_cap;
+  uint32_t xcds;               // workgroups on the last `xcds` XCDs store
 };
 
-// At most two extract lanes, so that the lanes and the delivery stream use
-// three streams: a process gets four hardware queues by default, and
-// streams beyond that share a queue, which serialises their work (with four
-// streams the pipeline measured 15% slower than with three).
-constexpr int kMaxExtractLanes = 2;
+// Streams beyond the three roles stay idle: a process gets four hardware
+// queues by default, and streams beyond that share a queue, which
+// serialises their work.
 constexpr int kDeliverThreads = 256;
-// Stores into host memory are slow to complete, and an XCD with many of
-// them outstanding serves its HBM reads far slower: a host-write kernel
-// spread over all 8 XCDs cut a concurrent HBM read kernel from 6.9 to
-// 1.8 TB/s.  Confined to 2 XCDs with 8 workgroups each it still fills the
-// host link (55.6 GB/s) while the reader keeps 6.6 TB/s.  Workgroup b runs
-// on XCD b mod 8, so the grid holds 8 workgroups per XCD and only those on
-// the last kDeliverXcds XCDs work (small kernels of one or a few
-// workgroups, such as the scans, run on the first XCDs).
+// Stores into host memory are slow to complete, and while many are
+// outstanding the GPU's HBM reads slow down: a host-write kernel spread over
+// all 8 XCDs cut a concurrent HBM read kernel from 6.9 to 1.8 TB/s.  So the
+// delivery runs few workgroups, on the last XCDs (workgroup b runs on XCD
+// b mod 8; the grid holds the same count per XCD and only those on the
+// last `xcds` work; small kernels of one or a few workgroups, such as the
+// scans, run on the first XCDs).  How few is a trade between filling the
+// host link and leaving the reads alone (Qwen3-14B, 2^27-word chunks,
+// plain / coded ms): 2 XCDs x 8 workgroups 30.4 / 17.1; 4 x 4 29.7 / 17.2;
+// 8 x 2 29.7-29.8 / 17.0; 1 x 4 35.0 / 13.7-14.1; 2 x 2 34.4 / 14.0;
+// 1 x 2 37.4 / 18.6.  The plain stream (10 bytes per entry) needs the
+// link's rate, the coded one (about 3.3) far less: it takes 1 x 4.
 constexpr int kXcds = 8;
-constexpr int kDeliverXcds = 2;
-constexpr int kDeliverPerXcd = 8;
-constexpr int kDeliverBlocks = kXcds * kDeliverPerXcd;
+struct DeliverShape {
+  uint32_t xcds, per_xcd;
+};
+constexpr DeliverShape kDeliverPlain = {4, 4};
+constexpr DeliverShape kDeliverCoded = {1, 4};
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 // four dwords at a 4-byte aligned address (one 16-byte load)
@@ -193,10 +201,11 @@ __global__ __launch_bounds__(kDeliverThreads) void deliver_kernel(DeliverArgs a)
   const uint64_t* r = a.run + 2 * (a.c & 1);
   const uint64_t be = r[0], bb = r[1];
   const uint32_t xcd = blockIdx.x % kXcds;
-  if (xcd < (uint32_t)(kXcds - kDeliverXcds)) return;
-  const uint64_t wg = (uint64_t)(blockIdx.x / kXcds) * kDeliverXcds + (xcd - (kXcds - kDeliverXcds));
+  const uint32_t first_xcd = kXcds - a.xcds;
+  if (xcd < first_xcd) return;
+  const uint64_t wg = (uint64_t)(blockIdx.x / kXcds) * a.xcds + (xcd - first_xcd);
   const uint64_t i0 = wg * blockDim.x + threadIdx.x;
-  const uint64_t stride = (uint64_t)(gridDim.x / kXcds) * kDeliverXcds * blockDim.x;
+  const uint64_t stride = (uint64_t)(gridDim.x / kXcds) * a.xcds * blockDim.x;
   if (i0 == 0) {
     uint64_t* w = a.run + 2 * ((a.c + 1) & 1);
     w[0] = be + cnt;
@@ -220,7 +229,8 @@ __global__ void run_reset_kernel(uint64_t* run) {
 }
 
 // Largest workspace any chunk's extract needs (tiles at worst alignment).
-size_t max_chunk_workspace(const uint64_t* numels, int32_t T, uint64_t total, uint64_t chunk) {
+size_t max_chunk_workspace(const uint64_t* numels, int32_t T, uint64_t total, uint64_t chunk,
+                           bool coded) {
   size_t best = 0;
   for (uint64_t lo = 0; lo < total; lo += chunk) {
     const uint64_t hi = (total - lo < chunk) ? total : lo + chunk;
@@ -234,7 +244,7 @@ size_t max_chunk_workspace(const uint64_t* numels, int32_t T, uint64_t total, ui
       }
       base += numels[t];
     }
-    const size_t need = workspace_bytes(tiles, rows, kDefaultStageCap);
+    const size_t need = workspace_bytes(tiles, rows, kDefaultStageCap, coded);
     if (need > best) best = need;
   }
   return best;
@@ -253,7 +263,7 @@ static size_t staging_bytes_impl(const uint64_t* numels, int32_t num_tensors,
   for (int32_t t = 0; t < num_tensors; ++t) total += numels[t];
   const uint64_t chunk = opts->chunk_elems < total ? opts->chunk_elems : (total ? total : 1);
   const uint64_t nchunks = (total + chunk - 1) / chunk;
-  const size_t ws = max_chunk_workspace(numels, num_tensors, total, chunk);
+  const size_t ws = max_chunk_workspace(numels, num_tensors, total, chunk, leb);
   return staging_layout(chunk, ws, leb, opts->num_streams, nchunks).total;
 }
 
@@ -329,7 +339,7 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
              staging_bytes, d_staging, need);
     return DELTA_ERR_WORKSPACE;
   }
-  const size_t ws = max_chunk_workspace(numels, T, total, chunk);
+  const size_t ws = max_chunk_workspace(numels, T, total, chunk, o.leb);
   const StagingLayout L = staging_layout(chunk, ws, o.leb, S, nchunks);
   const uint64_t bytes_cap = leb_bytes_per_entry(chunk) * chunk;
 
@@ -356,14 +366,27 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
   if (base.h_idx_cap && !base.h_idx) base.h_idx_cap = 0;
   if (base.h_bytes_cap && !base.h_bytes) base.h_bytes_cap = 0;
 
-  // E extract lanes, one delivery stream (the same one when S == 1)
-  const int E = S > 1 ? (S - 1 < kMaxExtractLanes ? S - 1 : kMaxExtractLanes) : 1;
-  hipStream_t const ds = S > 1 ? streams[E] : streams[0];
-  std::vector<hipEvent_t> extracted(S, nullptr), delivered(S, nullptr);
+  // Three roles: the reading stream runs every chunk's stage kernel (the
+  // pass over the weights) back to back; the coding stream takes each
+  // chunk's scan and finalize kernels as soon as its stage kernel is done,
+  // while the next chunk is read; the delivery stream stores the chunks
+  // into host memory in order.  With two streams reading and coding share
+  // the first; with one, everything runs in order on it.
+  const DeliverShape shape = o.leb ? kDeliverCoded : kDeliverPlain;
+  hipStream_t const rs = streams[0];
+  hipStream_t const cs = S > 2 ? streams[1] : streams[0];
+  hipStream_t const ds = S > 2 ? streams[2] : streams[S - 1];
+  // The events only order work on this device, so they skip the
+  // system-scope fence (an L2 write-back on every record: about 20 us
+  // between two kernels of the reading stream).  The host reads its
+  // arrays after synchronising the streams.
+  std::vector<hipEvent_t> staged(S, nullptr), extracted(S, nullptr), delivered(S, nullptr);
+  const unsigned ev_flags = hipEventDisableTiming | hipEventDisableSystemFence;
   hipError_t e = hipSuccess;
   for (int i = 0; i < S && e == hipSuccess; ++i) {
-    e = hipEventCreateWithFlags(&extracted[i], hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&delivered[i], hipEventDisableTiming);
+    e = hipEventCreateWithFlags(&staged[i], ev_flags);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&extracted[i], ev_flags);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&delivered[i], ev_flags);
   }
   char* const stg = (char*)d_staging;
   uint64_t* const run = (uint64_t*)(stg + L.run);
@@ -374,49 +397,36 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
   }
   delta_status_t status = DELTA_OK;
   std::vector<SliceIn> sl;
-  const EncLayout EL = enc_layout(chunk);
   for (uint64_t c = 0; c < nchunks && e == hipSuccess; ++c) {
     const int slot = (int)(c % (uint64_t)S);
-    hipStream_t xs = streams[c % (uint64_t)E];
     char* stage = stg + L.per_stream * (size_t)slot;
-    if (c >= (uint64_t)S) {   // the slot's previous chunk must have been delivered
-      e = hipStreamWaitEvent(xs, delivered[slot], 0);
+    if (c >= (uint64_t)S && ds != rs) {   // the slot's previous chunk must have been delivered
+      e = hipStreamWaitEvent(rs, delivered[slot], 0);
       if (e != hipSuccess) break;
     }
     const uint64_t lo = c * chunk;
     const uint64_t hi = (total - lo < chunk) ? total : lo + chunk;
     chunk_slices(prevs, nexts, numels, T, lo, hi, sl);
+    // coded: the chunk's positions as one gap + LEB128 segment based at
+    // its first word, written by the extract itself
+    const CodedOut co = {(uint8_t*)(stage + L.bytes), bytes_cap, (uint64_t*)(stage + L.nbytes),
+                         (int64_t)lo};
+    const StageSplit split = {staged[slot], cs};
     const delta_status_t st =
         enqueue_extract(sl.data(), sl.size(), 0, true, stage + L.idx, (uint16_t*)(stage + L.val),
-                        chunk, (uint64_t*)(stage + L.count), nullptr, stage + L.ws, L.ws_bytes, xs);
+                        chunk, (uint64_t*)(stage + L.count), nullptr, stage + L.ws, L.ws_bytes, rs,
+                        o.leb ? &co : nullptr, &split);
     if (st != DELTA_OK) {
       status = st;
       break;
     }
-    if (o.leb) {
-      // the chunk's indices as one segment based at its first word; the
-      // encoder reads the entry count the extract left in device memory
-      EncArgs a;
-      memset(&a, 0, sizeof(a));
-      a.idx = (const int64_t*)(stage + L.idx);
-      a.count = chunk;
-      a.d_count_in = (const uint64_t*)(stage + L.count);
-      a.segs = {nullptr, nullptr, 0, (int64_t)(c * chunk)};
-      a.out = (uint8_t*)(stage + L.bytes);
-      a.capacity = bytes_cap;
-      a.d_nbytes = (uint64_t*)(stage + L.nbytes);
-      a.tile_bytes = (uint32_t*)(stage + L.enc_ws + EL.tile_bytes);
-      e = launch_leb128_encode(a, (uint64_t*)(stage + L.enc_ws + EL.group_sum),
-                               (uint64_t*)(stage + L.enc_ws + EL.group_excl), xs);
-      if (e != hipSuccess) break;
-    }
-    if (xs != ds) {
-      e = hipEventRecord(extracted[slot], xs);
+    if (cs != ds) {
+      e = hipEventRecord(extracted[slot], cs);
       if (e == hipSuccess) e = hipStreamWaitEvent(ds, extracted[slot], 0);
       if (e != hipSuccess) break;
     }
     DeliverArgs d = base;
-    d.idx = (const int64_t*)(stage + L.idx);
+    d.idx = o.leb ? nullptr : (const int64_t*)(stage + L.idx);
     d.val = (const uint16_t*)(stage + L.val);
     d.bytes = o.leb ? (const uint8_t*)(stage + L.bytes) : nullptr;
     d.d_count = (const uint64_t*)(stage + L.count);
@@ -424,7 +434,9 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     d.run = run;
     d.chunk_counts = o.leb ? d_chunk_counts : nullptr;
     d.c = c;
-    hipLaunchKernelGGL(deliver_kernel, dim3(kDeliverBlocks), dim3(kDeliverThreads), 0, ds, d);
+    d.xcds = shape.xcds;
+    hipLaunchKernelGGL(deliver_kernel, dim3(kXcds * shape.per_xcd), dim3(kDeliverThreads), 0, ds,
+                       d);
     e = hipGetLastError();
     if (e == hipSuccess) e = hipEventRecord(delivered[slot], ds);
   }
@@ -441,6 +453,7 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
                     hipMemcpyDeviceToHost);
   }
   for (int i = 0; i < S; ++i) {
+    if (staged[i]) (void)hipEventDestroy(staged[i]);
     if (extracted[i]) (void)hipEventDestroy(extracted[i]);
     if (delivered[i]) (void)hipEventDestroy(delivered[i]);
   }

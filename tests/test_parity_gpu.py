@@ -381,6 +381,49 @@ def test_pipeline_plan_reused_across_steps():
         np.testing.assert_array_equal(v2.view(torch.int16).numpy().view(np.uint16), ref_val)
 
 
+def mixed_layout_list(seed):
+    """Tensors that exercise every branch of the coded extract: many small
+    ones (chunks with a tensor table), a dense one (tiles overflow their
+    staging slots and windows span thousands of entries), an unchanged one
+    and a very sparse long one (empty tiles and groups, long gaps), a view
+    that starts mid-line and a pair whose copies differ in alignment."""
+    prevs, news = [], []
+    for i in range(40):
+        p, q = rand_pair(3000 + 17 * i, 0.03, seed + i)
+        prevs.append(p)
+        news.append(q)
+    for n, dens in [(200_003, 0.4), (50_000, 0.0), (700_001, 0.0004), (90_000, 0.13)]:
+        p, q = rand_pair(n, dens, seed + n)
+        prevs.append(p)
+        news.append(q)
+    p, q = rand_pair(120_002, 0.02, seed + 7)
+    prevs.append(p[3:100_003])       # starts 6 bytes into a 16-byte line
+    news.append(q[3:100_003])
+    p, q = rand_pair(80_010, 0.05, seed + 8)
+    prevs.append(p[1:80_001])        # the two copies at different alignments
+    news.append(q[5:80_005])
+    return prevs, news
+
+
+@pytest.mark.parametrize("chunk,streams", [(10_007, 4), (1 << 16, 3), (1 << 20, 4),
+                                           (1 << 27, 1)])
+def test_pipeline_leb128_mixed_layouts(chunk, streams):
+    prevs, news = mixed_layout_list(seed=900)
+    ref_idx, ref_val, _, _ = oracle.extract_multi(
+        [host_u16(p) for p in prevs], [host_u16(q) for q in news])
+    total = sum(p.numel() for p in prevs)
+    hb, hv, counts, used = ad.delta_extract_pipelined_leb128(prevs, news, chunk_elems=chunk,
+                                                            num_streams=streams)
+    ref_bytes, ref_counts = oracle_chunk_stream(ref_idx, used, total)
+    np.testing.assert_array_equal(np.array(counts), ref_counts)
+    np.testing.assert_array_equal(hb.numpy(), ref_bytes)
+    np.testing.assert_array_equal(hv.view(torch.int16).numpy().view(np.uint16), ref_val)
+    h_idx, h_val = ad.delta_extract_pipelined(prevs, news, chunk_elems=chunk,
+                                              num_streams=streams)
+    np.testing.assert_array_equal(h_idx.numpy(), ref_idx)
+    np.testing.assert_array_equal(h_val.view(torch.int16).numpy().view(np.uint16), ref_val)
+
+
 def test_pipeline_leb128_capacity_retry():
     prevs, news = make_list([40_000, 20_000], 0.05, seed=19)
     hb = torch.empty(5, dtype=torch.uint8, pin_memory=True)
