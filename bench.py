@@ -201,10 +201,12 @@ def pipeline_measurement(args, dev):
     }
 
 
-def leb128_measurement(ad, idx, val, d_offs, numels, rollout, stream, reps):
+def leb128_measurement(ad, plan, idx, val, d_offs, numels, rollout, stream, reps):
     """Gap + LEB128 encode of the extracted global indices with one segment
     per tensor (tensor-local first index), then decode, each timed with HIP
-    events on the launch stream; the decode must return the indices."""
+    events on the launch stream; the decode must return the indices.  Also
+    the extract that writes the coded indices itself
+    (delta_extract_multi_leb128), whose bytes must equal the encoder's."""
     import torch
     lib = ad.library()
     dev = idx.device
@@ -263,8 +265,28 @@ def leb128_measurement(ad, idx, val, d_offs, numels, rollout, stream, reps):
     stream.synchronize()
     if int(flag2.item()):
         raise RuntimeError("decode-in-apply flagged an error")
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(reps)]
-    for e0, e1, e2, e3, e4 in ev:
+    # the sender's side in one call: extract straight to the coded stream
+    cws = torch.empty(ad.delta_extract_multi_leb128_workspace_bytes(numels), dtype=torch.uint8,
+                      device=dev)
+    ccode = torch.empty(nb + 64, dtype=torch.uint8, device=dev)
+    cval = torch.empty(K + 64, dtype=val.dtype, device=dev)
+    ccnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    cnb = torch.zeros(1, dtype=torch.int64, device=dev)
+    coffs = torch.zeros(T + 1, dtype=torch.int64, device=dev)
+    cboffs = torch.zeros(T + 1, dtype=torch.int64, device=dev)
+
+    def extract_coded():
+        ad.delta_extract_multi_leb128_into(plan, ccode, cval, ccnt, cnb, cws, coffs, cboffs,
+                                           stream)
+
+    extract_coded()
+    stream.synchronize()
+    if (int(ccnt.item()) != K or int(cnb.item()) != nb or not torch.equal(ccode[:nb], code)
+            or not torch.equal(cboffs, seg_bytes) or not torch.equal(coffs, d_offs)
+            or not torch.equal(cval[:K].view(torch.int16), val.view(torch.int16))):
+        raise RuntimeError("the coded extract differs from extract + encode")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
+    for e0, e1, e2, e3, e4, e5 in ev:
         e0.record(stream)
         encode()
         e1.record(stream)
@@ -274,12 +296,16 @@ def leb128_measurement(ad, idx, val, d_offs, numels, rollout, stream, reps):
         e3.record(stream)
         ad.delta_apply_multi(rollout, out[:K], val, workspace=multi_ws, stream=stream)
         e4.record(stream)
+        extract_coded()
+        e5.record(stream)
     stream.synchronize()
     med = lambda xs: sorted(xs)[len(xs) // 2]
     enc = med([e[0].elapsed_time(e[1]) for e in ev])
     dec = med([e[1].elapsed_time(e[2]) for e in ev])
     app_coded = med([e[2].elapsed_time(e[3]) for e in ev])
     app_plain = med([e[3].elapsed_time(e[4]) for e in ev])
+    ext_coded = med([e[4].elapsed_time(e[5]) for e in ev])
+    N = sum(numels)
     return {
         "workload": f"the {K} extracted int64 global indices, one segment per tensor",
         "bytes": nb,
@@ -291,6 +317,12 @@ def leb128_measurement(ad, idx, val, d_offs, numels, rollout, stream, reps):
         "decode_GBps_algorithmic": round((nb + 8 * K) / (dec / 1e3) / 1e9, 1),
         "apply_from_code_ms": round(app_coded, 4),
         "decode_then_apply_ms": round(dec + app_plain, 4),
+        # delta_extract_multi_leb128: both copies read once, the words and the
+        # code written (no index stream)
+        "extract_coded_ms": round(ext_coded, 4),
+        "extract_coded_GBps_scanned": round(4 * N / (ext_coded / 1e3) / 1e9, 1),
+        "extract_coded_GBps_algorithmic": round((4 * N + 2 * K + nb) / (ext_coded / 1e3) / 1e9,
+                                                1),
     }
 
 
@@ -439,8 +471,8 @@ def extras(args, ad, synth, ws, rollout, plan, out_idx, out_val, d_offs, work, s
     hashing, the fused layout and delta chains (the last one overwrites the
     rollout copy)."""
     import torch
-    result["leb128"] = leb128_measurement(ad, out_idx[:K], out_val[:K], d_offs, plan.numels,
-                                          rollout, stream, args.steps)
+    result["leb128"] = leb128_measurement(ad, plan, out_idx[:K], out_val[:K], d_offs,
+                                          plan.numels, rollout, stream, args.steps)
     # the delta's two streams as one byte buffer, as an artifact holds them
     payload = torch.cat([out_idx[:K].view(torch.uint8), out_val[:K].view(torch.uint8)])
     result["hash"] = hash_measurement(ad, payload, stream, args.steps)

@@ -286,6 +286,43 @@ delta_status_t delta_leb128_decode(const uint8_t* in, uint64_t nbytes,
                                    uint64_t* d_count, uint32_t* d_error_flag, void* workspace,
                                    size_t workspace_bytes, hipStream_t stream);
 
+/* Workspace bytes for delta_extract_multi_leb128 over tensors of the given
+ * sizes (host array). */
+size_t delta_extract_multi_leb128_workspace_bytes(const uint64_t* numels, int32_t num_tensors);
+
+/*
+ * delta_extract_multi_leb128 — delta_extract_multi whose index stream leaves
+ * the extract already gap + LEB128 coded (Sec. 5.1 "Sparse encoding"): the
+ * int64 index stream is never formed.  One segment per tensor: the bytes
+ * equal delta_leb128_encode of delta_extract_multi's indices with
+ * seg_offsets = tensor_offsets and seg_bases = the tensor bases, so each
+ * tensor's first entry is its tensor-local index and the rest are gaps.
+ *   prev_ptrs, next_ptrs, numels, num_tensors  as delta_extract_multi.
+ *   out_code      device bytes [code_capacity]: the coded indices; only the
+ *                 first code_capacity bytes are written.
+ *   d_nbytes      device uint64: the true code length.
+ *   out_val       device words [capacity], as delta_extract_multi.
+ *   d_count       device uint64: the true number of entries.
+ *   d_tensor_offsets       device uint64 [num_tensors + 1] or NULL: entry
+ *                 offsets, as delta_extract_multi.
+ *   d_tensor_byte_offsets  device uint64 [num_tensors + 1] or NULL: byte
+ *                 offset in out_code where each tensor's numbers start, and
+ *                 the total (what delta_leb128_encode returns as
+ *                 d_seg_byte_offsets).
+ *   workspace     delta_extract_multi_leb128_workspace_bytes(numels, T).
+ * Enqueues on `stream`.  At most 9 code bytes per entry (indices are below
+ * 2^63); at 1% density about 1.3.
+ */
+delta_status_t delta_extract_multi_leb128(const uint16_t* const* prev_ptrs,
+                                          const uint16_t* const* next_ptrs,
+                                          const uint64_t* numels, int32_t num_tensors,
+                                          uint8_t* out_code, uint64_t code_capacity,
+                                          uint64_t* d_nbytes, uint16_t* out_val,
+                                          uint64_t capacity, uint64_t* d_count,
+                                          uint64_t* d_tensor_offsets,
+                                          uint64_t* d_tensor_byte_offsets, void* workspace,
+                                          size_t workspace_bytes, hipStream_t stream);
+
 /*
  * Delta chains — Sec. 5.4, "Version-predicate join and delta catch-up": a
  * worker K versions behind replays the missed deltas D_1 .. D_K in order.

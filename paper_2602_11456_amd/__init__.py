@@ -102,6 +102,11 @@ def delta_extract_multi_workspace_bytes(numels: Sequence[int]) -> int:
     return int(library().delta_extract_multi_workspace_bytes(arr, len(numels)))
 
 
+def delta_extract_multi_leb128_workspace_bytes(numels: Sequence[int]) -> int:
+    arr = _u64_array(numels)
+    return int(library().delta_extract_multi_leb128_workspace_bytes(arr, len(numels)))
+
+
 def delta_apply_multi_workspace_bytes(num_tensors: int) -> int:
     return int(library().delta_apply_multi_workspace_bytes(int(num_tensors)))
 
@@ -226,6 +231,58 @@ def delta_extract_multi(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tens
         if k <= cap:
             return idx[:k], val[:k], offs
         cap = k
+    raise AssertionError("count changed between two runs on the same input")
+
+
+def delta_extract_multi_leb128_into(plan: MultiPlan, out_code: torch.Tensor,
+                                    out_val: torch.Tensor, d_count: torch.Tensor,
+                                    d_nbytes: torch.Tensor, workspace: torch.Tensor,
+                                    d_offsets: Optional[torch.Tensor] = None,
+                                    d_byte_offsets: Optional[torch.Tensor] = None,
+                                    stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Enqueue ``delta_extract_multi_leb128`` into preallocated buffers (no
+    sync): the coded indices (one segment per tensor) to ``out_code``."""
+    if out_code.dtype != torch.uint8:
+        raise TypeError("out_code must be uint8")
+    for name, t in (("d_offsets", d_offsets), ("d_byte_offsets", d_byte_offsets)):
+        if t is not None and t.numel() < plan.T + 1:
+            raise ValueError(f"{name} needs num_tensors + 1 entries")
+    _check(library().delta_extract_multi_leb128(
+        plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, plan.T, out_code.data_ptr(),
+        out_code.numel(), d_nbytes.data_ptr(), _words(out_val, "out_val"), out_val.numel(),
+        d_count.data_ptr(), d_offsets.data_ptr() if d_offsets is not None else None,
+        d_byte_offsets.data_ptr() if d_byte_offsets is not None else None,
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def delta_extract_multi_leb128(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tensor],
+                               capacity: Optional[int] = None,
+                               code_capacity: Optional[int] = None,
+                               stream: Optional[torch.cuda.Stream] = None):
+    """The delta of a tensor list with its indices gap + LEB128 coded by the
+    extract itself, one segment per tensor (Sec. 5.1).  Returns (code bytes,
+    new words, tensor_offsets [T+1] in entries, tensor byte offsets [T+1]).
+    Synchronises; reruns once with exact capacities if an output was short."""
+    plan = MultiPlan(prevs, news)
+    dev = plan.device
+    ws = _workspace(delta_extract_multi_leb128_workspace_bytes(plan.numels), dev)
+    cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    nb = torch.zeros(1, dtype=torch.int64, device=dev)
+    offs = torch.zeros(plan.T + 1, dtype=torch.int64, device=dev)
+    boffs = torch.zeros(plan.T + 1, dtype=torch.int64, device=dev)
+    cap = _default_capacity(plan.total) if capacity is None else int(capacity)
+    ccap = 2 * cap + 64 if code_capacity is None else int(code_capacity)
+    dtype = prevs[0].dtype if plan.T else torch.bfloat16
+    for _ in range(2):
+        code = torch.empty(max(ccap, 1), dtype=torch.uint8, device=dev)
+        val = torch.empty(max(cap, 1), dtype=dtype, device=dev)
+        delta_extract_multi_leb128_into(plan, code[:ccap], val[:cap], cnt, nb, ws, offs, boffs,
+                                        stream)
+        (stream or torch.cuda.current_stream()).synchronize()
+        k, n = int(cnt.item()), int(nb.item())
+        if k <= cap and n <= ccap:
+            return code[:n], val[:k], offs, boffs
+        cap, ccap = max(cap, k), max(ccap, n)
     raise AssertionError("count changed between two runs on the same input")
 
 

@@ -76,6 +76,9 @@ SIGNATURES = {
     "delta_extract": (STATUS, [P, P, U64, ctypes.c_int, P, P, U64, P, P, SZ, P]),
     "delta_extract_multi": (STATUS, [P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
     "delta_extract_fused": (STATUS, [P, P, P, I32, P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
+    "delta_extract_multi_leb128_workspace_bytes": (SZ, [P, I32]),
+    "delta_extract_multi_leb128": (STATUS, [P, P, P, I32, P, U64, P, P, U64, P, P, P, P, SZ,
+                                            P]),
     "delta_apply": (STATUS, [P, U64, ctypes.c_int, P, P, U64, P, P]),
     "delta_apply_multi": (STATUS, [P, P, I32, P, P, U64, P, P, SZ, P]),
     "delta_apply_checked": (STATUS, [P, U64, ctypes.c_int, P, P, U64, P, U64, U64, P]),

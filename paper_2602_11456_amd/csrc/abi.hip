@@ -87,6 +87,7 @@ uint64_t build_descs(const SliceIn* slices, size_t num_slices, std::vector<Tenso
     d.head = d.vec ? hp : 0u;
     d.off_lo = next_slot;
     d.slot = s.tensor;
+    d.seg_base = s.seg_base;
     next_slot = s.tensor + 1;
     tiles += tiles_for(d.n, d.head);
     out.push_back(d);
@@ -94,10 +95,36 @@ uint64_t build_descs(const SliceIn* slices, size_t num_slices, std::vector<Tenso
   return tiles;
 }
 
-size_t multi_workspace_bound(const uint64_t* numels, int32_t T) {
+size_t multi_workspace_bound(const uint64_t* numels, int32_t T, bool coded = false) {
   uint64_t tiles = 0;
   for (int32_t t = 0; t < T; ++t) tiles += tiles_bound(numels[t]);
-  return workspace_bytes(tiles, (uint64_t)(T > 0 ? T : 0), kDefaultStageCap);
+  return workspace_bytes(tiles, (uint64_t)(T > 0 ? T : 0), kDefaultStageCap, coded);
+}
+
+// The slices of a tensor list (one per tensor, word 0 of tensor t at the
+// sum of the sizes before it), after the checks every list entry point
+// shares.
+delta_status_t list_slices(const uint16_t* const* prev_ptrs, const uint16_t* const* next_ptrs,
+                           const uint64_t* numels, int32_t num_tensors,
+                           std::vector<SliceIn>& slices) {
+  if (num_tensors < 0) return fail(DELTA_ERR_INVALID_ARG, "num_tensors < 0");
+  if (num_tensors > 0 && (!prev_ptrs || !next_ptrs || !numels))
+    return fail(DELTA_ERR_INVALID_ARG, "tensor arrays are NULL");
+  slices.clear();
+  slices.reserve(num_tensors);
+  uint64_t base = 0;
+  for (int32_t t = 0; t < num_tensors; ++t) {
+    if (numels[t] > 0 && (!prev_ptrs[t] || !next_ptrs[t]))
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: NULL pointer", t);
+    if (odd(prev_ptrs[t]) || odd(next_ptrs[t]))
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: not 2-byte aligned", t);
+    if (base + numels[t] < base) return fail(DELTA_ERR_INVALID_ARG, "total size overflows");
+    slices.push_back({prev_ptrs[t], next_ptrs[t], numels[t], base, (uint32_t)t, base});
+    base += numels[t];
+  }
+  if (base > 0 && base - 1 > 0x7FFFFFFFFFFFFFFFull)
+    return fail(DELTA_ERR_INDEX_OVERFLOW, "total size exceeds int64");
+  return DELTA_OK;
 }
 
 delta_status_t check_workspace(void* ws, size_t have, size_t need) {
@@ -124,10 +151,13 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
   if (tiles > 0xFFFFFFFFull / kThreads)
     return fail(DELTA_ERR_INVALID_ARG, "too many words for one launch (%llu tiles)",
                 (unsigned long long)tiles);
-  if (coded) d_offsets = nullptr;
+  if (coded && !coded->per_tensor) d_offsets = nullptr;
+  uint64_t* d_byte_offsets = (coded && coded->per_tensor) ? coded->d_byte_offsets : nullptr;
   if (tiles == 0) {
     hipError_t e = launch_reset(d_count, d_offsets, d_offsets ? num_tensors + 1 : 0, stream);
-    if (e == hipSuccess && coded) e = launch_reset(coded->d_nbytes, nullptr, 0, stream);
+    if (e == hipSuccess && coded)
+      e = launch_reset(coded->d_nbytes, d_byte_offsets, d_byte_offsets ? num_tensors + 1 : 0,
+                       stream);
     if (e == hipSuccess && split) {
       e = hipEventRecord(split->staged, stream);
       if (e == hipSuccess && split->rest != stream) e = hipStreamWaitEvent(split->rest, split->staged, 0);
@@ -175,14 +205,16 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
   bool all_vec = true;
   for (const TensorDesc& t : descs) all_vec = all_vec && t.vec;
   if (coded) {
-    a.tile_code = (uint32_t*)(ws + L.tile_code);
-    a.tile_fl = (int64_t*)(ws + L.tile_fl);
+    a.tile_rec = (uint64_t*)(ws + L.tile_rec);
     a.group_bexcl = (uint64_t*)(ws + L.group_bexcl);
     a.group_prev = (int64_t*)(ws + L.group_prev);
     a.code_out = coded->out;
     a.code_capacity = coded->capacity;
     a.d_nbytes = coded->d_nbytes;
-    a.code_base = coded->base;
+    a.code_base = coded->per_tensor ? 0 : coded->base;
+    a.seg_per_tensor = coded->per_tensor ? 1u : 0u;
+    a.group_first_local = (int64_t*)(ws + L.group_first_local);
+    a.d_tensor_byte_offsets = d_byte_offsets;
     e = launch_extract_coded(a, all_vec, stream, split);
   } else {
     e = launch_extract(a, idx64, all_vec, stream, split);
@@ -250,7 +282,7 @@ delta_status_t delta_extract(const uint16_t* prev, const uint16_t* next, uint64_
   if (index_type == DELTA_INDEX_I32 && numel > 0 && numel - 1 > 0x7FFFFFFFull)
     return fail(DELTA_ERR_INDEX_OVERFLOW, "numel %llu needs int64 indices",
                 (unsigned long long)numel);
-  const SliceIn slice{prev, next, numel, 0, 0};
+  const SliceIn slice{prev, next, numel, 0, 0, 0};
   return enqueue_extract(&slice, 1, 1, index_type == DELTA_INDEX_I64, out_idx, out_val, capacity,
                          d_count, nullptr, workspace, workspace_bytes, stream);
 }
@@ -261,30 +293,46 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
                                    uint64_t capacity, uint64_t* d_count,
                                    uint64_t* d_tensor_offsets, void* workspace,
                                    size_t workspace_bytes, hipStream_t stream) {
-  if (num_tensors < 0) return fail(DELTA_ERR_INVALID_ARG, "num_tensors < 0");
-  if (num_tensors > 0 && (!prev_ptrs || !next_ptrs || !numels))
-    return fail(DELTA_ERR_INVALID_ARG, "tensor arrays are NULL");
   if (!d_count) return fail(DELTA_ERR_INVALID_ARG, "d_count is NULL");
   if (capacity > 0 && (!out_idx || !out_val))
     return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val is NULL with capacity %llu",
                 (unsigned long long)capacity);
   std::vector<SliceIn> slices;
-  slices.reserve(num_tensors);
-  uint64_t base = 0;
-  for (int32_t t = 0; t < num_tensors; ++t) {
-    if (numels[t] > 0 && (!prev_ptrs[t] || !next_ptrs[t]))
-      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: NULL pointer", t);
-    if (odd(prev_ptrs[t]) || odd(next_ptrs[t]))
-      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: not 2-byte aligned", t);
-    if (base + numels[t] < base) return fail(DELTA_ERR_INVALID_ARG, "total size overflows");
-    slices.push_back({prev_ptrs[t], next_ptrs[t], numels[t], base, (uint32_t)t});
-    base += numels[t];
-  }
-  if (base > 0 && base - 1 > 0x7FFFFFFFFFFFFFFFull)
-    return fail(DELTA_ERR_INDEX_OVERFLOW, "total size exceeds int64");
+  const delta_status_t st = list_slices(prev_ptrs, next_ptrs, numels, num_tensors, slices);
+  if (st != DELTA_OK) return st;
   return enqueue_extract(slices.data(), slices.size(), (uint32_t)num_tensors, true, out_idx,
                          out_val, capacity, d_count, d_tensor_offsets, workspace,
                          workspace_bytes, stream);
+}
+
+size_t delta_extract_multi_leb128_workspace_bytes(const uint64_t* numels, int32_t num_tensors) {
+  if (num_tensors < 0 || (num_tensors > 0 && !numels)) return 0;
+  return multi_workspace_bound(numels, num_tensors, true);
+}
+
+delta_status_t delta_extract_multi_leb128(const uint16_t* const* prev_ptrs,
+                                          const uint16_t* const* next_ptrs,
+                                          const uint64_t* numels, int32_t num_tensors,
+                                          uint8_t* out_code, uint64_t code_capacity,
+                                          uint64_t* d_nbytes, uint16_t* out_val,
+                                          uint64_t capacity, uint64_t* d_count,
+                                          uint64_t* d_tensor_offsets,
+                                          uint64_t* d_tensor_byte_offsets, void* workspace,
+                                          size_t workspace_bytes, hipStream_t stream) {
+  if (!d_count || !d_nbytes) return fail(DELTA_ERR_INVALID_ARG, "d_count/d_nbytes is NULL");
+  if (capacity > 0 && !out_val)
+    return fail(DELTA_ERR_INVALID_ARG, "out_val is NULL with capacity %llu",
+                (unsigned long long)capacity);
+  if (code_capacity > 0 && !out_code)
+    return fail(DELTA_ERR_INVALID_ARG, "out_code is NULL with code_capacity %llu",
+                (unsigned long long)code_capacity);
+  std::vector<SliceIn> slices;
+  const delta_status_t st = list_slices(prev_ptrs, next_ptrs, numels, num_tensors, slices);
+  if (st != DELTA_OK) return st;
+  const CodedOut co = {out_code, code_capacity, d_nbytes, 0, true, d_tensor_byte_offsets};
+  return enqueue_extract(slices.data(), slices.size(), (uint32_t)num_tensors, true, nullptr,
+                         out_val, capacity, d_count, d_tensor_offsets, workspace,
+                         workspace_bytes, stream, &co);
 }
 
 delta_status_t delta_extract_fused(const uint16_t* const* prev_ptrs,
@@ -328,7 +376,7 @@ delta_status_t delta_extract_fused(const uint16_t* const* prev_ptrs,
       return fail(DELTA_ERR_INVALID_ARG, "tensor %d: block [%llu, +%llu) outside target %d", t,
                   (unsigned long long)block_offset[t], (unsigned long long)numels[t], f);
     slices.push_back({prev_ptrs[t], next_ptrs[t], numels[t], tbase[f] + block_offset[t],
-                      (uint32_t)f});
+                      (uint32_t)f, tbase[f]});
   }
   // output order is the fused index order: blocks sorted by their base
   std::stable_sort(slices.begin(), slices.end(),

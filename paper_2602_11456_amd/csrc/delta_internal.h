@@ -57,7 +57,7 @@ struct TensorDesc {
   uint32_t vec;           // 1: prev and next share alignment, 16-byte loads
   uint32_t off_lo;        // first tensor_offsets slot written by this slice's first tile
   uint32_t slot;          // the caller's tensor index of this slice
-  uint64_t pad1;
+  uint64_t seg_base;      // output index of word 0 of the tensor holding the slice
 };
 static_assert(sizeof(TensorDesc) == 64, "TensorDesc layout");
 
@@ -90,14 +90,15 @@ __host__ __device__ inline uint64_t groups_for(uint64_t tiles) {
 //   map         uint32 [tiles]       tile -> slice row (tensor lists)
 //   table       TensorDesc [tensors]
 //   coded output only (see CodedOut):
-//   tile_code   uint32 [tiles][4]    code bytes of the gaps inside the tile, per wavefront
-//   tile_fl     int64 [tiles][2]     first and last kept index of the tile
+//   tile_rec    uint64 [tiles]       kept words, code bytes of the gaps between them,
+//                                    offsets of the first and last (coded stage record)
 //   group_bexcl uint64 [groups]      code bytes before each group
 //   group_prev  int64 [groups]       index the group's first entry is coded against
+//   group_first_local int64 [groups] tensor-local index of the group's first entry
 //   stage       uint32 [tiles * cap] per-tile staging slots
 struct WorkspaceLayout {
-  size_t counts, group_sum, group_excl, map, table, tile_code, tile_fl, group_bexcl, group_prev,
-      stage, fixed;
+  size_t counts, group_sum, group_excl, map, table, tile_rec, group_bexcl, group_prev,
+      group_first_local, stage, fixed;
 };
 
 inline WorkspaceLayout workspace_layout(uint64_t tiles, uint64_t tensors, bool coded = false) {
@@ -108,11 +109,11 @@ inline WorkspaceLayout workspace_layout(uint64_t tiles, uint64_t tensors, bool c
   w.group_excl = align_up(w.group_sum + 8 * groups);
   w.map = align_up(w.group_excl + 8 * groups);
   w.table = align_up(w.map + 4 * tiles);
-  w.tile_code = align_up(w.table + sizeof(TensorDesc) * tensors);
-  w.tile_fl = align_up(w.tile_code + (coded ? 16 * tiles : 0));
-  w.group_bexcl = align_up(w.tile_fl + (coded ? 16 * tiles : 0));
+  w.tile_rec = align_up(w.table + sizeof(TensorDesc) * tensors);
+  w.group_bexcl = align_up(w.tile_rec + (coded ? 8 * tiles : 0));
   w.group_prev = align_up(w.group_bexcl + (coded ? 8 * groups : 0));
-  w.stage = align_up(w.group_prev + (coded ? 8 * groups : 0));
+  w.group_first_local = align_up(w.group_prev + (coded ? 8 * groups : 0));
+  w.stage = align_up(w.group_first_local + (coded ? 8 * groups : 0));
   w.fixed = w.stage;
   return w;
 }
@@ -170,16 +171,20 @@ struct ExtractArgs {
   uint64_t* group_excl;
   uint32_t* stage;
   // Coded output (launch_extract_coded): no indices; the kept positions
-  // leave as one gap + LEB128 segment whose first entry is coded against
-  // code_base.  Per-tile and per-group tables as in WorkspaceLayout.
-  uint32_t* tile_code;
-  int64_t* tile_fl;
+  // leave gap + LEB128 coded, as one segment whose first entry is coded
+  // against code_base, or (seg_per_tensor) as one segment per tensor whose
+  // first entry is coded as its tensor-local index.  Per-tile and per-group
+  // tables as in WorkspaceLayout.
+  uint64_t* tile_rec;
   uint64_t* group_bexcl;
   int64_t* group_prev;
   uint8_t* code_out;
   uint64_t code_capacity;
   uint64_t* d_nbytes;
   int64_t code_base;
+  uint32_t seg_per_tensor;
+  int64_t* group_first_local;
+  uint64_t* d_tensor_byte_offsets;   // nullable (seg_per_tensor): first code byte of each tensor
 };
 
 hipError_t launch_reset(uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets,
@@ -220,23 +225,30 @@ hipError_t launch_apply_multi(const uint64_t* bases, uint16_t* const* ptrs, uint
                               uint32_t* err, hipStream_t stream);
 
 // One slice of a tensor list for enqueue_extract: `n` words of both copies
-// whose word 0 has output index `base`; `tensor` is the caller's index.
+// whose word 0 has output index `base`; `tensor` is the caller's index and
+// `seg_base` the output index of that tensor's word 0.
 struct SliceIn {
   const uint16_t* prev;
   const uint16_t* next;
   uint64_t n;
   uint64_t base;
   uint32_t tensor;
+  uint64_t seg_base;
 };
 
-// Coded output of enqueue_extract: the positions as one gap + LEB128
-// segment (first entry relative to `base`) of at most `capacity` bytes at
-// `out`, its length in *d_nbytes; no index stream.
+// Coded output of enqueue_extract: the positions gap + LEB128 coded, at
+// most `capacity` bytes at `out`, the length in *d_nbytes; no index stream.
+// One segment whose first entry is coded relative to `base`, or
+// (per_tensor) one segment per tensor, each tensor's first entry coded as
+// its tensor-local index; then d_offsets (entries) and d_byte_offsets
+// (bytes, nullable) get num_tensors + 1 entries.
 struct CodedOut {
   uint8_t* out;
   uint64_t capacity;
   uint64_t* d_nbytes;
   int64_t base;
+  bool per_tensor;
+  uint64_t* d_byte_offsets;
 };
 
 // Builds the slice table in `workspace`, then enqueues the extract kernels

@@ -221,10 +221,24 @@ __device__ __forceinline__ void scan_tile(const TensorDesc& d, uint64_t tile, ui
 
 static_assert(kLdsStage >= kElemsPerTile, "the LDS staging area holds a whole tile");
 
+// Record a coded tile leaves in place of its count, in one 8-byte store:
+// kept words (bits 0-13), code bytes of the gaps between consecutive kept
+// words (14-27; each gap is below 8192, so one or two bytes), and the tile
+// offsets of the first (28-40) and last (41-53) kept word.
+static_assert(kElemsPerTile <= 8192, "tile record field widths");
+__device__ __forceinline__ uint64_t tile_record(uint32_t count, uint32_t inner, uint32_t first,
+                                                uint32_t last) {
+  return (uint64_t)count | ((uint64_t)inner << 14) | ((uint64_t)first << 28) |
+         ((uint64_t)last << 41);
+}
+__device__ __forceinline__ uint32_t rec_count(uint64_t r) { return (uint32_t)(r & 0x3FFFu); }
+__device__ __forceinline__ uint32_t rec_inner(uint64_t r) { return (uint32_t)((r >> 14) & 0x3FFFu); }
+__device__ __forceinline__ uint32_t rec_first(uint64_t r) { return (uint32_t)((r >> 28) & 0x1FFFu); }
+__device__ __forceinline__ uint32_t rec_last(uint64_t r) { return (uint32_t)((r >> 41) & 0x1FFFu); }
+
 // kCoded (the coded output of launch_extract_coded): the LDS area holds
-// every entry of the tile, and the tile also leaves the code bytes of the
-// gaps between its consecutive entries (each below 8192: one or two bytes),
-// one sum per wavefront, and its first and last kept index.
+// every entry of the tile, and the tile leaves its record (above) instead
+// of its count; wavefront 0 sums the gaps' code bytes.
 template <bool kMulti, bool kVec, bool kCoded>
 __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
   __shared__ uint32_t s_wave_total[kWaves];
@@ -260,20 +274,23 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
   for (uint32_t r = threadIdx.x; r < keep; r += kThreads)
     __builtin_nontemporal_store(s_stage[r], slot + r);
   if (kCoded) {
-    uint64_t bytes = 0;
-    for (uint32_t r = threadIdx.x + 1; r < s.tile_total; r += kThreads) {
-      const uint32_t gap = (s_stage[r] & 0xFFFFu) - (s_stage[r - 1] & 0xFFFFu);
-      bytes += gap < 128u ? 1u : 2u;
+    if (wave == 0) {
+      uint32_t bytes = 0;
+      for (uint32_t r = lane + 1; r < s.tile_total; r += 64) {
+        const uint32_t gap = (s_stage[r] & 0xFFFFu) - (s_stage[r - 1] & 0xFFFFu);
+        bytes += gap < 128u ? 1u : 2u;
+      }
+#pragma unroll
+      for (int sh = 32; sh >= 1; sh >>= 1) bytes += __shfl_xor(bytes, sh);
+      if (lane == 0) {
+        const uint32_t n = s.tile_total;
+        a.tile_rec[tile] = tile_record(n, bytes, n ? (s_stage[0] & 0xFFFFu) : 0u,
+                                       n ? (s_stage[n - 1] & 0xFFFFu) : 0u);
+      }
     }
-    bytes = wave_sum64(bytes);
-    if (lane == 0) a.tile_code[4 * tile + wave] = (uint32_t)bytes;
-    if (threadIdx.x == 0 && s.tile_total) {
-      const int64_t ob = tile_out_base(d, tile);
-      a.tile_fl[2 * tile] = ob + (int64_t)(s_stage[0] & 0xFFFFu);
-      a.tile_fl[2 * tile + 1] = ob + (int64_t)(s_stage[s.tile_total - 1] & 0xFFFFu);
-    }
+  } else if (threadIdx.x == 0) {
+    a.counts[tile] = s.tile_total;
   }
-  if (threadIdx.x == 0) a.counts[tile] = s.tile_total;
 }
 
 // ----------------------------------------------------------------- scan
@@ -531,13 +548,19 @@ __device__ __forceinline__ uint32_t leb_bytes(uint64_t v) {
   return (bits + 6) / 7;
 }
 
-__device__ __forceinline__ int64_t wave_max_incl(int64_t x, uint32_t lane) {
-#pragma unroll
-  for (int s = 1; s < 64; s <<= 1) {
-    const int64_t y = __shfl_up(x, s);
-    if ((int)lane >= s) x = y > x ? y : x;
-  }
-  return x;
+// Last kept index of the nearest lower lane that kept anything (-1: none)
+// and of the highest such lane, where `last` is -1 for lanes that kept
+// nothing.  Kept indices grow with the lane, so these are the exclusive and
+// the total maximum of `last` over the wavefront: one ballot and one
+// shuffle instead of a scan.
+__device__ __forceinline__ void lower_last(int64_t last, uint32_t lane, int64_t& before,
+                                           int64_t& top) {
+  const uint64_t nz = __ballot(last >= 0);
+  const uint64_t below = nz & ((1ull << lane) - 1ull);
+  const int src = below ? 63 - __builtin_clzll(below) : (int)lane;
+  const int64_t b = __shfl(last, src);
+  before = below ? b : -1;
+  top = nz ? __shfl(last, 63 - __builtin_clzll(nz)) : -1;
 }
 
 template <typename T>
@@ -550,103 +573,215 @@ __device__ __forceinline__ T wave_incl_sum(T x, uint32_t lane) {
   return x;
 }
 
+// Index a tile's first entry is coded against, given the last kept index
+// before it (-1: none): with one segment per tensor, never below the
+// tensor's word 0, so that a tensor's first entry is coded as its
+// tensor-local index.
+__device__ __forceinline__ int64_t coded_pred(const ExtractArgs& a, int64_t before,
+                                              int64_t seg_base) {
+  return (a.seg_per_tensor && seg_base > before) ? seg_base : before;
+}
+
+// Descriptor of `tile`'s slice (tile ids differ per lane).
+__device__ __forceinline__ TensorDesc any_desc(const ExtractArgs& a, uint64_t tile) {
+  return a.table ? a.table[a.tile_map[tile]] : a.inl[inline_row(a, tile)];
+}
+
 // Per group of kTilesPerGroup tiles (one wavefront each): its entries, the
 // code bytes of every entry whose predecessor lies in the group, its last
 // (largest) index and the first index of its first tile that kept
 // anything; that first entry's code length is settled by the scan, once
-// the group's predecessor index is known.  Written into the tables the
-// scan then overwrites in place: group_sum = entries | bytes << 32,
-// group_prev = last index, group_bexcl = first index (-1: none kept).
+// the group's predecessor index is known (with one segment per tensor, the
+// group's first entry is never coded against less than its tensor-local
+// index, kept in group_first_local).  Written into the tables the scan
+// then overwrites in place: group_sum = entries | bytes << 32, group_prev =
+// last index, group_bexcl = first index (-1: none kept).
 __global__ __launch_bounds__(64) void coded_group_kernel(ExtractArgs a) {
   const uint32_t lane = lane_id();
   const uint64_t g = blockIdx.x;
   const uint64_t t = g * kTilesPerGroup + lane;
   const bool in = t < a.num_tiles;
-  const uint32_t c = in ? a.counts[t] : 0u;
-  const u32x4 code = in ? *reinterpret_cast<const u32x4*>(a.tile_code + 4 * t) : u32x4{0, 0, 0, 0};
-  const int64_t f = in ? a.tile_fl[2 * t] : 0;
-  const int64_t l = in ? a.tile_fl[2 * t + 1] : 0;
-  const int64_t incl = wave_max_incl(c ? l : -1, lane);
-  int64_t before = __shfl_up(incl, 1);
-  if (lane == 0) before = -1;
-  const uint64_t inner = (uint64_t)code[0] + code[1] + code[2] + code[3];
-  const uint64_t own = c ? inner + (before >= 0 ? leb_bytes((uint64_t)(f - before)) : 0u) : 0u;
+  const uint64_t rec = in ? a.tile_rec[t] : 0;
+  const uint32_t c = rec_count(rec);
+  int64_t f = 0, l = 0, seg_base = -1;
+  if (c) {
+    const TensorDesc d = any_desc(a, t);
+    const int64_t ob = tile_out_base(d, t);
+    f = ob + (int64_t)rec_first(rec);
+    l = ob + (int64_t)rec_last(rec);
+    if (a.seg_per_tensor) seg_base = (int64_t)d.seg_base;
+  }
+  int64_t before, last;
+  lower_last(c ? l : -1, lane, before, last);
+  const uint64_t inner = rec_inner(rec);
+  const uint64_t own =
+      c ? inner + (before >= 0 ? leb_bytes((uint64_t)(f - coded_pred(a, before, seg_base))) : 0u)
+        : 0u;
   const uint64_t nz = __ballot(c != 0);
-  const int64_t first = nz ? __shfl(f, (int)__builtin_ctzll(nz)) : -1;
+  const int first_lane = nz ? (int)__builtin_ctzll(nz) : 0;
+  const int64_t first = nz ? __shfl(f, first_lane) : -1;
+  const int64_t first_local = nz ? __shfl(f - seg_base, first_lane) : 0;
   const uint64_t cnt = wave_sum64(c);
   const uint64_t bytes = wave_sum64(own);
-  const int64_t last = __shfl(incl, 63);
   if (lane == 0) {
     a.group_sum[g] = cnt | (bytes << 32);
     a.group_prev[g] = last;
     a.group_bexcl[g] = (uint64_t)first;
+    if (a.seg_per_tensor) a.group_first_local[g] = first_local;
   }
 }
 
-// One workgroup: per group, the entries and code bytes before it and the
-// index its first entry is coded against; the totals.  Groups are taken
-// kScanThreads at a time, one per thread, with carries between rounds; a
-// thread reads its group's sums before it overwrites them.
+// Code length of a group's (or tile's) first entry, given the index it
+// follows: the gap from it, or (one segment per tensor) the tensor-local
+// index if that is smaller.
+__device__ __forceinline__ uint32_t first_entry_bytes(const ExtractArgs& a, int64_t first,
+                                                      int64_t prev, int64_t local) {
+  int64_t gap = first - prev;
+  if (a.seg_per_tensor && local < gap) gap = local;
+  return leb_bytes((uint64_t)gap);
+}
+
+// One block of 64 groups of the coded scan, one per lane.
+struct CodedBlock {
+  uint64_t packed;   // entries | code bytes of every entry but the first << 32
+  int64_t last;      // last kept index (-1: none)
+  int64_t first;     // first kept index (-1: none)
+  int64_t local;     // its tensor-local index (one segment per tensor)
+};
+
+__device__ __forceinline__ CodedBlock load_coded_block(const ExtractArgs& a, uint64_t gi,
+                                                       bool in) {
+  CodedBlock b;
+  b.packed = in ? a.group_sum[gi] : 0;
+  b.last = in ? a.group_prev[gi] : -1;
+  b.first = in ? (int64_t)a.group_bexcl[gi] : -1;
+  b.local = (in && a.seg_per_tensor) ? a.group_first_local[gi] : 0;
+  return b;
+}
+
+// One workgroup of kScanWaves wavefronts: per group, the entries and code
+// bytes before it and the index its first entry is coded against (the
+// largest kept index of the groups before it, at least code_base); the
+// totals.  Wavefront w owns a contiguous range of groups, in blocks of 64
+// (one per lane, kScanBatch blocks loaded at a time).  Inside a range, a
+// group's predecessor index lies in the range once any earlier group of
+// the range kept something, so only the range's first nonempty group
+// depends on the ranges before it.  Pass 1: each wavefront sums its
+// range's entries and code bytes, leaving out that one group's first
+// entry, and takes the range's largest index.  The ranges are then
+// chained (sixteen steps, in every thread), which settles each range's
+// deferred entry.  Pass 2: each wavefront walks its range again with its
+// carries and writes every group's offsets (a thread reads its group's
+// sums before it overwrites them, and pass 1 has read everything before
+// the barrier).
 __global__ __launch_bounds__(kScanThreads) void coded_scan_kernel(ExtractArgs a) {
-  __shared__ int64_t s_wmax[kScanWaves];
-  __shared__ uint64_t s_wcnt[kScanWaves];
-  __shared__ uint64_t s_wbytes[kScanWaves];
+  __shared__ uint64_t s_cnt[kScanWaves], s_bytes[kScanWaves];
+  __shared__ int64_t s_max[kScanWaves], s_dfirst[kScanWaves], s_dlocal[kScanWaves];
   const uint32_t lane = lane_id();
   const uint32_t wave = threadIdx.x >> 6;
   const uint64_t groups = groups_for(a.num_tiles);
-  uint64_t carry_cnt = 0, carry_bytes = 0;
-  int64_t carry_prev = a.code_base;
-  for (uint64_t r0 = 0; r0 < groups; r0 += kScanThreads) {
-    const uint64_t gi = r0 + threadIdx.x;
-    const bool in = gi < groups;
-    const uint64_t packed = in ? a.group_sum[gi] : 0;
-    const int64_t last = in ? a.group_prev[gi] : -1;
-    const int64_t first = in ? (int64_t)a.group_bexcl[gi] : -1;
-    const uint64_t cnt = packed & 0xFFFFFFFFull;
-    const int64_t incl = wave_max_incl(last, lane);
-    if (lane == 63) s_wmax[wave] = incl;
-    __syncthreads();
-    int64_t prev = carry_prev;
-    for (uint32_t w = 0; w < wave; ++w) prev = s_wmax[w] > prev ? s_wmax[w] : prev;
-    const int64_t below = __shfl_up(incl, 1);
-    if (lane > 0 && below > prev) prev = below;
-    const uint64_t bytes =
-        (packed >> 32) + (first >= 0 ? leb_bytes((uint64_t)(first - prev)) : 0u);
-    const uint64_t xc = wave_incl_sum(cnt, lane);
-    const uint64_t xb = wave_incl_sum(bytes, lane);
-    if (lane == 63) {
-      s_wcnt[wave] = xc;
-      s_wbytes[wave] = xb;
+  const uint64_t blocks = (groups + 63) / 64;
+  const uint64_t per = (blocks + kScanWaves - 1) / kScanWaves;   // blocks per wavefront
+  const uint64_t b0 = (uint64_t)wave * per;
+  const uint64_t b1 = b0 + per < blocks ? b0 + per : blocks;
+  // pass 1
+  uint64_t cnt = 0, bytes = 0;
+  int64_t run_max = -1, dfirst = -1, dlocal = 0;
+  for (uint64_t b = b0; b < b1; b += kScanBatch) {
+    CodedBlock v[kScanBatch];
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) {
+      const uint64_t gi = (b + k) * 64 + lane;
+      v[k] = load_coded_block(a, gi, b + k < b1 && gi < groups);
     }
-    __syncthreads();
-    uint64_t oc = carry_cnt, ob = carry_bytes;
-    for (uint32_t w = 0; w < wave; ++w) {
-      oc += s_wcnt[w];
-      ob += s_wbytes[w];
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) {
+      int64_t before, bmax;
+      lower_last(v[k].last, lane, before, bmax);
+      const int64_t pred = before > run_max ? before : run_max;
+      uint64_t own = v[k].packed >> 32;
+      if (v[k].first >= 0 && pred >= 0) own += first_entry_bytes(a, v[k].first, pred, v[k].local);
+      // the range's first nonempty group: at most one lane of one block
+      const uint64_t defer = __ballot(v[k].first >= 0 && pred < 0);
+      if (defer) {
+        const int l = (int)__builtin_ctzll(defer);
+        dfirst = __shfl(v[k].first, l);
+        dlocal = __shfl(v[k].local, l);
+      }
+      cnt += v[k].packed & 0xFFFFFFFFull;
+      bytes += own;
+      run_max = bmax > run_max ? bmax : run_max;
     }
-    if (in) {
-      a.group_excl[gi] = oc + xc - cnt;
-      a.group_bexcl[gi] = ob + xb - bytes;
-      a.group_prev[gi] = prev;
+  }
+  cnt = wave_sum64(cnt);
+  bytes = wave_sum64(bytes);
+  if (lane == 0) {
+    s_cnt[wave] = cnt;
+    s_bytes[wave] = bytes;
+    s_max[wave] = run_max;
+    s_dfirst[wave] = dfirst;
+    s_dlocal[wave] = dlocal;
+  }
+  __syncthreads();
+  // chain the ranges
+  uint64_t carry_cnt = 0, carry_bytes = 0, total_cnt = 0, total_bytes = 0;
+  int64_t carry_prev = a.code_base, prev = a.code_base;
+  for (uint32_t w = 0; w < (uint32_t)kScanWaves; ++w) {
+    if (w == wave) {
+      carry_cnt = total_cnt;
+      carry_bytes = total_bytes;
+      carry_prev = prev;
     }
-    for (int w = 0; w < kScanWaves; ++w) {
-      carry_cnt += s_wcnt[w];
-      carry_bytes += s_wbytes[w];
-      carry_prev = s_wmax[w] > carry_prev ? s_wmax[w] : carry_prev;
+    uint64_t rb = s_bytes[w];
+    if (s_dfirst[w] >= 0) rb += first_entry_bytes(a, s_dfirst[w], prev, s_dlocal[w]);
+    total_cnt += s_cnt[w];
+    total_bytes += rb;
+    prev = s_max[w] > prev ? s_max[w] : prev;
+  }
+  // pass 2
+  for (uint64_t b = b0; b < b1; b += kScanBatch) {
+    CodedBlock v[kScanBatch];
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) {
+      const uint64_t gi = (b + k) * 64 + lane;
+      v[k] = load_coded_block(a, gi, b + k < b1 && gi < groups);
     }
-    __syncthreads();   // the LDS sums are rewritten by the next round
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) {
+      int64_t before, bmax;
+      lower_last(v[k].last, lane, before, bmax);
+      const int64_t pred = before > carry_prev ? before : carry_prev;
+      // a group holds at most 2^19 entries of at most 2 code bytes each
+      // (plus one longer number), so a block's sums fit 32 bits
+      const uint32_t c = (uint32_t)(v[k].packed & 0xFFFFFFFFull);
+      const uint32_t own = (uint32_t)(v[k].packed >> 32) +
+                           (v[k].first >= 0 ? first_entry_bytes(a, v[k].first, pred, v[k].local)
+                                            : 0u);
+      const uint32_t xc = wave_incl_sum(c, lane);
+      const uint32_t xb = wave_incl_sum(own, lane);
+      const uint64_t gi = (b + k) * 64 + lane;
+      if (b + k < b1 && gi < groups) {
+        a.group_excl[gi] = carry_cnt + xc - c;
+        a.group_bexcl[gi] = carry_bytes + xb - own;
+        a.group_prev[gi] = pred;
+      }
+      carry_cnt += __shfl(xc, 63);
+      carry_bytes += __shfl(xb, 63);
+      carry_prev = bmax > carry_prev ? bmax : carry_prev;
+    }
   }
   if (threadIdx.x == 0) {
-    *a.d_count = carry_cnt;
-    *a.d_nbytes = carry_bytes;
+    *a.d_count = total_cnt;
+    *a.d_nbytes = total_bytes;
   }
 }
 
 // A group's entries are coded in windows of kCodeWin consecutive entries,
-// eight per thread.  A window's code is at most two bytes per entry plus
+// kCodePer per thread.  A window's code is at most two bytes per entry plus
 // the longer codes of at most one first entry per tile (an index gap of
 // up to 2^63 takes 9 bytes).
-constexpr int kCodeWin = kThreads * 8;
+constexpr int kCodePer = 8;
+constexpr int kCodeWin = kThreads * kCodePer;
 constexpr int kCodeWinBytes = 2 * kCodeWin + kTilesPerGroup * 8;
 
 struct CodedGroup {
@@ -676,44 +811,50 @@ __device__ __forceinline__ void flush_code(const uint8_t* src, uint32_t n, uint8
   for (uint32_t i = h + 4 * words + threadIdx.x; i < n; i += kThreads) dst[i] = src[i];
 }
 
+// Walks the kCodePer consecutive window entries of this thread, from
+// window entry j0 on, calling f(k, gap) for each entry inside the window:
+// a tile's first entry is coded against the tile's predecessor index, any
+// other entry against the entry before it.
+template <typename F>
+__device__ __forceinline__ void walk_gaps(const CodedGroup& sg, uint32_t e_lo, uint32_t n,
+                                          uint32_t j0, F f) {
+  uint32_t lo = 0, hi = kTilesPerGroup;   // begin[lo] <= e_lo + j0 < begin[hi]
+#pragma unroll
+  for (int step = 0; step < 6; ++step) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (sg.begin[mid] <= e_lo + j0) lo = mid; else hi = mid;
+  }
+  uint32_t ti = lo;
+  uint32_t prev_off = j0 > 0 ? (sg.win[j0 - 1] & 0xFFFFu) : sg.last_off;
+#pragma unroll
+  for (int k = 0; k < kCodePer; ++k) {
+    const uint32_t j = j0 + k;
+    if (j < n) {
+      const uint32_t e = e_lo + j;
+      while (e >= sg.begin[ti + 1]) ++ti;
+      const uint32_t off = sg.win[j] & 0xFFFFu;
+      f(k, e == sg.begin[ti] ? (uint64_t)(sg.out_base[ti] + (int64_t)off - sg.prev[ti])
+                             : (uint64_t)(off - prev_off));
+      prev_off = off;
+    }
+  }
+}
+
 // Codes the window of n entries that starts at group entry e_lo (entries in
 // sg.win): values to out_val, code bytes after the `written` bytes the
-// group has already put out.  Returns the window's code bytes.
+// group has already put out.  Returns the window's code bytes.  The gaps
+// are walked twice (lengths, then bytes) rather than held in registers.
 __device__ __forceinline__ uint32_t code_window(const ExtractArgs& a, CodedGroup& sg,
                                                 uint32_t e_lo, uint32_t n, uint64_t eg,
                                                 uint64_t bg, uint64_t written) {
   const uint32_t lane = lane_id();
   const uint32_t wave = threadIdx.x >> 6;
-  const uint32_t j0 = 8 * threadIdx.x;
-  uint64_t gap[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  uint32_t len[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const uint32_t j0 = kCodePer * threadIdx.x;
   uint32_t sum = 0;
-  if (j0 < n) {
-    uint32_t lo = 0, hi = kTilesPerGroup;   // begin[lo] <= e_lo + j0 < begin[hi]
-#pragma unroll
-    for (int step = 0; step < 6; ++step) {
-      const uint32_t mid = (lo + hi) >> 1;
-      if (sg.begin[mid] <= e_lo + j0) lo = mid; else hi = mid;
-    }
-    uint32_t ti = lo;
-    uint32_t prev_off = j0 > 0 ? (sg.win[j0 - 1] & 0xFFFFu) : sg.last_off;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const uint32_t j = j0 + k;
-      if (j < n) {
-        const uint32_t e = e_lo + j;
-        while (e >= sg.begin[ti + 1]) ++ti;
-        const uint32_t v = sg.win[j];
-        const uint32_t off = v & 0xFFFFu;
-        gap[k] = e == sg.begin[ti] ? (uint64_t)(sg.out_base[ti] + (int64_t)off - sg.prev[ti])
-                                   : (uint64_t)(off - prev_off);
-        prev_off = off;
-        len[k] = leb_bytes(gap[k]);
-        sum += len[k];
-        if (eg + e < a.capacity) a.out_val[eg + e] = (uint16_t)(v >> 16);
-      }
-    }
-  }
+  if (j0 < n) walk_gaps(sg, e_lo, n, j0, [&](int, uint64_t gap) { sum += leb_bytes(gap); });
+  // the window's words, one entry per thread in turn (coalesced stores)
+  for (uint32_t j = threadIdx.x; j < n; j += kThreads)
+    if (eg + e_lo + j < a.capacity) a.out_val[eg + e_lo + j] = (uint16_t)(sg.win[j] >> 16);
   const uint32_t incl = wave_incl_sum(sum, lane);
   if (lane == 63) sg.wave_total[wave] = incl;
   __syncthreads();
@@ -723,13 +864,14 @@ __device__ __forceinline__ uint32_t code_window(const ExtractArgs& a, CodedGroup
     pos += (uint32_t)w < wave ? sg.wave_total[w] : 0u;
     nb += sg.wave_total[w];
   }
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    uint64_t v = gap[k];
-    for (uint32_t m = 0; m < len[k]; ++m) {
-      sg.code[pos++] = (uint8_t)((v & 0x7Fu) | (m + 1 < len[k] ? 0x80u : 0u));
-      v >>= 7;
-    }
+  if (j0 < n) {
+    walk_gaps(sg, e_lo, n, j0, [&](int, uint64_t gap) {
+      const uint32_t len = leb_bytes(gap);
+      for (uint32_t m = 0; m < len; ++m) {
+        sg.code[pos++] = (uint8_t)((gap & 0x7Fu) | (m + 1 < len ? 0x80u : 0u));
+        gap >>= 7;
+      }
+    });
   }
   __syncthreads();
   const uint64_t at = bg + written;
@@ -741,11 +883,13 @@ __device__ __forceinline__ uint32_t code_window(const ExtractArgs& a, CodedGroup
 }
 
 // One workgroup per group: the window entries come from the staging slots,
-// loaded kFinBatch per thread at a time.  A group with a tile that
+// loaded kCodePer per thread at a time.  A group with a tile that
 // overflowed its slot is coded tile by tile instead, that tile read again
-// and its entries placed into the window by rank.
+// and its entries placed into the window by rank.  The launch bound asks
+// for six wavefronts per SIMD (at most 80 registers): measured faster than
+// the five the unbounded allocation gives.
 template <bool kMulti, bool kVec>
-__global__ __launch_bounds__(kThreads) void finalize_coded_kernel(ExtractArgs a) {
+__global__ __launch_bounds__(kThreads, 6) void finalize_coded_kernel(ExtractArgs a) {
   __shared__ CodedGroup sg;
   __shared__ uint32_t s_wave_total[kWaves];
   const uint64_t g = blockIdx.x;
@@ -754,38 +898,69 @@ __global__ __launch_bounds__(kThreads) void finalize_coded_kernel(ExtractArgs a)
   const uint32_t n_here = left < (uint64_t)kTilesPerGroup ? (uint32_t)left : kTilesPerGroup;
   const uint32_t lane = lane_id();
   const uint32_t wave = threadIdx.x >> 6;
+  const uint64_t eg = a.group_excl[g];
+  const uint64_t bg = a.group_bexcl[g];
   if (wave == 0) {
     const uint64_t t = t0 + lane;
     const bool in = lane < n_here;
-    const uint32_t c = in ? a.counts[t] : 0u;
-    const int64_t l = in ? a.tile_fl[2 * t + 1] : 0;
-    const int64_t incl = wave_max_incl(c ? l : -1, lane);
-    int64_t before = __shfl_up(incl, 1);
+    const uint64_t rec = in ? a.tile_rec[t] : 0;
+    const uint32_t c = rec_count(rec);
+    TensorDesc d = {};
+    int64_t ob = 0;
+    if (in) {
+      d = lane_desc<kMulti>(a, t);
+      ob = tile_out_base(d, t);
+    }
+    int64_t before, top;
+    lower_last(c ? ob + (int64_t)rec_last(rec) : -1, lane, before, top);
     const int64_t gp = a.group_prev[g];
-    if (lane == 0 || before < gp) before = gp;
+    if (before < gp) before = gp;
     const uint32_t x = wave_incl_sum(c, lane);
+    const int64_t prev = in ? coded_pred(a, before, (int64_t)d.seg_base) : before;
     sg.begin[lane] = x - c;
     if (lane == 63) sg.begin[64] = x;
     sg.count[lane] = c;
-    sg.prev[lane] = before;
-    sg.out_base[lane] = in ? tile_out_base(lane_desc<kMulti>(a, t), t) : 0;
+    sg.prev[lane] = prev;
+    sg.out_base[lane] = ob;
     const uint64_t over = __ballot(c > a.stage_cap);
     if (lane == 0) {
       sg.overflow = over != 0;
       sg.last_off = 0;
     }
+    if (a.seg_per_tensor && (a.d_tensor_offsets || a.d_tensor_byte_offsets)) {
+      // Entry and byte offsets of each tensor's segment: the first tile of
+      // a slice owns the slots of its tensor and of the empty tensors just
+      // before it; the last tile owns the slots after its tensor.  A tile's
+      // code is its inner gaps plus its first entry's number.
+      const int64_t f = ob + (int64_t)rec_first(rec);
+      const uint64_t own = c ? rec_inner(rec) + leb_bytes((uint64_t)(f - prev)) : 0u;
+      const uint64_t bx = wave_incl_sum(own, lane) - own;
+      if (in) {
+        const uint64_t eo = eg + (x - c), bo = bg + bx;
+        if (t == d.first_tile) {
+          for (uint32_t s = d.off_lo; s <= d.slot; ++s) {
+            if (a.d_tensor_offsets) a.d_tensor_offsets[s] = eo;
+            if (a.d_tensor_byte_offsets) a.d_tensor_byte_offsets[s] = bo;
+          }
+        }
+        if (t == a.num_tiles - 1) {
+          for (uint32_t s = d.slot + 1; s <= a.num_tensors; ++s) {
+            if (a.d_tensor_offsets) a.d_tensor_offsets[s] = eo + c;
+            if (a.d_tensor_byte_offsets) a.d_tensor_byte_offsets[s] = bo + own;
+          }
+        }
+      }
+    }
   }
   __syncthreads();
-  const uint64_t eg = a.group_excl[g];
-  const uint64_t bg = a.group_bexcl[g];
   const uint32_t total = sg.begin[64];
   uint64_t written = 0;
   if (!sg.overflow) {
     for (uint32_t w0 = 0; w0 < total; w0 += kCodeWin) {
       const uint32_t n = total - w0 < (uint32_t)kCodeWin ? total - w0 : (uint32_t)kCodeWin;
-      uint32_t v[kFinBatch];
+      uint32_t v[kCodePer];
 #pragma unroll
-      for (int k = 0; k < kFinBatch; ++k) {
+      for (int k = 0; k < kCodePer; ++k) {
         const uint32_t j = threadIdx.x + kThreads * k;
         uint32_t lo = 0, hi = kTilesPerGroup;
 #pragma unroll
@@ -798,7 +973,7 @@ __global__ __launch_bounds__(kThreads) void finalize_coded_kernel(ExtractArgs a)
                      : 0u;
       }
 #pragma unroll
-      for (int k = 0; k < kFinBatch; ++k) {
+      for (int k = 0; k < kCodePer; ++k) {
         const uint32_t j = threadIdx.x + kThreads * k;
         if (j < n) sg.win[j] = v[k];
       }
@@ -821,12 +996,14 @@ __global__ __launch_bounds__(kThreads) void finalize_coded_kernel(ExtractArgs a)
       }
       continue;
     }
+    // an overflowed tile: read again for every window (a rare path; the
+    // tile's registers are not kept across the windows)
     const TensorDesc d = tile_desc<kMulti>(a, tile);
-    TileScan s;
-    scan_tile<kVec>(d, tile, lane, wave, s_wave_total, s);
     const uint32_t lane_word = (wave * kGroupsPerWave + lane) * 8;
     for (uint32_t r0 = 0; r0 < c; r0 += kCodeWin) {
       const uint32_t n = c - r0 < (uint32_t)kCodeWin ? c - r0 : (uint32_t)kCodeWin;
+      TileScan s;
+      scan_tile<kVec>(d, tile, lane, wave, s_wave_total, s);
 #pragma unroll
       for (int u = 0; u < kChunks; ++u) {
         uint32_t m = s.mask[u];
@@ -842,7 +1019,6 @@ __global__ __launch_bounds__(kThreads) void finalize_coded_kernel(ExtractArgs a)
       __syncthreads();
       written += code_window(a, sg, sg.begin[i] + r0, n, eg, bg, written);
     }
-    __syncthreads();   // s_wave_total is reused by the next overflowed tile
   }
 }
 

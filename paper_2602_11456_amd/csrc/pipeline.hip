@@ -43,7 +43,7 @@ void chunk_slices(const uint16_t* const* prevs, const uint16_t* const* nexts,
     const uint64_t a = lo > base ? lo : base;
     const uint64_t b = hi < base + n ? hi : base + n;
     if (a < b)
-      out.push_back({prevs[t] + (a - base), nexts[t] + (a - base), b - a, a, (uint32_t)t});
+      out.push_back({prevs[t] + (a - base), nexts[t] + (a - base), b - a, a, (uint32_t)t, base});
     base += n;
   }
 }
@@ -410,7 +410,7 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     // coded: the chunk's positions as one gap + LEB128 segment based at
     // its first word, written by the extract itself
     const CodedOut co = {(uint8_t*)(stage + L.bytes), bytes_cap, (uint64_t*)(stage + L.nbytes),
-                         (int64_t)lo};
+                         (int64_t)lo, false, nullptr};
     const StageSplit split = {staged[slot], cs};
     const delta_status_t st =
         enqueue_extract(sl.data(), sl.size(), 0, true, stage + L.idx, (uint16_t*)(stage + L.val),

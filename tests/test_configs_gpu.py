@@ -128,6 +128,31 @@ def leb128_full(ws, idx, val, offs, label):
         assert n == sb[t + 1] - sb[t], (label, t)
         np.testing.assert_array_equal(buf[sb[t]:sb[t + 1]].cpu().numpy(), ref)
     say(label, "leb128 ok:", buf.numel(), "bytes for", idx.numel(), "indices")
+    return buf, sb
+
+
+def coded_full(ws, idx, val, offs, label, buf, sb):
+    """The extract that writes the index stream LEB128 coded itself, over
+    the whole set: its entries and offsets equal extract_multi's, its code
+    decodes to extract_multi's indices, sampled tensors' segments equal the
+    oracle's bytes, and the stream equals the standalone encoder's."""
+    bases = np.concatenate([[0], np.cumsum(ws.numels)[:-1]]).astype(np.int64)
+    offs_h = offs.cpu().numpy()
+    code, cval, coffs, cb = ad.delta_extract_multi_leb128(ws.prev, ws.new)
+    assert torch.equal(coffs, offs), label
+    assert torch.equal(cval.view(torch.int16), val.view(torch.int16)), label
+    back = ad.delta_leb128_decode(code, offs_h, bases)
+    assert torch.equal(back, idx), label
+    del back
+    cb_h = cb.cpu().numpy()
+    for t in sample_tensors(ws.names, ws.shapes):
+        a, b = int(offs_h[t]), int(offs_h[t + 1])
+        ref, n = oracle.leb128_encode(idx[a:b].cpu().numpy() - bases[t])
+        assert n == cb_h[t + 1] - cb_h[t], (label, t)
+        np.testing.assert_array_equal(code[cb_h[t]:cb_h[t + 1]].cpu().numpy(), ref)
+    assert torch.equal(code, buf), label
+    np.testing.assert_array_equal(cb_h, sb)
+    say(label, "coded extract ok:", code.numel(), "bytes")
 
 
 @pytest.mark.parametrize("model,density", [("qwen3-4b", 0.01), ("qwen3-8b", 0.001),
@@ -141,7 +166,8 @@ def test_weight_set(model, density):
     torch.cuda.synchronize()
     check_set(ws, idx, val, offs, label)
     round_trip(ws, idx, val, label)
-    leb128_full(ws, idx, val, offs, label)
+    buf, sb = leb128_full(ws, idx, val, offs, label)
+    coded_full(ws, idx, val, offs, label, buf, sb)
 
 
 def test_qwen3_8b_clustered():
@@ -158,7 +184,9 @@ def test_qwen3_8b_clustered():
     tile_hist = torch.bincount(idx // 8192)
     assert int(tile_hist.max()) > 5 * 82
     round_trip(ws, idx, val, "qwen3-8b clustered")
-    leb128_full(ws, idx, val, offs, "qwen3-8b clustered")
+    buf, sb = leb128_full(ws, idx, val, offs, "qwen3-8b clustered")
+    coded_full(ws, idx, val, offs, "qwen3-8b clustered", buf, sb)
+    del buf
     artifact_full(ws, idx, val, offs, "qwen3-8b clustered")
 
 
