@@ -392,6 +392,58 @@ def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
     }
 
 
+def single_tensor_measurement(ad, synth, stream, reps):
+    """One 2048 x 2048 bf16 tensor with 1% of its words changed, int32
+    indices (delta_extract).  Its two copies (16.8 MB) fit in the 256 MB
+    last-level cache: "warm" repeats the call back to back; "cold" first
+    writes a 1 GiB scratch buffer, which evicts them.  HIP events on the
+    launch stream around each call; the scan kernel's own events beside."""
+    import torch
+    dev = torch.device("cuda")
+    n = 2048 * 2048
+    prev, new, pos = synth.make_pair(n, 0.01, seed=synth.config_seed(1), device=dev)
+    K = pos.numel()
+    idx = torch.empty(K + 64, dtype=torch.int32, device=dev)
+    val = torch.empty(K + 64, dtype=torch.bfloat16, device=dev)
+    cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+    ws = torch.empty(ad.delta_extract_workspace_bytes(n), dtype=torch.uint8, device=dev)
+    scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    lib = ad.library()
+
+    def call():
+        ad.delta_extract_into(prev, new, idx, val, cnt, ws, stream)
+
+    for _ in range(3):
+        call()
+    stream.synchronize()
+    if int(cnt.item()) != K:
+        raise RuntimeError("config 1: wrong count")
+    out = {}
+    for mode in ("warm", "cold"):
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+        for i, (e0, e1, s0, s1) in enumerate(ev):
+            if mode == "cold":
+                scratch.fill_(i & 0xFF)
+            s0.record(stream)
+            s1.record(stream)
+            if lib.delta_set_scan_events(s0.cuda_event, s1.cuda_event):
+                raise RuntimeError(lib.delta_last_error().decode())
+            e0.record(stream)
+            call()
+            e1.record(stream)
+        stream.synchronize()
+        lib.delta_set_scan_events(None, None)
+        med = lambda xs: sorted(xs)[len(xs) // 2]
+        call_ms = med([e0.elapsed_time(e1) for e0, e1, _, _ in ev])
+        scan_ms = med([s0.elapsed_time(s1) for _, _, s0, s1 in ev])
+        out[mode] = {"ms": round(call_ms, 4), "scan_kernel_ms": round(scan_ms, 4),
+                     "GBps_scanned": round(4 * n / (call_ms / 1e3) / 1e9, 1),
+                     "scan_kernel_GBps": round(4 * n / (scan_ms / 1e3) / 1e9, 1)}
+    del scratch
+    return {"workload": f"one 2048 x 2048 bf16 tensor, {K} changed words (1%), int32 indices",
+            **out}
+
+
 def hash_measurement(ad, buf, stream, reps):
     """XXH64 segment hashes (Sec. 5.2 integrity) of the extracted delta's
     bytes, timed with HIP events, for two segment sizes."""
@@ -480,6 +532,7 @@ def extras(args, ad, synth, ws, rollout, plan, out_idx, out_val, d_offs, work, s
     result["fused"] = fused_measurement(ad, synth, ws, args.model, out_idx, out_val, work, stream,
                                         args.steps)
     result["compose"] = compose_measurement(ad, rollout, N, K, stream, max(args.steps // 2, 3))
+    result["single_tensor"] = single_tensor_measurement(ad, synth, stream, max(args.steps, 20))
 
 
 def main():
