@@ -279,6 +279,8 @@ delta_status_t delta_extract(const uint16_t* prev, const uint16_t* next, uint64_
   if (capacity > 0 && (!out_idx || !out_val))
     return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val is NULL with capacity %llu",
                 (unsigned long long)capacity);
+  if ((uintptr_t)out_idx % (index_type == DELTA_INDEX_I64 ? 8 : 4) || odd(out_val))
+    return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val not aligned to their element size");
   if (index_type == DELTA_INDEX_I32 && numel > 0 && numel - 1 > 0x7FFFFFFFull)
     return fail(DELTA_ERR_INDEX_OVERFLOW, "numel %llu needs int64 indices",
                 (unsigned long long)numel);
@@ -297,6 +299,8 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
   if (capacity > 0 && (!out_idx || !out_val))
     return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val is NULL with capacity %llu",
                 (unsigned long long)capacity);
+  if ((uintptr_t)out_idx % 8 || odd(out_val))
+    return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val not aligned to their element size");
   std::vector<SliceIn> slices;
   const delta_status_t st = list_slices(prev_ptrs, next_ptrs, numels, num_tensors, slices);
   if (st != DELTA_OK) return st;
@@ -323,6 +327,7 @@ delta_status_t delta_extract_multi_leb128(const uint16_t* const* prev_ptrs,
   if (capacity > 0 && !out_val)
     return fail(DELTA_ERR_INVALID_ARG, "out_val is NULL with capacity %llu",
                 (unsigned long long)capacity);
+  if (odd(out_val)) return fail(DELTA_ERR_INVALID_ARG, "out_val not 2-byte aligned");
   if (code_capacity > 0 && !out_code)
     return fail(DELTA_ERR_INVALID_ARG, "out_code is NULL with code_capacity %llu",
                 (unsigned long long)code_capacity);
@@ -353,6 +358,8 @@ delta_status_t delta_extract_fused(const uint16_t* const* prev_ptrs,
   if (capacity > 0 && (!out_idx || !out_val))
     return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val is NULL with capacity %llu",
                 (unsigned long long)capacity);
+  if ((uintptr_t)out_idx % 8 || odd(out_val))
+    return fail(DELTA_ERR_INVALID_ARG, "out_idx/out_val not aligned to their element size");
   // global base of every target
   std::vector<uint64_t> tbase(num_targets + 1, 0);
   for (int32_t f = 0; f < num_targets; ++f) {

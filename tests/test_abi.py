@@ -106,6 +106,13 @@ def test_extract_validation(lib):
     # outputs missing with a nonzero capacity
     assert lib.delta_extract(FAKE, FAKE, 10, 0, None, FAKE, 10, cnt, ws, 1 << 20, None) == \
         _abi.DELTA_ERR_INVALID_ARG
+    # outputs not aligned to their element size
+    assert lib.delta_extract(FAKE, FAKE, 10, _abi.DELTA_INDEX_I32, FAKE + 2, FAKE, 10, cnt, ws,
+                             1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_extract(FAKE, FAKE, 10, _abi.DELTA_INDEX_I64, FAKE + 4, FAKE, 10, cnt, ws,
+                             1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_extract(FAKE, FAKE, 10, 0, FAKE, FAKE + 1, 10, cnt, ws, 1 << 20, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
 
 
 def test_extract_multi_validation(lib):
@@ -120,6 +127,40 @@ def test_extract_multi_validation(lib):
                                    1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
     assert lib.delta_extract_multi(prevs, prevs, numels, 2, FAKE, FAKE, 10, FAKE, None, FAKE,
                                    64, None) == _abi.DELTA_ERR_WORKSPACE
+    # int64 indices at a 4-byte boundary, words at an odd address
+    assert lib.delta_extract_multi(prevs, prevs, numels, 2, FAKE + 4, FAKE, 10, FAKE, None, FAKE,
+                                   1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_extract_multi(prevs, prevs, numels, 2, FAKE, FAKE + 1, 10, FAKE, None, FAKE,
+                                   1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
+
+
+def test_extract_multi_leb128_validation(lib):
+    P = ctypes.c_void_p
+    prevs = (P * 2)(FAKE, FAKE)
+    nexts = (P * 2)(FAKE, None)
+    numels = (ctypes.c_uint64 * 2)(10, 10)
+    need = lib.delta_extract_multi_leb128_workspace_bytes(numels, 2)
+    assert need >= lib.delta_extract_multi_workspace_bytes(numels, 2)
+    assert lib.delta_extract_multi_leb128_workspace_bytes(None, 2) == 0
+    assert lib.delta_extract_multi_leb128_workspace_bytes(numels, -1) == 0
+    args = dict(code=FAKE, ccap=100, nb=FAKE, val=FAKE, cap=10, cnt=FAKE, ws=FAKE, wsb=1 << 20)
+
+    def call(pp=prevs, qq=prevs, T=2, **kw):
+        a = dict(args, **kw)
+        return lib.delta_extract_multi_leb128(pp, qq, numels, T, a["code"], a["ccap"], a["nb"],
+                                              a["val"], a["cap"], a["cnt"], None, None, a["ws"],
+                                              a["wsb"], None)
+
+    assert call(qq=nexts) == _abi.DELTA_ERR_INVALID_ARG          # NULL tensor pointer
+    assert b"tensor 1" in lib.delta_last_error()
+    assert call(T=-1) == _abi.DELTA_ERR_INVALID_ARG
+    assert call(nb=None) == _abi.DELTA_ERR_INVALID_ARG            # d_nbytes
+    assert call(cnt=None) == _abi.DELTA_ERR_INVALID_ARG           # d_count
+    assert call(code=None) == _abi.DELTA_ERR_INVALID_ARG          # code output, capacity > 0
+    assert call(val=None) == _abi.DELTA_ERR_INVALID_ARG           # words output, capacity > 0
+    assert call(val=FAKE + 1) == _abi.DELTA_ERR_INVALID_ARG       # odd word output
+    assert call(wsb=64) == _abi.DELTA_ERR_WORKSPACE
+    assert call(ws=FAKE + 8) == _abi.DELTA_ERR_WORKSPACE
 
 
 def test_apply_validation(lib):
