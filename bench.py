@@ -330,7 +330,9 @@ def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
     """Sec. 5.4 catch-up over a chain of `chain` deltas, each ~1% of the
     Qwen3-8B index space at uniformly random positions (drawn on the GPU):
     delta_compose timed with HIP events, then one apply of the composed
-    delta against replaying the chain delta by delta."""
+    delta, against replaying the chain delta by delta and against applying
+    the chain in one pass (delta_apply_chain, checked first on a second
+    copy of the rollout to leave exactly what the composed delta leaves)."""
     import torch
     dev = rollout[0].device
     g = torch.Generator(device=dev)
@@ -364,8 +366,19 @@ def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
     k = int(cnt.item())
     apply_ws = torch.empty(max(ad.delta_apply_multi_workspace_bytes(len(rollout)), 1),
                            dtype=torch.uint8, device=dev)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
-    for e0, e1, e2, e3 in ev:
+    chain_ws = torch.empty(ad.delta_apply_chain_workspace_bytes(counts, len(rollout)),
+                           dtype=torch.uint8, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    second = [t.clone() for t in rollout]
+    ad.delta_apply_multi(rollout, out_i[:k], out_v[:k], workspace=apply_ws, stream=stream)
+    ad.delta_apply_chain(second, deltas, error_flag=flag, workspace=chain_ws, stream=stream)
+    stream.synchronize()
+    if int(flag.item()) or not all(torch.equal(a.view(torch.int16), b.view(torch.int16))
+                                   for a, b in zip(rollout, second)):
+        raise RuntimeError("the one-pass chain apply differs from applying the composed delta")
+    del second
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(reps)]
+    for e0, e1, e2, e3, e4 in ev:
         e0.record(stream)
         compose()
         e1.record(stream)
@@ -374,11 +387,14 @@ def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
         for idx, val in deltas:
             ad.delta_apply_multi(rollout, idx, val, workspace=apply_ws, stream=stream)
         e3.record(stream)
+        ad.delta_apply_chain(rollout, deltas, workspace=chain_ws, stream=stream)
+        e4.record(stream)
     stream.synchronize()
     med = lambda xs: sorted(xs)[len(xs) // 2]
-    tc = med([e0.elapsed_time(e1) for e0, e1, _, _ in ev])
-    ta = med([e1.elapsed_time(e2) for _, e1, e2, _ in ev])
-    tr = med([e2.elapsed_time(e3) for _, _, e2, e3 in ev])
+    tc = med([e[0].elapsed_time(e[1]) for e in ev])
+    ta = med([e[1].elapsed_time(e[2]) for e in ev])
+    tr = med([e[2].elapsed_time(e[3]) for e in ev])
+    tch = med([e[3].elapsed_time(e[4]) for e in ev])
     moved = (sum(counts) + k) * 10   # every input entry read once, the result written once
     return {
         "workload": f"{chain} deltas of ~1% random positions of the {N}-word index space "
@@ -389,6 +405,7 @@ def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
         "apply_composed_ms": round(ta, 4),
         "replay_chain_ms": round(tr, 4),
         "catch_up_compose_plus_apply_ms": round(tc + ta, 4),
+        "catch_up_one_pass_ms": round(tch, 4),
     }
 
 

@@ -389,6 +389,40 @@ delta_status_t delta_compose(const int64_t* const* idx_ptrs, const uint16_t* con
                              uint32_t* d_error_flag, void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
 
+/* Workspace bytes for delta_apply_chain of `num_deltas` deltas with these
+ * entry counts (host array) onto `num_tensors` tensors; 0 if the arguments
+ * are invalid. */
+size_t delta_apply_chain_workspace_bytes(const uint64_t* counts, int32_t num_deltas,
+                                         int32_t num_tensors);
+
+/*
+ * delta_apply_chain — Sec. 5.4 catch-up in one pass: brings the tensor list
+ * forward over the deltas D_1 .. D_K (oldest first) by writing every index
+ * of the chain once, with the word of the newest delta that holds it.  The
+ * result equals replaying the chain (delta_apply_multi of each delta in
+ * order) and applying delta_compose's output, without forming the composed
+ * delta.
+ *   weight_ptrs, numels, num_tensors  as delta_apply_multi (host arrays).
+ *   idx_ptrs, val_ptrs, counts  host arrays of num_deltas (0..16) entries:
+ *                 each delta's int64 global indices (strictly increasing, as
+ *                 delta_extract_multi writes them) and words, in device
+ *                 memory, and its entry count.
+ *   d_error_flag  device uint32 or NULL: set when an index falls outside
+ *                 the tensor list (that entry is skipped) or the input is
+ *                 found unsorted (the result is then unspecified, but no
+ *                 access leaves the given buffers).
+ *   workspace     delta_apply_chain_workspace_bytes(counts, num_deltas,
+ *                 num_tensors).
+ * Enqueues on `stream`.  The index space is cut into value ranges holding a
+ * fixed number of entries of the largest delta; deltas of very uneven
+ * density stay correct but slower.
+ */
+delta_status_t delta_apply_chain(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                 int32_t num_tensors, const int64_t* const* idx_ptrs,
+                                 const uint16_t* const* val_ptrs, const uint64_t* counts,
+                                 int32_t num_deltas, uint32_t* d_error_flag, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
+
 /*
  * Versioned delta checkpoints — Sec. 5.1: the trainer writes each step's
  * delta as an immutable, versioned file with an integrity hash; Sec. 5.2:

@@ -394,17 +394,65 @@ def delta_compose(deltas: Sequence[Tuple[torch.Tensor, torch.Tensor]],
     return out_idx[:k], out_val[:k]
 
 
+def delta_apply_chain_workspace_bytes(counts: Sequence[int], num_tensors: int) -> int:
+    return int(library().delta_apply_chain_workspace_bytes(_u64_array(counts), len(counts),
+                                                            int(num_tensors)))
+
+
+def delta_apply_chain(weights: Sequence[torch.Tensor],
+                      deltas: Sequence[Tuple[torch.Tensor, torch.Tensor]],
+                      error_flag: Optional[torch.Tensor] = None, check: bool = False,
+                      workspace: Optional[torch.Tensor] = None,
+                      stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Apply a chain of deltas (oldest first) in one pass: every index gets
+    the word of the newest delta holding it (Sec. 5.4 catch-up), as replay
+    would leave it.  At most 16 deltas per call."""
+    T = len(weights)
+    for i, (idx, val) in enumerate(deltas):
+        if idx.dtype != torch.int64 or not idx.is_contiguous():
+            raise TypeError(f"delta {i}: indices must be contiguous int64")
+        if idx.numel() != val.numel():
+            raise ValueError(f"delta {i}: idx and val differ in length")
+    ptrs = _ptr_array([_words(w, f"weights[{i}]") for i, w in enumerate(weights)])
+    numels = _u64_array([w.numel() for w in weights])
+    counts = [idx.numel() for idx, _ in deltas]
+    ip = _ptr_array([idx.data_ptr() for idx, _ in deltas])
+    vp = _ptr_array([_words(val, f"val[{i}]") for i, (_, val) in enumerate(deltas)])
+    dev = weights[0].device if T else (deltas[0][0].device if deltas else torch.device("cuda"))
+    need = delta_apply_chain_workspace_bytes(counts, T)
+    ws = workspace if workspace is not None else _workspace(need, dev)
+    flag = error_flag
+    if check and flag is None:
+        flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    _check(library().delta_apply_chain(
+        ptrs, numels, T, ip, vp, _u64_array(counts), len(deltas),
+        flag.data_ptr() if flag is not None else None, ws.data_ptr(),
+        ws.numel() * ws.element_size(), _stream(stream)))
+    if check:
+        (stream or torch.cuda.current_stream()).synchronize()
+        if int(flag.item()) != 0:
+            raise DeltaError(_abi.DELTA_ERR_OUT_OF_RANGE,
+                             "an index was outside the tensors or a delta was not sorted")
+
+
 def delta_catch_up(weights: Sequence[torch.Tensor],
-                   deltas: Sequence[Tuple[torch.Tensor, torch.Tensor]], compose: bool = True,
+                   deltas: Sequence[Tuple[torch.Tensor, torch.Tensor]], method: str = "chain",
                    stream: Optional[torch.cuda.Stream] = None) -> None:
     """Bring a rollout copy forward over a chain of missed deltas (Sec. 5.4):
-    either compose them and apply once, or replay them in order."""
-    if compose:
+    "chain" applies them in one pass (delta_apply_chain, up to 16 at a
+    time), "compose" composes them and applies once, "replay" applies them
+    in order."""
+    if method == "chain":
+        for c0 in range(0, len(deltas), 16):
+            delta_apply_chain(weights, deltas[c0:c0 + 16], check=True, stream=stream)
+    elif method == "compose":
         idx, val = delta_compose(deltas, stream=stream)
         delta_apply_multi(weights, idx, val, check=True, stream=stream)
-    else:
+    elif method == "replay":
         for idx, val in deltas:
             delta_apply_multi(weights, idx, val, check=True, stream=stream)
+    else:
+        raise ValueError(f"unknown catch-up method {method!r}")
 
 
 # ---------------------------------------------------------------- fused

@@ -91,6 +91,8 @@ SIGNATURES = {
                                           SZ, P]),
     "delta_compose_workspace_bytes": (SZ, [P, I32]),
     "delta_compose": (STATUS, [P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
+    "delta_apply_chain_workspace_bytes": (SZ, [P, I32, I32]),
+    "delta_apply_chain": (STATUS, [P, P, I32, P, P, P, I32, P, P, SZ, P]),
     "delta_artifact_layout": (STATUS, [U64, U64, U64, U64, ctypes.POINTER(delta_artifact_layout_t)]),
     "delta_hash_segments": (STATUS, [P, U64, U64, U64, P, P]),
     "delta_artifact_seal": (STATUS, [P, SZ, ctypes.POINTER(delta_artifact_header_t), P]),

@@ -430,17 +430,16 @@ delta_status_t delta_apply_checked(uint16_t* weights, uint64_t numel, delta_inde
   return delta_apply(weights, numel, index_type, idx, val, count, d_error_flag, stream);
 }
 
-delta_status_t delta_apply_multi(uint16_t* const* weight_ptrs, const uint64_t* numels,
-                                 int32_t num_tensors, const int64_t* idx, const uint16_t* val,
-                                 uint64_t count, uint32_t* d_error_flag, void* workspace,
-                                 size_t workspace_bytes, hipStream_t stream) {
+// Host table of a tensor list for the apply kernels: bases[t] = first
+// global index of tensor t (bases[T] = total) and the tensors' addresses.
+static delta_status_t weight_table(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                   int32_t num_tensors, std::vector<uint64_t>& bases,
+                                   std::vector<uint64_t>& ptrs) {
   if (num_tensors < 0) return fail(DELTA_ERR_INVALID_ARG, "num_tensors < 0");
   if (num_tensors > 0 && (!weight_ptrs || !numels))
     return fail(DELTA_ERR_INVALID_ARG, "tensor arrays are NULL");
-  if (count > 0 && (!idx || !val)) return fail(DELTA_ERR_INVALID_ARG, "idx/val is NULL");
-  if (odd(val) || ((uintptr_t)idx % 8)) return fail(DELTA_ERR_INVALID_ARG, "idx/val misaligned");
-  std::vector<uint64_t> bases(num_tensors + 1);
-  std::vector<uint64_t> ptrs(num_tensors);
+  bases.assign(num_tensors + 1, 0);
+  ptrs.assign(num_tensors, 0);
   uint64_t base = 0;
   for (int32_t t = 0; t < num_tensors; ++t) {
     if (numels[t] > 0 && !weight_ptrs[t])
@@ -452,20 +451,128 @@ delta_status_t delta_apply_multi(uint16_t* const* weight_ptrs, const uint64_t* n
     base += numels[t];
   }
   bases[num_tensors] = base;
+  return DELTA_OK;
+}
+
+// Uploads the table into the start of the workspace (the layout of
+// delta_apply_multi_workspace_bytes).
+static hipError_t upload_weight_table(const std::vector<uint64_t>& bases,
+                                      const std::vector<uint64_t>& ptrs, char* ws,
+                                      uint64_t*& d_bases, uint64_t*& d_ptrs, hipStream_t stream) {
+  d_bases = (uint64_t*)ws;
+  d_ptrs = (uint64_t*)(ws + align_up(8 * bases.size()));
+  hipError_t e = launch_upload_words(bases.data(), bases.size(), d_bases, stream);
+  if (e == hipSuccess && !ptrs.empty()) e = launch_upload_words(ptrs.data(), ptrs.size(), d_ptrs, stream);
+  return e;
+}
+
+delta_status_t delta_apply_multi(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                 int32_t num_tensors, const int64_t* idx, const uint16_t* val,
+                                 uint64_t count, uint32_t* d_error_flag, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  std::vector<uint64_t> bases, ptrs;
+  delta_status_t s = weight_table(weight_ptrs, numels, num_tensors, bases, ptrs);
+  if (s != DELTA_OK) return s;
+  if (count > 0 && (!idx || !val)) return fail(DELTA_ERR_INVALID_ARG, "idx/val is NULL");
+  if (odd(val) || ((uintptr_t)idx % 8)) return fail(DELTA_ERR_INVALID_ARG, "idx/val misaligned");
   const size_t need = delta_apply_multi_workspace_bytes(num_tensors);
-  delta_status_t s = check_workspace(workspace, workspace_bytes, need);
+  s = check_workspace(workspace, workspace_bytes, need);
   if (s != DELTA_OK) return s;
   if (count == 0) return ok();
-  char* ws = (char*)workspace;
-  uint64_t* d_bases = (uint64_t*)ws;
-  uint64_t* d_ptrs = (uint64_t*)(ws + align_up(8 * ((size_t)num_tensors + 1)));
-  hipError_t e = launch_upload_words(bases.data(), bases.size(), d_bases, stream);
-  if (e == hipSuccess && num_tensors > 0)
-    e = launch_upload_words(ptrs.data(), ptrs.size(), d_ptrs, stream);
+  uint64_t *d_bases, *d_ptrs;
+  hipError_t e = upload_weight_table(bases, ptrs, (char*)workspace, d_bases, d_ptrs, stream);
   if (e != hipSuccess) return hip_fail(e, "table upload launch");
   e = launch_apply_multi(d_bases, (uint16_t* const*)d_ptrs, (uint32_t)num_tensors, idx, val,
                          count, d_error_flag, stream);
   if (e != hipSuccess) return hip_fail(e, "apply_multi launch");
+  return ok();
+}
+
+// delta_apply_chain: tiles of `per_tile` entries of the largest delta, so
+// that a tile of deltas of similar density stages about kChainLds indices.
+struct ChainPlan {
+  uint32_t ref;
+  uint64_t per_tile, tiles;
+  size_t deltas, pos, total;   // workspace offsets after the weight table
+};
+
+static ChainPlan chain_plan(const uint64_t* counts, int32_t K, int32_t T) {
+  ChainPlan c;
+  c.ref = 0;
+  for (int32_t k = 1; k < K; ++k)
+    if (counts[k] > counts[c.ref]) c.ref = (uint32_t)k;
+  uint64_t s = ((uint64_t)kChainLds / (uint64_t)(K + 1)) / 16 * 16;
+  c.per_tile = s < 16 ? 16 : s;
+  const uint64_t n_ref = K > 0 ? counts[c.ref] : 0;
+  c.tiles = (n_ref + c.per_tile - 1) / c.per_tile;
+  c.deltas = delta_apply_multi_workspace_bytes(T);
+  c.pos = align_up(c.deltas + sizeof(ChainDelta) * (size_t)(K > 0 ? K : 1));
+  c.total = align_up(c.pos + 8 * (c.tiles + 1) * (uint64_t)(K > 0 ? K : 1));
+  return c;
+}
+
+size_t delta_apply_chain_workspace_bytes(const uint64_t* counts, int32_t num_deltas,
+                                         int32_t num_tensors) {
+  if (num_deltas < 0 || num_tensors < 0 || (num_deltas > 0 && !counts)) return 0;
+  return chain_plan(counts, num_deltas, num_tensors).total;
+}
+
+delta_status_t delta_apply_chain(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                 int32_t num_tensors, const int64_t* const* idx_ptrs,
+                                 const uint16_t* const* val_ptrs, const uint64_t* counts,
+                                 int32_t num_deltas, uint32_t* d_error_flag, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  std::vector<uint64_t> bases, ptrs;
+  delta_status_t s = weight_table(weight_ptrs, numels, num_tensors, bases, ptrs);
+  if (s != DELTA_OK) return s;
+  if (num_deltas < 0 || num_deltas > kChainMaxDeltas)
+    return fail(DELTA_ERR_INVALID_ARG, "%d deltas: 0 to %d per call (compose longer chains first)",
+                num_deltas, kChainMaxDeltas);
+  if (num_deltas > 0 && (!idx_ptrs || !val_ptrs || !counts))
+    return fail(DELTA_ERR_INVALID_ARG, "delta arrays are NULL");
+  std::vector<uint64_t> table;
+  uint64_t entries = 0;
+  for (int32_t k = 0; k < num_deltas; ++k) {
+    if (counts[k] > 0 && (!idx_ptrs[k] || !val_ptrs[k]))
+      return fail(DELTA_ERR_INVALID_ARG, "delta %d: NULL pointer", k);
+    if ((uintptr_t)idx_ptrs[k] % 8 || odd(val_ptrs[k]))
+      return fail(DELTA_ERR_INVALID_ARG, "delta %d: idx/val misaligned", k);
+    table.push_back((uint64_t)(uintptr_t)idx_ptrs[k]);
+    table.push_back((uint64_t)(uintptr_t)val_ptrs[k]);
+    table.push_back(counts[k]);
+    entries += counts[k];
+  }
+  const ChainPlan c = chain_plan(counts, num_deltas, num_tensors);
+  s = check_workspace(workspace, workspace_bytes, c.total);
+  if (s != DELTA_OK) return s;
+  if (entries == 0) return ok();
+  char* ws = (char*)workspace;
+  uint64_t *d_bases, *d_ptrs;
+  hipError_t e = upload_weight_table(bases, ptrs, ws, d_bases, d_ptrs, stream);
+  if (e != hipSuccess) return hip_fail(e, "table upload launch");
+  if (num_deltas == 1) {
+    e = launch_apply_multi(d_bases, (uint16_t* const*)d_ptrs, (uint32_t)num_tensors, idx_ptrs[0],
+                           val_ptrs[0], counts[0], d_error_flag, stream);
+    if (e != hipSuccess) return hip_fail(e, "apply_multi launch");
+    return ok();
+  }
+  if (c.tiles > 0xFFFFFFFFull) return fail(DELTA_ERR_INVALID_ARG, "too many entries");
+  e = launch_upload_words(table.data(), table.size(), (uint64_t*)(ws + c.deltas), stream);
+  if (e != hipSuccess) return hip_fail(e, "delta table upload launch");
+  ChainArgs a;
+  memset(&a, 0, sizeof(a));
+  a.deltas = (const ChainDelta*)(ws + c.deltas);
+  a.K = (uint32_t)num_deltas;
+  a.ref = c.ref;
+  a.per_tile = c.per_tile;
+  a.tiles = c.tiles;
+  a.pos = (uint64_t*)(ws + c.pos);
+  a.bases = d_bases;
+  a.ptrs = (uint16_t* const*)d_ptrs;
+  a.T = (uint32_t)num_tensors;
+  a.err = d_error_flag;
+  e = launch_apply_chain(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "apply_chain launch");
   return ok();
 }
 

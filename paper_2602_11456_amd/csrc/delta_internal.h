@@ -224,6 +224,31 @@ hipError_t launch_apply_multi(const uint64_t* bases, uint16_t* const* ptrs, uint
                               const int64_t* idx, const uint16_t* val, uint64_t count,
                               uint32_t* err, hipStream_t stream);
 
+// Catch-up in one pass (delta_apply_chain): the chain's deltas, oldest
+// first, in a device table; tiles of `per_tile` entries of the reference
+// (largest) delta; pos = (tiles + 1) x K split positions (workspace).
+constexpr int kChainMaxDeltas = 16;
+constexpr uint32_t kChainLds = 2048;   // indices a tile stages in LDS
+struct ChainDelta {
+  const int64_t* idx;
+  const uint16_t* val;
+  uint64_t n;
+};
+static_assert(sizeof(ChainDelta) == 24, "uploaded as three 64-bit words per delta");
+struct ChainArgs {
+  const ChainDelta* deltas;   // device [K]
+  uint32_t K;
+  uint32_t ref;
+  uint64_t per_tile;
+  uint64_t tiles;
+  uint64_t* pos;
+  const uint64_t* bases;      // device [T + 1]
+  uint16_t* const* ptrs;      // device [T]
+  uint32_t T;
+  uint32_t* err;
+};
+hipError_t launch_apply_chain(const ChainArgs& a, hipStream_t stream);
+
 // One slice of a tensor list for enqueue_extract: `n` words of both copies
 // whose word 0 has output index `base`; `tensor` is the caller's index and
 // `seg_base` the output index of that tensor's word 0.

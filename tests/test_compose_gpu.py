@@ -119,12 +119,96 @@ def test_catch_up_compose_equals_replay():
     for v in range(5):
         idx, val, _ = ad.delta_extract_multi(versions[v], versions[v + 1])
         deltas.append((idx.clone(), val.clone()))
-    a = [t.clone() for t in w0]
-    b = [t.clone() for t in w0]
-    ad.delta_catch_up(a, deltas, compose=True)
-    ad.delta_catch_up(b, deltas, compose=False)
-    for x, y, z in zip(a, b, versions[-1]):
-        assert torch.equal(x.view(torch.int16), z.view(torch.int16))
-        assert torch.equal(y.view(torch.int16), z.view(torch.int16))
+    for method in ("chain", "compose", "replay"):
+        a = [t.clone() for t in w0]
+        ad.delta_catch_up(a, deltas, method=method)
+        for x, z in zip(a, versions[-1]):
+            assert torch.equal(x.view(torch.int16), z.view(torch.int16)), method
     # and the composed delta is the oracle's
     check([(i.cpu().numpy(), host_u16(v)) for i, v in deltas])
+
+
+# ------------------------------------------------------ catch-up in one pass
+
+def weight_list(sizes, seed):
+    r = np.random.default_rng(seed)
+    hs = [r.integers(0, 1 << 16, size=n, dtype=np.uint16) for n in sizes]
+    ds = [torch.from_numpy(h.view(np.int16)).view(torch.bfloat16).to(DEV) for h in hs]
+    return hs, ds
+
+
+def oracle_replay(hs, deltas_h):
+    """The chain applied delta by delta by the oracle onto host copies."""
+    flat = np.concatenate(hs) if hs else np.zeros(0, np.uint16)
+    for i, v in deltas_h:
+        assert oracle.apply_(flat, i, v) == 0
+    out, pos = [], 0
+    for h in hs:
+        out.append(flat[pos:pos + h.size])
+        pos += h.size
+    return out
+
+
+def check_chain(sizes, deltas_h, seed=0):
+    hs, ws = weight_list(sizes, seed)
+    want = oracle_replay([h.copy() for h in hs], deltas_h)
+    ad.delta_apply_chain(ws, [to_dev(i, v) for i, v in deltas_h], check=True)
+    for t, (w, r) in enumerate(zip(ws, want)):
+        np.testing.assert_array_equal(host_u16(w), r, err_msg=f"tensor {t}")
+
+
+SIZES = [0, 70_001, 3, 0, 2 * 8192 + 5, 250_000, 1, 0]
+
+
+@pytest.mark.parametrize("K", [1, 2, 3, 4, 5, 9, 16])
+@pytest.mark.parametrize("density", [0.01, 0.2, 0.9])
+def test_apply_chain_matches_oracle(K, density):
+    N = sum(SIZES)
+    say("apply_chain K", K, "density", density)
+    deltas = [rand_delta(N, density, seed=7000 + 100 * K + d + int(density * 10))
+              for d in range(K)]
+    check_chain(SIZES, deltas, seed=K)
+
+
+def test_apply_chain_edge_cases():
+    N = sum(SIZES)
+    e = (np.zeros(0, np.int64), np.zeros(0, np.uint16))
+    a = rand_delta(N, 0.05, seed=11)
+    b = rand_delta(N, 0.05, seed=12)
+    check_chain(SIZES, [])
+    check_chain(SIZES, [e, e])
+    check_chain(SIZES, [e, a, e])
+    check_chain(SIZES, [a, a, a])                                  # same indices: newest wins
+    check_chain(SIZES, [a, (a[0], a[1][::-1].copy()), b])
+    # every index once, then every index again
+    full = (np.arange(N, dtype=np.int64), np.arange(N, dtype=np.uint16))
+    check_chain(SIZES, [full, b, full])
+
+
+def test_apply_chain_uneven_deltas():
+    """A large delta sets the tiles; a small one packed into a narrow range
+    overfills some of them (their runs are searched in global memory), and
+    one that sits past the large delta's last entry goes to the last tile."""
+    N = sum(SIZES)
+    big = rand_delta(N, 0.05, seed=21)
+    r = np.random.default_rng(22)
+    packed = np.sort(r.choice(np.arange(100_000, 130_000), size=20_000, replace=False))
+    packed = (packed.astype(np.int64), r.integers(0, 1 << 16, size=packed.size, dtype=np.uint16))
+    tail = (np.arange(N - 50, N, dtype=np.int64), np.full(50, 7, np.uint16))
+    head = (np.arange(0, 30, dtype=np.int64), np.full(30, 9, np.uint16))
+    check_chain(SIZES, [packed, big, packed])
+    check_chain(SIZES, [big, packed, tail, head, big])
+
+
+def test_apply_chain_flags_and_limits():
+    N = sum(SIZES)
+    hs, ws = weight_list(SIZES, 3)
+    a = rand_delta(N, 0.05, seed=31)
+    bad = (np.array([5, N + 3], np.int64), np.array([1, 2], np.uint16))
+    with pytest.raises(ad.DeltaError):
+        ad.delta_apply_chain(ws, [to_dev(*a), to_dev(*bad)], check=True)
+    unsorted = (np.array([9, 4, 100], np.int64), np.array([1, 2, 3], np.uint16))
+    with pytest.raises(ad.DeltaError):
+        ad.delta_apply_chain(ws, [to_dev(*unsorted), to_dev(*a)], check=True)
+    with pytest.raises(ad.DeltaError):
+        ad.delta_apply_chain(ws, [to_dev(*a)] * 17)

@@ -240,6 +240,35 @@ def test_compose_chain_full_index_space():
     np.testing.assert_array_equal(out_v.view(torch.int16).cpu().numpy().view(np.uint16), ref_v)
 
 
+def test_apply_chain_full_weight_set():
+    """Catch-up over three ~1% deltas of the Qwen3-8B tensor list in one
+    pass: sampled tensors equal the oracle replaying the chain on them."""
+    ws = synth.make_weight_set("qwen3-8b", 0.0, seed=synth.config_seed(3), device=DEV)
+    roll = [p.clone() for p in ws.prev]
+    bases = np.concatenate([[0], np.cumsum(ws.numels)]).astype(np.int64)
+    N = int(bases[-1])
+    g = torch.Generator(device=DEV)
+    g.manual_seed(78)
+    deltas = []
+    for d in range(3):
+        idx = torch.unique(torch.randint(0, N, (81_907_354,), device=DEV, generator=g))
+        val = torch.randint(-32768, 32767, (idx.numel(),), device=DEV, generator=g,
+                            dtype=torch.int16).view(torch.bfloat16)
+        deltas.append((idx, val))
+    say("apply_chain: deltas of", [i.numel() for i, _ in deltas], "entries")
+    ad.delta_apply_chain(roll, deltas, check=True)
+    torch.cuda.synchronize()
+    for t in sample_tensors(ws.names, ws.shapes):
+        lo, hi = int(bases[t]), int(bases[t + 1])
+        want = host_u16(ws.prev[t]).copy()
+        for idx, val in deltas:
+            a = int(torch.searchsorted(idx, lo))
+            b = int(torch.searchsorted(idx, hi))
+            assert oracle.apply_(want, idx[a:b].cpu().numpy() - lo, host_u16(val[a:b])) == 0
+        np.testing.assert_array_equal(host_u16(roll[t]), want, err_msg=ws.names[t])
+    say("apply_chain full ok")
+
+
 def test_qwen3_8b_fused_layout():
     ws = synth.make_weight_set("qwen3-8b", 0.01, seed=synth.config_seed(3), device=DEV)
     targets, sources = synth.qwen3_fused_layout("qwen3-8b")
