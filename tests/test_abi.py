@@ -134,6 +134,41 @@ def test_extract_multi_validation(lib):
                                    1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
 
 
+def test_apply_chain_validation(lib):
+    P = ctypes.c_void_p
+    U = ctypes.c_uint64
+    w = (P * 2)(FAKE, FAKE)
+    numels = (U * 2)(1000, 24)
+    ip = (P * 3)(FAKE, FAKE, FAKE)
+    vp = (P * 3)(FAKE, FAKE, FAKE)
+    counts = (U * 3)(10, 20, 5)
+    need = lib.delta_apply_chain_workspace_bytes(counts, 3, 2)
+    assert need >= lib.delta_apply_multi_workspace_bytes(2)
+    assert lib.delta_apply_chain_workspace_bytes(None, 3, 2) == 0
+    assert lib.delta_apply_chain_workspace_bytes(counts, -1, 2) == 0
+    assert lib.delta_apply_chain_workspace_bytes(counts, 3, -1) == 0
+
+    def call(K=3, ips=ip, vps=vp, ws=FAKE, wsb=1 << 20, cnts=counts, ww=w):
+        return lib.delta_apply_chain(ww, numels, 2, ips, vps, cnts, K, None, ws, wsb, None)
+
+    many = (U * 17)(*([1] * 17))
+    assert call(K=17, cnts=many) == _abi.DELTA_ERR_INVALID_ARG      # more than 16 deltas
+    assert b"16" in lib.delta_last_error()
+    assert call(K=-1) == _abi.DELTA_ERR_INVALID_ARG
+    assert call(ips=None) == _abi.DELTA_ERR_INVALID_ARG
+    assert call(ips=(P * 3)(FAKE, None, FAKE)) == _abi.DELTA_ERR_INVALID_ARG   # NULL delta
+    assert b"delta 1" in lib.delta_last_error()
+    assert call(ips=(P * 3)(FAKE, FAKE + 4, FAKE)) == _abi.DELTA_ERR_INVALID_ARG
+    assert call(vps=(P * 3)(FAKE, FAKE, FAKE + 1)) == _abi.DELTA_ERR_INVALID_ARG
+    assert call(ww=(P * 2)(FAKE, None)) == _abi.DELTA_ERR_INVALID_ARG      # NULL tensor
+    assert call(wsb=need - 1) == _abi.DELTA_ERR_WORKSPACE
+    assert call(ws=None) == _abi.DELTA_ERR_WORKSPACE
+    # nothing to apply: accepted without touching the device
+    zero = (U * 3)(0, 0, 0)
+    assert call(cnts=zero, ips=(P * 3)(None, None, None), vps=(P * 3)(None, None, None)) == \
+        _abi.DELTA_OK
+
+
 def test_extract_multi_leb128_validation(lib):
     P = ctypes.c_void_p
     prevs = (P * 2)(FAKE, FAKE)
