@@ -561,12 +561,12 @@ delta_status_t delta_apply_chain(uint16_t* const* weight_ptrs, const uint64_t* n
   if (e != hipSuccess) return hip_fail(e, "delta table upload launch");
   ChainArgs a;
   memset(&a, 0, sizeof(a));
-  a.deltas = (const ChainDelta*)(ws + c.deltas);
-  a.K = (uint32_t)num_deltas;
-  a.ref = c.ref;
-  a.per_tile = c.per_tile;
-  a.tiles = c.tiles;
-  a.pos = (uint64_t*)(ws + c.pos);
+  a.r.deltas = (const ChainDelta*)(ws + c.deltas);
+  a.r.K = (uint32_t)num_deltas;
+  a.r.tiles = c.tiles;
+  a.r.bsrc = idx_ptrs[c.ref];   // tiles cut at every per_tile-th index of the largest delta
+  a.r.bstride = c.per_tile;
+  a.r.pos = (uint64_t*)(ws + c.pos);
   a.bases = d_bases;
   a.ptrs = (uint16_t* const*)d_ptrs;
   a.T = (uint32_t)num_tensors;

@@ -6,6 +6,7 @@
 // rather than adds: the result is bit-exact and applying a delta twice
 // changes nothing.  Indices are distinct, so no two lanes write one word
 // and no atomics are needed.
+#include "chain.h"
 #include "delta_internal.h"
 
 namespace aurora {
@@ -125,66 +126,46 @@ __global__ __launch_bounds__(kApplyThreads) void apply_multi_kernel(
 // Applies D_1..D_K (oldest first) so that every index gets the word of the
 // newest delta holding it: the result of replaying the chain (Sec. 5.4) or
 // of applying its composition, without forming the composed delta.  The
-// index space is cut into value ranges at every S-th index of the largest
-// delta (the reference): tile t takes the indices from R[t S] (from minus
-// infinity for t = 0) up to R[(t + 1) S] (to plus infinity for the last
-// tile), so every entry of every delta lies in exactly one tile; a tile
-// holds S reference entries (the last one fewer) and, for deltas of
-// similar density, about as many of every other.  A split kernel finds
-// where each tile starts in each delta.  One workgroup per tile stages the
-// tile's runs of all deltas in LDS and takes its entries in turn
-// (lane-strided, so each store instruction writes 64 consecutive entries of
-// one run); an entry is written unless a newer delta's run holds its index
-// (binary search, in LDS, or in global memory for a tile whose runs do not
-// fit).
+// tiles (chain.h) are cut at every S-th index of the largest delta, so a
+// tile holds S of its entries and, for deltas of similar density, about
+// as many of every other.  A tile whose runs fit in LDS is ranked into
+// merged order and its kept words (the newest of equal indices) are stored
+// in index order, as a composed delta would store them; a larger tile
+// (deltas of very uneven density) searches newer runs in global memory and
+// stores in run order.
 
-// The deltas' addresses come from a table in memory, so the compiler
-// cannot tell they are global; flat accesses would also count against the
-// LDS wait counter, so the kernels below use these global-space views.
-template <typename T>
-__device__ __forceinline__ const __attribute__((address_space(1))) T* gview(const T* p) {
-  return (const __attribute__((address_space(1))) T*)p;
-}
-
-__global__ void chain_split_kernel(ChainArgs a) {
+__global__ void chain_split_kernel(ChainRuns r) {
   const uint64_t q = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= (a.tiles + 1) * a.K) return;
-  const uint64_t b = q / a.K;
-  const uint32_t k = (uint32_t)(q % a.K);
-  const ChainDelta d = a.deltas[k];
+  if (q >= (r.tiles + 1) * r.K) return;
+  const uint64_t b = q / r.K;
+  const uint32_t k = (uint32_t)(q % r.K);
+  const ChainDelta d = r.deltas[k];
   uint64_t p;
   if (b == 0) {
     p = 0;
-  } else if (b == a.tiles) {
+  } else if (b == r.tiles) {
     p = d.n;
   } else {
-    const int64_t v = gview(a.deltas[a.ref].idx)[b * a.per_tile];
-    const auto x = gview(d.idx);
+    const int64_t v = gview(r.bsrc)[b * r.bstride];
     uint64_t lo = 0, hi = d.n;
+    const auto x = gview(d.idx);
     while (lo < hi) {
       const uint64_t mid = (lo + hi) >> 1;
       if (x[mid] < v) lo = mid + 1; else hi = mid;
     }
     p = lo;
   }
-  a.pos[q] = p;
+  r.pos[q] = p;
 }
 
-// Entries of the sorted run x[0, n) below v (lower bound) or at most v
-// (upper bound).
-__device__ __forceinline__ uint32_t run_rank(const int64_t* x, uint32_t n, int64_t v,
-                                             bool upper) {
-  uint32_t lo = 0, hi = n;
-  while (lo < hi) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (x[mid] < v || (upper && x[mid] == v)) lo = mid + 1; else hi = mid;
-  }
-  return lo;
+hipError_t launch_chain_split(const ChainRuns& r, hipStream_t stream) {
+  const uint64_t bounds = (r.tiles + 1) * r.K;
+  hipLaunchKernelGGL(chain_split_kernel, dim3((uint32_t)((bounds + 255) / 256)), dim3(256), 0,
+                     stream, r);
+  return hipGetLastError();
 }
 
 constexpr int kChainPer = 8;   // entries per thread loaded before any is processed
-static_assert(kChainLds <= 4096 && kChainMaxDeltas <= 16,
-              "a merged position holds (delta << 12) | staged entry in 16 bits");
 
 // Stores word v at global index g of the tensor list (the lane caches the
 // tensor it wrote last); false if g is outside the list.
@@ -206,88 +187,17 @@ __device__ __forceinline__ bool store_global(const ChainArgs& a, uint64_t words,
   return true;
 }
 
+static_assert(kApplyThreads == kChainThreads, "the chain helpers assume 256 threads");
+
 __global__ __launch_bounds__(kApplyThreads) void chain_apply_kernel(ChainArgs a) {
-  __shared__ int64_t s_idx[kChainLds];
-  __shared__ uint16_t s_perm[kChainLds];          // merged position -> (delta << 12) | entry
-  __shared__ ChainDelta s_d[kChainMaxDeltas];
-  __shared__ uint64_t s_start[kChainMaxDeltas];   // the run's first entry in its delta
-  __shared__ uint32_t s_off[kChainMaxDeltas + 1];  // run offsets in the tile's order
-  const uint64_t t = blockIdx.x;
-  const uint32_t K = a.K;
+  __shared__ ChainSmem s;
+  const uint32_t K = a.r.K;
   bool bad = false;
-  if (threadIdx.x < K) {
-    const uint32_t k = threadIdx.x;
-    const uint64_t p0 = a.pos[t * K + k];
-    uint64_t p1 = a.pos[(t + 1) * K + k];
-    if (p1 < p0) {   // only unsorted input gets here
-      bad = true;
-      p1 = p0;
-    }
-    // a tile of 2^32 entries or more (only from grossly uneven deltas) is
-    // cut short and flagged rather than applied in part silently
-    if (p1 - p0 >= 0xFFFFFFFFull) bad = true;
-    s_d[k] = a.deltas[k];
-    s_start[k] = p0;
-    s_off[k + 1] = (uint32_t)(p1 - p0 < 0xFFFFFFFFull ? p1 - p0 : 0xFFFFFFFFull);
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint64_t acc = 0;
-    s_off[0] = 0;
-    for (uint32_t k = 0; k < K; ++k) {
-      acc += s_off[k + 1];
-      if (acc >= 0xFFFFFFFFull) bad = true;
-      s_off[k + 1] = (uint32_t)(acc < 0xFFFFFFFFull ? acc : 0xFFFFFFFFull);
-    }
-  }
-  __syncthreads();
-  const uint32_t total = s_off[K];
+  const uint32_t total = chain_tile_setup(a.r, blockIdx.x, s, bad);
   const uint64_t words = a.bases[a.T];
   TensorCursor cur;
   if (total <= kChainLds) {   // uniform
-    // Stage the tile's runs, then give every entry its position in the
-    // merged order of all runs (ties: older delta first): its place in its
-    // own run plus, in every other run, the entries below it (newer runs)
-    // or at most it (older runs).  Of equal indices the newest then comes
-    // last and is the one kept, and the kept words are stored in index
-    // order, as a composed delta would be.
-    {
-      // kChainPer loads per thread in flight before any is stored
-      uint32_t k = 0;
-      for (uint32_t q0 = threadIdx.x; q0 < total; q0 += kApplyThreads * kChainPer) {
-        int64_t x[kChainPer];
-#pragma unroll
-        for (int u = 0; u < kChainPer; ++u) {
-          const uint32_t q = q0 + kApplyThreads * u;
-          x[u] = 0;
-          if (q < total) {
-            while (q >= s_off[k + 1]) ++k;
-            x[u] = gview(s_d[k].idx)[s_start[k] + (q - s_off[k])];
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < kChainPer; ++u) {
-          const uint32_t q = q0 + kApplyThreads * u;
-          if (q < total) s_idx[q] = x[u];
-        }
-      }
-    }
-    __syncthreads();
-    {
-      uint32_t k = 0;
-      for (uint32_t q = threadIdx.x; q < total; q += kApplyThreads) {
-        while (q >= s_off[k + 1]) ++k;
-        const int64_t x = s_idx[q];
-        if (q + 1 < s_off[k + 1] && s_idx[q + 1] <= x) bad = true;   // unsorted run
-        uint32_t pos = q - s_off[k];
-        for (uint32_t k2 = 0; k2 < K; ++k2)   // older runs first on equal indices
-          if (k2 != k) pos += run_rank(s_idx + s_off[k2], s_off[k2 + 1] - s_off[k2], x, k2 < k);
-        // sorted runs give a permutation of [0, total); the bound keeps
-        // unsorted ones inside the array
-        s_perm[pos < total ? pos : total - 1] = (uint16_t)((k << 12) | q);
-      }
-    }
-    __syncthreads();
+    chain_stage_rank(K, total, s, bad);
     for (uint32_t p0 = threadIdx.x; p0 < total; p0 += kApplyThreads * kChainPer) {
       int64_t x[kChainPer];
       uint16_t v[kChainPer];
@@ -298,16 +208,14 @@ __global__ __launch_bounds__(kApplyThreads) void chain_apply_kernel(ChainArgs a)
         keep[u] = false;
         x[u] = 0;
         v[u] = 0;
+        uint32_t k, q;
         if (p < total) {
-          const uint32_t code = s_perm[p];
-          const uint32_t k = code >> 12, q = code & 0xFFFu;
-          if (k >= K || q < s_off[k] || q >= s_off[k + 1]) {   // unsorted input only
+          if (!chain_entry(s, K, total, p, k, q, keep[u])) {
             bad = true;
             continue;
           }
-          x[u] = s_idx[q];
-          keep[u] = p + 1 == total || s_idx[s_perm[p + 1] & 0xFFFu] != x[u];
-          if (keep[u]) v[u] = gview(s_d[k].val)[s_start[k] + (q - s_off[k])];
+          x[u] = s.idx[q];
+          if (keep[u]) v[u] = gview(s.d[k].val)[s.start[k] + (q - s.off[k])];
         }
       }
 #pragma unroll
@@ -315,42 +223,34 @@ __global__ __launch_bounds__(kApplyThreads) void chain_apply_kernel(ChainArgs a)
         if (keep[u] && !store_global(a, words, cur, x[u], v[u])) bad = true;
     }
   } else {
-    // A tile too large for LDS (deltas of very uneven density): each entry
-    // in turn, written unless a newer run holds its index (binary search in
-    // global memory); stored in run order.
+    // A tile too large for LDS: each entry in turn, written unless a newer
+    // run holds its index (binary search in global memory).
     uint32_t k = 0;
     for (uint32_t q = threadIdx.x; q < total; q += kApplyThreads) {
-      while (q >= s_off[k + 1]) ++k;
-      const uint64_t e = s_start[k] + (q - s_off[k]);
-      const auto xs = gview(s_d[k].idx);
+      while (q >= s.off[k + 1]) ++k;
+      const uint64_t e = s.start[k] + (q - s.off[k]);
+      const auto xs = gview(s.d[k].idx);
       const int64_t x = xs[e];
-      if (q + 1 < s_off[k + 1] && xs[e + 1] <= x) bad = true;
+      if (q + 1 < s.off[k + 1] && xs[e + 1] <= x) bad = true;
       bool newer = false;
       for (uint32_t k2 = k + 1; k2 < K && !newer; ++k2) {
-        const uint32_t n2 = s_off[k2 + 1] - s_off[k2];
-        const auto r = gview(s_d[k2].idx) + s_start[k2];
-        uint32_t lo = 0, hi = n2;
-        while (lo < hi) {
-          const uint32_t mid = (lo + hi) >> 1;
-          if (r[mid] < x) lo = mid + 1; else hi = mid;
-        }
-        newer = lo < n2 && r[lo] == x;
+        const uint32_t n2 = s.off[k2 + 1] - s.off[k2];
+        const auto r = gview(s.d[k2].idx) + s.start[k2];
+        const uint32_t at = run_rank(r, n2, x, false);
+        newer = at < n2 && r[at] == x;
       }
-      if (!newer && !store_global(a, words, cur, x, gview(s_d[k].val)[e])) bad = true;
+      if (!newer && !store_global(a, words, cur, x, gview(s.d[k].val)[e])) bad = true;
     }
   }
   if (bad) flag_error(a.err);
 }
 
 hipError_t launch_apply_chain(const ChainArgs& a, hipStream_t stream) {
-  if (a.tiles == 0) return hipSuccess;
-  const uint64_t bounds = (a.tiles + 1) * a.K;
-  hipLaunchKernelGGL(chain_split_kernel, dim3((uint32_t)((bounds + 255) / 256)), dim3(256), 0,
-                     stream, a);
-  hipError_t e = hipGetLastError();
+  if (a.r.tiles == 0) return hipSuccess;
+  hipError_t e = launch_chain_split(a.r, stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(chain_apply_kernel, dim3((uint32_t)a.tiles), dim3(kApplyThreads), 0, stream,
-                     a);
+  hipLaunchKernelGGL(chain_apply_kernel, dim3((uint32_t)a.r.tiles), dim3(kApplyThreads), 0,
+                     stream, a);
   return hipGetLastError();
 }
 

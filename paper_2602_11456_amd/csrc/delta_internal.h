@@ -235,19 +235,25 @@ struct ChainDelta {
   uint64_t n;
 };
 static_assert(sizeof(ChainDelta) == 24, "uploaded as three 64-bit words per delta");
-struct ChainArgs {
+// The tiles of a chain (chain.h): boundary b (0 < b < tiles) is
+// bsrc[b * bstride].
+struct ChainRuns {
   const ChainDelta* deltas;   // device [K]
   uint32_t K;
-  uint32_t ref;
-  uint64_t per_tile;
   uint64_t tiles;
-  uint64_t* pos;
+  const int64_t* bsrc;
+  uint64_t bstride;
+  uint64_t* pos;              // [(tiles + 1) * K]: entries of delta k before tile t
+};
+struct ChainArgs {
+  ChainRuns r;
   const uint64_t* bases;      // device [T + 1]
   uint16_t* const* ptrs;      // device [T]
   uint32_t T;
   uint32_t* err;
 };
 hipError_t launch_apply_chain(const ChainArgs& a, hipStream_t stream);
+hipError_t launch_chain_split(const ChainRuns& r, hipStream_t stream);
 
 // One slice of a tensor list for enqueue_extract: `n` words of both copies
 // whose word 0 has output index `base`; `tensor` is the caller's index and
