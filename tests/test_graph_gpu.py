@@ -103,3 +103,100 @@ def test_apply_multi_graph_replays():
         assert oracle.apply_multi_(ref, idx.cpu().numpy(), host_u16(val)) == 0
         for r, w in zip(rollout, ref):
             np.testing.assert_array_equal(host_u16(r), w)
+
+
+@pytest.mark.parametrize("sizes", [[70_001, 3, 50_000, 8192 * 3 + 1],        # inline slices
+                                   [3000 + 17 * i for i in range(40)]])     # tensor table
+def test_extract_multi_leb128_graph_replays(sizes):
+    """The extract that writes LEB128 itself, captured once: every replay's
+    bytes, words and offsets equal the oracle's for the data it saw."""
+    prevs = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    news = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    fill_random(prevs, 3)
+    for p, q in zip(prevs, news):
+        q.copy_(p)
+    plan = ad.MultiPlan(prevs, news)
+    total = sum(sizes)
+    code = torch.empty(3 * total, dtype=torch.uint8, device=DEV)
+    val = torch.empty(total, dtype=torch.bfloat16, device=DEV)
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    nb = torch.zeros(1, dtype=torch.int64, device=DEV)
+    offs = torch.zeros(plan.T + 1, dtype=torch.int64, device=DEV)
+    boffs = torch.zeros(plan.T + 1, dtype=torch.int64, device=DEV)
+    work = torch.empty(ad.delta_extract_multi_leb128_workspace_bytes(plan.numels),
+                       dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        ad.delta_extract_multi_leb128_into(plan, code, val, cnt, nb, work, offs, boffs, stream=s)
+    s.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        ad.delta_extract_multi_leb128_into(plan, code, val, cnt, nb, work, offs, boffs, stream=s)
+    bases = np.concatenate([[0], np.cumsum(sizes)])[:-1].astype(np.int64)
+    for rep, density in enumerate([0.01, 0.3, 0.0, 0.002]):
+        g = torch.Generator(device=DEV)
+        g.manual_seed(300 + rep)
+        for p, q in zip(prevs, news):
+            q.copy_(p)
+            m = torch.rand(q.shape, device=DEV, generator=g) < density
+            q.view(torch.int16)[m] ^= 0x0301
+        code.fill_(0xEE)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        ref_idx, ref_val, ref_offs, ref_cnt = oracle.extract_multi(
+            [host_u16(p) for p in prevs], [host_u16(q) for q in news])
+        ref_offs = ref_offs.astype(np.int64)
+        parts, starts = [], [0]
+        for t in range(len(sizes)):
+            b, n = oracle.leb128_encode(ref_idx[ref_offs[t]:ref_offs[t + 1]] - bases[t])
+            parts.append(b)
+            starts.append(starts[-1] + n)
+        ref_code = np.concatenate(parts)
+        assert int(cnt.item()) == ref_cnt and int(nb.item()) == ref_code.size, rep
+        np.testing.assert_array_equal(code[:ref_code.size].cpu().numpy(), ref_code)
+        np.testing.assert_array_equal(host_u16(val[:ref_cnt]), ref_val)
+        np.testing.assert_array_equal(offs.cpu().numpy(), ref_offs)
+        np.testing.assert_array_equal(boffs.cpu().numpy(), np.array(starts, np.int64))
+
+
+def test_apply_chain_graph_replays():
+    """A catch-up over three deltas in one pass, captured once and replayed
+    onto fresh copies of the old weights."""
+    sizes = [70_001, 3, 50_000, 8192 * 3 + 1]
+    N = sum(sizes)
+    prevs = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    fill_random(prevs, 4)
+    r = np.random.default_rng(9)
+    deltas_h = []
+    for d in range(3):
+        idx = np.sort(r.choice(N, size=N // 20, replace=False)).astype(np.int64)
+        deltas_h.append((idx, r.integers(0, 1 << 16, size=idx.size, dtype=np.uint16)))
+    deltas = [(torch.from_numpy(i).to(DEV),
+               torch.from_numpy(v.view(np.int16)).view(torch.bfloat16).to(DEV))
+              for i, v in deltas_h]
+    rollout = [torch.empty_like(p) for p in prevs]
+    work = torch.empty(ad.delta_apply_chain_workspace_bytes([i.size for i, _ in deltas_h],
+                                                            len(sizes)),
+                       dtype=torch.uint8, device=DEV)
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        ad.delta_apply_chain(rollout, deltas, error_flag=flag, workspace=work, stream=s)
+    s.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        ad.delta_apply_chain(rollout, deltas, error_flag=flag, workspace=work, stream=s)
+    flat = np.concatenate([host_u16(p) for p in prevs])
+    for i, v in deltas_h:
+        assert oracle.apply_(flat, i, v) == 0
+    for rep in range(3):
+        for x, p in zip(rollout, prevs):   # eager work: back to the old weights
+            x.copy_(p)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert int(flag.item()) == 0
+        np.testing.assert_array_equal(np.concatenate([host_u16(x) for x in rollout]), flat)
