@@ -134,15 +134,18 @@ constexpr int kDeliverThreads = 256;
 // scans, run on the first XCDs).  How few is a trade between filling the
 // host link and leaving the reads alone (Qwen3-14B, 2^27-word chunks,
 // plain / coded ms): 2 XCDs x 8 workgroups 30.4 / 17.1; 4 x 4 29.7 / 17.2;
-// 8 x 2 29.7-29.8 / 17.0; 1 x 4 35.0 / 13.7-14.1; 2 x 2 34.4 / 14.0;
-// 1 x 2 37.4 / 18.6.  The plain stream (10 bytes per entry) needs the
-// link's rate, the coded one (about 3.3) far less: it takes 1 x 4.
+// 8 x 2 29.7-29.8 / 17.0; 1 x 4 35.0 / 13.7-14.5; 2 x 2 34.4 / 14.0;
+// 1 x 2 37.4 / 18.6; plain 4 x 5 / 4 x 6 / 4 x 8 / 3 x 6 / 6 x 4 29.4 /
+// 29.2-29.4 / 32.4 / 29.8 / 34.5; coded 1 x 3 / 1 x 5 / 1 x 6 / 1 x 7 /
+// 1 x 8 / 2 x 4 16.3 / 13.7 / 13.3-13.5 / 13.9 / 14.4 / 15.2.  The plain
+// stream (10 bytes per entry) needs the link's rate and takes 4 x 6; the
+// coded one (about 3.3) far less: 1 x 6.
 constexpr int kXcds = 8;
 struct DeliverShape {
   uint32_t xcds, per_xcd;
 };
-constexpr DeliverShape kDeliverPlain = {4, 4};
-constexpr DeliverShape kDeliverCoded = {1, 4};
+constexpr DeliverShape kDeliverPlain = {4, 6};
+constexpr DeliverShape kDeliverCoded = {1, 6};
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 // four dwords at a 4-byte aligned address (one 16-byte load)
