@@ -1036,11 +1036,15 @@ __global__ void upload_words_kernel(WordBatch b, uint64_t* dst) {
   for (uint32_t i = threadIdx.x; i < b.count; i += blockDim.x) dst[i] = b.w[i];
 }
 
+// Row t of the table fills its tiles' map entries; a row's tiles are spread
+// over gridDim.y workgroups (the largest tensors span tens of thousands).
 __global__ void build_tile_map_kernel(const TensorDesc* table, uint32_t* tile_map) {
   const uint32_t t = blockIdx.x;
   const TensorDesc d = table[t];
   const uint64_t nt = tiles_for(d.n, d.head);
-  for (uint64_t i = threadIdx.x; i < nt; i += blockDim.x) tile_map[d.first_tile + i] = t;
+  const uint64_t stride = (uint64_t)gridDim.y * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.y * blockDim.x + threadIdx.x; i < nt; i += stride)
+    tile_map[d.first_tile + i] = t;
 }
 
 hipError_t launch_reset(uint64_t* d_count, uint64_t* d_offsets, uint32_t num_offsets,
@@ -1069,7 +1073,7 @@ hipError_t launch_upload_words(const uint64_t* host_words, size_t nwords, uint64
 hipError_t launch_build_tile_map(const TensorDesc* table, uint32_t num_tensors,
                                  uint32_t* tile_map, hipStream_t stream) {
   if (num_tensors == 0) return hipSuccess;
-  hipLaunchKernelGGL(build_tile_map_kernel, dim3(num_tensors), dim3(256), 0, stream, table,
+  hipLaunchKernelGGL(build_tile_map_kernel, dim3(num_tensors, 8), dim3(256), 0, stream, table,
                      tile_map);
   return hipGetLastError();
 }
