@@ -534,6 +534,68 @@ def _prefix(xs):
         yield s
 
 
+def count_measurement(ad, lib, plan, work, stream, reps, K, scanned, stage_ms):
+    """delta_count_changed_multi on the same set: the extract's reads and
+    compares with nothing staged or written, i.e. the read cost of the scan
+    at the same tile shape; its count must equal the extract's."""
+    import torch
+    cnt = torch.zeros(1, dtype=torch.int64, device=work.device)
+    ad.delta_count_changed_multi_into(plan, cnt, work, stream)
+    stream.synchronize()
+    if int(cnt.item()) != K:
+        raise RuntimeError(f"count {int(cnt.item())} differs from the extract's {K}")
+    call, kern = [], []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        s1.record(stream)
+        if lib.delta_set_scan_events(s0.cuda_event, s1.cuda_event):
+            raise RuntimeError(lib.delta_last_error().decode())
+        e0.record(stream)
+        ad.delta_count_changed_multi_into(plan, cnt, work, stream)
+        e1.record(stream)
+        stream.synchronize()
+        lib.delta_set_scan_events(None, None)
+        call.append(e0.elapsed_time(e1))
+        kern.append(s0.elapsed_time(s1))
+    call_ms = sum(call) / len(call)
+    kern_ms = sum(kern) / len(kern)
+    return {
+        "workload": "delta_count_changed_multi over the same set (both copies read once, "
+                    "nothing staged or written)",
+        "ms": round(call_ms, 4),
+        "count_kernel_ms": round(kern_ms, 4),
+        "count_kernel_GBps": round(scanned / (kern_ms / 1e3) / 1e9, 2),
+        "count_kernel_frac_of_peak": round(scanned / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "stage_kernel_vs_count_kernel": round(kern_ms / stage_ms, 4),
+    }
+
+
+def torch_reference_measurement(ws, reps=3):
+    """Informational: the same extract written with torch operations only
+    (compare, nonzero, gather per tensor; nonzero waits for the host), not
+    part of the library."""
+    import torch
+    times = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        total = 0
+        for p, q in zip(ws.prev, ws.new):
+            pv, qv = p.reshape(-1).view(torch.int16), q.reshape(-1).view(torch.int16)
+            i = torch.nonzero(pv != qv).reshape(-1)
+            v = qv[i]
+            total += i.numel()
+            del i, v
+        torch.cuda.synchronize()
+        times.append((time.perf_counter() - t0) * 1e3)
+    ms = sorted(times)[len(times) // 2]
+    return {"workload": "torch.nonzero(prev != new) and a gather, tensor by tensor",
+            "ms": round(ms, 3), "changed": total,
+            "GBps_scanned": round(4 * ws.total / (ms / 1e3) / 1e9, 1)}
+
+
 def extras(args, ad, synth, ws, rollout, plan, out_idx, out_val, d_offs, work, stream, K, N,
            result):
     """The measurements beside the headline step: LEB128 coding, integrity
@@ -550,6 +612,7 @@ def extras(args, ad, synth, ws, rollout, plan, out_idx, out_val, d_offs, work, s
                                         args.steps)
     result["compose"] = compose_measurement(ad, rollout, N, K, stream, max(args.steps // 2, 3))
     result["single_tensor"] = single_tensor_measurement(ad, synth, stream, max(args.steps, 20))
+    result["torch_reference"] = torch_reference_measurement(ws)
 
 
 def main():
@@ -735,6 +798,8 @@ def main():
             "algorithmic_bytes": alg_bytes,
         },
     }
+    result["count_only"] = count_measurement(ad, lib, plan, work, stream, args.steps, K, scanned,
+                                             scan_avg)
     if not args.no_extras:
         extras(args, ad, synth, ws, rollout, plan, out_idx, out_val, d_offs, work, stream, K, N,
                result)

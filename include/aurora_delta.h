@@ -166,6 +166,26 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
                                    size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * delta_count_changed_multi — Sec. 5.1: the number of changed words of a
+ * tensor list, i.e. the entry count of its sparse delta, without forming
+ * the delta.  It runs the extract's read-and-compare and count steps only
+ * (both copies read once, nothing staged or written), so a caller can size
+ * the outputs exactly before extracting, and it gives the read cost alone.
+ *   prev_ptrs, next_ptrs, numels, num_tensors  as for delta_extract_multi.
+ *   d_count       device uint64: the total (overwritten).
+ *   workspace     device, 256-byte aligned, at least
+ *                 delta_extract_multi_workspace_bytes(numels, num_tensors)
+ *                 bytes (the extract's workspace fits).
+ * Errors: DELTA_ERR_INVALID_ARG (NULL d_count, bad tensor arguments as for
+ * delta_extract_multi), DELTA_ERR_WORKSPACE, DELTA_ERR_HIP.
+ */
+delta_status_t delta_count_changed_multi(const uint16_t* const* prev_ptrs,
+                                         const uint16_t* const* next_ptrs,
+                                         const uint64_t* numels, int32_t num_tensors,
+                                         uint64_t* d_count, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream);
+
+/*
  * delta_extract_fused — Sec. 5.1: the delta written under the inference
  * engine's fused names, where blocks of several training tensors are
  * stacked into one (q, k, v rows into qkv_proj; gate, up into

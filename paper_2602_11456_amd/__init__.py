@@ -25,7 +25,8 @@ from . import _abi
 
 __all__ = [
     "DeltaError", "library", "delta_extract", "delta_extract_into", "delta_extract_multi",
-    "delta_extract_multi_into", "delta_apply", "delta_apply_multi", "delta_apply_checked",
+    "delta_extract_multi_into", "delta_count_changed_multi", "delta_count_changed_multi_into",
+    "delta_apply", "delta_apply_multi", "delta_apply_checked",
     "delta_extract_pipelined", "delta_extract_workspace_bytes",
     "delta_extract_multi_workspace_bytes", "delta_apply_multi_workspace_bytes",
     "delta_pipeline_staging_bytes", "MultiPlan", "delta_leb128_encode", "delta_leb128_decode",
@@ -207,6 +208,28 @@ def delta_extract_multi_into(plan: MultiPlan, out_idx: torch.Tensor, out_val: to
         _words(out_val, "out_val"), cap, d_count.data_ptr(),
         d_offsets.data_ptr() if d_offsets is not None else None, workspace.data_ptr(),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def delta_count_changed_multi_into(plan: MultiPlan, d_count: torch.Tensor,
+                                   workspace: torch.Tensor,
+                                   stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Enqueue ``delta_count_changed_multi`` (no sync): the number of
+    changed words of the plan's tensors into ``d_count`` (int64, 1 entry)."""
+    _check(library().delta_count_changed_multi(
+        plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, plan.T, d_count.data_ptr(),
+        workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def delta_count_changed_multi(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tensor],
+                              stream: Optional[torch.cuda.Stream] = None) -> int:
+    """Number of changed words over a tensor list: the entry count of the
+    delta (Sec. 5.1), without forming it."""
+    plan = MultiPlan(prevs, news)
+    ws = _workspace(plan.workspace_bytes, plan.device)
+    cnt = torch.zeros(1, dtype=torch.int64, device=plan.device)
+    delta_count_changed_multi_into(plan, cnt, ws, stream)
+    (stream or torch.cuda.current_stream()).synchronize()
+    return int(cnt.item())
 
 
 def delta_extract_multi(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tensor],

@@ -145,7 +145,12 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
                                bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
                                uint64_t* d_count, uint64_t* d_offsets, void* workspace,
                                size_t have, hipStream_t stream, const CodedOut* coded,
-                               const StageSplit* split) {
+                               const StageSplit* split, bool count_only) {
+  if (count_only) {
+    coded = nullptr;
+    split = nullptr;
+    d_offsets = nullptr;
+  }
   std::vector<TensorDesc> descs;
   const uint64_t tiles = build_descs(slices, num_slices, descs);
   if (tiles > 0xFFFFFFFFull / kThreads)
@@ -204,7 +209,9 @@ delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_
   }
   bool all_vec = true;
   for (const TensorDesc& t : descs) all_vec = all_vec && t.vec;
-  if (coded) {
+  if (count_only) {
+    e = launch_count(a, all_vec, stream);
+  } else if (coded) {
     a.tile_rec = (uint64_t*)(ws + L.tile_rec);
     a.group_bexcl = (uint64_t*)(ws + L.group_bexcl);
     a.group_prev = (int64_t*)(ws + L.group_prev);
@@ -307,6 +314,20 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
   return enqueue_extract(slices.data(), slices.size(), (uint32_t)num_tensors, true, out_idx,
                          out_val, capacity, d_count, d_tensor_offsets, workspace,
                          workspace_bytes, stream);
+}
+
+delta_status_t delta_count_changed_multi(const uint16_t* const* prev_ptrs,
+                                         const uint16_t* const* next_ptrs,
+                                         const uint64_t* numels, int32_t num_tensors,
+                                         uint64_t* d_count, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream) {
+  if (!d_count) return fail(DELTA_ERR_INVALID_ARG, "d_count is NULL");
+  std::vector<SliceIn> slices;
+  const delta_status_t st = list_slices(prev_ptrs, next_ptrs, numels, num_tensors, slices);
+  if (st != DELTA_OK) return st;
+  return enqueue_extract(slices.data(), slices.size(), (uint32_t)num_tensors, true, nullptr,
+                         nullptr, 0, d_count, nullptr, workspace, workspace_bytes, stream,
+                         nullptr, nullptr, true);
 }
 
 size_t delta_extract_multi_leb128_workspace_bytes(const uint64_t* numels, int32_t num_tensors) {

@@ -212,6 +212,10 @@ struct StageSplit {
 hipError_t launch_extract(const ExtractArgs& a, bool idx64, bool all_vec, hipStream_t stream,
                           const StageSplit* split = nullptr);
 
+// Count only: the scan and the tile counts, then the group sums and scan
+// that leave the total in *a.d_count; nothing is staged or written.
+hipError_t launch_count(const ExtractArgs& a, bool all_vec, hipStream_t stream);
+
 // The same extract with coded output: values to out_val, the gap + LEB128
 // code of the positions to code_out, *d_count and *d_nbytes.
 hipError_t launch_extract_coded(const ExtractArgs& a, bool all_vec, hipStream_t stream,
@@ -287,13 +291,14 @@ struct CodedOut {
 // has num_tensors + 1 entries.  With `coded`, out_idx, idx64 and d_offsets
 // are unused and the workspace follows the coded layout.  `split` as for
 // launch_extract (with nothing to read, split->rest still waits for the
-// launch stream).  Sets the error text on failure.
+// launch stream).  With `count_only`, only *d_count is written (outputs,
+// d_offsets, coded and split unused).  Sets the error text on failure.
 delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_t num_tensors,
                                bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
                                uint64_t* d_count, uint64_t* d_offsets, void* workspace,
                                size_t workspace_bytes, hipStream_t stream,
                                const CodedOut* coded = nullptr,
-                               const StageSplit* split = nullptr);
+                               const StageSplit* split = nullptr, bool count_only = false);
 
 // Delta chain composition (compose.hip): workspace layout for `K` deltas
 // of the given counts, and the enqueue of the whole chain on `stream`.

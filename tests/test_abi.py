@@ -134,6 +134,22 @@ def test_extract_multi_validation(lib):
                                    1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
 
 
+def test_count_changed_multi_validation(lib):
+    P = ctypes.c_void_p
+    prevs = (P * 2)(FAKE, FAKE)
+    nexts = (P * 2)(FAKE, None)
+    numels = (ctypes.c_uint64 * 2)(10, 10)
+    assert lib.delta_count_changed_multi(prevs, prevs, numels, 2, None, FAKE, 1 << 20,
+                                         None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_count_changed_multi(prevs, nexts, numels, 2, FAKE, FAKE, 1 << 20,
+                                         None) == _abi.DELTA_ERR_INVALID_ARG
+    assert b"tensor 1" in lib.delta_last_error()
+    assert lib.delta_count_changed_multi(prevs, prevs, numels, 2, FAKE, FAKE, 64,
+                                         None) == _abi.DELTA_ERR_WORKSPACE
+    assert lib.delta_count_changed_multi(prevs, prevs, numels, 2, FAKE, FAKE + 8, 1 << 20,
+                                         None) == _abi.DELTA_ERR_WORKSPACE
+
+
 def test_apply_chain_validation(lib):
     P = ctypes.c_void_p
     U = ctypes.c_uint64

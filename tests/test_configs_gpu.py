@@ -165,6 +165,7 @@ def test_weight_set(model, density):
     idx, val, offs = ad.delta_extract_multi(ws.prev, ws.new)
     torch.cuda.synchronize()
     check_set(ws, idx, val, offs, label)
+    assert ad.delta_count_changed_multi(ws.prev, ws.new) == ws.total_planted, label
     round_trip(ws, idx, val, label)
     buf, sb = leb128_full(ws, idx, val, offs, label)
     coded_full(ws, idx, val, offs, label, buf, sb)
