@@ -801,12 +801,18 @@ constexpr int kCodePer = 8;
 constexpr int kCodeWin = kThreads * kCodePer;
 constexpr int kCodeWinBytes = 2 * kCodeWin + kTilesPerGroup * 8;
 
+// Window entry j sits at win[wslot(j)]: one padding word after every
+// kCodePer entries, so that the threads of a wavefront, each walking its
+// own kCodePer consecutive entries, read different LDS banks.
+constexpr uint32_t kWinPad = 1;
+__device__ __forceinline__ uint32_t wslot(uint32_t j) { return kWinPad ? j + j / kCodePer : j; }
+
 struct CodedGroup {
   uint32_t begin[kTilesPerGroup + 1];   // first entry of each tile within the group, total
   uint32_t count[kTilesPerGroup];
   int64_t out_base[kTilesPerGroup];     // index of word 0 of each tile
   int64_t prev[kTilesPerGroup];         // index each tile's first entry is coded against
-  uint32_t win[kCodeWin];               // the window's entries, (word << 16) | offset
+  uint32_t win[kCodeWin + kCodeWin / kCodePer];   // the window's entries, (word << 16) | offset
   uint8_t code[kCodeWinBytes];
   uint32_t wave_total[kWaves];
   uint32_t last_off;                    // offset of the previous window's last entry
@@ -842,14 +848,14 @@ __device__ __forceinline__ void walk_gaps(const CodedGroup& sg, uint32_t e_lo, u
     if (sg.begin[mid] <= e_lo + j0) lo = mid; else hi = mid;
   }
   uint32_t ti = lo;
-  uint32_t prev_off = j0 > 0 ? (sg.win[j0 - 1] & 0xFFFFu) : sg.last_off;
+  uint32_t prev_off = j0 > 0 ? (sg.win[wslot(j0 - 1)] & 0xFFFFu) : sg.last_off;
 #pragma unroll
   for (int k = 0; k < kCodePer; ++k) {
     const uint32_t j = j0 + k;
     if (j < n) {
       const uint32_t e = e_lo + j;
       while (e >= sg.begin[ti + 1]) ++ti;
-      const uint32_t off = sg.win[j] & 0xFFFFu;
+      const uint32_t off = sg.win[wslot(j)] & 0xFFFFu;
       f(k, e == sg.begin[ti] ? (uint64_t)(sg.out_base[ti] + (int64_t)off - sg.prev[ti])
                              : (uint64_t)(off - prev_off));
       prev_off = off;
@@ -871,7 +877,7 @@ __device__ __forceinline__ uint32_t code_window(const ExtractArgs& a, CodedGroup
   if (j0 < n) walk_gaps(sg, e_lo, n, j0, [&](int, uint64_t gap) { sum += leb_bytes(gap); });
   // the window's words, one entry per thread in turn (coalesced stores)
   for (uint32_t j = threadIdx.x; j < n; j += kThreads)
-    if (eg + e_lo + j < a.capacity) a.out_val[eg + e_lo + j] = (uint16_t)(sg.win[j] >> 16);
+    if (eg + e_lo + j < a.capacity) a.out_val[eg + e_lo + j] = (uint16_t)(sg.win[wslot(j)] >> 16);
   const uint32_t incl = wave_incl_sum(sum, lane);
   if (lane == 63) sg.wave_total[wave] = incl;
   __syncthreads();
@@ -894,7 +900,7 @@ __device__ __forceinline__ uint32_t code_window(const ExtractArgs& a, CodedGroup
   const uint64_t at = bg + written;
   const uint64_t room = a.code_capacity > at ? a.code_capacity - at : 0;
   flush_code(sg.code, room < nb ? (uint32_t)room : nb, a.code_out + at);
-  if (threadIdx.x == 0) sg.last_off = sg.win[n - 1] & 0xFFFFu;
+  if (threadIdx.x == 0) sg.last_off = sg.win[wslot(n - 1)] & 0xFFFFu;
   __syncthreads();
   return nb;
 }
@@ -992,7 +998,7 @@ __global__ __launch_bounds__(kThreads, 6) void finalize_coded_kernel(ExtractArgs
 #pragma unroll
       for (int k = 0; k < kCodePer; ++k) {
         const uint32_t j = threadIdx.x + kThreads * k;
-        if (j < n) sg.win[j] = v[k];
+        if (j < n) sg.win[wslot(j)] = v[k];
       }
       __syncthreads();
       written += code_window(a, sg, w0, n, eg, bg, written);
@@ -1007,7 +1013,7 @@ __global__ __launch_bounds__(kThreads, 6) void finalize_coded_kernel(ExtractArgs
       const uint32_t* slot = a.stage + tile * a.stage_stride;
       for (uint32_t r0 = 0; r0 < c; r0 += kCodeWin) {
         const uint32_t n = c - r0 < (uint32_t)kCodeWin ? c - r0 : (uint32_t)kCodeWin;
-        for (uint32_t j = threadIdx.x; j < n; j += kThreads) sg.win[j] = slot[r0 + j];
+        for (uint32_t j = threadIdx.x; j < n; j += kThreads) sg.win[wslot(j)] = slot[r0 + j];
         __syncthreads();
         written += code_window(a, sg, sg.begin[i] + r0, n, eg, bg, written);
       }
@@ -1029,7 +1035,7 @@ __global__ __launch_bounds__(kThreads, 6) void finalize_coded_kernel(ExtractArgs
         while (m) {
           const int j = __builtin_ctz(m);
           m &= m - 1;
-          if (r >= r0 && r < r0 + n) sg.win[r - r0] = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
+          if (r >= r0 && r < r0 + n) sg.win[wslot(r - r0)] = ((uint32_t)word_of(s.q[u], j) << 16) | (w0 + j);
           ++r;
         }
       }
