@@ -73,6 +73,34 @@ def test_cfg1_single_tensor_int32():
     assert cnt == synth.planted_count(n, 0.01) == 41_943
 
 
+def test_int32_maximum_size():
+    """The largest tensor int32 indices can address: 2^31 words, changed at
+    both ends, next to both ends of a tile boundary and at random places.
+    Expected values: the oracle on host copies."""
+    n = 2 ** 31
+    prev = torch.zeros(n, dtype=torch.int16, device=DEV)
+    new = prev.clone()
+    r = np.random.default_rng(31)
+    pos = np.unique(np.concatenate([[0, 1, TILE - 1, TILE, n // 2, n - TILE - 1, n - 2, n - 1],
+                                    r.choice(n, size=5000, replace=False)]))
+    new[torch.from_numpy(pos).to(DEV)] = torch.from_numpy(
+        r.integers(1, 1 << 15, size=pos.size, dtype=np.int16)).to(DEV)
+    say("int32 maximum: planted", pos.size)
+    ref_idx, ref_val, ref_cnt = oracle.extract(host_u16(prev), host_u16(new), np.int32,
+                                               capacity=pos.size + 16)
+    assert ref_cnt == pos.size and ref_idx[-1] == n - 1
+    idx, val = ad.delta_extract(prev.view(torch.bfloat16), new.view(torch.bfloat16), torch.int32)
+    assert idx.dtype == torch.int32 and idx.numel() == ref_cnt
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
+    np.testing.assert_array_equal(host_u16(val), ref_val)
+    assert ad.delta_count_changed_multi([prev.view(torch.bfloat16)],
+                                        [new.view(torch.bfloat16)]) == ref_cnt
+    # apply at the same size: the old copy becomes the new one
+    w = prev.view(torch.bfloat16).clone()
+    ad.delta_apply(w, idx, val)
+    assert torch.equal(w.view(torch.int16), new)
+
+
 SIZES = [0, 1, 7, 8, 9, 63, 64, 65, 511, 512, 513, 2047, 2048, 2049,
          TILE - 1, TILE, TILE + 1, 3 * TILE + 77, 100_003]
 
