@@ -200,3 +200,39 @@ def test_apply_chain_graph_replays():
         torch.cuda.synchronize()
         assert int(flag.item()) == 0
         np.testing.assert_array_equal(np.concatenate([host_u16(x) for x in rollout]), flat)
+
+
+def test_count_changed_multi_graph_replays():
+    """The count-only pass captured once (tensor-table path): every replay
+    gives the oracle's count for the data it saw."""
+    sizes = [3000 + 17 * i for i in range(40)] + [70_001, 0, 8192 * 3 + 1]
+    prevs = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    news = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
+    fill_random(prevs, 5)
+    for p, q in zip(prevs, news):
+        q.copy_(p)
+    plan = ad.MultiPlan(prevs, news)
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    work = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        ad.delta_count_changed_multi_into(plan, cnt, work, stream=s)
+    s.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        ad.delta_count_changed_multi_into(plan, cnt, work, stream=s)
+    for rep, density in enumerate([0.01, 0.5, 0.0, 0.003]):
+        g = torch.Generator(device=DEV)
+        g.manual_seed(500 + rep)
+        for p, q in zip(prevs, news):
+            q.copy_(p)
+            m = torch.rand(q.shape, device=DEV, generator=g) < density
+            q.view(torch.int16)[m] ^= 0x0110
+        cnt.fill_(-1)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        want = sum(oracle.extract(host_u16(p), host_u16(q), capacity=0)[2]
+                   for p, q in zip(prevs, news))
+        assert int(cnt.item()) == want, rep
