@@ -142,6 +142,31 @@ delta_status_t delta_extract(const uint16_t* prev, const uint16_t* next, uint64_
                              uint64_t capacity, uint64_t* d_count, void* workspace,
                              size_t workspace_bytes, hipStream_t stream);
 
+/* Scratch bytes of delta_extract_noalloc (one array per GPU, held by the
+ * library until the process ends) and the largest numel it accepts. */
+#define DELTA_NOALLOC_SCRATCH_BYTES (32u << 20)
+#define DELTA_NOALLOC_MAX_WORDS (1ull << 27)
+
+/*
+ * delta_extract_noalloc — for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): delta_extract with no workspace argument.  Its scratch is a
+ * fixed device array of DELTA_NOALLOC_SCRATCH_BYTES inside the library, one
+ * per GPU, whose address the first call on each GPU looks up (make that
+ * first call outside graph capture).  No call allocates memory.
+ *   prev, next, numel, index_type, out_idx, out_val, capacity, d_count,
+ *   stream        as delta_extract; outputs and results are identical.
+ * numel above DELTA_NOALLOC_MAX_WORDS (2^27 words, 256 MiB per copy) is
+ * refused with DELTA_ERR_WORKSPACE before anything is enqueued.  Every call
+ * on one GPU shares that GPU's array, which keeps the last call's contents
+ * (nothing in it needs to start at zero): calls that overlap in time on one
+ * GPU (other streams, other threads) race and give wrong results; enqueue
+ * them on one stream.
+ */
+delta_status_t delta_extract_noalloc(const uint16_t* prev, const uint16_t* next, uint64_t numel,
+                                     delta_index_t index_type, void* out_idx, uint16_t* out_val,
+                                     uint64_t capacity, uint64_t* d_count, hipStream_t stream);
+
 /*
  * delta_extract_multi — Sec. 5.1, a tensor list in one index space.
  *   prev_ptrs, next_ptrs, numels

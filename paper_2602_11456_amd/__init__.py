@@ -24,7 +24,8 @@ import torch
 from . import _abi
 
 __all__ = [
-    "DeltaError", "library", "delta_extract", "delta_extract_into", "delta_extract_multi",
+    "DeltaError", "library", "delta_extract", "delta_extract_into", "delta_extract_noalloc_into",
+    "delta_extract_multi",
     "delta_extract_multi_into", "delta_count_changed_multi", "delta_count_changed_multi_into",
     "delta_apply", "delta_apply_multi", "delta_apply_checked",
     "delta_extract_pipelined", "delta_extract_workspace_bytes",
@@ -142,6 +143,22 @@ def delta_extract_into(prev: torch.Tensor, new: torch.Tensor, out_idx: torch.Ten
         _words(prev, "prev"), _words(new, "new"), prev.numel(), _index_type(out_idx.dtype),
         out_idx.data_ptr(), _words(out_val, "out_val"), cap, d_count.data_ptr(),
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def delta_extract_noalloc_into(prev: torch.Tensor, new: torch.Tensor, out_idx: torch.Tensor,
+                               out_val: torch.Tensor, d_count: torch.Tensor,
+                               stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Enqueue ``delta_extract_noalloc``: :func:`delta_extract_into` without a
+    workspace (the library's fixed per-GPU scratch array is used; at most
+    ``_abi.DELTA_NOALLOC_MAX_WORDS`` words).  Calls that overlap in time on
+    one GPU race; enqueue them on one stream."""
+    if prev.shape != new.shape:
+        raise ValueError("prev and new differ in shape")
+    cap = min(out_idx.numel(), out_val.numel())
+    _check(library().delta_extract_noalloc(
+        _words(prev, "prev"), _words(new, "new"), prev.numel(), _index_type(out_idx.dtype),
+        out_idx.data_ptr(), _words(out_val, "out_val"), cap, d_count.data_ptr(),
+        _stream(stream)))
 
 
 def _default_capacity(n: int) -> int:

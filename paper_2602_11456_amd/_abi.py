@@ -25,6 +25,10 @@ DELTA_INDEX_I64 = 1
 
 ABI_VERSION = 1
 
+# delta_extract_noalloc's fixed scratch and largest input
+DELTA_NOALLOC_SCRATCH_BYTES = 32 << 20
+DELTA_NOALLOC_MAX_WORDS = 1 << 27
+
 P = ctypes.c_void_p
 U64 = ctypes.c_uint64
 I32 = ctypes.c_int32
@@ -74,6 +78,7 @@ SIGNATURES = {
     "delta_extract_multi_workspace_bytes": (SZ, [P, I32]),
     "delta_apply_multi_workspace_bytes": (SZ, [I32]),
     "delta_extract": (STATUS, [P, P, U64, ctypes.c_int, P, P, U64, P, P, SZ, P]),
+    "delta_extract_noalloc": (STATUS, [P, P, U64, ctypes.c_int, P, P, U64, P, P]),
     "delta_extract_multi": (STATUS, [P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
     "delta_count_changed_multi": (STATUS, [P, P, P, I32, P, P, SZ, P]),
     "delta_extract_fused": (STATUS, [P, P, P, I32, P, P, P, I32, P, P, U64, P, P, P, SZ, P]),

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -274,10 +275,13 @@ size_t delta_apply_multi_workspace_bytes(int32_t num_tensors) {
   return align_up(8 * ((size_t)num_tensors + 1)) + align_up(8 * (size_t)num_tensors);
 }
 
-delta_status_t delta_extract(const uint16_t* prev, const uint16_t* next, uint64_t numel,
-                             delta_index_t index_type, void* out_idx, uint16_t* out_val,
-                             uint64_t capacity, uint64_t* d_count, void* workspace,
-                             size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+// Argument checks of delta_extract and delta_extract_noalloc (no HIP call).
+static delta_status_t check_extract_args(const uint16_t* prev, const uint16_t* next,
+                                         uint64_t numel, delta_index_t index_type,
+                                         void* out_idx, uint16_t* out_val, uint64_t capacity,
+                                         uint64_t* d_count) {
   if (index_type != DELTA_INDEX_I32 && index_type != DELTA_INDEX_I64)
     return fail(DELTA_ERR_INVALID_ARG, "unknown index type %d", (int)index_type);
   if (!d_count) return fail(DELTA_ERR_INVALID_ARG, "d_count is NULL");
@@ -291,9 +295,93 @@ delta_status_t delta_extract(const uint16_t* prev, const uint16_t* next, uint64_
   if (index_type == DELTA_INDEX_I32 && numel > 0 && numel - 1 > 0x7FFFFFFFull)
     return fail(DELTA_ERR_INDEX_OVERFLOW, "numel %llu needs int64 indices",
                 (unsigned long long)numel);
+  return DELTA_OK;
+}
+
+extern "C" {
+
+delta_status_t delta_extract(const uint16_t* prev, const uint16_t* next, uint64_t numel,
+                             delta_index_t index_type, void* out_idx, uint16_t* out_val,
+                             uint64_t capacity, uint64_t* d_count, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  const delta_status_t s =
+      check_extract_args(prev, next, numel, index_type, out_idx, out_val, capacity, d_count);
+  if (s != DELTA_OK) return s;
   const SliceIn slice{prev, next, numel, 0, 0, 0};
   return enqueue_extract(&slice, 1, 1, index_type == DELTA_INDEX_I64, out_idx, out_val, capacity,
                          d_count, nullptr, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+// ----------------------------------------------- extract without allocation
+//
+// delta_extract_noalloc keeps its scratch (tile counts, group sums, staging
+// slots) in this file-scope device array instead of a caller workspace.
+// Every GPU the library runs on holds its own copy, at its own address,
+// until the process ends.  Host code never passes `noalloc_scratch` itself
+// to a kernel (in host code the name is only a stand-in for the symbol):
+// the device address comes from hipGetSymbolAddress, resolved once per
+// device with that device current, and kept in g_noalloc_ptr.  Nothing in
+// the array has to start at zero: the extract writes every tile count and
+// group sum it later reads.
+static __device__ __align__(256) unsigned char noalloc_scratch[DELTA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_noalloc_mu;
+void* g_noalloc_ptr[kMaxDevices] = {};
+
+// Device address of `noalloc_scratch` on the device that runs `stream`.
+delta_status_t noalloc_scratch_for(hipStream_t stream, void** out) {
+  int dev = -1;
+  hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "device of the stream");
+  if (dev < 0 || dev >= kMaxDevices) return fail(DELTA_ERR_HIP, "device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  if (!g_noalloc_ptr[dev]) {
+    int cur = -1;
+    e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    if (e != hipSuccess) return hip_fail(e, "select the stream's device");
+    void* p = nullptr;
+    const hipError_t es = hipGetSymbolAddress(&p, HIP_SYMBOL(noalloc_scratch));
+    if (cur != dev) e = hipSetDevice(cur);
+    if (es != hipSuccess) return hip_fail(es, "hipGetSymbolAddress(noalloc_scratch)");
+    if (e != hipSuccess) return hip_fail(e, "restore the current device");
+    if (!p || (uintptr_t)p % kAlign)
+      return fail(DELTA_ERR_HIP, "scratch array at %p is not %zu-byte aligned", p, kAlign);
+    g_noalloc_ptr[dev] = p;
+  }
+  *out = g_noalloc_ptr[dev];
+  return DELTA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+delta_status_t delta_extract_noalloc(const uint16_t* prev, const uint16_t* next, uint64_t numel,
+                                     delta_index_t index_type, void* out_idx, uint16_t* out_val,
+                                     uint64_t capacity, uint64_t* d_count, hipStream_t stream) {
+  delta_status_t s =
+      check_extract_args(prev, next, numel, index_type, out_idx, out_val, capacity, d_count);
+  if (s != DELTA_OK) return s;
+  if (numel > DELTA_NOALLOC_MAX_WORDS)
+    return fail(DELTA_ERR_WORKSPACE,
+                "delta_extract_noalloc: numel %llu exceeds its maximum of %llu words (use "
+                "delta_extract with a workspace)",
+                (unsigned long long)numel, (unsigned long long)DELTA_NOALLOC_MAX_WORDS);
+  void* ws = nullptr;
+  if (numel > 0) {
+    s = noalloc_scratch_for(stream, &ws);
+    if (s != DELTA_OK) return s;
+  }
+  const SliceIn slice{prev, next, numel, 0, 0, 0};
+  return enqueue_extract(&slice, 1, 1, index_type == DELTA_INDEX_I64, out_idx, out_val, capacity,
+                         d_count, nullptr, ws, numel > 0 ? (size_t)DELTA_NOALLOC_SCRATCH_BYTES : 0,
+                         stream);
 }
 
 delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,

@@ -115,6 +115,26 @@ def test_extract_validation(lib):
         _abi.DELTA_ERR_INVALID_ARG
 
 
+def test_extract_noalloc_validation(lib):
+    cnt = FAKE
+    big = _abi.DELTA_NOALLOC_MAX_WORDS + 1
+    # above the fixed scratch's maximum: refused before anything is enqueued
+    assert lib.delta_extract_noalloc(FAKE, FAKE, big, _abi.DELTA_INDEX_I64, FAKE, FAKE, 10, cnt,
+                                     None) == _abi.DELTA_ERR_WORKSPACE
+    assert b"maximum" in lib.delta_last_error()
+    # the argument checks of delta_extract come first
+    assert lib.delta_extract_noalloc(FAKE, FAKE, 10, 0, FAKE, FAKE, 10, None, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_extract_noalloc(FAKE, FAKE, 10, 7, FAKE, FAKE, 10, cnt, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_extract_noalloc(FAKE + 1, FAKE, 10, 0, FAKE, FAKE, 10, cnt, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_extract_noalloc(FAKE, FAKE, 10, _abi.DELTA_INDEX_I64, FAKE + 4, FAKE, 10,
+                                     cnt, None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_extract_noalloc(FAKE, FAKE, 10, 0, None, FAKE, 10, cnt, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
+
+
 def test_extract_multi_validation(lib):
     P = ctypes.c_void_p
     prevs = (P * 2)(FAKE, FAKE)
