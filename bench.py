@@ -32,6 +32,7 @@ METRIC = "delta extract GB/s scanned (% of HBM peak) + apply GB/s, Qwen3-8B shap
 HBM_PEAK_GBPS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "extract_qwen3-8b_traffic.json")
+CEILINGS_PROBE = os.path.join(ROOT, "paper_2602_11456_amd", "probes", "ceilings")
 
 
 def log(*a):
@@ -56,6 +57,11 @@ def parse():
                     help="skip the chunked extract -> pinned host pipeline measurement "
                          "(Qwen3-14B-shaped set)")
     ap.add_argument("--pipeline-reps", type=int, default=5)
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the write-ceiling probe of apply")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the other weight sets (Qwen3-8B at 0.1%% and 10%%, clustered, "
+                         "Qwen3-4B)")
     ap.add_argument("--only-pipeline", action="store_true",
                     help="measure only the pipelines on the Qwen3-14B-shaped set and print "
                          "their figures (for profiling; not the benchmark line)")
@@ -69,56 +75,156 @@ def parse():
 
 
 def kernel_source_digest():
-    """Digest of the extract kernels' sources: stored traffic figures are
-    only used while the kernels they were measured on are unchanged."""
+    """Digest of the extract and apply kernels' sources: stored traffic
+    figures are only used while the kernels they were measured on are
+    unchanged."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("extract.hip", "delta_internal.h"):
+    for f in ("extract.hip", "delta_internal.h", "apply.hip"):
         with open(os.path.join(ROOT, "paper_2602_11456_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
+def measure_ceilings():
+    """The scatter's write ceilings on this device, from the measurement
+    probe (paper_2602_11456_amd/probes/ceilings.hip, built with the
+    library): partial and full 64-byte line writes per second at the
+    spacing of a 1% delta over the Qwen3-8B set's size, with no loads.  Run
+    as a child process before this process touches the GPU."""
+    import subprocess
+    if not os.path.exists(CEILINGS_PROBE):
+        return {"error": f"{CEILINGS_PROBE} is not built (run __graft_entry__.build())"}
+    try:
+        r = subprocess.run([CEILINGS_PROBE], capture_output=True, text=True, timeout=120)
+    except subprocess.TimeoutExpired:
+        return {"error": "the ceilings probe timed out"}
+    if r.returncode != 0:
+        return {"error": f"the ceilings probe failed ({r.returncode}): {r.stderr.strip()[-300:]}"}
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
+def touched_lines(weights, idx, numels):
+    """Distinct 64-byte lines of the weight tensors that a delta's entries
+    fall in (counted with torch on the GPU, outside any timed region): the
+    fewest write transactions a scatter of the delta can issue."""
+    import itertools
+    import torch
+    if idx.numel() == 0:
+        return 0
+    dev = idx.device
+    bases = torch.tensor([0] + list(itertools.accumulate(numels))[:-1], dtype=torch.int64,
+                         device=dev)
+    ptrs = torch.tensor([w.data_ptr() for w in weights], dtype=torch.int64, device=dev)
+    t = torch.searchsorted(bases, idx, right=True) - 1
+    line = (ptrs[t] + 2 * (idx - bases[t])) >> 6
+    del t
+    return int((line[1:] != line[:-1]).sum().item()) + 1
+
+
+def cpu_info():
+    """CPU model (from /proc/cpuinfo) and the cores this process may run on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count() or 1
+    return model, nproc
+
+
 def cpu_baseline(ws, budget_s, reps=4):
-    """The CPU oracle on the same set, tensor by tensor, each tensor scanned
-    `reps` times back to back while its host copy is resident (the copies
-    are not timed), until the time budget is used: GB/s scanned over the
-    words it processed."""
+    """The CPU oracle on the same weight set, timed on the host's cores.
+
+    Single thread: tensor by tensor, each scanned ``reps`` times back to
+    back while its host copy is resident, for half the budget.  All cores:
+    the threaded oracle (contiguous per-thread ranges, concatenated in
+    order) over batches of whole tensors of about 2 G words, each batch
+    scanned ``reps`` times, for the other half.  Host copies are not timed.
+    GB/s scanned = 4 bytes per word over the oracle's own time."""
     import numpy as np
     import torch
     import oracle
 
     oracle.build(force=False)
-    words = 0
-    spent = 0.0
-    tensors = 0
+    model, nproc = cpu_info()
+    threads = int(os.environ.get("OMP_NUM_THREADS") or 0) or nproc
+    threads = max(1, min(threads, nproc))
+
+    def host(t):
+        return t.view(torch.int16).reshape(-1).cpu().numpy().view(np.uint16)
+
+    # single thread
+    words1 = 0
+    spent1 = 0.0
+    tensors1 = 0
     for p, q, k in zip(ws.prev, ws.new, ws.planted):
-        hp = p.view(torch.int16).reshape(-1).cpu().numpy().view(np.uint16)
-        hq = q.view(torch.int16).reshape(-1).cpu().numpy().view(np.uint16)
+        hp, hq = host(p), host(q)
         for _ in range(reps):
             t0 = time.perf_counter()
             _, _, cnt = oracle.extract(hp, hq, np.int64, capacity=k)
-            spent += time.perf_counter() - t0
-            words += hp.size
+            spent1 += time.perf_counter() - t0
+            words1 += hp.size
             if cnt != k:
                 raise RuntimeError(f"oracle found {cnt} changed words, {k} planted")
-        tensors += 1
-        if spent >= budget_s:
+        tensors1 += 1
+        if spent1 >= budget_s / 2:
             break
+    # all cores, batches of whole tensors
+    wordsm = 0
+    spentm = 0.0
+    tensorsm = 0
+    batch_words = 2 << 30
+    i = 0
+    T = len(ws.prev)
+    while i < T and spentm < budget_s / 2:
+        j, n = i, 0
+        while j < T and (j == i or n + ws.prev[j].numel() <= batch_words):
+            n += ws.prev[j].numel()
+            j += 1
+        hps = [host(p) for p in ws.prev[i:j]]
+        hqs = [host(q) for q in ws.new[i:j]]
+        k = sum(ws.planted[i:j])
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            _, _, _, cnt = oracle.extract_multi(hps, hqs, capacity=k, threads=threads)
+            spentm += time.perf_counter() - t0
+            wordsm += n
+            if cnt != k:
+                raise RuntimeError(f"threaded oracle found {cnt} changed words, {k} planted")
+        del hps, hqs
+        tensorsm += j - i
+        i = j
+    single = 4 * words1 / spent1 / 1e9
+    multi = 4 * wordsm / spentm / 1e9
     return {
-        "value": round(4 * words / spent / 1e9, 3),
+        "value": round(multi, 3),
         "unit": "GB/s",
-        "cores": 1,
+        "cores": threads,
         "kind": "oracle",
-        "sample": f"first {tensors} of {len(ws.prev)} tensors of the same weight set, each "
-                  f"scanned {reps} times ({words} words, {4 * words / 1e9:.2f} GB scanned) in "
-                  f"{spent:.1f} s, single-threaded C loop",
+        "sample": f"threaded oracle on {threads} threads: the first {tensorsm} of {T} tensors "
+                  f"of the same weight set in batches of up to {batch_words} words, each batch "
+                  f"scanned {reps} times ({wordsm} words, {4 * wordsm / 1e9:.1f} GB) in "
+                  f"{spentm:.1f} s; single-threaded C loop: the first {tensors1} tensors, each "
+                  f"scanned {reps} times ({4 * words1 / 1e9:.1f} GB) in {spent1:.1f} s",
+        "single_thread_GBps": round(single, 3),
+        "all_cores_GBps": round(multi, 3),
+        "nproc": nproc,
+        "cpu_model": model,
     }
 
 
 def pipeline_measurement(args, dev):
-    """Chunked extract -> pinned host memory over 4 HIP streams on the
-    Qwen3-14B-shaped set at 1% (2^27-word chunks), host-synchronous calls
+    """Chunked extract -> pinned host memory with 4 HIP streams passed (3
+    of them busy: reading, finishing, delivering) on the Qwen3-14B-shaped
+    set at 1% (2^27-word chunks), host-synchronous calls
     over a tensor plan built once (as a training loop keeps its weights)
     timed with the wall clock, next to a pinned device-to-host copy of the
     same number of bytes (the host-link ceiling)."""
@@ -183,8 +289,12 @@ def pipeline_measurement(args, dev):
     coded_bytes = b.numel() + 2 * K
     return {
         "workload": f"qwen3-14b weight set, {len(ws.prev)} tensors, {ws.total} bf16 words, "
-                    f"{args.density:.2%} changed, {chunk}-word chunks over {nstreams} streams "
-                    "into pinned host memory",
+                    f"{args.density:.2%} changed, {chunk}-word chunks, {nstreams} streams passed "
+                    "of which 3 carry work (one reads every chunk, one finishes each read "
+                    "chunk, one delivers into pinned host memory; a process has 4 hardware "
+                    "queues, and more busy streams would share them and serialise)",
+        "streams_passed": nstreams,
+        "streams_busy": min(nstreams, 3),
         "ms": round(t * 1e3, 3),
         "GBps_scanned": round(4 * ws.total / t / 1e9, 1),
         "d2h_GBps": round(out_bytes / t / 1e9, 2),
@@ -571,6 +681,64 @@ def count_measurement(ad, lib, plan, work, stream, reps, K, scanned, stage_ms):
     }
 
 
+def sweep_measurement(ad, synth, dev, stream, reps):
+    """The other weight sets of the benchmark suite beside the headline:
+    the Qwen3-8B set at 0.1% and 10% density, the clustered Qwen3-8B set
+    (80% of the changes in 5% of the rows) and the Qwen3-4B set, each
+    extracted (delta_extract_multi, int64 global indices) and applied
+    (delta_apply_multi) ``reps`` times after one warm-up, HIP events around
+    every call; the count and the applied rollout are checked."""
+    import torch
+    out = {}
+    cases = [("qwen3-8b_d0.1pct", "qwen3-8b", 0.001, False, 3),
+             ("qwen3-8b_d10pct", "qwen3-8b", 0.10, False, 3),
+             ("qwen3-8b_clustered", "qwen3-8b", 0.01, True, 4),
+             ("qwen3-4b", "qwen3-4b", 0.01, False, 2)]
+    for key, model, density, clustered, cfg in cases:
+        ws = synth.make_weight_set(model, density, seed=synth.config_seed(cfg), device=dev,
+                                   clustered=clustered)
+        N, Kp = ws.total, ws.total_planted
+        plan = ad.MultiPlan(ws.prev, ws.new)
+        out_idx = torch.empty(Kp + 1024, dtype=torch.int64, device=dev)
+        out_val = torch.empty(Kp + 1024, dtype=torch.bfloat16, device=dev)
+        cnt = torch.zeros(1, dtype=torch.int64, device=dev)
+        work = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=dev)
+        roll = [p.clone() for p in ws.prev]
+        aws = torch.empty(max(ad.delta_apply_multi_workspace_bytes(plan.T), 1),
+                          dtype=torch.uint8, device=dev)
+        ad.delta_extract_multi_into(plan, out_idx, out_val, cnt, work, None, stream)
+        torch.cuda.synchronize()
+        K = int(cnt.item())
+        if K != Kp:
+            raise RuntimeError(f"{key}: extract found {K} changed words, {Kp} planted")
+        ad.delta_apply_multi(roll, out_idx[:K], out_val[:K], workspace=aws, stream=stream)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+        for e0, e1, e2 in ev:
+            e0.record(stream)
+            ad.delta_extract_multi_into(plan, out_idx, out_val, cnt, work, None, stream)
+            e1.record(stream)
+            ad.delta_apply_multi(roll, out_idx[:K], out_val[:K], workspace=aws, stream=stream)
+            e2.record(stream)
+        torch.cuda.synchronize()
+        for r, q in zip(roll, ws.new):
+            if not torch.equal(r.view(torch.int16), q.view(torch.int16)):
+                raise RuntimeError(f"{key}: rollout differs from the updated weights")
+        med = lambda xs: sorted(xs)[len(xs) // 2]
+        te = med([a.elapsed_time(b) for a, b, _ in ev])
+        ta = med([b.elapsed_time(c) for _, b, c in ev])
+        alg = 4 * N + 10 * K
+        out[key] = {"words": N, "changed": K, "extract_ms": round(te, 4),
+                    "extract_GBps_scanned": round(4 * N / (te / 1e3) / 1e9, 1),
+                    "extract_pct_hbm_peak": round(100 * alg / (te / 1e3) / 1e9 / HBM_PEAK_GBPS, 2),
+                    "apply_ms": round(ta, 4),
+                    "apply_GBps_algorithmic": round(12 * K / (ta / 1e3) / 1e9, 1),
+                    "apply_changed_words_per_s": round(K / (ta / 1e3), 1)}
+        log(f"{key}: extract {te:.3f} ms, apply {ta:.3f} ms")
+        del ws, plan, out_idx, out_val, work, roll
+        torch.cuda.empty_cache()
+    return out
+
+
 def torch_reference_measurement(ws, reps=3):
     """Informational: the same extract written with torch operations only
     (compare, nonzero, gather per tensor; nonzero waits for the host), not
@@ -620,6 +788,11 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the hot path has no multi-GPU form in this library)", file=sys.stderr)
         return 2
+
+    # the probe runs first, in a process of its own, before this one touches the GPU
+    ceilings = None if args.no_ceilings else measure_ceilings()
+    if ceilings is not None:
+        log(f"write ceilings: {ceilings}")
 
     import torch
     import paper_2602_11456_amd as ad
@@ -736,6 +909,20 @@ def main():
     scan_avg = sum(scan_ms) / len(scan_ms)
     scan_achieved = scanned / (scan_avg / 1e3) / 1e9
 
+    lines = touched_lines(rollout, out_idx[:K], plan.numels)
+    apply_traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            rec = json.load(f)
+        if rec.get("kernel_source_sha256") == kernel_source_digest():
+            for name, k in rec.get("kernels", {}).items():
+                if "apply_multi_kernel" in name:
+                    apply_traffic = round(k["bytes_per_dispatch"])
+    ceiling = (ceilings["partial_line_writes_per_s"]
+               if ceilings and "partial_line_writes_per_s" in ceilings else None)
+    app_s = app_avg / 1e3
+    apply_achieved = apply_bytes / app_s / 1e9
+
     ext_sorted = sorted(ext_ms)
     result = {
         "metric": METRIC,
@@ -772,8 +959,27 @@ def main():
         },
         "apply": {
             "ms": round(app_avg, 4),
-            "GBps_algorithmic": round(apply_bytes / (app_avg / 1e3) / 1e9, 2),
-            "changed_words_per_s": round(K / (app_avg / 1e3), 1),
+            "GBps_algorithmic": round(apply_achieved, 2),
+            "changed_words_per_s": round(K / app_s, 1),
+            "roofline": {
+                "kernel": "apply_multi_kernel (scattered 2-byte stores)",
+                "bound": "hbm",
+                "achieved": round(apply_achieved, 2),
+                "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s",
+                "frac": round(apply_achieved / HBM_PEAK_GBPS, 4),
+                "traffic": apply_traffic,
+                "algorithmic_bytes": apply_bytes,
+                "lines_touched": lines,
+                "line_writes_per_s": round(lines / app_s, 1),
+                "ceiling_line_writes_per_s": ceiling,
+                "frac_of_ceiling": round(lines / app_s / ceiling, 4) if ceiling else None,
+                "ceilings_probe": ceilings,
+                "note": "each touched 64-byte line costs one partial-line write at the memory; "
+                        "the ceiling is the rate of such writes with no loads at all, measured "
+                        "in this run by paper_2602_11456_amd/probes/ceilings (full-line writes "
+                        "are faster, but making a line full needs its old words: a read)",
+            },
         },
         "roofline": {
             "kernel": "stage_kernel (reads and compares both copies)",
@@ -812,11 +1018,14 @@ def main():
         del src, dst
     if not args.no_cpu_baseline:
         del rollout
-        result["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
-    if not args.no_pipeline:
-        del ws, plan, out_idx, out_val, work
         rollout = None
-        torch.cuda.empty_cache()
+        result["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
+    del ws, plan, out_idx, out_val, work
+    rollout = None
+    torch.cuda.empty_cache()
+    if not args.no_sweep:
+        result["sweep"] = sweep_measurement(ad, synth, dev, stream, 5)
+    if not args.no_pipeline:
         result["pipeline"] = pipeline_measurement(args, dev)
     print(json.dumps(result), flush=True)
     return 0

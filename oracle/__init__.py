@@ -38,7 +38,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
         subprocess.check_call(
-            ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fPIC", "-shared",
+            ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fPIC", "-shared", "-pthread",
              _SRC, "-o", tmp])
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
@@ -60,6 +60,9 @@ def _load():
         f.restype = U64
     lib.oracle_extract_multi.argtypes = [P, P, P, ctypes.c_int32, P, P, U64, P]
     lib.oracle_extract_multi.restype = U64
+    lib.oracle_extract_multi_threaded.argtypes = [P, P, P, ctypes.c_int32, P, P, U64, P,
+                                                  ctypes.c_int32]
+    lib.oracle_extract_multi_threaded.restype = U64
     for name in ("oracle_apply_i64", "oracle_apply_i32"):
         f = getattr(lib, name)
         f.argtypes = [P, U64, P, P, U64]
@@ -122,10 +125,13 @@ def extract(prev, new, index_dtype=np.int64, capacity=None):
     return idx[:w].copy(), val[:w].copy(), int(cnt)
 
 
-def extract_multi(prevs, news, capacity=None):
+def extract_multi(prevs, news, capacity=None, threads=1):
     """Global-index extract over a tensor list; Sec. 5.1 block offsets.
 
-    Returns ``(idx_int64, val, tensor_offsets[T+1], count)``.
+    Returns ``(idx_int64, val, tensor_offsets[T+1], count)``.  With
+    ``threads`` > 1 the same result comes from the threaded form (contiguous
+    per-thread ranges, concatenated in order), used to time the CPU on all
+    its cores.
     """
     lib = _load()
     ps = [_u16(a) for a in prevs]
@@ -144,10 +150,18 @@ def extract_multi(prevs, news, capacity=None):
     idx = np.empty(max(cap, 1), dtype=np.int64)
     val = np.empty(max(cap, 1), dtype=np.uint16)
     offs = np.empty(T + 1, dtype=np.uint64)
-    cnt = lib.oracle_extract_multi(ctypes.cast(pp, ctypes.c_void_p),
-                                   ctypes.cast(qq, ctypes.c_void_p),
-                                   _ptr(numels), T, _ptr(idx), _ptr(val), cap,
-                                   _ptr(offs))
+    if int(threads) > 1:
+        cnt = lib.oracle_extract_multi_threaded(ctypes.cast(pp, ctypes.c_void_p),
+                                                ctypes.cast(qq, ctypes.c_void_p),
+                                                _ptr(numels), T, _ptr(idx), _ptr(val), cap,
+                                                _ptr(offs), int(threads))
+        if cnt == U64_MAX:
+            raise MemoryError("threaded oracle: a thread or its memory could not be had")
+    else:
+        cnt = lib.oracle_extract_multi(ctypes.cast(pp, ctypes.c_void_p),
+                                       ctypes.cast(qq, ctypes.c_void_p),
+                                       _ptr(numels), T, _ptr(idx), _ptr(val), cap,
+                                       _ptr(offs))
     w = min(cnt, cap)
     return idx[:w].copy(), val[:w].copy(), offs, int(cnt)
 

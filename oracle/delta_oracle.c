@@ -50,6 +50,7 @@
  * when it exceeds the caller's capacity, and only the first `capacity`
  * entries are written.
  */
+#include <pthread.h>
 #include <stdint.h>
 #include <stddef.h>
 #include <stdlib.h>
@@ -130,6 +131,146 @@ uint64_t oracle_extract_multi(const uint16_t *const *prevs,
     if (tensor_offsets)
         tensor_offsets[num_tensors] = count;
     return count;
+}
+
+/* ------------------------------------------------------------------ */
+/* extract_multi on several host threads (CPU baseline timing only)     */
+/* ------------------------------------------------------------------ */
+
+/* One thread's share: the global index range [lo, hi) scanned with the
+ * plain loop of oracle_extract_multi into a list of its own, and the
+ * number of its entries in each tensor. */
+struct oracle_range_job {
+    const uint16_t *const *prevs;
+    const uint16_t *const *nexts;
+    const uint64_t *numels;
+    int32_t num_tensors;
+    uint64_t lo, hi;
+    int64_t *idx;
+    uint16_t *val;
+    uint64_t count, room;
+    uint64_t *tensor_counts;
+    int failed;
+};
+
+static void *oracle_range_scan(void *arg)
+{
+    struct oracle_range_job *j = (struct oracle_range_job *)arg;
+    uint64_t base = 0;
+    for (int32_t t = 0; t < j->num_tensors; ++t) {
+        const uint64_t n = j->numels[t];
+        if (j->hi > base && j->lo < base + n) {
+            const uint64_t a = j->lo > base ? j->lo - base : 0;
+            const uint64_t b = j->hi < base + n ? j->hi - base : n;
+            const uint16_t *p = j->prevs[t];
+            const uint16_t *q = j->nexts[t];
+            for (uint64_t i = a; i < b; ++i) {
+                if (p[i] != q[i]) {
+                    if (j->count == j->room) {
+                        const uint64_t room = j->room ? 2 * j->room : 4096;
+                        int64_t *ni = (int64_t *)realloc(j->idx, room * sizeof(int64_t));
+                        if (ni) j->idx = ni;
+                        uint16_t *nv = (uint16_t *)realloc(j->val, room * sizeof(uint16_t));
+                        if (nv) j->val = nv;
+                        if (!ni || !nv) {
+                            j->failed = 1;
+                            return NULL;
+                        }
+                        j->room = room;
+                    }
+                    j->idx[j->count] = (int64_t)(base + i);
+                    j->val[j->count] = q[i];
+                    ++j->count;
+                    ++j->tensor_counts[t];
+                }
+            }
+        }
+        base += n;
+    }
+    return NULL;
+}
+
+/* The result of oracle_extract_multi, computed by `num_threads` POSIX
+ * threads for timing the CPU on all its cores: the global index space is
+ * cut into num_threads contiguous ranges of equal size, every thread runs
+ * the plain loop over its range into its own list, and the lists are
+ * concatenated in range order (the ranges are disjoint and ascending, so
+ * this is the definition's sorted list).  At most 256 threads are used.
+ * Returns UINT64_MAX if a thread or its memory could not be had. */
+uint64_t oracle_extract_multi_threaded(const uint16_t *const *prevs,
+                                       const uint16_t *const *nexts,
+                                       const uint64_t *numels, int32_t num_tensors,
+                                       int64_t *idx, uint16_t *val, uint64_t capacity,
+                                       uint64_t *tensor_offsets, int32_t num_threads)
+{
+    if (num_threads < 1)
+        num_threads = 1;
+    if (num_threads > 256)
+        num_threads = 256;
+    uint64_t total = 0;
+    for (int32_t t = 0; t < num_tensors; ++t)
+        total += numels[t];
+    const size_t T = num_tensors > 0 ? (size_t)num_tensors : 1;
+    struct oracle_range_job *jobs =
+        (struct oracle_range_job *)calloc((size_t)num_threads, sizeof(*jobs));
+    pthread_t *tids = (pthread_t *)calloc((size_t)num_threads, sizeof(pthread_t));
+    char *started = (char *)calloc((size_t)num_threads, 1);
+    uint64_t *tcounts = (uint64_t *)calloc((size_t)num_threads * T, sizeof(uint64_t));
+    uint64_t result = UINT64_MAX;
+    if (!jobs || !tids || !started || !tcounts)
+        goto done;
+    for (int32_t r = 0; r < num_threads; ++r) {
+        struct oracle_range_job *j = &jobs[r];
+        j->prevs = prevs;
+        j->nexts = nexts;
+        j->numels = numels;
+        j->num_tensors = num_tensors;
+        j->lo = (uint64_t)((unsigned __int128)total * (uint64_t)r / (uint64_t)num_threads);
+        j->hi = (uint64_t)((unsigned __int128)total * (uint64_t)(r + 1) / (uint64_t)num_threads);
+        j->tensor_counts = tcounts + (size_t)r * T;
+        if (pthread_create(&tids[r], NULL, oracle_range_scan, j) != 0)
+            goto join;
+        started[r] = 1;
+    }
+join:
+    for (int32_t r = 0; r < num_threads; ++r)
+        if (started[r])
+            pthread_join(tids[r], NULL);
+    for (int32_t r = 0; r < num_threads; ++r)
+        if (!started[r] || jobs[r].failed)
+            goto done;
+    /* concatenate in range order */
+    uint64_t count = 0;
+    for (int32_t r = 0; r < num_threads; ++r) {
+        for (uint64_t k = 0; k < jobs[r].count; ++k) {
+            if (count < capacity) {
+                idx[count] = jobs[r].idx[k];
+                val[count] = jobs[r].val[k];
+            }
+            ++count;
+        }
+    }
+    if (tensor_offsets) {
+        uint64_t before = 0;
+        for (int32_t t = 0; t < num_tensors; ++t) {
+            tensor_offsets[t] = before;
+            for (int32_t r = 0; r < num_threads; ++r)
+                before += tcounts[(size_t)r * T + (size_t)t];
+        }
+        tensor_offsets[num_tensors] = before;
+    }
+    result = count;
+done:
+    if (jobs)
+        for (int32_t r = 0; r < num_threads; ++r) {
+            free(jobs[r].idx);
+            free(jobs[r].val);
+        }
+    free(jobs);
+    free(tids);
+    free(started);
+    free(tcounts);
+    return result;
 }
 
 /* ------------------------------------------------------------------ */

@@ -44,8 +44,33 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+PROBES = os.path.join(HERE, "probes")
+
+
+def probe_sources():
+    return sorted(glob.glob(os.path.join(PROBES, "*.hip")))
+
+
+def build_probes(verbose: bool = False) -> list:
+    """Compile every probes/*.hip (measurement executables the benchmark runs
+    beside the library, e.g. the write ceilings of apply) into an executable
+    of the same name; returns their paths."""
+    out = []
+    for src in probe_sources():
+        exe = os.path.splitext(src)[0]
+        tmp = exe + ".tmp"
+        cmd = [hipcc(), *[f for f in HIPCC_FLAGS if f != "-fPIC"], src, "-o", tmp]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.check_call(cmd)
+        os.replace(tmp, exe)
+        out.append(exe)
+    return out
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every csrc/*.hip into one shared library; returns its path."""
+    """Compile every csrc/*.hip into one shared library (and the measurement
+    probes); returns the library's path."""
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     objs = []
@@ -62,6 +87,7 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
     os.replace(tmp, LIB_PATH)
+    build_probes(verbose)
     return LIB_PATH
 
 

@@ -2,16 +2,16 @@
 benchmark times (delta_extract_multi over the whole set with the default
 workspace).
 
-At these sizes every output is checked through properties that hold at
-any size, computed on the GPU with plain torch ops:
-  * the count equals the number of planted changes, per tensor as well
-    (tensor_offsets differences);
-  * indices are strictly increasing, and inside their tensor;
-  * val[k] == new[idx[k]] and prev[idx[k]] != new[idx[k]] (so every kept
-    word really changed; with the count this means none is missing);
-  * applying the delta to a copy of prev gives new, bit for bit.
-In addition a sample of whole tensors (the largest, the smallest and some
-in between) is compared entry by entry with the CPU oracle.
+Every tensor of every set is compared entry by entry with the CPU oracle
+(its two copies streamed to the host one tensor at a time): the indices,
+the words, the per-tensor offsets, and each tensor's gap + LEB128 segment
+from the standalone encoder and from the extract that writes the code
+itself.  The Qwen3-14B pipeline's host output is compared with the oracle
+tensor by tensor, and its coded form chunk by chunk.  Beside the oracle,
+properties that hold at any size are checked on the GPU with plain torch
+ops (counts per tensor equal the planted changes, indices strictly
+increasing and inside their tensor, val[k] == new[idx[k]] != prev[idx[k]]),
+and applying the delta to a copy of prev gives new, bit for bit.
 """
 import numpy as np
 import pytest
@@ -31,16 +31,6 @@ def say(*a):
 
 def host_u16(t):
     return t.detach().reshape(-1).view(torch.int16).cpu().numpy().view(np.uint16)
-
-
-def sample_tensors(names, shapes):
-    """Largest, smallest, the first layer's tensors and every 37th."""
-    n = len(names)
-    sizes = [synth.numel(s) for s in shapes]
-    pick = {0, n - 1, int(np.argmax(sizes)), int(np.argmin(sizes))}
-    pick |= set(range(1, min(12, n)))
-    pick |= set(range(0, n, 37))
-    return sorted(pick)
 
 
 def check_set(ws, idx, val, offs, label):
@@ -63,14 +53,41 @@ def check_set(ws, idx, val, offs, label):
         q = ws.new[t].reshape(-1).view(torch.int16)
         assert torch.equal(q[local], val[a:b].view(torch.int16)), (label, t)
         assert bool((p[local] != q[local]).all()), (label, t)
-    # sampled tensors against the oracle
-    for t in sample_tensors(ws.names, ws.shapes):
+    say(label, "properties ok:", idx.numel(), "entries,", T, "tensors")
+
+
+def oracle_every_tensor(ws, idx, val, offs, label, codes=()):
+    """Every tensor against the oracle: its two copies are copied to the
+    host one tensor at a time and extracted there; the GPU's global indices
+    (minus the tensor base), words and tensor_offsets must equal the
+    oracle's, and every coded stream in ``codes`` (pairs of a device byte
+    buffer and its per-tensor byte offsets) must hold, for each tensor, the
+    oracle's LEB128 bytes of the oracle's tensor-local indices."""
+    T = len(ws.prev)
+    bases = np.concatenate([[0], np.cumsum(ws.numels)]).astype(np.int64)
+    idx_h = idx.cpu().numpy()
+    val_h = host_u16(val)
+    offs_h = offs.cpu().numpy().astype(np.int64)
+    codes_h = [(c.cpu().numpy(), np.asarray(o).astype(np.int64)) for c, o in codes]
+    before = 0
+    for t in range(T):
         r_idx, r_val, r_cnt = oracle.extract(host_u16(ws.prev[t]), host_u16(ws.new[t]))
         a, b = int(offs_h[t]), int(offs_h[t + 1])
-        assert b - a == r_cnt, (label, t)
-        np.testing.assert_array_equal(idx[a:b].cpu().numpy() - bases[t], r_idx)
-        np.testing.assert_array_equal(host_u16(val[a:b]), r_val)
-    say(label, "ok:", idx.numel(), "entries,", T, "tensors")
+        assert a == before and b - a == r_cnt, (label, ws.names[t])
+        np.testing.assert_array_equal(idx_h[a:b] - bases[t], r_idx, err_msg=f"{label} {t}")
+        np.testing.assert_array_equal(val_h[a:b], r_val, err_msg=f"{label} {t}")
+        if codes_h:
+            ref, n = oracle.leb128_encode(r_idx)
+            for c_h, cb in codes_h:
+                assert cb[t + 1] - cb[t] == n, (label, ws.names[t])
+                np.testing.assert_array_equal(c_h[cb[t]:cb[t + 1]], ref,
+                                              err_msg=f"{label} {t}")
+        before = b
+    assert before == idx_h.size == int(offs_h[T]), label
+    for c_h, cb in codes_h:
+        assert cb[0] == 0 and cb[T] == c_h.size, label
+    say(label, "oracle ok on every tensor:", T, "tensors,", idx_h.size, "entries",
+        f"({len(codes_h)} coded streams)")
 
 
 def round_trip(ws, idx, val, label):
@@ -83,20 +100,18 @@ def round_trip(ws, idx, val, label):
 
 
 def artifact_full(ws, idx, val, offs, label):
-    """A sealed LEB128 artifact of the whole set: verifies, its segment
-    hashes equal the oracle's on sampled segments, and activating it onto a
+    """A sealed LEB128 artifact of the whole set: verifies, every segment
+    hash equals the oracle's XXH64 of that segment, and activating it onto a
     copy of prev gives new."""
     art, h = ad.pack_artifact(idx, val, offs, ws.numels, version=2, base_version=1,
                               coding="leb128", seg_bytes=1 << 20)
     assert ad.delta_artifact_verify(art, h) == (0, None, False), label
     L = ad.delta_artifact_layout(h.num_tensors, h.count, h.idx_bytes, h.seg_bytes)
     stored = art[L["hashes"]:L["total"]].view(torch.int64).cpu().numpy().view(np.uint64)
-    nseg = int(h.num_segments)
-    for s in sorted({0, 1, nseg // 2, nseg - 1}):
-        lo = L["table"] + s * (1 << 20)
-        hi = min(lo + (1 << 20), L["hashes"])
-        piece = art[lo:hi].cpu().numpy()
-        assert stored[s] == oracle.xxh64(piece.tobytes(), seed=2), (label, s)
+    payload = art[L["table"]:L["hashes"]].cpu().numpy()
+    want = oracle.hash_segments(payload, 1 << 20, seed=2)
+    assert int(h.num_segments) == want.size
+    np.testing.assert_array_equal(stored, want)
     roll = [p.clone() for p in ws.prev]
     assert ad.activate_artifact(art, roll, active_version=1) == 2
     for r, q in zip(roll, ws.new):
@@ -107,8 +122,9 @@ def artifact_full(ws, idx, val, offs, label):
 
 def leb128_full(ws, idx, val, offs, label):
     """Gap + LEB128 code of the whole set's indices with one segment per
-    tensor: decodes to the indices; sampled tensors' segments equal the
-    oracle's bytes for that tensor's local indices."""
+    tensor: decodes to the indices and applies straight from the code
+    (every tensor's segment is compared with the oracle's bytes by
+    oracle_every_tensor)."""
     bases = np.concatenate([[0], np.cumsum(ws.numels)[:-1]]).astype(np.int64)
     offs_h = offs.cpu().numpy()
     buf, seg_bytes = ad.delta_leb128_encode(idx, offs_h, bases)
@@ -122,11 +138,6 @@ def leb128_full(ws, idx, val, offs, label):
     for r, q in zip(roll, ws.new):
         assert torch.equal(r.view(torch.int16), q.view(torch.int16)), label
     del roll
-    for t in sample_tensors(ws.names, ws.shapes):
-        a, b = int(offs_h[t]), int(offs_h[t + 1])
-        ref, n = oracle.leb128_encode(idx[a:b].cpu().numpy() - bases[t])
-        assert n == sb[t + 1] - sb[t], (label, t)
-        np.testing.assert_array_equal(buf[sb[t]:sb[t + 1]].cpu().numpy(), ref)
     say(label, "leb128 ok:", buf.numel(), "bytes for", idx.numel(), "indices")
     return buf, sb
 
@@ -134,8 +145,9 @@ def leb128_full(ws, idx, val, offs, label):
 def coded_full(ws, idx, val, offs, label, buf, sb):
     """The extract that writes the index stream LEB128 coded itself, over
     the whole set: its entries and offsets equal extract_multi's, its code
-    decodes to extract_multi's indices, sampled tensors' segments equal the
-    oracle's bytes, and the stream equals the standalone encoder's."""
+    decodes to extract_multi's indices and equals the standalone encoder's
+    stream (every tensor's segment is compared with the oracle's bytes by
+    oracle_every_tensor)."""
     bases = np.concatenate([[0], np.cumsum(ws.numels)[:-1]]).astype(np.int64)
     offs_h = offs.cpu().numpy()
     code, cval, coffs, cb = ad.delta_extract_multi_leb128(ws.prev, ws.new)
@@ -145,14 +157,10 @@ def coded_full(ws, idx, val, offs, label, buf, sb):
     assert torch.equal(back, idx), label
     del back
     cb_h = cb.cpu().numpy()
-    for t in sample_tensors(ws.names, ws.shapes):
-        a, b = int(offs_h[t]), int(offs_h[t + 1])
-        ref, n = oracle.leb128_encode(idx[a:b].cpu().numpy() - bases[t])
-        assert n == cb_h[t + 1] - cb_h[t], (label, t)
-        np.testing.assert_array_equal(code[cb_h[t]:cb_h[t + 1]].cpu().numpy(), ref)
     assert torch.equal(code, buf), label
     np.testing.assert_array_equal(cb_h, sb)
     say(label, "coded extract ok:", code.numel(), "bytes")
+    return code, cb_h
 
 
 @pytest.mark.parametrize("model,density", [("qwen3-4b", 0.01), ("qwen3-8b", 0.001),
@@ -168,7 +176,8 @@ def test_weight_set(model, density):
     assert ad.delta_count_changed_multi(ws.prev, ws.new) == ws.total_planted, label
     round_trip(ws, idx, val, label)
     buf, sb = leb128_full(ws, idx, val, offs, label)
-    coded_full(ws, idx, val, offs, label, buf, sb)
+    code, cb = coded_full(ws, idx, val, offs, label, buf, sb)
+    oracle_every_tensor(ws, idx, val, offs, label, codes=[(buf, sb), (code, cb)])
 
 
 def test_qwen3_8b_clustered():
@@ -186,8 +195,10 @@ def test_qwen3_8b_clustered():
     assert int(tile_hist.max()) > 5 * 82
     round_trip(ws, idx, val, "qwen3-8b clustered")
     buf, sb = leb128_full(ws, idx, val, offs, "qwen3-8b clustered")
-    coded_full(ws, idx, val, offs, "qwen3-8b clustered", buf, sb)
-    del buf
+    code, cb = coded_full(ws, idx, val, offs, "qwen3-8b clustered", buf, sb)
+    oracle_every_tensor(ws, idx, val, offs, "qwen3-8b clustered",
+                        codes=[(buf, sb), (code, cb)])
+    del buf, code
     artifact_full(ws, idx, val, offs, "qwen3-8b clustered")
 
 
@@ -201,23 +212,48 @@ def test_qwen3_14b_pipeline():
                                               num_streams=4, h_idx=h_idx, h_val=h_val)
     say("pipeline done", h_idx.numel())
     assert h_idx.numel() == ws.total_planted
-    # identical to the device-resident multi-tensor extract
+    # the oracle, tensor by tensor, against the pipeline's host output
+    bases = np.concatenate([[0], np.cumsum(ws.numels)]).astype(np.int64)
+    hi_np = h_idx.numpy()
+    hv_np = h_val.view(torch.int16).numpy().view(np.uint16)
+    ref_global = np.empty(ws.total_planted, dtype=np.int64)
+    pos = 0
+    for t in range(len(ws.prev)):
+        r_idx, r_val, r_cnt = oracle.extract(host_u16(ws.prev[t]), host_u16(ws.new[t]))
+        np.testing.assert_array_equal(hi_np[pos:pos + r_cnt] - bases[t], r_idx,
+                                      err_msg=ws.names[t])
+        np.testing.assert_array_equal(hv_np[pos:pos + r_cnt], r_val, err_msg=ws.names[t])
+        ref_global[pos:pos + r_cnt] = r_idx + bases[t]
+        pos += r_cnt
+    assert pos == h_idx.numel()
+    say("pipeline equals the oracle on every tensor")
+    # properties on the device-resident extract of the same set
     idx, val, offs = ad.delta_extract_multi(ws.prev, ws.new)
     torch.cuda.synchronize()
-    assert torch.equal(h_idx, idx.cpu())
-    assert torch.equal(h_val.view(torch.int16), val.view(torch.int16).cpu())
     check_set(ws, idx, val, offs, "qwen3-14b")
+    del idx, val, offs, h_idx
 
-    del h_idx
-    # the coded pipeline: values identical, indices decode to the same stream
+    # the coded pipeline: values equal the oracle's; every chunk's bytes
+    # equal the oracle's LEB128 of that chunk's global indices minus the
+    # chunk's first word
     hb = torch.empty(3 * cap, dtype=torch.uint8, pin_memory=True)
     hb, hv, counts, used = ad.delta_extract_pipelined_leb128(
         ws.prev, ws.new, chunk_elems=1 << 27, num_streams=4, h_bytes=hb, h_val=h_val)
     say("coded pipeline done", hb.numel(), "bytes")
-    assert torch.equal(hv.view(torch.int16), val.view(torch.int16).cpu())
-    o, b = ad.chunk_segments(counts, used)
-    back = ad.delta_leb128_decode(hb.to(DEV), o, b)
-    assert torch.equal(back, idx)
+    np.testing.assert_array_equal(hv.view(torch.int16).numpy().view(np.uint16), hv_np[:pos])
+    hb_np = hb.numpy()
+    nchunks = (ws.total + used - 1) // used
+    assert len(counts) == nchunks
+    bounds = np.searchsorted(ref_global, np.arange(nchunks + 1, dtype=np.int64) * used)
+    byte = 0
+    for c in range(nchunks):
+        a, b = int(bounds[c]), int(bounds[c + 1])
+        assert counts[c] == b - a, c
+        ref, n = oracle.leb128_encode(ref_global[a:b] - c * used)
+        np.testing.assert_array_equal(hb_np[byte:byte + n], ref, err_msg=f"chunk {c}")
+        byte += n
+    assert byte == hb.numel()
+    say("coded pipeline equals the oracle in every chunk:", nchunks, "chunks")
 
 
 def test_compose_chain_full_index_space():
@@ -243,7 +279,7 @@ def test_compose_chain_full_index_space():
 
 def test_apply_chain_full_weight_set():
     """Catch-up over three ~1% deltas of the Qwen3-8B tensor list in one
-    pass: sampled tensors equal the oracle replaying the chain on them."""
+    pass: every tensor equals the oracle replaying the chain on it."""
     ws = synth.make_weight_set("qwen3-8b", 0.0, seed=synth.config_seed(3), device=DEV)
     roll = [p.clone() for p in ws.prev]
     bases = np.concatenate([[0], np.cumsum(ws.numels)]).astype(np.int64)
@@ -259,7 +295,7 @@ def test_apply_chain_full_weight_set():
     say("apply_chain: deltas of", [i.numel() for i, _ in deltas], "entries")
     ad.delta_apply_chain(roll, deltas, check=True)
     torch.cuda.synchronize()
-    for t in sample_tensors(ws.names, ws.shapes):
+    for t in range(len(ws.prev)):
         lo, hi = int(bases[t]), int(bases[t + 1])
         want = host_u16(ws.prev[t]).copy()
         for idx, val in deltas:
@@ -286,16 +322,19 @@ def test_qwen3_8b_fused_layout():
         want[f] += k
     np.testing.assert_array_equal(np.diff(offs_h), want)
     tbase = np.concatenate([[0], np.cumsum(tn)])
-    # sampled targets against the oracle on their stacked blocks
+    # every target against the oracle on its stacked blocks
     members = {}
     for t, (f, off) in enumerate(sources):
         members.setdefault(f, []).append((off, t))
-    for f in sorted({0, 1, 5, 4, len(targets) // 2, len(targets) - 1}):
+    idx_h = idx.cpu().numpy()
+    val_h = host_u16(val)
+    for f in range(len(targets)):
         parts = [t for _, t in sorted(members[f])]
         p = np.concatenate([host_u16(ws.prev[t]) for t in parts])
         q = np.concatenate([host_u16(ws.new[t]) for t in parts])
         r_idx, r_val, r_cnt = oracle.extract(p, q)
         a, b = int(offs_h[f]), int(offs_h[f + 1])
         assert b - a == r_cnt, targets[f][0]
-        np.testing.assert_array_equal(idx[a:b].cpu().numpy() - tbase[f], r_idx)
-        np.testing.assert_array_equal(host_u16(val[a:b]), r_val)
+        np.testing.assert_array_equal(idx_h[a:b] - tbase[f], r_idx, err_msg=targets[f][0])
+        np.testing.assert_array_equal(val_h[a:b], r_val, err_msg=targets[f][0])
+    say("qwen3-8b fused: every target equals the oracle")

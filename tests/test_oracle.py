@@ -181,6 +181,49 @@ def test_multi_equals_single_on_concatenation():
     del r
 
 
+@pytest.mark.parametrize("threads", [2, 3, 8, 16, 64, 1000])
+def test_multi_threaded_equals_numpy_on_concatenation(threads):
+    """The threaded form (contiguous per-thread ranges, concatenated in
+    order) gives the definition's list: numpy's flatnonzero over the
+    concatenated tensors, per-tensor offsets from np.cumsum, at every thread
+    count (more threads than words included), with capacity truncation."""
+    sizes = [0, 1, 7, 128, 0, 4096, 33, 0, 10_000, 3, 65_537]
+    ps, qs = [], []
+    for i, n in enumerate(sizes):
+        p, q, _ = random_pair(n, 0.2 if n else 0.0, seed=300 + i)
+        ps.append(p)
+        qs.append(q)
+    cat_p, cat_q = np.concatenate(ps), np.concatenate(qs)
+    want = np.flatnonzero(cat_p != cat_q)
+    idx, val, offs, cnt = oracle.extract_multi(ps, qs, threads=threads)
+    assert cnt == want.size
+    np.testing.assert_array_equal(idx, want)
+    np.testing.assert_array_equal(val, cat_q[want])
+    per = [int(np.count_nonzero(p != q)) for p, q in zip(ps, qs)]
+    np.testing.assert_array_equal(offs, np.concatenate([[0], np.cumsum(per)]).astype(np.uint64))
+    for cap in (0, 1, want.size // 2, want.size):
+        i2, v2, o2, c2 = oracle.extract_multi(ps, qs, capacity=cap, threads=threads)
+        assert c2 == want.size
+        np.testing.assert_array_equal(i2, want[:cap])
+        np.testing.assert_array_equal(v2, cat_q[want[:cap]])
+        np.testing.assert_array_equal(o2, offs)
+
+
+def test_multi_threaded_dense_and_empty():
+    # every word changed: every range boundary falls on a kept word
+    p = np.arange(5000, dtype=np.uint16)
+    q = p ^ np.uint16(1)
+    for threads in (2, 7, 4999, 5000, 5001):
+        idx, val, offs, cnt = oracle.extract_multi([p[:1234], p[1234:]], [q[:1234], q[1234:]],
+                                                   threads=threads)
+        assert cnt == 5000
+        np.testing.assert_array_equal(idx, np.arange(5000))
+        np.testing.assert_array_equal(val, q)
+        assert offs.tolist() == [0, 1234, 5000]
+    idx, val, offs, cnt = oracle.extract_multi([], [], threads=4)
+    assert cnt == 0 and offs.tolist() == [0]
+
+
 def test_multi_all_empty():
     idx, val, offs, cnt = oracle.extract_multi([np.empty(0, np.uint16)] * 3,
                                                [np.empty(0, np.uint16)] * 3)
@@ -574,6 +617,12 @@ MUTANTS = {
     # a duplicate index stepped past in only one stream
     "compose_single_advance": ("                    have = 1;\n                }\n                ++pos[d];",
                                "                    have = 1;\n                    ++pos[d];\n                }"),
+    # threaded form: the per-thread lists concatenated in reverse range order
+    "threaded_reverse_concat": ("    for (int32_t r = 0; r < num_threads; ++r) {\n        for (uint64_t k = 0; k < jobs[r].count; ++k) {",
+                                "    for (int32_t r = num_threads - 1; r >= 0; --r) {\n        for (uint64_t k = 0; k < jobs[r].count; ++k) {"),
+    # threaded form: the last word of every range skipped
+    "threaded_range_end": ("            for (uint64_t i = a; i < b; ++i) {",
+                           "            for (uint64_t i = a; i + 1 < b; ++i) {"),
 }
 
 
@@ -584,7 +633,8 @@ def _build_mutant(tmp_path, name, old, new):
     c = tmp_path / f"{name}.c"
     so = tmp_path / f"{name}.so"
     c.write_text(mut)
-    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", str(c), "-o", str(so)])
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread", str(c), "-o",
+                           str(so)])
     return ctypes.CDLL(str(so))
 
 
@@ -628,6 +678,20 @@ def _pins_pass(lib):
                                  idx.ctypes.data, val.ctypes.data, 120, offs.ctypes.data)
     if not np.array_equal(idx[:c], np.flatnonzero(np.concatenate(ps) != np.concatenate(qs))):
         return False
+    # the threaded form against numpy on the concatenation (every word of
+    # the second tensor changed, so every range ends on a kept word)
+    lib.oracle_extract_multi_threaded.argtypes = [P, P, P, ctypes.c_int32, P, P, U64, P,
+                                                  ctypes.c_int32]
+    lib.oracle_extract_multi_threaded.restype = U64
+    qs2 = [qs[0], ps[1] ^ np.uint16(0x0100)]
+    qq2 = (ctypes.c_void_p * 2)(*[a.ctypes.data for a in qs2])
+    want = np.flatnonzero(np.concatenate(ps) != np.concatenate(qs2))
+    for nt in (2, 3, 5):
+        c = lib.oracle_extract_multi_threaded(ctypes.cast(pp, P), ctypes.cast(qq2, P),
+                                              numels.ctypes.data, 2, idx.ctypes.data,
+                                              val.ctypes.data, 120, offs.ctypes.data, nt)
+        if c != want.size or not np.array_equal(idx[:c], want):
+            return False
     # LEB128 worked example
     out = np.empty(10, np.uint8)
     n = lib.oracle_leb128_encode(np.array([198], np.int64).ctypes.data, 1, out.ctypes.data, 10)
@@ -665,7 +729,8 @@ def _pins_pass(lib):
 def test_unmutated_passes_mini_pins(tmp_path):
     src = os.path.join(os.path.dirname(oracle.__file__), "delta_oracle.c")
     so = tmp_path / "ok.so"
-    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", src, "-o", str(so)])
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread", src, "-o",
+                           str(so)])
     assert _pins_pass(ctypes.CDLL(str(so)))
 
 
