@@ -87,7 +87,8 @@ typedef enum {
   DELTA_ERR_OUT_OF_RANGE = 4,   /* host-synchronous calls: an index was skipped */
   DELTA_ERR_VERSION = 5,        /* apply_checked: active != base version */
   DELTA_ERR_WORKSPACE = 6,      /* workspace missing, too small or misaligned */
-  DELTA_ERR_HIP = 7             /* a HIP runtime call failed */
+  DELTA_ERR_HIP = 7,            /* a HIP runtime call failed */
+  DELTA_ERR_INTEGRITY = 8       /* artifact_activate: a hash does not match */
 } delta_status_t;
 
 typedef enum { DELTA_INDEX_I32 = 0, DELTA_INDEX_I64 = 1 } delta_index_t;
@@ -392,7 +393,10 @@ size_t delta_apply_leb128_workspace_bytes(uint64_t nbytes, int32_t num_tensors);
  *                 tensor_offsets, seg_bases = tensor bases) as
  *                 delta_leb128_encode writes them for delta_extract_multi's
  *                 output, or one per chunk as the coded pipeline writes
- *                 them (seg_bases[c] = c * chunk).
+ *                 them (delta_chunk_segments).  d_seg_bases NULL with
+ *                 num_segs == num_tensors: one segment per tensor, each
+ *                 based at its tensor's first global index (derived from
+ *                 numels).
  *   val, count    device words [count]: entry k's new word.
  *   d_error_flag  device, nullable: set when the stream is malformed, when
  *                 it holds a number of entries other than `count`, or when
@@ -553,6 +557,74 @@ delta_status_t delta_artifact_verify(const void* d_artifact, size_t artifact_byt
                                      uint32_t* d_header_bad, void* workspace,
                                      size_t workspace_bytes, hipStream_t stream);
 
+/* Workspace bytes of delta_artifact_pack for `count` entries over
+ * `num_tensors` tensors with this index coding (0 if invalid). */
+size_t delta_artifact_pack_workspace_bytes(uint64_t count, int32_t num_tensors,
+                                           uint32_t index_coding);
+
+/*
+ * delta_artifact_pack — Sec. 5.1: the trainer's versioned delta file, in
+ * device memory, from delta_extract_multi's output: header, tensor table,
+ * index stream, value stream and segment hashes, sealed (the same bytes
+ * delta_artifact_seal gives for the same parts).
+ *   idx, val, count   device: the global int64 indices and words of a
+ *                     delta_extract_multi call, and their number.
+ *   d_tensor_offsets  device uint64 [num_tensors + 1]: its tensor_offsets
+ *                     (entry 0 must be 0 and entry T must be count).
+ *   numels            host array [num_tensors]: the tensor list's sizes;
+ *                     the tensor bases (Sec. 5.1 block offsets) and the
+ *                     table are derived from them here.
+ *   index_coding      DELTA_CODING_INT64 (the indices as they are) or
+ *                     DELTA_CODING_LEB128 (gap + LEB128, one segment per
+ *                     tensor, each tensor's first entry coded as its
+ *                     tensor-local index).
+ *   version, base_version, seg_bytes   the header's fields.
+ *   d_artifact, artifact_bytes  device output, 8-byte aligned.
+ *   workspace         delta_artifact_pack_workspace_bytes(count, T, coding).
+ *   h_header          host, nullable: the sealed header (with its hash).
+ *   h_total_bytes     host, nullable: the artifact's size.
+ * Host-synchronous (the LEB128 stream's length decides where the values
+ * go): returns when the artifact is sealed.  DELTA_ERR_CAPACITY, with
+ * *h_total_bytes set, when artifact_bytes is too small; DELTA_ERR_INVALID_ARG
+ * when the offsets or the order of the indices are inconsistent.
+ */
+delta_status_t delta_artifact_pack(const int64_t* idx, const uint16_t* val, uint64_t count,
+                                   const uint64_t* d_tensor_offsets, const uint64_t* numels,
+                                   int32_t num_tensors, uint32_t index_coding, uint64_t version,
+                                   uint64_t base_version, uint64_t seg_bytes, void* d_artifact,
+                                   size_t artifact_bytes, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream, delta_artifact_header_t* h_header,
+                                   uint64_t* h_total_bytes);
+
+/* Workspace bytes of delta_artifact_activate for this header (0 if the
+ * header is invalid). */
+size_t delta_artifact_activate_workspace_bytes(const delta_artifact_header_t* header);
+
+/*
+ * delta_artifact_activate — Sec. 5.2 staged activation: a worker applies a
+ * received artifact only if it is intact and was made against the version
+ * the worker holds.
+ *   d_artifact, artifact_bytes, header  the artifact in device memory and
+ *                     the caller's host copy of its header (which fixes
+ *                     the layout; a changed header fails the artifact hash).
+ *   weight_ptrs, numels, num_tensors  the rollout copy (host arrays), in
+ *                     the artifact's tensor order; updated in place.
+ *   active_version    the version the weights hold now.
+ * Checks, in this order, before any weight is written: the header's base
+ * version against active_version (DELTA_ERR_VERSION, nothing enqueued);
+ * the tensor count and sizes (DELTA_ERR_INVALID_ARG); every segment hash
+ * and the artifact hash (DELTA_ERR_INTEGRITY).  Then the delta is applied
+ * (LEB128 indices decoded inside the apply).  Host-synchronous; a malformed
+ * index stream or an index outside the tensors gives
+ * DELTA_ERR_OUT_OF_RANGE after the other words were written.
+ */
+delta_status_t delta_artifact_activate(const void* d_artifact, size_t artifact_bytes,
+                                       const delta_artifact_header_t* header,
+                                       uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                       int32_t num_tensors, uint64_t active_version,
+                                       void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream);
+
 /* Options of the chunked pipeline. */
 typedef struct {
   uint64_t chunk_elems; /* words of the global index space per chunk (> 0) */
@@ -629,6 +701,18 @@ delta_status_t delta_extract_pipelined_leb128(
     void* d_staging, size_t staging_bytes, uint8_t* h_bytes, uint64_t h_bytes_capacity,
     uint16_t* h_val, uint64_t h_val_capacity, uint64_t* h_chunk_counts, uint64_t h_num_chunks,
     uint64_t* h_count, uint64_t* h_nbytes);
+
+/*
+ * delta_chunk_segments — the segments of a coded pipeline's index stream
+ * for delta_leb128_decode and delta_apply_leb128_multi (Sec. 5.2: each
+ * chunk is a segment of its own): chunk c starts at entry seg_offsets[c]
+ * (the counts of the chunks before it; seg_offsets[num_chunks] = total)
+ * and is based at word c * chunk_elems.  Host arrays: chunk_counts
+ * [num_chunks], seg_offsets [num_chunks + 1], seg_bases [num_chunks].
+ */
+delta_status_t delta_chunk_segments(const uint64_t* chunk_counts, uint64_t num_chunks,
+                                    uint64_t chunk_elems, uint64_t* seg_offsets,
+                                    uint64_t* seg_bases);
 
 #ifdef __cplusplus
 }

@@ -537,6 +537,8 @@ def _segs(seg_offsets, seg_bases, device):
     if seg_offsets is None:
         return None, None, 0
     offs = torch.as_tensor(seg_offsets, dtype=torch.int64, device=device).contiguous()
+    if seg_bases is None:
+        return offs, None, offs.numel() - 1
     bases = torch.as_tensor(seg_bases, dtype=torch.int64, device=device).contiguous()
     if bases.numel() + 1 != offs.numel():
         raise ValueError("seg_offsets needs one entry more than seg_bases")
@@ -617,7 +619,9 @@ def delta_apply_leb128_multi(weights: Sequence[torch.Tensor], code: torch.Tensor
     """Apply a delta whose indices are gap + LEB128 coded (Sec. 5.1) straight
     into a tensor list, decoding them on the fly (Sec. 5.2 activation on the
     receiving side).  ``seg_offsets`` / ``seg_bases`` as for
-    :func:`delta_leb128_decode`.  With ``check`` it synchronises and raises
+    :func:`delta_leb128_decode`; ``seg_bases=None`` with one segment per
+    tensor bases each at its tensor's first global index (the library
+    derives them from the sizes).  With ``check`` it synchronises and raises
     DeltaError on a malformed stream, a count mismatch or an index outside
     the tensors."""
     if code.dtype != torch.uint8 or not code.is_cuda or not code.is_contiguous():
@@ -634,7 +638,7 @@ def delta_apply_leb128_multi(weights: Sequence[torch.Tensor], code: torch.Tensor
         flag = torch.zeros(1, dtype=torch.int32, device=dev)
     _check(library().delta_apply_leb128_multi(
         ptrs, numels, T, code.data_ptr(), code.numel(), offs.data_ptr() if S else None,
-        bases.data_ptr() if S else None, S, _words(val, "val"), val.numel(),
+        bases.data_ptr() if S and bases is not None else None, S, _words(val, "val"), val.numel(),
         flag.data_ptr() if flag is not None else None, ws.data_ptr(),
         ws.numel() * ws.element_size(), _stream(stream)))
     if check:
@@ -705,14 +709,14 @@ def delta_extract_pipelined_plan(plan: MultiPlan, chunk_elems: int = 1 << 27,
 
 def chunk_segments(chunk_counts: Sequence[int], chunk_elems: int):
     """Segment offsets (entries) and bases (words) of a coded pipeline
-    stream: chunk c is one segment based at its first word c * chunk_elems.
-    Pass them to :func:`delta_leb128_decode`."""
-    counts = [int(c) for c in chunk_counts]
-    offs = [0]
-    for c in counts:
-        offs.append(offs[-1] + c)
-    bases = [c * int(chunk_elems) for c in range(len(counts))]
-    return offs, bases
+    stream (``delta_chunk_segments``): chunk c is one segment based at its
+    first word c * chunk_elems.  Pass them to :func:`delta_leb128_decode`."""
+    n = len(chunk_counts)
+    offs = (ctypes.c_uint64 * (n + 1))()
+    bases = (ctypes.c_uint64 * max(n, 1))()
+    _check(library().delta_chunk_segments(_u64_array(chunk_counts), n, int(chunk_elems), offs,
+                                          bases))
+    return list(offs), list(bases)[:n]
 
 
 def delta_extract_pipelined_leb128(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tensor],
@@ -803,48 +807,35 @@ def pack_artifact(idx: torch.Tensor, val: torch.Tensor, tensor_offsets: torch.Te
                   coding: str = "int64", seg_bytes: int = 1 << 14,
                   stream: Optional[torch.cuda.Stream] = None):
     """A sealed delta checkpoint (Sec. 5.1) in GPU memory from
-    delta_extract_multi's output: header, tensor table, index stream (int64
-    or gap + LEB128 per tensor), values, segment hashes.  Returns the uint8
-    GPU tensor and the header."""
+    delta_extract_multi's output (``delta_artifact_pack``): header, tensor
+    table, index stream (int64 or gap + LEB128 per tensor), values, segment
+    hashes.  Returns the uint8 GPU tensor and the header."""
+    if coding not in ("int64", "leb128"):
+        raise ValueError("coding must be 'int64' or 'leb128'")
+    if idx.dtype != torch.int64 or not idx.is_contiguous():
+        raise TypeError("idx must be contiguous int64")
+    coding_id = _abi.DELTA_CODING_LEB128 if coding == "leb128" else _abi.DELTA_CODING_INT64
     dev = idx.device
     T = len(numels)
-    bases = [0]
-    for n in numels[:-1]:
-        bases.append(bases[-1] + int(n))
-    offs = tensor_offsets.to(torch.int64)
-    if coding == "leb128":
-        code, seg_starts = delta_leb128_encode(idx, offs.cpu().tolist(), bases, stream=stream)
-        byte_offs = seg_starts
-        idx_bytes = code.numel()
-        coding_id = _abi.DELTA_CODING_LEB128
-    elif coding == "int64":
-        code = idx.contiguous().view(torch.uint8)
-        byte_offs = offs * 8
-        idx_bytes = code.numel()
-        coding_id = _abi.DELTA_CODING_INT64
-    else:
-        raise ValueError("coding must be 'int64' or 'leb128'")
     K = idx.numel()
-    L = delta_artifact_layout(T, K, idx_bytes, seg_bytes)
-    art = torch.zeros(L["total"], dtype=torch.uint8, device=dev)
-    table = torch.stack([torch.tensor(list(numels), dtype=torch.int64, device=dev),
-                         offs[:T], byte_offs[:T].to(dev)], dim=1).contiguous()
-    art[L["table"]:L["table"] + 24 * T].copy_(table.view(torch.uint8).reshape(-1))
-    art[L["idx"]:L["idx"] + idx_bytes].copy_(code)
-    art[L["val"]:L["val"] + 2 * K].copy_(val.contiguous().view(torch.uint8).reshape(-1))
+    offs = tensor_offsets.to(torch.int64).contiguous()
+    nums = _u64_array(numels)
+    ws = _workspace(library().delta_artifact_pack_workspace_bytes(K, T, coding_id), dev)
+    # an int64 stream's size is known; a coded one at most 9 bytes per entry
+    size = delta_artifact_layout(T, K, (8 if coding == "int64" else 2) * K, seg_bytes)["total"]
     h = _abi.delta_artifact_header_t()
-    h.index_coding = coding_id
-    h.version = int(version)
-    h.base_version = int(base_version)
-    h.num_tensors = T
-    h.total_words = sum(int(n) for n in numels)
-    h.count = K
-    h.idx_bytes = idx_bytes
-    h.seg_bytes = int(seg_bytes)
-    _check(library().delta_artifact_seal(art.data_ptr(), art.numel(), ctypes.byref(h),
-                                         _stream(stream)))
-    (stream or torch.cuda.current_stream()).synchronize()
-    return art, read_artifact_header(art)
+    total = ctypes.c_uint64(0)
+    for _ in range(2):
+        art = torch.empty(max(size, 8), dtype=torch.uint8, device=dev)
+        status = library().delta_artifact_pack(
+            idx.data_ptr(), _words(val, "val"), K, offs.data_ptr(), nums, T, coding_id,
+            int(version), int(base_version), int(seg_bytes), art.data_ptr(), art.numel(),
+            ws.data_ptr(), ws.numel(), _stream(stream), ctypes.byref(h), ctypes.byref(total))
+        if status != _abi.DELTA_ERR_CAPACITY:
+            break
+        size = total.value
+    _check(status)
+    return art[:total.value], h
 
 
 def read_artifact_header(art: torch.Tensor):
@@ -873,37 +864,17 @@ def delta_artifact_verify(art: torch.Tensor, header=None,
 
 
 def activate_artifact(art: torch.Tensor, weights: Sequence[torch.Tensor], active_version: int,
-                      stream: Optional[torch.cuda.Stream] = None) -> int:
-    """Staged activation (Sec. 5.2): verify the artifact, refuse it unless
-    its base version is the active one, then apply it in place.  Returns
-    the new active version."""
-    h = read_artifact_header(art)
-    n_bad, first, header_bad = delta_artifact_verify(art, h, stream)
-    if n_bad or header_bad:
-        raise DeltaError(_abi.DELTA_ERR_INVALID_ARG,
-                         f"artifact fails its hashes ({n_bad} segments, first {first}; "
-                         f"header {'bad' if header_bad else 'ok'})")
-    if int(h.base_version) != int(active_version):
-        raise DeltaError(_abi.DELTA_ERR_VERSION,
-                         f"delta of version {h.version} is based on {h.base_version}, "
-                         f"active version is {active_version}")
-    if len(weights) != h.num_tensors:
-        raise ValueError("the artifact is for a different tensor list")
-    L = delta_artifact_layout(h.num_tensors, h.count, h.idx_bytes, h.seg_bytes)
-    T, K = int(h.num_tensors), int(h.count)
-    table = art[L["table"]:L["table"] + 24 * T].view(torch.int64).reshape(T, 3)
-    numels = table[:, 0].cpu().tolist()
-    if numels != [w.numel() for w in weights]:
-        raise ValueError("the artifact is for tensors of other sizes")
-    val = art[L["val"]:L["val"] + 2 * K].view(weights[0].dtype if weights else torch.bfloat16)
-    code = art[L["idx"]:L["idx"] + int(h.idx_bytes)]
-    if h.index_coding == _abi.DELTA_CODING_LEB128:
-        bases = [0]
-        for n in numels[:-1]:
-            bases.append(bases[-1] + n)
-        offs = table[:, 1].cpu().tolist() + [K]
-        # decode-in-apply: the indices are never materialised
-        delta_apply_leb128_multi(weights, code, offs, bases, val, check=True, stream=stream)
-    else:
-        delta_apply_multi(weights, code.view(torch.int64), val, check=True, stream=stream)
+                      header=None, stream: Optional[torch.cuda.Stream] = None) -> int:
+    """Staged activation (Sec. 5.2, ``delta_artifact_activate``): the artifact
+    is applied in place only if it is intact and based on the active
+    version.  Returns the new active version; raises DeltaError
+    (DELTA_ERR_VERSION, DELTA_ERR_INTEGRITY, ...) otherwise."""
+    h = header if header is not None else read_artifact_header(art)
+    ws = _workspace(library().delta_artifact_activate_workspace_bytes(ctypes.byref(h)),
+                    art.device)
+    ptrs = _ptr_array([_words(w, f"weights[{i}]") for i, w in enumerate(weights)])
+    numels = _u64_array([w.numel() for w in weights])
+    _check(library().delta_artifact_activate(
+        art.data_ptr(), art.numel(), ctypes.byref(h), ptrs, numels, len(weights),
+        int(active_version), ws.data_ptr(), ws.numel(), _stream(stream)))
     return int(h.version)

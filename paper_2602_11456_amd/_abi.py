@@ -19,6 +19,7 @@ DELTA_ERR_OUT_OF_RANGE = 4
 DELTA_ERR_VERSION = 5
 DELTA_ERR_WORKSPACE = 6
 DELTA_ERR_HIP = 7
+DELTA_ERR_INTEGRITY = 8
 
 DELTA_INDEX_I32 = 0
 DELTA_INDEX_I64 = 1
@@ -105,6 +106,14 @@ SIGNATURES = {
     "delta_artifact_verify_workspace_bytes": (SZ, [ctypes.POINTER(delta_artifact_header_t)]),
     "delta_artifact_verify": (STATUS, [P, SZ, ctypes.POINTER(delta_artifact_header_t), P, P, P,
                                        P, SZ, P]),
+    "delta_artifact_pack_workspace_bytes": (SZ, [U64, I32, ctypes.c_uint32]),
+    "delta_artifact_pack": (STATUS, [P, P, U64, P, P, I32, ctypes.c_uint32, U64, U64, U64, P,
+                                     SZ, P, SZ, P, ctypes.POINTER(delta_artifact_header_t),
+                                     ctypes.POINTER(U64)]),
+    "delta_artifact_activate_workspace_bytes": (SZ, [ctypes.POINTER(delta_artifact_header_t)]),
+    "delta_artifact_activate": (STATUS, [P, SZ, ctypes.POINTER(delta_artifact_header_t), P, P,
+                                         I32, U64, P, SZ, P]),
+    "delta_chunk_segments": (STATUS, [P, U64, U64, P, P]),
     "delta_pipeline_staging_bytes": (SZ, [P, I32, ctypes.POINTER(delta_pipeline_opts_t)]),
     "delta_extract_pipelined": (STATUS, [P, P, P, I32, ctypes.POINTER(delta_pipeline_opts_t), P,
                                          P, SZ, P, P, U64, P]),

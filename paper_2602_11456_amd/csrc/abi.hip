@@ -247,6 +247,7 @@ const char* delta_status_string(int status) {
     case DELTA_ERR_VERSION: return "DELTA_ERR_VERSION";
     case DELTA_ERR_WORKSPACE: return "DELTA_ERR_WORKSPACE";
     case DELTA_ERR_HIP: return "DELTA_ERR_HIP";
+    case DELTA_ERR_INTEGRITY: return "DELTA_ERR_INTEGRITY";
     default: return "DELTA_ERR_UNKNOWN";
   }
 }
@@ -787,27 +788,25 @@ delta_status_t delta_apply_leb128_multi(uint16_t* const* weight_ptrs, const uint
                                         const uint16_t* val, uint64_t count,
                                         uint32_t* d_error_flag, void* workspace,
                                         size_t workspace_bytes, hipStream_t stream) {
-  if (num_tensors < 0 || (num_tensors > 0 && (!weight_ptrs || !numels)))
-    return fail(DELTA_ERR_INVALID_ARG, "bad tensor list");
+  std::vector<uint64_t> bases, ptrs;
+  delta_status_t st = weight_table(weight_ptrs, numels, num_tensors, bases, ptrs);
+  if (st != DELTA_OK) return st;
   if (nbytes > 0 && !code) return fail(DELTA_ERR_INVALID_ARG, "code is NULL");
   if (count > 0 && !val) return fail(DELTA_ERR_INVALID_ARG, "val is NULL");
-  if (num_segs > 0 && (!d_seg_offsets || !d_seg_bases))
-    return fail(DELTA_ERR_INVALID_ARG, "segment arrays are NULL");
+  if (odd(val)) return fail(DELTA_ERR_INVALID_ARG, "val not 2-byte aligned");
+  const bool tensor_bases = num_segs > 0 && !d_seg_bases;
+  if (num_segs > 0 && !d_seg_offsets) return fail(DELTA_ERR_INVALID_ARG, "d_seg_offsets is NULL");
+  if (tensor_bases && num_segs != (uint32_t)num_tensors)
+    return fail(DELTA_ERR_INVALID_ARG,
+                "d_seg_bases NULL means one segment per tensor: num_segs %u, %d tensors",
+                num_segs, num_tensors);
   if (nbytes == 0 && count > 0)
     return fail(DELTA_ERR_INVALID_ARG, "%llu values but an empty index stream",
                 (unsigned long long)count);
-  std::vector<uint64_t> bases((size_t)num_tensors + 1, 0);
-  std::vector<uint64_t> ptrs((size_t)num_tensors, 0);
-  for (int32_t t = 0; t < num_tensors; ++t) {
-    if (numels[t] > 0 && (!weight_ptrs[t] || odd(weight_ptrs[t])))
-      return fail(DELTA_ERR_INVALID_ARG, "tensor %d: NULL or odd pointer", t);
-    bases[t + 1] = bases[t] + numels[t];
-    ptrs[t] = (uint64_t)(uintptr_t)weight_ptrs[t];
-  }
   const DecLayout D = dec_layout(nbytes);
   if (D.btiles > 0xFFFFFFFFull / 256) return fail(DELTA_ERR_INVALID_ARG, "stream too long");
   const ApplyLebLayout L = apply_leb_layout(nbytes, num_tensors);
-  delta_status_t st = check_workspace(workspace, workspace_bytes, L.total);
+  st = check_workspace(workspace, workspace_bytes, L.total);
   if (st != DELTA_OK) return st;
   if (nbytes == 0) return ok();   // nothing to apply
   char* ws = (char*)workspace;
@@ -819,7 +818,10 @@ delta_status_t delta_apply_leb128_multi(uint16_t* const* weight_ptrs, const uint
   memset(&a, 0, sizeof(a));
   a.in = code;
   a.nbytes = nbytes;
-  a.segs = {d_seg_offsets, d_seg_bases, num_segs, 0};
+  // with d_seg_bases NULL, segment t is based at tensor t's first global
+  // index: the first T entries of the uploaded tensor bases
+  a.segs = {d_seg_offsets, tensor_bases ? (const uint64_t*)(ws + L.bases) : d_seg_bases, num_segs,
+            0};
   a.capacity = count;
   a.d_count = (uint64_t*)(ws + L.count);
   a.err = d_error_flag;
@@ -956,6 +958,305 @@ delta_status_t delta_artifact_verify(const void* d_artifact, size_t artifact_byt
                                         header->version, (uint64_t*)workspace, d_bad_segments,
                                         d_first_bad, d_header_bad, stream);
   if (e != hipSuccess) return hip_fail(e, "verify launch");
+  return ok();
+}
+
+
+// ------------------------------------------------ artifact pack / activate
+
+}  // extern "C"
+
+namespace {
+
+// Reads `n` bytes of device memory after the stream's work so far.
+delta_status_t read_back(void* host, const void* dev, size_t n, hipStream_t stream) {
+  hipError_t e = hipStreamSynchronize(stream);
+  if (e == hipSuccess && n) e = hipMemcpy(host, dev, n, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "read back");
+  return DELTA_OK;
+}
+
+// Workspace of delta_artifact_pack: numels [T], tensor bases [T], first
+// index byte of each tensor [T + 1], the code length, the encoder's error
+// flag, then the encoder's own workspace.
+struct PackLayout {
+  size_t numels, bases, byte_offs, nbytes, err, enc, total;
+};
+PackLayout pack_layout(uint64_t count, int32_t T, bool leb) {
+  const uint64_t t = T > 0 ? (uint64_t)T : 0;
+  PackLayout L;
+  L.numels = 0;
+  L.bases = align_up(L.numels + 8 * t);
+  L.byte_offs = align_up(L.bases + 8 * t);
+  L.nbytes = align_up(L.byte_offs + 8 * (t + 1));
+  L.err = align_up(L.nbytes + 8);
+  L.enc = align_up(L.err + 8);
+  L.total = align_up(L.enc + (leb ? enc_layout(count).total : 0));
+  return L;
+}
+
+// Workspace of delta_artifact_activate: the verify results and fresh
+// segment hashes, the segment offsets [T + 1], the error flag, then the
+// apply's own workspace.
+struct ActivateLayout {
+  size_t bad, first_bad, header_bad, err, offs, fresh, apply, total;
+};
+ActivateLayout activate_layout(const ArtifactLayout& A, const delta_artifact_header_t& h) {
+  ActivateLayout L;
+  L.bad = 0;
+  L.first_bad = 8;
+  L.header_bad = 16;
+  L.err = 24;
+  L.offs = align_up(32);
+  L.fresh = align_up(L.offs + 8 * (h.num_tensors + 1));
+  L.apply = align_up(L.fresh + 8 * (A.num_segments ? A.num_segments : 1));
+  const size_t apply_ws = h.index_coding == DELTA_CODING_LEB128
+                              ? delta_apply_leb128_workspace_bytes(h.idx_bytes, (int32_t)h.num_tensors)
+                              : delta_apply_multi_workspace_bytes((int32_t)h.num_tensors);
+  L.total = align_up(L.apply + apply_ws);
+  return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t delta_artifact_pack_workspace_bytes(uint64_t count, int32_t num_tensors,
+                                           uint32_t index_coding) {
+  if (num_tensors < 0 || index_coding > DELTA_CODING_LEB128 || count > (1ull << 56)) return 0;
+  return pack_layout(count, num_tensors, index_coding == DELTA_CODING_LEB128).total;
+}
+
+delta_status_t delta_artifact_pack(const int64_t* idx, const uint16_t* val, uint64_t count,
+                                   const uint64_t* d_tensor_offsets, const uint64_t* numels,
+                                   int32_t num_tensors, uint32_t index_coding, uint64_t version,
+                                   uint64_t base_version, uint64_t seg_bytes, void* d_artifact,
+                                   size_t artifact_bytes, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream, delta_artifact_header_t* h_header,
+                                   uint64_t* h_total_bytes) {
+  if (num_tensors < 0 || (num_tensors > 0 && (!numels || !d_tensor_offsets)))
+    return fail(DELTA_ERR_INVALID_ARG, "bad tensor list");
+  if (count > 0 && (!idx || !val)) return fail(DELTA_ERR_INVALID_ARG, "idx/val is NULL");
+  if ((uintptr_t)idx % 8 || odd(val)) return fail(DELTA_ERR_INVALID_ARG, "idx/val misaligned");
+  if (index_coding > DELTA_CODING_LEB128)
+    return fail(DELTA_ERR_INVALID_ARG, "unknown index coding %u", index_coding);
+  if (seg_bytes < 32 || seg_bytes % 32)
+    return fail(DELTA_ERR_INVALID_ARG, "seg_bytes must be a positive multiple of 32");
+  if (!d_artifact || (uintptr_t)d_artifact % 8)
+    return fail(DELTA_ERR_INVALID_ARG, "artifact must be a non-NULL, 8-byte aligned buffer");
+  if (count > (1ull << 56)) return fail(DELTA_ERR_INVALID_ARG, "count too large");
+  const bool leb = index_coding == DELTA_CODING_LEB128;
+  // tensor bases (Sec. 5.1 block offsets) from the sizes
+  const size_t T = (size_t)num_tensors;
+  std::vector<uint64_t> nums(numels, numels + T), bases(T, 0);
+  uint64_t words = 0;
+  for (size_t t = 0; t < T; ++t) {
+    bases[t] = words;
+    if (words + nums[t] < words) return fail(DELTA_ERR_INVALID_ARG, "total size overflows");
+    words += nums[t];
+  }
+  if (count > words) return fail(DELTA_ERR_INVALID_ARG, "more entries than words");
+  const PackLayout P = pack_layout(count, num_tensors, leb);
+  delta_status_t st = check_workspace(workspace, workspace_bytes, P.total);
+  if (st != DELTA_OK) return st;
+  char* ws = (char*)workspace;
+  uint8_t* art = (uint8_t*)d_artifact;
+  // the entry offsets must describe `count` entries
+  if (T > 0) {
+    uint64_t ends[2];
+    st = read_back(&ends[0], d_tensor_offsets, 8, stream);
+    if (st == DELTA_OK) st = read_back(&ends[1], d_tensor_offsets + T, 8, stream);
+    if (st != DELTA_OK) return st;
+    if (ends[0] != 0 || ends[1] != count)
+      return fail(DELTA_ERR_INVALID_ARG, "tensor_offsets run from %llu to %llu, not 0 to %llu",
+                  (unsigned long long)ends[0], (unsigned long long)ends[1],
+                  (unsigned long long)count);
+  } else if (count > 0) {
+    return fail(DELTA_ERR_INVALID_ARG, "entries without tensors");
+  }
+  hipError_t e = hipSuccess;
+  if (T > 0) {
+    e = launch_upload_words(nums.data(), T, (uint64_t*)(ws + P.numels), stream);
+    if (e == hipSuccess) e = launch_upload_words(bases.data(), T, (uint64_t*)(ws + P.bases), stream);
+    if (e != hipSuccess) return hip_fail(e, "table upload launch");
+  }
+  // The index stream starts right after the table whatever its length; with
+  // LEB128 coding its length (hence where the values go) is known only
+  // after encoding.
+  const ArtifactLayout L0 = artifact_layout(T, count, 0, seg_bytes);
+  uint64_t idx_bytes = 8 * count;
+  if (leb) {
+    EncArgs a;
+    memset(&a, 0, sizeof(a));
+    a.idx = idx;
+    a.count = count;
+    // one segment per tensor, its first entry coded as its tensor-local index
+    if (T > 0) a.segs = {d_tensor_offsets, (const uint64_t*)(ws + P.bases), (uint32_t)T, 0};
+    a.out = art + L0.idx;
+    a.capacity = artifact_bytes > L0.idx ? artifact_bytes - L0.idx : 0;
+    a.d_nbytes = (uint64_t*)(ws + P.nbytes);
+    a.seg_byte_offsets = T > 0 ? (uint64_t*)(ws + P.byte_offs) : nullptr;
+    a.err = (uint32_t*)(ws + P.err);
+    a.tile_bytes = (uint32_t*)(ws + P.enc + enc_layout(count).tile_bytes);
+    a.group_excl = nullptr;
+    e = launch_reset((uint64_t*)(ws + P.err), nullptr, 0, stream);
+    const EncLayout EL = enc_layout(count);
+    if (e == hipSuccess)
+      e = launch_leb128_encode(a, (uint64_t*)(ws + P.enc + EL.group_sum),
+                               (uint64_t*)(ws + P.enc + EL.group_excl), stream);
+    if (e != hipSuccess) return hip_fail(e, "encode launch");
+    uint64_t got[2];
+    st = read_back(&got[0], ws + P.nbytes, 8, stream);
+    if (st == DELTA_OK) st = read_back(&got[1], ws + P.err, 8, stream);
+    if (st != DELTA_OK) return st;
+    if (got[1] & 0xFFFFFFFFull)
+      return fail(DELTA_ERR_INVALID_ARG, "indices not strictly increasing within a tensor");
+    idx_bytes = got[0];
+  }
+  const ArtifactLayout L = artifact_layout(T, count, idx_bytes, seg_bytes);
+  if (h_total_bytes) *h_total_bytes = L.total;
+  if (artifact_bytes < L.total)
+    return fail(DELTA_ERR_CAPACITY, "artifact needs %llu bytes, buffer has %zu",
+                (unsigned long long)L.total, artifact_bytes);
+  if (!leb && count > 0)
+    e = hipMemcpyAsync(art + L.idx, idx, 8 * count, hipMemcpyDeviceToDevice, stream);
+  if (e == hipSuccess && count > 0)
+    e = hipMemcpyAsync(art + L.val, val, 2 * count, hipMemcpyDeviceToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "stream copy");
+  e = launch_artifact_table(art, L, (const uint64_t*)(ws + P.numels), d_tensor_offsets,
+                            leb ? (const uint64_t*)(ws + P.byte_offs) : nullptr, (uint32_t)T,
+                            idx_bytes, count, stream);
+  if (e != hipSuccess) return hip_fail(e, "table launch");
+  delta_artifact_header_t h;
+  memset(&h, 0, sizeof(h));
+  memcpy(h.magic, "AURDELTA", 8);
+  h.format = DELTA_ARTIFACT_FORMAT;
+  h.index_coding = index_coding;
+  h.version = version;
+  h.base_version = base_version;
+  h.num_tensors = T;
+  h.total_words = words;
+  h.count = count;
+  h.idx_bytes = idx_bytes;
+  h.seg_bytes = seg_bytes;
+  h.num_segments = L.num_segments;
+  e = launch_artifact_seal(art, L, h, stream);
+  if (e != hipSuccess) return hip_fail(e, "seal launch");
+  st = read_back(h_header ? (void*)h_header : (void*)&h, art, sizeof(h), stream);
+  if (st != DELTA_OK) return st;
+  return ok();
+}
+
+size_t delta_artifact_activate_workspace_bytes(const delta_artifact_header_t* header) {
+  ArtifactLayout A;
+  if (!layout_of(header, &A) || header->index_coding > DELTA_CODING_LEB128) return 0;
+  return activate_layout(A, *header).total;
+}
+
+delta_status_t delta_artifact_activate(const void* d_artifact, size_t artifact_bytes,
+                                       const delta_artifact_header_t* header,
+                                       uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                       int32_t num_tensors, uint64_t active_version,
+                                       void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream) {
+  ArtifactLayout A;
+  if (!layout_of(header, &A) || header->index_coding > DELTA_CODING_LEB128)
+    return fail(DELTA_ERR_INVALID_ARG, "bad header");
+  if (memcmp(header->magic, "AURDELTA", 8) || header->format != DELTA_ARTIFACT_FORMAT)
+    return fail(DELTA_ERR_VERSION, "not an artifact of format %d", DELTA_ARTIFACT_FORMAT);
+  if (header->num_segments != A.num_segments)
+    return fail(DELTA_ERR_INVALID_ARG, "header says %llu segments, layout %llu",
+                (unsigned long long)header->num_segments, (unsigned long long)A.num_segments);
+  if (!d_artifact || (uintptr_t)d_artifact % 8 || artifact_bytes < A.total)
+    return fail(DELTA_ERR_INVALID_ARG, "artifact buffer too small or misaligned");
+  // Sec. 5.2: a delta is activated only onto the version it was made against
+  if (header->base_version != active_version)
+    return fail(DELTA_ERR_VERSION, "delta of version %llu is based on %llu, active version is %llu",
+                (unsigned long long)header->version, (unsigned long long)header->base_version,
+                (unsigned long long)active_version);
+  std::vector<uint64_t> bases, ptrs;
+  delta_status_t st = weight_table(weight_ptrs, numels, num_tensors, bases, ptrs);
+  if (st != DELTA_OK) return st;
+  if ((uint64_t)num_tensors != header->num_tensors || bases[num_tensors] != header->total_words)
+    return fail(DELTA_ERR_INVALID_ARG, "the artifact is for %llu tensors of %llu words, got %d of %llu",
+                (unsigned long long)header->num_tensors, (unsigned long long)header->total_words,
+                num_tensors, (unsigned long long)bases[num_tensors]);
+  const ActivateLayout W = activate_layout(A, *header);
+  st = check_workspace(workspace, workspace_bytes, W.total);
+  if (st != DELTA_OK) return st;
+  char* ws = (char*)workspace;
+  const uint8_t* art = (const uint8_t*)d_artifact;
+  // verify every segment hash and the artifact hash before touching the weights
+  hipError_t e = launch_artifact_verify(art, A, header->seg_bytes, header->version,
+                                        (uint64_t*)(ws + W.fresh), (uint64_t*)(ws + W.bad),
+                                        (uint64_t*)(ws + W.first_bad),
+                                        (uint32_t*)(ws + W.header_bad), stream);
+  if (e != hipSuccess) return hip_fail(e, "verify launch");
+  uint64_t res[3];
+  st = read_back(res, ws + W.bad, 24, stream);
+  if (st != DELTA_OK) return st;
+  if (res[0] != 0 || (res[2] & 0xFFFFFFFFull))
+    return fail(DELTA_ERR_INTEGRITY, "artifact fails its hashes: %llu segments differ (first %llu), "
+                "artifact hash %s", (unsigned long long)res[0], (unsigned long long)res[1],
+                (res[2] & 0xFFFFFFFFull) ? "differs" : "ok");
+  // the (verified) tensor table: sizes must match, entry offsets ascending
+  const size_t T = (size_t)num_tensors;
+  std::vector<uint64_t> table(3 * T + 1, 0);
+  st = read_back(table.data(), art + A.table, 24 * T, stream);
+  if (st != DELTA_OK) return st;
+  std::vector<uint64_t> offs(T + 1, 0);
+  for (size_t t = 0; t < T; ++t) {
+    if (table[3 * t] != numels[t])
+      return fail(DELTA_ERR_INVALID_ARG, "tensor %zu: the artifact has %llu words, got %llu", t,
+                  (unsigned long long)table[3 * t], (unsigned long long)numels[t]);
+    offs[t] = table[3 * t + 1];
+    if (offs[t] > header->count || (t > 0 && offs[t] < offs[t - 1]))
+      return fail(DELTA_ERR_INVALID_ARG, "artifact table: entry offsets out of order");
+  }
+  offs[T] = header->count;
+  if (T > 0 && offs[0] != 0) return fail(DELTA_ERR_INVALID_ARG, "artifact table: first offset");
+  e = launch_reset((uint64_t*)(ws + W.err), nullptr, 0, stream);
+  if (e != hipSuccess) return hip_fail(e, "reset launch");
+  uint32_t* err = (uint32_t*)(ws + W.err);
+  const uint16_t* val = (const uint16_t*)(art + A.val);
+  if (header->index_coding == DELTA_CODING_LEB128) {
+    e = launch_upload_words(offs.data(), T + 1, (uint64_t*)(ws + W.offs), stream);
+    if (e != hipSuccess) return hip_fail(e, "offsets upload launch");
+    // one segment per tensor, each based at its tensor's first global index
+    st = delta_apply_leb128_multi(weight_ptrs, numels, num_tensors, art + A.idx, header->idx_bytes,
+                                  (const uint64_t*)(ws + W.offs), nullptr, (uint32_t)T, val,
+                                  header->count, err, ws + W.apply, workspace_bytes - W.apply,
+                                  stream);
+  } else {
+    st = delta_apply_multi(weight_ptrs, numels, num_tensors, (const int64_t*)(art + A.idx), val,
+                           header->count, err, ws + W.apply, workspace_bytes - W.apply, stream);
+  }
+  if (st != DELTA_OK) return st;
+  uint64_t flag = 0;
+  st = read_back(&flag, err, 8, stream);
+  if (st != DELTA_OK) return st;
+  if (flag & 0xFFFFFFFFull)
+    return fail(DELTA_ERR_OUT_OF_RANGE, "malformed index stream or an index outside the tensors");
+  return ok();
+}
+
+delta_status_t delta_chunk_segments(const uint64_t* chunk_counts, uint64_t num_chunks,
+                                    uint64_t chunk_elems, uint64_t* seg_offsets,
+                                    uint64_t* seg_bases) {
+  if (num_chunks > 0 && (!chunk_counts || !seg_bases))
+    return fail(DELTA_ERR_INVALID_ARG, "NULL host array");
+  if (!seg_offsets) return fail(DELTA_ERR_INVALID_ARG, "seg_offsets is NULL");
+  if (num_chunks > 0 && chunk_elems == 0) return fail(DELTA_ERR_INVALID_ARG, "chunk_elems is 0");
+  if (num_chunks > 0 && num_chunks - 1 > UINT64_MAX / (chunk_elems ? chunk_elems : 1))
+    return fail(DELTA_ERR_INVALID_ARG, "chunk bases overflow");
+  uint64_t at = 0;
+  for (uint64_t c = 0; c < num_chunks; ++c) {
+    seg_offsets[c] = at;
+    seg_bases[c] = c * chunk_elems;
+    if (at + chunk_counts[c] < at) return fail(DELTA_ERR_INVALID_ARG, "counts overflow");
+    at += chunk_counts[c];
+  }
+  seg_offsets[num_chunks] = at;
   return ok();
 }
 

@@ -23,6 +23,12 @@ ArtifactLayout artifact_layout(uint64_t num_tensors, uint64_t count, uint64_t id
 
 hipError_t launch_hash_segments(const uint8_t* data, uint64_t nbytes, uint64_t seg_bytes,
                                 uint64_t seed, uint64_t* out, hipStream_t stream);
+// Writes the tensor table from device arrays (numels [T], entry offsets
+// [T + 1], first index bytes [T] or NULL for 8 bytes per entry) and zeroes
+// the alignment padding after the index and value streams.
+hipError_t launch_artifact_table(uint8_t* art, const ArtifactLayout& L, const uint64_t* numels,
+                                 const uint64_t* offs, const uint64_t* byte_offs, uint32_t T,
+                                 uint64_t idx_bytes, uint64_t count, hipStream_t stream);
 hipError_t launch_artifact_seal(uint8_t* art, const ArtifactLayout& L,
                                 const delta_artifact_header_t& h, hipStream_t stream);
 hipError_t launch_artifact_verify(const uint8_t* art, const ArtifactLayout& L, uint64_t seg_bytes,

@@ -175,6 +175,38 @@ ArtifactLayout artifact_layout(uint64_t num_tensors, uint64_t count, uint64_t id
   return L;
 }
 
+// The artifact's tensor table (one row {words, first entry, first index
+// byte} per tensor) and the zero padding that aligns the value stream and
+// the hash table: every byte of [table, hashes) is then written, so the
+// segment hashes do not depend on what the buffer held before.
+__global__ __launch_bounds__(256) void artifact_table_kernel(uint8_t* art, ArtifactLayout L,
+                                                             const uint64_t* numels,
+                                                             const uint64_t* offs,
+                                                             const uint64_t* byte_offs,
+                                                             uint32_t T, uint64_t idx_bytes,
+                                                             uint64_t count) {
+  uint64_t* rows = (uint64_t*)(art + L.table);
+  for (uint32_t t = blockIdx.x * blockDim.x + threadIdx.x; t < T; t += gridDim.x * blockDim.x) {
+    rows[3 * (uint64_t)t + 0] = numels[t];
+    rows[3 * (uint64_t)t + 1] = offs[t];
+    rows[3 * (uint64_t)t + 2] = byte_offs ? byte_offs[t] : 8 * offs[t];
+  }
+  if (blockIdx.x == 0 && threadIdx.x < 8) {
+    const uint64_t a = L.idx + idx_bytes, b = L.val + 2 * count;
+    if (a + threadIdx.x < L.val) art[a + threadIdx.x] = 0;
+    if (b + threadIdx.x < L.hashes) art[b + threadIdx.x] = 0;
+  }
+}
+
+hipError_t launch_artifact_table(uint8_t* art, const ArtifactLayout& L, const uint64_t* numels,
+                                 const uint64_t* offs, const uint64_t* byte_offs, uint32_t T,
+                                 uint64_t idx_bytes, uint64_t count, hipStream_t stream) {
+  const uint32_t blocks = T ? (T + 255) / 256 : 1;
+  hipLaunchKernelGGL(artifact_table_kernel, dim3(blocks < 64 ? blocks : 64), dim3(256), 0, stream,
+                     art, L, numels, offs, byte_offs, T, idx_bytes, count);
+  return hipGetLastError();
+}
+
 hipError_t launch_artifact_seal(uint8_t* art, const ArtifactLayout& L,
                                 const delta_artifact_header_t& h, hipStream_t stream) {
   hipLaunchKernelGGL(artifact_header_kernel, dim3(1), dim3(128), 0, stream, art, h);

@@ -263,7 +263,10 @@ static size_t staging_bytes_impl(const uint64_t* numels, int32_t num_tensors,
       num_tensors < 0 || (num_tensors > 0 && !numels))
     return 0;
   uint64_t total = 0;
-  for (int32_t t = 0; t < num_tensors; ++t) total += numels[t];
+  for (int32_t t = 0; t < num_tensors; ++t) {
+    if (total + numels[t] < total) return 0;   // sizes overflow
+    total += numels[t];
+  }
   const uint64_t chunk = opts->chunk_elems < total ? opts->chunk_elems : (total ? total : 1);
   const uint64_t nchunks = (total + chunk - 1) / chunk;
   const size_t ws = max_chunk_workspace(numels, num_tensors, total, chunk, leb);
@@ -323,7 +326,15 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
       set_error("tensor %d: odd address", t);
       return DELTA_ERR_INVALID_ARG;
     }
+    if (total + numels[t] < total) {
+      set_error("total size overflows");
+      return DELTA_ERR_INVALID_ARG;
+    }
     total += numels[t];
+  }
+  if (total > 0 && total - 1 > 0x7FFFFFFFFFFFFFFFull) {
+    set_error("total size exceeds int64");
+    return DELTA_ERR_INDEX_OVERFLOW;
   }
   const int S = opts->num_streams;
   *h_count = 0;

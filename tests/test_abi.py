@@ -406,3 +406,106 @@ def test_fused_validation(lib):
     assert call([0, 12], [16]) == _abi.DELTA_ERR_INVALID_ARG     # block outside target
     bad_t = (ctypes.c_int32 * 2)(0, 2)
     assert call([0, 0], [10, 6], nt=2, tgt=bad_t) == _abi.DELTA_ERR_INVALID_ARG
+
+
+def test_chunk_segments(lib):
+    U = ctypes.c_uint64
+    counts = (U * 4)(5, 0, 7, 1)
+    offs = (U * 5)()
+    bases = (U * 4)()
+    assert lib.delta_chunk_segments(counts, 4, 100, offs, bases) == _abi.DELTA_OK
+    assert list(offs) == [0, 5, 5, 12, 13]
+    assert list(bases) == [0, 100, 200, 300]
+    assert lib.delta_chunk_segments(None, 0, 100, offs, None) == _abi.DELTA_OK
+    assert offs[0] == 0
+    assert lib.delta_chunk_segments(counts, 4, 0, offs, bases) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_chunk_segments(counts, 4, 100, None, bases) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_chunk_segments(counts, 3, 1 << 63, offs, bases) == \
+        _abi.DELTA_ERR_INVALID_ARG   # chunk bases overflow
+
+
+def test_artifact_pack_and_activate_validation(lib):
+    U = ctypes.c_uint64
+    numels = (U * 2)(100, 50)
+    h = _abi.delta_artifact_header_t()
+    tot = U(0)
+    ws_need = lib.delta_artifact_pack_workspace_bytes(10, 2, _abi.DELTA_CODING_LEB128)
+    assert ws_need > 0
+    assert lib.delta_artifact_pack_workspace_bytes(10, 2, 7) == 0
+    args = dict(idx=FAKE, val=FAKE, count=10, offs=FAKE, coding=_abi.DELTA_CODING_INT64,
+                seg=64, art=FAKE, art_bytes=1 << 20, ws=FAKE, ws_bytes=1 << 20)
+
+    def pack(**kw):
+        a = dict(args, **kw)
+        return lib.delta_artifact_pack(a["idx"], a["val"], a["count"], a["offs"], numels, 2,
+                                       a["coding"], 2, 1, a["seg"], a["art"], a["art_bytes"],
+                                       a["ws"], a["ws_bytes"], None, ctypes.byref(h),
+                                       ctypes.byref(tot))
+    assert pack(coding=5) == _abi.DELTA_ERR_INVALID_ARG
+    assert pack(seg=48) == _abi.DELTA_ERR_INVALID_ARG
+    assert pack(idx=FAKE + 4) == _abi.DELTA_ERR_INVALID_ARG
+    assert pack(val=FAKE + 1) == _abi.DELTA_ERR_INVALID_ARG
+    assert pack(art=FAKE + 4) == _abi.DELTA_ERR_INVALID_ARG
+    assert pack(count=151) == _abi.DELTA_ERR_INVALID_ARG   # more entries than words
+    assert pack(offs=None) == _abi.DELTA_ERR_INVALID_ARG
+    assert pack(ws_bytes=8) == _abi.DELTA_ERR_WORKSPACE
+    # activate: the base version is checked before anything is enqueued
+    h = _abi.delta_artifact_header_t()
+    h.magic = b"AURDELTA"
+    h.format = _abi.DELTA_ARTIFACT_FORMAT
+    h.index_coding = _abi.DELTA_CODING_INT64
+    h.version, h.base_version = 5, 4
+    h.num_tensors, h.total_words, h.count = 2, 150, 10
+    h.idx_bytes, h.seg_bytes = 80, 64
+    L = _abi.delta_artifact_layout_t()
+    assert lib.delta_artifact_layout(2, 10, 80, 64, ctypes.byref(L)) == _abi.DELTA_OK
+    h.num_segments = L.num_segments
+    ptrs = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    wsb = lib.delta_artifact_activate_workspace_bytes(ctypes.byref(h))
+    assert wsb > 0
+    assert lib.delta_artifact_activate(FAKE, L.total, ctypes.byref(h), ptrs, numels, 2, 3, FAKE,
+                                       wsb, None) == _abi.DELTA_ERR_VERSION
+    assert b"based on 4" in lib.delta_last_error()
+    # other tensors than the artifact's
+    assert lib.delta_artifact_activate(FAKE, L.total, ctypes.byref(h), ptrs, numels, 1, 4, FAKE,
+                                       wsb, None) == _abi.DELTA_ERR_INVALID_ARG
+    # a buffer shorter than the layout, a bad magic
+    assert lib.delta_artifact_activate(FAKE, L.total - 8, ctypes.byref(h), ptrs, numels, 2, 4,
+                                       FAKE, wsb, None) == _abi.DELTA_ERR_INVALID_ARG
+    h.magic = b"NOTDELTA"
+    assert lib.delta_artifact_activate(FAKE, L.total, ctypes.byref(h), ptrs, numels, 2, 4, FAKE,
+                                       wsb, None) == _abi.DELTA_ERR_VERSION
+    assert lib.delta_status_string(_abi.DELTA_ERR_INTEGRITY) == b"DELTA_ERR_INTEGRITY"
+
+
+def test_apply_leb128_multi_validation(lib):
+    U = ctypes.c_uint64
+    numels = (U * 2)(100, 50)
+    ptrs = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    need = lib.delta_apply_leb128_workspace_bytes(64, 2)
+    # odd value stream
+    assert lib.delta_apply_leb128_multi(ptrs, numels, 2, FAKE, 64, FAKE, FAKE, 2, FAKE + 1, 10,
+                                        None, FAKE, need, None) == _abi.DELTA_ERR_INVALID_ARG
+    # tensor sizes whose sum overflows
+    big = (U * 2)(1 << 63, 1 << 63)
+    assert lib.delta_apply_leb128_multi(ptrs, big, 2, FAKE, 64, FAKE, FAKE, 2, FAKE, 10, None,
+                                        FAKE, need, None) == _abi.DELTA_ERR_INVALID_ARG
+    # per-tensor bases (d_seg_bases NULL) need one segment per tensor
+    assert lib.delta_apply_leb128_multi(ptrs, numels, 2, FAKE, 64, FAKE, None, 3, FAKE, 10, None,
+                                        FAKE, need, None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_apply_leb128_multi(ptrs, numels, 2, FAKE, 64, None, None, 2, FAKE, 10, None,
+                                        FAKE, need, None) == _abi.DELTA_ERR_INVALID_ARG
+
+
+def test_pipeline_sizes_overflow(lib):
+    numels = (ctypes.c_uint64 * 2)(1 << 63, 1 << 63)
+    opts = _abi.delta_pipeline_opts_t(1 << 27, 4, 0)
+    assert lib.delta_pipeline_staging_bytes(numels, 2, ctypes.byref(opts)) == 0
+    P = ctypes.c_void_p
+    ptrs = (P * 2)(FAKE, FAKE)
+    streams = (P * 4)(None, None, None, None)
+    cnt = ctypes.c_uint64(0)
+    assert lib.delta_extract_pipelined(ptrs, ptrs, numels, 2, ctypes.byref(opts), streams, FAKE,
+                                       1 << 20, FAKE, FAKE, 10, ctypes.byref(cnt)) == \
+        _abi.DELTA_ERR_INVALID_ARG
+    assert b"overflows" in lib.delta_last_error()
