@@ -520,10 +520,16 @@ def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
 
 def single_tensor_measurement(ad, synth, stream, reps):
     """One 2048 x 2048 bf16 tensor with 1% of its words changed, int32
-    indices (delta_extract).  Its two copies (16.8 MB) fit in the 256 MB
-    last-level cache: "warm" repeats the call back to back; "cold" first
-    writes a 1 GiB scratch buffer, which evicts them.  HIP events on the
-    launch stream around each call; the scan kernel's own events beside."""
+    indices.  Its two copies (16.8 MB) fit in the 256 MB last-level cache:
+    "warm" repeats the call; "cold" first writes a 1 GiB scratch buffer,
+    which evicts them.  Times are the GPU's: HIP events on the launch stream
+    around each call, with a short spin kernel enqueued first so that the
+    host has enqueued the whole call before the GPU reaches it (as in a
+    stream of calls); the host's own enqueue time and the time with the host
+    enqueuing inside the bracket are reported beside.  delta_extract (two
+    launches: scan, then a per-tile finalize) and delta_extract_noalloc
+    (the same kernels on the library's fixed scratch), each also replayed
+    from a HIP graph."""
     import torch
     dev = torch.device("cuda")
     n = 2048 * 2048
@@ -535,39 +541,88 @@ def single_tensor_measurement(ad, synth, stream, reps):
     ws = torch.empty(ad.delta_extract_workspace_bytes(n), dtype=torch.uint8, device=dev)
     scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     lib = ad.library()
+    med = lambda xs: sorted(xs)[len(xs) // 2]
+    spin = 200_000   # cycles of the spin kernel ahead of each timed call
 
-    def call():
-        ad.delta_extract_into(prev, new, idx, val, cnt, ws, stream)
-
-    for _ in range(3):
-        call()
-    stream.synchronize()
-    if int(cnt.item()) != K:
-        raise RuntimeError("config 1: wrong count")
-    out = {}
-    for mode in ("warm", "cold"):
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
-        for i, (e0, e1, s0, s1) in enumerate(ev):
-            if mode == "cold":
-                scratch.fill_(i & 0xFF)
-            s0.record(stream)
-            s1.record(stream)
-            if lib.delta_set_scan_events(s0.cuda_event, s1.cuda_event):
-                raise RuntimeError(lib.delta_last_error().decode())
-            e0.record(stream)
+    def run(call, graph):
+        out = {}
+        for _ in range(3):
             call()
-            e1.record(stream)
         stream.synchronize()
-        lib.delta_set_scan_events(None, None)
-        med = lambda xs: sorted(xs)[len(xs) // 2]
-        call_ms = med([e0.elapsed_time(e1) for e0, e1, _, _ in ev])
-        scan_ms = med([s0.elapsed_time(s1) for _, _, s0, s1 in ev])
-        out[mode] = {"ms": round(call_ms, 4), "scan_kernel_ms": round(scan_ms, 4),
-                     "GBps_scanned": round(4 * n / (call_ms / 1e3) / 1e9, 1),
-                     "scan_kernel_GBps": round(4 * n / (scan_ms / 1e3) / 1e9, 1)}
+        if int(cnt.item()) != K:
+            raise RuntimeError("config 1: wrong count")
+        t = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            call()
+            t.append(time.perf_counter() - t0)
+            stream.synchronize()
+        out["host_enqueue_us"] = round(med(t) * 1e6, 2)
+        for mode in ("warm", "cold", "host_bound"):
+            # the whole call, then (a second pass) the scan kernel alone,
+            # bracketed by the library's own events
+            times = []
+            for scan in (False, True):
+                ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                      for _ in range(reps)]
+                with torch.cuda.stream(stream):
+                    for i, (e0, e1) in enumerate(ev):
+                        if mode == "cold":
+                            scratch.fill_(i & 0xFF)
+                        if scan:
+                            e0.record(stream)   # torch creates an event on its first record
+                            e1.record(stream)
+                            if lib.delta_set_scan_events(e0.cuda_event, e1.cuda_event):
+                                raise RuntimeError(lib.delta_last_error().decode())
+                        if mode != "host_bound":
+                            torch.cuda._sleep(spin)
+                        if not scan:
+                            e0.record(stream)
+                        call()
+                        if not scan:
+                            e1.record(stream)
+                stream.synchronize()
+                lib.delta_set_scan_events(None, None)
+                times.append(med([e0.elapsed_time(e1) for e0, e1 in ev]))
+            call_ms, scan_ms = times
+            if mode == "host_bound":
+                out["host_bound_ms"] = round(call_ms, 4)
+                continue
+            out[mode] = {"ms": round(call_ms, 4), "scan_kernel_ms": round(scan_ms, 4),
+                         "GBps_scanned": round(4 * n / (call_ms / 1e3) / 1e9, 1)}
+        # the same call captured once into a HIP graph (on a side stream, as
+        # capture requires) and replayed on the launch stream
+        cs = torch.cuda.Stream()
+        cs.wait_stream(stream)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cs):
+            graph(cs)
+        stream.wait_stream(cs)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps)]
+        with torch.cuda.stream(stream):
+            for e0, e1 in ev:
+                torch.cuda._sleep(spin)
+                e0.record(stream)
+                g.replay()
+                e1.record(stream)
+        stream.synchronize()
+        if int(cnt.item()) != K:
+            raise RuntimeError("config 1: wrong count after graph replays")
+        gm = med([e0.elapsed_time(e1) for e0, e1 in ev])
+        out["graph_warm"] = {"ms": round(gm, 4), "GBps_scanned": round(4 * n / (gm / 1e3) / 1e9, 1)}
+        del g
+        return out
+
+    noalloc = run(lambda: ad.delta_extract_noalloc_into(prev, new, idx, val, cnt, stream),
+                  lambda s: ad.delta_extract_noalloc_into(prev, new, idx, val, cnt, s))
+    extract = run(lambda: ad.delta_extract_into(prev, new, idx, val, cnt, ws, stream),
+                  lambda s: ad.delta_extract_into(prev, new, idx, val, cnt, ws, s))
     del scratch
     return {"workload": f"one 2048 x 2048 bf16 tensor, {K} changed words (1%), int32 indices",
-            **out}
+            "entry": "delta_extract (two launches: scan, per-tile finalize)",
+            "warm": extract["warm"], "cold": extract["cold"],
+            "delta_extract": dict(extract, launches=2),
+            "delta_extract_noalloc": noalloc}
 
 
 def hash_measurement(ad, buf, stream, reps):

@@ -62,7 +62,7 @@ struct TensorDesc {
 static_assert(sizeof(TensorDesc) == 64, "TensorDesc layout");
 
 constexpr size_t kAlign = 256;
-__host__ __device__ inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+__host__ __device__ constexpr size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
 
 // Words between the 16-byte boundary at or below p and p (p is 2-aligned).
 __host__ __device__ inline uint32_t head_words(const void* p) {
@@ -211,6 +211,10 @@ struct StageSplit {
 // split: nullable, as above.
 hipError_t launch_extract(const ExtractArgs& a, bool idx64, bool all_vec, hipStream_t stream,
                           const StageSplit* split = nullptr);
+
+// A single-tensor call over at most this many tiles finalizes each tile in
+// its own workgroup (two launches in all, no group scan).
+constexpr uint64_t kSmallTiles = 1024;
 
 // Count only: the scan and the tile counts, then the group sums and scan
 // that leave the total in *a.d_count; nothing is staged or written.

@@ -548,6 +548,81 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(ExtractArgs a) {
   }
 }
 
+// -------------------------------------------------- small single-tensor calls
+//
+// A call over few tiles is bound by its launches, not by memory: the
+// group scan and a finalize of one workgroup per 64 tiles (8 workgroups
+// for a 2048 x 2048 tensor) cost more than the scan itself.  For one
+// tensor over at most kSmallTiles tiles, finalize_small runs one workgroup
+// per tile after the stage kernel: it sums the counts of the tiles before
+// its own (read from L2) and copies its slot, two launches in all.
+
+// Sum of counts[0, n) over the workgroup (every thread gets it).
+__device__ __forceinline__ uint64_t sum_counts_before(const uint32_t* counts, uint64_t n,
+                                                      uint64_t* s_part) {
+  uint64_t v = 0;
+  for (uint64_t i = threadIdx.x; i < n; i += kThreads) v += counts[i];
+  v = wave_sum64(v);
+  if (lane_id() == 0) s_part[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint64_t total = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) total += s_part[w];
+  return total;
+}
+
+// Writes one tile's entries in output order straight from a tile scan,
+// entry r of the tile at position excl + r (for a tile that overflowed its
+// staging slot).
+template <typename IdxT>
+__device__ __forceinline__ void write_scanned_tile(const ExtractArgs& a, const TileScan& s,
+                                                   int64_t lane_out, uint64_t excl) {
+  IdxT* out_idx = reinterpret_cast<IdxT*>(a.out_idx);
+#pragma unroll
+  for (int u = 0; u < kChunks; ++u) {
+    uint32_t m = s.mask[u];
+    uint64_t pos = excl + s.rank[u];
+    const int64_t e0 = lane_out + 512 * u;
+    while (m) {
+      const int j = __builtin_ctz(m);
+      m &= m - 1;
+      if (pos < a.capacity) {
+        out_idx[pos] = (IdxT)(e0 + j);
+        a.out_val[pos] = word_of(s.q[u], j);
+      }
+      ++pos;
+    }
+  }
+}
+
+template <typename IdxT, bool kVec>
+__global__ __launch_bounds__(kThreads) void finalize_small_kernel(ExtractArgs a) {
+  __shared__ uint64_t s_part[kWaves];
+  __shared__ uint32_t s_wave_total[kWaves];
+  const uint64_t tile = blockIdx.x;
+  const uint64_t excl = sum_counts_before(a.counts, tile, s_part);
+  const uint32_t count = a.counts[tile];
+  if (tile == a.num_tiles - 1 && threadIdx.x == 0) *a.d_count = excl + count;
+  const TensorDesc d = a.inl[0];
+  const int64_t base = tile_out_base(d, tile);
+  IdxT* out_idx = reinterpret_cast<IdxT*>(a.out_idx);
+  if (count <= a.stage_cap) {
+    const uint32_t* slot = a.stage + tile * a.stage_stride;
+    for (uint32_t r = threadIdx.x; r < count; r += kThreads) {
+      if (excl + r >= a.capacity) break;
+      const uint32_t v = __builtin_nontemporal_load(slot + r);
+      out_idx[excl + r] = (IdxT)(base + (v & 0xFFFFu));
+      a.out_val[excl + r] = (uint16_t)(v >> 16);
+    }
+  } else {
+    // the tile overflowed its slot: read it again
+    const uint32_t lane = lane_id(), wave = threadIdx.x >> 6;
+    TileScan s;
+    scan_tile<kVec>(d, tile, lane, wave, s_wave_total, s);
+    write_scanned_tile<IdxT>(a, s, base + (int64_t)(wave * kGroupsPerWave + lane) * 8, excl);
+  }
+}
+
 // ------------------------------------------------------------ coded output
 //
 // The chunked pipeline's coded form (gap + LEB128, one segment per call,
@@ -1143,6 +1218,14 @@ static hipError_t launch_all(const ExtractArgs& a, hipStream_t stream, const Sta
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   e = record_scan_event(1, stream);
+  if (e != hipSuccess) return e;
+  // one tensor over few tiles: each tile finalizes itself (two launches)
+  if (!kMulti && !split && a.num_inline == 1 && !a.d_tensor_offsets &&
+      a.num_tiles <= kSmallTiles) {
+    hipLaunchKernelGGL((finalize_small_kernel<IdxT, kVec>), dim3((uint32_t)a.num_tiles),
+                       dim3(kThreads), 0, stream, a);
+    return hipGetLastError();
+  }
   hipStream_t rest;
   if (e == hipSuccess) e = split_after_stage(stream, split, rest);
   if (e != hipSuccess) return e;

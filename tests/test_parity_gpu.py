@@ -113,6 +113,18 @@ def test_sizes(n, density):
     check_extract(prev, new, torch.int32)
 
 
+# A single tensor over at most 1024 tiles takes a two-launch form (each
+# tile finalizes itself); one more tile, the group-scan form.
+@pytest.mark.parametrize("n", [1024 * TILE - 5, 1024 * TILE, 1024 * TILE + 1,
+                               1025 * TILE + 4000])
+@pytest.mark.parametrize("density", [0.01, 0.2])
+def test_small_call_boundary(n, density):
+    say(f"small-call boundary: {n} words at {density}")
+    prev, new = rand_pair(n + 3, density, seed=n % 1000 + int(density * 100))
+    check_extract(prev[:n], new[:n], torch.int32)
+    check_extract(prev[3:], new[3:], torch.int64)   # misaligned, n words
+
+
 @pytest.mark.parametrize("off_p,off_q", [(1, 1), (3, 3), (7, 7), (0, 1), (2, 5), (6, 0), (4, 4)])
 def test_misaligned_views(off_p, off_q):
     n = 3 * TILE + 1001

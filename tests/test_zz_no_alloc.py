@@ -113,3 +113,14 @@ def test_noalloc_refuses_above_maximum():
     with pytest.raises(ad.DeltaError) as ei:
         ad.delta_extract_noalloc_into(p, p, idx, val, cnt)
     assert ei.value.status == _abi.DELTA_ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("n", [8192 * 1024 - 1, 8192 * 1024, 8192 * 1024 + 1])
+def test_noalloc_small_call_boundary(n):
+    say(f"noalloc at the small-call boundary: {n} words")
+    p, q = pair(n + 1, 0.02, 31)
+    check(p[:n], q[:n], torch.int32)
+    check(p[1:], q[1:], torch.int64)
+    # dense: every tile has thousands of entries
+    p, q = pair(n, 0.6, 32)
+    check(p, q, torch.int64)
