@@ -845,7 +845,7 @@ def main():
         return 2
 
     # the probe runs first, in a process of its own, before this one touches the GPU
-    ceilings = None if args.no_ceilings else measure_ceilings()
+    ceilings = None if (args.no_ceilings or args.only_pipeline) else measure_ceilings()
     if ceilings is not None:
         log(f"write ceilings: {ceilings}")
 
