@@ -93,6 +93,27 @@ def _workspace(nbytes: int, device) -> torch.Tensor:
     return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
 
 
+def _adopt(stream: Optional[torch.cuda.Stream], *temps) -> int:
+    """The handle of ``stream`` for a call that uses device buffers this
+    binding has just allocated, filled or copied on the current stream
+    (``temps``; None entries are skipped).
+
+    When ``stream`` is another stream, it first waits for the current one,
+    so the call runs after those fills and copies and after any earlier use
+    of the memory the allocator handed out; and every buffer is recorded on
+    ``stream``, so that its memory is not handed out again before the call
+    has run (the allocator otherwise only waits for the current stream)."""
+    cur = torch.cuda.current_stream()
+    if stream is None or stream == cur:
+        return cur.cuda_stream
+    live = [t for t in temps if t is not None]
+    if live:
+        stream.wait_stream(cur)
+        for t in live:
+            t.record_stream(stream)
+    return stream.cuda_stream
+
+
 # --------------------------------------------------------------- sizes
 
 def delta_extract_workspace_bytes(numel: int) -> int:
@@ -180,6 +201,7 @@ def delta_extract(prev: torch.Tensor, new: torch.Tensor, index_dtype: torch.dtyp
     for _ in range(2):
         idx = torch.empty(cap, dtype=index_dtype, device=dev)
         val = torch.empty(cap, dtype=prev.dtype, device=dev)
+        _adopt(stream, ws, cnt, idx, val)
         delta_extract_into(prev, new, idx, val, cnt, ws, stream)
         (stream or torch.cuda.current_stream()).synchronize()
         k = int(cnt.item())
@@ -244,6 +266,7 @@ def delta_count_changed_multi(prevs: Sequence[torch.Tensor], news: Sequence[torc
     plan = MultiPlan(prevs, news)
     ws = _workspace(plan.workspace_bytes, plan.device)
     cnt = torch.zeros(1, dtype=torch.int64, device=plan.device)
+    _adopt(stream, ws, cnt)
     delta_count_changed_multi_into(plan, cnt, ws, stream)
     (stream or torch.cuda.current_stream()).synchronize()
     return int(cnt.item())
@@ -265,6 +288,7 @@ def delta_extract_multi(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tens
     for _ in range(2):
         idx = torch.empty(cap, dtype=torch.int64, device=dev)
         val = torch.empty(cap, dtype=dtype, device=dev)
+        _adopt(stream, ws, cnt, offs, idx, val)
         delta_extract_multi_into(plan, idx, val, cnt, ws, offs, stream)
         (stream or torch.cuda.current_stream()).synchronize()
         k = int(cnt.item())
@@ -316,6 +340,7 @@ def delta_extract_multi_leb128(prevs: Sequence[torch.Tensor], news: Sequence[tor
     for _ in range(2):
         code = torch.empty(max(ccap, 1), dtype=torch.uint8, device=dev)
         val = torch.empty(max(cap, 1), dtype=dtype, device=dev)
+        _adopt(stream, ws, cnt, nb, offs, boffs, code, val)
         delta_extract_multi_leb128_into(plan, code[:ccap], val[:cap], cnt, nb, ws, offs, boffs,
                                         stream)
         (stream or torch.cuda.current_stream()).synchronize()
@@ -346,7 +371,7 @@ def delta_apply(weights: torch.Tensor, idx: torch.Tensor, val: torch.Tensor,
     _check(library().delta_apply(
         _words(weights, "weights"), weights.numel(), _index_type(idx.dtype), idx.data_ptr(),
         _words(val, "val"), idx.numel(), flag.data_ptr() if flag is not None else None,
-        _stream(stream)))
+        _adopt(stream, flag if flag is not error_flag else None)))
     if check:
         (stream or torch.cuda.current_stream()).synchronize()
         if int(flag.item()) != 0:
@@ -385,7 +410,9 @@ def delta_apply_multi(weights: Sequence[torch.Tensor], idx: torch.Tensor, val: t
     _check(library().delta_apply_multi(
         ptrs, numels, T, idx.data_ptr(), _words(val, "val"), idx.numel(),
         flag.data_ptr() if flag is not None else None, ws.data_ptr(),
-        ws.numel() * ws.element_size(), _stream(stream)))
+        ws.numel() * ws.element_size(),
+        _adopt(stream, ws if ws is not workspace else None,
+               flag if flag is not error_flag else None)))
     if check:
         (stream or torch.cuda.current_stream()).synchronize()
         if int(flag.item()) != 0:
@@ -424,7 +451,8 @@ def delta_compose(deltas: Sequence[Tuple[torch.Tensor, torch.Tensor]],
     _check(library().delta_compose(
         _ptr_array([i.data_ptr() for i, _ in deltas]), _ptr_array([v.data_ptr() for _, v in deltas]),
         _u64_array(counts), len(deltas), out_idx.data_ptr(), out_val.data_ptr(), cap,
-        cnt.data_ptr(), flag.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)))
+        cnt.data_ptr(), flag.data_ptr(), ws.data_ptr(), ws.numel(),
+        _adopt(stream, ws, out_idx, out_val, cnt, flag)))
     (stream or torch.cuda.current_stream()).synchronize()
     if int(flag.item()):
         raise DeltaError(_abi.DELTA_ERR_INVALID_ARG, "index streams are not sorted")
@@ -467,7 +495,9 @@ def delta_apply_chain(weights: Sequence[torch.Tensor],
     _check(library().delta_apply_chain(
         ptrs, numels, T, ip, vp, _u64_array(counts), len(deltas),
         flag.data_ptr() if flag is not None else None, ws.data_ptr(),
-        ws.numel() * ws.element_size(), _stream(stream)))
+        ws.numel() * ws.element_size(),
+        _adopt(stream, ws if ws is not workspace else None,
+               flag if flag is not error_flag else None)))
     if check:
         (stream or torch.cuda.current_stream()).synchronize()
         if int(flag.item()) != 0:
@@ -522,7 +552,7 @@ def delta_extract_fused(prevs: Sequence[torch.Tensor], news: Sequence[torch.Tens
         _check(library().delta_extract_fused(
             plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, T, tgt, boff, tn, F,
             idx.data_ptr(), val.data_ptr(), cap, cnt.data_ptr(), offs.data_ptr(),
-            ws.data_ptr(), ws.numel(), _stream(stream)))
+            ws.data_ptr(), ws.numel(), _adopt(stream, ws, cnt, offs, idx, val)))
         (stream or torch.cuda.current_stream()).synchronize()
         k = int(cnt.item())
         if k <= cap:
@@ -569,7 +599,7 @@ def delta_leb128_encode(idx: torch.Tensor, seg_offsets=None, seg_bases=None,
     _check(library().delta_leb128_encode(
         idx.data_ptr(), K, offs.data_ptr() if S else None, bases.data_ptr() if S else None, S,
         out.data_ptr(), cap, nbytes.data_ptr(), sbo.data_ptr() if S else None, flag.data_ptr(),
-        ws.data_ptr(), ws.numel(), _stream(stream)))
+        ws.data_ptr(), ws.numel(), _adopt(stream, offs, bases, ws, nbytes, flag, sbo, out)))
     (stream or torch.cuda.current_stream()).synchronize()
     if int(flag.item()):
         raise DeltaError(_abi.DELTA_ERR_INVALID_ARG, "indices not increasing within a segment")
@@ -597,7 +627,7 @@ def delta_leb128_decode(buf: torch.Tensor, seg_offsets=None, seg_bases=None,
     _check(library().delta_leb128_decode(
         buf.data_ptr(), nb, offs.data_ptr() if S else None, bases.data_ptr() if S else None, S,
         out.data_ptr(), cap, cnt.data_ptr(), flag.data_ptr(), ws.data_ptr(), ws.numel(),
-        _stream(stream)))
+        _adopt(stream, offs, bases, ws, out, cnt, flag)))
     (stream or torch.cuda.current_stream()).synchronize()
     if int(flag.item()):
         raise DeltaError(_abi.DELTA_ERR_INVALID_ARG, "malformed LEB128 stream")
@@ -640,7 +670,9 @@ def delta_apply_leb128_multi(weights: Sequence[torch.Tensor], code: torch.Tensor
         ptrs, numels, T, code.data_ptr(), code.numel(), offs.data_ptr() if S else None,
         bases.data_ptr() if S and bases is not None else None, S, _words(val, "val"), val.numel(),
         flag.data_ptr() if flag is not None else None, ws.data_ptr(),
-        ws.numel() * ws.element_size(), _stream(stream)))
+        ws.numel() * ws.element_size(),
+        _adopt(stream, offs, bases, ws if ws is not workspace else None,
+               flag if flag is not error_flag else None)))
     if check:
         (stream or torch.cuda.current_stream()).synchronize()
         if int(flag.item()) != 0:
@@ -791,7 +823,7 @@ def delta_hash_segments(data: torch.Tensor, seg_bytes: int, seed: int = 0,
     out = torch.empty(max(n, 1), dtype=torch.int64, device=data.device)
     _check(library().delta_hash_segments(data.data_ptr(), nbytes, int(seg_bytes),
                                          int(seed) & ((1 << 64) - 1), out.data_ptr(),
-                                         _stream(stream)))
+                                         _adopt(stream, out)))
     return out[:n]
 
 
@@ -830,7 +862,8 @@ def pack_artifact(idx: torch.Tensor, val: torch.Tensor, tensor_offsets: torch.Te
         status = library().delta_artifact_pack(
             idx.data_ptr(), _words(val, "val"), K, offs.data_ptr(), nums, T, coding_id,
             int(version), int(base_version), int(seg_bytes), art.data_ptr(), art.numel(),
-            ws.data_ptr(), ws.numel(), _stream(stream), ctypes.byref(h), ctypes.byref(total))
+            ws.data_ptr(), ws.numel(), _adopt(stream, offs, ws, art), ctypes.byref(h),
+            ctypes.byref(total))
         if status != _abi.DELTA_ERR_CAPACITY:
             break
         size = total.value
@@ -857,7 +890,7 @@ def delta_artifact_verify(art: torch.Tensor, header=None,
     hb = torch.zeros(1, dtype=torch.int32, device=art.device)
     _check(library().delta_artifact_verify(art.data_ptr(), art.numel(), ctypes.byref(h),
                                            bad.data_ptr(), bad[1:].data_ptr(), hb.data_ptr(),
-                                           ws.data_ptr(), ws.numel(), _stream(stream)))
+                                           ws.data_ptr(), ws.numel(), _adopt(stream, ws, bad, hb)))
     (stream or torch.cuda.current_stream()).synchronize()
     n_bad, first = bad.cpu().tolist()
     return int(n_bad), (None if n_bad == 0 else int(first)), bool(hb.item())
@@ -876,5 +909,5 @@ def activate_artifact(art: torch.Tensor, weights: Sequence[torch.Tensor], active
     numels = _u64_array([w.numel() for w in weights])
     _check(library().delta_artifact_activate(
         art.data_ptr(), art.numel(), ctypes.byref(h), ptrs, numels, len(weights),
-        int(active_version), ws.data_ptr(), ws.numel(), _stream(stream)))
+        int(active_version), ws.data_ptr(), ws.numel(), _adopt(stream, ws)))
     return int(h.version)
