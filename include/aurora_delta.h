@@ -659,6 +659,9 @@ size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
  *                 h_capacity entries; kernels store into them, so pageable
  *                 memory is refused with DELTA_ERR_INVALID_ARG.
  *   h_count       host: the true total.
+ * The streams start on the chunks at once and wait for no other stream:
+ * writes to the weights or the staging queued elsewhere must have finished
+ * (the Python binding synchronises its current stream first).
  * Host-synchronous: returns after every store has landed.  Returns
  * DELTA_ERR_CAPACITY (with *h_count = true total, the first h_capacity
  * entries written) if the output did not fit.
