@@ -230,6 +230,31 @@ class MultiPlan:
         self.device = prevs[0].device if prevs else torch.device("cuda")
         self.workspace_bytes = delta_extract_multi_workspace_bytes(self.numels)
         self._keep = (list(prevs), list(news))
+        self._c_plan = None
+
+    def prepare(self, stream: Optional[torch.cuda.Stream] = None) -> "MultiPlan":
+        """Builds the library's plan of these tensors (``delta_multi_plan``:
+        the slice table and tile map in device memory, made once), which
+        :func:`delta_extract_multi_into` then uses instead of uploading the
+        table on every call.  Host-synchronous; returns self."""
+        if self._c_plan is None:
+            h = ctypes.c_void_p(None)
+            lib = library()
+            _check(lib.delta_multi_plan_create(
+                self.prev_ptrs, self.next_ptrs, self.numel_arr, self.T, _stream(stream),
+                ctypes.byref(h)))
+            self._c_plan, self._c_lib = h, lib
+        return self
+
+    @property
+    def prepared(self) -> bool:
+        return self._c_plan is not None
+
+    def __del__(self):
+        h = getattr(self, "_c_plan", None)
+        if h is not None:
+            self._c_lib.delta_multi_plan_destroy(h)
+            self._c_plan = None
 
 
 def delta_extract_multi_into(plan: MultiPlan, out_idx: torch.Tensor, out_val: torch.Tensor,
@@ -242,6 +267,13 @@ def delta_extract_multi_into(plan: MultiPlan, out_idx: torch.Tensor, out_val: to
     if d_offsets is not None and d_offsets.numel() < plan.T + 1:
         raise ValueError("d_offsets needs num_tensors + 1 entries")
     cap = min(out_idx.numel(), out_val.numel())
+    if plan.prepared:
+        _check(plan._c_lib.delta_extract_multi_planned(
+            plan._c_plan, out_idx.data_ptr(), _words(out_val, "out_val"), cap,
+            d_count.data_ptr(), d_offsets.data_ptr() if d_offsets is not None else None,
+            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+            _stream(stream)))
+        return
     _check(library().delta_extract_multi(
         plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, plan.T, out_idx.data_ptr(),
         _words(out_val, "out_val"), cap, d_count.data_ptr(),

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include <hip/hip_runtime.h>
 
 #include "aurora_delta.h"
@@ -290,19 +292,32 @@ struct CodedOut {
   uint64_t* d_byte_offsets;
 };
 
+// The slice descriptors of a tensor list and, past kInlineDescs of them,
+// their device table and tile map, built once for many calls (a
+// delta_multi_plan).
+struct PreparedTable {
+  std::vector<TensorDesc> descs;   // host copy
+  uint64_t tiles;
+  TensorDesc* d_table;             // nullptr when the descriptors go inline
+  uint32_t* d_map;
+};
+
 // Builds the slice table in `workspace`, then enqueues the extract kernels
 // on `stream` (abi.hip).  Empty slices are skipped; d_offsets (nullable)
 // has num_tensors + 1 entries.  With `coded`, out_idx, idx64 and d_offsets
 // are unused and the workspace follows the coded layout.  `split` as for
 // launch_extract (with nothing to read, split->rest still waits for the
 // launch stream).  With `count_only`, only *d_count is written (outputs,
-// d_offsets, coded and split unused).  Sets the error text on failure.
+// d_offsets, coded and split unused).  With `prepared` the slices come
+// from it (slices and num_slices unused) and nothing is uploaded.  Sets
+// the error text on failure.
 delta_status_t enqueue_extract(const SliceIn* slices, size_t num_slices, uint32_t num_tensors,
                                bool idx64, void* out_idx, uint16_t* out_val, uint64_t capacity,
                                uint64_t* d_count, uint64_t* d_offsets, void* workspace,
                                size_t workspace_bytes, hipStream_t stream,
                                const CodedOut* coded = nullptr,
-                               const StageSplit* split = nullptr, bool count_only = false);
+                               const StageSplit* split = nullptr, bool count_only = false,
+                               const PreparedTable* prepared = nullptr);
 
 // Delta chain composition (compose.hip): workspace layout for `K` deltas
 // of the given counts, and the enqueue of the whole chain on `stream`.

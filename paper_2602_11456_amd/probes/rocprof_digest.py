@@ -121,10 +121,10 @@ def traffic(fetch_csv, write_csv, copy_bytes, out_json):
     for f in ("extract.hip", "delta_internal.h", "apply.hip"):
         with open(os.path.join(CSRC, f), "rb") as fh:
             h.update(fh.read())
-    per_call = sum(v["bytes_per_dispatch"] * (10 if "upload_words" in k else 1)
-                   for k, v in kernels.items()
-                   if any(s in k for s in ("upload_words", "build_tile_map",
-                                           "stage_kernel<true, true, false>",
+    # one planned extract call: the tensor table and tile map are the plan's,
+    # built once, so only the stage, scan and finalize kernels run per call
+    per_call = sum(v["bytes_per_dispatch"] for k, v in kernels.items()
+                   if any(s in k for s in ("stage_kernel<true, true, false>",
                                            "group_sum_kernel<unsigned int>",
                                            "group_scan_kernel", "finalize_kernel<long, true, true>")))
     out = {"bytes_per_call": per_call, "fetch_factor": fetch_factor,
@@ -138,7 +138,7 @@ def traffic(fetch_csv, write_csv, copy_bytes, out_json):
         print(f"{k:60s} n={v['dispatches']:3d} read "
               f"{v['fetch_kib'] * 1024 * fetch_factor / 1e9:8.4f} GB write "
               f"{v['write_kib'] * 1024 * write_factor / 1e9:8.4f} GB")
-    print(f"extract call (stage, scans, finalize, table): {per_call / 1e9:.3f} GB")
+    print(f"extract call (stage, scans, finalize): {per_call / 1e9:.3f} GB")
 
 
 def counters(path):

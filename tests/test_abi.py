@@ -154,6 +154,30 @@ def test_extract_multi_validation(lib):
                                    1 << 20, None) == _abi.DELTA_ERR_INVALID_ARG
 
 
+def test_multi_plan_validation(lib):
+    P = ctypes.c_void_p
+    prevs = (P * 2)(FAKE, FAKE)
+    nexts = (P * 2)(FAKE, None)
+    numels = (ctypes.c_uint64 * 2)(10, 10)
+    plan = P(FAKE)
+    assert lib.delta_multi_plan_create(prevs, prevs, numels, 2, None,
+                                       None) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_multi_plan_create(prevs, nexts, numels, 2, None,
+                                       ctypes.byref(plan)) == _abi.DELTA_ERR_INVALID_ARG
+    assert b"tensor 1" in lib.delta_last_error()
+    assert plan.value is None   # cleared on failure
+    odd = (P * 2)(FAKE, FAKE + 1)
+    assert lib.delta_multi_plan_create(prevs, odd, numels, 2, None,
+                                       ctypes.byref(plan)) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_multi_plan_create(prevs, prevs, numels, -1, None,
+                                       ctypes.byref(plan)) == _abi.DELTA_ERR_INVALID_ARG
+    assert lib.delta_multi_plan_destroy(None) == _abi.DELTA_OK
+    assert lib.delta_multi_plan_workspace_bytes(None) == 0
+    assert lib.delta_extract_multi_planned(None, FAKE, FAKE, 10, FAKE, None, FAKE, 1 << 20,
+                                           None) == _abi.DELTA_ERR_INVALID_ARG
+    assert b"plan" in lib.delta_last_error()
+
+
 def test_count_changed_multi_validation(lib):
     P = ctypes.c_void_p
     prevs = (P * 2)(FAKE, FAKE)

@@ -90,6 +90,27 @@ def oracle_every_tensor(ws, idx, val, offs, label, codes=()):
         f"({len(codes_h)} coded streams)")
 
 
+def planned_equals(ws, idx, val, offs, label):
+    """The planned call (tensor table built once, as the benchmark times
+    it) writes exactly what delta_extract_multi wrote, which is compared
+    with the oracle on every tensor."""
+    plan = ad.MultiPlan(ws.prev, ws.new).prepare()
+    k = idx.numel()
+    pidx = torch.empty(k + 1, dtype=torch.int64, device=DEV)
+    pval = torch.empty(k + 1, dtype=val.dtype, device=DEV)
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    poffs = torch.zeros(plan.T + 1, dtype=torch.int64, device=DEV)
+    work = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV)
+    torch.cuda.synchronize()
+    ad.delta_extract_multi_into(plan, pidx, pval, cnt, work, poffs)
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == k, label
+    assert torch.equal(pidx[:k], idx) and torch.equal(poffs, offs), label
+    assert torch.equal(pval[:k].view(torch.int16), val.view(torch.int16)), label
+    del plan, pidx, pval, work
+    say(label, "planned call ok")
+
+
 def round_trip(ws, idx, val, label):
     roll = [p.clone() for p in ws.prev]
     ad.delta_apply_multi(roll, idx, val, check=True)
@@ -173,6 +194,7 @@ def test_weight_set(model, density):
     idx, val, offs = ad.delta_extract_multi(ws.prev, ws.new)
     torch.cuda.synchronize()
     check_set(ws, idx, val, offs, label)
+    planned_equals(ws, idx, val, offs, label)
     assert ad.delta_count_changed_multi(ws.prev, ws.new) == ws.total_planted, label
     round_trip(ws, idx, val, label)
     buf, sb = leb128_full(ws, idx, val, offs, label)

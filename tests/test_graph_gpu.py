@@ -28,15 +28,18 @@ def fill_random(ts, seed):
                                                 generator=g, dtype=torch.int16))
 
 
+@pytest.mark.parametrize("planned", [False, True])
 @pytest.mark.parametrize("sizes", [[70_001, 3, 50_000, 8192 * 3 + 1],        # inline slices
                                    [3000 + 17 * i for i in range(40)]])     # tensor table
-def test_extract_multi_graph_replays(sizes):
+def test_extract_multi_graph_replays(sizes, planned):
     prevs = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
     news = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
     fill_random(prevs, 1)
     for p, q in zip(prevs, news):
         q.copy_(p)
     plan = ad.MultiPlan(prevs, news)
+    if planned:
+        plan.prepare()
     cap = sum(sizes)
     out_idx = torch.empty(cap, dtype=torch.int64, device=DEV)
     out_val = torch.empty(cap, dtype=torch.bfloat16, device=DEV)
