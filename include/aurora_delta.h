@@ -212,6 +212,10 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
  *   (outputs, workspace and errors as there).  The stream must be on the
  *   plan's device (DELTA_ERR_INVALID_ARG otherwise).  Calls on one plan may
  *   overlap in time if each has its own workspace and outputs.
+ * delta_count_changed_multi_planned, delta_extract_multi_leb128_planned:
+ *   delta_count_changed_multi and delta_extract_multi_leb128 over the
+ *   plan's tensors, the same way (the coded call's workspace is
+ *   delta_extract_multi_leb128_workspace_bytes of the same sizes).
  */
 typedef struct delta_multi_plan delta_multi_plan_t;
 delta_status_t delta_multi_plan_create(const uint16_t* const* prev_ptrs,
@@ -225,6 +229,17 @@ delta_status_t delta_extract_multi_planned(const delta_multi_plan_t* plan, int64
                                            uint64_t* d_count, uint64_t* d_tensor_offsets,
                                            void* workspace, size_t workspace_bytes,
                                            hipStream_t stream);
+delta_status_t delta_count_changed_multi_planned(const delta_multi_plan_t* plan,
+                                                 uint64_t* d_count, void* workspace,
+                                                 size_t workspace_bytes, hipStream_t stream);
+delta_status_t delta_extract_multi_leb128_planned(const delta_multi_plan_t* plan,
+                                                  uint8_t* out_code, uint64_t code_capacity,
+                                                  uint64_t* d_nbytes, uint16_t* out_val,
+                                                  uint64_t capacity, uint64_t* d_count,
+                                                  uint64_t* d_tensor_offsets,
+                                                  uint64_t* d_tensor_byte_offsets,
+                                                  void* workspace, size_t workspace_bytes,
+                                                  hipStream_t stream);
 
 /*
  * delta_count_changed_multi — Sec. 5.1: the number of changed words of a

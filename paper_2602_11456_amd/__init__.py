@@ -286,6 +286,11 @@ def delta_count_changed_multi_into(plan: MultiPlan, d_count: torch.Tensor,
                                    stream: Optional[torch.cuda.Stream] = None) -> None:
     """Enqueue ``delta_count_changed_multi`` (no sync): the number of
     changed words of the plan's tensors into ``d_count`` (int64, 1 entry)."""
+    if plan.prepared:
+        _check(plan._c_lib.delta_count_changed_multi_planned(
+            plan._c_plan, d_count.data_ptr(), workspace.data_ptr(),
+            workspace.numel() * workspace.element_size(), _stream(stream)))
+        return
     _check(library().delta_count_changed_multi(
         plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, plan.T, d_count.data_ptr(),
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(stream)))
@@ -343,6 +348,15 @@ def delta_extract_multi_leb128_into(plan: MultiPlan, out_code: torch.Tensor,
     for name, t in (("d_offsets", d_offsets), ("d_byte_offsets", d_byte_offsets)):
         if t is not None and t.numel() < plan.T + 1:
             raise ValueError(f"{name} needs num_tensors + 1 entries")
+    if plan.prepared:
+        _check(plan._c_lib.delta_extract_multi_leb128_planned(
+            plan._c_plan, out_code.data_ptr(), out_code.numel(), d_nbytes.data_ptr(),
+            _words(out_val, "out_val"), out_val.numel(), d_count.data_ptr(),
+            d_offsets.data_ptr() if d_offsets is not None else None,
+            d_byte_offsets.data_ptr() if d_byte_offsets is not None else None,
+            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+            _stream(stream)))
+        return
     _check(library().delta_extract_multi_leb128(
         plan.prev_ptrs, plan.next_ptrs, plan.numel_arr, plan.T, out_code.data_ptr(),
         out_code.numel(), d_nbytes.data_ptr(), _words(out_val, "out_val"), out_val.numel(),

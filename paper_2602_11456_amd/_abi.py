@@ -86,6 +86,8 @@ SIGNATURES = {
     "delta_multi_plan_destroy": (STATUS, [P]),
     "delta_multi_plan_workspace_bytes": (SZ, [P]),
     "delta_extract_multi_planned": (STATUS, [P, P, P, U64, P, P, P, SZ, P]),
+    "delta_count_changed_multi_planned": (STATUS, [P, P, P, SZ, P]),
+    "delta_extract_multi_leb128_planned": (STATUS, [P, P, U64, P, P, U64, P, P, P, P, SZ, P]),
     "delta_extract_fused": (STATUS, [P, P, P, I32, P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
     "delta_extract_multi_leb128_workspace_bytes": (SZ, [P, I32]),
     "delta_extract_multi_leb128": (STATUS, [P, P, P, I32, P, U64, P, P, U64, P, P, P, P, SZ,

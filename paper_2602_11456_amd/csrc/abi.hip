@@ -519,6 +519,51 @@ delta_status_t delta_extract_multi_planned(const delta_multi_plan_t* plan, int64
                          nullptr, nullptr, false, &plan->table);
 }
 
+delta_status_t delta_count_changed_multi_planned(const delta_multi_plan_t* plan,
+                                                 uint64_t* d_count, void* workspace,
+                                                 size_t workspace_bytes, hipStream_t stream) {
+  if (!plan) return fail(DELTA_ERR_INVALID_ARG, "plan is NULL");
+  if (!d_count) return fail(DELTA_ERR_INVALID_ARG, "d_count is NULL");
+  int dev = -1;
+  const delta_status_t st = stream_device(stream, &dev);
+  if (st != DELTA_OK) return st;
+  if (dev != plan->device)
+    return fail(DELTA_ERR_INVALID_ARG, "the stream is on device %d, the plan on device %d", dev,
+                plan->device);
+  return enqueue_extract(nullptr, 0, (uint32_t)plan->num_tensors, true, nullptr, nullptr, 0,
+                         d_count, nullptr, workspace, workspace_bytes, stream, nullptr, nullptr,
+                         true, &plan->table);
+}
+
+delta_status_t delta_extract_multi_leb128_planned(const delta_multi_plan_t* plan,
+                                                  uint8_t* out_code, uint64_t code_capacity,
+                                                  uint64_t* d_nbytes, uint16_t* out_val,
+                                                  uint64_t capacity, uint64_t* d_count,
+                                                  uint64_t* d_tensor_offsets,
+                                                  uint64_t* d_tensor_byte_offsets,
+                                                  void* workspace, size_t workspace_bytes,
+                                                  hipStream_t stream) {
+  if (!plan) return fail(DELTA_ERR_INVALID_ARG, "plan is NULL");
+  if (!d_count || !d_nbytes) return fail(DELTA_ERR_INVALID_ARG, "d_count/d_nbytes is NULL");
+  if (capacity > 0 && !out_val)
+    return fail(DELTA_ERR_INVALID_ARG, "out_val is NULL with capacity %llu",
+                (unsigned long long)capacity);
+  if (odd(out_val)) return fail(DELTA_ERR_INVALID_ARG, "out_val not 2-byte aligned");
+  if (code_capacity > 0 && !out_code)
+    return fail(DELTA_ERR_INVALID_ARG, "out_code is NULL with code_capacity %llu",
+                (unsigned long long)code_capacity);
+  int dev = -1;
+  const delta_status_t st = stream_device(stream, &dev);
+  if (st != DELTA_OK) return st;
+  if (dev != plan->device)
+    return fail(DELTA_ERR_INVALID_ARG, "the stream is on device %d, the plan on device %d", dev,
+                plan->device);
+  const CodedOut co = {out_code, code_capacity, d_nbytes, 0, true, d_tensor_byte_offsets};
+  return enqueue_extract(nullptr, 0, (uint32_t)plan->num_tensors, true, nullptr, out_val,
+                         capacity, d_count, d_tensor_offsets, workspace, workspace_bytes, stream,
+                         &co, nullptr, false, &plan->table);
+}
+
 delta_status_t delta_count_changed_multi(const uint16_t* const* prev_ptrs,
                                          const uint16_t* const* next_ptrs,
                                          const uint64_t* numels, int32_t num_tensors,

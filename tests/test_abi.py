@@ -176,6 +176,13 @@ def test_multi_plan_validation(lib):
     assert lib.delta_extract_multi_planned(None, FAKE, FAKE, 10, FAKE, None, FAKE, 1 << 20,
                                            None) == _abi.DELTA_ERR_INVALID_ARG
     assert b"plan" in lib.delta_last_error()
+    assert lib.delta_count_changed_multi_planned(None, FAKE, FAKE, 1 << 20,
+                                                 None) == _abi.DELTA_ERR_INVALID_ARG
+    assert b"plan" in lib.delta_last_error()
+    assert lib.delta_extract_multi_leb128_planned(None, FAKE, 100, FAKE, FAKE, 10, FAKE, None,
+                                                  None, FAKE, 1 << 20,
+                                                  None) == _abi.DELTA_ERR_INVALID_ARG
+    assert b"plan" in lib.delta_last_error()
 
 
 def test_count_changed_multi_validation(lib):

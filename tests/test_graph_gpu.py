@@ -108,9 +108,10 @@ def test_apply_multi_graph_replays():
             np.testing.assert_array_equal(host_u16(r), w)
 
 
+@pytest.mark.parametrize("planned", [False, True])
 @pytest.mark.parametrize("sizes", [[70_001, 3, 50_000, 8192 * 3 + 1],        # inline slices
                                    [3000 + 17 * i for i in range(40)]])     # tensor table
-def test_extract_multi_leb128_graph_replays(sizes):
+def test_extract_multi_leb128_graph_replays(sizes, planned):
     """The extract that writes LEB128 itself, captured once: every replay's
     bytes, words and offsets equal the oracle's for the data it saw."""
     prevs = [torch.empty(n, dtype=torch.bfloat16, device=DEV) for n in sizes]
@@ -119,6 +120,8 @@ def test_extract_multi_leb128_graph_replays(sizes):
     for p, q in zip(prevs, news):
         q.copy_(p)
     plan = ad.MultiPlan(prevs, news)
+    if planned:
+        plan.prepare()
     total = sum(sizes)
     code = torch.empty(3 * total, dtype=torch.uint8, device=DEV)
     val = torch.empty(total, dtype=torch.bfloat16, device=DEV)
@@ -205,7 +208,8 @@ def test_apply_chain_graph_replays():
         np.testing.assert_array_equal(np.concatenate([host_u16(x) for x in rollout]), flat)
 
 
-def test_count_changed_multi_graph_replays():
+@pytest.mark.parametrize("planned", [False, True])
+def test_count_changed_multi_graph_replays(planned):
     """The count-only pass captured once (tensor-table path): every replay
     gives the oracle's count for the data it saw."""
     sizes = [3000 + 17 * i for i in range(40)] + [70_001, 0, 8192 * 3 + 1]
@@ -215,6 +219,8 @@ def test_count_changed_multi_graph_replays():
     for p, q in zip(prevs, news):
         q.copy_(p)
     plan = ad.MultiPlan(prevs, news)
+    if planned:
+        plan.prepare()
     cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
     work = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV)
     s = torch.cuda.Stream()

@@ -1,8 +1,9 @@
-"""The planned multi-tensor extract (delta_multi_plan: the tensor table and
+"""The planned multi-tensor calls (delta_multi_plan: the tensor table and
 tile map built once in device memory) against the CPU oracle (Sec. 5.1
-block offsets): lists held inline and in a device table, empty tensors,
-misaligned views, new contents under one plan step after step, and
-capacity truncation."""
+block offsets and sparse encoding): the extract, the count and the extract
+that writes LEB128 itself, over lists held inline and in a device table,
+empty tensors, misaligned views, new contents under one plan step after
+step, and capacity truncation."""
 import numpy as np
 import pytest
 import torch
@@ -49,6 +50,37 @@ def run(plan, cap=None):
     return idx, val, int(cnt.item()), offs
 
 
+def check_coded(plan, hp, hn):
+    """The planned extract that writes LEB128 itself: every tensor's code
+    segment equals the oracle encoder's bytes of the oracle's tensor-local
+    indices; words and offsets as the oracle's."""
+    ri, rv, ro, rc = oracle.extract_multi(hp, hn)
+    cap = max(rc, 1)
+    code = torch.empty(3 * cap + 64, dtype=torch.uint8, device=DEV)
+    val = torch.empty(cap, dtype=torch.bfloat16, device=DEV)
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    nb = torch.zeros(1, dtype=torch.int64, device=DEV)
+    offs = torch.zeros(plan.T + 1, dtype=torch.int64, device=DEV)
+    boffs = torch.zeros(plan.T + 1, dtype=torch.int64, device=DEV)
+    ws = torch.empty(ad.delta_extract_multi_leb128_workspace_bytes(plan.numels),
+                     dtype=torch.uint8, device=DEV)
+    torch.cuda.synchronize()
+    ad.delta_extract_multi_leb128_into(plan, code, val, cnt, nb, ws, offs, boffs)
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == rc
+    np.testing.assert_array_equal(host_u16(val[:rc]), rv)
+    o = offs.cpu().numpy()
+    np.testing.assert_array_equal(o.astype(np.uint64), ro)
+    b = boffs.cpu().numpy()
+    c = code[:int(nb.item())].cpu().numpy()
+    base = 0
+    for t, p in enumerate(hp):
+        ref, n = oracle.leb128_encode(ri[o[t]:o[t + 1]] - base)
+        np.testing.assert_array_equal(c[b[t]:b[t + 1]], ref)
+        base += p.size
+    assert b[-1] == c.size
+
+
 def check(hp, hn, idx, val, k, offs, cap=None):
     ri, rv, ro, rc = oracle.extract_multi(hp, hn)
     assert k == rc
@@ -84,6 +116,14 @@ def test_planned_matches_oracle_step_after_step(sizes):
         idx2, val2, k2, offs2 = run(plain)
         assert k2 == k
         assert torch.equal(idx2[:k], idx[:k]) and torch.equal(offs2, offs), step
+        # the planned count and the planned coded extract
+        cnt = torch.full((1,), -1, dtype=torch.int64, device=DEV)
+        ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=DEV)
+        torch.cuda.synchronize()
+        ad.delta_count_changed_multi_into(plan, cnt, ws)
+        torch.cuda.synchronize()
+        assert int(cnt.item()) == k, step
+        check_coded(plan, hp, hn)
 
 
 def test_planned_misaligned_views_and_capacity():
