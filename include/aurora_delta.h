@@ -204,8 +204,10 @@ delta_status_t delta_extract_multi(const uint16_t* const* prev_ptrs,
  *   contents may change) while the plan is used.  Allocates device memory
  *   on the stream's device and is host-synchronous.  *out_plan is NULL on
  *   failure.
- * delta_multi_plan_destroy: frees the plan (NULL: nothing); hipFree waits
- *   for the device, so calls already enqueued finish first.
+ * delta_multi_plan_destroy: frees the plan (NULL: nothing).  With a device
+ *   table it first waits for the plan's device (hipDeviceSynchronize), so
+ *   calls already enqueued on any stream finish first; not during a graph
+ *   capture on that device.
  * delta_multi_plan_workspace_bytes: the workspace a planned call needs
  *   (the same as delta_extract_multi_workspace_bytes); 0 for NULL.
  * delta_extract_multi_planned: delta_extract_multi over the plan's tensors

@@ -488,8 +488,18 @@ delta_status_t delta_multi_plan_create(const uint16_t* const* prev_ptrs,
 }
 
 delta_status_t delta_multi_plan_destroy(delta_multi_plan_t* plan) {
+  if (!plan) return ok();
+  hipError_t e = hipSuccess;
+  if (plan->table.d_table || plan->table.d_map) {
+    // calls enqueued on any stream may still read the table: finish them
+    int cur = -1;
+    e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != plan->device) e = hipSetDevice(plan->device);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (cur >= 0 && cur != plan->device) (void)hipSetDevice(cur);
+  }
   plan_free(plan);
-  return ok();
+  return e == hipSuccess ? ok() : hip_fail(e, "finishing the plan's calls");
 }
 
 size_t delta_multi_plan_workspace_bytes(const delta_multi_plan_t* plan) {
