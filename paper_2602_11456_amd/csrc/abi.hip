@@ -892,9 +892,7 @@ delta_status_t delta_leb128_encode(const int64_t* idx, uint64_t count,
   a.d_nbytes = d_nbytes;
   a.seg_byte_offsets = d_seg_byte_offsets;
   a.err = d_error_flag;
-  a.tile_bytes = (uint32_t*)(ws + L.tile_bytes);
-  hipError_t e = launch_leb128_encode(a, (uint64_t*)(ws + L.group_sum),
-                                      (uint64_t*)(ws + L.group_excl), stream);
+  hipError_t e = launch_leb128_encode(a, ws, L, stream);
   if (e != hipSuccess) return hip_fail(e, "leb128 encode launch");
   return ok();
 }
@@ -1266,13 +1264,9 @@ delta_status_t delta_artifact_pack(const int64_t* idx, const uint16_t* val, uint
     a.d_nbytes = (uint64_t*)(ws + P.nbytes);
     a.seg_byte_offsets = T > 0 ? (uint64_t*)(ws + P.byte_offs) : nullptr;
     a.err = (uint32_t*)(ws + P.err);
-    a.tile_bytes = (uint32_t*)(ws + P.enc + enc_layout(count).tile_bytes);
-    a.group_excl = nullptr;
     e = launch_reset((uint64_t*)(ws + P.err), nullptr, 0, stream);
     const EncLayout EL = enc_layout(count);
-    if (e == hipSuccess)
-      e = launch_leb128_encode(a, (uint64_t*)(ws + P.enc + EL.group_sum),
-                               (uint64_t*)(ws + P.enc + EL.group_excl), stream);
+    if (e == hipSuccess) e = launch_leb128_encode(a, ws + P.enc, EL, stream);
     if (e != hipSuccess) return hip_fail(e, "encode launch");
     uint64_t got[2];
     st = read_back(&got[0], ws + P.nbytes, 8, stream);

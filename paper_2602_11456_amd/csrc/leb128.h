@@ -28,6 +28,7 @@ struct EncArgs {
   uint32_t* err;                // nullable
   uint32_t* tile_bytes;
   uint64_t* group_excl;
+  uint8_t* stage;               // per tile, its staged code
 };
 
 struct DecArgs {
@@ -56,7 +57,7 @@ struct DecArgs {
 
 struct EncLayout {
   uint64_t tiles;
-  size_t tile_bytes, group_sum, group_excl, total;
+  size_t tile_bytes, group_sum, group_excl, stage, total;
 };
 // Encoder grid for up to `count` entries.
 uint32_t enc_grid(uint64_t count, bool count_on_device);
@@ -67,8 +68,9 @@ struct DecLayout {
 };
 EncLayout enc_layout(uint64_t count);
 DecLayout dec_layout(uint64_t nbytes);
-hipError_t launch_leb128_encode(EncArgs a, uint64_t* group_sum, uint64_t* group_excl,
-                                hipStream_t stream);
+// Enqueues the encoder; its tables and staging slots live in `ws` at the
+// offsets of `L` (enc_layout of a.count).
+hipError_t launch_leb128_encode(EncArgs a, char* ws, const EncLayout& L, hipStream_t stream);
 // Decodes a.in; writes the indices to a.out, or, with `apply`, applies
 // a.val to the tensors a.ptrs (capacity = entries of a.val; a stream with
 // another entry count raises a.err).

@@ -10,10 +10,11 @@
 // stored as idx - base[s], i.e. as the tensor-local index.
 //
 // Encode, per tile of 4096 entries (one workgroup, each wavefront 1024
-// consecutive entries, 64 per step, so every load is coalesced):
-// enc_count sums the tile's code lengths, the tile sums are scanned in
-// groups (the same group scan as extract), and enc_write writes each
-// entry's bytes at its offset (wavefront scan of the lengths per step).
+// consecutive entries, 64 per step, so every load is coalesced): enc_stage
+// reads the indices once and stages each tile's code (wavefront scan of
+// the code lengths per step) with its byte count; the byte counts are
+// scanned in groups (the same group scan as extract), and enc_copy moves
+// every tile's code to its place.
 //
 // Decode, per tile of 16 KiB of bytes: dec_count counts the terminating
 // bytes (high bit clear; 4 bytes per 32-bit test); their scan numbers the
@@ -197,8 +198,23 @@ __device__ __forceinline__ void raise_flag(uint32_t* err) {
 }
 
 // ---------------------------------------------------------------- encode
+//
+// One read of the indices.  enc_stage: per tile, the gaps and their code
+// lengths, a wavefront scan of the lengths per step, the tile's bytes
+// assembled in LDS and stored to the tile's staging slot (16-byte stores),
+// its byte count, and the tile-local byte offset of every segment that
+// opens in it.  The byte counts are scanned in groups.  enc_copy: every
+// tile's staged bytes to their place in the output; a tile whose code
+// outgrew its slot is encoded again straight to the output.  enc_seg_fix
+// makes the segment byte offsets absolute.  Traffic per index: 8 bytes
+// read once, its code written, read and written again (about 1.3 bytes
+// each at 1% density), where counting and then writing read the indices
+// twice.
 
-constexpr int kEncLds = 16384;   // a tile's code is assembled in LDS up to this size
+constexpr int kEncLds = 16384;                  // LDS assembly area of a tile's code
+constexpr uint32_t kEncSlot = 2 * kEncTile;     // staged code bytes per tile
+static_assert(kEncSlot <= (uint32_t)kEncLds && kEncSlot % 16 == 0, "encoder slot size");
+typedef uint32_t enc_u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint64_t enc_count_of(const EncArgs& a) {
   if (!a.d_count_in) return a.count;
@@ -206,42 +222,52 @@ __device__ __forceinline__ uint64_t enc_count_of(const EncArgs& a) {
   return c < a.count ? c : a.count;
 }
 
-// Gaps of this lane's entries kw + 64 it (it < kEncSteps) below t1: idx -
-// base for an entry that opens its segment, else idx - previous idx (the
-// previous index comes from the neighbouring lane).  Sets bit it of
-// `starts` for an entry that opens a segment, `bad` for a gap below 0 / 1;
-// returns the lane's code bytes.
-__device__ __forceinline__ uint32_t enc_gaps(const EncArgs& a, const TileSegs& c,
-                                             const uint64_t* s_lo, uint64_t kw, uint64_t t1,
-                                             uint64_t (&gap)[kEncSteps], uint32_t& starts,
-                                             bool& bad) {
-  const uint32_t lane = lane_id();
+// This lane's indices kw + 64 it (it < kEncSteps) below t1, and the index
+// just before the wavefront's first entry (0 for the stream's first).
+struct EncLoad {
   int64_t cur[kEncSteps];
+  int64_t last;
+};
+
+__device__ __forceinline__ void enc_load(const EncArgs& a, uint64_t kw, uint64_t t1, EncLoad& L) {
+  const uint32_t lane = lane_id();
 #pragma unroll
   for (int it = 0; it < kEncSteps; ++it) {
     const uint64_t k = kw + 64 * it;
-    cur[it] = k < t1 ? a.idx[k] : 0;
+    L.cur[it] = k < t1 ? a.idx[k] : 0;
   }
   const uint64_t first = kw - lane;   // the wavefront's first entry
-  int64_t last = (first > 0 && first < t1) ? a.idx[first - 1] : 0;
+  L.last = (first > 0 && first < t1) ? a.idx[first - 1] : 0;
+}
+
+// Gaps of the loaded entries: idx - base for an entry that opens its
+// segment, else idx - previous idx (the previous index comes from the
+// neighbouring lane).  Sets bit it of `starts` for an entry that opens a
+// segment, `bad` for a gap below 0 / 1; returns the lane's code bytes.
+__device__ __forceinline__ uint32_t enc_gaps(const EncArgs& a, const TileSegs& c,
+                                             const uint64_t* s_lo, uint64_t kw, uint64_t t1,
+                                             const EncLoad& L, uint64_t (&gap)[kEncSteps],
+                                             uint32_t& starts, bool& bad) {
+  const uint32_t lane = lane_id();
+  int64_t last = L.last;
   uint32_t bytes = 0;
   starts = 0;
 #pragma unroll
   for (int it = 0; it < kEncSteps; ++it) {
     const uint64_t k = kw + 64 * it;
-    int64_t prev = __shfl_up(cur[it], 1);
+    int64_t prev = __shfl_up(L.cur[it], 1);
     if (lane == 0) prev = last;
-    last = __shfl(cur[it], 63);
+    last = __shfl(L.cur[it], 63);
     gap[it] = 0;
     if (k < t1) {
       bool start;
       const uint32_t seg = tile_seg(a.segs, c, s_lo, k, start);
       int64_t d;
       if (start) {
-        d = cur[it] - seg_base(a.segs, seg);
+        d = L.cur[it] - seg_base(a.segs, seg);
         bad |= d < 0;
       } else {
-        d = cur[it] - prev;
+        d = L.cur[it] - prev;
         bad |= d < 1;
       }
       gap[it] = d < 0 ? 0 : (uint64_t)d;
@@ -252,31 +278,80 @@ __device__ __forceinline__ uint32_t enc_gaps(const EncArgs& a, const TileSegs& c
   return bytes;
 }
 
+// Position of every entry's code inside the tile (wavefront scans of the
+// lengths, starting at `pos`, this wavefront's offset in the tile); calls
+// f(it, k, len, p, gap) for each of the lane's entries inside the tile.
+template <typename F>
+__device__ __forceinline__ void enc_walk(uint64_t kw, uint64_t t1, const uint64_t (&gap)[kEncSteps],
+                                         uint32_t pos, F f) {
+#pragma unroll
+  for (int it = 0; it < kEncSteps; ++it) {
+    const uint64_t k = kw + 64 * it;
+    const uint32_t len = k < t1 ? leb_len(gap[it]) : 0;
+    const uint32_t incl = wave_incl_scan(len);
+    if (len) f(it, k, len, pos + incl - len, gap[it]);
+    pos += __shfl(incl, 63);
+  }
+}
+
+// The bytes of one number: 7 payload bits each, low group first.
+template <typename Put>
+__device__ __forceinline__ void enc_bytes(uint64_t v, uint32_t len, Put put) {
+  for (uint32_t m = 0; m < len; ++m) {
+    put(m, (uint8_t)((v & 0x7F) | (m + 1 < len ? 0x80u : 0u)));
+    v >>= 7;
+  }
+}
+
 // Tiles loop grid-stride (the entry count may only be known on the device).
-__global__ __launch_bounds__(kLebThreads) void enc_count_kernel(EncArgs a) {
+__global__ __launch_bounds__(kLebThreads) void enc_stage_kernel(EncArgs a) {
   __shared__ uint64_t s_lo[kSegLds];
   __shared__ uint32_t s_meta[2];
   __shared__ uint32_t s_wave[kLebWaves];
+  __shared__ __align__(16) uint8_t s_out[kEncSlot];
   const uint64_t count = enc_count_of(a);
   const uint64_t tiles = (count + kEncTile - 1) / kEncTile;
+  const uint32_t lane = lane_id(), wave = wave_id();
   bool bad = false;
   for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
     const uint64_t t0 = tile * kEncTile;
     const uint64_t t1 = t0 + kEncTile < count ? t0 + kEncTile : count;
-    const TileSegs c = tile_segs(a.segs, t0, t1, s_lo, s_meta);
+    const TileSegs c = tile_segs(a.segs, t0, t1, s_lo, s_meta);   // barriers
+    const uint64_t kw = t0 + (uint64_t)wave * kEncWave + lane;
+    EncLoad L;
+    enc_load(a, kw, t1, L);
     uint64_t gap[kEncSteps];
     uint32_t starts;
-    uint32_t bytes = enc_gaps(a, c, s_lo, t0 + (uint64_t)wave_id() * kEncWave + lane_id(), t1, gap,
-                              starts, bad);
-    bytes = wave_sum(bytes);
-    if (lane_id() == 0) s_wave[wave_id()] = bytes;
+    const uint32_t bytes = wave_sum(enc_gaps(a, c, s_lo, kw, t1, L, gap, starts, bad));
+    if (lane == 0) s_wave[wave] = bytes;
     __syncthreads();
-    if (threadIdx.x == 0) {
-      uint32_t t = 0;
-      for (int w = 0; w < kLebWaves; ++w) t += s_wave[w];
-      a.tile_bytes[tile] = t;
+    uint32_t pos = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < kLebWaves; ++w) {
+      pos += (uint32_t)w < wave ? s_wave[w] : 0u;
+      total += s_wave[w];
     }
+    const bool staged = total <= kEncSlot;
+    const bool segs_out = a.seg_byte_offsets && a.segs.num;
+    enc_walk(kw, t1, gap, pos, [&](int it, uint64_t k, uint32_t len, uint32_t p, uint64_t v) {
+      if (segs_out && ((starts >> it) & 1u)) {
+        // this entry opens its segment and every empty one just before it:
+        // their tile-local offset (made absolute by enc_seg_fix)
+        bool st;
+        const uint32_t sg = tile_seg(a.segs, c, s_lo, k, st);
+        for (int64_t s = sg; s >= 0 && a.segs.offs[s] == k; --s) a.seg_byte_offsets[s] = p;
+      }
+      if (staged) enc_bytes(v, len, [&](uint32_t m, uint8_t b) { s_out[p + m] = b; });
+    });
     __syncthreads();
+    if (staged) {
+      enc_u32x4* slot = (enc_u32x4*)(a.stage + tile * kEncSlot);
+      const enc_u32x4* src = (const enc_u32x4*)s_out;
+      for (uint32_t i = threadIdx.x; i < (total + 15) / 16; i += kLebThreads)
+        __builtin_nontemporal_store(src[i], slot + i);
+    }
+    if (threadIdx.x == 0) a.tile_bytes[tile] = total;
+    __syncthreads();   // s_out and s_wave are reused by the next tile
   }
   if (bad) raise_flag(a.err);
 }
@@ -308,85 +383,82 @@ __device__ __forceinline__ void enc_flush(const uint8_t* s_out, uint64_t n, uint
   for (uint64_t i = h + 4 * words + threadIdx.x; i < n; i += kLebThreads) dst[i] = s_out[i];
 }
 
-__global__ __launch_bounds__(kLebThreads) void enc_write_kernel(EncArgs a) {
+__global__ __launch_bounds__(kLebThreads) void enc_copy_kernel(EncArgs a) {
   __shared__ uint64_t s_lo[kSegLds];
   __shared__ uint32_t s_meta[2];
   __shared__ uint32_t s_wave[kLebWaves];
   __shared__ uint64_t s_before;
-  __shared__ uint8_t s_out[kEncLds];
+  __shared__ __align__(16) uint8_t s_out[kEncSlot];
   const uint64_t count = enc_count_of(a);
   const uint64_t tiles = (count + kEncTile - 1) / kEncTile;
   const uint32_t lane = lane_id(), wave = wave_id();
   for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
-    const uint64_t t0 = tile * kEncTile;
-    const uint64_t t1 = t0 + kEncTile < count ? t0 + kEncTile : count;
     // the tile's output position: its group's offset plus the byte counts
-    // of the group's earlier tiles, loaded now so that the loads overlap
-    // the segment lookup and the index loads
+    // of the group's earlier tiles
     const uint64_t gt = tile / kTilesPerGroup * kTilesPerGroup + lane;
     const uint64_t before_part = (wave == 0 && gt < tile) ? (uint64_t)a.tile_bytes[gt] : 0;
     const uint64_t gexcl = a.group_excl[tile / kTilesPerGroup];
-    const uint64_t total = a.tile_bytes[tile];
-    const TileSegs c = tile_segs(a.segs, t0, t1, s_lo, s_meta);
-    const uint64_t kw = t0 + (uint64_t)wave * kEncWave + lane;
-    uint64_t gap[kEncSteps];
-    uint32_t starts;
-    bool bad = false;   // reported by enc_count
-    uint32_t bytes = enc_gaps(a, c, s_lo, kw, t1, gap, starts, bad);
-    bytes = wave_sum(bytes);
-    if (lane == 0) s_wave[wave] = bytes;
+    const uint32_t total = a.tile_bytes[tile];
     if (wave == 0) {
       const uint64_t b = wave_sum(before_part);
       if (lane == 0) s_before = b;
     }
+    if (total <= kEncSlot) {
+      const enc_u32x4* slot = (const enc_u32x4*)(a.stage + tile * kEncSlot);
+      enc_u32x4* dst = (enc_u32x4*)s_out;
+      for (uint32_t i = threadIdx.x; i < (total + 15) / 16; i += kLebThreads)
+        dst[i] = __builtin_nontemporal_load(slot + i);
+    }
     __syncthreads();
     const uint64_t tile_pos = gexcl + s_before;
-    const bool staged = total <= (uint64_t)kEncLds;
-    uint64_t pos = 0;   // within the tile
-    for (uint32_t w = 0; w < wave; ++w) pos += s_wave[w];
-#pragma unroll
-    for (int it = 0; it < kEncSteps; ++it) {
-      const uint64_t k = kw + 64 * it;
-      const uint32_t len = k < t1 ? leb_len(gap[it]) : 0;
-      const uint32_t incl = wave_incl_scan(len);
-      uint64_t p = pos + incl - len;
-      if (((starts >> it) & 1u) && a.seg_byte_offsets && a.segs.num) {
-        // this entry opens its segment and every empty one just before it
-        bool st;
-        const uint32_t sg = tile_seg(a.segs, c, s_lo, k, st);
-        for (int64_t s = sg; s >= 0 && a.segs.offs[s] == k; --s)
-          a.seg_byte_offsets[s] = tile_pos + p;
-      }
-      uint64_t v = gap[it];
-      for (uint32_t m = 0; m < len; ++m) {
-        uint8_t b = (uint8_t)(v & 0x7F);
-        v >>= 7;
-        if (m + 1 < len) b |= 0x80;
-        if (staged)
-          s_out[p] = b;
-        else if (tile_pos + p < a.capacity)
-          a.out[tile_pos + p] = b;
-        ++p;
-      }
-      pos += __shfl(incl, 63);
-    }
-    __syncthreads();
-    if (staged) {
-      const uint64_t room = a.capacity > tile_pos ? a.capacity - tile_pos : 0;
+    const uint64_t room = a.capacity > tile_pos ? a.capacity - tile_pos : 0;
+    if (total <= kEncSlot) {
       enc_flush(s_out, total < room ? total : room, a.out, tile_pos);
+    } else {
+      // the code outgrew the slot: encode the tile again, each entry's bytes
+      // stored straight to the output
+      const uint64_t t0 = tile * kEncTile;
+      const uint64_t t1 = t0 + kEncTile < count ? t0 + kEncTile : count;
+      const TileSegs c = tile_segs(a.segs, t0, t1, s_lo, s_meta);   // barriers
+      const uint64_t kw = t0 + (uint64_t)wave * kEncWave + lane;
+      EncLoad L;
+      enc_load(a, kw, t1, L);
+      uint64_t gap[kEncSteps];
+      uint32_t starts;
+      bool bad = false;   // reported by enc_stage
+      const uint32_t bytes = wave_sum(enc_gaps(a, c, s_lo, kw, t1, L, gap, starts, bad));
+      if (lane == 0) s_wave[wave] = bytes;
+      __syncthreads();
+      uint32_t pos = 0;
+#pragma unroll
+      for (int w = 0; w < kLebWaves; ++w) pos += (uint32_t)w < wave ? s_wave[w] : 0u;
+      enc_walk(kw, t1, gap, pos, [&](int, uint64_t, uint32_t len, uint32_t p, uint64_t v) {
+        enc_bytes(v, len, [&](uint32_t m, uint8_t b) {
+          if (tile_pos + p + m < a.capacity) a.out[tile_pos + p + m] = b;
+        });
+      });
     }
-    __syncthreads();
+    __syncthreads();   // s_out, s_before and s_wave are reused by the next tile
   }
 }
 
-// Segments that open at or after the last entry (and the end slot) start
+// Segment byte offsets: a segment that opens at entry k < count gets its
+// tile's output position added to the tile-local offset enc_stage left;
+// segments that open at or after the last entry (and the end slot) start
 // at the total byte count.
-__global__ void enc_seg_tail_kernel(EncArgs a) {
+__global__ void enc_seg_fix_kernel(EncArgs a) {
   const uint64_t total = *a.d_nbytes;
   const uint64_t count = enc_count_of(a);
   for (uint32_t s = threadIdx.x + blockIdx.x * blockDim.x; s <= a.segs.num;
        s += blockDim.x * gridDim.x) {
-    if (s == a.segs.num || a.segs.offs[s] >= count) a.seg_byte_offsets[s] = total;
+    if (s == a.segs.num || a.segs.offs[s] >= count) {
+      a.seg_byte_offsets[s] = total;
+      continue;
+    }
+    const uint64_t tile = a.segs.offs[s] / kEncTile;
+    uint64_t pos = a.group_excl[tile / kTilesPerGroup];
+    for (uint64_t t = tile / kTilesPerGroup * kTilesPerGroup; t < tile; ++t) pos += a.tile_bytes[t];
+    a.seg_byte_offsets[s] += pos;
   }
 }
 
@@ -1080,7 +1152,8 @@ EncLayout enc_layout(uint64_t count) {
   L.tile_bytes = 0;
   L.group_sum = align_up(4 * tiles);
   L.group_excl = align_up(L.group_sum + 8 * groups);
-  L.total = align_up(L.group_excl + 8 * groups);
+  L.stage = align_up(L.group_excl + 8 * groups);
+  L.total = align_up(L.stage + (size_t)kEncSlot * tiles);
   return L;
 }
 
@@ -1108,37 +1181,38 @@ uint32_t enc_grid(uint64_t count, bool count_on_device) {
   return (uint32_t)(tiles < cap ? (tiles ? tiles : 1) : cap);
 }
 
-hipError_t launch_leb128_encode(EncArgs a, uint64_t* group_sum, uint64_t* group_excl,
-                                hipStream_t stream) {
+hipError_t launch_leb128_encode(EncArgs a, char* ws, const EncLayout& L, hipStream_t stream) {
   const uint64_t tiles = enc_tiles(a.count);   // at most
+  a.tile_bytes = (uint32_t*)(ws + L.tile_bytes);
+  a.group_excl = (uint64_t*)(ws + L.group_excl);
+  a.stage = (uint8_t*)(ws + L.stage);
   hipError_t e;
   if (tiles == 0) {
     e = launch_reset(a.d_nbytes, nullptr, 0, stream);
   } else {
     const uint32_t grid = enc_grid(a.count, a.d_count_in != nullptr);
     const uint64_t groups = groups_for(tiles);
-    hipLaunchKernelGGL(enc_count_kernel, dim3(grid), dim3(kLebThreads), 0, stream, a);
+    hipLaunchKernelGGL(enc_stage_kernel, dim3(grid), dim3(kLebThreads), 0, stream, a);
     e = hipGetLastError();
     if (e == hipSuccess) {
       hipLaunchKernelGGL(enc_group_sum_kernel, dim3((uint32_t)groups), dim3(64), 0, stream, a,
-                         group_sum);
+                         (uint64_t*)(ws + L.group_sum));
       e = hipGetLastError();
     }
     if (e == hipSuccess) {
       hipLaunchKernelGGL(seg_group_scan_kernel, dim3(1), dim3(kSegScanThreads), 0, stream,
-                         (const uint32_t*)nullptr, (const uint64_t*)group_sum, groups, group_excl,
-                         a.d_nbytes);
+                         (const uint32_t*)nullptr, (const uint64_t*)(ws + L.group_sum), groups,
+                         a.group_excl, a.d_nbytes);
       e = hipGetLastError();
     }
-    a.group_excl = group_excl;
     if (e == hipSuccess) {
-      hipLaunchKernelGGL(enc_write_kernel, dim3(grid), dim3(kLebThreads), 0, stream, a);
+      hipLaunchKernelGGL(enc_copy_kernel, dim3(grid), dim3(kLebThreads), 0, stream, a);
       e = hipGetLastError();
     }
   }
   if (e == hipSuccess && a.seg_byte_offsets) {
     const uint32_t n = a.segs.num + 1;
-    hipLaunchKernelGGL(enc_seg_tail_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(enc_seg_fix_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, a);
     e = hipGetLastError();
   }
   return e;
