@@ -134,9 +134,40 @@ def make_segments(numels, density, seed):
     return idx, np.array(offs, dtype=np.int64), bases
 
 
+def long_gap_segments(seed):
+    """Segments whose entries are ~3-byte gaps apart beside a dense one, so
+    that whole 4096-entry encoder tiles need more than 2 bytes per entry
+    (more than the encoder's staging slot: encoded again in its copy pass)
+    next to tiles that stage."""
+    r = np.random.default_rng(seed)
+    numels = [1 << 30, 1 << 30, 200_000, 1 << 30]
+    counts = [9000, 5000, 60_000, 4097]
+    bases = np.concatenate([[0], np.cumsum(numels)[:-1]]).astype(np.int64)
+    parts, offs = [], [0]
+    for n, k, b in zip(numels, counts, bases):
+        loc = np.unique(r.integers(0, n, size=k + k // 4 + 8))
+        loc = np.sort(r.choice(loc, size=k, replace=False)).astype(np.int64)
+        parts.append(loc + b)
+        offs.append(offs[-1] + k)
+    return np.concatenate(parts), np.array(offs, dtype=np.int64), bases
+
+
 @pytest.mark.parametrize("case", ["mixed", "empty_ends", "all_empty", "one", "many_tiny",
-                                  "few_hundred"])
+                                  "few_hundred", "long_gaps"])
 def test_segmented_matches_oracle(case):
+    if case == "long_gaps":
+        say("leb128 segmented", case)
+        idx, offs, bases = long_gap_segments(seed=17)
+        ref, ref_starts = oracle_segmented(idx, offs, bases)
+        # the long-gap segments outgrow 2 bytes per entry, the dense one not
+        assert ref_starts[1] - ref_starts[0] > 2 * (offs[1] - offs[0])
+        assert ref_starts[3] - ref_starts[2] < 2 * (offs[3] - offs[2])
+        got, starts = ad.delta_leb128_encode(to_dev(idx), offs, bases)
+        np.testing.assert_array_equal(host_bytes(got), ref)
+        np.testing.assert_array_equal(starts.cpu().numpy(), ref_starts)
+        back = ad.delta_leb128_decode(got, offs, bases)
+        np.testing.assert_array_equal(back.cpu().numpy(), idx)
+        return
     if case == "many_tiny":
         # thousands of 1..199-word tensors: one 16 KiB decode tile spans far
         # more segments than it caches, and a lane's 16 bytes open several
