@@ -16,6 +16,13 @@ struct LebSegs {
   int64_t base0;
 };
 
+// Segments of one encoder tile: the first and the last segment its entries
+// fall in, and the first entry of the first.
+struct EncTileSegs {
+  uint32_t first, last;
+  uint64_t lo0;
+};
+
 struct EncArgs {
   const int64_t* idx;
   uint64_t count;               // entries, or the most there can be if d_count_in is set
@@ -29,6 +36,7 @@ struct EncArgs {
   uint32_t* tile_bytes;
   uint64_t* group_excl;
   uint8_t* stage;               // per tile, its staged code
+  EncTileSegs* tile_segs;       // per tile (with segments)
 };
 
 struct DecArgs {
@@ -57,7 +65,7 @@ struct DecArgs {
 
 struct EncLayout {
   uint64_t tiles;
-  size_t tile_bytes, group_sum, group_excl, stage, total;
+  size_t tile_bytes, group_sum, group_excl, tile_segs, stage, total;
 };
 // Encoder grid for up to `count` entries.
 uint32_t enc_grid(uint64_t count, bool count_on_device);

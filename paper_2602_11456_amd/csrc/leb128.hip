@@ -107,6 +107,7 @@ __device__ __forceinline__ int64_t seg_base(const LebSegs& g, uint32_t s) {
 struct TileSegs {
   uint32_t first, last;
   bool cached;
+  uint64_t lo0;   // first entry of segment `first`
 };
 
 // seg_of by a whole wavefront: 64 evenly spaced candidates per round, so
@@ -128,7 +129,7 @@ __device__ __forceinline__ uint32_t seg_of_wave(const LebSegs& g, uint64_t k) {
 // Block-wide: contains barriers when there are segments.  e0 < e1.
 __device__ __forceinline__ TileSegs tile_segs(const LebSegs& g, uint64_t e0, uint64_t e1,
                                               uint64_t* s_lo, uint32_t* s_meta) {
-  TileSegs c{0, 0, false};
+  TileSegs c{0, 0, false, 0};
   if (g.num == 0) return c;
   if (threadIdx.x < 64) {   // wavefront 0
     const uint32_t first = seg_of_wave(g, e0);
@@ -147,6 +148,7 @@ __device__ __forceinline__ TileSegs tile_segs(const LebSegs& g, uint64_t e0, uin
     c.cached = true;
   }
   __syncthreads();
+  c.lo0 = c.cached ? s_lo[0] : g.offs[c.first];
   return c;
 }
 
@@ -162,7 +164,7 @@ __device__ __forceinline__ uint32_t tile_seg(const LebSegs& g, const TileSegs& c
   uint64_t lo;
   if (c.first == c.last) {
     s = c.first;
-    lo = c.cached ? s_lo[0] : g.offs[s];
+    lo = c.lo0;
   } else if (c.cached) {
     uint32_t a = 0, b = c.last - c.first + 1;
     while (b - a > 1) {
@@ -303,6 +305,42 @@ __device__ __forceinline__ void enc_bytes(uint64_t v, uint32_t len, Put put) {
   }
 }
 
+// Segment range of every encoder tile (first and last segment of its
+// entries, and the first entry of the first), one thread per tile, so that
+// the tile's workgroups take it with one load instead of searching.
+__global__ void enc_segs_kernel(EncArgs a) {
+  const uint64_t count = enc_count_of(a);
+  const uint64_t tiles = (count + kEncTile - 1) / kEncTile;
+  for (uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; t < tiles;
+       t += (uint64_t)gridDim.x * blockDim.x) {
+    const uint64_t t0 = t * kEncTile;
+    const uint64_t t1 = t0 + kEncTile < count ? t0 + kEncTile : count;
+    const uint32_t first = seg_of(a.segs, t0), last = seg_of(a.segs, t1 - 1);
+    a.tile_segs[t] = EncTileSegs{first, last, a.segs.offs[first]};
+  }
+}
+
+// The tile's segments from its record (contains a barrier when it spans
+// several segments, whose starts are then cached in LDS).
+__device__ __forceinline__ TileSegs enc_tile_segs(const EncArgs& a, uint64_t tile,
+                                                  uint64_t* s_lo) {
+  TileSegs c{0, 0, false, 0};
+  if (a.segs.num == 0) return c;
+  const EncTileSegs r = a.tile_segs[tile];
+  c.first = r.first;
+  c.last = r.last;
+  c.lo0 = r.lo0;
+  const uint32_t n = c.last - c.first + 1;
+  if (n > 1) {   // uniform
+    if (n <= (uint32_t)kSegLds) {
+      for (uint32_t j = threadIdx.x; j < n; j += kLebThreads) s_lo[j] = a.segs.offs[c.first + j];
+      c.cached = true;
+    }
+    __syncthreads();
+  }
+  return c;
+}
+
 // Tiles loop grid-stride (the entry count may only be known on the device).
 __global__ __launch_bounds__(kLebThreads) void enc_stage_kernel(EncArgs a) {
   __shared__ uint64_t s_lo[kSegLds];
@@ -316,10 +354,10 @@ __global__ __launch_bounds__(kLebThreads) void enc_stage_kernel(EncArgs a) {
   for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
     const uint64_t t0 = tile * kEncTile;
     const uint64_t t1 = t0 + kEncTile < count ? t0 + kEncTile : count;
-    const TileSegs c = tile_segs(a.segs, t0, t1, s_lo, s_meta);   // barriers
     const uint64_t kw = t0 + (uint64_t)wave * kEncWave + lane;
     EncLoad L;
     enc_load(a, kw, t1, L);
+    const TileSegs c = enc_tile_segs(a, tile, s_lo);
     uint64_t gap[kEncSteps];
     uint32_t starts;
     const uint32_t bytes = wave_sum(enc_gaps(a, c, s_lo, kw, t1, L, gap, starts, bad));
@@ -419,10 +457,10 @@ __global__ __launch_bounds__(kLebThreads) void enc_copy_kernel(EncArgs a) {
       // stored straight to the output
       const uint64_t t0 = tile * kEncTile;
       const uint64_t t1 = t0 + kEncTile < count ? t0 + kEncTile : count;
-      const TileSegs c = tile_segs(a.segs, t0, t1, s_lo, s_meta);   // barriers
       const uint64_t kw = t0 + (uint64_t)wave * kEncWave + lane;
       EncLoad L;
       enc_load(a, kw, t1, L);
+      const TileSegs c = enc_tile_segs(a, tile, s_lo);
       uint64_t gap[kEncSteps];
       uint32_t starts;
       bool bad = false;   // reported by enc_stage
@@ -1152,7 +1190,8 @@ EncLayout enc_layout(uint64_t count) {
   L.tile_bytes = 0;
   L.group_sum = align_up(4 * tiles);
   L.group_excl = align_up(L.group_sum + 8 * groups);
-  L.stage = align_up(L.group_excl + 8 * groups);
+  L.tile_segs = align_up(L.group_excl + 8 * groups);
+  L.stage = align_up(L.tile_segs + sizeof(EncTileSegs) * tiles);
   L.total = align_up(L.stage + (size_t)kEncSlot * tiles);
   return L;
 }
@@ -1186,14 +1225,24 @@ hipError_t launch_leb128_encode(EncArgs a, char* ws, const EncLayout& L, hipStre
   a.tile_bytes = (uint32_t*)(ws + L.tile_bytes);
   a.group_excl = (uint64_t*)(ws + L.group_excl);
   a.stage = (uint8_t*)(ws + L.stage);
+  a.tile_segs = (EncTileSegs*)(ws + L.tile_segs);
   hipError_t e;
   if (tiles == 0) {
     e = launch_reset(a.d_nbytes, nullptr, 0, stream);
   } else {
     const uint32_t grid = enc_grid(a.count, a.d_count_in != nullptr);
     const uint64_t groups = groups_for(tiles);
-    hipLaunchKernelGGL(enc_stage_kernel, dim3(grid), dim3(kLebThreads), 0, stream, a);
-    e = hipGetLastError();
+    e = hipSuccess;
+    if (a.segs.num) {
+      const uint64_t blocks = (tiles + 255) / 256;
+      hipLaunchKernelGGL(enc_segs_kernel, dim3((uint32_t)(blocks < 2048 ? blocks : 2048)),
+                         dim3(256), 0, stream, a);
+      e = hipGetLastError();
+    }
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(enc_stage_kernel, dim3(grid), dim3(kLebThreads), 0, stream, a);
+      e = hipGetLastError();
+    }
     if (e == hipSuccess) {
       hipLaunchKernelGGL(enc_group_sum_kernel, dim3((uint32_t)groups), dim3(64), 0, stream, a,
                          (uint64_t*)(ws + L.group_sum));
