@@ -246,10 +246,11 @@ __device__ __forceinline__ void enc_load(const EncArgs& a, uint64_t kw, uint64_t
 // segment, else idx - previous idx (the previous index comes from the
 // neighbouring lane).  Sets bit it of `starts` for an entry that opens a
 // segment, `bad` for a gap below 0 / 1; returns the lane's code bytes.
+// The gaps replace the indices in L.cur (each step reads its own index, and
+// its neighbour's through a shuffle, before writing the gap).
 __device__ __forceinline__ uint32_t enc_gaps(const EncArgs& a, const TileSegs& c,
                                              const uint64_t* s_lo, uint64_t kw, uint64_t t1,
-                                             const EncLoad& L, uint64_t (&gap)[kEncSteps],
-                                             uint32_t& starts, bool& bad) {
+                                             EncLoad& L, uint32_t& starts, bool& bad) {
   const uint32_t lane = lane_id();
   int64_t last = L.last;
   uint32_t bytes = 0;
@@ -257,25 +258,27 @@ __device__ __forceinline__ uint32_t enc_gaps(const EncArgs& a, const TileSegs& c
 #pragma unroll
   for (int it = 0; it < kEncSteps; ++it) {
     const uint64_t k = kw + 64 * it;
-    int64_t prev = __shfl_up(L.cur[it], 1);
+    const int64_t cur = L.cur[it];
+    int64_t prev = __shfl_up(cur, 1);
     if (lane == 0) prev = last;
-    last = __shfl(L.cur[it], 63);
-    gap[it] = 0;
+    last = __shfl(cur, 63);
+    uint64_t g = 0;
     if (k < t1) {
       bool start;
       const uint32_t seg = tile_seg(a.segs, c, s_lo, k, start);
       int64_t d;
       if (start) {
-        d = L.cur[it] - seg_base(a.segs, seg);
+        d = cur - seg_base(a.segs, seg);
         bad |= d < 0;
       } else {
-        d = L.cur[it] - prev;
+        d = cur - prev;
         bad |= d < 1;
       }
-      gap[it] = d < 0 ? 0 : (uint64_t)d;
+      g = d < 0 ? 0 : (uint64_t)d;
       starts |= (uint32_t)start << it;
-      bytes += leb_len(gap[it]);
+      bytes += leb_len(g);
     }
+    L.cur[it] = (int64_t)g;
   }
   return bytes;
 }
@@ -284,14 +287,15 @@ __device__ __forceinline__ uint32_t enc_gaps(const EncArgs& a, const TileSegs& c
 // lengths, starting at `pos`, this wavefront's offset in the tile); calls
 // f(it, k, len, p, gap) for each of the lane's entries inside the tile.
 template <typename F>
-__device__ __forceinline__ void enc_walk(uint64_t kw, uint64_t t1, const uint64_t (&gap)[kEncSteps],
+__device__ __forceinline__ void enc_walk(uint64_t kw, uint64_t t1, const int64_t (&gap)[kEncSteps],
                                          uint32_t pos, F f) {
 #pragma unroll
   for (int it = 0; it < kEncSteps; ++it) {
     const uint64_t k = kw + 64 * it;
-    const uint32_t len = k < t1 ? leb_len(gap[it]) : 0;
+    const uint64_t g = (uint64_t)gap[it];
+    const uint32_t len = k < t1 ? leb_len(g) : 0;
     const uint32_t incl = wave_incl_scan(len);
-    if (len) f(it, k, len, pos + incl - len, gap[it]);
+    if (len) f(it, k, len, pos + incl - len, g);
     pos += __shfl(incl, 63);
   }
 }
@@ -358,9 +362,8 @@ __global__ __launch_bounds__(kLebThreads) void enc_stage_kernel(EncArgs a) {
     EncLoad L;
     enc_load(a, kw, t1, L);
     const TileSegs c = enc_tile_segs(a, tile, s_lo);
-    uint64_t gap[kEncSteps];
     uint32_t starts;
-    const uint32_t bytes = wave_sum(enc_gaps(a, c, s_lo, kw, t1, L, gap, starts, bad));
+    const uint32_t bytes = wave_sum(enc_gaps(a, c, s_lo, kw, t1, L, starts, bad));
     if (lane == 0) s_wave[wave] = bytes;
     __syncthreads();
     uint32_t pos = 0, total = 0;
@@ -371,7 +374,7 @@ __global__ __launch_bounds__(kLebThreads) void enc_stage_kernel(EncArgs a) {
     }
     const bool staged = total <= kEncSlot;
     const bool segs_out = a.seg_byte_offsets && a.segs.num;
-    enc_walk(kw, t1, gap, pos, [&](int it, uint64_t k, uint32_t len, uint32_t p, uint64_t v) {
+    enc_walk(kw, t1, L.cur, pos, [&](int it, uint64_t k, uint32_t len, uint32_t p, uint64_t v) {
       if (segs_out && ((starts >> it) & 1u)) {
         // this entry opens its segment and every empty one just before it:
         // their tile-local offset (made absolute by enc_seg_fix)
@@ -461,16 +464,15 @@ __global__ __launch_bounds__(kLebThreads) void enc_copy_kernel(EncArgs a) {
       EncLoad L;
       enc_load(a, kw, t1, L);
       const TileSegs c = enc_tile_segs(a, tile, s_lo);
-      uint64_t gap[kEncSteps];
       uint32_t starts;
       bool bad = false;   // reported by enc_stage
-      const uint32_t bytes = wave_sum(enc_gaps(a, c, s_lo, kw, t1, L, gap, starts, bad));
+      const uint32_t bytes = wave_sum(enc_gaps(a, c, s_lo, kw, t1, L, starts, bad));
       if (lane == 0) s_wave[wave] = bytes;
       __syncthreads();
       uint32_t pos = 0;
 #pragma unroll
       for (int w = 0; w < kLebWaves; ++w) pos += (uint32_t)w < wave ? s_wave[w] : 0u;
-      enc_walk(kw, t1, gap, pos, [&](int, uint64_t, uint32_t len, uint32_t p, uint64_t v) {
+      enc_walk(kw, t1, L.cur, pos, [&](int, uint64_t, uint32_t len, uint32_t p, uint64_t v) {
         enc_bytes(v, len, [&](uint32_t m, uint8_t b) {
           if (tile_pos + p + m < a.capacity) a.out[tile_pos + p + m] = b;
         });
