@@ -39,6 +39,14 @@ struct EncArgs {
   EncTileSegs* tile_segs;       // per tile (with segments)
 };
 
+// A 16 KiB decode tile's first entry and, with segments, the first and the
+// last segment of its entries and the first entry of the first.
+struct DecTileRec {
+  uint64_t e0;
+  uint32_t first, last;
+  uint64_t lo0;
+};
+
 struct DecArgs {
   const uint8_t* in;
   uint64_t nbytes;
@@ -61,6 +69,7 @@ struct DecArgs {
   uint32_t num_tensors;
   const uint16_t* val;          // device [capacity]
   uint64_t* gexcl_v;            // index just before each group of tiles
+  DecTileRec* tile_recs;        // per byte tile (dec_recs_kernel)
 };
 
 struct EncLayout {
@@ -72,7 +81,7 @@ uint32_t enc_grid(uint64_t count, bool count_on_device);
 struct DecLayout {
   uint64_t btiles;
   size_t tile_terms, group_sum, group_excl, tile_f, tile_v, wave_f, wave_v, gsum_f, gsum_v,
-      gexcl_v, total;
+      gexcl_v, tile_recs, total;
 };
 EncLayout enc_layout(uint64_t count);
 DecLayout dec_layout(uint64_t nbytes);

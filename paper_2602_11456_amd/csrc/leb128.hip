@@ -102,55 +102,14 @@ __device__ __forceinline__ int64_t seg_base(const LebSegs& g, uint32_t s) {
   return g.num ? (int64_t)g.bases[s] : g.base0;
 }
 
-// The segments that a tile's entries [e0, e1) fall in: first..last, with
-// their starts cached in LDS when there are few.
+// The segments that a tile's entries fall in: first..last, with their
+// starts cached in LDS when there are few (from the tile's record, written
+// by enc_segs_kernel or dec_recs_kernel).
 struct TileSegs {
   uint32_t first, last;
   bool cached;
   uint64_t lo0;   // first entry of segment `first`
 };
-
-// seg_of by a whole wavefront: 64 evenly spaced candidates per round, so
-// that a table of up to 4096 segments takes two dependent loads, not twelve.
-__device__ __forceinline__ uint32_t seg_of_wave(const LebSegs& g, uint64_t k) {
-  if (g.num == 0) return 0;
-  uint32_t lo = 0, hi = g.num;   // the answer is in [lo, hi)
-  while (hi - lo > 1) {
-    const uint32_t step = (hi - lo + 63) / 64;
-    const uint32_t cand = lo + lane_id() * step;
-    const uint64_t m = __ballot(cand < hi && g.offs[cand] <= k);
-    const uint32_t last = m ? 63 - __builtin_clzll(m) : 0;
-    lo = lo + last * step;
-    hi = lo + step < hi ? lo + step : hi;
-  }
-  return lo;
-}
-
-// Block-wide: contains barriers when there are segments.  e0 < e1.
-__device__ __forceinline__ TileSegs tile_segs(const LebSegs& g, uint64_t e0, uint64_t e1,
-                                              uint64_t* s_lo, uint32_t* s_meta) {
-  TileSegs c{0, 0, false, 0};
-  if (g.num == 0) return c;
-  if (threadIdx.x < 64) {   // wavefront 0
-    const uint32_t first = seg_of_wave(g, e0);
-    const uint32_t last = seg_of_wave(g, e1 - 1);
-    if (threadIdx.x == 0) {
-      s_meta[0] = first;
-      s_meta[1] = last;
-    }
-  }
-  __syncthreads();
-  c.first = s_meta[0];
-  c.last = s_meta[1];
-  const uint32_t n = c.last - c.first + 1;
-  if (n <= (uint32_t)kSegLds) {
-    for (uint32_t j = threadIdx.x; j < n; j += kLebThreads) s_lo[j] = g.offs[c.first + j];
-    c.cached = true;
-  }
-  __syncthreads();
-  c.lo0 = c.cached ? s_lo[0] : g.offs[c.first];
-  return c;
-}
 
 // Segment of entry e of the tile, and whether e opens it (entry 0 always
 // opens the first segment).
@@ -179,20 +138,6 @@ __device__ __forceinline__ uint32_t tile_seg(const LebSegs& g, const TileSegs& c
   }
   start = e == 0 || e == lo;
   return s;
-}
-
-// Sum of counts[g * kTilesPerGroup .. tile) by wavefront 0, returned to
-// every thread through LDS (contains a barrier).
-template <typename T>
-__device__ __forceinline__ uint64_t group_before(const T* counts, uint64_t tile, uint64_t* s_out) {
-  if (threadIdx.x < 64) {
-    const uint64_t t = tile / kTilesPerGroup * kTilesPerGroup + threadIdx.x;
-    uint64_t v = t < tile ? (uint64_t)counts[t] : 0;
-    v = wave_sum(v);
-    if (threadIdx.x == 0) *s_out = v;
-  }
-  __syncthreads();
-  return *s_out;
 }
 
 __device__ __forceinline__ void raise_flag(uint32_t* err) {
@@ -348,7 +293,6 @@ __device__ __forceinline__ TileSegs enc_tile_segs(const EncArgs& a, uint64_t til
 // Tiles loop grid-stride (the entry count may only be known on the device).
 __global__ __launch_bounds__(kLebThreads) void enc_stage_kernel(EncArgs a) {
   __shared__ uint64_t s_lo[kSegLds];
-  __shared__ uint32_t s_meta[2];
   __shared__ uint32_t s_wave[kLebWaves];
   __shared__ __align__(16) uint8_t s_out[kEncSlot];
   const uint64_t count = enc_count_of(a);
@@ -426,7 +370,6 @@ __device__ __forceinline__ void enc_flush(const uint8_t* s_out, uint64_t n, uint
 
 __global__ __launch_bounds__(kLebThreads) void enc_copy_kernel(EncArgs a) {
   __shared__ uint64_t s_lo[kSegLds];
-  __shared__ uint32_t s_meta[2];
   __shared__ uint32_t s_wave[kLebWaves];
   __shared__ uint64_t s_before;
   __shared__ __align__(16) uint8_t s_out[kEncSlot];
@@ -816,22 +759,59 @@ __device__ __forceinline__ void dec_wave_fold(const DecArgs& a, const TileSegs& 
   }
 }
 
+// First entry and segment range of every byte tile, after the count scan:
+// one wavefront per group of 64 tiles (a tile per lane, an exclusive scan
+// of their terms), so that the decode kernels take them with one load
+// instead of a group sum and a search per workgroup.
+__global__ __launch_bounds__(256) void dec_recs_kernel(DecArgs a, uint64_t btiles) {
+  const uint64_t g = (uint64_t)blockIdx.x * 4 + wave_id();
+  const uint64_t t = g * kTilesPerGroup + lane_id();
+  if (g * kTilesPerGroup >= btiles) return;   // uniform per wavefront
+  const uint32_t terms = t < btiles ? a.tile_terms[t] : 0u;
+  const uint32_t incl = wave_incl_scan(terms);
+  if (t >= btiles) return;
+  DecTileRec r{a.group_excl[g] + (incl - terms), 0u, 0u, 0ull};
+  if (terms && a.segs.num) {
+    r.first = seg_of(a.segs, r.e0);
+    r.last = seg_of(a.segs, r.e0 + terms - 1);
+    r.lo0 = a.segs.offs[r.first];
+  }
+  a.tile_recs[t] = r;
+}
+
+// The tile's segments from its record; their starts go to s_lo, which the
+// caller's next barrier publishes.
+__device__ __forceinline__ TileSegs dec_tile_segs(const DecArgs& a, const DecTileRec& r,
+                                                  uint64_t* s_lo) {
+  TileSegs c{0, 0, false, 0};
+  if (a.segs.num == 0) return c;
+  c.first = r.first;
+  c.last = r.last;
+  c.lo0 = r.lo0;
+  const uint32_t n = c.last - c.first + 1;
+  if (n <= (uint32_t)kSegLds) {
+    for (uint32_t j = threadIdx.x; j < n; j += kLebThreads)
+      s_lo[j] = j == 0 ? r.lo0 : a.segs.offs[c.first + j];
+    c.cached = true;
+  }
+  return c;
+}
+
 __global__ __launch_bounds__(kLebThreads) void dec_fold_kernel(DecArgs a, bool aligned) {
   __shared__ __align__(16) uint8_t s_bytes[kDecBack + kDecTile];
   __shared__ uint64_t s_lo[kSegLds];
-  __shared__ uint32_t s_meta[2];
   __shared__ uint32_t s_wterm[kLebWaves];
   __shared__ uint32_t s_wf[kLebWaves];
   __shared__ uint64_t s_wv[kLebWaves];
-  __shared__ uint64_t s_tmp;
   const uint64_t tile = blockIdx.x;
   const uint64_t b0 = tile * kDecTile;
+  const DecTileRec rec = a.tile_recs[tile];
   dec_load_tile(a, b0, aligned, s_bytes);                                    // barrier
-  const uint64_t e0 = a.group_excl[tile / kTilesPerGroup] +
-                      group_before(a.tile_terms, tile, &s_tmp);              // barrier
+  const uint64_t e0 = rec.e0;
   const uint32_t terms = a.tile_terms[tile];
   const uint32_t wt = dec_wave_terms(s_bytes, b0, a.nbytes);
   if (lane_id() == 0) s_wterm[wave_id()] = wt;
+  const TileSegs c = dec_tile_segs(a, rec, s_lo);
   __syncthreads();
   bool bad = false;
   if (terms == 0) {   // uniform: no number ends in this tile
@@ -846,7 +826,6 @@ __global__ __launch_bounds__(kLebThreads) void dec_fold_kernel(DecArgs a, bool a
     if (bad) raise_flag(a.err);
     return;
   }
-  const TileSegs c = tile_segs(a.segs, e0, e0 + terms, s_lo, s_meta);     // barriers
   uint32_t f;
   uint64_t v;
   dec_wave_fold(a, c, s_lo, s_bytes, b0, dec_wave_e0(e0, s_wterm), bad, f, v);
@@ -950,9 +929,7 @@ constexpr int kDecStepEntries = 64 * 16;
 __global__ __launch_bounds__(kLebThreads) void dec_write_kernel(DecArgs a, bool aligned) {
   __shared__ __align__(16) uint8_t s_bytes[kDecBack + kDecTile];
   __shared__ uint64_t s_lo[kSegLds];
-  __shared__ uint32_t s_meta[2];
   __shared__ uint32_t s_wterm[kLebWaves];
-  __shared__ uint64_t s_tmp;
   __shared__ uint64_t s_carry;
   // every wavefront's decoded indices of one step, written out coalesced
   __shared__ uint64_t s_out[kLebWaves][kDecStepEntries];
@@ -960,9 +937,9 @@ __global__ __launch_bounds__(kLebThreads) void dec_write_kernel(DecArgs a, bool 
   const uint32_t terms = a.tile_terms[tile];
   if (terms == 0) return;   // uniform
   const uint64_t b0 = tile * kDecTile;
+  const DecTileRec rec = a.tile_recs[tile];
   dec_load_tile(a, b0, aligned, s_bytes);                                    // barrier
-  const uint64_t e0 = a.group_excl[tile / kTilesPerGroup] +
-                      group_before(a.tile_terms, tile, &s_tmp);              // barrier
+  const uint64_t e0 = rec.e0;
   if (e0 >= a.capacity) return;   // uniform: nothing of this tile is kept
   const uint32_t lane = lane_id(), wave = wave_id();
   if (threadIdx.x < 64) {   // index of the entry just before the tile
@@ -974,8 +951,8 @@ __global__ __launch_bounds__(kLebThreads) void dec_write_kernel(DecArgs a, bool 
   }
   const uint32_t wt = dec_wave_terms(s_bytes, b0, a.nbytes);
   if (lane == 0) s_wterm[wave] = wt;
+  const TileSegs c = dec_tile_segs(a, rec, s_lo);
   __syncthreads();
-  const TileSegs c = tile_segs(a.segs, e0, e0 + terms, s_lo, s_meta);     // barriers
   const uint64_t ew = dec_wave_e0(e0, s_wterm);
   // index of the entry before this wavefront's first, from dec_fold's
   // per-wavefront folds
@@ -1069,9 +1046,7 @@ __device__ __forceinline__ uint32_t dec_find_tensor(const uint64_t* tbases, uint
 __global__ __launch_bounds__(kLebThreads) void dec_apply_kernel(DecArgs a, bool aligned) {
   __shared__ __align__(16) uint8_t s_bytes[kDecBack + kDecTile];
   __shared__ uint64_t s_lo[kSegLds];
-  __shared__ uint32_t s_meta[2];
   __shared__ uint32_t s_wterm[kLebWaves];
-  __shared__ uint64_t s_tmp;
   __shared__ uint64_t s_carry;
   __shared__ uint64_t s_out[kLebWaves][kDecStepEntries];
   const uint64_t tile = blockIdx.x;
@@ -1079,9 +1054,9 @@ __global__ __launch_bounds__(kLebThreads) void dec_apply_kernel(DecArgs a, bool 
   const uint32_t terms = a.tile_terms[tile];
   if (terms == 0) return;   // uniform
   const uint64_t b0 = tile * kDecTile;
+  const DecTileRec rec = a.tile_recs[tile];
   dec_load_tile(a, b0, aligned, s_bytes);                                    // barrier
-  const uint64_t e0 = a.group_excl[tile / kTilesPerGroup] +
-                      group_before(a.tile_terms, tile, &s_tmp);              // barrier
+  const uint64_t e0 = rec.e0;
   if (e0 >= a.capacity) {   // uniform: no value for any entry of this tile
     if (threadIdx.x == 0) raise_flag(a.err);
     return;
@@ -1096,8 +1071,8 @@ __global__ __launch_bounds__(kLebThreads) void dec_apply_kernel(DecArgs a, bool 
   }
   const uint32_t wt = dec_wave_terms(s_bytes, b0, a.nbytes);
   if (lane == 0) s_wterm[wave] = wt;
+  const TileSegs c = dec_tile_segs(a, rec, s_lo);
   __syncthreads();
-  const TileSegs c = tile_segs(a.segs, e0, e0 + terms, s_lo, s_meta);     // barriers
   const uint64_t ew = dec_wave_e0(e0, s_wterm);
   uint64_t run = s_carry;
   for (uint32_t w = 0; w < wave; ++w)
@@ -1212,7 +1187,8 @@ DecLayout dec_layout(uint64_t nbytes) {
   L.gsum_f = align_up(L.wave_v + 8 * kLebWaves * bt);
   L.gsum_v = align_up(L.gsum_f + 4 * gb);
   L.gexcl_v = align_up(L.gsum_v + 8 * gb);
-  L.total = align_up(L.gexcl_v + 8 * gb);
+  L.tile_recs = align_up(L.gexcl_v + 8 * gb);
+  L.total = align_up(L.tile_recs + sizeof(DecTileRec) * bt);
   return L;
 }
 
@@ -1289,6 +1265,11 @@ hipError_t launch_leb128_decode(DecArgs a, const DecLayout& L, char* ws, hipStre
   if ((e = launch_group_scan(a.tile_terms, L.btiles, (uint64_t*)(ws + L.group_sum), a.group_excl,
                              a.d_count, stream)) != hipSuccess)
     return e;
+  a.tile_recs = (DecTileRec*)(ws + L.tile_recs);
+  const uint64_t rec_blocks = (groups_for(L.btiles) + 3) / 4;
+  hipLaunchKernelGGL(dec_recs_kernel, dim3((uint32_t)rec_blocks), dim3(256), 0, stream, a,
+                     L.btiles);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(dec_fold_kernel, grid, block, 0, stream, a, aligned);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const uint64_t groups = groups_for(L.btiles);
