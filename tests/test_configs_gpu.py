@@ -91,9 +91,10 @@ def oracle_every_tensor(ws, idx, val, offs, label, codes=()):
 
 
 def planned_equals(ws, idx, val, offs, label):
-    """The planned call (tensor table built once, as the benchmark times
-    it) writes exactly what delta_extract_multi wrote, which is compared
-    with the oracle on every tensor."""
+    """The planned calls (tensor table built once, as the benchmark times
+    them): the extract writes exactly what delta_extract_multi wrote, which
+    is compared with the oracle on every tensor, and the count-only pass
+    gives its count."""
     plan = ad.MultiPlan(ws.prev, ws.new).prepare()
     k = idx.numel()
     pidx = torch.empty(k + 1, dtype=torch.int64, device=DEV)
@@ -107,8 +108,37 @@ def planned_equals(ws, idx, val, offs, label):
     assert int(cnt.item()) == k, label
     assert torch.equal(pidx[:k], idx) and torch.equal(poffs, offs), label
     assert torch.equal(pval[:k].view(torch.int16), val.view(torch.int16)), label
+    cnt.fill_(-1)
+    torch.cuda.synchronize()
+    ad.delta_count_changed_multi_into(plan, cnt, work)
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == k, label
     del plan, pidx, pval, work
-    say(label, "planned call ok")
+    say(label, "planned calls ok")
+
+
+def planned_coded_equals(ws, code, cb, label):
+    """The planned extract that writes LEB128 itself writes the same bytes
+    and per-tensor byte offsets as the unplanned one."""
+    plan = ad.MultiPlan(ws.prev, ws.new).prepare()
+    K = ws.total_planted
+    pcode = torch.empty(code.numel() + 64, dtype=torch.uint8, device=DEV)
+    pval = torch.empty(K + 1, dtype=torch.bfloat16, device=DEV)
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    nb = torch.zeros(1, dtype=torch.int64, device=DEV)
+    poffs = torch.zeros(plan.T + 1, dtype=torch.int64, device=DEV)
+    pboffs = torch.zeros(plan.T + 1, dtype=torch.int64, device=DEV)
+    work = torch.empty(ad.delta_extract_multi_leb128_workspace_bytes(plan.numels),
+                       dtype=torch.uint8, device=DEV)
+    torch.cuda.synchronize()
+    ad.delta_extract_multi_leb128_into(plan, pcode, pval, cnt, nb, work, poffs, pboffs)
+    torch.cuda.synchronize()
+    n = int(nb.item())
+    assert int(cnt.item()) == K and n == code.numel(), label
+    assert torch.equal(pcode[:n], code), label
+    np.testing.assert_array_equal(pboffs.cpu().numpy(), cb)
+    del plan, pcode, pval, work
+    say(label, "planned coded extract ok")
 
 
 def round_trip(ws, idx, val, label):
@@ -199,6 +229,7 @@ def test_weight_set(model, density):
     round_trip(ws, idx, val, label)
     buf, sb = leb128_full(ws, idx, val, offs, label)
     code, cb = coded_full(ws, idx, val, offs, label, buf, sb)
+    planned_coded_equals(ws, code, cb, label)
     oracle_every_tensor(ws, idx, val, offs, label, codes=[(buf, sb), (code, cb)])
 
 
