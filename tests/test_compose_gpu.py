@@ -77,6 +77,39 @@ def test_compose_edge_cases():
     check([y, x])
 
 
+def test_compose_windows_and_rounds():
+    # tiles whose index range is wider than one window (sparse indices over
+    # 2^40 values), a run denser than its chunk (a cluster in the smaller
+    # delta), negative and extreme indices, the widest single pass (16
+    # deltas) and chains that need a second and a third round
+    r = np.random.default_rng(77)
+
+    def sparse(k, seed):
+        g = np.random.default_rng(seed)
+        return (np.sort(g.choice(1 << 40, k, replace=False)).astype(np.int64),
+                g.integers(0, 1 << 16, k, dtype=np.uint16))
+
+    check([sparse(3000, s) for s in range(3)])
+    cluster = (np.arange(5_000_000, 5_006_000, dtype=np.int64),
+               r.integers(0, 1 << 16, 6000, dtype=np.uint16))
+    check([rand_delta(1_000_000, 0.01, seed=3), cluster])
+    check([cluster, rand_delta(1_000_000, 0.01, seed=4)])
+    top = (1 << 63) - 1
+    check([(np.array([-(1 << 62), -5, 0, 7, 1 << 62, top - 1, top], np.int64),
+            np.arange(7, dtype=np.uint16)),
+           (np.array([-(1 << 62), 3, top], np.int64), np.array([100, 101, 102], np.uint16))])
+    for K, n, dens in ((16, 60_000, 0.05), (17, 20_000, 0.05), (40, 5_000, 0.2)):
+        say("compose rounds K", K)
+        check([rand_delta(n, dens, seed=500 + K * 100 + d) for d in range(K)])
+
+
+def test_compose_flags_unsorted_input():
+    a = rand_delta(100_000, 0.05, seed=9)
+    bad = (a[0][::-1].copy(), a[1])
+    with pytest.raises(ad.DeltaError):
+        ad.delta_compose([to_dev(*a), to_dev(*bad)])
+
+
 def test_compose_capacity_truncates():
     deltas_h = [rand_delta(200_000, 0.05, seed=40 + d) for d in range(3)]
     ref_idx, ref_val, ref_cnt = oracle.compose(deltas_h)
