@@ -98,8 +98,16 @@ __device__ __forceinline__ uint32_t seg_of(const LebSegs& g, uint64_t k) {
   }
   return lo;
 }
+// base0 as a value with no address: otherwise the compiler may merge the
+// two reads of a base into one load through a pointer chosen between
+// base0 and bases[s], which needs base0 in (slow) scratch memory.
+__device__ __forceinline__ int64_t seg_base0(const LebSegs& g) {
+  int64_t b = g.base0;
+  __asm__ volatile("" : "+v"(b));
+  return b;
+}
 __device__ __forceinline__ int64_t seg_base(const LebSegs& g, uint32_t s) {
-  return g.num ? (int64_t)g.bases[s] : g.base0;
+  return g.num ? (int64_t)g.bases[s] : seg_base0(g);
 }
 
 // The segments that a tile's entries fall in: first..last, with their
@@ -647,7 +655,7 @@ __device__ __forceinline__ bool seg_step(const LebSegs& g, const TileSegs& c,
                                          const uint64_t* s_lo, SegCursor& r, uint64_t e,
                                          int64_t& base) {
   if (g.num == 0) {
-    base = g.base0;
+    base = seg_base0(g);
     return e == 0;
   }
   while (r.next <= e) {
