@@ -25,8 +25,10 @@ Single tensors (int32 and int64 indices, the workspace and the no-allocation
 entry points) and delta chains (composition of random chains of 1-20
 deltas against the oracle's composition; the one-pass catch-up, or for more
 than 16 deltas the composed delta applied, against the oracle's replay)
-are swept the same way.  The expected values come from the oracle
-alone.
+are swept the same way, and so are the chunked pipelines to pinned host
+memory (random chunk sizes and 1-4 streams; the coded kind against the
+oracle's coding of every chunk's indices relative to the chunk's first
+word).  The expected values come from the oracle alone.
 """
 import numpy as np
 import pytest
@@ -276,3 +278,29 @@ def test_random_chain(seed):
         ad.delta_apply_multi(ws, c_idx, c_val, check=True)
     got = np.concatenate([host_u16(w) for w in ws]) if ws else np.zeros(0, np.uint16)
     np.testing.assert_array_equal(got, ref)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_pipeline(seed):
+    sizes, hp, hn, dp, dn = make_case(40_000 + seed)
+    r = np.random.default_rng(50_000 + seed)
+    chunk = int(r.choice([int(r.integers(1, 50_000)), TILE * int(r.integers(1, 9)) + 3,
+                          1 << 20, 1 << 27]))
+    streams = int(r.integers(1, 5))
+    total = sum(sizes)
+    ref_idx, ref_val, _, ref_cnt = oracle.extract_multi(hp, hn)
+    say(f"pipeline {seed}: {len(sizes)} tensors, {total} words, chunk {chunk}, "
+        f"{streams} streams, {ref_cnt} changed")
+    h_idx, h_val = ad.delta_extract_pipelined(dp, dn, chunk_elems=chunk, num_streams=streams)
+    np.testing.assert_array_equal(h_idx.numpy(), ref_idx)
+    np.testing.assert_array_equal(h_val.view(torch.int16).numpy().view(np.uint16), ref_val)
+    hb, hv, counts, used = ad.delta_extract_pipelined_leb128(dp, dn, chunk_elems=chunk,
+                                                            num_streams=streams)
+    nchunks = -(-total // used) if total else 0
+    edges = np.searchsorted(ref_idx, np.arange(nchunks + 1, dtype=np.int64) * used)
+    parts = [oracle.leb128_encode(ref_idx[edges[c]:edges[c + 1]] - c * used)[0]
+             for c in range(nchunks)]
+    ref_bytes = np.concatenate(parts) if parts else np.zeros(0, np.uint8)
+    np.testing.assert_array_equal(np.array(counts, dtype=np.int64), np.diff(edges))
+    np.testing.assert_array_equal(hb.numpy(), ref_bytes)
+    np.testing.assert_array_equal(hv.view(torch.int16).numpy().view(np.uint16), ref_val)
