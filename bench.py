@@ -104,6 +104,53 @@ def measure_ceilings():
     return json.loads(r.stdout.strip().splitlines()[-1])
 
 
+def apply_path(words, count):
+    """Which path delta_apply_multi_sorted takes for `count` entries over
+    `words` words: the tile merge from one word in 32, the scatter below."""
+    return "tile merge" if count > 0 and count >= words // 32 else "scatter"
+
+
+def apply_roofline(N, K, app_s, apply_bytes, apply_achieved, apply_traffic, lines, ceiling,
+                   ceilings):
+    """The apply's roofline for the path it took: the scatter against the
+    measured rate of partial-line writes, the tile merge against HBM peak
+    for its bytes (every word read and written once, plus the delta)."""
+    if apply_path(N, K) == "tile merge":
+        moved = 4 * N + 10 * K
+        return {
+            "kernel": "apply_merge_kernel (16384-word tiles read, patched in LDS, written whole)",
+            "bound": "hbm",
+            "achieved": round(moved / app_s / 1e9, 2),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(moved / app_s / 1e9 / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "algorithmic_bytes": moved,
+            "note": "a delta of at least one word in 32 touches nearly every 64-byte line; "
+                    "the merge reads and writes every word once instead of one partial-line "
+                    "write per touched line",
+        }
+    return {
+        "kernel": "apply_multi_kernel (scattered 2-byte stores)",
+        "bound": "hbm",
+        "achieved": round(apply_achieved, 2),
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": round(apply_achieved / HBM_PEAK_GBPS, 4),
+        "traffic": apply_traffic,
+        "algorithmic_bytes": apply_bytes,
+        "lines_touched": lines,
+        "line_writes_per_s": round(lines / app_s, 1),
+        "ceiling_line_writes_per_s": ceiling,
+        "frac_of_ceiling": round(lines / app_s / ceiling, 4) if ceiling else None,
+        "ceilings_probe": ceilings,
+        "note": "each touched 64-byte line costs one partial-line write at the memory; "
+                "the ceiling is the rate of such writes with no loads at all, measured "
+                "in this run by paper_2602_11456_amd/probes/ceilings (full-line writes "
+                "are faster, but making a line full needs its old words: a read)",
+    }
+
+
 def touched_lines(weights, idx, numels):
     """Distinct 64-byte lines of the weight tensors that a delta's entries
     fall in (counted with torch on the GPU, outside any timed region): the
@@ -759,20 +806,22 @@ def sweep_measurement(ad, synth, dev, stream, reps):
         cnt = torch.zeros(1, dtype=torch.int64, device=dev)
         work = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=dev)
         roll = [p.clone() for p in ws.prev]
-        aws = torch.empty(max(ad.delta_apply_multi_workspace_bytes(plan.T), 1),
+        aws = torch.empty(max(ad.delta_apply_multi_sorted_workspace_bytes(plan.T), 1),
                           dtype=torch.uint8, device=dev)
         ad.delta_extract_multi_into(plan, out_idx, out_val, cnt, work, None, stream)
         torch.cuda.synchronize()
         K = int(cnt.item())
         if K != Kp:
             raise RuntimeError(f"{key}: extract found {K} changed words, {Kp} planted")
-        ad.delta_apply_multi(roll, out_idx[:K], out_val[:K], workspace=aws, stream=stream)
+        ad.delta_apply_multi(roll, out_idx[:K], out_val[:K], workspace=aws, stream=stream,
+                             sorted_indices=True)
         ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
         for e0, e1, e2 in ev:
             e0.record(stream)
             ad.delta_extract_multi_into(plan, out_idx, out_val, cnt, work, None, stream)
             e1.record(stream)
-            ad.delta_apply_multi(roll, out_idx[:K], out_val[:K], workspace=aws, stream=stream)
+            ad.delta_apply_multi(roll, out_idx[:K], out_val[:K], workspace=aws, stream=stream,
+                                 sorted_indices=True)
             e2.record(stream)
         torch.cuda.synchronize()
         for r, q in zip(roll, ws.new):
@@ -786,6 +835,7 @@ def sweep_measurement(ad, synth, dev, stream, reps):
                     "extract_GBps_scanned": round(4 * N / (te / 1e3) / 1e9, 1),
                     "extract_pct_hbm_peak": round(100 * alg / (te / 1e3) / 1e9 / HBM_PEAK_GBPS, 2),
                     "apply_ms": round(ta, 4),
+                    "apply_path": apply_path(N, K),
                     "apply_GBps_algorithmic": round(12 * K / (ta / 1e3) / 1e9, 1),
                     "apply_changed_words_per_s": round(K / (ta / 1e3), 1)}
         log(f"{key}: extract {te:.3f} ms, apply {ta:.3f} ms")
@@ -892,7 +942,7 @@ def main():
     d_offs = torch.zeros(plan.T + 1, dtype=torch.int64, device=dev)
     work = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=dev)
     rollout = [p.clone() for p in ws.prev]
-    apply_ws = torch.empty(max(ad.delta_apply_multi_workspace_bytes(plan.T), 1),
+    apply_ws = torch.empty(max(ad.delta_apply_multi_sorted_workspace_bytes(plan.T), 1),
                            dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
@@ -900,8 +950,9 @@ def main():
         ad.delta_extract_multi_into(plan, out_idx, out_val, d_count, work, d_offs, stream)
 
     def apply(k):
+        # the extract's indices are strictly increasing: the sorted entry point
         ad.delta_apply_multi(rollout, out_idx[:k], out_val[:k], workspace=apply_ws,
-                             stream=stream)
+                             stream=stream, sorted_indices=True)
 
     # warm-up (also checks the count once)
     extract()
@@ -1029,25 +1080,9 @@ def main():
             "ms": round(app_avg, 4),
             "GBps_algorithmic": round(apply_achieved, 2),
             "changed_words_per_s": round(K / app_s, 1),
-            "roofline": {
-                "kernel": "apply_multi_kernel (scattered 2-byte stores)",
-                "bound": "hbm",
-                "achieved": round(apply_achieved, 2),
-                "peak": HBM_PEAK_GBPS,
-                "unit": "GB/s",
-                "frac": round(apply_achieved / HBM_PEAK_GBPS, 4),
-                "traffic": apply_traffic,
-                "algorithmic_bytes": apply_bytes,
-                "lines_touched": lines,
-                "line_writes_per_s": round(lines / app_s, 1),
-                "ceiling_line_writes_per_s": ceiling,
-                "frac_of_ceiling": round(lines / app_s / ceiling, 4) if ceiling else None,
-                "ceilings_probe": ceilings,
-                "note": "each touched 64-byte line costs one partial-line write at the memory; "
-                        "the ceiling is the rate of such writes with no loads at all, measured "
-                        "in this run by paper_2602_11456_amd/probes/ceilings (full-line writes "
-                        "are faster, but making a line full needs its old words: a read)",
-            },
+            "path": apply_path(N, K),
+            "roofline": apply_roofline(N, K, app_s, apply_bytes, apply_achieved, apply_traffic,
+                                       lines, ceiling, ceilings),
         },
         "roofline": {
             "kernel": "stage_kernel (reads and compares both copies)",

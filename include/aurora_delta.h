@@ -314,6 +314,29 @@ delta_status_t delta_apply_multi(uint16_t* const* weight_ptrs, const uint64_t* n
                                  uint64_t count, uint32_t* d_error_flag, void* workspace,
                                  size_t workspace_bytes, hipStream_t stream);
 
+/* Workspace bytes for delta_apply_multi_sorted over `num_tensors` tensors. */
+size_t delta_apply_multi_sorted_workspace_bytes(int32_t num_tensors);
+
+/*
+ * delta_apply_multi_sorted — delta_apply_multi (Sec. 5.1 scatter into the
+ * flattened tensor list, Sec. 5.2 activation) for a delta whose indices are
+ * strictly increasing, as delta_extract_multi writes them.  Same arguments;
+ * workspace: delta_apply_multi_sorted_workspace_bytes(num_tensors).
+ * When the delta holds at least one word in 32 of the tensor list, every
+ * tile of 16384 words of each tensor is read once, patched in LDS with its
+ * slice of the delta and written back whole (a delta that dense touches
+ * nearly every 64-byte line, and a line written whole costs less than a
+ * partially written one); below that density it scatters as
+ * delta_apply_multi does.  Entries outside the tensor list set the flag and
+ * are skipped; input out of order gives an unspecified result (no access
+ * leaves the tensors) and may set the flag.
+ */
+delta_status_t delta_apply_multi_sorted(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                        int32_t num_tensors, const int64_t* idx,
+                                        const uint16_t* val, uint64_t count,
+                                        uint32_t* d_error_flag, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
 /*
  * delta_apply_checked — Sec. 5.2: a delta is activated only on top of the
  * version it was made against.  Returns DELTA_ERR_VERSION without touching

@@ -437,23 +437,33 @@ def delta_apply_checked(weights: torch.Tensor, idx: torch.Tensor, val: torch.Ten
         int(base_version), _stream(stream)))
 
 
+def delta_apply_multi_sorted_workspace_bytes(num_tensors: int) -> int:
+    return int(library().delta_apply_multi_sorted_workspace_bytes(int(num_tensors)))
+
+
 def delta_apply_multi(weights: Sequence[torch.Tensor], idx: torch.Tensor, val: torch.Tensor,
                       error_flag: Optional[torch.Tensor] = None, check: bool = False,
                       workspace: Optional[torch.Tensor] = None,
-                      stream: Optional[torch.cuda.Stream] = None) -> None:
-    """Scatter global int64 indices into a tensor list in place."""
+                      stream: Optional[torch.cuda.Stream] = None,
+                      sorted_indices: bool = False) -> None:
+    """Scatter global int64 indices into a tensor list in place.  With
+    ``sorted_indices`` (strictly increasing indices, as the extract writes
+    them) it calls ``delta_apply_multi_sorted``, which merges dense deltas
+    tile by tile instead of scattering them."""
     if idx.dtype != torch.int64:
         raise TypeError("multi-tensor indices are int64")
     T = len(weights)
     ptrs = _ptr_array([_words(w, f"weights[{i}]") for i, w in enumerate(weights)])
     numels = _u64_array([w.numel() for w in weights])
     dev = weights[0].device if T else idx.device
-    need = delta_apply_multi_workspace_bytes(T)
+    need = (delta_apply_multi_sorted_workspace_bytes(T) if sorted_indices
+            else delta_apply_multi_workspace_bytes(T))
     ws = workspace if workspace is not None else _workspace(need, dev)
     flag = error_flag
     if check and flag is None:
         flag = torch.zeros(1, dtype=torch.int32, device=dev)
-    _check(library().delta_apply_multi(
+    entry = library().delta_apply_multi_sorted if sorted_indices else library().delta_apply_multi
+    _check(entry(
         ptrs, numels, T, idx.data_ptr(), _words(val, "val"), idx.numel(),
         flag.data_ptr() if flag is not None else None, ws.data_ptr(),
         ws.numel() * ws.element_size(),

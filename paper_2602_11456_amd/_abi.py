@@ -78,6 +78,7 @@ SIGNATURES = {
     "delta_extract_workspace_bytes": (SZ, [U64]),
     "delta_extract_multi_workspace_bytes": (SZ, [P, I32]),
     "delta_apply_multi_workspace_bytes": (SZ, [I32]),
+    "delta_apply_multi_sorted_workspace_bytes": (SZ, [I32]),
     "delta_extract": (STATUS, [P, P, U64, ctypes.c_int, P, P, U64, P, P, SZ, P]),
     "delta_extract_noalloc": (STATUS, [P, P, U64, ctypes.c_int, P, P, U64, P, P]),
     "delta_extract_multi": (STATUS, [P, P, P, I32, P, P, U64, P, P, P, SZ, P]),
@@ -94,6 +95,7 @@ SIGNATURES = {
                                             P]),
     "delta_apply": (STATUS, [P, U64, ctypes.c_int, P, P, U64, P, P]),
     "delta_apply_multi": (STATUS, [P, P, I32, P, P, U64, P, P, SZ, P]),
+    "delta_apply_multi_sorted": (STATUS, [P, P, I32, P, P, U64, P, P, SZ, P]),
     "delta_apply_checked": (STATUS, [P, U64, ctypes.c_int, P, P, U64, P, U64, U64, P]),
     "delta_leb128_encode_workspace_bytes": (SZ, [U64]),
     "delta_leb128_decode_workspace_bytes": (SZ, [U64, U64, ctypes.c_uint32]),

@@ -282,6 +282,11 @@ size_t delta_apply_multi_workspace_bytes(int32_t num_tensors) {
   return align_up(8 * ((size_t)num_tensors + 1)) + align_up(8 * (size_t)num_tensors);
 }
 
+size_t delta_apply_multi_sorted_workspace_bytes(int32_t num_tensors) {
+  if (num_tensors < 0) return 0;
+  return delta_apply_multi_workspace_bytes(num_tensors) + align_up(8 * ((size_t)num_tensors + 1));
+}
+
 }  // extern "C"
 
 // Argument checks of delta_extract and delta_extract_noalloc (no HIP call).
@@ -764,6 +769,42 @@ delta_status_t delta_apply_multi(uint16_t* const* weight_ptrs, const uint64_t* n
   e = launch_apply_multi(d_bases, (uint16_t* const*)d_ptrs, (uint32_t)num_tensors, idx, val,
                          count, d_error_flag, stream);
   if (e != hipSuccess) return hip_fail(e, "apply_multi launch");
+  return ok();
+}
+
+delta_status_t delta_apply_multi_sorted(uint16_t* const* weight_ptrs, const uint64_t* numels,
+                                        int32_t num_tensors, const int64_t* idx,
+                                        const uint16_t* val, uint64_t count,
+                                        uint32_t* d_error_flag, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  std::vector<uint64_t> bases, ptrs;
+  delta_status_t s = weight_table(weight_ptrs, numels, num_tensors, bases, ptrs);
+  if (s != DELTA_OK) return s;
+  if (count > 0 && (!idx || !val)) return fail(DELTA_ERR_INVALID_ARG, "idx/val is NULL");
+  if (odd(val) || ((uintptr_t)idx % 8)) return fail(DELTA_ERR_INVALID_ARG, "idx/val misaligned");
+  s = check_workspace(workspace, workspace_bytes,
+                      delta_apply_multi_sorted_workspace_bytes(num_tensors));
+  if (s != DELTA_OK) return s;
+  if (count == 0) return ok();
+  char* ws = (char*)workspace;
+  uint64_t *d_bases, *d_ptrs;
+  hipError_t e = upload_weight_table(bases, ptrs, ws, d_bases, d_ptrs, stream);
+  if (e != hipSuccess) return hip_fail(e, "table upload launch");
+  const uint32_t T = (uint32_t)num_tensors;
+  std::vector<uint64_t> tile_first(T + 1);
+  const uint64_t tiles = merge_tiles(numels, T, tile_first.data());
+  if (tiles == 0 || !merge_pays(count, bases[T]) || tiles > 0xFFFFFFFFull) {
+    e = launch_apply_multi(d_bases, (uint16_t* const*)d_ptrs, T, idx, val, count, d_error_flag,
+                           stream);
+    if (e != hipSuccess) return hip_fail(e, "apply_multi launch");
+    return ok();
+  }
+  uint64_t* d_tile_first = (uint64_t*)(ws + delta_apply_multi_workspace_bytes(num_tensors));
+  e = launch_upload_words(tile_first.data(), tile_first.size(), d_tile_first, stream);
+  if (e != hipSuccess) return hip_fail(e, "tile table upload launch");
+  e = launch_apply_merge(d_bases, (uint16_t* const*)d_ptrs, d_tile_first, T, tiles, idx, val,
+                         count, d_error_flag, stream);
+  if (e != hipSuccess) return hip_fail(e, "apply_merge launch");
   return ok();
 }
 

@@ -254,6 +254,144 @@ hipError_t launch_apply_chain(const ChainArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+
+// ------------------------------------------- dense deltas: tiles merged
+//
+// For a delta in increasing index order that touches most 64-byte lines of
+// the weights (from about 1 word in 32), scattered 2-byte stores cost one
+// partial-line write each, which the memory serves as a read-modify-write.
+// Here every workgroup takes one tile of kMergeTile words of one tensor:
+// it reads the tile (16-byte loads), finds the tile's slice of the delta
+// (two 64-wide searches over the sorted indices, issued beside the tile's
+// loads), patches the slice into the tile in LDS and writes the tile back
+// whole.  Each word of the weights is read and written once, in full lines.
+
+constexpr int kMergeTile = 16384;                      // words per tile
+constexpr int kMergeVec = kMergeTile / 8 / kApplyThreads;   // 16-byte vectors per thread
+constexpr int kMergeLoads = 4;                         // slice entries per thread in flight
+
+typedef uint32_t mg_u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) mg_u32x4 mg_gv4;
+
+// First position p in [lo, hi) of the sorted x with x[p] >= target (hi if
+// none), by one wavefront: each round probes 64 evenly spaced positions.
+__device__ __forceinline__ uint64_t wave_lower_bound(const int64_t* x, uint64_t lo, uint64_t hi,
+                                                     int64_t target) {
+  const uint32_t lane = threadIdx.x & 63;
+  const auto g = gview(x);
+  while (hi - lo > 64) {
+    const uint64_t span = hi - lo;
+    const uint64_t p = lo + span / 65 * (lane + 1) + span % 65 * (lane + 1) / 65;
+    const uint32_t c = (uint32_t)__builtin_popcountll(__ballot(g[p] < target));
+    const uint64_t nlo = c ? (uint64_t)__shfl((long long)p, (int)c - 1) + 1 : lo;
+    const uint64_t nhi = c < 64 ? (uint64_t)__shfl((long long)p, (int)(c < 64 ? c : 63)) : hi;
+    lo = nlo;
+    hi = nhi;
+  }
+  const uint64_t p = lo + lane;
+  const bool less = p < hi && g[p] < target;
+  return lo + (uint64_t)__builtin_popcountll(__ballot(less));
+}
+
+// tile_first[t]: first tile of tensor t (tile_first[T] = all tiles).
+struct MergeArgs {
+  const uint64_t* bases;
+  uint16_t* const* ptrs;
+  const uint64_t* tile_first;
+  uint32_t T;
+  uint64_t tiles;
+  const int64_t* idx;
+  const uint16_t* val;
+  uint64_t count;
+  uint32_t* err;
+};
+
+__global__ __launch_bounds__(kApplyThreads) void apply_merge_kernel(MergeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t s_w[kMergeTile];
+  __shared__ uint64_t s_r[2];
+  __shared__ uint32_t s_t;
+  const uint64_t b = blockIdx.x;
+  const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (wave == 0) {
+    // the tensor of tile b: the last t with tile_first[t] <= b (tiles of
+    // an empty tensor start where the next tensor's do, so no later t
+    // qualifies).  Lane l probes lo + floor(n l / 64): lane 0 probes lo,
+    // which always qualifies, and with n <= 64 every candidate is probed.
+    uint32_t lo = 0, hi = a.T;   // tile_first[lo] <= b; the answer is in [lo, hi)
+    while (hi - lo > 1) {
+      const uint32_t n = hi - lo;
+      const uint32_t p = lo + (uint32_t)(((uint64_t)n * lane) >> 6);
+      const uint64_t m = __ballot(a.tile_first[p] <= b);   // a prefix of the lanes
+      const uint32_t c = 63 - (uint32_t)__builtin_clzll(m);
+      const uint32_t last = (uint32_t)__shfl((int)p, (int)c);
+      const uint32_t next = (uint32_t)__shfl((int)p, (int)(c < 63 ? c + 1 : 63));
+      lo = last;
+      if (c < 63) hi = next;
+    }
+    if (lane == 0) s_t = lo;
+  }
+  __syncthreads();
+  const uint32_t t = s_t;
+  const uint64_t lo_w = (b - a.tile_first[t]) * kMergeTile;
+  const uint64_t n_t = a.bases[t + 1] - a.bases[t];
+  const uint64_t len = n_t - lo_w < (uint64_t)kMergeTile ? n_t - lo_w : kMergeTile;
+  const uint64_t g0 = a.bases[t] + lo_w;
+  uint16_t* w = a.ptrs[t] + lo_w;
+  const bool vec = len == (uint64_t)kMergeTile && ((uintptr_t)w & 15) == 0;
+  mg_u32x4 x[kMergeVec];
+  if (vec) {
+#pragma unroll
+    for (int j = 0; j < kMergeVec; ++j)
+      x[j] = __builtin_nontemporal_load((const mg_gv4*)w + threadIdx.x + kApplyThreads * j);
+  }
+  if (wave < 2) {
+    const uint64_t r = wave_lower_bound(a.idx, 0, a.count, (int64_t)(g0 + (wave ? len : 0)));
+    if (lane == 0) s_r[wave] = r;
+  }
+  if (vec) {
+#pragma unroll
+    for (int j = 0; j < kMergeVec; ++j) ((mg_u32x4*)s_w)[threadIdx.x + kApplyThreads * j] = x[j];
+  } else {
+    for (uint32_t i = threadIdx.x; i < (uint32_t)len; i += kApplyThreads)
+      s_w[i] = gview((const uint16_t*)w)[i];
+  }
+  __syncthreads();
+  const uint64_t e0 = s_r[0], e1 = s_r[1];
+  bool bad = false;
+  // entries below the first word or past the last of the tensor list
+  if (threadIdx.x == 0 && ((b == 0 && e0 > 0) || (b + 1 == a.tiles && e1 < a.count))) bad = true;
+  for (uint64_t e = e0 + threadIdx.x; e < e1; e += kApplyThreads * kMergeLoads) {
+    int64_t i[kMergeLoads];
+    uint16_t v[kMergeLoads];
+#pragma unroll
+    for (int u = 0; u < kMergeLoads; ++u) {
+      const uint64_t k = e + kApplyThreads * u;
+      i[u] = k < e1 ? gview(a.idx)[k] : 0;
+      v[u] = k < e1 ? gview(a.val)[k] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kMergeLoads; ++u) {
+      if (e + kApplyThreads * u >= e1) continue;
+      const uint64_t o = (uint64_t)i[u] - g0;
+      if (o < len)
+        s_w[o] = v[u];
+      else
+        bad = true;   // only out-of-order input puts an entry outside its tile
+    }
+  }
+  __syncthreads();
+  if (vec) {
+#pragma unroll
+    for (int j = 0; j < kMergeVec; ++j)
+      __builtin_nontemporal_store(((mg_u32x4*)s_w)[threadIdx.x + kApplyThreads * j],
+                                  (mg_gv4*)w + threadIdx.x + kApplyThreads * j);
+  } else {
+    for (uint32_t i = threadIdx.x; i < (uint32_t)len; i += kApplyThreads)
+      ((__attribute__((address_space(1))) uint16_t*)w)[i] = s_w[i];
+  }
+  if (bad) flag_error(a.err);
+}
+
 static uint32_t apply_blocks(uint64_t count) {
   const uint64_t per_block = (uint64_t)kApplyWaves * kApplyPerWave;
   uint64_t blocks = (count + per_block - 1) / per_block;
@@ -281,6 +419,30 @@ hipError_t launch_apply_multi(const uint64_t* bases, uint16_t* const* ptrs, uint
   if (count == 0) return hipSuccess;
   hipLaunchKernelGGL(apply_multi_kernel, dim3(apply_blocks(count)), dim3(kApplyThreads), 0, stream,
                      bases, ptrs, T, idx, val, count, err);
+  return hipGetLastError();
+}
+
+
+uint64_t merge_tiles(const uint64_t* numels, uint32_t T, uint64_t* tile_first) {
+  uint64_t tiles = 0;
+  for (uint32_t t = 0; t < T; ++t) {
+    if (tile_first) tile_first[t] = tiles;
+    tiles += (numels[t] + kMergeTile - 1) / kMergeTile;
+  }
+  if (tile_first) tile_first[T] = tiles;
+  return tiles;
+}
+
+bool merge_pays(uint64_t count, uint64_t words) { return count > 0 && count >= words / 32; }
+
+hipError_t launch_apply_merge(const uint64_t* bases, uint16_t* const* ptrs,
+                              const uint64_t* tile_first, uint32_t T, uint64_t tiles,
+                              const int64_t* idx, const uint16_t* val, uint64_t count,
+                              uint32_t* err, hipStream_t stream) {
+  if (tiles == 0) return hipSuccess;
+  MergeArgs a{bases, ptrs, tile_first, T, tiles, idx, val, count, err};
+  hipLaunchKernelGGL(apply_merge_kernel, dim3((uint32_t)tiles), dim3(kApplyThreads), 0, stream,
+                     a);
   return hipGetLastError();
 }
 

@@ -233,6 +233,16 @@ hipError_t launch_apply(uint16_t* w, uint64_t n, bool idx64, const void* idx,
 hipError_t launch_apply_multi(const uint64_t* bases, uint16_t* const* ptrs, uint32_t T,
                               const int64_t* idx, const uint16_t* val, uint64_t count,
                               uint32_t* err, hipStream_t stream);
+// The tile-merge apply of a sorted delta (apply.hip): merge_tiles gives the
+// number of tiles over the tensors and, when tile_first is not NULL, each
+// tensor's first tile (T + 1 entries); merge_pays says whether a delta of
+// `count` entries over `words` words is dense enough for it.
+uint64_t merge_tiles(const uint64_t* numels, uint32_t T, uint64_t* tile_first);
+bool merge_pays(uint64_t count, uint64_t words);
+hipError_t launch_apply_merge(const uint64_t* bases, uint16_t* const* ptrs,
+                              const uint64_t* tile_first, uint32_t T, uint64_t tiles,
+                              const int64_t* idx, const uint16_t* val, uint64_t count,
+                              uint32_t* err, hipStream_t stream);
 
 // Catch-up in one pass (delta_apply_chain): the chain's deltas, oldest
 // first, in a device table; tiles of `per_tile` entries of the reference

@@ -279,6 +279,22 @@ def test_apply_validation(lib):
     numels = (ctypes.c_uint64 * 1)(10)
     assert lib.delta_apply_multi(ws, numels, 1, FAKE, FAKE, 5, None, FAKE, 1 << 20, None) == \
         _abi.DELTA_ERR_INVALID_ARG
+    # the sorted form checks the same arguments and its own workspace size
+    F = lib.delta_apply_multi_sorted
+    need = lib.delta_apply_multi_sorted_workspace_bytes(1)
+    assert need > lib.delta_apply_multi_workspace_bytes(1)
+    assert lib.delta_apply_multi_sorted_workspace_bytes(-1) == 0
+    assert F(ws, numels, 1, FAKE, FAKE, 5, None, FAKE, 1 << 20, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # tensor 0 has words but no pointer
+    good = (P * 1)(FAKE)
+    assert F(good, numels, 1, None, FAKE, 5, None, FAKE, need, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # NULL idx
+    assert F(good, numels, 1, FAKE + 4, FAKE, 5, None, FAKE, need, None) == \
+        _abi.DELTA_ERR_INVALID_ARG   # idx not 8-byte aligned
+    assert F(good, numels, 1, FAKE, FAKE, 5, None, FAKE, need - 1, None) == \
+        _abi.DELTA_ERR_WORKSPACE
+    assert F(good, numels, -1, FAKE, FAKE, 5, None, FAKE, need, None) == \
+        _abi.DELTA_ERR_INVALID_ARG
 
 
 def test_pipeline_validation(lib):

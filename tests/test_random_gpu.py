@@ -16,8 +16,9 @@ or clustered runs.  On the same bytes it then checks, entry by entry:
   every segment's byte offset;
 - the device encoder on the extracted indices (the same bytes) and the
   device decoder (the same indices);
-- delta_apply_multi and the decode-in-apply onto copies of the previous
-  words, against the new words;
+- delta_apply_multi, its sorted form (tiles merged when the delta is
+  dense) and the decode-in-apply onto copies of the previous words, against
+  the new words;
 - a truncated extract (capacity below the count): the first entries and
   the true count.
 
@@ -179,6 +180,9 @@ def test_random_case(seed):
 
     rollout = [p.clone() for p in dp]
     ad.delta_apply_multi(rollout, idx, val, check=True)
+    same_words(rollout, hn)
+    rollout = [p.clone() for p in dp]
+    ad.delta_apply_multi(rollout, idx, val, check=True, sorted_indices=True)
     same_words(rollout, hn)
     rollout = [p.clone() for p in dp]
     ad.delta_apply_leb128_multi(rollout, code, coffs, None, cval, check=True)
