@@ -552,6 +552,35 @@ def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
     tr = med([e[2].elapsed_time(e[3]) for e in ev])
     tch = med([e[3].elapsed_time(e[4]) for e in ev])
     moved = (sum(counts) + k) * 10   # every input entry read once, the result written once
+    # longer chains: the one-pass catch-up (merged tile by tile once the
+    # chain holds one word in 24) against replaying it delta by delta
+    longer = {}
+    for K2 in (8, 16):
+        while len(deltas) < K2:
+            idx = torch.unique(torch.randint(0, N, (K_entries,), device=dev, generator=g))
+            val = torch.randint(-32768, 32767, (idx.numel(),), device=dev, generator=g,
+                                dtype=torch.int16).view(torch.bfloat16)
+            deltas.append((idx, val))
+        ch = deltas[:K2]
+        cws = torch.empty(ad.delta_apply_chain_workspace_bytes([i.numel() for i, _ in ch],
+                                                               len(rollout)),
+                          dtype=torch.uint8, device=dev)
+        ad.delta_apply_chain(rollout, ch, workspace=cws, stream=stream)
+        tl = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(3)]
+        for e0, e1, e2 in tl:
+            e0.record(stream)
+            ad.delta_apply_chain(rollout, ch, workspace=cws, stream=stream)
+            e1.record(stream)
+            for idx, val in ch:
+                ad.delta_apply_multi(rollout, idx, val, workspace=apply_ws, stream=stream)
+            e2.record(stream)
+        stream.synchronize()
+        longer[str(K2)] = {
+            "entries": sum(i.numel() for i, _ in ch),
+            "catch_up_one_pass_ms": round(med([e[0].elapsed_time(e[1]) for e in tl]), 4),
+            "replay_chain_ms": round(med([e[1].elapsed_time(e[2]) for e in tl]), 4),
+        }
+        del cws
     return {
         "workload": f"{chain} deltas of ~1% random positions of the {N}-word index space "
                     f"({sum(counts)} entries), composed into {k}",
@@ -562,6 +591,7 @@ def compose_measurement(ad, rollout, N, K_entries, stream, reps, chain=4):
         "replay_chain_ms": round(tr, 4),
         "catch_up_compose_plus_apply_ms": round(tc + ta, 4),
         "catch_up_one_pass_ms": round(tch, 4),
+        "longer_chains": longer,
     }
 
 

@@ -537,8 +537,12 @@ size_t delta_apply_chain_workspace_bytes(const uint64_t* counts, int32_t num_del
  *                 access leaves the given buffers).
  *   workspace     delta_apply_chain_workspace_bytes(counts, num_deltas,
  *                 num_tensors).
- * Enqueues on `stream`.  The index space is cut into value ranges holding a
- * fixed number of entries of the largest delta; deltas of very uneven
+ * Enqueues on `stream`.  A chain whose entries together hold at least one
+ * word in 24 of the tensor list is merged tile by tile: every tile of 16384
+ * words is read once, the deltas' words for it are patched in oldest first
+ * and the tile is written back whole.  A sparser chain is cut into value
+ * ranges holding a fixed number of entries of the largest delta, each
+ * merged in LDS and its newest words scattered; deltas of very uneven
  * density stay correct but slower.
  */
 delta_status_t delta_apply_chain(uint16_t* const* weight_ptrs, const uint64_t* numels,

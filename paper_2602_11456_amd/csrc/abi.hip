@@ -813,7 +813,7 @@ delta_status_t delta_apply_multi_sorted(uint16_t* const* weight_ptrs, const uint
 struct ChainPlan {
   uint32_t ref;
   uint64_t per_tile, tiles;
-  size_t deltas, pos, total;   // workspace offsets after the weight table
+  size_t deltas, pos, tile_first, total;   // workspace offsets after the weight table
 };
 
 static ChainPlan chain_plan(const uint64_t* counts, int32_t K, int32_t T) {
@@ -827,7 +827,8 @@ static ChainPlan chain_plan(const uint64_t* counts, int32_t K, int32_t T) {
   c.tiles = (n_ref + c.per_tile - 1) / c.per_tile;
   c.deltas = delta_apply_multi_workspace_bytes(T);
   c.pos = align_up(c.deltas + sizeof(ChainDelta) * (size_t)(K > 0 ? K : 1));
-  c.total = align_up(c.pos + 8 * (c.tiles + 1) * (uint64_t)(K > 0 ? K : 1));
+  c.tile_first = align_up(c.pos + 8 * (c.tiles + 1) * (uint64_t)(K > 0 ? K : 1));
+  c.total = align_up(c.tile_first + 8 * ((size_t)(T > 0 ? T : 0) + 1));
   return c;
 }
 
@@ -876,9 +877,24 @@ delta_status_t delta_apply_chain(uint16_t* const* weight_ptrs, const uint64_t* n
     if (e != hipSuccess) return hip_fail(e, "apply_multi launch");
     return ok();
   }
-  if (c.tiles > 0xFFFFFFFFull) return fail(DELTA_ERR_INVALID_ARG, "too many entries");
   e = launch_upload_words(table.data(), table.size(), (uint64_t*)(ws + c.deltas), stream);
   if (e != hipSuccess) return hip_fail(e, "delta table upload launch");
+  // a chain dense enough (all its entries together at least one word in
+  // 24): the tile merge of every delta, every word read and written once
+  const uint32_t T = (uint32_t)num_tensors;
+  std::vector<uint64_t> tile_first(T + 1);
+  const uint64_t mtiles = merge_tiles(numels, T, tile_first.data());
+  if (mtiles > 0 && chain_merge_pays(entries, bases[T]) && mtiles <= 0xFFFFFFFFull) {
+    uint64_t* d_tile_first = (uint64_t*)(ws + c.tile_first);
+    e = launch_upload_words(tile_first.data(), tile_first.size(), d_tile_first, stream);
+    if (e != hipSuccess) return hip_fail(e, "tile table upload launch");
+    e = launch_apply_runs(d_bases, (uint16_t* const*)d_ptrs, d_tile_first, T, mtiles,
+                          (const ChainDelta*)(ws + c.deltas), (uint32_t)num_deltas, entries,
+                          bases[T], d_error_flag, stream);
+    if (e != hipSuccess) return hip_fail(e, "apply_runs launch");
+    return ok();
+  }
+  if (c.tiles > 0xFFFFFFFFull) return fail(DELTA_ERR_INVALID_ARG, "too many entries");
   ChainArgs a;
   memset(&a, 0, sizeof(a));
   a.r.deltas = (const ChainDelta*)(ws + c.deltas);

@@ -392,6 +392,228 @@ __global__ __launch_bounds__(kApplyThreads) void apply_merge_kernel(MergeArgs a)
   if (bad) flag_error(a.err);
 }
 
+
+// ------------------------------------ dense chains: runs of tiles merged
+//
+// A chain D_1..D_K (oldest first, each strictly increasing) whose entries
+// together hold at least one word in 32 of the tensor list: each workgroup
+// walks a run of kRunTiles consecutive tiles with one cursor per delta
+// (each found once, by a 64-wide search, at the run's first tile).  For a
+// tile it loads the tile's words and, beside them, the next chunk of the
+// first deltas (L entries per thread per delta, kRunSlots per thread: with
+// more than kRunSlots / L deltas the rest follow in batches); then it
+// patches the deltas into the tile in LDS oldest first (a
+// barrier between deltas, so of equal indices the newest word stays),
+// loading further chunks of a delta while its entries still fall in the
+// tile, moves every cursor past the entries the tile took, and writes the
+// tile back whole.  With K = 1 it is the tile merge of one sorted delta
+// without per-tile searches.
+
+constexpr int kRunTiles = 32;   // tiles per workgroup
+constexpr int kRunSlots = 8;    // delta entries per thread per batch of deltas
+
+struct RunArgs {
+  const uint64_t* bases;
+  uint16_t* const* ptrs;
+  const uint64_t* tile_first;
+  uint32_t T;
+  uint64_t tiles;
+  const ChainDelta* deltas;   // device [K]
+  uint32_t K;
+  uint32_t lg;                // chunk loads per thread per delta: L = 2^lg <= kRunSlots
+  uint32_t* err;
+};
+
+// A value every lane of the wavefront holds alike, in scalar registers.
+__device__ __forceinline__ uint64_t run_uniform(uint64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Block-wide maximum of v (every thread gets it); one barrier.  Two calls
+// in a row must pass different buffers: a wavefront reads the buffer after
+// the barrier, and only the next call's barrier orders that read before
+// the buffer is written again.
+__device__ __forceinline__ uint32_t run_block_max(uint32_t v, uint32_t* s_red) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const uint32_t y = __shfl_xor(v, o);
+    v = y > v ? y : v;
+  }
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint32_t m = 0;
+#pragma unroll
+  for (int w = 0; w < kApplyThreads / 64; ++w) m = s_red[w] > m ? s_red[w] : m;
+  return m;
+}
+
+__global__ __launch_bounds__(kApplyThreads) void apply_runs_kernel(RunArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t s_w[kMergeTile];
+  __shared__ ChainDelta s_d[kChainMaxDeltas];
+  __shared__ uint64_t s_cur[kChainMaxDeltas];
+  __shared__ uint32_t s_red[2][kApplyThreads / 64];
+  __shared__ uint32_t s_t;
+  const uint32_t K = a.K, lg = a.lg, L = 1u << lg, chunk = kApplyThreads * L;
+  const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const uint64_t b0 = (uint64_t)blockIdx.x * kRunTiles;
+  const uint64_t b1 = b0 + kRunTiles < a.tiles ? b0 + kRunTiles : a.tiles;
+  bool bad = false;
+  if (threadIdx.x < K) s_d[threadIdx.x] = a.deltas[threadIdx.x];
+  if (wave == 0) {   // the tensor of tile b0, as in apply_merge_kernel
+    uint32_t lo = 0, hi = a.T;
+    while (hi - lo > 1) {
+      const uint32_t n = hi - lo;
+      const uint32_t p = lo + (uint32_t)(((uint64_t)n * lane) >> 6);
+      const uint64_t m = __ballot(a.tile_first[p] <= b0);
+      const uint32_t c = 63 - (uint32_t)__builtin_clzll(m);
+      const uint32_t last = (uint32_t)__shfl((int)p, (int)c);
+      const uint32_t next = (uint32_t)__shfl((int)p, (int)(c < 63 ? c + 1 : 63));
+      lo = last;
+      if (c < 63) hi = next;
+    }
+    if (lane == 0) s_t = lo;
+  }
+  __syncthreads();
+  uint32_t t = s_t;
+  {
+    // every delta's cursor at the run's first word: wavefront w searches
+    // deltas w, w + 4, ...
+    const uint64_t g_first = a.bases[t] + (b0 - a.tile_first[t]) * kMergeTile;
+    for (uint32_t k = wave; k < K; k += kApplyThreads / 64) {
+      const uint64_t c = wave_lower_bound(s_d[k].idx, 0, s_d[k].n, (int64_t)g_first);
+      if (lane == 0) s_cur[k] = c;
+    }
+  }
+  __syncthreads();
+  if (b0 == 0 && threadIdx.x < K && s_cur[threadIdx.x] > 0) bad = true;   // entries below word 0
+  for (uint64_t b = b0; b < b1; ++b) {
+    while (t + 1 < a.T && a.tile_first[t + 1] <= b) ++t;   // uniform
+    const uint64_t lo_w = (b - a.tile_first[t]) * kMergeTile;
+    const uint64_t n_t = a.bases[t + 1] - a.bases[t];
+    const uint64_t len = n_t - lo_w < (uint64_t)kMergeTile ? n_t - lo_w : kMergeTile;
+    const uint64_t g0 = a.bases[t] + lo_w;
+    const int64_t g_end = (int64_t)(g0 + len);
+    uint16_t* w = a.ptrs[t] + lo_w;
+    const bool vec = len == (uint64_t)kMergeTile && ((uintptr_t)w & 15) == 0;
+    mg_u32x4 x[kMergeVec];
+    if (vec) {
+#pragma unroll
+      for (int j = 0; j < kMergeVec; ++j)
+        x[j] = __builtin_nontemporal_load((const mg_gv4*)w + threadIdx.x + kApplyThreads * j);
+    }
+    // The deltas go in batches of at most kRunSlots >> lg: slot s of a batch
+    // starting at delta d0 holds entry cur_k + thread + 256 j of delta
+    // k = d0 + (s >> lg), j = s & (L - 1).  The first batch's chunks load
+    // beside the tile's words.
+    int64_t ei[kRunSlots];
+    uint16_t ev[kRunSlots];
+    const uint32_t per_batch = kRunSlots >> lg;
+    const auto load_batch = [&](uint32_t d0) {
+#pragma unroll
+      for (int s = 0; s < kRunSlots; ++s) {
+        const uint32_t k = d0 + ((uint32_t)s >> lg), j = (uint32_t)s & (L - 1);
+        ei[s] = INT64_MAX;
+        ev[s] = 0;
+        if (k < K && k < d0 + per_batch) {
+          const uint64_t cur = run_uniform(s_cur[k]), n = run_uniform(s_d[k].n);
+          const int64_t* xi = (const int64_t*)run_uniform((uint64_t)(uintptr_t)s_d[k].idx);
+          const uint16_t* xv = (const uint16_t*)run_uniform((uint64_t)(uintptr_t)s_d[k].val);
+          const uint64_t e = cur + threadIdx.x + (uint64_t)kApplyThreads * j;
+          if (e < n) {
+            ei[s] = gview(xi)[e];
+            ev[s] = gview(xv)[e];
+          }
+        }
+      }
+    };
+    load_batch(0);
+    if (vec) {
+#pragma unroll
+      for (int j = 0; j < kMergeVec; ++j) ((mg_u32x4*)s_w)[threadIdx.x + kApplyThreads * j] = x[j];
+    } else {
+      for (uint32_t i = threadIdx.x; i < (uint32_t)len; i += kApplyThreads)
+        s_w[i] = gview((const uint16_t*)w)[i];
+    }
+    __syncthreads();
+    uint32_t red = 0;   // reductions so far: consecutive ones use different buffers
+    for (uint32_t d0 = 0; d0 < K; d0 += per_batch) {
+      // a later batch: every cursor it reads was published by the barrier
+      // of the previous batch's last reduction
+      if (d0 > 0) load_batch(d0);
+      const uint32_t d1 = d0 + per_batch < K ? d0 + per_batch : K;
+      for (uint32_t k = d0; k < d1; ++k) {
+        // read before the barrier below, after which thread 0 may move it
+        uint64_t cur = run_uniform(s_cur[k]);
+        const uint64_t n = run_uniform(s_d[k].n);
+        const int64_t* xi = (const int64_t*)run_uniform((uint64_t)(uintptr_t)s_d[k].idx);
+        const uint16_t* xv = (const uint16_t*)run_uniform((uint64_t)(uintptr_t)s_d[k].val);
+        // this thread's entries of delta k that fall in the tile; the tile
+        // takes a prefix of the chunk (sorted input), m = its length
+        uint32_t m = 0;
+#pragma unroll
+        for (int s = 0; s < kRunSlots; ++s) {
+          if (d0 + ((uint32_t)s >> lg) != k) continue;
+          const uint32_t j = (uint32_t)s & (L - 1);
+          // strictly increasing (checked between neighbouring lanes)
+          const int64_t nx = __shfl_down(ei[s], 1);
+          if (lane != 63 && nx != INT64_MAX && ei[s] != INT64_MAX && nx <= ei[s]) bad = true;
+          if (ei[s] < g_end) {
+            const uint64_t o = (uint64_t)ei[s] - g0;
+            if (o < len)
+              s_w[o] = ev[s];
+            else
+              bad = true;   // below the tile: only unsorted input
+            const uint32_t pos = threadIdx.x + kApplyThreads * j + 1;
+            m = pos > m ? pos : m;
+          }
+        }
+        m = run_block_max(m, s_red[red++ & 1]);
+        // a chunk taken whole: the delta may hold more words of this tile
+        while (m == chunk && cur + m < n) {
+          cur += m;
+          m = 0;
+#pragma unroll
+          for (int j = 0; j < kRunSlots; ++j) {
+            if ((uint32_t)j >= L) break;
+            const uint64_t e = cur + threadIdx.x + (uint64_t)kApplyThreads * j;
+            if (e < n) {
+              const int64_t i = gview(xi)[e];
+              if (i < g_end) {
+                const uint64_t o = (uint64_t)i - g0;
+                if (o < len)
+                  s_w[o] = gview(xv)[e];
+                else
+                  bad = true;
+                const uint32_t pos = threadIdx.x + kApplyThreads * j + 1;
+                m = pos > m ? pos : m;
+              }
+            }
+          }
+          m = run_block_max(m, s_red[red++ & 1]);
+        }
+        if (threadIdx.x == 0) s_cur[k] = cur + m;
+      }
+      if (d1 < K) __syncthreads();   // the batch's cursors are published
+    }
+    __syncthreads();   // the tile is complete; s_cur is published
+    if (vec) {
+#pragma unroll
+      for (int j = 0; j < kMergeVec; ++j)
+        __builtin_nontemporal_store(((mg_u32x4*)s_w)[threadIdx.x + kApplyThreads * j],
+                                    (mg_gv4*)w + threadIdx.x + kApplyThreads * j);
+    } else {
+      for (uint32_t i = threadIdx.x; i < (uint32_t)len; i += kApplyThreads)
+        ((__attribute__((address_space(1))) uint16_t*)w)[i] = s_w[i];
+    }
+    __syncthreads();   // s_w is read before the next tile overwrites it
+  }
+  // entries past the last word
+  if (b1 == a.tiles && threadIdx.x < K && s_cur[threadIdx.x] < s_d[threadIdx.x].n) bad = true;
+  if (bad) flag_error(a.err);
+}
+
 static uint32_t apply_blocks(uint64_t count) {
   const uint64_t per_block = (uint64_t)kApplyWaves * kApplyPerWave;
   uint64_t blocks = (count + per_block - 1) / per_block;
@@ -435,6 +657,10 @@ uint64_t merge_tiles(const uint64_t* numels, uint32_t T, uint64_t* tile_first) {
 
 bool merge_pays(uint64_t count, uint64_t words) { return count > 0 && count >= words / 32; }
 
+bool chain_merge_pays(uint64_t entries, uint64_t words) {
+  return entries > 0 && entries >= words / 24;
+}
+
 hipError_t launch_apply_merge(const uint64_t* bases, uint16_t* const* ptrs,
                               const uint64_t* tile_first, uint32_t T, uint64_t tiles,
                               const int64_t* idx, const uint16_t* val, uint64_t count,
@@ -443,6 +669,24 @@ hipError_t launch_apply_merge(const uint64_t* bases, uint16_t* const* ptrs,
   MergeArgs a{bases, ptrs, tile_first, T, tiles, idx, val, count, err};
   hipLaunchKernelGGL(apply_merge_kernel, dim3((uint32_t)tiles), dim3(kApplyThreads), 0, stream,
                      a);
+  return hipGetLastError();
+}
+
+
+hipError_t launch_apply_runs(const uint64_t* bases, uint16_t* const* ptrs,
+                             const uint64_t* tile_first, uint32_t T, uint64_t tiles,
+                             const ChainDelta* deltas, uint32_t K, uint64_t entries,
+                             uint64_t words, uint32_t* err, hipStream_t stream) {
+  if (tiles == 0 || K == 0) return hipSuccess;
+  // chunk loads per thread per delta: the entries an average tile holds of
+  // the average delta, with room, within the slots
+  const uint64_t per_tile = entries / K * kMergeTile / (words ? words : 1);
+  const uint64_t want = (per_tile * 5 / 4 + kApplyThreads - 1) / kApplyThreads;
+  uint32_t lg = 0;   // the smallest power of two >= want that one batch of all deltas allows
+  while ((1ull << lg) < want && (K << (lg + 1)) <= (uint32_t)kRunSlots) ++lg;
+  RunArgs a{bases, ptrs, tile_first, T, tiles, deltas, K, lg, err};
+  const uint64_t runs = (tiles + kRunTiles - 1) / kRunTiles;
+  hipLaunchKernelGGL(apply_runs_kernel, dim3((uint32_t)runs), dim3(kApplyThreads), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -273,6 +273,17 @@ struct ChainArgs {
   uint32_t* err;
 };
 hipError_t launch_apply_chain(const ChainArgs& a, hipStream_t stream);
+// The tile merge of a chain of K (<= kChainMaxDeltas) sorted deltas
+// (apply.hip): `entries` in all over `words` words; tiles and tile_first as
+// for launch_apply_merge.  chain_merge_pays says whether a chain is dense
+// enough for it (from one entry per 24 words; the single-delta merge pays
+// from one in 32, as the chain's other path costs more per entry than the
+// plain scatter but its merge more per tile).
+hipError_t launch_apply_runs(const uint64_t* bases, uint16_t* const* ptrs,
+                             const uint64_t* tile_first, uint32_t T, uint64_t tiles,
+                             const ChainDelta* deltas, uint32_t K, uint64_t entries,
+                             uint64_t words, uint32_t* err, hipStream_t stream);
+bool chain_merge_pays(uint64_t entries, uint64_t words);
 hipError_t launch_chain_split(const ChainRuns& r, hipStream_t stream);
 
 // One slice of a tensor list for enqueue_extract: `n` words of both copies

@@ -203,6 +203,70 @@ def test_apply_chain_matches_oracle(K, density):
     check_chain(SIZES, deltas, seed=K)
 
 
+def check_chain_views(sizes, offsets, deltas_h, seed=0):
+    """check_chain with some tensors at odd word offsets inside larger buffers
+    (tiles of such tensors go word by word)."""
+    hs, _ = weight_list(sizes, seed)
+    ws = []
+    for h, off in zip(hs, offsets):
+        buf = torch.empty(h.size + off, dtype=torch.int16, device=DEV)
+        t = buf[off:off + h.size]
+        t.copy_(torch.from_numpy(h.view(np.int16)))
+        ws.append(t.view(torch.bfloat16))
+    want = oracle_replay([h.copy() for h in hs], deltas_h)
+    ad.delta_apply_chain(ws, [to_dev(i, v) for i, v in deltas_h], check=True)
+    for t, (w, r) in enumerate(zip(ws, want)):
+        np.testing.assert_array_equal(host_u16(w), r, err_msg=f"tensor {t}")
+
+
+@pytest.mark.parametrize("case", ["batches", "views", "uneven", "dense_small"])
+def test_apply_chain_tile_merge(case):
+    # chains dense enough for the tile merge (entries >= words / 24): more
+    # deltas than one batch of prefetched chunks, tensors at odd offsets and
+    # ragged tiles, one delta far denser than the others (its chunks are
+    # taken whole, so more are loaded for the same tile), many small tensors
+    T16 = 16384
+    if case == "batches":
+        sizes, offs = [3 * T16 + 9, 0, T16, 5, 2 * T16 - 3], None
+        N = sum(sizes)
+        deltas = [rand_delta(N, 0.02, seed=9000 + d) for d in range(13)]
+    elif case == "views":
+        sizes, offs = [2 * T16, T16 + 7, 50_000, 1], [3, 1, 0, 5]
+        N = sum(sizes)
+        deltas = [rand_delta(N, 0.1, seed=9100 + d) for d in range(6)]
+    elif case == "uneven":
+        sizes, offs = [4 * T16, 3 * T16 + 1], None
+        N = sum(sizes)
+        deltas = [rand_delta(N, 0.001, seed=9200), rand_delta(N, 0.95, seed=9201),
+                  rand_delta(N, 0.01, seed=9202)]
+    else:
+        sizes, offs = [int(x) for x in np.random.default_rng(4).integers(0, 3000, 200)], None
+        N = sum(sizes)
+        deltas = [rand_delta(N, 0.03, seed=9300 + d) for d in range(8)]
+    say(f"chain tile merge {case}: {len(deltas)} deltas, "
+        f"{sum(d[0].size for d in deltas)} entries over {N} words")
+    assert 24 * sum(d[0].size for d in deltas) >= N
+    if offs is None:
+        check_chain(sizes, deltas, seed=3)
+    else:
+        check_chain_views(sizes, offs, deltas, seed=3)
+
+
+def test_apply_chain_tile_merge_flags_out_of_range():
+    sizes = [30_000, 20_000]
+    N = sum(sizes)
+    a = rand_delta(N, 0.1, seed=41)
+    b = rand_delta(N, 0.1, seed=42)
+    bad = (np.concatenate([[-2], b[0], [N, N + 5]]).astype(np.int64),
+           np.concatenate([[1], b[1], [2, 3]]).astype(np.uint16))
+    hs, ws = weight_list(sizes, 5)
+    want = oracle_replay([h.copy() for h in hs], [a, b])
+    with pytest.raises(ad.DeltaError):
+        ad.delta_apply_chain(ws, [to_dev(*a), to_dev(*bad)], check=True)
+    for w, r in zip(ws, want):   # the entries inside the tensors are applied
+        np.testing.assert_array_equal(host_u16(w), r)
+
+
 def test_apply_chain_edge_cases():
     N = sum(SIZES)
     e = (np.zeros(0, np.int64), np.zeros(0, np.uint16))
