@@ -239,11 +239,22 @@ __device__ __forceinline__ uint32_t rec_last(uint64_t r) { return (uint32_t)((r 
 // kCoded (the coded output of launch_extract_coded): the LDS area holds
 // every entry of the tile, and the tile leaves its record (above) instead
 // of its count; wavefront 0 sums the gaps' code bytes.
+
+// The dispatcher hands workgroup b to XCD b % 8.  With tile b for workgroup
+// b, neighbouring tiles (and the HBM pages they read) go to different XCDs;
+// this order gives XCD x a contiguous eighth of the tiles instead (measured
+// 4.5% faster for the stage kernel on 8.19 G words).  A bijection of
+// [0, tiles).
+__device__ __forceinline__ uint64_t xcd_tile(uint64_t b, uint64_t tiles) {
+  const uint64_t x = b % 8, q = b / 8, per = tiles / 8, rem = tiles % 8;
+  return x * per + (x < rem ? x : rem) + q;
+}
+
 template <bool kMulti, bool kVec, bool kCoded>
 __global__ __launch_bounds__(kThreads) void stage_kernel(ExtractArgs a) {
   __shared__ uint32_t s_wave_total[kWaves];
   __shared__ __attribute__((aligned(16))) uint32_t s_stage[kLdsStage];
-  const uint64_t tile = blockIdx.x;
+  const uint64_t tile = xcd_tile(blockIdx.x, a.num_tiles);
   const uint32_t lane = lane_id();
   const uint32_t wave = threadIdx.x >> 6;
   const TensorDesc d = tile_desc<kMulti>(a, tile);
@@ -303,7 +314,7 @@ constexpr size_t kCountLds = 48 * 1024;
 template <bool kMulti, bool kVec>
 __global__ __launch_bounds__(kThreads) void count_kernel(ExtractArgs a) {
   __shared__ uint32_t s_wave_total[kWaves];
-  const uint64_t tile = blockIdx.x;
+  const uint64_t tile = xcd_tile(blockIdx.x, a.num_tiles);
   const TensorDesc d = tile_desc<kMulti>(a, tile);
   TileScan s;
   scan_tile<kVec>(d, tile, lane_id(), threadIdx.x >> 6, s_wave_total, s);
@@ -449,7 +460,7 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(ExtractArgs a) {
   __shared__ uint32_t s_count[kTilesPerGroup];
   __shared__ int64_t s_out_base[kTilesPerGroup];
   __shared__ uint32_t s_wave_total[kWaves];
-  const uint64_t g = blockIdx.x;
+  const uint64_t g = xcd_tile(blockIdx.x, (a.num_tiles + kTilesPerGroup - 1) / kTilesPerGroup);
   const uint64_t t0 = g * kTilesPerGroup;
   const uint64_t left = a.num_tiles - t0;
   const uint32_t n_here = left < (uint64_t)kTilesPerGroup ? (uint32_t)left : kTilesPerGroup;
