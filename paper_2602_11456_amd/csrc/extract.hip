@@ -454,19 +454,60 @@ __device__ __forceinline__ TensorDesc lane_desc(const ExtractArgs& a, uint64_t t
 
 constexpr int kFinBatch = 8;
 
-template <typename IdxT, bool kMulti, bool kVec>
+// Calls over at most kOwnScanGroups groups (2^28 words: the pipeline's
+// chunks) launch no scan between the stage and finalize kernels: each
+// finalize workgroup sums the tile counts before its own group itself (at
+// most 128 KiB, just written by the stage kernel), and the last group's
+// workgroup writes the total.  A one-workgroup scan is a chain of
+// dependent loads plus a launch; beside a running stage kernel (the
+// pipeline's next chunk) it took 50-90 us per chunk.
+constexpr uint64_t kOwnScanGroups = 512;
+
+// Sum of counts[0, t0) over the workgroup (every thread gets it); t0 is a
+// multiple of kTilesPerGroup and counts 16-byte aligned, so the range is
+// whole 16-byte vectors, loaded eight per thread at a time.
+constexpr int kOwnScanBatch = 8;
+__device__ __forceinline__ uint64_t counts_before_group(const uint32_t* counts, uint64_t t0,
+                                                        uint64_t* s_part) {
+  const u32x4* c4 = reinterpret_cast<const u32x4*>(counts);
+  const uint64_t n4 = t0 / 4;
+  uint64_t v = 0;
+  for (uint64_t i0 = threadIdx.x; i0 < n4; i0 += (uint64_t)kThreads * kOwnScanBatch) {
+    u32x4 w[kOwnScanBatch];
+#pragma unroll
+    for (int k = 0; k < kOwnScanBatch; ++k) {
+      const uint64_t i = i0 + (uint64_t)kThreads * k;
+      w[k] = i < n4 ? c4[i] : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int k = 0; k < kOwnScanBatch; ++k)
+      v += (uint64_t)w[k][0] + (uint64_t)w[k][1] + (uint64_t)w[k][2] + (uint64_t)w[k][3];
+  }
+  v = wave_sum64(v);
+  if (lane_id() == 0) s_part[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint64_t total = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) total += s_part[w];
+  return total;
+}
+
+template <typename IdxT, bool kMulti, bool kVec, bool kOwnScan>
 __global__ __launch_bounds__(kThreads) void finalize_kernel(ExtractArgs a) {
   __shared__ uint32_t s_begin[kTilesPerGroup + 1];   // run start of each tile in the group
   __shared__ uint32_t s_count[kTilesPerGroup];
   __shared__ int64_t s_out_base[kTilesPerGroup];
   __shared__ uint32_t s_wave_total[kWaves];
-  const uint64_t g = xcd_tile(blockIdx.x, (a.num_tiles + kTilesPerGroup - 1) / kTilesPerGroup);
+  __shared__ uint64_t s_part[kWaves];
+  const uint64_t groups = (a.num_tiles + kTilesPerGroup - 1) / kTilesPerGroup;
+  const uint64_t g = xcd_tile(blockIdx.x, groups);
   const uint64_t t0 = g * kTilesPerGroup;
   const uint64_t left = a.num_tiles - t0;
   const uint32_t n_here = left < (uint64_t)kTilesPerGroup ? (uint32_t)left : kTilesPerGroup;
   const uint32_t lane = lane_id();
   const uint32_t wave = threadIdx.x >> 6;
-  const uint64_t group_excl = a.group_excl[g];
+  const uint64_t group_excl = kOwnScan ? counts_before_group(a.counts, t0, s_part)
+                                       : a.group_excl[g];
   if (wave == 0) {
     // exclusive scan of the group's tile counts (one tile per lane)
     const uint64_t t = t0 + lane;
@@ -499,6 +540,7 @@ __global__ __launch_bounds__(kThreads) void finalize_kernel(ExtractArgs a) {
   __syncthreads();
   IdxT* out_idx = reinterpret_cast<IdxT*>(a.out_idx);
   const uint32_t total = s_begin[64];
+  if (kOwnScan && g == groups - 1 && threadIdx.x == 0) *a.d_count = group_excl + total;
   // Every staged entry of the group, in output order, spread over all
   // threads; the tile of entry e is found by binary search over s_begin.
   // Each thread loads kFinBatch entries before it stores any, so that many
@@ -903,7 +945,41 @@ struct CodedGroup {
   uint32_t wave_total[kWaves];
   uint32_t last_off;                    // offset of the previous window's last entry
   uint32_t overflow;
+  uint64_t eg, bg;                      // entries and code bytes before the group (own scan)
 };
+
+// The coded scan for one group, by one wavefront of its finalize workgroup
+// (calls over at most kOwnScanGroups groups): the entries and code bytes
+// of groups [0, g) and the index group g's first entry is coded against,
+// from the records coded_group_kernel left, walked in blocks of 64 groups
+// as the second pass of coded_scan_kernel walks them.
+constexpr int kOwnCodedBatch = 4;
+__device__ __forceinline__ void own_coded_scan(const ExtractArgs& a, uint64_t g, uint32_t lane,
+                                               uint64_t& eg, uint64_t& bg, int64_t& gp) {
+  uint64_t cnt = 0, bytes = 0;
+  int64_t carry_prev = a.code_base;
+  for (uint64_t b = 0; b * 64 < g; b += kOwnCodedBatch) {
+    CodedBlock v[kOwnCodedBatch];
+#pragma unroll
+    for (int k = 0; k < kOwnCodedBatch; ++k) {
+      const uint64_t gi = (b + k) * 64 + lane;
+      v[k] = load_coded_block(a, gi, gi < g);
+    }
+#pragma unroll
+    for (int k = 0; k < kOwnCodedBatch; ++k) {
+      int64_t before, bmax;
+      lower_last(v[k].last, lane, before, bmax);
+      const int64_t pred = before > carry_prev ? before : carry_prev;
+      cnt += v[k].packed & 0xFFFFFFFFull;
+      bytes += (v[k].packed >> 32) +
+               (v[k].first >= 0 ? first_entry_bytes(a, v[k].first, pred, v[k].local) : 0u);
+      carry_prev = bmax > carry_prev ? bmax : carry_prev;
+    }
+  }
+  eg = wave_sum64(cnt);
+  bg = wave_sum64(bytes);
+  gp = carry_prev;
+}
 
 // Stores bytes [0, n) of `src` at dst (4-byte stores where dst is aligned).
 __device__ __forceinline__ void flush_code(const uint8_t* src, uint32_t n, uint8_t* dst) {
@@ -997,19 +1073,33 @@ __device__ __forceinline__ uint32_t code_window(const ExtractArgs& a, CodedGroup
 // and its entries placed into the window by rank.  The launch bound asks
 // for six wavefronts per SIMD (at most 80 registers): measured faster than
 // the five the unbounded allocation gives.
-template <bool kMulti, bool kVec>
+template <bool kMulti, bool kVec, bool kOwnScan>
 __global__ __launch_bounds__(kThreads, 6) void finalize_coded_kernel(ExtractArgs a) {
   __shared__ CodedGroup sg;
   __shared__ uint32_t s_wave_total[kWaves];
+  const uint64_t groups = (a.num_tiles + kTilesPerGroup - 1) / kTilesPerGroup;
   const uint64_t g = blockIdx.x;
   const uint64_t t0 = g * kTilesPerGroup;
   const uint64_t left = a.num_tiles - t0;
   const uint32_t n_here = left < (uint64_t)kTilesPerGroup ? (uint32_t)left : kTilesPerGroup;
   const uint32_t lane = lane_id();
   const uint32_t wave = threadIdx.x >> 6;
-  const uint64_t eg = a.group_excl[g];
-  const uint64_t bg = a.group_bexcl[g];
+  uint64_t eg = 0, bg = 0;
+  if (!kOwnScan) {
+    eg = a.group_excl[g];
+    bg = a.group_bexcl[g];
+  }
   if (wave == 0) {
+    int64_t gp;
+    if (kOwnScan) {
+      own_coded_scan(a, g, lane, eg, bg, gp);
+      if (lane == 0) {
+        sg.eg = eg;
+        sg.bg = bg;
+      }
+    } else {
+      gp = a.group_prev[g];
+    }
     const uint64_t t = t0 + lane;
     const bool in = lane < n_here;
     const uint64_t rec = in ? a.tile_rec[t] : 0;
@@ -1022,7 +1112,6 @@ __global__ __launch_bounds__(kThreads, 6) void finalize_coded_kernel(ExtractArgs
     }
     int64_t before, top;
     lower_last(c ? ob + (int64_t)rec_last(rec) : -1, lane, before, top);
-    const int64_t gp = a.group_prev[g];
     if (before < gp) before = gp;
     const uint32_t x = wave_incl_sum(c, lane);
     const int64_t prev = in ? coded_pred(a, before, (int64_t)d.seg_base) : before;
@@ -1062,7 +1151,18 @@ __global__ __launch_bounds__(kThreads, 6) void finalize_coded_kernel(ExtractArgs
     }
   }
   __syncthreads();
+  if (kOwnScan) {
+    eg = sg.eg;
+    bg = sg.bg;
+  }
   const uint32_t total = sg.begin[64];
+  // the last group's workgroup leaves the call's totals (own scan)
+  auto finish = [&](uint64_t written) {
+    if (kOwnScan && g == groups - 1 && threadIdx.x == 0) {
+      *a.d_count = eg + total;
+      *a.d_nbytes = bg + written;
+    }
+  };
   uint64_t written = 0;
   if (!sg.overflow) {
     for (uint32_t w0 = 0; w0 < total; w0 += kCodeWin) {
@@ -1089,6 +1189,7 @@ __global__ __launch_bounds__(kThreads, 6) void finalize_coded_kernel(ExtractArgs
       __syncthreads();
       written += code_window(a, sg, w0, n, eg, bg, written);
     }
+    finish(written);
     return;
   }
   for (uint32_t i = 0; i < n_here; ++i) {
@@ -1129,6 +1230,7 @@ __global__ __launch_bounds__(kThreads, 6) void finalize_coded_kernel(ExtractArgs
       written += code_window(a, sg, sg.begin[i] + r0, n, eg, bg, written);
     }
   }
+  finish(written);
 }
 
 // ------------------------------------------------------- small kernels
@@ -1240,9 +1342,14 @@ static hipError_t launch_all(const ExtractArgs& a, hipStream_t stream, const Sta
   hipStream_t rest;
   if (e == hipSuccess) e = split_after_stage(stream, split, rest);
   if (e != hipSuccess) return e;
+  if (groups <= kOwnScanGroups) {
+    hipLaunchKernelGGL((finalize_kernel<IdxT, kMulti, kVec, true>), dim3((uint32_t)groups),
+                       dim3(kThreads), 0, rest, a);
+    return hipGetLastError();
+  }
   e = launch_group_scan(a.counts, a.num_tiles, a.group_sum, a.group_excl, a.d_count, rest);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((finalize_kernel<IdxT, kMulti, kVec>), dim3((uint32_t)groups),
+  hipLaunchKernelGGL((finalize_kernel<IdxT, kMulti, kVec, false>), dim3((uint32_t)groups),
                      dim3(kThreads), 0, rest, a);
   return hipGetLastError();
 }
@@ -1270,10 +1377,15 @@ static hipError_t launch_coded(const ExtractArgs& a, hipStream_t stream, const S
   hipLaunchKernelGGL(coded_group_kernel, dim3((uint32_t)groups), dim3(64), 0, rest, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (groups <= kOwnScanGroups) {
+    hipLaunchKernelGGL((finalize_coded_kernel<kMulti, kVec, true>), dim3((uint32_t)groups),
+                       dim3(kThreads), 0, rest, a);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(coded_scan_kernel, dim3(1), dim3(kScanThreads), 0, rest, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((finalize_coded_kernel<kMulti, kVec>), dim3((uint32_t)groups),
+  hipLaunchKernelGGL((finalize_coded_kernel<kMulti, kVec, false>), dim3((uint32_t)groups),
                      dim3(kThreads), 0, rest, a);
   return hipGetLastError();
 }

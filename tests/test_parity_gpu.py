@@ -348,7 +348,7 @@ def test_apply_multi_round_trip():
 # --------------------------------------------------------------- pipeline
 
 @pytest.mark.parametrize("chunk,streams", [(10_007, 4), (TILE, 3), (1 << 20, 4), (1 << 27, 2),
-                                           (777, 1)])
+                                           (777, 1), (10_007, 5), (4096, 8), (3000, 16)])
 def test_pipeline_equals_multi(chunk, streams):
     sizes = [0, 128, 4096 * 3, 1, 7, 2 * TILE + 5, 5000, 0, 100_000, 33_333]
     prevs, news = make_list(sizes, 0.02, seed=500)
@@ -372,7 +372,7 @@ def oracle_chunk_stream(ref_idx, chunk, total):
 
 
 @pytest.mark.parametrize("chunk,streams", [(10_007, 4), (TILE, 3), (1 << 20, 4), (1 << 27, 2),
-                                           (777, 1)])
+                                           (777, 1), (10_007, 5), (4096, 8), (3000, 16)])
 def test_pipeline_leb128_matches_oracle(chunk, streams):
     sizes = [0, 128, 4096 * 3, 1, 7, 2 * TILE + 5, 5000, 0, 100_000, 33_333]
     prevs, news = make_list(sizes, 0.02, seed=501)
