@@ -138,14 +138,18 @@ constexpr int kDeliverThreads = 256;
 // 8 x 2 29.7-29.8 / 17.0; 1 x 4 35.0 / 13.7-14.5; 2 x 2 34.4 / 14.0;
 // 1 x 2 37.4 / 18.6; plain 4 x 5 / 4 x 6 / 4 x 8 / 3 x 6 / 6 x 4 29.4 /
 // 29.2-29.4 / 32.4 / 29.8 / 34.5; coded 1 x 3 / 1 x 5 / 1 x 6 / 1 x 7 /
-// 1 x 8 / 2 x 4 16.3 / 13.7 / 13.3-13.5 / 13.9 / 14.4 / 15.2.  The plain
-// stream (10 bytes per entry) needs the link's rate and takes 4 x 6; the
-// coded one (about 3.3) far less: 1 x 6.
+// 1 x 8 / 2 x 4 16.3 / 13.7 / 13.3-13.5 / 13.9 / 14.4 / 15.2.  Once the
+// finalize pass scanned for itself, a second sweep (same order of runs)
+// gave plain 4 x 6 / 2 x 6 / 2 x 8 / 1 x 8 / 1 x 12 / 1 x 16 30.4 / 29.8 /
+// 29.8 / 31.1 / 30.4 / 30.5 and coded 1 x 6 / 2 x 3 / 1 x 4 / 1 x 8 /
+// 1 x 10 / 1 x 12 13.3-13.5 / 13.7-13.8 / 14.6 / 14.2 / 15.4 / 15.7.  The
+// plain stream (10 bytes per entry) needs the link's rate and takes 2 x 6;
+// the coded one (about 3.3) far less: 1 x 6.
 constexpr int kXcds = 8;
 struct DeliverShape {
   uint32_t xcds, per_xcd;
 };
-constexpr DeliverShape kDeliverPlain = {4, 6};
+constexpr DeliverShape kDeliverPlain = {2, 6};
 constexpr DeliverShape kDeliverCoded = {1, 6};
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));

@@ -4,9 +4,9 @@ tooling, not part of the library).
     python3 -m paper_2602_11456_amd.probes.rocprof_digest stats KERNEL_STATS_CSV
         per-kernel calls and average duration (rocprofv3 --kernel-trace --stats)
     python3 -m paper_2602_11456_amd.probes.rocprof_digest pipeline KERNEL_TRACE_CSV [COPY_TRACE_CSV]
-        per call of the chunked pipeline: wall span, busy time per kernel
-        and per stream, and the DMA copies' rate (rocprofv3 --kernel-trace
-        [--memory-copy-trace] of bench.py --only-pipeline)
+        per call of the chunked pipeline: span, busy time per kernel and per
+        stream, and any device-to-host DMA copies inside it (rocprofv3
+        --kernel-trace [--memory-copy-trace] of bench.py --only-pipeline)
     python3 -m paper_2602_11456_amd.probes.rocprof_digest traffic FETCH_CSV WRITE_CSV COPY_BYTES OUT_JSON
         HBM bytes per dispatch from two rocprofv3 --pmc runs (FETCH_SIZE,
         then WRITE_SIZE, in KiB), each scaled by what the same counter reads
@@ -46,6 +46,9 @@ def stats(path):
 
 
 def pipeline(trace_path, copy_path=None):
+    """Per pipeline call (each starts with run_reset_kernel): its span from
+    the first kernel's start to the last one's end, and per kernel and per
+    stream the dispatches and busy time."""
     rows = list(csv.DictReader(open(trace_path)))
     ev = []
     for r in rows:
@@ -60,35 +63,34 @@ def pipeline(trace_path, copy_path=None):
                 copies.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]),
                                int(r.get("Size", 0) or 0)))
     ev.sort()
-    # a call is a run of kernels with no gap above 2 ms between starts
-    calls, cur = [], []
+    calls, cur = [], None
     for e in ev:
-        if cur and e[0] - cur[-1][0] > 2_000_000:
-            calls.append(cur)
+        if e[2] == "run_reset_kernel":
             cur = []
-        cur.append(e)
-    if cur:
-        calls.append(cur)
+            calls.append(cur)
+        if cur is not None and e[2] != "__amd_rocclr_copyBuffer":
+            cur.append(e)
     for ci, c in enumerate(calls):
         names = collections.defaultdict(list)
+        streams = collections.defaultdict(list)
         for s, e, n, q in c:
             names[n].append(e - s)
-        if "post_counts_kernel" not in names:
-            continue
+            streams[q].append(e - s)
+        kind = "coded" if "coded_group_kernel" in names else "plain"
         t0 = min(s for s, *_ in c)
         t1 = max(e for _, e, *_ in c)
-        cc = [x for x in copies if t0 <= x[0] <= t1 + 5_000_000]
-        span = (max([t1] + [x[1] for x in cc]) - t0) / 1e6
-        print(f"call {ci}: {len(c)} kernels, first kernel to last kernel end "
-              f"{(t1 - t0) / 1e6:.2f} ms, to last copy end {span:.2f} ms")
+        print(f"call {ci} ({kind}): {len(c)} kernels, first kernel start to last kernel end "
+              f"{(t1 - t0) / 1e6:.2f} ms")
         for n, d in sorted(names.items(), key=lambda x: -sum(x[1])):
             print(f"   {n:28s} x{len(d):4d}  avg {statistics.mean(d) / 1e3:8.1f} us  "
                   f"med {statistics.median(d) / 1e3:8.1f}  busy {sum(d) / 1e6:6.2f} ms")
+        for q, d in sorted(streams.items(), key=lambda x: -sum(x[1])):
+            print(f"   stream {q}: {len(d)} kernels, busy {sum(d) / 1e6:6.2f} ms")
+        cc = [x for x in copies if t0 <= x[0] <= t1]
         if cc:
-            busy = sum(e - s for s, e, _ in cc)
             nbytes = sum(b for *_, b in cc)
-            print(f"   D2H copies x{len(cc)}: {nbytes / 1e9:.3f} GB, busy {busy / 1e6:.2f} ms "
-                  f"(summed over streams), {nbytes / (span / 1e3) / 1e9:.2f} GB/s over the call")
+            busy = sum(e - s for s, e, _ in cc)
+            print(f"   D2H copies x{len(cc)}: {nbytes / 1e9:.3f} GB, busy {busy / 1e6:.2f} ms")
 
 
 def traffic(fetch_csv, write_csv, copy_bytes, out_json):
