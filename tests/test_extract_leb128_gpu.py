@@ -225,3 +225,15 @@ def test_equals_encoder_over_extract_multi():
     assert torch.equal(boffs, seg_bytes)
     assert torch.equal(offs2, offs)
     assert torch.equal(val2.view(torch.int16), val.view(torch.int16))
+
+
+# Up to 512 groups of 64 tiles the coded finalize pass scans the group
+# records itself; above, the coded scan kernel runs first.  Both sides: a
+# two-tensor list cut at a tile boundary holds 32768 tiles (512 groups) at
+# 2^28 words and 32769 one word later.
+@pytest.mark.parametrize("n", [512 * 64 * TILE, 512 * 64 * TILE + 1])
+def test_own_scan_boundary(n):
+    say(f"coded own-scan boundary: {n} words")
+    p, q = rand_pair(n, 0.01, n % 10_009)
+    cut = (n // 3) // TILE * TILE
+    check([p[:cut], p[cut:]], [q[:cut], q[cut:]], round_trip=False)

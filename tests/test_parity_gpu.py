@@ -125,6 +125,26 @@ def test_small_call_boundary(n, density):
     check_extract(prev[3:], new[3:], torch.int64)   # misaligned, n words
 
 
+# Calls over at most 512 groups of 64 tiles (2^28 words) scan inside their
+# finalize pass, the last group's workgroup writing the total; above that a
+# separate scan kernel runs first.  Both sides of the switch, as one tensor
+# and as a two-tensor list (tensor offsets), the list's second tensor
+# starting mid-line.
+OWN_SCAN_WORDS = 512 * 64 * TILE
+
+
+@pytest.mark.parametrize("n", [OWN_SCAN_WORDS - 3, OWN_SCAN_WORDS, OWN_SCAN_WORDS + 1,
+                               OWN_SCAN_WORDS + 64 * TILE + 5])
+def test_own_scan_boundary(n):
+    say(f"own-scan boundary: {n} words")
+    prev, new = rand_pair(n, 0.01, seed=n % 10_007)
+    check_extract(prev, new, torch.int64)
+    if n == OWN_SCAN_WORDS + 1:
+        check_extract(prev, new, torch.int32)
+    cut = n // 3 + 5
+    check_multi([prev[:cut], prev[cut:]], [new[:cut], new[cut:]])
+
+
 @pytest.mark.parametrize("off_p,off_q", [(1, 1), (3, 3), (7, 7), (0, 1), (2, 5), (6, 0), (4, 4)])
 def test_misaligned_views(off_p, off_q):
     n = 3 * TILE + 1001
