@@ -1049,7 +1049,7 @@ def main():
         if rec.get("kernel_source_sha256") == kernel_source_digest():
             traffic = rec.get("bytes_per_call")
             for name, k in rec.get("kernels", {}).items():
-                if "stage_kernel" in name:
+                if name == "stage_kernel<true, true, false>":   # the planned headline call's
                     scan_traffic = round(k["bytes_per_dispatch"])
     # the dominant kernel: the scan (stage_kernel), whose algorithmic bytes
     # are both copies read once

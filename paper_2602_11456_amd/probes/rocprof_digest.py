@@ -128,7 +128,8 @@ def traffic(fetch_csv, write_csv, copy_bytes, out_json):
     per_call = sum(v["bytes_per_dispatch"] for k, v in kernels.items()
                    if any(s in k for s in ("stage_kernel<true, true, false>",
                                            "group_sum_kernel<unsigned int>",
-                                           "group_scan_kernel", "finalize_kernel<long, true, true>")))
+                                           "group_scan_kernel",
+                                           "finalize_kernel<long, true, true, false>")))
     out = {"bytes_per_call": per_call, "fetch_factor": fetch_factor,
            "write_factor": write_factor,
            "calibration": f"3 device-to-device copies of {copy_bytes} bytes",
