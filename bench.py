@@ -1161,8 +1161,26 @@ def main():
         result["sweep"] = sweep_measurement(ad, synth, dev, stream, 5)
     if pipeline is not None:
         result["pipeline"] = pipeline
+    result["device"] = device_info(dev)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def device_info(dev):
+    """The device's properties as the runtime reports them (CU count, cache
+    and memory sizes), next to the figures they bound."""
+    import torch
+    p = torch.cuda.get_device_properties(dev)
+    return {
+        "name": p.name,
+        "arch": getattr(p, "gcnArchName", ""),
+        "compute_units": p.multi_processor_count,
+        "hbm_bytes": p.total_memory,
+        "l2_bytes": getattr(p, "L2_cache_size", None),
+        "lds_bytes_per_workgroup": getattr(p, "shared_memory_per_block", None),
+        "torch": torch.__version__,
+        "hip": torch.version.hip,
+    }
 
 
 if __name__ == "__main__":
