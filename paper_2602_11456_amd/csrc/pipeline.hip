@@ -125,7 +125,6 @@ struct DeliverArgs {
 // Streams beyond the three roles stay idle: a process gets four hardware
 // queues by default, and streams beyond that share a queue, which
 // serialises their work.
-constexpr int kDeliverThreads = 256;
 // Stores into host memory are slow to complete, and while many are
 // outstanding the GPU's HBM reads slow down: a host-write kernel spread over
 // all 8 XCDs cut a concurrent HBM read kernel from 6.9 to 1.8 TB/s.  So the
@@ -144,24 +143,34 @@ constexpr int kDeliverThreads = 256;
 // 29.8 / 31.1 / 30.4 / 30.5 and coded 1 x 6 / 2 x 3 / 1 x 4 / 1 x 8 /
 // 1 x 10 / 1 x 12 13.3-13.5 / 13.7-13.8 / 14.6 / 14.2 / 15.4 / 15.7.  The
 // plain stream (10 bytes per entry) needs the link's rate and takes 2 x 6;
-// the coded one (about 3.3) far less: 1 x 6.
+// the coded one (about 3.3) far less.  Its chunks are small (about 4.4 MB),
+// and a workgroup's rounds of loads wait on the reads beside them, so the
+// bytes each round keeps in flight matter as much as the workgroup count:
+// coded 1 x 3 workgroups of 512 threads with 8 vectors per thread per
+// round 12.4-12.7 ms, against 13.3-13.5 for 1 x 6 of 256 threads with 4
+// (1 x 2 / 1 x 4 of 512 x 8: 15.8 / 13.8; 1 x 3 of 512 x 16: 12.9; 1 x 3
+// of 256 x 8 / 1024 x 8: 15.5 / 14.5; 1 x 6 of 256 x 8 / 256 x 16 / 512 x
+// 4: 14.2 / 15.2 / 15.3).  The plain kind measured 29.8-30.5 ms in every
+// one of these forms and keeps 256 threads with 4.
 constexpr int kXcds = 8;
 struct DeliverShape {
   uint32_t xcds, per_xcd;
 };
 constexpr DeliverShape kDeliverPlain = {2, 6};
-constexpr DeliverShape kDeliverCoded = {1, 6};
+constexpr DeliverShape kDeliverCoded = {1, 3};
+constexpr int kPlainThreads = 256, kPlainUnroll = 4;
+constexpr int kCodedThreads = 512, kCodedUnroll = 8;
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 // four dwords at a 4-byte aligned address (one 16-byte load)
 typedef uint32_t u32x4a_t __attribute__((ext_vector_type(4), aligned(4)));
-constexpr int kCopyUnroll = 4;
 
 // dst[0, n) = src[0, n) by the whole grid, where src is 4-byte aligned and
 // readable up to 4 bytes past n, and dst (host memory) has any alignment:
 // the bytes before dst's first 16-byte boundary and after its last one are
 // stored one by one; in between every store is a whole aligned 16 bytes,
 // assembled from five aligned source dwords with byte-aligning shifts.
+template <int kCopyUnroll>
 __device__ void copy_bytes(uint8_t* dst, const uint8_t* src, uint64_t n, uint64_t i0,
                            uint64_t stride) {
   uint64_t head = (16 - ((uintptr_t)dst & 15)) & 15;
@@ -203,7 +212,10 @@ __device__ void copy_bytes(uint8_t* dst, const uint8_t* src, uint64_t n, uint64_
   }
 }
 
-__global__ __launch_bounds__(kDeliverThreads) void deliver_kernel(DeliverArgs a) {
+// kThreads threads per workgroup, each with kUnroll 16-byte vectors in
+// flight per round.
+template <int kThreads, int kUnroll>
+__global__ __launch_bounds__(kThreads) void deliver_kernel(DeliverArgs a) {
   const uint64_t cnt = *a.d_count;
   const uint64_t nb = a.bytes ? *a.d_nbytes : 0;
   const uint64_t* r = a.run + 2 * (a.c & 1);
@@ -221,14 +233,14 @@ __global__ __launch_bounds__(kDeliverThreads) void deliver_kernel(DeliverArgs a)
     if (a.chunk_counts) a.chunk_counts[a.c] = cnt;
   }
   const uint64_t ne = be < a.h_val_cap ? (a.h_val_cap - be < cnt ? a.h_val_cap - be : cnt) : 0;
-  copy_bytes((uint8_t*)(a.h_val + be), (const uint8_t*)a.val, 2 * ne, i0, stride);
+  copy_bytes<kUnroll>((uint8_t*)(a.h_val + be), (const uint8_t*)a.val, 2 * ne, i0, stride);
   if (a.h_idx) {
     const uint64_t ni = be < a.h_idx_cap ? (a.h_idx_cap - be < cnt ? a.h_idx_cap - be : cnt) : 0;
-    copy_bytes((uint8_t*)(a.h_idx + be), (const uint8_t*)a.idx, 8 * ni, i0, stride);
+    copy_bytes<kUnroll>((uint8_t*)(a.h_idx + be), (const uint8_t*)a.idx, 8 * ni, i0, stride);
   }
   if (a.bytes) {
     const uint64_t n = bb < a.h_bytes_cap ? (a.h_bytes_cap - bb < nb ? a.h_bytes_cap - bb : nb) : 0;
-    copy_bytes(a.h_bytes + bb, a.bytes, n, i0, stride);
+    copy_bytes<kUnroll>(a.h_bytes + bb, a.bytes, n, i0, stride);
   }
 }
 
@@ -463,8 +475,12 @@ static delta_status_t pipeline_impl(const uint16_t* const* prevs, const uint16_t
     d.chunk_counts = o.leb ? d_chunk_counts : nullptr;
     d.c = c;
     d.xcds = shape.xcds;
-    hipLaunchKernelGGL(deliver_kernel, dim3(kXcds * shape.per_xcd), dim3(kDeliverThreads), 0, ds,
-                       d);
+    if (o.leb)
+      hipLaunchKernelGGL((deliver_kernel<kCodedThreads, kCodedUnroll>),
+                         dim3(kXcds * shape.per_xcd), dim3(kCodedThreads), 0, ds, d);
+    else
+      hipLaunchKernelGGL((deliver_kernel<kPlainThreads, kPlainUnroll>),
+                         dim3(kXcds * shape.per_xcd), dim3(kPlainThreads), 0, ds, d);
     e = hipGetLastError();
     if (e == hipSuccess) e = hipEventRecord(delivered[slot], ds);
   }
