@@ -727,7 +727,8 @@ size_t delta_pipeline_staging_bytes(const uint64_t* numels, int32_t num_tensors,
  *                 of every chunk, one after the other; streams[1] the
  *                 kernels that finish a chunk once it has been read;
  *                 streams[2] delivers the chunks in order, one kernel per
- *                 chunk storing into the host arrays.  S == 2: streams[0]
+ *                 chunk (with S >= 4, per two chunks) storing into the
+ *                 host arrays.  S == 2: streams[0]
  *                 also finishes the chunks, streams[1] delivers; S == 1:
  *                 everything in order on streams[0].  Streams past the
  *                 third are not used (more streams than hardware queues

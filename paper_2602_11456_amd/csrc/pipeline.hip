@@ -11,13 +11,13 @@
 // taking the kernels that finish each chunk (its finalize pass, and for
 // the coded form the group records before it) once its stage kernel is
 // done, while the next chunk is being read; streams[2] delivers the chunks
-// in order: one kernel per chunk reads the chunk's counts and the running
-// totals from device memory and stores its entries straight into the
-// pinned host arrays over the host link (kernel stores into pinned memory
-// reach the 55 GB/s of DMA copies and need no host round trip per chunk).
-// Coded, the extract writes the chunk's positions gap + LEB128 coded
-// instead of as indices (three kernels per chunk, no index stream in
-// between).  A delivery waits on its chunk's coding; the reading of a chunk
+// in order: one kernel per chunk (plain, with four or more slots, per two
+// chunks) reads the counts and the running totals from device memory and
+// stores the entries straight into the pinned host arrays over the host
+// link (kernel stores into pinned memory reach the 55 GB/s of DMA copies
+// and need no host round trip per chunk).  Coded, the extract writes the
+// chunk's positions gap + LEB128 coded instead of as indices (no index
+// stream in between).  A delivery waits on its chunk's coding; the reading of a chunk
 // that reuses a slot waits on the delivery of the slot's previous chunk.
 // The host only enqueues and waits once, at the end.  With S == 2 reading
 // and coding share streams[0]; with S == 1 everything runs in order on it.
