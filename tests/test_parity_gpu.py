@@ -497,8 +497,9 @@ def test_pipeline_leb128_capacity_retry():
     np.testing.assert_array_equal(v.view(torch.int16).numpy().view(np.uint16), ref_val)
 
 
+@pytest.mark.parametrize("streams", [3, 4])   # four: the plain kind delivers chunks in pairs
 @pytest.mark.parametrize("shift_idx,shift_val", [(1, 1), (3, 5), (0, 7)])
-def test_pipeline_host_arrays_at_odd_offsets(shift_idx, shift_val):
+def test_pipeline_host_arrays_at_odd_offsets(shift_idx, shift_val, streams):
     # host outputs that start inside a pinned buffer, off any 16-byte line:
     # the delivery kernel's unaligned heads and tails and the device view of
     # an interior host pointer
@@ -510,7 +511,7 @@ def test_pipeline_host_arrays_at_odd_offsets(shift_idx, shift_val):
     big_v = torch.zeros(ref_cnt + 64, dtype=torch.int16, pin_memory=True)
     h_idx = big_i[shift_idx:shift_idx + ref_cnt + 8]
     h_val = big_v[shift_val:shift_val + ref_cnt + 8].view(torch.bfloat16)
-    i, v = ad.delta_extract_pipelined(prevs, news, chunk_elems=10_007, num_streams=3,
+    i, v = ad.delta_extract_pipelined(prevs, news, chunk_elems=10_007, num_streams=streams,
                                       h_idx=h_idx, h_val=h_val)
     np.testing.assert_array_equal(i.numpy(), ref_idx)
     np.testing.assert_array_equal(v.view(torch.int16).numpy().view(np.uint16), ref_val)
@@ -520,7 +521,7 @@ def test_pipeline_host_arrays_at_odd_offsets(shift_idx, shift_val):
     hb_big = torch.zeros(3 * ref_cnt + 64, dtype=torch.uint8, pin_memory=True)
     hb = hb_big[shift_val:]
     b, v2, counts, used = ad.delta_extract_pipelined_leb128(prevs, news, chunk_elems=10_007,
-                                                           num_streams=3, h_bytes=hb,
+                                                           num_streams=streams, h_bytes=hb,
                                                            h_val=h_val)
     ref_bytes, ref_counts = oracle_chunk_stream(ref_idx, used, sum(sizes))
     np.testing.assert_array_equal(b.numpy(), ref_bytes)
